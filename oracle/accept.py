@@ -1,0 +1,142 @@
+"""Acceptance along a verified draft tree (Sec. 3.1, Eq. 1; Sec. 5.1 for T = 0).
+
+Greedy (T = 0): walk from the root; at node u let t_u be the target's argmax over the
+allowed ids (lowest id on ties); move to the child whose token is t_u while one exists.
+The accepted path ends at u and t_u is the bonus token.
+
+Exact sampling: Eq. 1 accepts a drafted token with probability min(1, p/q).  The
+drafted children are deterministic top-k proposals, so q is read as a point mass on the
+proposed token; the test becomes 'accept x with probability p(x)', and after a
+rejection the residual distribution is p with x removed and renormalised.  Siblings are
+tried in order (highest draft score first); if all are rejected the bonus is drawn from
+the residual.  The committed token's law is exactly p.
+
+Relaxed mode (config of the ADT-Tree+LANTERN rows, Tables I-II): a drafted token x is
+also credited with the target mass of its nearest codebook neighbours, taken in
+similarity order for as long as their summed mass stays within delta of the remaining
+mass; x is accepted with probability (mass of x + credited mass), and on rejection the
+whole credited neighbourhood is removed from the residual.  delta = 0 or one neighbour
+reduces it to exact mode.
+
+Numbers: p is quantised once per row to integer weights w = rint(exp(z - max z) * 2^32)
+with z = logit / T over the top-K allowed ids, computed in float32 (the precision the
+kernel decides in); all later arithmetic is exact integer.  A draw is
+r = floor(U * W / 2^64) with U the 64 bits of Philox4x32-10 at key = seed and
+counter = (step, node, trial, 0), and W the remaining total weight.
+
+Test infrastructure only; see the package docstring.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+from .numerics import draw_below, uniform_u64
+
+DELTA_FRAC_BITS = 16
+
+
+def greedy_targets(logits: np.ndarray, allowed: np.ndarray) -> np.ndarray:
+    """t_u = argmax over [lo_u, hi_u) (np.argmax returns the lowest index among ties)."""
+    out = np.zeros(len(logits), dtype=np.int64)
+    for u in range(len(logits)):
+        lo, hi = int(allowed[u][0]), int(allowed[u][1])
+        out[u] = lo + int(np.argmax(logits[u][lo:hi]))
+    return out
+
+
+def children_of(parent: Sequence[int]) -> List[List[int]]:
+    ch: List[List[int]] = [[] for _ in parent]
+    for i in range(1, len(parent)):
+        ch[int(parent[i])].append(i)
+    return ch
+
+
+def accept_greedy(logits: np.ndarray, parent, token, allowed) -> Tuple[List[int], int]:
+    """Returns (accepted node indices v_1..v_a, bonus token)."""
+    t = greedy_targets(logits, allowed)
+    ch = children_of(parent)
+    path: List[int] = []
+    u = 0
+    while True:
+        nxt = [c for c in ch[u] if int(token[c]) == int(t[u])]
+        if not nxt:
+            return path, int(t[u])
+        u = nxt[0]
+        path.append(u)
+
+
+def quantised_weights(logit_row: np.ndarray, lo: int, hi: int, temperature: float, top_k: int) -> np.ndarray:
+    """Integer weights (Python ints in an object array) of the sampling distribution p at
+    one row: softmax(logit / T) over the allowed ids, truncated to the top_k ids by
+    (logit desc, id asc), as w = rint(exp(z - max z) * 2^32) in float32."""
+    V = len(logit_row)
+    z = np.asarray(logit_row[lo:hi], dtype=np.float32) / np.float32(temperature)
+    ids = np.arange(lo, hi)
+    keep = np.lexsort((ids, -z.astype(np.float64)))
+    if top_k > 0:
+        keep = keep[:top_k]
+    zmax = z[keep].max()
+    e = np.exp(z[keep] - zmax)                              # float32
+    wq = np.rint(e.astype(np.float64) * 4294967296.0)       # e * 2^32 is exact in float64
+    w = np.zeros(V, dtype=object)
+    w[:] = 0
+    for i, val in zip(ids[keep], wq):
+        w[int(i)] = int(val)
+    return w
+
+
+def inverse_cdf(w: np.ndarray, r: int) -> int:
+    """Smallest id i with sum_{j <= i} w_j > r (ids ascending)."""
+    acc = 0
+    for i in range(len(w)):
+        acc += int(w[i])
+        if acc > r:
+            return i
+    raise ValueError("draw beyond total weight")
+
+
+def accept_sampling(logits: np.ndarray, parent, token, allowed, *, temperature: float, top_k: int,
+                    seed: int, step: int, mode: str = "exact", delta: float = 0.0,
+                    knn: Optional[np.ndarray] = None, knn_k: int = 1) -> Tuple[List[int], int]:
+    """Exact (mode='exact') or relaxed (mode='relaxed') acceptance.  Returns (path, bonus)."""
+    ch = children_of(parent)
+    delta_q = int(round(delta * (1 << DELTA_FRAC_BITS)))
+    path: List[int] = []
+    u = 0
+    while True:
+        lo, hi = int(allowed[u][0]), int(allowed[u][1])
+        w = quantised_weights(logits[u], lo, hi, temperature, top_k)
+        W = int(sum(int(x) for x in w))
+        accepted = None
+        trial = 0
+        for c in ch[u]:
+            x = int(token[c])
+            r = draw_below(uniform_u64(seed, step, u, trial), W)
+            trial += 1
+            credit = [x]
+            mass = int(w[x])
+            if mode == "relaxed":
+                thr = (W * delta_q) >> DELTA_FRAC_BITS
+                extra = 0
+                for y in knn[x][1:knn_k]:
+                    y = int(y)
+                    if extra + int(w[y]) > thr:
+                        break
+                    extra += int(w[y])
+                    credit.append(y)
+                mass += extra
+            if r < mass:
+                accepted = c
+                break
+            for y in credit:
+                W -= int(w[y])
+                w[y] = 0
+        if accepted is None:
+            if W <= 0:
+                raise ValueError("residual distribution is empty")
+            r = draw_below(uniform_u64(seed, step, u, trial), W)
+            return path, inverse_cdf(w, r)
+        path.append(accepted)
+        u = accepted

@@ -1,0 +1,240 @@
+"""Image decode with draft-then-verify cycles, and the plain AR reference.
+
+A cycle (Sec. 3.1): the draft head proposes a tree of depth d and width k chosen by the
+ADT rule (Sec. 4), the target verifies every node in one forward under the tree mask,
+the longest acceptable root-to-node path plus one bonus token is committed, and the
+caches are compacted so that the accepted nodes' K/V become the next prefix.
+
+State conventions (the paper gives none):
+  * the root of a tree is the last committed token; its target K/V are not cached yet,
+    so the target cache holds L = (committed tokens - 1) positions;
+  * tree node i is verified at position L + depth(i) and its K/V go to slot L + i;
+    compaction copies slot L + v_m to slot L + m for the accepted nodes v_1 < .. < v_a;
+  * the draft row of the token at position p takes the target feature of position p-1
+    (zeros before position 0); a tree node whose parent is not committed takes the draft
+    feature of its parent's row instead, the root's draft row standing in for the root;
+  * each cycle first runs the draft head over the tokens committed by the previous cycle
+    (catch-up rows, the root last), then d - 1 forwards over the frontier.
+
+Test infrastructure only; see the package docstring.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+from synth import DecodeCfg
+from . import accept as acc
+from .attention import tree_key_slots
+from .expand import Tree, build_tree, expand
+from .model import OracleModel
+from .numerics import draw_below, masked_logits, uniform_u64
+from .schedule import schedule
+from .tree import ancestors_and_self
+
+
+@dataclasses.dataclass
+class StepInfo:
+    step: int
+    d_hat: int
+    k_hat: int
+    tree: Tree
+    logits: np.ndarray          # [n][V] verify logits (allowed-range masking not applied)
+    allowed: np.ndarray         # [n][2] allowed id range of the token each row predicts
+    path: List[int]             # accepted node indices v_1..v_a
+    bonus: int
+    committed: List[int]        # tokens committed this cycle
+    L_before: int
+    draft_root_logits: Optional[np.ndarray] = None
+
+
+class Decoder:
+    """Oracle decode state for one image."""
+
+    def __init__(self, cfg: DecodeCfg, model: OracleModel, prefix: np.ndarray,
+                 poisson: Optional[np.ndarray] = None, knn: Optional[np.ndarray] = None,
+                 accept_seed: Optional[int] = None):
+        self.cfg = cfg
+        self.model = model
+        self.P = len(prefix)
+        self.tokens: List[int] = [int(t) for t in prefix]
+        s_cap = self.P + cfg.n_image + 256
+        self.tcache, self.dcache = model.new_caches(s_cap)
+        self.feat: Dict[int, np.ndarray] = {}          # target feature per committed position
+        self.records: Dict[int, Tuple[int, int]] = {}  # cell -> (d, k) of the committing tree
+        self.prev: Optional[Tuple[int, int]] = None    # (a, d) of the previous tree
+        self.prev_cell: Optional[int] = None
+        self.L = 0
+        self.Ld = 0
+        self.step_no = 0
+        self.poisson = poisson
+        self.knn = knn
+        self.accept_seed = cfg.seed if accept_seed is None else accept_seed
+
+    # ---------------------------------------------------------------- helpers
+    def allowed_pos(self, p: int) -> Tuple[int, int]:
+        """Allowed id range of the token at absolute position p (an image position)."""
+        return self.cfg.allowed(p - self.P)
+
+    def committed_image(self) -> int:
+        return len(self.tokens) - self.P
+
+    def done(self) -> bool:
+        return self.committed_image() >= self.cfg.n_image
+
+    def _pick(self, logit_rows: np.ndarray, parent, token, allowed, step: int):
+        a = self.cfg.accept
+        if a.mode == "greedy":
+            return acc.accept_greedy(logit_rows, parent, token, allowed)
+        return acc.accept_sampling(logit_rows, parent, token, allowed, temperature=a.temperature,
+                                   top_k=a.top_k, seed=self.accept_seed, step=step, mode=a.mode,
+                                   delta=a.delta, knn=self.knn, knn_k=a.knn_k)
+
+    def _feat_before(self, p: int) -> np.ndarray:
+        return self.feat[p - 1] if p > 0 else np.zeros(self.cfg.model.d_model)
+
+    # ---------------------------------------------------------------- prefill
+    def prefill(self) -> int:
+        """Target and draft over the prefix, then the first image token by one AR step."""
+        P = self.P
+        pos = list(range(P))
+        causal = [list(range(r + 1)) for r in range(P)]
+        logits, f = self.model.target_rows(self.tokens, pos, pos, causal, self.tcache)
+        for p in range(P):
+            self.feat[p] = f[p]
+        par = np.stack([self._feat_before(p) for p in range(P)])
+        self.model.draft_rows(self.tokens, par, pos, pos, causal, self.dcache)
+        lo, hi = self.allowed_pos(P)
+        _, first = self._pick(logits[P - 1:P], [-1], [self.tokens[-1]], np.array([[lo, hi]]), 0)
+        self.tokens.append(first)
+        self.L = P
+        self.Ld = P
+        self.step_no = 1
+        return first
+
+    # ---------------------------------------------------------------- draft side
+    def _draft_catch_up(self):
+        """Draft rows for committed positions Ld..L (the root last).  Returns the root row's
+        (logits, draft feature)."""
+        ps = list(range(self.Ld, self.L + 1))
+        toks = [self.tokens[p] for p in ps]
+        par = np.stack([self._feat_before(p) for p in ps])
+        keys = [list(range(p + 1)) for p in ps]
+        lg, fd = self.model.draft_rows(toks, par, ps, ps, keys, self.dcache)
+        return lg[-1], fd[-1]
+
+    def expand_tree(self, d_hat: int, k_hat: int):
+        L = self.L
+        root_logits, root_feat = self._draft_catch_up()
+        row_slot: Dict[int, int] = {}       # pool index -> draft cache slot of its row
+        row_feat: Dict[int, np.ndarray] = {}
+        next_slot = [L + 1]
+
+        def level_fn(frontier, pool):
+            toks, feats, pos, slots, keys = [], [], [], [], []
+            for u in frontier:
+                node = pool[u]
+                toks.append(node.token)
+                feats.append(root_feat if node.parent == -1 else row_feat[node.parent])
+                pos.append(L + node.depth)
+                slot = next_slot[0]
+                next_slot[0] += 1
+                row_slot[u] = slot
+                slots.append(slot)
+                anc = []
+                v = node.parent
+                while v != -1:
+                    anc.append(row_slot[v])
+                    v = pool[v].parent
+                keys.append(list(range(L + 1)) + sorted(anc) + [slot])
+            lg, fd = self.model.draft_rows(toks, np.stack(feats), pos, slots, keys, self.dcache)
+            for u, frow in zip(frontier, fd):
+                row_feat[u] = frow
+            return lg
+
+        pool, sel = expand(root_logits, level_fn, d_hat, k_hat, self.cfg.sched.n_budget,
+                           lambda depth: self.allowed_pos(L + depth))
+        return build_tree(self.tokens[-1], pool, sel), root_logits
+
+    # ---------------------------------------------------------------- one cycle
+    def verify(self, tree: Tree):
+        L = self.L
+        anc = ancestors_and_self(tree.parent)
+        pos = [L + int(dp) for dp in tree.depth]
+        slots = [L + i for i in range(tree.n)]
+        logits, f = self.model.target_rows(tree.token, pos, slots, tree_key_slots(L, anc), self.tcache)
+        allowed = np.array([self.allowed_pos(L + int(dp) + 1) for dp in tree.depth], dtype=np.int64)
+        return logits, f, allowed
+
+    def schedule_next(self) -> Tuple[int, int]:
+        cell = self.L + 1 - self.P                   # cell of the first drafted token
+        remaining = self.cfg.n_image - cell
+        prev = self.prev
+        if prev is not None and self.cfg.sched.alpha_source == "poisson" and self.poisson is not None:
+            prev = (min(int(self.poisson[self.prev_cell]), prev[1]), prev[1])
+        return schedule(self.cfg.sched, self.records.get(cell - 1), prev, remaining)
+
+    def compact(self, path: List[int]):
+        L = self.L
+        for m, v in enumerate(path, start=1):
+            self.tcache.k[:, :, L + m, :] = self.tcache.k[:, :, L + v, :]
+            self.tcache.v[:, :, L + m, :] = self.tcache.v[:, :, L + v, :]
+
+    def step(self) -> StepInfo:
+        L = self.L
+        d_hat, k_hat = self.schedule_next()
+        draft_root = None
+        if d_hat >= 1:
+            tree, draft_root = self.expand_tree(d_hat, k_hat)
+        else:
+            tree = build_tree(self.tokens[-1], [], [])
+        logits, f, allowed = self.verify(tree)
+        masked = np.stack([masked_logits(logits[i], *allowed[i]) for i in range(tree.n)])
+        path, bonus = self._pick(masked, tree.parent, tree.token, allowed, self.step_no)
+        committed = [int(tree.token[v]) for v in path] + [int(bonus)]
+        self.compact(path)
+        self.feat[L] = f[0]
+        for m, v in enumerate(path, start=1):
+            self.feat[L + m] = f[v]
+        cell0 = L + 1 - self.P
+        for c in range(cell0, cell0 + len(committed)):
+            self.records[c] = (d_hat, k_hat)
+        self.prev = (len(path), d_hat)
+        self.prev_cell = cell0
+        self.tokens += committed
+        self.Ld = L + 1
+        self.L = L + 1 + len(path)
+        info = StepInfo(self.step_no, d_hat, k_hat, tree, logits, allowed, path, int(bonus), committed, L,
+                        draft_root)
+        self.step_no += 1
+        return info
+
+    def run(self, max_steps: Optional[int] = None) -> List[StepInfo]:
+        out = []
+        while not self.done() and (max_steps is None or len(out) < max_steps):
+            out.append(self.step())
+        return out
+
+
+def ar_decode(cfg: DecodeCfg, model: OracleModel, prefix: np.ndarray, n_tokens: Optional[int] = None):
+    """Plain greedy AR reference: prefill, then one target row per token.  Returns
+    (image tokens, per-token logits of the row that predicted each token after the first)."""
+    assert cfg.accept.mode == "greedy"
+    dec = Decoder(cfg, model, prefix)
+    P = dec.P
+    n_tokens = cfg.n_image if n_tokens is None else n_tokens
+    pos = list(range(P))
+    causal = [list(range(r + 1)) for r in range(P)]
+    logits, _ = model.target_rows(dec.tokens, pos, pos, causal, dec.tcache)
+    lo, hi = cfg.allowed(0)
+    toks = [lo + int(np.argmax(logits[P - 1][lo:hi]))]
+    rows = []
+    for i in range(1, n_tokens):
+        p = P + i - 1                                  # position of the latest token
+        lg, _ = model.target_rows([toks[-1]], [p], [p], [list(range(p + 1))], dec.tcache)
+        rows.append(lg[0])
+        lo, hi = cfg.allowed(i)
+        toks.append(lo + int(np.argmax(lg[0][lo:hi])))
+    return toks, rows
