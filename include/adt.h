@@ -1,0 +1,265 @@
+/*
+ * adt.h -- C ABI of the ADT-Tree draft-then-verify hot path on one MI355X (gfx950).
+ *
+ * The method is ADT-Tree, "Fast Inference of Visual Autoregressive Model with
+ * Adjacency-Adaptive Dynamical Draft Trees" (arXiv 2512.21857).  One cycle: a draft head
+ * proposes a tree whose depth and width are chosen per image-grid position (Sec. 4.1,
+ * Sec. 4.2 Eq. 2), the target model verifies all tree nodes in one forward under the
+ * ancestor mask (Sec. 3.1), the accepted root-to-node path plus one bonus token is
+ * committed (Sec. 3.1 Eq. 1; greedy decoding at T = 0 per Sec. 5.1), and the KV cache
+ * is compacted so the accepted nodes become the prefix.
+ *
+ * Conventions for every call:
+ *  - Status: ADT_OK (0) or a negative ADT_E_* code.  On an error nothing is enqueued and
+ *    adt_last_error() returns a message (thread-local).  No C++ exception crosses the ABI.
+ *  - Ownership: the caller allocates and owns every device buffer (weights, caches, tree
+ *    arrays, logits, outputs, workspaces).  The library keeps non-owning pointers and never
+ *    allocates device memory.  Pointers marked [host] are host memory; all others device.
+ *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
+ *    it unless marked "synchronises".
+ *  - Dtypes: ADT_F32 (float) or ADT_BF16 (bfloat16 stored as uint16 bit patterns).
+ *    Row-major layouts.  A KV cache is [slices][S_cap][Dh] with a slice per (layer, head).
+ *  - Trees: node 0 is the root (the last committed token), nodes are in BFS order
+ *    (parent[i] < i), at most ADT_MAX_NODES nodes.  Ancestor masks are packed uint64
+ *    words, ADT_MASK_WORDS per node: bit j of node i set iff j is on the path root..i.
+ */
+#ifndef ADT_H_
+#define ADT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t adt_status;
+
+#define ADT_OK 0
+#define ADT_E_ARG (-1)         /* null pointer, bad enum, bad scalar */
+#define ADT_E_SHAPE (-2)       /* dimension not supported by the kernels (alignment, head size) */
+#define ADT_E_CAPACITY (-3)    /* tree, cache or workspace too small */
+#define ADT_E_HIP (-4)         /* a HIP runtime call failed */
+#define ADT_E_UNSUPPORTED (-5) /* valid request outside what this build implements */
+#define ADT_E_STATE (-6)       /* session used out of order (e.g. step before prefill) */
+
+#define ADT_F32 0
+#define ADT_BF16 1
+
+#define ADT_MAX_NODES 128
+#define ADT_MASK_WORDS 2
+
+#define ADT_ACCEPT_GREEDY 0
+#define ADT_ACCEPT_EXACT 1
+#define ADT_ACCEPT_RELAXED 2
+
+#define ADT_ALPHA_REAL 0
+#define ADT_ALPHA_POISSON 1
+
+int32_t adt_version(void);
+/* Copies the last error message of this thread into buf (NUL-terminated, truncated to cap);
+ * returns its full length. */
+size_t adt_last_error(char* buf, size_t cap);
+
+/* ------------------------------------------------------------------ b2: tree attention
+ * Sec. 3.1: node i attends to the committed prefix and to the nodes on its own
+ * root-to-node path.  For sequence b and head h:
+ *   O[b][i][h] = softmax(scale * q[b][i][h] . K_S^T) V_S,
+ *   S = slots [0, kv_len[b]) (prefix, unmasked) plus slots kv_len[b] + j for every j < n_tail[b]
+ *       whose bit j is set in anc_mask[b][i] (the tail holds the tree nodes' own K/V).
+ * q:        [B][nq_max][H][Dh]        dtype; rows i < n_q[b] are used
+ * k_cache, v_cache: element (b, h, slot, :) at base + b*stride_b + h*stride_h + slot*Dh
+ * kv_len, n_q, n_tail: [B] int32 device arrays; n_q[b] <= n_tail[b] <= ADT_MAX_NODES and
+ *   kv_len[b] + n_tail[b] <= kv_cap (host bound used to size the launch)
+ * anc_mask: [B][nq_max][ADT_MASK_WORDS] uint64
+ * out:      [B][nq_max][H][Dh] dtype (rows >= n_q[b] untouched)
+ * workspace: adt_tree_attn_workspace_size() bytes (split-KV partials)
+ * Dh must be 64 or 128.  bf16 uses MFMA with fp32 accumulation and fp32 softmax; f32 is
+ * computed in fp32 on the vector units. */
+size_t adt_tree_attn_workspace_size(int32_t B, int32_t H, int32_t Dh, int32_t nq_max, int32_t kv_cap);
+adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                         int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                         const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
+                         int32_t kv_cap, float scale, int32_t dtype, void* out, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ a3 support: masks
+ * Ancestor bitmask and depth of every node of B BFS-ordered trees (Sec. 3.1 tree mask):
+ * mask[i] = mask[parent[i]] | bit(i), depth[i] = depth[parent[i]] + 1, root depth 0.
+ * parent: [B][n_max] (parent[b][0] = -1), n_nodes: [B] device; mask: [B][n_max][ADT_MASK_WORDS];
+ * depth may be NULL.  Rows >= n_nodes[b] are zeroed. */
+adt_status adt_tree_masks(const int32_t* parent, const int32_t* n_nodes, int32_t B, int32_t n_max,
+                          uint64_t* mask, int32_t* depth, void* stream);
+
+/* ------------------------------------------------------------------ d1: KV compaction
+ * Implicit in Sec. 3.1 (the accepted tokens become the prefix): for each sequence b and
+ * each cache slice (layer x head), slot L + m <- slot L + path[b][m] for m = 1..n_acc[b],
+ * L = kv_len[b].  path[b][0] is the root (0) and is not read; path[b][m] >= m is required
+ * (BFS order of an accepted chain) so every source is at or after its destination; all
+ * reads of a slice happen before its writes.  Both K and V caches are compacted.
+ * Slice s of sequence b starts at base + b*stride_b + s*stride_slice; rows are Dh long.
+ * n_acc[b] <= a_max <= ADT_MAX_NODES - 1. */
+adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, int32_t slices, int32_t Dh, int64_t stride_b,
+                          int64_t stride_slice, const int32_t* kv_len, const int32_t* path, int32_t path_stride,
+                          const int32_t* n_acc, int32_t a_max, int32_t dtype, void* stream);
+
+/* ------------------------------------------------------------------ c1-c3: acceptance
+ * Walk from the root of one verified tree (Sec. 3.1 Eq. 1; Sec. 5.1).
+ *  GREEDY: t_u = argmax of logits row u over its allowed ids (lowest id on ties); move to
+ *    the child whose token is t_u while one exists; the bonus is t_u of the last node.
+ *  EXACT: Eq. 1 with the drafted top-k children read as point-mass proposals: child x is
+ *    accepted with probability p(x) and on rejection removed from p; siblings are tried in
+ *    node order; with all rejected the bonus is drawn from the residual.  p = softmax of
+ *    logits / temperature over the allowed ids truncated to the top_k largest (0 = all),
+ *    held as integer weights rint(exp(z - max z) * 2^32).
+ *  RELAXED: as EXACT but x is credited with the weights of its nearest codebook neighbours
+ *    knn[x][1..knn_k-1] taken in order while their sum stays <= delta * (remaining total);
+ *    on rejection the credited set is removed.
+ *  Draws: r = floor(U * W / 2^64), U = Philox4x32-10(key = seed, counter = (step, node,
+ *    trial, 0)) words (x1 << 32 | x0), W = remaining total weight.
+ * logits: [n][ld] fp32 (row u gives the target distribution of u's successor)
+ * parent, token: [n] BFS tree; allowed: [n][2] allowed id range [lo, hi) per row; n_nodes: device
+ *   scalar n; n_max [host] = rows allocated in logits/parent/token/allowed (n <= n_max <= ADT_MAX_NODES)
+ * path: [ADT_MAX_NODES] out, path[0] = 0 then v_1..v_a; n_acc, bonus: device scalars out.
+ * workspace: adt_accept_workspace_size(); only sampling modes use it. */
+typedef struct {
+  int32_t mode;        /* ADT_ACCEPT_* */
+  float temperature;   /* > 0 for sampling modes */
+  int32_t top_k;       /* sampling truncation, 0 = none; <= 4096 */
+  float delta;         /* relaxed-mode mass bound, in [0, 1) */
+  int32_t knn_k;       /* neighbours per code used in relaxed mode (row 0 is the code itself) */
+  int32_t knn_rows;    /* rows of the knn table (ids >= knn_rows have no neighbours) */
+  int32_t knn_stride;  /* int32 per knn row */
+  const int32_t* knn;  /* device [knn_rows][knn_stride] */
+  uint64_t seed;
+} adt_accept_cfg;
+
+size_t adt_accept_workspace_size(int32_t V);
+adt_status adt_verify_accept(const float* logits, int64_t ld, int32_t V, const int32_t* parent, const int32_t* token,
+                             const int32_t* allowed, const int32_t* n_nodes, int32_t n_max,
+                             const adt_accept_cfg* cfg /*[host]*/,
+                             uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ weights
+ * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM
+ * kernels stream.  srcs/rows: [host] arrays of n_src device pointers and their row counts;
+ * the sources are stacked in order (mode 0) or, for a gate/up pair (mode 1, n_src = 2,
+ * equal rows), interleaved in blocks of 16 rows (gate block t, up block t, ...).
+ * bf16: rows and K multiples of 16 and 32; dst holds sum(rows)*K bf16.  f32: same order,
+ * row-major.  adt_packed_bytes() gives the size. */
+size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype);
+adt_status adt_pack_weight(const void* const* srcs, const int32_t* rows, int32_t n_src, int32_t K, int32_t mode,
+                           int32_t dtype, void* dst, void* stream);
+
+/* ------------------------------------------------------------------ a0: schedule (host)
+ * Adjacent initialisation (Sec. 4.1, Horizontal Repeat) + bisectional adaptation
+ * (Sec. 4.2, Eq. 2) + the bounds of Sec. 4.2, as inclusive ranges.
+ * have_left: whether the left neighbour cell has a recorded (d, k); have_prev: whether a
+ * previous tree exists, with a_prev accepted draft tokens at depth d_prev; remaining =
+ * image tokens still to commit including this cycle's bonus.  Writes (d_hat, k_hat);
+ * d_hat = 0 means a plain AR step. */
+typedef struct {
+  int32_t d_lo, d_hi, k_lo, k_hi; /* inclusive bounds */
+  int32_t l_d, l_k;               /* adjustment steps of Eq. 2 */
+  float beta;                     /* positive threshold of Eq. 2 */
+  int32_t n_budget;               /* draft nodes kept by the top-N rerank (Eq. 3) */
+  int32_t d0, k0;                 /* first tree */
+  int32_t alpha_source;           /* ADT_ALPHA_REAL or ADT_ALPHA_POISSON */
+} adt_sched_cfg;
+
+adt_status adt_schedule_next(const adt_sched_cfg* cfg, int32_t have_left, int32_t d_left, int32_t k_left,
+                             int32_t have_prev, int32_t a_prev, int32_t d_prev, int32_t remaining, int32_t* d_hat,
+                             int32_t* k_hat);
+
+/* ------------------------------------------------------------------ model and session */
+typedef struct adt_model_s adt_model;
+typedef struct adt_session_s adt_session;
+
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, ffn, vocab;
+  int32_t dtype;
+  float rope_theta, norm_eps;
+  const void* embed;            /* [vocab][d_model] row-major, dtype */
+  const void* lm_head;          /* packed [vocab][d_model] */
+  const void* draft_fc;         /* packed [d_model][2 d_model] (input = [embedding ; parent feature]) */
+  const void* const* w_qkv;     /* [host] n_layers + 1 packed [3d][d] (rows q, k, v); last = draft layer */
+  const void* const* w_o;       /* [host] n_layers + 1 packed [d][d] */
+  const void* const* w_gu;      /* [host] n_layers + 1 packed gate/up interleaved (mode 1) [2F][d] */
+  const void* const* w_down;    /* [host] n_layers + 1 packed [d][F] */
+} adt_model_desc;
+
+adt_status adt_model_create(const adt_model_desc* desc, adt_model** out);
+void adt_model_destroy(adt_model* m);
+
+typedef struct {
+  int32_t prefix_len;           /* committed prompt tokens before the image */
+  int32_t n_image;              /* image tokens (grid cells, raster order) */
+  int32_t s_cap;                /* cache slots; >= prefix_len + n_image + ADT_MAX_NODES */
+  void* k_cache;                /* target [n_layers][n_heads][s_cap][head_dim] */
+  void* v_cache;
+  void* dk_cache;               /* draft  [n_heads][s_cap][head_dim] */
+  void* dv_cache;
+  const int32_t* allowed;       /* [host] [n_image][2] allowed id range [lo, hi) per image cell (copied) */
+  adt_sched_cfg sched;
+  adt_accept_cfg accept;
+  const int32_t* poisson;       /* [host] [n_image] acceptance lengths for ADT_ALPHA_POISSON, else NULL */
+  int32_t fixed_tree;           /* 1: skip the schedule, always (sched.d_hi, sched.k_hi) */
+  void* workspace;
+  size_t workspace_bytes;
+} adt_session_desc;
+
+typedef struct {
+  int32_t step;                 /* cycle index (1 for the first tree) */
+  int32_t d_hat, k_hat;         /* tree shape chosen by the schedule */
+  int32_t n_nodes;              /* verified rows, root included */
+  int32_t n_accepted;           /* a */
+  int32_t n_committed;          /* a + 1 */
+  int32_t tokens[ADT_MAX_NODES];/* committed ids */
+  int32_t done;                 /* 1 once every image token is committed */
+} adt_step_out;
+
+typedef struct {
+  int32_t L;                    /* committed target KV length (root position) */
+  int32_t Ld;                   /* valid draft KV length */
+  int32_t step;                 /* next cycle index */
+  int32_t n_tokens;             /* committed tokens, prompt included */
+  int32_t n_nodes;              /* rows of the current tree */
+  float* logits;                /* [ADT_MAX_NODES][vocab] last verify logits (unmasked) */
+  void* feat;                   /* [ADT_MAX_NODES][d_model] last verify features */
+  float* draft_logits;          /* [1 + (d_hi-1) k_hi][vocab] root row then frontier rows, per level */
+  int32_t* parent; int32_t* token; int32_t* depth; float* score; uint64_t* mask;  /* current tree */
+  int32_t* allowed_rows;        /* [ADT_MAX_NODES][2] allowed range of each row's successor */
+  int32_t* path; int32_t* n_acc; int32_t* bonus;  /* last acceptance */
+  const int32_t* tokens_host;   /* [host] committed ids */
+} adt_session_view;
+
+size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* desc);
+adt_status adt_session_create(const adt_model* m, const adt_session_desc* desc, adt_session** out);
+void adt_session_destroy(adt_session* s);
+/* Target and draft over the prompt, then the first image token by one AR step (greedy or a
+ * draw at step 0).  prefix: [host] prefix_len ids.  Synchronises. */
+adt_status adt_session_prefill(adt_session* s, const int32_t* prefix, int32_t* first_token, void* stream);
+adt_status adt_session_get_view(const adt_session* s, adt_session_view* v);
+
+/* a1-a3: the draft head's catch-up rows then d_hat - 1 frontier forwards (Sec. 4.2, Eq. 4),
+ * top-k children scored by summed log-probability (Eq. 3), frontier select, top-N rerank and
+ * the BFS tree arrays + masks of the session's current tree.  n_nodes_out [host] gets the
+ * tree size (root included). */
+adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_hat, int32_t n_budget, int32_t* n_nodes_out,
+                           void* stream);
+/* Replaces the session's current tree with a caller tree: parent/token [host] n ids. */
+adt_status adt_session_set_tree(adt_session* s, const int32_t* parent, const int32_t* token, int32_t n,
+                                void* stream);
+/* b1-b3: the target forward of the session's current tree at the committed length L:
+ * K/V of node i go to slot L + i, logits and features into the session buffers. */
+adt_status adt_verify_forward(adt_session* s, void* stream);
+/* c + d1 for the session: accept on the last verify, compact both caches, commit.  Synchronises. */
+adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_hat, adt_step_out* out, void* stream);
+/* One full cycle: a0 + a1-a3 + b + c + d1.  Synchronises once (the accepted path). */
+adt_status adt_step(adt_session* s, adt_step_out* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ADT_H_ */

@@ -50,6 +50,14 @@ class StepInfo:
     draft_root_logits: Optional[np.ndarray] = None
 
 
+def compact_cache(k: np.ndarray, v: np.ndarray, L: int, path: List[int]) -> None:
+    """KV compaction: the accepted nodes v_1 < .. < v_a take cache slots L+1 .. L+a (slot axis
+    is the second to last), in order, so that they become the committed prefix."""
+    for m, node in enumerate(path, start=1):
+        k[..., L + m, :] = k[..., L + node, :]
+        v[..., L + m, :] = v[..., L + node, :]
+
+
 class Decoder:
     """Oracle decode state for one image."""
 
@@ -177,19 +185,20 @@ class Decoder:
         return schedule(self.cfg.sched, self.records.get(cell - 1), prev, remaining)
 
     def compact(self, path: List[int]):
-        L = self.L
-        for m, v in enumerate(path, start=1):
-            self.tcache.k[:, :, L + m, :] = self.tcache.k[:, :, L + v, :]
-            self.tcache.v[:, :, L + m, :] = self.tcache.v[:, :, L + v, :]
+        compact_cache(self.tcache.k, self.tcache.v, self.L, path)
 
     def step(self) -> StepInfo:
-        L = self.L
         d_hat, k_hat = self.schedule_next()
-        draft_root = None
         if d_hat >= 1:
             tree, draft_root = self.expand_tree(d_hat, k_hat)
-        else:
-            tree = build_tree(self.tokens[-1], [], [])
+            return self.verify_commit(tree, d_hat, k_hat, expanded=True, draft_root=draft_root)
+        return self.verify_commit(build_tree(self.tokens[-1], [], []), d_hat, k_hat, expanded=False)
+
+    def verify_commit(self, tree: Tree, d_hat: int, k_hat: int, expanded: bool = False,
+                      draft_root: Optional[np.ndarray] = None) -> StepInfo:
+        """Verify a tree, accept along it, compact and commit.  Without a preceding expansion
+        (expanded=False) the draft cache was not advanced, so its valid length stays."""
+        L = self.L
         logits, f, allowed = self.verify(tree)
         masked = np.stack([masked_logits(logits[i], *allowed[i]) for i in range(tree.n)])
         path, bonus = self._pick(masked, tree.parent, tree.token, allowed, self.step_no)
@@ -204,7 +213,8 @@ class Decoder:
         self.prev = (len(path), d_hat)
         self.prev_cell = cell0
         self.tokens += committed
-        self.Ld = L + 1
+        if expanded:
+            self.Ld = L + 1
         self.L = L + 1 + len(path)
         info = StepInfo(self.step_no, d_hat, k_hat, tree, logits, allowed, path, int(bonus), committed, L,
                         draft_root)

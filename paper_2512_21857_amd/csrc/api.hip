@@ -1,0 +1,796 @@
+// C ABI of the ADT-Tree hot path: argument checks, the host-side schedule, workspace
+// layout and the orchestration of one draft-then-verify cycle.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "launch.h"
+
+namespace adt {
+
+static thread_local char g_err[512];
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+static inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Bump {
+  char* base;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    off = align_up(off, 256);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+}  // namespace adt
+
+using namespace adt;
+
+static constexpr int R = ADT_MAX_NODES;
+
+extern "C" int32_t adt_version(void) { return 1; }
+
+extern "C" size_t adt_last_error(char* buf, size_t cap) {
+  const size_t n = strlen(g_err);
+  if (buf && cap) {
+    const size_t c = n < cap - 1 ? n : cap - 1;
+    memcpy(buf, g_err, c);
+    buf[c] = 0;
+  }
+  return n;
+}
+
+static bool valid_dtype(int32_t dt) { return dt == ADT_F32 || dt == ADT_BF16; }
+static size_t esize(int32_t dt) { return dt == ADT_BF16 ? 2 : 4; }
+
+// ============================================================================ standalone calls
+extern "C" size_t adt_tree_attn_workspace_size(int32_t B, int32_t H, int32_t Dh, int32_t nq_max, int32_t kv_cap) {
+  return tree_attn_ws_bytes(B, H, Dh, nq_max, kv_cap, ADT_BF16);
+}
+
+extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                                    int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                                    const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
+                                    int32_t kv_cap, float scale, int32_t dtype, void* out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  ADT_CHECK_ARG(q && k_cache && v_cache && kv_len && n_q && n_tail && anc_mask && out, ADT_E_ARG,
+                "tree_attn: null pointer");
+  ADT_CHECK_ARG(valid_dtype(dtype), ADT_E_ARG, "tree_attn: bad dtype %d", dtype);
+  ADT_CHECK_ARG(B >= 1 && H >= 1 && kv_cap >= 1, ADT_E_ARG, "tree_attn: B=%d H=%d kv_cap=%d", B, H, kv_cap);
+  ADT_CHECK_ARG(Dh == 64 || Dh == 128, ADT_E_SHAPE, "tree_attn: head_dim %d not in {64, 128}", Dh);
+  ADT_CHECK_ARG(nq_max >= 1 && nq_max <= ADT_MAX_NODES, ADT_E_CAPACITY, "tree_attn: nq_max %d", nq_max);
+  ADT_CHECK_ARG(stride_h >= (int64_t)kv_cap * Dh, ADT_E_SHAPE, "tree_attn: stride_h %lld < kv_cap*Dh",
+                (long long)stride_h);
+  ADT_CHECK_ARG(B == 1 || stride_b >= (int64_t)H * stride_h, ADT_E_SHAPE, "tree_attn: stride_b too small");
+  ADT_CHECK_ARG(std::isfinite(scale) && scale > 0.f, ADT_E_ARG, "tree_attn: scale");
+  return launch_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask, B, H, Dh, nq_max,
+                          kv_cap, scale, dtype, out, workspace, workspace_bytes, (hipStream_t)stream);
+}
+
+extern "C" adt_status adt_tree_masks(const int32_t* parent, const int32_t* n_nodes, int32_t B, int32_t n_max,
+                                     uint64_t* mask, int32_t* depth, void* stream) {
+  ADT_CHECK_ARG(parent && n_nodes && mask && B >= 1, ADT_E_ARG, "tree_masks: bad arguments");
+  ADT_CHECK_ARG(n_max >= 1 && n_max <= ADT_MAX_NODES, ADT_E_CAPACITY, "tree_masks: n_max %d", n_max);
+  return launch_tree_masks(parent, n_nodes, B, n_max, mask, depth, (hipStream_t)stream);
+}
+
+extern "C" adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, int32_t slices, int32_t Dh,
+                                     int64_t stride_b, int64_t stride_slice, const int32_t* kv_len, const int32_t* path,
+                                     int32_t path_stride, const int32_t* n_acc, int32_t a_max, int32_t dtype,
+                                     void* stream) {
+  ADT_CHECK_ARG(k_cache && v_cache && kv_len && path && n_acc, ADT_E_ARG, "kv_compact: null pointer");
+  ADT_CHECK_ARG(valid_dtype(dtype) && B >= 1 && slices >= 1 && Dh >= 1, ADT_E_ARG, "kv_compact: bad sizes");
+  ADT_CHECK_ARG(a_max >= 0 && a_max < ADT_MAX_NODES && path_stride >= a_max + 1, ADT_E_CAPACITY,
+                "kv_compact: a_max %d path_stride %d", a_max, path_stride);
+  if (a_max == 0) return ADT_OK;
+  return launch_kv_compact(k_cache, v_cache, B, slices, Dh, stride_b, stride_slice, kv_len, path, path_stride, n_acc,
+                           a_max, dtype, (hipStream_t)stream);
+}
+
+extern "C" size_t adt_accept_workspace_size(int32_t V) {
+  return align_up(accept_ws_bytes(V), 256) + (size_t)R * 16 * 8 + (size_t)R * 4 + 1024;
+}
+
+static adt_status accept_impl(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
+                              const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
+                              uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
+                              hipStream_t st) {
+  ADT_CHECK_ARG(ws && ws_bytes >= adt_accept_workspace_size(V), ADT_E_CAPACITY, "accept: workspace too small");
+  Bump b{(char*)ws};
+  int32_t* top_id = b.take<int32_t>((size_t)R * 16);
+  float* top_val = b.take<float>((size_t)R * 16);
+  float* lse = b.take<float>(R);
+  void* rest = b.take<char>(accept_ws_bytes(V));
+  if (cfg.mode == ADT_ACCEPT_GREEDY) {
+    adt_status e = launch_row_topk(logits, ld, V, allowed, n_max, 1, 1, top_id, top_val, lse, st);
+    if (e) return e;
+    return launch_accept_greedy(top_id, 1, parent, token, n_nodes, n_max, path, n_acc, bonus, st);
+  }
+  return launch_accept_sample(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg, step, path, n_acc, bonus,
+                              rest, accept_ws_bytes(V), st);
+}
+
+static adt_status check_accept_cfg(const adt_accept_cfg* cfg) {
+  ADT_CHECK_ARG(cfg != nullptr, ADT_E_ARG, "accept: null cfg");
+  ADT_CHECK_ARG(cfg->mode >= ADT_ACCEPT_GREEDY && cfg->mode <= ADT_ACCEPT_RELAXED, ADT_E_ARG, "accept: mode %d",
+                cfg->mode);
+  if (cfg->mode != ADT_ACCEPT_GREEDY) {
+    ADT_CHECK_ARG(cfg->temperature > 0.f && std::isfinite(cfg->temperature), ADT_E_ARG, "accept: temperature");
+    ADT_CHECK_ARG(cfg->top_k >= 0 && cfg->top_k <= 4096, ADT_E_UNSUPPORTED, "accept: top_k %d", cfg->top_k);
+  }
+  if (cfg->mode == ADT_ACCEPT_RELAXED) {
+    ADT_CHECK_ARG(cfg->delta >= 0.f && cfg->delta < 1.f, ADT_E_ARG, "accept: delta");
+    ADT_CHECK_ARG(cfg->knn_k >= 1 && (cfg->knn_k == 1 || (cfg->knn && cfg->knn_stride >= cfg->knn_k)), ADT_E_ARG,
+                  "accept: knn table");
+  }
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_verify_accept(const float* logits, int64_t ld, int32_t V, const int32_t* parent,
+                                        const int32_t* token, const int32_t* allowed, const int32_t* n_nodes,
+                                        int32_t n_max, const adt_accept_cfg* cfg, uint64_t step, int32_t* path,
+                                        int32_t* n_acc, int32_t* bonus, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+  ADT_CHECK_ARG(logits && parent && token && allowed && n_nodes && path && n_acc && bonus, ADT_E_ARG,
+                "verify_accept: null pointer");
+  ADT_CHECK_ARG(V >= 1 && ld >= V, ADT_E_ARG, "verify_accept: V %d ld %lld", V, (long long)ld);
+  ADT_CHECK_ARG(n_max >= 1 && n_max <= ADT_MAX_NODES, ADT_E_CAPACITY, "verify_accept: n_max %d", n_max);
+  adt_status e = check_accept_cfg(cfg);
+  if (e) return e;
+  return accept_impl(logits, ld, V, parent, token, allowed, n_nodes, n_max, *cfg, step, path, n_acc, bonus, workspace,
+                     workspace_bytes, (hipStream_t)stream);
+}
+
+extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype) {
+  return packed_bytes(total_rows, K, dtype);
+}
+
+extern "C" adt_status adt_pack_weight(const void* const* srcs, const int32_t* rows, int32_t n_src, int32_t K,
+                                      int32_t mode, int32_t dtype, void* dst, void* stream) {
+  ADT_CHECK_ARG(valid_dtype(dtype) && K >= 1, ADT_E_ARG, "pack: dtype/K");
+  return launch_pack(srcs, rows, n_src, K, mode, dtype, dst, (hipStream_t)stream);
+}
+
+extern "C" adt_status adt_schedule_next(const adt_sched_cfg* c, int32_t have_left, int32_t d_left, int32_t k_left,
+                                        int32_t have_prev, int32_t a_prev, int32_t d_prev, int32_t remaining,
+                                        int32_t* d_hat, int32_t* k_hat) {
+  ADT_CHECK_ARG(c && d_hat && k_hat, ADT_E_ARG, "schedule: null pointer");
+  ADT_CHECK_ARG(c->d_lo >= 1 && c->d_lo <= c->d_hi && c->k_lo >= 1 && c->k_lo <= c->k_hi, ADT_E_ARG,
+                "schedule: bad bounds");
+  ADT_CHECK_ARG(remaining >= 1, ADT_E_ARG, "schedule: nothing remains");
+  int d, k;
+  if (!have_left) {
+    d = c->d0;
+    k = c->k0;
+  } else {
+    d = d_left;
+    k = k_left;
+    if (have_prev && d_prev > 0) {
+      // Eq. 2: alpha = a / d compared with beta exactly as a >= beta * d.
+      if ((double)a_prev >= (double)c->beta * (double)d_prev) {
+        d += c->l_d;
+        k -= c->l_k;
+      } else {
+        d -= c->l_d;
+        k += c->l_k;
+      }
+    }
+  }
+  d = std::max(c->d_lo, std::min(c->d_hi, d));
+  k = std::max(c->k_lo, std::min(c->k_hi, k));
+  d = std::min(d, remaining - 1);
+  *d_hat = d;
+  *k_hat = k;
+  return ADT_OK;
+}
+
+// ============================================================================ model
+struct adt_model_s {
+  adt_model_desc d;
+  std::vector<const void*> qkv, o, gu, down;
+};
+
+extern "C" adt_status adt_model_create(const adt_model_desc* d, adt_model** out) {
+  ADT_CHECK_ARG(d && out, ADT_E_ARG, "model_create: null pointer");
+  ADT_CHECK_ARG(valid_dtype(d->dtype), ADT_E_ARG, "model_create: dtype");
+  ADT_CHECK_ARG(d->n_layers >= 1 && d->n_heads >= 1 && d->ffn >= 1 && d->vocab >= 1, ADT_E_ARG, "model_create: dims");
+  ADT_CHECK_ARG(d->head_dim == 64 || d->head_dim == 128, ADT_E_SHAPE, "model_create: head_dim %d", d->head_dim);
+  ADT_CHECK_ARG(d->d_model == d->n_heads * d->head_dim, ADT_E_SHAPE, "model_create: d_model != heads*head_dim");
+  if (d->dtype == ADT_BF16)
+    ADT_CHECK_ARG(d->d_model % 32 == 0 && d->ffn % 32 == 0 && d->vocab % 16 == 0, ADT_E_SHAPE,
+                  "model_create: bf16 needs d_model, ffn multiples of 32 and vocab of 16");
+  ADT_CHECK_ARG(d->embed && d->lm_head && d->draft_fc && d->w_qkv && d->w_o && d->w_gu && d->w_down, ADT_E_ARG,
+                "model_create: missing weights");
+  adt_model_s* m = new (std::nothrow) adt_model_s();
+  ADT_CHECK_ARG(m != nullptr, ADT_E_ARG, "model_create: out of host memory");
+  m->d = *d;
+  for (int l = 0; l <= d->n_layers; ++l) {
+    if (!d->w_qkv[l] || !d->w_o[l] || !d->w_gu[l] || !d->w_down[l]) {
+      delete m;
+      set_error("model_create: layer %d weight missing", l);
+      return ADT_E_ARG;
+    }
+    m->qkv.push_back(d->w_qkv[l]);
+    m->o.push_back(d->w_o[l]);
+    m->gu.push_back(d->w_gu[l]);
+    m->down.push_back(d->w_down[l]);
+  }
+  m->d.w_qkv = m->d.w_o = m->d.w_gu = m->d.w_down = nullptr;
+  *out = m;
+  return ADT_OK;
+}
+
+extern "C" void adt_model_destroy(adt_model* m) { delete m; }
+
+// ============================================================================ session
+struct TreeBufs {
+  int32_t *parent, *token, *depth, *pos, *allowed_rows, *n, *path, *nacc, *bonus;
+  float* score;
+  uint64_t* mask;
+};
+
+struct adt_session_s {
+  const adt_model_s* m;
+  adt_session_desc d;
+  int dt, Lr, dm, H, Dh, F, V, P, T;
+  int C0;       // first draft-feature row of draft tree rows
+  int DR;       // draft-feature rows
+  int DLR;      // draft logits rows
+  int KR;       // frontier rows capacity
+  int C;        // pool capacity
+  // host state
+  bool prefilled = false;
+  bool expanded = false;   // the current tree came from adt_tree_expand (draft root row written)
+  int L = 0, Ld = 0, step = 1, n_nodes = 0;
+  std::vector<int32_t> tokens, allowed_h, poisson;
+  std::vector<int32_t> rec_d, rec_k, has_rec;
+  bool have_prev = false;
+  int a_prev = 0, d_prev = 0, prev_cell = 0;
+  // device buffers
+  float *h, *part, *logits, *dlogits;
+  void *act, *xin, *q, *att, *sw, *feat, *cfeat, *dfeat;
+  size_t part_elems;
+  TreeBufs tr;
+  int32_t* allowed_img;
+  Pool pool;
+  int32_t *sel_rank, *bfs_of;
+  NextRows nx[2];
+  int32_t *ctok, *cfsrc, *cpos, *idx;
+  uint64_t* cmask;
+  int32_t *top_id, *allowed_lvl, *scal;
+  float *top_val, *lse;
+  void* attn_ws;
+  size_t attn_ws_bytes;
+  void* acc_ws;
+  size_t acc_ws_bytes;
+};
+
+static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_session_desc* d) {
+  const adt_model_desc& md = m->d;
+  s->m = m;
+  s->d = *d;
+  s->dt = md.dtype;
+  s->Lr = md.n_layers;
+  s->dm = md.d_model;
+  s->H = md.n_heads;
+  s->Dh = md.head_dim;
+  s->F = md.ffn;
+  s->V = md.vocab;
+  s->P = d->prefix_len;
+  s->T = d->n_image;
+  const int dh = d->sched.d_hi, kh = d->sched.k_hi;
+  s->C0 = dh + 2;
+  s->DR = s->C0 + std::max(1, (dh - 1) * kh);
+  s->DLR = 1 + std::max(0, (dh - 1) * kh);
+  s->KR = std::max(kh, 1);
+  s->C = std::max(1, kh + (dh - 1) * kh * kh);
+  const int S = std::max({gemm_splits(R, 3 * s->dm, s->dm, s->dt), gemm_splits(R, s->dm, s->dm, s->dt),
+                          gemm_splits(R, 2 * s->F, s->dm, s->dt), gemm_splits(R, s->dm, s->F, s->dt),
+                          gemm_splits(R, s->V, s->dm, s->dt), gemm_splits(R, s->dm, 2 * s->dm, s->dt)});
+  (void)S;
+  size_t pe = 0;
+  const int shapes[6][2] = {{3 * s->dm, s->dm}, {s->dm, s->dm}, {2 * s->F, s->dm},
+                            {s->dm, s->F},      {s->V, s->dm},  {s->dm, 2 * s->dm}};
+  for (auto& sh : shapes) pe = std::max(pe, (size_t)gemm_splits(R, sh[0], sh[1], s->dt) * R * sh[0]);
+  s->part_elems = pe;
+}
+
+static size_t session_layout(adt_session_s* s, char* base) {
+  Bump b{base};
+  const size_t es = esize(s->dt);
+  const int dm = s->dm;
+  s->h = b.take<float>((size_t)R * dm);
+  s->act = b.take<char>((size_t)R * dm * es);
+  s->xin = b.take<char>((size_t)R * 2 * dm * es);
+  s->q = b.take<char>((size_t)R * dm * es);
+  s->att = b.take<char>((size_t)R * dm * es);
+  s->sw = b.take<char>((size_t)R * s->F * es);
+  s->feat = b.take<char>((size_t)R * dm * es);
+  s->cfeat = b.take<char>((size_t)s->C0 * dm * es);
+  s->dfeat = b.take<char>((size_t)s->DR * dm * es);
+  s->part = b.take<float>(s->part_elems);
+  s->logits = b.take<float>((size_t)R * s->V);
+  s->dlogits = b.take<float>((size_t)s->DLR * s->V);
+  TreeBufs& t = s->tr;
+  t.parent = b.take<int32_t>(R);
+  t.token = b.take<int32_t>(R);
+  t.depth = b.take<int32_t>(R);
+  t.pos = b.take<int32_t>(R);
+  t.allowed_rows = b.take<int32_t>(2 * R);
+  t.n = b.take<int32_t>(4);
+  t.path = b.take<int32_t>(R);
+  t.nacc = b.take<int32_t>(4);
+  t.bonus = b.take<int32_t>(4);
+  t.score = b.take<float>(R);
+  t.mask = b.take<uint64_t>(2 * R);
+  s->allowed_img = b.take<int32_t>((size_t)2 * s->T);
+  s->pool.token = b.take<int32_t>(s->C);
+  s->pool.score = b.take<float>(s->C);
+  s->pool.depth = b.take<int32_t>(s->C);
+  s->pool.parent = b.take<int32_t>(s->C);
+  s->pool.drow = b.take<int32_t>(s->C);
+  s->pool.rmask = b.take<uint64_t>((size_t)2 * std::max(1, s->DR - s->C0));
+  s->sel_rank = b.take<int32_t>(s->C);
+  s->bfs_of = b.take<int32_t>(s->C);
+  for (int i = 0; i < 2; ++i) {
+    s->nx[i].tok = b.take<int32_t>(s->KR);
+    s->nx[i].fsrc = b.take<int32_t>(s->KR);
+    s->nx[i].pos = b.take<int32_t>(s->KR);
+    s->nx[i].mask = b.take<uint64_t>(2 * s->KR);
+    s->nx[i].frontier = b.take<int32_t>(s->KR);
+  }
+  s->ctok = b.take<int32_t>(R);
+  s->cfsrc = b.take<int32_t>(R);
+  s->cpos = b.take<int32_t>(R);
+  s->idx = b.take<int32_t>(R);
+  s->cmask = b.take<uint64_t>(2 * R);
+  s->top_id = b.take<int32_t>((size_t)R * 16);
+  s->top_val = b.take<float>((size_t)R * 16);
+  s->lse = b.take<float>(R);
+  s->allowed_lvl = b.take<int32_t>(2 * R);
+  s->scal = b.take<int32_t>(16);
+  s->attn_ws_bytes = tree_attn_ws_bytes(1, s->H, s->Dh, R, s->d.s_cap, s->dt);
+  s->attn_ws = b.take<char>(std::max<size_t>(s->attn_ws_bytes, 256));
+  s->acc_ws_bytes = adt_accept_workspace_size(s->V);
+  s->acc_ws = b.take<char>(s->acc_ws_bytes);
+  return align_up(b.off, 256);
+}
+
+static adt_status check_session_desc(const adt_model* m, const adt_session_desc* d) {
+  ADT_CHECK_ARG(m && d, ADT_E_ARG, "session: null pointer");
+  ADT_CHECK_ARG(d->prefix_len >= 1 && d->prefix_len <= R, ADT_E_CAPACITY, "session: prefix_len %d not in [1,%d]",
+                d->prefix_len, R);
+  ADT_CHECK_ARG(d->n_image >= 1, ADT_E_ARG, "session: n_image");
+  ADT_CHECK_ARG(d->s_cap >= d->prefix_len + d->n_image + R, ADT_E_CAPACITY, "session: s_cap %d too small", d->s_cap);
+  ADT_CHECK_ARG(d->k_cache && d->v_cache && d->dk_cache && d->dv_cache && d->allowed, ADT_E_ARG,
+                "session: caches / allowed table missing");
+  const adt_sched_cfg& c = d->sched;
+  ADT_CHECK_ARG(c.d_lo >= 1 && c.d_lo <= c.d_hi && c.k_lo >= 1 && c.k_lo <= c.k_hi, ADT_E_ARG, "session: bounds");
+  ADT_CHECK_ARG(c.d_hi <= 30 && c.k_hi <= 16, ADT_E_UNSUPPORTED, "session: d_hi <= 30 and k_hi <= 16 supported");
+  ADT_CHECK_ARG(c.n_budget >= 1 && c.n_budget <= R - 1, ADT_E_CAPACITY, "session: n_budget %d", c.n_budget);
+  ADT_CHECK_ARG((c.d_hi - 1) * c.k_hi <= R, ADT_E_CAPACITY, "session: draft tree rows exceed %d", R);
+  ADT_CHECK_ARG(c.alpha_source == ADT_ALPHA_REAL || (c.alpha_source == ADT_ALPHA_POISSON && d->poisson), ADT_E_ARG,
+                "session: alpha source");
+  for (int g = 0; g < d->n_image; ++g) {
+    const int lo = d->allowed[2 * g], hi = d->allowed[2 * g + 1];
+    ADT_CHECK_ARG(0 <= lo && lo < hi && hi <= m->d.vocab, ADT_E_ARG, "session: allowed range of cell %d", g);
+  }
+  return check_accept_cfg(&d->accept);
+}
+
+extern "C" size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* d) {
+  if (check_session_desc(m, d)) return 0;
+  adt_session_s s;
+  session_dims(&s, m, d);
+  return session_layout(&s, nullptr);
+}
+
+extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_desc* d, adt_session** out) {
+  adt_status e = check_session_desc(m, d);
+  if (e) return e;
+  ADT_CHECK_ARG(out != nullptr, ADT_E_ARG, "session_create: null out");
+  adt_session_s* s = new (std::nothrow) adt_session_s();
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "session_create: out of host memory");
+  session_dims(s, m, d);
+  const size_t need = session_layout(s, nullptr);
+  if (!d->workspace || d->workspace_bytes < need) {
+    delete s;
+    set_error("session_create: workspace %zu < %zu bytes", d->workspace_bytes, need);
+    return ADT_E_CAPACITY;
+  }
+  session_layout(s, (char*)d->workspace);
+  s->allowed_h.assign(d->allowed, d->allowed + 2 * d->n_image);
+  if (d->poisson) s->poisson.assign(d->poisson, d->poisson + d->n_image);
+  s->rec_d.assign(d->n_image, 0);
+  s->rec_k.assign(d->n_image, 0);
+  s->has_rec.assign(d->n_image, 0);
+  s->d.allowed = nullptr;
+  s->d.poisson = nullptr;
+  hipError_t he = hipMemcpy(s->allowed_img, s->allowed_h.data(), sizeof(int32_t) * 2 * s->T, hipMemcpyHostToDevice);
+  if (he != hipSuccess) {
+    delete s;
+    set_error("session_create: %s", hipGetErrorString(he));
+    return ADT_E_HIP;
+  }
+  *out = s;
+  return ADT_OK;
+}
+
+extern "C" void adt_session_destroy(adt_session* s) { delete s; }
+
+#define TRY(x)                \
+  do {                        \
+    adt_status e__ = (x);     \
+    if (e__ != ADT_OK) return e__; \
+  } while (0)
+
+static SmallI32 small_of(const int32_t* v, int n) {
+  SmallI32 s{};
+  for (int i = 0; i < n && i < 32; ++i) s.v[i] = v[i];
+  return s;
+}
+
+static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, hipStream_t st) {
+  int32_t v[3] = {kv_len, nq, ntail};
+  return launch_set_i32(s->scal, small_of(v, 3), 3, st);
+}
+
+// Decoder layers over M rows.  Cache stack `kc/vc` has stride_layer between layers.
+static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
+                             const uint64_t* mask, void* final_out, hipStream_t st) {
+  const adt_model_s* m = s->m;
+  const int dm = s->dm, H = s->H, Dh = s->Dh, F = s->F, dt = s->dt;
+  const size_t es = esize(dt);
+  const int64_t stride_h = (int64_t)s->d.s_cap * Dh;
+  const float eps = m->d.norm_eps;
+  const float scale = 1.f / std::sqrt((float)Dh);
+  TRY(set_scalars(s, L_pre, M, n_tail, st));
+  const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
+  for (int l = l0; l < l1; ++l) {
+    char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
+    char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
+    int S = gemm_splits(M, 3 * dm, dm, dt);
+    TRY(launch_gemm(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
+    TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, slot0, m->d.rope_theta, s->q, kc, vc, stride_h, dt, st));
+    TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M,
+                         L_pre + n_tail, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
+    S = gemm_splits(M, dm, dm, dt);
+    TRY(launch_gemm(s->att, dm, m->o[l], M, dm, dm, S, dt, s->part, st));
+    TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, s->act, dt, st));
+    S = gemm_splits(M, 2 * F, dm, dt);
+    TRY(launch_gemm(s->act, dm, m->gu[l], M, 2 * F, dm, S, dt, s->part, st));
+    TRY(launch_swiglu(s->part, S, M, F, s->sw, dt, st));
+    S = gemm_splits(M, dm, F, dt);
+    TRY(launch_gemm(s->sw, F, m->down[l], M, dm, F, S, dt, s->part, st));
+    TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
+  }
+  return ADT_OK;
+}
+
+static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, hipStream_t st) {
+  const int S = gemm_splits(M, s->V, s->dm, s->dt);
+  TRY(launch_gemm(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, S, s->dt, s->part, st));
+  return launch_reduce_store(s->part, S, M, s->V, out, s->V, st);
+}
+
+// Target forward of M rows with tokens tok; features into s->feat; logits of rows
+// [lm_row0, lm_row0 + lm_rows) into s->logits.
+static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, const int32_t* pos, int slot0, int L_pre,
+                                 int n_tail, const uint64_t* mask, int lm_row0, int lm_rows, hipStream_t st) {
+  TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, st));
+  TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, st));
+  if (lm_rows > 0)
+    TRY(lm_head(s, (const char*)s->feat + (size_t)lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits, st));
+  return ADT_OK;
+}
+
+// Draft-head forward: FC over [embedding ; parent feature], one decoder layer, final norm
+// into feature rows fout (may be null), target LM head for rows [lm_row0, +lm_rows) into out.
+static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int32_t* fsrc, const void* fa, int M,
+                                const int32_t* pos, int slot0, int L_pre, int n_tail, const uint64_t* mask, void* fout,
+                                int lm_row0, int lm_rows, float* lout, hipStream_t st) {
+  const int dm = s->dm, dt = s->dt;
+  TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, st));
+  const int S = gemm_splits(M, dm, 2 * dm, dt);
+  TRY(launch_gemm(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, st));
+  TRY(launch_add_norm(s->part, S, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, st));
+  TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, st));
+  if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, st));
+  return ADT_OK;
+}
+
+static adt_status sync_stream(hipStream_t st) {
+  ADT_HIP(hipStreamSynchronize(st));
+  return ADT_OK;
+}
+
+static adt_status set_root_only_tree(adt_session_s* s, int root_token, int L, hipStream_t st) {
+  int32_t v[1] = {1};
+  TRY(launch_set_i32(s->tr.n, small_of(v, 1), 1, st));
+  int32_t p[1] = {-1};
+  TRY(launch_set_i32(s->tr.parent, small_of(p, 1), 1, st));
+  int32_t t[1] = {root_token};
+  TRY(launch_set_i32(s->tr.token, small_of(t, 1), 1, st));
+  TRY(launch_tree_masks(s->tr.parent, s->tr.n, 1, R, s->tr.mask, s->tr.depth, st));
+  TRY(launch_tree_rows(s->tr.depth, s->tr.n, R, L, s->P, s->T, s->allowed_img, s->tr.pos, s->tr.allowed_rows,
+                       s->tr.score, st));
+  s->n_nodes = 1;
+  s->expanded = false;
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_session_prefill(adt_session* s, const int32_t* prefix, int32_t* first_token, void* stream) {
+  ADT_CHECK_ARG(s && prefix, ADT_E_ARG, "prefill: null pointer");
+  ADT_CHECK_ARG(!s->prefilled, ADT_E_STATE, "prefill: already prefilled");
+  hipStream_t st = (hipStream_t)stream;
+  const int P = s->P;
+  for (int i = 0; i < P; ++i) ADT_CHECK_ARG(prefix[i] >= 0 && prefix[i] < s->V, ADT_E_ARG, "prefill: id %d", prefix[i]);
+  ADT_HIP(hipMemcpyAsync(s->ctok, prefix, sizeof(int32_t) * P, hipMemcpyHostToDevice, st));
+  TRY(sync_stream(st));
+  TRY(launch_iota(s->cpos, P, 0, 1, st));
+  TRY(launch_chain_masks(s->cmask, P, st));
+  // target over the prompt; logits of the last row predict the first image token
+  TRY(target_forward(s, s->ctok, P, s->cpos, 0, 0, P, s->cmask, P - 1, 1, st));
+  TRY(set_root_only_tree(s, prefix[P - 1], P - 1, st));
+  // the root-only tree's successor is image cell 0
+  TRY(launch_fill_pairs(s->tr.allowed_rows, 1, s->allowed_h[0], s->allowed_h[1], st));
+  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, 1, s->d.accept, 0,
+                  s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
+  // draft head over the prompt: row p takes the target feature of p-1 (zeros for p = 0)
+  TRY(launch_iota(s->cfsrc, P, -1, 1, st));
+  TRY(draft_forward(s, s->ctok, s->cfsrc, s->feat, P, s->cpos, 0, 0, P, s->cmask, nullptr, 0, 0, nullptr, st));
+  int32_t li[1] = {P - 1};
+  TRY(launch_set_i32(s->idx, small_of(li, 1), 1, st));
+  TRY(launch_gather_rows(s->feat, s->idx, 1, s->dm, s->cfeat, s->dt, st));
+  int32_t first = 0;
+  ADT_HIP(hipMemcpyAsync(&first, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  TRY(sync_stream(st));
+  s->tokens.assign(prefix, prefix + P);
+  s->tokens.push_back(first);
+  s->L = P;
+  s->Ld = P;
+  s->step = 1;
+  s->prefilled = true;
+  s->have_prev = false;
+  if (first_token) *first_token = first;
+  return ADT_OK;
+}
+
+static void cell_range(const adt_session_s* s, int cell, int& lo, int& hi) {
+  cell = std::max(0, std::min(s->T - 1, cell));
+  lo = s->allowed_h[2 * cell];
+  hi = s->allowed_h[2 * cell + 1];
+}
+
+extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_hat, int32_t n_budget,
+                                      int32_t* n_nodes_out, void* stream) {
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "tree_expand: null session");
+  ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "tree_expand: session not prefilled");
+  const adt_sched_cfg& c = s->d.sched;
+  ADT_CHECK_ARG(d_hat >= 1 && d_hat <= c.d_hi && k_hat >= 1 && k_hat <= c.k_hi, ADT_E_ARG,
+                "tree_expand: (d,k)=(%d,%d) outside the session bounds", d_hat, k_hat);
+  ADT_CHECK_ARG(n_budget >= 1 && n_budget <= R - 1, ADT_E_CAPACITY, "tree_expand: n_budget %d", n_budget);
+  const int L = s->L, Ld = s->Ld, P = s->P;
+  ADT_CHECK_ARG(L + 1 + d_hat - P <= s->T, ADT_E_ARG, "tree_expand: depth %d runs past the image", d_hat);
+  hipStream_t st = (hipStream_t)stream;
+  const int V = s->V;
+  // catch-up rows: committed positions Ld..L, the root last
+  const int cu = L - Ld + 1;
+  ADT_CHECK_ARG(cu >= 1 && cu <= std::min(32, s->C0), ADT_E_STATE, "tree_expand: %d catch-up rows", cu);
+  std::vector<int32_t> ctok(s->tokens.begin() + Ld, s->tokens.begin() + L + 1), cf(cu);
+  for (int i = 0; i < cu; ++i) cf[i] = i;
+  TRY(launch_set_i32(s->ctok, small_of(ctok.data(), cu), cu, st));
+  TRY(launch_set_i32(s->cfsrc, small_of(cf.data(), cu), cu, st));
+  TRY(launch_iota(s->cpos, cu, Ld, 1, st));
+  TRY(launch_chain_masks(s->cmask, cu, st));
+  TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
+                    s->dlogits, st));
+  // layer 1: the root's top-k children
+  int lo, hi;
+  cell_range(s, L + 1 - P, lo, hi);
+  TRY(launch_fill_pairs(s->allowed_lvl, 1, lo, hi, st));
+  TRY(launch_row_topk(s->dlogits, V, V, s->allowed_lvl, 1, k_hat, 16, s->top_id, s->top_val, s->lse, st));
+  int cnt = std::min(k_hat, hi - lo);
+  TRY(launch_expand_level(s->pool, nullptr, 1, cnt, 0, 1, k_hat, s->top_id, s->top_val, s->lse, 16, d_hat > 1 ? 1 : 0,
+                          L, 0, cu - 1, s->C0, s->nx[0], st));
+  int pool_n = cnt, nf = std::min(k_hat, cnt), drow = 0, cur = 0;
+  for (int lvl = 2; lvl <= d_hat; ++lvl) {
+    const int dl_row = 1 + (lvl - 2) * c.k_hi;
+    float* lrows = s->dlogits + (size_t)dl_row * V;
+    void* fout = (char*)s->dfeat + (size_t)(s->C0 + drow) * s->dm * esize(s->dt);
+    TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1, drow + nf,
+                      s->nx[cur].mask, fout, 0, nf, lrows, st));
+    cell_range(s, L + lvl - P, lo, hi);
+    TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
+    TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, st));
+    cnt = std::min(k_hat, hi - lo);
+    TRY(launch_expand_level(s->pool, s->nx[cur].frontier, nf, cnt, pool_n, lvl, k_hat, s->top_id, s->top_val, s->lse,
+                            16, lvl < d_hat ? 1 : 0, L, drow + nf, cu - 1, s->C0, s->nx[cur ^ 1], st));
+    pool_n += nf * cnt;
+    drow += nf;
+    nf = std::min(k_hat, nf * cnt);
+    cur ^= 1;
+  }
+  TRY(launch_expand_finalize(s->pool, pool_n, n_budget, s->tokens[L], L, P, s->T, s->allowed_img, s->sel_rank,
+                             s->bfs_of, s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
+                             s->tr.allowed_rows, s->tr.n, st));
+  s->n_nodes = std::min(n_budget, pool_n) + 1;
+  s->expanded = true;
+  if (n_nodes_out) *n_nodes_out = s->n_nodes;
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_session_set_tree(adt_session* s, const int32_t* parent, const int32_t* token, int32_t n,
+                                           void* stream) {
+  ADT_CHECK_ARG(s && parent && token, ADT_E_ARG, "set_tree: null pointer");
+  ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "set_tree: session not prefilled");
+  ADT_CHECK_ARG(n >= 1 && n <= R, ADT_E_CAPACITY, "set_tree: n %d", n);
+  ADT_CHECK_ARG(parent[0] == -1, ADT_E_ARG, "set_tree: node 0 must be the root");
+  std::vector<int> dep(n, 0);
+  for (int i = 1; i < n; ++i) {
+    ADT_CHECK_ARG(parent[i] >= 0 && parent[i] < i, ADT_E_ARG, "set_tree: parent[%d]=%d not BFS ordered", i, parent[i]);
+    ADT_CHECK_ARG(token[i] >= 0 && token[i] < s->V, ADT_E_ARG, "set_tree: token[%d]", i);
+    dep[i] = dep[parent[i]] + 1;
+  }
+  const int dmax = *std::max_element(dep.begin(), dep.end());
+  ADT_CHECK_ARG(s->L + 1 + dmax - s->P <= s->T, ADT_E_ARG, "set_tree: tree deeper than the image remainder");
+  ADT_CHECK_ARG(s->L + n <= s->d.s_cap, ADT_E_CAPACITY, "set_tree: cache capacity");
+  ADT_CHECK_ARG(token[0] == s->tokens[s->L], ADT_E_ARG, "set_tree: token[0] must be the root token %d",
+                s->tokens[s->L]);
+  hipStream_t st = (hipStream_t)stream;
+  ADT_HIP(hipMemcpyAsync(s->tr.parent, parent, sizeof(int32_t) * n, hipMemcpyHostToDevice, st));
+  ADT_HIP(hipMemcpyAsync(s->tr.token, token, sizeof(int32_t) * n, hipMemcpyHostToDevice, st));
+  int32_t v[1] = {n};
+  TRY(launch_set_i32(s->tr.n, small_of(v, 1), 1, st));
+  TRY(launch_tree_masks(s->tr.parent, s->tr.n, 1, R, s->tr.mask, s->tr.depth, st));
+  TRY(launch_tree_rows(s->tr.depth, s->tr.n, R, s->L, s->P, s->T, s->allowed_img, s->tr.pos, s->tr.allowed_rows,
+                       s->tr.score, st));
+  TRY(sync_stream(st));
+  s->n_nodes = n;
+  s->expanded = false;
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_verify_forward(adt_session* s, void* stream) {
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "verify: null session");
+  ADT_CHECK_ARG(s->prefilled && s->n_nodes >= 1, ADT_E_STATE, "verify: no tree");
+  ADT_CHECK_ARG(s->L + s->n_nodes <= s->d.s_cap, ADT_E_CAPACITY, "verify: cache capacity");
+  const int n = s->n_nodes;
+  return target_forward(s, s->tr.token, n, s->tr.pos, s->L, s->L, n, s->tr.mask, 0, n, (hipStream_t)stream);
+}
+
+extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_hat, adt_step_out* out,
+                                                void* stream) {
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "accept_commit: null session");
+  ADT_CHECK_ARG(s->prefilled && s->n_nodes >= 1, ADT_E_STATE, "accept_commit: no verified tree");
+  hipStream_t st = (hipStream_t)stream;
+  const int n = s->n_nodes, L = s->L, P = s->P;
+  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, s->d.accept,
+                  (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
+  std::vector<int32_t> path(R), tok(R);
+  int32_t a = 0, bonus = 0;
+  ADT_HIP(hipMemcpyAsync(path.data(), s->tr.path, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(tok.data(), s->tr.token, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(&a, s->tr.nacc, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(&bonus, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  TRY(sync_stream(st));
+  ADT_CHECK_ARG(a >= 0 && a < n, ADT_E_STATE, "accept_commit: accepted length %d out of range", a);
+  // Catch-up features are kept for committed positions Ld-1 .. L_new-1.  After an expansion
+  // the draft cache covers the root, so the next catch-up starts at L + 1.
+  const int new_Ld = s->expanded ? L + 1 : s->Ld;
+  const int frow0 = L - (new_Ld - 1);
+  ADT_CHECK_ARG(frow0 >= 0 && frow0 + a + 1 <= s->C0, ADT_E_CAPACITY,
+                "accept_commit: %d catch-up rows exceed %d (too many cycles without expansion)", frow0 + a + 1, s->C0);
+  if (a > 0) {
+    int32_t lv[1] = {L};
+    TRY(launch_set_i32(s->scal + 3, small_of(lv, 1), 1, st));
+    TRY(launch_kv_compact(s->d.k_cache, s->d.v_cache, 1, s->Lr * s->H, s->Dh, 0, (int64_t)s->d.s_cap * s->Dh,
+                          s->scal + 3, s->tr.path, R, s->tr.nacc, a, s->dt, st));
+  }
+  TRY(launch_gather_rows(s->feat, s->tr.path, a + 1, s->dm,
+                         (char*)s->cfeat + (size_t)frow0 * s->dm * esize(s->dt), s->dt, st));
+  const int cell0 = L + 1 - P;
+  std::vector<int32_t> committed;
+  for (int m = 1; m <= a; ++m) committed.push_back(tok[path[m]]);
+  committed.push_back(bonus);
+  for (int c = 0; c < (int)committed.size(); ++c)
+    if (cell0 + c < s->T) {
+      s->rec_d[cell0 + c] = d_hat;
+      s->rec_k[cell0 + c] = k_hat;
+      s->has_rec[cell0 + c] = 1;
+    }
+  s->have_prev = true;
+  s->a_prev = a;
+  s->d_prev = d_hat;
+  s->prev_cell = cell0;
+  s->tokens.insert(s->tokens.end(), committed.begin(), committed.end());
+  s->Ld = new_Ld;
+  s->L = L + 1 + a;
+  s->expanded = false;
+  if (out) {
+    out->step = s->step;
+    out->d_hat = d_hat;
+    out->k_hat = k_hat;
+    out->n_nodes = n;
+    out->n_accepted = a;
+    out->n_committed = a + 1;
+    for (int i = 0; i <= a; ++i) out->tokens[i] = committed[i];
+    out->done = ((int)s->tokens.size() - P >= s->T) ? 1 : 0;
+  }
+  s->step += 1;
+  return ADT_OK;
+}
+
+static void schedule_for(adt_session_s* s, int& d_hat, int& k_hat) {
+  const adt_sched_cfg& c = s->d.sched;
+  const int cell = s->L + 1 - s->P;
+  const int remaining = s->T - cell;
+  if (s->d.fixed_tree) {
+    d_hat = std::min(c.d_hi, remaining - 1);
+    k_hat = c.k_hi;
+    return;
+  }
+  const int have_left = (cell >= 1 && s->has_rec[cell - 1]) ? 1 : 0;
+  int a_prev = s->a_prev;
+  if (c.alpha_source == ADT_ALPHA_POISSON && s->have_prev) a_prev = std::min(s->poisson[s->prev_cell], s->d_prev);
+  adt_schedule_next(&c, have_left, have_left ? s->rec_d[cell - 1] : 0, have_left ? s->rec_k[cell - 1] : 0,
+                    s->have_prev ? 1 : 0, a_prev, s->d_prev, remaining, &d_hat, &k_hat);
+}
+
+extern "C" adt_status adt_step(adt_session* s, adt_step_out* out, void* stream) {
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "step: null session");
+  ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "step: session not prefilled");
+  hipStream_t st = (hipStream_t)stream;
+  if ((int)s->tokens.size() - s->P >= s->T) {
+    if (out) {
+      memset(out, 0, sizeof(*out));
+      out->done = 1;
+    }
+    return ADT_OK;
+  }
+  int d_hat = 0, k_hat = 0;
+  schedule_for(s, d_hat, k_hat);
+  if (d_hat >= 1) {
+    TRY(adt_tree_expand(s, d_hat, k_hat, s->d.sched.n_budget, nullptr, st));
+  } else {
+    TRY(set_root_only_tree(s, s->tokens[s->L], s->L, st));
+  }
+  TRY(adt_verify_forward(s, st));
+  return adt_session_accept_commit(s, d_hat, k_hat, out, st);
+}
+
+extern "C" adt_status adt_session_get_view(const adt_session* s, adt_session_view* v) {
+  ADT_CHECK_ARG(s && v, ADT_E_ARG, "get_view: null pointer");
+  v->L = s->L;
+  v->Ld = s->Ld;
+  v->step = s->step;
+  v->n_tokens = (int32_t)s->tokens.size();
+  v->n_nodes = s->n_nodes;
+  v->logits = s->logits;
+  v->feat = s->feat;
+  v->draft_logits = s->dlogits;
+  v->parent = s->tr.parent;
+  v->token = s->tr.token;
+  v->depth = s->tr.depth;
+  v->score = s->tr.score;
+  v->mask = s->tr.mask;
+  v->allowed_rows = s->tr.allowed_rows;
+  v->path = s->tr.path;
+  v->n_acc = s->tr.nacc;
+  v->bonus = s->tr.bonus;
+  v->tokens_host = s->tokens.data();
+  return ADT_OK;
+}

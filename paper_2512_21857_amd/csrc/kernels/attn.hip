@@ -1,0 +1,328 @@
+// Tree attention (Sec. 3.1): every tree node attends to the committed prefix and to the
+// nodes on its own root-to-node path (the ancestor bitmask).
+//
+// bf16 path: one workgroup per (split of the key range, head, sequence).  K and V tiles of
+// 64 keys are streamed from HBM once per workgroup and staged in LDS (V transposed), all
+// query rows of the tree are held in registers, and both products run on MFMA 16x16x32:
+//   S^T[key][q] = K[key][:] . Q[q][:]        (A = K rows, B = Q^T)
+//   O^T[d][q]  += V^T[d][key] . P^T[key][q]  (A = V^T rows, B = P^T)
+// so each lane owns one query column and the online-softmax rescale is a per-lane scalar.
+// Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
+#include "../launch.h"
+
+namespace adt {
+
+constexpr int ATT_KT = 64;      // keys per LDS tile
+constexpr int ATT_THREADS = 256;
+
+__device__ __forceinline__ bool tail_visible(uint64_t w0, uint64_t w1, int j) {
+  const uint64_t w = j < 64 ? w0 : w1;
+  return (w >> (j & 63)) & 1ull;
+}
+
+// TPW = query tiles (of 16) per wave: 1 covers up to 64 queries, 2 up to 128.
+template <int DH, int TPW>
+__global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap,
+    int chunk, int splits, float scale_log2, float* __restrict__ part_o, float* __restrict__ part_ml) {
+  constexpr int DT = DH / 16;   // 16-wide dimension tiles of O
+  constexpr int KS = DH / 32;   // 32-deep k-steps of Q.K
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[ATT_KT][DH + 8];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH][ATT_KT + 8];
+
+  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int L = kv_len[b];
+  const int nq = min(n_q[b], nq_max);
+  const int total = min(L + n_tail[b], kv_cap);
+  const int k_begin = s * chunk;
+  const int k_end = min(total, k_begin + chunk);
+  const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
+  const int lq = lane & 15, g = lane >> 4;
+  const int QT = (nq + 15) / 16;
+
+  const int64_t pbase = (((int64_t)b * H + h) * splits + s) * nq_max;
+  float* po = part_o + pbase * DH;
+  float* pml = part_ml + pbase * 2;
+  const uint16_t* kbase = kc + b * stride_b + h * stride_h;
+  const uint16_t* vbase = vc + b * stride_b + h * stride_h;
+
+  // This wave's query tiles: wave, wave + 4, ...
+  int n_my = 0;
+  for (int t = wave; t < QT && n_my < TPW; t += 4) ++n_my;
+
+  bf16x8 qf[TPW][KS];
+  uint64_t mw0[TPW], mw1[TPW];
+  f32x4 o[TPW][DT];
+  float m_run[TPW], l_run[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    m_run[i] = -INFINITY;
+    l_run[i] = 0.f;
+    mw0[i] = mw1[i] = 0;
+#pragma unroll
+    for (int d = 0; d < DT; ++d) o[i][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < KS; ++t) qf[i][t] = bf16x8{};
+    if (i < n_my) {
+      const int qr = (wave + 4 * i) * 16 + lq;
+      if (qr < nq) {
+        const uint16_t* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+#pragma unroll
+        for (int t = 0; t < KS; ++t) qf[i][t] = *reinterpret_cast<const bf16x8*>(qp + t * 32 + g * 8);
+        const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+        mw0[i] = mp[0];
+        mw1[i] = mp[1];
+      }
+    }
+  }
+
+  for (int kb = k_begin; kb < k_end; kb += ATT_KT) {
+    __syncthreads();
+    for (int p = tid; p < ATT_KT * DH / 8; p += ATT_THREADS) {
+      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
+      const int key = kb + r;
+      u16x8 kv = u16x8{0, 0, 0, 0, 0, 0, 0, 0}, vv = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      if (key < k_end) {
+        kv = *reinterpret_cast<const u16x8*>(kbase + (int64_t)key * DH + c);
+        vv = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + c);
+      }
+      *reinterpret_cast<u16x8*>(&Ks[r][c]) = kv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vv[e];
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+      if (i >= n_my) break;
+      f32x4 st[4];
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+        st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < KS; ++t) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[sub * 16 + lq][t * 32 + g * 8]);
+          st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[i][t], st[sub], 0, 0, 0);
+        }
+      }
+      // lane (lq, g) now holds S for query (wave + 4i)*16 + lq and keys kb + sub*16 + 4g + r.
+      float mx = -INFINITY;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kb + sub * 16 + 4 * g + r;
+          const bool vis = key < k_end && (key < L || tail_visible(mw0[i], mw1[i], key - L));
+          const float v = vis ? st[sub][r] * scale_log2 : -INFINITY;
+          st[sub][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      const float m_new = fmaxf(m_run[i], mx);
+      const bool none = (m_new == -INFINITY);
+      const float alpha = none ? 1.f : exp2f(m_run[i] - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int sub = 0; sub < 4; ++sub) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = none ? 0.f : exp2f(st[sub][r] - m_new);
+          st[sub][r] = p;
+          rs += p;
+        }
+      }
+      rs += __shfl_xor(rs, 16, WAVE);
+      rs += __shfl_xor(rs, 32, WAVE);
+      l_run[i] = l_run[i] * alpha + rs;
+      m_run[i] = m_new;
+#pragma unroll
+      for (int d = 0; d < DT; ++d) o[i][d] *= alpha;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        bf16x8 pb;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pb[r] = __builtin_bit_cast(__bf16, f2bf(st[2 * h2][r]));
+          pb[4 + r] = __builtin_bit_cast(__bf16, f2bf(st[2 * h2 + 1][r]));
+        }
+#pragma unroll
+        for (int d = 0; d < DT; ++d) {
+          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 4 * g]);
+          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 16 + 4 * g]);
+          const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[i][d], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // lane (lq, g) holds O^T[d = dt*16 + 4g + r][q].
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) {
+    const int qr = (wave + 4 * i) * 16 + lq;
+    if (i >= n_my || qr >= nq) continue;
+#pragma unroll
+    for (int d = 0; d < DT; ++d) *reinterpret_cast<f32x4*>(po + (int64_t)qr * DH + d * 16 + 4 * g) = o[i][d];
+    if (g == 0) {
+      pml[qr * 2] = m_run[i];
+      pml[qr * 2 + 1] = l_run[i];
+    }
+  }
+  // Query rows of idle waves / empty splits still need a neutral partial.
+  if (k_begin >= k_end) {
+    for (int qr = tid; qr < nq; qr += ATT_THREADS) {
+      pml[qr * 2] = -INFINITY;
+      pml[qr * 2 + 1] = 0.f;
+    }
+  }
+}
+
+// Log-sum-exp merge of the split partials; one block of DH threads per (query, head, seq).
+template <typename OutT>
+__global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const float* __restrict__ part_ml,
+                                         const int32_t* __restrict__ n_q, int H, int nq_max, int splits, int DH,
+                                         OutT* __restrict__ out) {
+  const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
+  if (qr >= min(n_q[b], nq_max)) return;
+  const int64_t base = (((int64_t)b * H + h) * splits) * nq_max;
+  float M = -INFINITY;
+  for (int s = 0; s < splits; ++s) M = fmaxf(M, part_ml[(base + (int64_t)s * nq_max + qr) * 2]);
+  float lsum = 0.f, acc = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    const int64_t row = base + (int64_t)s * nq_max + qr;
+    const float m = part_ml[row * 2];
+    if (m == -INFINITY) continue;
+    const float w = exp2f(m - M);
+    lsum += w * part_ml[row * 2 + 1];
+    acc += w * part_o[row * DH + d];
+  }
+  Elem<OutT>::store(out, (((int64_t)b * nq_max + qr) * H + h) * DH + d, lsum > 0.f ? acc / lsum : 0.f);
+}
+
+// fp32 path: one block per (query, head, sequence); scores staged in LDS.
+__global__ __launch_bounds__(128) void tree_attn_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ kc, const float* __restrict__ vc, int64_t stride_b,
+    int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap, int DH,
+    float scale, float* __restrict__ out) {
+  extern __shared__ float smem[];      // DH query values, then kv_cap scores
+  __shared__ float red[16];
+  const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
+  if (qr >= min(n_q[b], nq_max)) return;
+  const int L = kv_len[b];
+  const int total = min(L + n_tail[b], kv_cap);
+  const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+  const uint64_t w0 = mp[0], w1 = mp[1];
+  float* qs = smem;
+  float* sc = smem + DH;
+  const float* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+  for (int d = tid; d < DH; d += blockDim.x) qs[d] = qp[d];
+  __syncthreads();
+  const float* kb = kc + b * stride_b + h * stride_h;
+  const float* vb = vc + b * stride_b + h * stride_h;
+  float mx = -INFINITY;
+  for (int k = tid; k < total; k += blockDim.x) {
+    float v = -INFINITY;
+    if (k < L || tail_visible(w0, w1, k - L)) {
+      float acc = 0.f;
+      for (int d = 0; d < DH; ++d) acc += qs[d] * kb[(int64_t)k * DH + d];
+      v = acc * scale;
+    }
+    sc[k] = v;
+    mx = fmaxf(mx, v);
+  }
+  mx = wave_max(mx);
+  __syncthreads();
+  if (tid % WAVE == 0) red[tid / WAVE] = mx;
+  __syncthreads();
+  mx = -INFINITY;
+  for (int i = 0; i < (int)blockDim.x / WAVE; ++i) mx = fmaxf(mx, red[i]);
+  float sum = 0.f;
+  for (int k = tid; k < total; k += blockDim.x) {
+    const float p = sc[k] == -INFINITY ? 0.f : expf(sc[k] - mx);
+    sc[k] = p;
+    sum += p;
+  }
+  sum = block_sum(sum, red + 8);
+  __syncthreads();
+  for (int d = tid; d < DH; d += blockDim.x) {
+    float acc = 0.f;
+    for (int k = 0; k < total; ++k) acc += sc[k] * vb[(int64_t)k * DH + d];
+    out[(((int64_t)b * nq_max + qr) * H + h) * DH + d] = acc / sum;
+  }
+}
+
+// ----------------------------------------------------------------------------- host
+struct AttnPlan {
+  int splits, chunk;
+};
+
+static AttnPlan attn_plan(int B, int H, int kv_cap) {
+  // Aim for about two workgroups per CU (256 CUs); at least 128 keys per split.
+  const int want = (512 + B * H - 1) / (B * H);
+  const int max_splits = (kv_cap + 127) / 128;
+  int splits = want < 1 ? 1 : want;
+  if (splits > max_splits) splits = max_splits;
+  if (splits < 1) splits = 1;
+  int chunk = (kv_cap + splits - 1) / splits;
+  chunk = (chunk + ATT_KT - 1) / ATT_KT * ATT_KT;
+  splits = (kv_cap + chunk - 1) / chunk;
+  return {splits, chunk};
+}
+
+// Upper bound over every kv_cap: a plan never uses more than ceil(512 / (B*H)) splits.
+size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
+  (void)kv_cap;
+  if (dtype == ADT_F32) return 0;
+  const int max_splits = (512 + B * H - 1) / (B * H);
+  return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
+}
+
+adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
+                            int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
+                            hipStream_t st) {
+  if (dtype == ADT_F32) {
+    const size_t sm = (size_t)(Dh + kv_cap) * sizeof(float);
+    ADT_CHECK_ARG(sm <= 60 * 1024, ADT_E_CAPACITY, "tree_attn f32: kv_cap %d too large for LDS scores", kv_cap);
+    dim3 grid(nq_max, H, B);
+    tree_attn_f32_kernel<<<grid, 128, sm, st>>>((const float*)q, (const float*)k, (const float*)v, sb, sh, kv_len,
+                                                n_q, n_tail, mask, H, nq_max, kv_cap, Dh, scale, (float*)out);
+    ADT_LAUNCH_CHECK();
+    return ADT_OK;
+  }
+  const AttnPlan p = attn_plan(B, H, kv_cap);
+  const size_t need = (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
+  ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
+                need);
+  float* part_o = (float*)ws;
+  float* part_ml = part_o + (size_t)B * H * p.splits * nq_max * Dh;
+  dim3 grid(p.splits, H, B);
+  const float sl2 = scale * LOG2E;
+#define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
+  tree_attn_bf16_kernel<DHV, TPWV><<<grid, ATT_THREADS, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,            \
+                                                                 (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,    \
+                                                                 mask, H, nq_max, kv_cap, p.chunk, p.splits, sl2,    \
+                                                                 part_o, part_ml)
+  const bool wide = nq_max > 64;
+  if (Dh == 128) {
+    if (wide) ADT_ATTN_LAUNCH(128, 2);
+    else ADT_ATTN_LAUNCH(128, 1);
+  } else {
+    if (wide) ADT_ATTN_LAUNCH(64, 2);
+    else ADT_ATTN_LAUNCH(64, 1);
+  }
+#undef ADT_ATTN_LAUNCH
+  ADT_LAUNCH_CHECK();
+  dim3 g2(nq_max, H, B);
+  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, H, nq_max, p.splits, Dh,
+                                                         (uint16_t*)out);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+}  // namespace adt

@@ -1,0 +1,300 @@
+// Row-wise kernels of the forwards and of the cache bookkeeping: embedding, RMSNorm fused
+// with the split-K reduction of the preceding projection, RoPE + KV append, SwiGLU, logits,
+// feature gathers, KV compaction and ancestor masks.  Each kernel handles whole rows (at
+// most 128 tree rows per launch), so they are latency-bound and kept as simple as possible.
+#include "../launch.h"
+
+namespace adt {
+
+constexpr int ROW_THREADS = 256;
+
+// h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) in dtype T.
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
+                                                                 int d, float eps, float* __restrict__ h,
+                                                                 T* __restrict__ a) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  const T* e = E + (int64_t)tok[m] * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = Elem<T>::load(e, i);
+    h[(int64_t)m * d + i] = v;
+    ss += v * v;
+  }
+  const float r = rsqrtf(block_sum(ss, red) / d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+}
+
+// Draft-head input row m: [E[tok[m]] ; parent feature].  fsrc[m] >= 0 picks row fsrc of the
+// committed-feature buffer fa, fsrc[m] == -1 gives zeros, fsrc[m] <= -2 picks row -fsrc-2 of
+// the draft-feature buffer fb.
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
+                                                                  const int32_t* __restrict__ fsrc, const T* __restrict__ fa,
+                                                                  const T* __restrict__ fb, int d, T* __restrict__ x) {
+  const int m = blockIdx.x;
+  const T* e = E + (int64_t)tok[m] * d;
+  const int s = fsrc[m];
+  const T* f = s >= 0 ? fa + (int64_t)s * d : (s <= -2 ? fb + (int64_t)(-s - 2) * d : nullptr);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    x[(int64_t)m * 2 * d + i] = e[i];
+    if (f) x[(int64_t)m * 2 * d + d + i] = f[i];
+    else Elem<T>::store(x, (int64_t)m * 2 * d + d + i, 0.f);
+  }
+}
+
+// y = sum_s part[s][m][:]; h[m] = (assign ? y : h[m] + y); if a: a[m] = RMSNorm(h[m]).
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void add_norm_kernel(const float* __restrict__ part, int splits, int M, int d,
+                                                               int assign, float eps, float* __restrict__ h,
+                                                               T* __restrict__ a) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    float y = 0.f;
+    for (int s = 0; s < splits; ++s) y += part[((int64_t)s * M + m) * d + i];
+    const float v = assign ? y : h[(int64_t)m * d + i] + y;
+    h[(int64_t)m * d + i] = v;
+    ss += v * v;
+  }
+  if (a == nullptr) return;
+  const float r = rsqrtf(block_sum(ss, red) / d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+}
+
+// Sum the QKV partials of row m, rotate q and k (rotate-half RoPE at position pos[m], angles
+// in double precision), write q to qout[m][H][Dh] and k, v to cache slot slot0 + m of every
+// head.  Cache element (h, slot, :) at kc + h*stride_h + slot*Dh.
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __restrict__ part, int splits, int M,
+                                                               int H, int Dh, const int32_t* __restrict__ pos,
+                                                               int slot0, double theta, T* __restrict__ qout,
+                                                               T* __restrict__ kc, T* __restrict__ vc,
+                                                               int64_t stride_h) {
+  const int m = blockIdx.x;
+  const int d = H * Dh, N = 3 * d, half = Dh / 2;
+  const double p = (double)pos[m];
+  const int64_t slot = slot0 + m;
+  auto y = [&](int c) {
+    float acc = 0.f;
+    for (int s = 0; s < splits; ++s) acc += part[((int64_t)s * M + m) * N + c];
+    return acc;
+  };
+  for (int i = threadIdx.x; i < H * half; i += blockDim.x) {
+    const int hh = i / half, j = i % half;
+    const double ang = p * pow(theta, -2.0 * j / Dh);
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    const int c1 = hh * Dh + j, c2 = c1 + half;
+    const double q1 = y(c1), q2 = y(c2), k1 = y(d + c1), k2 = y(d + c2);
+    Elem<T>::store(qout, (int64_t)m * d + c1, (float)(q1 * cs - q2 * sn));
+    Elem<T>::store(qout, (int64_t)m * d + c2, (float)(q2 * cs + q1 * sn));
+    T* kr = kc + hh * stride_h + slot * Dh;
+    Elem<T>::store(kr, j, (float)(k1 * cs - k2 * sn));
+    Elem<T>::store(kr, j + half, (float)(k2 * cs + k1 * sn));
+    T* vr = vc + hh * stride_h + slot * Dh;
+    Elem<T>::store(vr, j, y(2 * d + c1));
+    Elem<T>::store(vr, j + half, y(2 * d + c2));
+  }
+}
+
+// SwiGLU over gate/up partials packed in interleaved 16-column blocks: out[m][j] = silu(g) u.
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void swiglu_kernel(const float* __restrict__ part, int splits, int M, int F,
+                                                             T* __restrict__ out) {
+  const int m = blockIdx.x, N = 2 * F;
+  for (int j = threadIdx.x; j < F; j += blockDim.x) {
+    const int cg = (j / 16) * 32 + j % 16, cu = cg + 16;
+    float g = 0.f, u = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      g += part[((int64_t)s * M + m) * N + cg];
+      u += part[((int64_t)s * M + m) * N + cu];
+    }
+    Elem<T>::store(out, (int64_t)m * F + j, g / (1.f + expf(-g)) * u);
+  }
+}
+
+// out[m][n] = sum_s part[s][m][n]  (logits).
+__global__ void reduce_store_kernel(const float* __restrict__ part, int splits, int M, int N, float* __restrict__ out,
+                                    int64_t ldo) {
+  const int m = blockIdx.y;
+  for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < N; n += gridDim.x * blockDim.x) {
+    float y = 0.f;
+    for (int s = 0; s < splits; ++s) y += part[((int64_t)s * M + m) * N + n];
+    out[(int64_t)m * ldo + n] = y;
+  }
+}
+
+// dst[i] = src[idx[i]] for i < cnt (rows of length d, element type T).
+template <typename T>
+__global__ void gather_rows_kernel(const T* __restrict__ src, const int32_t* __restrict__ idx, int d,
+                                   T* __restrict__ dst) {
+  const int i = blockIdx.x;
+  const T* s = src + (int64_t)idx[i] * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[(int64_t)i * d + c] = s[c];
+}
+
+// KV compaction: one block per (slice, sequence).  Reads every moved row into registers,
+// then writes them, so in-place moves never read a row already overwritten.
+template <typename T, int ROWS_MAX>
+__global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__ kc, T* __restrict__ vc, int Dh,
+                                                                 int64_t stride_b, int64_t stride_s,
+                                                                 const int32_t* __restrict__ kv_len,
+                                                                 const int32_t* __restrict__ path, int path_stride,
+                                                                 const int32_t* __restrict__ n_acc, int a_max) {
+  const int sl = blockIdx.x, b = blockIdx.y;
+  const int a = min(n_acc[b], a_max);
+  const int L = kv_len[b];
+  const int per_row = Dh * (int)sizeof(T) / 16;        // 16-byte pieces per row
+  const int pieces = a * per_row;
+  u16x8 kr[ROWS_MAX], vr[ROWS_MAX];
+  T* kb = kc + b * stride_b + sl * stride_s;
+  T* vb = vc + b * stride_b + sl * stride_s;
+#pragma unroll
+  for (int it = 0; it < ROWS_MAX; ++it) {
+    const int p = threadIdx.x + it * ROW_THREADS;
+    if (p < pieces) {
+      const int m = p / per_row + 1, c = p % per_row;
+      const int src = path[(int64_t)b * path_stride + m];
+      kr[it] = reinterpret_cast<const u16x8*>(kb + (int64_t)(L + src) * Dh)[c];
+      vr[it] = reinterpret_cast<const u16x8*>(vb + (int64_t)(L + src) * Dh)[c];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < ROWS_MAX; ++it) {
+    const int p = threadIdx.x + it * ROW_THREADS;
+    if (p < pieces) {
+      const int m = p / per_row + 1, c = p % per_row;
+      reinterpret_cast<u16x8*>(kb + (int64_t)(L + m) * Dh)[c] = kr[it];
+      reinterpret_cast<u16x8*>(vb + (int64_t)(L + m) * Dh)[c] = vr[it];
+    }
+  }
+}
+
+// Ancestor masks and depths of B BFS-ordered trees; one thread per tree.
+__global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int32_t* __restrict__ n_nodes, int B,
+                                  int n_max, uint64_t* __restrict__ mask, int32_t* __restrict__ depth) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int n = min(n_nodes[b], n_max);
+  const int32_t* par = parent + (int64_t)b * n_max;
+  uint64_t* mk = mask + (int64_t)b * n_max * ADT_MASK_WORDS;
+  for (int i = 0; i < n_max; ++i) {
+    uint64_t w0 = 0, w1 = 0;
+    int dp = 0;
+    if (i < n) {
+      const int p = par[i];
+      if (i > 0 && p >= 0 && p < i) {
+        w0 = mk[p * ADT_MASK_WORDS];
+        w1 = mk[p * ADT_MASK_WORDS + 1];
+        if (depth) dp = depth[(int64_t)b * n_max + p] + 1;
+      }
+      if (i < 64) w0 |= 1ull << i;
+      else w1 |= 1ull << (i - 64);
+    }
+    mk[i * ADT_MASK_WORDS] = w0;
+    mk[i * ADT_MASK_WORDS + 1] = w1;
+    if (depth) depth[(int64_t)b * n_max + i] = dp;
+  }
+}
+
+// ----------------------------------------------------------------------------- host
+#define ADT_DISPATCH_T(dtype, ...)             \
+  if ((dtype) == ADT_BF16) {                   \
+    using T = uint16_t;                        \
+    __VA_ARGS__;                               \
+  } else {                                     \
+    using T = float;                           \
+    __VA_ARGS__;                               \
+  }
+
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
+                             hipStream_t st) {
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
+                              int M, int d, void* x, int dtype, hipStream_t st) {
+  ADT_DISPATCH_T(dtype, draft_input_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, fsrc, (const T*)fa,
+                                                                          (const T*)fb, d, (T*)x));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
+                           int dtype, hipStream_t st) {
+  ADT_DISPATCH_T(dtype, add_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, d, assign, eps, h, (T*)a));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos, int slot0,
+                           double theta, void* qout, void* kc, void* vc, int64_t stride_h, int dtype, hipStream_t st) {
+  ADT_DISPATCH_T(dtype, qkv_rope_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, H, Dh, pos, slot0, theta,
+                                                                       (T*)qout, (T*)kc, (T*)vc, stride_h));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st) {
+  ADT_DISPATCH_T(dtype, swiglu_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, F, (T*)out));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_reduce_store(const float* part, int splits, int M, int N, float* out, int64_t ldo, hipStream_t st) {
+  dim3 grid((N + 1023) / 1024 < 64 ? (N + 1023) / 1024 : 64, M);
+  reduce_store_kernel<<<grid, 1024, 0, st>>>(part, splits, M, N, out, ldo);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,
+                              hipStream_t st) {
+  if (cnt <= 0) return ADT_OK;
+  ADT_DISPATCH_T(dtype, gather_rows_kernel<T><<<cnt, ROW_THREADS, 0, st>>>((const T*)src, idx, d, (T*)dst));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_kv_compact(void* k, void* v, int B, int slices, int Dh, int64_t sb, int64_t ss, const int32_t* kv_len,
+                             const int32_t* path, int path_stride, const int32_t* n_acc, int a_max, int dtype,
+                             hipStream_t st) {
+  const int bytes_row = Dh * (dtype == ADT_BF16 ? 2 : 4);
+  ADT_CHECK_ARG(bytes_row % 16 == 0, ADT_E_SHAPE, "kv_compact: row of %d bytes not a multiple of 16", bytes_row);
+  const int pieces = a_max * bytes_row / 16;
+  dim3 grid(slices, B);
+  if (dtype == ADT_BF16) {
+    if (pieces <= 4 * ROW_THREADS)
+      kv_compact_kernel<uint16_t, 4><<<grid, ROW_THREADS, 0, st>>>((uint16_t*)k, (uint16_t*)v, Dh, sb, ss, kv_len, path,
+                                                                  path_stride, n_acc, a_max);
+    else
+      kv_compact_kernel<uint16_t, 16><<<grid, ROW_THREADS, 0, st>>>((uint16_t*)k, (uint16_t*)v, Dh, sb, ss, kv_len,
+                                                                   path, path_stride, n_acc, a_max);
+  } else {
+    if (pieces <= 4 * ROW_THREADS)
+      kv_compact_kernel<float, 4><<<grid, ROW_THREADS, 0, st>>>((float*)k, (float*)v, Dh, sb, ss, kv_len, path,
+                                                               path_stride, n_acc, a_max);
+    else
+      kv_compact_kernel<float, 16><<<grid, ROW_THREADS, 0, st>>>((float*)k, (float*)v, Dh, sb, ss, kv_len, path,
+                                                                path_stride, n_acc, a_max);
+  }
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_tree_masks(const int32_t* parent, const int32_t* n_nodes, int B, int n_max, uint64_t* mask,
+                             int32_t* depth, hipStream_t st) {
+  tree_masks_kernel<<<(B + 63) / 64, 64, 0, st>>>(parent, n_nodes, B, n_max, mask, depth);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+}  // namespace adt

@@ -1,0 +1,334 @@
+// Draft-tree expansion and greedy acceptance (Sec. 3.1; Sec. 4.2, Eq. 3-5).
+//
+// row_topk: per logits row, over its allowed id range, the top-k ids ordered by
+//   (logit desc, id asc) and the log-sum-exp; one workgroup per row.  Each thread keeps a
+//   sorted private list over a strided slice, then k rounds of a block-wide argmax merge.
+// expand_level: children of the frontier rows (score = parent score + logit - lse, i.e. the
+//   log of the product of confidences of Eq. 3), appended to the candidate pool, and the
+//   next frontier (top-k of the new layer by (score desc, creation asc)); it also lays out
+//   the next draft forward: tokens, parent-feature rows, positions, draft-cache tail masks.
+// expand_finalize: top-N rerank of the pool by (score desc, depth asc, creation asc), BFS
+//   order by (depth asc, score desc, creation asc), parent indices, masks, positions.
+// accept_greedy: the root-to-node walk along target argmaxes.
+#include "../launch.h"
+
+namespace adt {
+
+constexpr int SEL_THREADS = 256;
+
+__device__ __forceinline__ bool better(float a, int ia, float b, int ib) { return a > b || (a == b && ia < ib); }
+
+template <int KMAX>
+__global__ __launch_bounds__(SEL_THREADS) void row_topk_kernel(const float* __restrict__ logits, int64_t ld, int V,
+                                                               const int32_t* __restrict__ allowed, int k,
+                                                               int32_t* __restrict__ top_id, float* __restrict__ top_val,
+                                                               float* __restrict__ lse) {
+  __shared__ float sv[SEL_THREADS / WAVE];
+  __shared__ int si[SEL_THREADS / WAVE];
+  __shared__ int st[SEL_THREADS / WAVE];
+  __shared__ float smx[SEL_THREADS / WAVE], ssum[SEL_THREADS / WAVE];
+  const int row = blockIdx.x, tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+  const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
+  const float* x = logits + (int64_t)row * ld;
+
+  float v[KMAX];
+  int id[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    v[j] = -INFINITY;
+    id[j] = 0x7FFFFFFF;
+  }
+  float m = -INFINITY, s = 0.f;
+  for (int i = lo + tid; i < hi; i += SEL_THREADS) {
+    const float xi = x[i];
+    if (xi > m) {
+      s = s * expf(m - xi) + 1.f;
+      m = xi;
+    } else {
+      s += expf(xi - m);
+    }
+    if (better(xi, i, v[KMAX - 1], id[KMAX - 1])) {
+      v[KMAX - 1] = xi;
+      id[KMAX - 1] = i;
+#pragma unroll
+      for (int j = KMAX - 1; j > 0; --j) {
+        if (better(v[j], id[j], v[j - 1], id[j - 1])) {
+          const float tv = v[j];
+          v[j] = v[j - 1];
+          v[j - 1] = tv;
+          const int ti = id[j];
+          id[j] = id[j - 1];
+          id[j - 1] = ti;
+        }
+      }
+    }
+  }
+  // log-sum-exp across the block
+  float M = wave_max(m);
+  float S = wave_sum(m == -INFINITY ? 0.f : s * expf(m - M));
+  if (lane == 0) {
+    smx[wave] = M;
+    ssum[wave] = S;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float gm = -INFINITY;
+    for (int w = 0; w < SEL_THREADS / WAVE; ++w) gm = fmaxf(gm, smx[w]);
+    float gs = 0.f;
+    for (int w = 0; w < SEL_THREADS / WAVE; ++w)
+      if (smx[w] != -INFINITY) gs += ssum[w] * expf(smx[w] - gm);
+    lse[row] = gm + logf(gs);
+  }
+  // k rounds of block argmax over the heads of the private lists
+  int head = 0;
+  const int kk = min(k, hi - lo);
+  for (int r = 0; r < kk; ++r) {
+    float hv = -INFINITY;
+    int hid = 0x7FFFFFFF;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j)
+      if (j == head) {
+        hv = v[j];
+        hid = id[j];
+      }
+    float bv = hv;
+    int bi = hid, bt = tid;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, WAVE);
+      const int oi = __shfl_xor(bi, o, WAVE), ot = __shfl_xor(bt, o, WAVE);
+      if (better(ov, oi, bv, bi)) {
+        bv = ov;
+        bi = oi;
+        bt = ot;
+      }
+    }
+    __syncthreads();
+    if (lane == 0) {
+      sv[wave] = bv;
+      si[wave] = bi;
+      st[wave] = bt;
+    }
+    __syncthreads();
+    float wv = sv[0];
+    int wi = si[0], wt = st[0];
+    for (int w = 1; w < SEL_THREADS / WAVE; ++w)
+      if (better(sv[w], si[w], wv, wi)) {
+        wv = sv[w];
+        wi = si[w];
+        wt = st[w];
+      }
+    if (tid == wt) ++head;
+    if (tid == 0) {
+      top_id[row * KMAX + r] = wi;
+      top_val[row * KMAX + r] = wv;
+    }
+  }
+}
+
+// Pool (see launch.h): device arrays of capacity C: token, score, depth, parent (pool index,
+// -1 = root), drow (draft tree row of an expanded node, -1 otherwise); draft tree row j has a
+// tail mask rmask[j][2] over draft tree rows.  Parent-feature sources of the next draft
+// forward use the draft_input encoding: row r of the draft-feature buffer is fsrc = -2 - r.
+
+// One block.  Frontier rows r < nf (pool indices front[r], or the root when front == null)
+// with top_id/top_val/lse rows; creates cnt children each at pool indices base + r*cnt + c.
+__global__ __launch_bounds__(SEL_THREADS) void expand_level_kernel(
+    Pool pool, const int32_t* __restrict__ front, int nf, int cnt, int base, int depth, int k_hat,
+    const int32_t* __restrict__ top_id, const float* __restrict__ top_val, const float* __restrict__ lse, int kmax,
+    int make_next, int L, int drow_base, int root_frow, int tree_frow0, NextRows nx) {
+  const int C = nf * cnt;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < C; i += SEL_THREADS) {
+    const int r = i / cnt, c = i % cnt;
+    const int par = front ? front[r] : -1;
+    const float ps = par >= 0 ? pool.score[par] : 0.f;
+    const int idx = base + i;
+    pool.token[idx] = top_id[r * kmax + c];
+    pool.score[idx] = ps + (top_val[r * kmax + c] - lse[r]);
+    pool.depth[idx] = depth;
+    pool.parent[idx] = par;
+    pool.drow[idx] = -1;
+  }
+  __syncthreads();
+  __threadfence_block();
+  if (!make_next) return;
+  for (int i = tid; i < C; i += SEL_THREADS) {
+    const int ci = base + i;
+    const float sc = pool.score[ci];
+    int rank = 0;
+    for (int j = 0; j < C; ++j) {
+      const int cj = base + j;
+      const float sj = pool.score[cj];
+      rank += (sj > sc || (sj == sc && cj < ci)) ? 1 : 0;
+    }
+    if (rank < k_hat) {
+      const int par = pool.parent[ci];
+      const int jrow = drow_base + rank;
+      pool.drow[ci] = jrow;
+      nx.frontier[rank] = ci;
+      nx.tok[rank] = pool.token[ci];
+      nx.pos[rank] = L + depth;
+      uint64_t w0 = 0, w1 = 0;
+      if (par >= 0) {
+        const int pr = pool.drow[par];
+        nx.fsrc[rank] = -2 - (tree_frow0 + pr);
+        w0 = pool.rmask[pr * 2];
+        w1 = pool.rmask[pr * 2 + 1];
+      } else {
+        nx.fsrc[rank] = -2 - root_frow;
+      }
+      if (jrow < 64) w0 |= 1ull << jrow;
+      else w1 |= 1ull << (jrow - 64);
+      pool.rmask[jrow * 2] = w0;
+      pool.rmask[jrow * 2 + 1] = w1;
+      nx.mask[rank * 2] = w0;
+      nx.mask[rank * 2 + 1] = w1;
+    }
+  }
+}
+
+// One block: rerank + BFS + tree arrays.  allowed_img [n_image][2]; row i's successor sits at
+// absolute position L + depth + 1, image cell L + depth + 1 - P.
+__global__ __launch_bounds__(SEL_THREADS) void expand_finalize_kernel(
+    Pool pool, int C, int n_budget, int root_token, int L, int P, int n_image, const int32_t* __restrict__ allowed_img,
+    int32_t* __restrict__ sel_rank, int32_t* __restrict__ bfs_of, int32_t* __restrict__ parent,
+    int32_t* __restrict__ token, int32_t* __restrict__ depth, float* __restrict__ score, int32_t* __restrict__ pos,
+    uint64_t* __restrict__ mask, int32_t* __restrict__ allowed_rows, int32_t* __restrict__ n_out) {
+  const int tid = threadIdx.x;
+  const int N = min(n_budget, C);
+  for (int i = tid; i < C; i += SEL_THREADS) {
+    const float si = pool.score[i];
+    const int di = pool.depth[i];
+    int rank = 0;
+    for (int j = 0; j < C; ++j) {
+      const float sj = pool.score[j];
+      const int dj = pool.depth[j];
+      rank += (sj > si || (sj == si && (dj < di || (dj == di && j < i)))) ? 1 : 0;
+    }
+    sel_rank[i] = rank;
+  }
+  __syncthreads();
+  for (int i = tid; i < C; i += SEL_THREADS) {
+    int b = -1;
+    if (sel_rank[i] < N) {
+      const float si = pool.score[i];
+      const int di = pool.depth[i];
+      b = 1;
+      for (int j = 0; j < C; ++j) {
+        if (sel_rank[j] >= N) continue;
+        const float sj = pool.score[j];
+        const int dj = pool.depth[j];
+        b += (dj < di || (dj == di && (sj > si || (sj == si && j < i)))) ? 1 : 0;
+      }
+    }
+    bfs_of[i] = b;
+  }
+  __syncthreads();
+  for (int i = tid; i < C; i += SEL_THREADS) {
+    const int b = bfs_of[i];
+    if (b < 0) continue;
+    const int p = pool.parent[i];
+    parent[b] = p < 0 ? 0 : bfs_of[p];
+    token[b] = pool.token[i];
+    depth[b] = pool.depth[i];
+    score[b] = pool.score[i];
+  }
+  if (tid == 0) {
+    parent[0] = -1;
+    token[0] = root_token;
+    depth[0] = 0;
+    score[0] = 0.f;
+    *n_out = N + 1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int i = 0; i <= N; ++i) {
+      uint64_t w0 = 0, w1 = 0;
+      if (i > 0) {
+        w0 = mask[parent[i] * 2];
+        w1 = mask[parent[i] * 2 + 1];
+      }
+      if (i < 64) w0 |= 1ull << i;
+      else w1 |= 1ull << (i - 64);
+      mask[i * 2] = w0;
+      mask[i * 2 + 1] = w1;
+    }
+  }
+  for (int i = tid; i <= N; i += SEL_THREADS) {
+    const int dp = (i == 0) ? 0 : depth[i];
+    pos[i] = L + dp;
+    int cell = L + dp + 1 - P;
+    cell = cell < 0 ? 0 : (cell >= n_image ? n_image - 1 : cell);
+    allowed_rows[i * 2] = allowed_img[cell * 2];
+    allowed_rows[i * 2 + 1] = allowed_img[cell * 2 + 1];
+  }
+}
+
+// Greedy acceptance: t[u] = argmax id of row u (from row_topk with k = 1).
+__global__ void accept_greedy_kernel(const int32_t* __restrict__ argmax, int kmax, const int32_t* __restrict__ parent,
+                                     const int32_t* __restrict__ token, const int32_t* __restrict__ n_nodes, int n_max,
+                                     int32_t* __restrict__ path, int32_t* __restrict__ n_acc,
+                                     int32_t* __restrict__ bonus) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int n = min(*n_nodes, n_max);
+  int u = 0, a = 0;
+  path[0] = 0;
+  for (;;) {
+    const int t = argmax[u * kmax];
+    int nxt = -1;
+    for (int c = u + 1; c < n; ++c)
+      if (parent[c] == u && token[c] == t) {
+        nxt = c;
+        break;
+      }
+    if (nxt < 0) break;
+    path[++a] = nxt;
+    u = nxt;
+  }
+  *n_acc = a;
+  *bonus = argmax[u * kmax];
+}
+
+// ----------------------------------------------------------------------------- host
+adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
+                           int32_t* top_id, float* top_val, float* lse, hipStream_t st) {
+  ADT_CHECK_ARG(k >= 1 && k <= kmax && (kmax == 1 || kmax == 16), ADT_E_UNSUPPORTED, "row_topk: k=%d kmax=%d", k, kmax);
+  if (kmax == 1)
+    row_topk_kernel<1><<<rows, SEL_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
+  else
+    row_topk_kernel<16><<<rows, SEL_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
+                               const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
+                               int L, int drow_base, int root_frow, int tree_frow0, const NextRows& nx,
+                               hipStream_t st) {
+  expand_level_kernel<<<1, SEL_THREADS, 0, st>>>(pool, front, nf, cnt, base, depth, k_hat, top_id, top_val, lse, kmax,
+                                                 make_next, L, drow_base, root_frow, tree_frow0, nx);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_expand_finalize(const Pool& pool, int C, int n_budget, int root_token, int L, int P, int n_image,
+                                  const int32_t* allowed_img, int32_t* sel_rank, int32_t* bfs_of, int32_t* parent,
+                                  int32_t* token, int32_t* depth, float* score, int32_t* pos, uint64_t* mask,
+                                  int32_t* allowed_rows, int32_t* n_out, hipStream_t st) {
+  expand_finalize_kernel<<<1, SEL_THREADS, 0, st>>>(pool, C, n_budget, root_token, L, P, n_image, allowed_img,
+                                                    sel_rank, bfs_of, parent, token, depth, score, pos, mask,
+                                                    allowed_rows, n_out);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_accept_greedy(const int32_t* argmax, int kmax, const int32_t* parent, const int32_t* token,
+                                const int32_t* n_nodes, int n_max, int32_t* path, int32_t* n_acc, int32_t* bonus,
+                                hipStream_t st) {
+  accept_greedy_kernel<<<1, 64, 0, st>>>(argmax, kmax, parent, token, n_nodes, n_max, path, n_acc, bonus);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+}  // namespace adt

@@ -1,0 +1,91 @@
+// Host-side launchers of the kernels in csrc/kernels (internal to the library).
+#pragma once
+
+#include "common.h"
+
+namespace adt {
+
+// attn.hip
+size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype);
+adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
+                            int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
+                            hipStream_t st);
+
+// gemm.hip
+size_t packed_bytes(int total_rows, int K, int dtype);
+adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int dtype, void* dst,
+                       hipStream_t st);
+int gemm_splits(int M, int N, int K, int dtype);
+adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int splits, int dtype, float* part,
+                       hipStream_t st);
+
+// rows.hip
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
+                             hipStream_t st);
+adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
+                              int M, int d, void* x, int dtype, hipStream_t st);
+adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
+                           int dtype, hipStream_t st);
+adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos, int slot0,
+                           double theta, void* qout, void* kc, void* vc, int64_t stride_h, int dtype, hipStream_t st);
+adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st);
+adt_status launch_reduce_store(const float* part, int splits, int M, int N, float* out, int64_t ldo, hipStream_t st);
+adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,
+                              hipStream_t st);
+adt_status launch_kv_compact(void* k, void* v, int B, int slices, int Dh, int64_t sb, int64_t ss, const int32_t* kv_len,
+                             const int32_t* path, int path_stride, const int32_t* n_acc, int a_max, int dtype,
+                             hipStream_t st);
+adt_status launch_tree_masks(const int32_t* parent, const int32_t* n_nodes, int B, int n_max, uint64_t* mask,
+                             int32_t* depth, hipStream_t st);
+
+// select.hip
+struct Pool {
+  int32_t* token;
+  float* score;
+  int32_t* depth;
+  int32_t* parent;
+  int32_t* drow;
+  uint64_t* rmask;
+};
+struct NextRows {
+  int32_t* tok;
+  int32_t* fsrc;
+  int32_t* pos;
+  uint64_t* mask;
+  int32_t* frontier;
+};
+adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
+                           int32_t* top_id, float* top_val, float* lse, hipStream_t st);
+adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
+                               const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
+                               int L, int drow_base, int root_frow, int tree_frow0, const NextRows& nx,
+                               hipStream_t st);
+adt_status launch_expand_finalize(const Pool& pool, int C, int n_budget, int root_token, int L, int P, int n_image,
+                                  const int32_t* allowed_img, int32_t* sel_rank, int32_t* bfs_of, int32_t* parent,
+                                  int32_t* token, int32_t* depth, float* score, int32_t* pos, uint64_t* mask,
+                                  int32_t* allowed_rows, int32_t* n_out, hipStream_t st);
+adt_status launch_accept_greedy(const int32_t* argmax, int kmax, const int32_t* parent, const int32_t* token,
+                                const int32_t* n_nodes, int n_max, int32_t* path, int32_t* n_acc, int32_t* bonus,
+                                hipStream_t st);
+
+// small.hip
+struct SmallI32 {
+  int32_t v[32];
+};
+adt_status launch_set_i32(int32_t* dst, const SmallI32& vals, int count, hipStream_t st);
+adt_status launch_fill_pairs(int32_t* dst, int rows, int lo, int hi, hipStream_t st);
+adt_status launch_iota(int32_t* dst, int count, int start, int step, hipStream_t st);
+adt_status launch_chain_masks(uint64_t* mask, int n, hipStream_t st);
+adt_status launch_tree_rows(const int32_t* depth, const int32_t* n_nodes, int n_max, int L, int P, int n_image,
+                            const int32_t* allowed_img, int32_t* pos, int32_t* allowed_rows, float* score,
+                            hipStream_t st);
+
+// accept_sample.hip
+size_t accept_ws_bytes(int V);
+adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
+                                const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
+                                uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
+                                hipStream_t st);
+
+}  // namespace adt

@@ -1,0 +1,287 @@
+"""Python side of the C ABI: torch owns device memory (weights, caches, workspaces) and the
+current HIP stream; every step of the hot path runs inside libadt.so.  These wrappers only
+marshal pointers, sizes and structs."""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import abi
+from .abi import check, lib
+
+DTYPES = {"f32": abi.F32, "bf16": abi.BF16}
+TORCH_DT = {abi.F32: torch.float32, abi.BF16: torch.bfloat16}
+
+
+def _stream() -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _require_cuda(*ts: torch.Tensor) -> None:
+    for t in ts:
+        if t is not None and not t.is_cuda:
+            raise ValueError("device tensors expected")
+
+
+def upload(arr: np.ndarray, device="cuda") -> torch.Tensor:
+    """uint16 arrays are bfloat16 bit patterns; float32 stays float32."""
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(device)
+
+
+# ============================================================================ standalone calls
+def tree_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
+              n_q: torch.Tensor, n_tail: torch.Tensor, mask: torch.Tensor, kv_cap: int,
+              scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+              workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """q [B][nq_max][H][Dh]; caches [B][H][S_cap][Dh]; kv_len/n_q/n_tail int32 [B];
+    mask uint64-as-int64 [B][nq_max][2]."""
+    _require_cuda(q, k_cache, v_cache, kv_len, n_q, n_tail, mask)
+    B, nq_max, H, Dh = q.shape
+    S_cap = k_cache.shape[2]
+    dt = abi.BF16 if q.dtype == torch.bfloat16 else abi.F32
+    out = torch.empty_like(q) if out is None else out
+    ws_bytes = lib().adt_tree_attn_workspace_size(B, H, Dh, nq_max, kv_cap)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=q.device)
+    scale = 1.0 / float(np.sqrt(Dh)) if scale is None else scale
+    check(lib().adt_tree_attn(_p(q), _p(k_cache), _p(v_cache), H * S_cap * Dh, S_cap * Dh, _p(kv_len), _p(n_q),
+                              _p(n_tail), _p(mask), B, H, Dh, nq_max, kv_cap, scale, dt, _p(out), _p(workspace),
+                              workspace.numel(), _stream()))
+    return out
+
+
+def tree_masks(parent: torch.Tensor, n_nodes: torch.Tensor, depth: bool = True):
+    """parent int32 [B][n_max] -> (mask int64 [B][n_max][2] holding uint64 bits, depth int32 [B][n_max])."""
+    _require_cuda(parent, n_nodes)
+    B, n_max = parent.shape
+    mask = torch.empty(B, n_max, 2, dtype=torch.int64, device=parent.device)
+    dep = torch.empty(B, n_max, dtype=torch.int32, device=parent.device) if depth else None
+    check(lib().adt_tree_masks(_p(parent), _p(n_nodes), B, n_max, _p(mask), _p(dep), _stream()))
+    return mask, dep
+
+
+def kv_compact(k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor, path: torch.Tensor,
+               n_acc: torch.Tensor, a_max: int) -> None:
+    """In place on caches [B][slices][S_cap][Dh]; path int32 [B][stride] (path[b][0] = 0)."""
+    _require_cuda(k_cache, v_cache, kv_len, path, n_acc)
+    B, slices, S_cap, Dh = k_cache.shape
+    dt = abi.BF16 if k_cache.dtype == torch.bfloat16 else abi.F32
+    check(lib().adt_kv_compact(_p(k_cache), _p(v_cache), B, slices, Dh, slices * S_cap * Dh, S_cap * Dh, _p(kv_len),
+                               _p(path), path.shape[1], _p(n_acc), a_max, dt, _stream()))
+
+
+def accept_cfg(mode: str = "greedy", temperature: float = 1.0, top_k: int = 0, delta: float = 0.0,
+               knn: Optional[torch.Tensor] = None, knn_k: int = 1, seed: int = 0) -> abi.AcceptCfg:
+    m = {"greedy": abi.ACCEPT_GREEDY, "exact": abi.ACCEPT_EXACT, "relaxed": abi.ACCEPT_RELAXED}[mode]
+    rows, stride = (knn.shape[0], knn.shape[1]) if knn is not None else (0, 0)
+    return abi.AcceptCfg(m, temperature, top_k, delta, knn_k, rows, stride, _p(knn), seed)
+
+
+def verify_accept(logits: torch.Tensor, parent: torch.Tensor, token: torch.Tensor, allowed: torch.Tensor,
+                  n_nodes: torch.Tensor, cfg: abi.AcceptCfg, step: int, workspace: Optional[torch.Tensor] = None):
+    """logits fp32 [n_max][V].  Returns device tensors (path [MAX_NODES], n_acc [1], bonus [1])."""
+    _require_cuda(logits, parent, token, allowed, n_nodes)
+    n_max, V = logits.shape
+    dev = logits.device
+    path = torch.zeros(abi.MAX_NODES, dtype=torch.int32, device=dev)
+    n_acc = torch.zeros(1, dtype=torch.int32, device=dev)
+    bonus = torch.zeros(1, dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty(lib().adt_accept_workspace_size(V), dtype=torch.uint8, device=dev)
+    check(lib().adt_verify_accept(_p(logits), logits.stride(0), V, _p(parent), _p(token), _p(allowed), _p(n_nodes),
+                                  n_max, C.byref(cfg), step, _p(path), _p(n_acc), _p(bonus), _p(workspace),
+                                  workspace.numel(), _stream()))
+    return path, n_acc, bonus
+
+
+def schedule_next(sched: abi.SchedCfg, left, prev, remaining: int):
+    """Host-only schedule: left = (d, k) or None, prev = (a, d) or None."""
+    d = C.c_int32()
+    k = C.c_int32()
+    check(lib().adt_schedule_next(C.byref(sched), 1 if left else 0, left[0] if left else 0, left[1] if left else 0,
+                                  1 if prev else 0, prev[0] if prev else 0, prev[1] if prev else 0, remaining,
+                                  C.byref(d), C.byref(k)))
+    return d.value, k.value
+
+
+def sched_struct(s) -> abi.SchedCfg:
+    src = abi.ALPHA_POISSON if getattr(s, "alpha_source", "real") == "poisson" else abi.ALPHA_REAL
+    return abi.SchedCfg(s.d_lo, s.d_hi, s.k_lo, s.k_hi, s.l_d, s.l_k, s.beta, s.n_budget, s.d0, s.k0, src)
+
+
+# ============================================================================ model + session
+class DeviceModel:
+    """Target model plus draft head on the GPU, weights packed for the GEMM kernels."""
+
+    def __init__(self, cfg, weights: Dict[str, np.ndarray], device="cuda"):
+        m = cfg.model
+        self.cfg = cfg
+        self.dtype = DTYPES[m.dtype]
+        self.device = device
+        self._keep: List[torch.Tensor] = []
+        self.embed = upload(weights["embed"], device)
+        self.lm_head = self._pack([weights["lm_head"]], 0)
+        self.draft_fc = self._pack([weights["draft.fc"]], 0)
+        qkv, o, gu, down = [], [], [], []
+        for pre in [f"layer{l}" for l in range(m.n_layers)] + ["draft"]:
+            qkv.append(self._pack([weights[pre + ".wq"], weights[pre + ".wk"], weights[pre + ".wv"]], 0))
+            o.append(self._pack([weights[pre + ".wo"]], 0))
+            gu.append(self._pack([weights[pre + ".wg"], weights[pre + ".wu"]], 1))
+            down.append(self._pack([weights[pre + ".wd"]], 0))
+        self.qkv, self.o, self.gu, self.down = qkv, o, gu, down
+        ptrs = lambda ts: (C.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
+        self._arrays = [ptrs(qkv), ptrs(o), ptrs(gu), ptrs(down)]
+        desc = abi.ModelDesc(m.n_layers, m.d_model, m.n_heads, m.head_dim, m.ffn, m.vocab, self.dtype, 10000.0, 1e-5,
+                             _p(self.embed), _p(self.lm_head), _p(self.draft_fc),
+                             C.cast(self._arrays[0], C.POINTER(C.c_void_p)),
+                             C.cast(self._arrays[1], C.POINTER(C.c_void_p)),
+                             C.cast(self._arrays[2], C.POINTER(C.c_void_p)),
+                             C.cast(self._arrays[3], C.POINTER(C.c_void_p)))
+        self.handle = C.c_void_p()
+        check(lib().adt_model_create(C.byref(desc), C.byref(self.handle)))
+
+    def _pack(self, arrays: Sequence[np.ndarray], mode: int) -> torch.Tensor:
+        srcs = [upload(a, self.device) for a in arrays]
+        rows = [int(a.shape[0]) for a in arrays]
+        K = int(arrays[0].shape[1])
+        nbytes = lib().adt_packed_bytes(sum(rows), K, self.dtype)
+        out = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        sp = (C.c_void_p * len(srcs))(*[s.data_ptr() for s in srcs])
+        rw = (C.c_int32 * len(rows))(*rows)
+        check(lib().adt_pack_weight(sp, rw, len(srcs), K, mode, self.dtype, _p(out), _stream()))
+        torch.cuda.current_stream().synchronize()
+        return out
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib_loaded():
+            lib().adt_model_destroy(self.handle)
+            self.handle = None
+
+
+def _lib_loaded() -> bool:
+    return abi._lib is not None
+
+
+class DeviceSession:
+    """One image decode on the GPU: caches, workspace and the library's session object."""
+
+    def __init__(self, model: DeviceModel, cfg, poisson: Optional[np.ndarray] = None,
+                 knn: Optional[torch.Tensor] = None, accept_seed: Optional[int] = None, fixed_tree: bool = False,
+                 accept_mode: Optional[str] = None):
+        m = cfg.model
+        self.model = model
+        self.cfg = cfg
+        dev = model.device
+        self.s_cap = ((cfg.prefix_len + cfg.n_image + abi.MAX_NODES + 63) // 64) * 64
+        tdt = TORCH_DT[model.dtype]
+        self.k_cache = torch.zeros(m.n_layers, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
+        self.v_cache = torch.zeros_like(self.k_cache)
+        self.dk_cache = torch.zeros(m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
+        self.dv_cache = torch.zeros_like(self.dk_cache)
+        allowed = np.ascontiguousarray(cfg.allowed_table().reshape(-1), dtype=np.int32)
+        self._allowed = (C.c_int32 * allowed.size)(*allowed.tolist())
+        self._poisson = None
+        if poisson is not None:
+            self._poisson = (C.c_int32 * len(poisson))(*[int(x) for x in poisson])
+        a = cfg.accept
+        mode = accept_mode or a.mode
+        self.knn = knn
+        self.accept = accept_cfg(mode, a.temperature, a.top_k, a.delta, knn, a.knn_k,
+                                 cfg.seed if accept_seed is None else accept_seed)
+        desc = abi.SessionDesc(cfg.prefix_len, cfg.n_image, self.s_cap, _p(self.k_cache), _p(self.v_cache),
+                               _p(self.dk_cache), _p(self.dv_cache),
+                               C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched), self.accept,
+                               C.cast(self._poisson, C.POINTER(C.c_int32)) if self._poisson is not None else None,
+                               1 if fixed_tree else 0, None, 0)
+        need = lib().adt_session_workspace_size(model.handle, C.byref(desc))
+        if need == 0:
+            check(lib().adt_session_create(model.handle, C.byref(desc), C.byref(C.c_void_p())))
+        self.workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        desc.workspace = _p(self.workspace)
+        desc.workspace_bytes = need
+        self._desc = desc
+        self.handle = C.c_void_p()
+        check(lib().adt_session_create(model.handle, C.byref(desc), C.byref(self.handle)))
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib_loaded():
+            lib().adt_session_destroy(self.handle)
+            self.handle = None
+
+    # -- cycle pieces ----------------------------------------------------------------------
+    def prefill(self, prefix: np.ndarray) -> int:
+        arr = (C.c_int32 * len(prefix))(*[int(x) for x in prefix])
+        first = C.c_int32()
+        check(lib().adt_session_prefill(self.handle, arr, C.byref(first), _stream()))
+        return first.value
+
+    def step(self) -> dict:
+        out = abi.StepOut()
+        check(lib().adt_step(self.handle, C.byref(out), _stream()))
+        return _step_dict(out)
+
+    def expand(self, d_hat: int, k_hat: int, n_budget: int) -> int:
+        n = C.c_int32()
+        check(lib().adt_tree_expand(self.handle, d_hat, k_hat, n_budget, C.byref(n), _stream()))
+        return n.value
+
+    def set_tree(self, parent: Sequence[int], token: Sequence[int]) -> None:
+        n = len(parent)
+        pa = (C.c_int32 * n)(*[int(x) for x in parent])
+        to = (C.c_int32 * n)(*[int(x) for x in token])
+        check(lib().adt_session_set_tree(self.handle, pa, to, n, _stream()))
+
+    def verify(self) -> None:
+        check(lib().adt_verify_forward(self.handle, _stream()))
+
+    def accept_commit(self, d_hat: int, k_hat: int) -> dict:
+        out = abi.StepOut()
+        check(lib().adt_session_accept_commit(self.handle, d_hat, k_hat, C.byref(out), _stream()))
+        return _step_dict(out)
+
+    # -- inspection (views into the session workspace) -------------------------------------
+    def view(self) -> abi.SessionView:
+        v = abi.SessionView()
+        check(lib().adt_session_get_view(self.handle, C.byref(v)))
+        return v
+
+    def _ws(self, ptr: int, count: int, dtype: torch.dtype) -> torch.Tensor:
+        off = ptr - self.workspace.data_ptr()
+        nb = count * torch.empty((), dtype=dtype).element_size()
+        assert 0 <= off and off + nb <= self.workspace.numel()
+        return self.workspace[off: off + nb].view(dtype)
+
+    def tensors(self) -> dict:
+        v = self.view()
+        m = self.cfg.model
+        n = v.n_nodes
+        tdt = TORCH_DT[self.model.dtype]
+        s = self.cfg.sched
+        return {
+            "L": v.L, "Ld": v.Ld, "n": n, "step": v.step,
+            "logits": self._ws(v.logits, n * m.vocab, torch.float32).view(n, m.vocab),
+            "feat": self._ws(v.feat, n * m.d_model, tdt).view(n, m.d_model),
+            "draft_logits": self._ws(v.draft_logits, (1 + (s.d_hi - 1) * s.k_hi) * m.vocab,
+                                     torch.float32).view(-1, m.vocab),
+            "parent": self._ws(v.parent, n, torch.int32), "token": self._ws(v.token, n, torch.int32),
+            "depth": self._ws(v.depth, n, torch.int32), "score": self._ws(v.score, n, torch.float32),
+            "mask": self._ws(v.mask, 2 * n, torch.int64).view(n, 2),
+            "allowed": self._ws(v.allowed_rows, 2 * n, torch.int32).view(n, 2),
+            "path": self._ws(v.path, n, torch.int32), "n_acc": self._ws(v.n_acc, 1, torch.int32),
+            "bonus": self._ws(v.bonus, 1, torch.int32),
+            "tokens": [v.tokens_host[i] for i in range(v.n_tokens)],
+        }
+
+
+def _step_dict(o: abi.StepOut) -> dict:
+    return {"step": o.step, "d_hat": o.d_hat, "k_hat": o.k_hat, "n_nodes": o.n_nodes, "n_accepted": o.n_accepted,
+            "n_committed": o.n_committed, "tokens": [o.tokens[i] for i in range(o.n_committed)], "done": o.done}

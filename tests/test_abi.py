@@ -1,0 +1,77 @@
+"""The C ABI on the CPU: libadt.so loads, exports every entry point declared in
+include/adt.h, validates arguments before launching anything, and its host-only schedule
+matches the oracle's (Sec. 4.1-4.2, Eq. 2)."""
+import json
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2512_21857_amd import abi
+    return abi.lib()
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "adt.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(adt_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(L):
+    from paper_2512_21857_amd import abi
+    names = declared_symbols()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(abi.EXPORTED)
+    assert L.adt_version() == 1
+
+
+def test_argument_errors_return_codes_without_launching(L):
+    from paper_2512_21857_amd import abi
+    assert L.adt_tree_attn(None, None, None, 0, 0, None, None, None, None, 1, 1, 64, 1, 1, 1.0, 1, None, None, 0,
+                           None) == abi.E_ARG
+    assert "null" in abi.last_error()
+    fake = 0x1000
+    # unsupported head size, oversize tree
+    assert L.adt_tree_attn(fake, fake, fake, 0, 96 * 10, fake, fake, fake, fake, 1, 1, 96, 1, 10, 1.0, 1, fake, fake, 0,
+                           None) == abi.E_SHAPE
+    assert L.adt_tree_attn(fake, fake, fake, 0, 64 * 10, fake, fake, fake, fake, 1, 1, 64, 129, 10, 1.0, 1, fake, fake,
+                           0, None) == abi.E_CAPACITY
+    assert L.adt_kv_compact(fake, fake, 1, 1, 64, 0, 64, fake, fake, 4, fake, 200, 1, None) == abi.E_CAPACITY
+    assert L.adt_tree_masks(fake, fake, 1, 300, fake, None, None) == abi.E_CAPACITY
+    cfg = abi.AcceptCfg(7, 1.0, 0, 0.0, 1, 0, 0, None, 0)
+    import ctypes as C
+    assert L.adt_verify_accept(fake, 16, 16, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake, fake, 1 << 20,
+                               None) == abi.E_ARG
+    sess = C.c_void_p()
+    assert L.adt_session_create(None, None, C.byref(sess)) == abi.E_ARG
+    assert L.adt_step(None, None, None) == abi.E_ARG
+
+
+def test_schedule_matches_oracle(L):
+    from paper_2512_21857_amd import runtime
+    from synth import SchedCfg
+    from oracle.schedule import schedule
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "schedule_trajectories.json")))
+    for case in gold["cases"]:
+        sc = SchedCfg(**case["sched"])
+        s = runtime.sched_struct(sc)
+        rec, prev = None, None
+        for a, tree in zip(case["accepted"], case["trees"]):
+            got = runtime.schedule_next(s, rec, prev, 10_000)
+            assert list(got) == tree == list(schedule(sc, rec, prev, 10_000))
+            rec, prev = got, (a, got[0])
+    sc = SchedCfg(1, 6, 4, 10, 1, 10, 1.0, 60, 5, 10)
+    s = runtime.sched_struct(sc)
+    for left in [None, (1, 4), (6, 10), (3, 7)]:
+        for prev in [None, (0, 3), (3, 3), (6, 6)]:
+            for rem in (1, 2, 3, 50):
+                if left is None and prev is not None:
+                    continue
+                assert runtime.schedule_next(s, left, prev, rem) == schedule(sc, left, prev, rem)

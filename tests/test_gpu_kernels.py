@@ -1,0 +1,185 @@
+"""GPU parity of the standalone ABI calls against the oracle, on seeded synthetic inputs.
+
+Floating point: |gpu - oracle| <= atol + rtol * |oracle| with (2e-2, 1e-2) for bf16 and
+(1e-5, 1e-5) for fp32.  Integer outputs (masks, depths, paths, tokens, compacted caches)
+are compared bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle.accept import accept_greedy
+from oracle.attention import attend_rows, tree_key_slots
+from oracle.decode import compact_cache
+from oracle.tree import ancestors_and_self, depths, packed_mask
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = (2e-2, 1e-2)
+F32_TOL = (1e-5, 1e-5)
+
+
+def _close(got, ref, tol, what):
+    atol, rtol = tol
+    err = np.abs(got - ref)
+    bad = err > atol + rtol * np.abs(ref)
+    assert not bad.any(), f"{what}: {bad.sum()} of {bad.size} outside tolerance, max err {err.max():.3e}"
+
+
+@pytest.fixture(scope="module")
+def rt():
+    from paper_2512_21857_amd import runtime
+    assert torch.cuda.is_available()
+    return runtime
+
+
+def _dev_tree(rt, parent_np, n_nodes_np):
+    parent = torch.from_numpy(parent_np.astype(np.int32)).cuda()
+    n = torch.from_numpy(n_nodes_np.astype(np.int32)).cuda()
+    mask, dep = rt.tree_masks(parent, n)
+    return mask, dep
+
+
+def _bits_to_f64(b):
+    return synth.bf16_bits_to_f32(b).astype(np.float64)
+
+
+def _attn_case(rt, B, H, Dh, n, l_lo, l_hi, seed, vary_n=False, rows=None):
+    ab = synth.attn_microbench(B, H, Dh, n, seed=seed, l_lo=l_lo, l_hi=l_hi, vary_n=vary_n)
+    mask, _ = _dev_tree(rt, ab.parent, ab.n_nodes)
+    q = torch.from_numpy(ab.q.view(np.int16)).cuda().view(torch.bfloat16)
+    k = torch.from_numpy(ab.k.view(np.int16)).cuda().view(torch.bfloat16)
+    v = torch.from_numpy(ab.v.view(np.int16)).cuda().view(torch.bfloat16)
+    kv_len = torch.from_numpy(ab.kv_len).cuda()
+    n_nodes = torch.from_numpy(ab.n_nodes).cuda()
+    kv_cap = int((ab.kv_len + ab.n_nodes).max())
+    out = rt.tree_attn(q, k, v, kv_len, n_nodes, n_nodes, mask, kv_cap)
+    got = out.float().cpu().numpy()
+    qf, kf, vf = _bits_to_f64(ab.q), _bits_to_f64(ab.k), _bits_to_f64(ab.v)
+    checked = 0
+    for b in range(B):
+        nb = int(ab.n_nodes[b])
+        anc = ancestors_and_self(ab.parent[b, :nb])
+        keys = tree_key_slots(int(ab.kv_len[b]), anc)
+        sel = range(nb) if rows is None else rows(b, nb)
+        for i in sel:
+            ref = attend_rows(qf[b, i:i + 1], kf[b], vf[b], [keys[i]], 1.0 / np.sqrt(Dh))[0]
+            _close(got[b, i], ref, BF16_TOL, f"tree_attn b={b} i={i}")
+            checked += 1
+    return checked
+
+
+@pytest.mark.parametrize("n", [1, 7, 16, 33, 64, 100, 128])
+def test_tree_attn_bf16_small(rt, n):
+    """Several 64-key tiles and a ragged tail: L in [0, 300]."""
+    print(f"tree_attn bf16 n={n}", flush=True)
+    assert _attn_case(rt, B=3, H=4, Dh=128, n=n, l_lo=0, l_hi=300, seed=11) == 3 * n
+
+
+def test_tree_attn_bf16_head64_ragged_batch(rt):
+    assert _attn_case(rt, B=5, H=3, Dh=64, n=61, l_lo=1, l_hi=700, seed=12, vary_n=True) > 0
+
+
+def test_tree_attn_bf16_full_microbench_sampled(rt):
+    """The 16 x 32 x 128 microbenchmark at its real size (L in [512, 2400], 128 nodes), checked
+    on sampled rows including the root, the last node and a deep node of every sequence."""
+    rows = lambda b, nb: sorted({0, nb - 1, nb // 2, (7 * b + 3) % nb})
+    assert _attn_case(rt, B=16, H=32, Dh=128, n=128, l_lo=512, l_hi=2400, seed=3, rows=rows) > 0
+
+
+def test_tree_attn_f32(rt):
+    rng = np.random.default_rng(5)
+    B, H, Dh, n = 2, 4, 64, 17
+    L = np.array([0, 321], dtype=np.int32)
+    S = int(L.max()) + n
+    parent = np.stack([synth.random_parents(rng, n) for _ in range(B)])
+    q = rng.standard_normal((B, n, H, Dh)).astype(np.float32)
+    k = rng.standard_normal((B, H, S, Dh)).astype(np.float32)
+    v = rng.standard_normal((B, H, S, Dh)).astype(np.float32)
+    nn = np.full(B, n, dtype=np.int32)
+    mask, _ = _dev_tree(rt, parent, nn)
+    tq, tk, tv = (torch.from_numpy(x).cuda() for x in (q, k, v))
+    kvl, nt = torch.from_numpy(L).cuda(), torch.from_numpy(nn).cuda()
+    out = rt.tree_attn(tq, tk, tv, kvl, nt, nt, mask, S).cpu().numpy()
+    for b in range(B):
+        keys = tree_key_slots(int(L[b]), ancestors_and_self(parent[b]))
+        ref = attend_rows(q[b].astype(np.float64), k[b].astype(np.float64), v[b].astype(np.float64), keys,
+                          1.0 / np.sqrt(Dh))
+        _close(out[b], ref, F32_TOL, "tree_attn f32")
+
+
+def test_tree_masks_bit_exact(rt):
+    rng = np.random.default_rng(6)
+    B, n_max = 6, 128
+    nn = np.array([1, 2, 17, 64, 65, 128], dtype=np.int32)
+    parent = np.full((B, n_max), -1, dtype=np.int32)
+    for b in range(B):
+        parent[b, :nn[b]] = synth.random_parents(rng, int(nn[b]))
+    mask, dep = _dev_tree(rt, parent, nn)
+    mask = mask.cpu().numpy().view(np.uint64)
+    dep = dep.cpu().numpy()
+    for b in range(B):
+        nb = int(nn[b])
+        assert np.array_equal(mask[b, :nb], packed_mask(parent[b, :nb], 2))
+        assert np.array_equal(dep[b, :nb], depths(parent[b, :nb]))
+        assert not mask[b, nb:].any()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_kv_compact_bit_exact(rt, dtype):
+    rng = np.random.default_rng(7)
+    B, slices, Dh = 4, 6, 128
+    nn = np.array([2, 13, 40, 128], dtype=np.int32)
+    L = np.array([0, 5, 300, 1000], dtype=np.int32)
+    S = int((L + nn).max())
+    path, a = synth.compaction_paths(rng, nn, a_max=12)
+    if dtype == "bf16":
+        kb = synth.draw_tensor(9, 1, (B, slices, S, Dh), True, std=np.float32(1.0))
+        vb = synth.draw_tensor(9, 2, (B, slices, S, Dh), True, std=np.float32(1.0))
+        tk = torch.from_numpy(kb.view(np.int16)).cuda().view(torch.bfloat16)
+        tv = torch.from_numpy(vb.view(np.int16)).cuda().view(torch.bfloat16)
+        rk, rv = kb.copy(), vb.copy()
+    else:
+        rk = rng.standard_normal((B, slices, S, Dh)).astype(np.float32)
+        rv = rng.standard_normal((B, slices, S, Dh)).astype(np.float32)
+        tk, tv = torch.from_numpy(rk.copy()).cuda(), torch.from_numpy(rv.copy()).cuda()
+    rt.kv_compact(tk, tv, torch.from_numpy(L).cuda(), torch.from_numpy(path).cuda(), torch.from_numpy(a).cuda(),
+                  int(a.max()))
+    for b in range(B):
+        compact_cache(rk[b], rv[b], int(L[b]), [int(x) for x in path[b, 1:a[b] + 1]])
+    gk = tk.view(torch.int16).cpu().numpy().view(np.uint16) if dtype == "bf16" else tk.cpu().numpy()
+    gv = tv.view(torch.int16).cpu().numpy().view(np.uint16) if dtype == "bf16" else tv.cpu().numpy()
+    assert np.array_equal(gk, rk) and np.array_equal(gv, rv)
+
+
+def test_accept_greedy_planted(rt):
+    """Trees holding a planted chain of length m at random sibling ranks: the GPU walk must
+    return exactly the oracle's path and bonus."""
+    rng = np.random.default_rng(8)
+    V = 1000
+    for trial in range(30):
+        m = int(rng.integers(0, 8))
+        n = int(rng.integers(m + 1, 61))
+        parent = synth.random_parents(rng, n, max_children=4, max_depth=12)
+        token = rng.integers(0, V, size=n).astype(np.int32)
+        for u in range(n):                        # siblings carry distinct tokens
+            kids = [c for c in range(n) if parent[c] == u]
+            token[kids] = rng.choice(V, size=len(kids), replace=False)
+        logits = rng.standard_normal((n, V)).astype(np.float32)
+        u = 0
+        for _ in range(m):
+            kids = [c for c in range(n) if parent[c] == u]
+            if not kids:
+                break
+            c = int(rng.choice(kids))
+            logits[u, token[c]] = 9.0
+            u = c
+        lo = int(rng.integers(0, 50))
+        allowed = np.tile([lo, V], (n, 1)).astype(np.int32)
+        ref_path, ref_bonus = accept_greedy(logits.astype(np.float64), parent, token, allowed)
+        cfg = rt.accept_cfg("greedy")
+        t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+        path, n_acc, bonus = rt.verify_accept(t(logits), t(parent.astype(np.int32)), t(token), t(allowed),
+                                              t(np.array([n], dtype=np.int32)), cfg, 0)
+        a = int(n_acc.item())
+        assert a == len(ref_path) and path[1:a + 1].cpu().tolist() == ref_path and int(bonus.item()) == ref_bonus
