@@ -205,6 +205,12 @@ typedef struct {
   adt_accept_cfg accept;
   const int32_t* poisson;       /* [host] [n_image] acceptance lengths for ADT_ALPHA_POISSON, else NULL */
   int32_t fixed_tree;           /* 1: skip the schedule, always (sched.d_hi, sched.k_hi) */
+  /* Optional caller-supplied draft distribution instead of the draft head: the draft logits
+   * of a row whose token is t at depth l (the root row has depth 0) are row
+   * (l * 131 + t) mod draft_table_rows of draft_table [rows][vocab] fp32.  Used to drive the
+   * expansion (a2, a3) with known logits; NULL = run the draft head. */
+  const float* draft_table;
+  int32_t draft_table_rows;
   void* workspace;
   size_t workspace_bytes;
 } adt_session_desc;
@@ -258,6 +264,19 @@ adt_status adt_verify_forward(adt_session* s, void* stream);
 adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_hat, adt_step_out* out, void* stream);
 /* One full cycle: a0 + a1-a3 + b + c + d1.  Synchronises once (the accepted path). */
 adt_status adt_step(adt_session* s, adt_step_out* out, void* stream);
+
+/* ------------------------------------------------------------------ profiling
+ * Optional timing of the session's kernels by class, with HIP events recorded on the
+ * caller's stream around each launch (adds a little host overhead while enabled).  Read
+ * values accumulate until reset: launches, summed kernel milliseconds, algorithmic bytes
+ * (what the method must move: weights once, inputs and outputs; prefix K/V once for
+ * attention) and flops. */
+#define ADT_PROF_GEMM 0     /* dense projections (bf16 MFMA or fp32) */
+#define ADT_PROF_ATTN 1     /* tree attention + split merge */
+#define ADT_PROF_COMPACT 2  /* KV compaction */
+#define ADT_PROF_CLASSES 3
+adt_status adt_profile_enable(int32_t on);
+adt_status adt_profile_read(int32_t cls, int64_t* launches, double* ms, double* bytes, double* flops, int32_t reset);
 
 #ifdef __cplusplus
 }

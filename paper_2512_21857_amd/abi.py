@@ -49,7 +49,8 @@ class ModelDesc(C.Structure):
 class SessionDesc(C.Structure):
     _fields_ = [("prefix_len", i32), ("n_image", i32), ("s_cap", i32), ("k_cache", p), ("v_cache", p),
                 ("dk_cache", p), ("dv_cache", p), ("allowed", ip), ("sched", SchedCfg), ("accept", AcceptCfg),
-                ("poisson", ip), ("fixed_tree", i32), ("workspace", p), ("workspace_bytes", sz)]
+                ("poisson", ip), ("fixed_tree", i32), ("draft_table", p), ("draft_table_rows", i32),
+                ("workspace", p), ("workspace_bytes", sz)]
 
 
 class StepOut(C.Structure):
@@ -88,7 +89,12 @@ _SIGS = {
     "adt_verify_forward": (i32, [p, p]),
     "adt_session_accept_commit": (i32, [p, i32, i32, C.POINTER(StepOut), p]),
     "adt_step": (i32, [p, C.POINTER(StepOut), p]),
+    "adt_profile_enable": (i32, [i32]),
+    "adt_profile_read": (i32, [i32, C.POINTER(i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
+                               C.POINTER(C.c_double), i32]),
 }
+
+PROF_GEMM, PROF_ATTN, PROF_COMPACT = 0, 1, 2
 
 EXPORTED = tuple(_SIGS)
 

@@ -35,11 +35,82 @@ struct Bump {
   }
 };
 
+// ---------------------------------------------------------------------------- profiling
+// Optional per-kernel-class timing: HIP events recorded on the caller's stream around each
+// launch of a class, read back at the next synchronisation of a cycle.  Off by default.
+struct ProfRec {
+  int cls;
+  int e0, e1;
+  double bytes, flops;
+};
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> ev;
+  int next = 0;
+  std::vector<ProfRec> pending;
+  double ms[ADT_PROF_CLASSES] = {};
+  double bytes[ADT_PROF_CLASSES] = {};
+  double flops[ADT_PROF_CLASSES] = {};
+  int64_t launches[ADT_PROF_CLASSES] = {};
+};
+static Profiler g_prof;
+
+static int prof_begin(hipStream_t st) {
+  if (!g_prof.on || g_prof.next + 2 > (int)g_prof.ev.size()) return -1;
+  const int e = g_prof.next;
+  g_prof.next += 2;
+  (void)hipEventRecord(g_prof.ev[e], st);
+  return e;
+}
+static void prof_end(int e, int cls, double bytes, double flops, hipStream_t st) {
+  if (e < 0) return;
+  (void)hipEventRecord(g_prof.ev[e + 1], st);
+  g_prof.pending.push_back({cls, e, e + 1, bytes, flops});
+}
+static void prof_collect() {
+  if (!g_prof.on) return;
+  for (const ProfRec& r : g_prof.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(g_prof.ev[r.e1]) == hipSuccess && hipEventElapsedTime(&ms, g_prof.ev[r.e0], g_prof.ev[r.e1]) == hipSuccess) {
+      g_prof.ms[r.cls] += ms;
+      g_prof.bytes[r.cls] += r.bytes;
+      g_prof.flops[r.cls] += r.flops;
+      g_prof.launches[r.cls] += 1;
+    }
+  }
+  g_prof.pending.clear();
+  g_prof.next = 0;
+}
+
 }  // namespace adt
 
 using namespace adt;
 
 static constexpr int R = ADT_MAX_NODES;
+
+extern "C" adt_status adt_profile_enable(int32_t on) {
+  if (on && g_prof.ev.empty()) {
+    g_prof.ev.resize(16384);
+    for (auto& e : g_prof.ev) ADT_HIP(hipEventCreate(&e));
+  }
+  g_prof.on = on != 0;
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_profile_read(int32_t cls, int64_t* launches, double* ms, double* bytes, double* flops,
+                                       int32_t reset) {
+  ADT_CHECK_ARG(cls >= 0 && cls < ADT_PROF_CLASSES, ADT_E_ARG, "profile_read: class %d", cls);
+  prof_collect();
+  if (launches) *launches = g_prof.launches[cls];
+  if (ms) *ms = g_prof.ms[cls];
+  if (bytes) *bytes = g_prof.bytes[cls];
+  if (flops) *flops = g_prof.flops[cls];
+  if (reset) {
+    g_prof.launches[cls] = 0;
+    g_prof.ms[cls] = g_prof.bytes[cls] = g_prof.flops[cls] = 0.0;
+  }
+  return ADT_OK;
+}
 
 extern "C" int32_t adt_version(void) { return 1; }
 
@@ -384,6 +455,7 @@ static adt_status check_session_desc(const adt_model* m, const adt_session_desc*
   ADT_CHECK_ARG((c.d_hi - 1) * c.k_hi <= R, ADT_E_CAPACITY, "session: draft tree rows exceed %d", R);
   ADT_CHECK_ARG(c.alpha_source == ADT_ALPHA_REAL || (c.alpha_source == ADT_ALPHA_POISSON && d->poisson), ADT_E_ARG,
                 "session: alpha source");
+  ADT_CHECK_ARG(d->draft_table == nullptr || d->draft_table_rows >= 1, ADT_E_ARG, "session: draft table rows");
   for (int g = 0; g < d->n_image; ++g) {
     const int lo = d->allowed[2 * g], hi = d->allowed[2 * g + 1];
     ADT_CHECK_ARG(0 <= lo && lo < hi && hi <= m->d.vocab, ADT_E_ARG, "session: allowed range of cell %d", g);
@@ -448,6 +520,16 @@ static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, h
   return launch_set_i32(s->scal, small_of(v, 3), 3, st);
 }
 
+// Algorithmic HBM bytes of a projection: weights once, the input rows, fp32 output rows.
+static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, int K, int S, int dt, float* part,
+                         hipStream_t st) {
+  const int e = prof_begin(st);
+  adt_status r = launch_gemm(X, ldx, W, M, N, K, S, dt, part, st);
+  prof_end(e, ADT_PROF_GEMM, (double)N * K * esize(dt) + (double)M * K * esize(dt) + (double)M * N * 4.0,
+           2.0 * M * N * K, st);
+  return r;
+}
+
 // Decoder layers over M rows.  Cache stack `kc/vc` has stride_layer between layers.
 static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
                              const uint64_t* mask, void* final_out, hipStream_t st) {
@@ -463,18 +545,24 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
     int S = gemm_splits(M, 3 * dm, dm, dt);
-    TRY(launch_gemm(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
+    TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
     TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, slot0, m->d.rope_theta, s->q, kc, vc, stride_h, dt, st));
-    TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M,
-                         L_pre + n_tail, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
+    {
+      // K1 + K1c: the prefix K/V once, tree Q/K/V in and O out, the masks.
+      const int e = prof_begin(st);
+      TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M,
+                           L_pre + n_tail, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
+      prof_end(e, ADT_PROF_ATTN, 2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es + 16.0 * M,
+               4.0 * M * (L_pre + n_tail) * H * Dh, st);
+    }
     S = gemm_splits(M, dm, dm, dt);
-    TRY(launch_gemm(s->att, dm, m->o[l], M, dm, dm, S, dt, s->part, st));
+    TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, S, dt, s->part, st));
     TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, s->act, dt, st));
     S = gemm_splits(M, 2 * F, dm, dt);
-    TRY(launch_gemm(s->act, dm, m->gu[l], M, 2 * F, dm, S, dt, s->part, st));
+    TRY(gemm_p(s->act, dm, m->gu[l], M, 2 * F, dm, S, dt, s->part, st));
     TRY(launch_swiglu(s->part, S, M, F, s->sw, dt, st));
     S = gemm_splits(M, dm, F, dt);
-    TRY(launch_gemm(s->sw, F, m->down[l], M, dm, F, S, dt, s->part, st));
+    TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, S, dt, s->part, st));
     TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
   }
   return ADT_OK;
@@ -482,7 +570,7 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
 
 static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, hipStream_t st) {
   const int S = gemm_splits(M, s->V, s->dm, s->dt);
-  TRY(launch_gemm(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, S, s->dt, s->part, st));
+  TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, S, s->dt, s->part, st));
   return launch_reduce_store(s->part, S, M, s->V, out, s->V, st);
 }
 
@@ -505,7 +593,7 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
   const int dm = s->dm, dt = s->dt;
   TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, st));
   const int S = gemm_splits(M, dm, 2 * dm, dt);
-  TRY(launch_gemm(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, st));
+  TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, st));
   TRY(launch_add_norm(s->part, S, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, st));
   TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, st));
   if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, st));
@@ -514,6 +602,7 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
 
 static adt_status sync_stream(hipStream_t st) {
   ADT_HIP(hipStreamSynchronize(st));
+  prof_collect();
   return ADT_OK;
 }
 
@@ -592,12 +681,19 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   ADT_CHECK_ARG(cu >= 1 && cu <= std::min(32, s->C0), ADT_E_STATE, "tree_expand: %d catch-up rows", cu);
   std::vector<int32_t> ctok(s->tokens.begin() + Ld, s->tokens.begin() + L + 1), cf(cu);
   for (int i = 0; i < cu; ++i) cf[i] = i;
+  const bool table = s->d.draft_table != nullptr;
+  const int trows = s->d.draft_table_rows;
   TRY(launch_set_i32(s->ctok, small_of(ctok.data(), cu), cu, st));
-  TRY(launch_set_i32(s->cfsrc, small_of(cf.data(), cu), cu, st));
-  TRY(launch_iota(s->cpos, cu, Ld, 1, st));
-  TRY(launch_chain_masks(s->cmask, cu, st));
-  TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
-                    s->dlogits, st));
+  if (table) {
+    TRY(launch_table_rows(s->ctok + (cu - 1), 1, 0, trows, s->idx, st));
+    TRY(launch_gather_rows(s->d.draft_table, s->idx, 1, V, s->dlogits, ADT_F32, st));
+  } else {
+    TRY(launch_set_i32(s->cfsrc, small_of(cf.data(), cu), cu, st));
+    TRY(launch_iota(s->cpos, cu, Ld, 1, st));
+    TRY(launch_chain_masks(s->cmask, cu, st));
+    TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
+                      s->dlogits, st));
+  }
   // layer 1: the root's top-k children
   int lo, hi;
   cell_range(s, L + 1 - P, lo, hi);
@@ -611,8 +707,13 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     const int dl_row = 1 + (lvl - 2) * c.k_hi;
     float* lrows = s->dlogits + (size_t)dl_row * V;
     void* fout = (char*)s->dfeat + (size_t)(s->C0 + drow) * s->dm * esize(s->dt);
-    TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1, drow + nf,
-                      s->nx[cur].mask, fout, 0, nf, lrows, st));
+    if (table) {
+      TRY(launch_table_rows(s->nx[cur].tok, nf, lvl - 1, trows, s->idx, st));
+      TRY(launch_gather_rows(s->d.draft_table, s->idx, nf, V, lrows, ADT_F32, st));
+    } else {
+      TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1,
+                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, st));
+    }
     cell_range(s, L + lvl - P, lo, hi);
     TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
     TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, st));
@@ -697,8 +798,10 @@ extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, i
   if (a > 0) {
     int32_t lv[1] = {L};
     TRY(launch_set_i32(s->scal + 3, small_of(lv, 1), 1, st));
+    const int e = prof_begin(st);
     TRY(launch_kv_compact(s->d.k_cache, s->d.v_cache, 1, s->Lr * s->H, s->Dh, 0, (int64_t)s->d.s_cap * s->Dh,
                           s->scal + 3, s->tr.path, R, s->tr.nacc, a, s->dt, st));
+    prof_end(e, ADT_PROF_COMPACT, 4.0 * a * s->Lr * s->H * s->Dh * esize(s->dt), 0.0, st);
   }
   TRY(launch_gather_rows(s->feat, s->tr.path, a + 1, s->dm,
                          (char*)s->cfeat + (size_t)frow0 * s->dm * esize(s->dt), s->dt, st));

@@ -43,6 +43,17 @@ __global__ void tree_rows_kernel(const int32_t* depth, const int32_t* n_nodes, i
   }
 }
 
+// Row indices of a caller-supplied draft-logit table: (depth * 131 + token) mod rows.
+__global__ void table_rows_kernel(const int32_t* tok, int count, int depth, int rows, int32_t* idx) {
+  for (int i = threadIdx.x; i < count; i += blockDim.x) idx[i] = (int)(((int64_t)depth * 131 + tok[i]) % rows);
+}
+
+adt_status launch_table_rows(const int32_t* tok, int count, int depth, int rows, int32_t* idx, hipStream_t st) {
+  table_rows_kernel<<<1, 128, 0, st>>>(tok, count, depth, rows, idx);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
 adt_status launch_set_i32(int32_t* dst, const SmallI32& vals, int count, hipStream_t st) {
   ADT_CHECK_ARG(count >= 0 && count <= 32, ADT_E_ARG, "set_i32: count %d", count);
   if (count == 0) return ADT_OK;

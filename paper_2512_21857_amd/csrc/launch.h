@@ -75,6 +75,7 @@ struct SmallI32 {
 };
 adt_status launch_set_i32(int32_t* dst, const SmallI32& vals, int count, hipStream_t st);
 adt_status launch_fill_pairs(int32_t* dst, int rows, int lo, int hi, hipStream_t st);
+adt_status launch_table_rows(const int32_t* tok, int count, int depth, int rows, int32_t* idx, hipStream_t st);
 adt_status launch_iota(int32_t* dst, int count, int start, int step, hipStream_t st);
 adt_status launch_chain_masks(uint64_t* mask, int n, hipStream_t st);
 adt_status launch_tree_rows(const int32_t* depth, const int32_t* n_nodes, int n_max, int L, int P, int n_image,

@@ -176,7 +176,7 @@ class DeviceSession:
 
     def __init__(self, model: DeviceModel, cfg, poisson: Optional[np.ndarray] = None,
                  knn: Optional[torch.Tensor] = None, accept_seed: Optional[int] = None, fixed_tree: bool = False,
-                 accept_mode: Optional[str] = None):
+                 accept_mode: Optional[str] = None, draft_table: Optional[torch.Tensor] = None):
         m = cfg.model
         self.model = model
         self.cfg = cfg
@@ -201,7 +201,9 @@ class DeviceSession:
                                _p(self.dk_cache), _p(self.dv_cache),
                                C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched), self.accept,
                                C.cast(self._poisson, C.POINTER(C.c_int32)) if self._poisson is not None else None,
-                               1 if fixed_tree else 0, None, 0)
+                               1 if fixed_tree else 0, _p(draft_table),
+                               0 if draft_table is None else draft_table.shape[0], None, 0)
+        self.draft_table = draft_table
         need = lib().adt_session_workspace_size(model.handle, C.byref(desc))
         if need == 0:
             check(lib().adt_session_create(model.handle, C.byref(desc), C.byref(C.c_void_p())))
