@@ -18,6 +18,9 @@ mass; x is accepted with probability (mass of x + credited mass), and on rejecti
 whole credited neighbourhood is removed from the residual.  delta = 0 or one neighbour
 reduces it to exact mode.
 
+If a rejection empties the truncated support (possible when top_k is small) the bonus is
+the top-1 id of p.
+
 Numbers: p is quantised once per row to integer weights w = rint(exp(z - max z) * 2^32)
 with z = logit / T over the top-K allowed ids, computed in float32 (the precision the
 kernel decides in); all later arithmetic is exact integer.  A draw is
@@ -87,6 +90,11 @@ def quantised_weights(logit_row: np.ndarray, lo: int, hi: int, temperature: floa
     return w
 
 
+def top1_id(logit_row: np.ndarray, lo: int, hi: int, temperature: float) -> int:
+    z = np.asarray(logit_row[lo:hi], dtype=np.float32) / np.float32(temperature)
+    return lo + int(np.argmax(z))
+
+
 def inverse_cdf(w: np.ndarray, r: int) -> int:
     """Smallest id i with sum_{j <= i} w_j > r (ids ascending)."""
     acc = 0
@@ -117,7 +125,7 @@ def accept_sampling(logits: np.ndarray, parent, token, allowed, *, temperature: 
             trial += 1
             credit = [x]
             mass = int(w[x])
-            if mode == "relaxed":
+            if mode == "relaxed" and x < len(knn):
                 thr = (W * delta_q) >> DELTA_FRAC_BITS
                 extra = 0
                 for y in knn[x][1:knn_k]:
@@ -135,7 +143,8 @@ def accept_sampling(logits: np.ndarray, parent, token, allowed, *, temperature: 
                 w[y] = 0
         if accepted is None:
             if W <= 0:
-                raise ValueError("residual distribution is empty")
+                # every id of the truncated support was removed: fall back to the top-1 id of p
+                return path, top1_id(logits[u], lo, hi, temperature)
             r = draw_below(uniform_u64(seed, step, u, trial), W)
             return path, inverse_cdf(w, r)
         path.append(accepted)

@@ -342,6 +342,7 @@ struct adt_session_s {
   int32_t *ctok, *cfsrc, *cpos, *idx;
   uint64_t* cmask;
   int32_t *top_id, *allowed_lvl, *scal;
+  float2* rope;   // [s_cap][head_dim / 2] cos/sin table
   float *top_val, *lse;
   void* attn_ws;
   size_t attn_ws_bytes;
@@ -433,6 +434,7 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->lse = b.take<float>(R);
   s->allowed_lvl = b.take<int32_t>(2 * R);
   s->scal = b.take<int32_t>(16);
+  s->rope = b.take<float2>((size_t)s->d.s_cap * (s->Dh / 2));
   s->attn_ws_bytes = tree_attn_ws_bytes(1, s->H, s->Dh, R, s->d.s_cap, s->dt);
   s->attn_ws = b.take<char>(std::max<size_t>(s->attn_ws_bytes, 256));
   s->acc_ws_bytes = adt_accept_workspace_size(s->V);
@@ -492,6 +494,8 @@ extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_d
   s->d.allowed = nullptr;
   s->d.poisson = nullptr;
   hipError_t he = hipMemcpy(s->allowed_img, s->allowed_h.data(), sizeof(int32_t) * 2 * s->T, hipMemcpyHostToDevice);
+  if (he == hipSuccess && launch_rope_table(s->rope, s->d.s_cap, s->Dh, m->d.rope_theta, nullptr) == ADT_OK)
+    he = hipDeviceSynchronize();
   if (he != hipSuccess) {
     delete s;
     set_error("session_create: %s", hipGetErrorString(he));
@@ -515,9 +519,10 @@ static SmallI32 small_of(const int32_t* v, int n) {
   return s;
 }
 
-static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, hipStream_t st) {
-  int32_t v[3] = {kv_len, nq, ntail};
-  return launch_set_i32(s->scal, small_of(v, 3), 3, st);
+// scal[0..3] = attention prefix length, query rows, tail rows, first cache slot of the rows.
+static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, int slot0, hipStream_t st) {
+  int32_t v[4] = {kv_len, nq, ntail, slot0};
+  return launch_set_i32(s->scal, small_of(v, 4), 4, st);
 }
 
 // Algorithmic HBM bytes of a projection: weights once, the input rows, fp32 output rows.
@@ -539,14 +544,14 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   const int64_t stride_h = (int64_t)s->d.s_cap * Dh;
   const float eps = m->d.norm_eps;
   const float scale = 1.f / std::sqrt((float)Dh);
-  TRY(set_scalars(s, L_pre, M, n_tail, st));
+  TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
   for (int l = l0; l < l1; ++l) {
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
     int S = gemm_splits(M, 3 * dm, dm, dt);
     TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
-    TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, slot0, m->d.rope_theta, s->q, kc, vc, stride_h, dt, st));
+    TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
     {
       // K1 + K1c: the prefix K/V once, tree Q/K/V in and O out, the masks.
       const int e = prof_begin(st);
@@ -797,10 +802,10 @@ extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, i
                 "accept_commit: %d catch-up rows exceed %d (too many cycles without expansion)", frow0 + a + 1, s->C0);
   if (a > 0) {
     int32_t lv[1] = {L};
-    TRY(launch_set_i32(s->scal + 3, small_of(lv, 1), 1, st));
+    TRY(launch_set_i32(s->scal + 8, small_of(lv, 1), 1, st));
     const int e = prof_begin(st);
     TRY(launch_kv_compact(s->d.k_cache, s->d.v_cache, 1, s->Lr * s->H, s->Dh, 0, (int64_t)s->d.s_cap * s->Dh,
-                          s->scal + 3, s->tr.path, R, s->tr.nacc, a, s->dt, st));
+                          s->scal + 8, s->tr.path, R, s->tr.nacc, a, s->dt, st));
     prof_end(e, ADT_PROF_COMPACT, 4.0 * a * s->Lr * s->H * s->Dh * esize(s->dt), 0.0, st);
   }
   TRY(launch_gather_rows(s->feat, s->tr.path, a + 1, s->dm,

@@ -1,15 +1,308 @@
-// Exact and relaxed tree acceptance by sampling (Sec. 3.1, Eq. 1).
+// Exact and relaxed acceptance by sampling along one verified tree (Sec. 3.1, Eq. 1).
+//
+// The drafted children are deterministic top-k proposals, so the proposal distribution
+// of Eq. 1 is a point mass: child x is accepted with probability p(x); on rejection x is
+// removed from p and the next sibling is tried; if every child is rejected the bonus
+// token is drawn from the residual.  Relaxed mode (the ADT-Tree+LANTERN rows of Tables
+// I-II) also credits x with the mass of its nearest codebook neighbours while that mass
+// stays within delta of the remaining total, and removes the credited set on rejection.
+//
+// p at a row is held as integer weights w = rint(exp(z - max z) * 2^32) over the top_k
+// allowed ids (z = logit / T, fp32); every later operation is exact integer arithmetic,
+// so the walk does not depend on summation order.  One workgroup per tree: the weights of
+// a row are built cooperatively (64-bit radix select for the top-k threshold, block
+// reductions), the sibling walk runs on one lane, the bonus is found by a block-wide
+// prefix scan over ids in ascending order.
 #include "../launch.h"
 
 namespace adt {
 
+constexpr int AS_THREADS = 1024;
+constexpr int AS_DELTA_BITS = 16;
+
+// Philox4x32-10 (Salmon et al., SC'11): counter (c0..c3), key (k0, k1).
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
+    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+    k0 += W0;
+    k1 += W1;
+  }
+}
+
+__device__ __forceinline__ uint64_t draw_below(uint64_t seed, uint32_t step, uint32_t node, uint32_t trial,
+                                               uint64_t W) {
+  uint32_t c[4] = {step, node, trial, 0u};
+  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+  const uint64_t U = ((uint64_t)c[1] << 32) | c[0];
+  return __umul64hi(U, W);
+}
+
+// Order-preserving 64-bit key: larger z first, then lower id first.
+__device__ __forceinline__ uint64_t zkey(float z, int id) {
+  uint32_t b = __float_as_uint(z);
+  b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)b << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)id);
+}
+
+struct SampleShared {
+  uint32_t hist[256];
+  uint64_t u64[AS_THREADS / WAVE];
+  float f32[AS_THREADS / WAVE];
+  uint64_t scan[AS_THREADS];
+  uint64_t thr;
+  uint64_t total;
+  float zmax;
+  int node, trial, accepted, done, bonus, a, need;
+};
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
+  const uint32_t lo = __shfl_xor((uint32_t)v, o, WAVE), hi = __shfl_xor((uint32_t)(v >> 32), o, WAVE);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ uint64_t block_sum_u64(uint64_t v, SampleShared& sh) {
+  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+  __syncthreads();
+  if (threadIdx.x % WAVE == 0) sh.u64[threadIdx.x / WAVE] = v;
+  __syncthreads();
+  uint64_t s = 0;
+  for (int i = 0; i < AS_THREADS / WAVE; ++i) s += sh.u64[i];
+  __syncthreads();
+  return s;
+}
+
+__device__ float block_max_f32(float v, SampleShared& sh) {
+  v = wave_max(v);
+  __syncthreads();
+  if (threadIdx.x % WAVE == 0) sh.f32[threadIdx.x / WAVE] = v;
+  __syncthreads();
+  float m = -INFINITY;
+  for (int i = 0; i < AS_THREADS / WAVE; ++i) m = fmaxf(m, sh.f32[i]);
+  __syncthreads();
+  return m;
+}
+
+// The K-th largest 64-bit key of the row (K < count): exactly K keys are >= it.
+__device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T, SampleShared& sh) {
+  uint64_t prefix = 0, mask = 0;
+  int need = K;   // rank (1-based) of the threshold among keys matching the prefix
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    for (int i = threadIdx.x; i < 256; i += AS_THREADS) sh.hist[i] = 0;
+    __syncthreads();
+    for (int i = lo + threadIdx.x; i < hi; i += AS_THREADS) {
+      const uint64_t k = zkey(x[i] / T, i);
+      if ((k & mask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int acc = 0, b = 255;
+      for (; b > 0; --b) {
+        if (acc + (int)sh.hist[b] >= need) break;
+        acc += sh.hist[b];
+      }
+      sh.thr = prefix | ((uint64_t)b << shift);
+      sh.need = need - acc;
+    }
+    __syncthreads();
+    prefix = sh.thr;
+    need = sh.need;
+    mask |= (uint64_t)255 << shift;
+    __syncthreads();
+  }
+  return prefix;
+}
+
+__global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
+    const float* __restrict__ logits, int64_t ld, int V, const int32_t* __restrict__ parent,
+    const int32_t* __restrict__ token, const int32_t* __restrict__ allowed, const int32_t* __restrict__ n_nodes,
+    int n_max, int mode, float T, int top_k, uint32_t delta_q, int knn_k, int knn_rows, int knn_stride,
+    const int32_t* __restrict__ knn, uint64_t seed, uint32_t step, uint64_t* __restrict__ w,
+    int32_t* __restrict__ path, int32_t* __restrict__ n_acc, int32_t* __restrict__ bonus) {
+  __shared__ SampleShared sh;
+  const int tid = threadIdx.x;
+  const int n = min(*n_nodes, n_max);
+  if (tid == 0) {
+    sh.node = 0;
+    sh.a = 0;
+    sh.done = 0;
+    sh.bonus = 0;
+    path[0] = 0;
+  }
+  __syncthreads();
+  for (int guard = 0; guard < ADT_MAX_NODES; ++guard) {
+    const int u = sh.node;
+    const int lo = max(0, min(allowed[u * 2], V)), hi = max(lo, min(allowed[u * 2 + 1], V));
+    const float* x = logits + (int64_t)u * ld;
+    const int cnt = hi - lo;
+    // --- top-k threshold over (z desc, id asc)
+    uint64_t thr = 0;
+    if (top_k > 0 && top_k < cnt) thr = radix_select(x, lo, hi, top_k, T, sh);
+    // --- max z of the kept set, weights, total
+    float zm = -INFINITY;
+    for (int i = lo + tid; i < hi; i += AS_THREADS) {
+      const float z = x[i] / T;
+      if (zkey(z, i) >= thr) zm = fmaxf(zm, z);
+    }
+    zm = block_max_f32(zm, sh);
+    uint64_t part = 0;
+    for (int i = tid; i < V; i += AS_THREADS) {
+      uint64_t wi = 0;
+      if (i >= lo && i < hi) {
+        const float z = x[i] / T;
+        if (zkey(z, i) >= thr) {
+          const float e = expf(z - zm);
+          wi = (uint64_t)rint((double)e * 4294967296.0);
+        }
+      }
+      w[i] = wi;
+      part += wi;
+    }
+    const uint64_t total = block_sum_u64(part, sh);
+    __threadfence_block();
+    __syncthreads();
+    // --- sibling walk (one lane; w lives in global memory and is only touched by this lane)
+    if (tid == 0) {
+      uint64_t W = total;
+      int trial = 0, acc = -1;
+      for (int c = u + 1; c < n; ++c) {
+        if (parent[c] != u) continue;
+        const int xt = min(max(token[c], 0), V - 1);
+        const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)trial, W);
+        ++trial;
+        uint64_t mass = w[xt];
+        int credit_n = 0;
+        if (mode == ADT_ACCEPT_RELAXED && xt < knn_rows) {
+          const uint64_t lim = (W * (uint64_t)delta_q) >> AS_DELTA_BITS;
+          uint64_t extra = 0;
+          const int32_t* nb = knn + (int64_t)xt * knn_stride;
+          for (int j = 1; j < knn_k; ++j) {
+            const int y = nb[j];
+            const uint64_t wy = (y >= 0 && y < V) ? w[y] : 0;
+            if (extra + wy > lim) break;
+            extra += wy;
+            ++credit_n;
+          }
+          mass += extra;
+        }
+        if (r < mass) {
+          acc = c;
+          break;
+        }
+        W -= w[xt];
+        w[xt] = 0;
+        if (credit_n > 0) {
+          const int32_t* nb = knn + (int64_t)xt * knn_stride;
+          for (int j = 1; j <= credit_n; ++j) {
+            const int y = nb[j];
+            if (y >= 0 && y < V) {
+              W -= w[y];
+              w[y] = 0;
+            }
+          }
+        }
+      }
+      sh.accepted = acc;
+      sh.trial = trial;
+      sh.total = W;
+      if (acc >= 0) {
+        sh.a += 1;
+        path[sh.a] = acc;
+        sh.node = acc;
+      }
+    }
+    __threadfence_block();
+    __syncthreads();
+    if (sh.accepted >= 0) continue;
+    // --- bonus from the residual: smallest id with prefix(w) > r
+    const uint64_t W = sh.total;
+    if (W == 0) {
+      // residual empty: the top-1 id of p (largest z, lowest id)
+      float bz = -INFINITY;
+      int bi = 0x7FFFFFFF;
+      for (int i = lo + tid; i < hi; i += AS_THREADS) {
+        const float z = x[i] / T;
+        if (z > bz || (z == bz && i < bi)) {
+          bz = z;
+          bi = i;
+        }
+      }
+      sh.scan[tid] = ((uint64_t)__float_as_uint(bz) << 32) | (uint32_t)bi;
+      __syncthreads();
+      if (tid == 0) {
+        float best = -INFINITY;
+        int bid = lo;
+        for (int t = 0; t < AS_THREADS; ++t) {
+          const float z = __uint_as_float((uint32_t)(sh.scan[t] >> 32));
+          const int id = (int)(uint32_t)sh.scan[t];
+          if (id == 0x7FFFFFFF) continue;
+          if (z > best || (z == best && id < bid)) {
+            best = z;
+            bid = id;
+          }
+        }
+        sh.bonus = bid;
+      }
+      __syncthreads();
+      break;
+    }
+    const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)sh.trial, W);
+    const int per = (cnt + AS_THREADS - 1) / AS_THREADS;
+    const int b0 = lo + tid * per, b1 = min(hi, b0 + per);
+    uint64_t s = 0;
+    for (int i = b0; i < b1; ++i) s += w[i];
+    sh.scan[tid] = s;
+    __syncthreads();
+    if (tid == 0) {   // exclusive scan of the per-thread sums
+      uint64_t run = 0;
+      for (int t = 0; t < AS_THREADS; ++t) {
+        const uint64_t v = sh.scan[t];
+        sh.scan[t] = run;
+        run += v;
+      }
+    }
+    __syncthreads();
+    uint64_t run = sh.scan[tid];
+    if (b0 < b1 && run <= r && r < run + s) {
+      for (int i = b0; i < b1; ++i) {
+        run += w[i];
+        if (run > r) {
+          sh.bonus = i;
+          break;
+        }
+      }
+    }
+    __syncthreads();
+    break;
+  }
+  if (tid == 0) {
+    *n_acc = sh.a;
+    *bonus = sh.bonus;
+  }
+}
+
 size_t accept_ws_bytes(int V) { return (size_t)V * 8 + 4096; }
 
-adt_status launch_accept_sample(const float*, int64_t, int, const int32_t*, const int32_t*, const int32_t*,
-                                const int32_t*, int, const adt_accept_cfg&, uint64_t, int32_t*, int32_t*, int32_t*,
-                                void*, size_t, hipStream_t) {
-  adt::set_error("sampling acceptance is not built yet");
-  return ADT_E_UNSUPPORTED;
+adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
+                                const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
+                                uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
+                                hipStream_t st) {
+  ADT_CHECK_ARG(ws_bytes >= (size_t)V * 8, ADT_E_CAPACITY, "accept_sample: workspace");
+  const uint32_t dq = (uint32_t)lrintf(cfg.delta * (float)(1 << AS_DELTA_BITS));
+  const int relaxed = cfg.mode == ADT_ACCEPT_RELAXED;
+  accept_sample_kernel<<<1, AS_THREADS, 0, st>>>(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg.mode,
+                                                 cfg.temperature, cfg.top_k, dq, relaxed ? cfg.knn_k : 1,
+                                                 relaxed ? cfg.knn_rows : 0, cfg.knn_stride, cfg.knn, cfg.seed,
+                                                 (uint32_t)step, (uint64_t*)ws, path, n_acc, bonus);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
 }
 
 }  // namespace adt

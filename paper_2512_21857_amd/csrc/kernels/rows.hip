@@ -45,77 +45,130 @@ __global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __res
   }
 }
 
+// Sum of the split-K partials of four consecutive columns.
+__device__ __forceinline__ float4 sum_parts4(const float* __restrict__ part, int splits, int64_t stride, int64_t off) {
+  float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int s = 0; s < splits; ++s) {
+    const float4 v = *reinterpret_cast<const float4*>(part + s * stride + off);
+    y.x += v.x;
+    y.y += v.y;
+    y.z += v.z;
+    y.w += v.w;
+  }
+  return y;
+}
+
 // y = sum_s part[s][m][:]; h[m] = (assign ? y : h[m] + y); if a: a[m] = RMSNorm(h[m]).
+// One block per row, four columns per thread (d % 4 == 0, d <= 4 * blockDim.x * 4).
 template <typename T>
-__global__ __launch_bounds__(ROW_THREADS) void add_norm_kernel(const float* __restrict__ part, int splits, int M, int d,
-                                                               int assign, float eps, float* __restrict__ h,
-                                                               T* __restrict__ a) {
+__global__ __launch_bounds__(1024) void add_norm_kernel(const float* __restrict__ part, int splits, int M, int d,
+                                                        int assign, float eps, float* __restrict__ h,
+                                                        T* __restrict__ a) {
   __shared__ float red[16];
   const int m = blockIdx.x;
+  const int64_t stride = (int64_t)M * d;
+  float4 hv[4];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    float y = 0.f;
-    for (int s = 0; s < splits; ++s) y += part[((int64_t)s * M + m) * d + i];
-    const float v = assign ? y : h[(int64_t)m * d + i] + y;
-    h[(int64_t)m * d + i] = v;
-    ss += v * v;
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int c = (threadIdx.x + it * blockDim.x) * 4;
+    if (c < d) {
+      const float4 y = sum_parts4(part, splits, stride, (int64_t)m * d + c);
+      float4 v = y;
+      if (!assign) {
+        const float4 o = *reinterpret_cast<const float4*>(h + (int64_t)m * d + c);
+        v = make_float4(o.x + y.x, o.y + y.y, o.z + y.z, o.w + y.w);
+      }
+      *reinterpret_cast<float4*>(h + (int64_t)m * d + c) = v;
+      hv[it] = v;
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
   }
   if (a == nullptr) return;
   const float r = rsqrtf(block_sum(ss, red) / d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+#pragma unroll
+  for (int it = 0; it < 4; ++it) {
+    const int c = (threadIdx.x + it * blockDim.x) * 4;
+    if (c < d) {
+      T* out = a + (int64_t)m * d + c;
+      Elem<T>::store(out, 0, hv[it].x * r);
+      Elem<T>::store(out, 1, hv[it].y * r);
+      Elem<T>::store(out, 2, hv[it].z * r);
+      Elem<T>::store(out, 3, hv[it].w * r);
+    }
+  }
 }
 
-// Sum the QKV partials of row m, rotate q and k (rotate-half RoPE at position pos[m], angles
-// in double precision), write q to qout[m][H][Dh] and k, v to cache slot slot0 + m of every
-// head.  Cache element (h, slot, :) at kc + h*stride_h + slot*Dh.
+// cos / sin of rotate-half RoPE for every slot position: tab[p][j] = (cos, sin)(p * theta^(-2j/Dh)),
+// computed in double precision and stored as fp32.
+__global__ void rope_table_kernel(float2* __restrict__ tab, int positions, int half, int Dh, double theta) {
+  const int64_t total = (int64_t)positions * half;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+    const int p = (int)(i / half), j = (int)(i % half);
+    double sn, cs;
+    sincos((double)p * pow(theta, -2.0 * j / Dh), &sn, &cs);
+    tab[i] = make_float2((float)cs, (float)sn);
+  }
+}
+
+// Sum the QKV partials of row m, rotate q and k at position pos[m] (table lookup), write q to
+// qout[m][H][Dh] and k, v to cache slot (*slot0 + m) of every head.  Cache element
+// (h, slot, :) at kc + h*stride_h + slot*Dh.  Grid (M, pairs / 256), one (head, pair) per thread.
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __restrict__ part, int splits, int M,
                                                                int H, int Dh, const int32_t* __restrict__ pos,
-                                                               int slot0, double theta, T* __restrict__ qout,
+                                                               const int32_t* __restrict__ slot0,
+                                                               const float2* __restrict__ rope, T* __restrict__ qout,
                                                                T* __restrict__ kc, T* __restrict__ vc,
                                                                int64_t stride_h) {
   const int m = blockIdx.x;
   const int d = H * Dh, N = 3 * d, half = Dh / 2;
-  const double p = (double)pos[m];
-  const int64_t slot = slot0 + m;
-  auto y = [&](int c) {
-    float acc = 0.f;
-    for (int s = 0; s < splits; ++s) acc += part[((int64_t)s * M + m) * N + c];
-    return acc;
-  };
-  for (int i = threadIdx.x; i < H * half; i += blockDim.x) {
-    const int hh = i / half, j = i % half;
-    const double ang = p * pow(theta, -2.0 * j / Dh);
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    const int c1 = hh * Dh + j, c2 = c1 + half;
-    const double q1 = y(c1), q2 = y(c2), k1 = y(d + c1), k2 = y(d + c2);
-    Elem<T>::store(qout, (int64_t)m * d + c1, (float)(q1 * cs - q2 * sn));
-    Elem<T>::store(qout, (int64_t)m * d + c2, (float)(q2 * cs + q1 * sn));
-    T* kr = kc + hh * stride_h + slot * Dh;
-    Elem<T>::store(kr, j, (float)(k1 * cs - k2 * sn));
-    Elem<T>::store(kr, j + half, (float)(k2 * cs + k1 * sn));
-    T* vr = vc + hh * stride_h + slot * Dh;
-    Elem<T>::store(vr, j, y(2 * d + c1));
-    Elem<T>::store(vr, j + half, y(2 * d + c2));
+  const int i = blockIdx.y * blockDim.x + threadIdx.x;
+  if (i >= H * half) return;
+  const int hh = i / half, j = i % half;
+  const int64_t stride = (int64_t)M * N, row = (int64_t)m * N;
+  const int c1 = hh * Dh + j, c2 = c1 + half;
+  float q1 = 0.f, q2 = 0.f, k1 = 0.f, k2 = 0.f, v1 = 0.f, v2 = 0.f;
+#pragma unroll 4
+  for (int s = 0; s < splits; ++s) {
+    const float* p = part + s * stride + row;
+    q1 += p[c1];
+    q2 += p[c2];
+    k1 += p[d + c1];
+    k2 += p[d + c2];
+    v1 += p[2 * d + c1];
+    v2 += p[2 * d + c2];
   }
+  const float2 cs = rope[(int64_t)pos[m] * half + j];
+  const int64_t slot = *slot0 + m;
+  Elem<T>::store(qout, (int64_t)m * d + c1, q1 * cs.x - q2 * cs.y);
+  Elem<T>::store(qout, (int64_t)m * d + c2, q2 * cs.x + q1 * cs.y);
+  T* kr = kc + hh * stride_h + slot * Dh;
+  Elem<T>::store(kr, j, k1 * cs.x - k2 * cs.y);
+  Elem<T>::store(kr, j + half, k2 * cs.x + k1 * cs.y);
+  T* vr = vc + hh * stride_h + slot * Dh;
+  Elem<T>::store(vr, j, v1);
+  Elem<T>::store(vr, j + half, v2);
 }
 
 // SwiGLU over gate/up partials packed in interleaved 16-column blocks: out[m][j] = silu(g) u.
+// Grid (M, F / (4 * 256)); four consecutive outputs per thread.
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void swiglu_kernel(const float* __restrict__ part, int splits, int M, int F,
                                                              T* __restrict__ out) {
   const int m = blockIdx.x, N = 2 * F;
-  for (int j = threadIdx.x; j < F; j += blockDim.x) {
-    const int cg = (j / 16) * 32 + j % 16, cu = cg + 16;
-    float g = 0.f, u = 0.f;
-    for (int s = 0; s < splits; ++s) {
-      g += part[((int64_t)s * M + m) * N + cg];
-      u += part[((int64_t)s * M + m) * N + cu];
-    }
-    Elem<T>::store(out, (int64_t)m * F + j, g / (1.f + expf(-g)) * u);
-  }
+  const int j = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+  if (j >= F) return;
+  const int cg = (j / 16) * 32 + j % 16;
+  const int64_t stride = (int64_t)M * N, row = (int64_t)m * N;
+  const float4 g = sum_parts4(part, splits, stride, row + cg);
+  const float4 u = sum_parts4(part, splits, stride, row + cg + 16);
+  T* o = out + (int64_t)m * F + j;
+  Elem<T>::store(o, 0, g.x / (1.f + expf(-g.x)) * u.x);
+  Elem<T>::store(o, 1, g.y / (1.f + expf(-g.y)) * u.y);
+  Elem<T>::store(o, 2, g.z / (1.f + expf(-g.z)) * u.z);
+  Elem<T>::store(o, 3, g.w / (1.f + expf(-g.w)) * u.w);
 }
 
 // out[m][n] = sum_s part[s][m][n]  (logits).
@@ -230,21 +283,34 @@ adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* 
 
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
                            int dtype, hipStream_t st) {
-  ADT_DISPATCH_T(dtype, add_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, d, assign, eps, h, (T*)a));
+  ADT_CHECK_ARG(d % 4 == 0 && d <= 16 * 1024, ADT_E_SHAPE, "add_norm: d=%d", d);
+  int threads = ((d / 4 + 3) / 4 + 63) / 64 * 64;
+  if (threads < 64) threads = 64;
+  ADT_DISPATCH_T(dtype, add_norm_kernel<T><<<M, threads, 0, st>>>(part, splits, M, d, assign, eps, h, (T*)a));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
-adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos, int slot0,
-                           double theta, void* qout, void* kc, void* vc, int64_t stride_h, int dtype, hipStream_t st) {
-  ADT_DISPATCH_T(dtype, qkv_rope_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, H, Dh, pos, slot0, theta,
-                                                                       (T*)qout, (T*)kc, (T*)vc, stride_h));
+adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, hipStream_t st) {
+  rope_table_kernel<<<512, 256, 0, st>>>(tab, positions, Dh / 2, Dh, theta);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos,
+                           const int32_t* slot0, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
+                           int dtype, hipStream_t st) {
+  dim3 grid(M, (H * Dh / 2 + ROW_THREADS - 1) / ROW_THREADS);
+  ADT_DISPATCH_T(dtype, qkv_rope_kernel<T><<<grid, ROW_THREADS, 0, st>>>(part, splits, M, H, Dh, pos, slot0, rope,
+                                                                          (T*)qout, (T*)kc, (T*)vc, stride_h));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
 adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st) {
-  ADT_DISPATCH_T(dtype, swiglu_kernel<T><<<M, ROW_THREADS, 0, st>>>(part, splits, M, F, (T*)out));
+  ADT_CHECK_ARG(F % 16 == 0, ADT_E_SHAPE, "swiglu: F=%d", F);
+  dim3 grid(M, (F / 4 + ROW_THREADS - 1) / ROW_THREADS);
+  ADT_DISPATCH_T(dtype, swiglu_kernel<T><<<grid, ROW_THREADS, 0, st>>>(part, splits, M, F, (T*)out));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

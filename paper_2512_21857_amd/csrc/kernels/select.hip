@@ -18,15 +18,34 @@ constexpr int SEL_THREADS = 256;
 
 __device__ __forceinline__ bool better(float a, int ia, float b, int ib) { return a > b || (a == b && ia < ib); }
 
+constexpr int TOPK_THREADS = 1024;
+constexpr int TOPK_WAVES = TOPK_THREADS / WAVE;
+
+// Wave-wide argmax of (value desc, id asc) with the owning lane.
+__device__ __forceinline__ void wave_best(float& v, int& id, int& lane) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const float ov = __shfl_xor(v, o, WAVE);
+    const int oi = __shfl_xor(id, o, WAVE), ol = __shfl_xor(lane, o, WAVE);
+    if (better(ov, oi, v, id)) {
+      v = ov;
+      id = oi;
+      lane = ol;
+    }
+  }
+}
+
+// Per row: top-k ids by (logit desc, id asc) over [lo, hi) and the log-sum-exp.  Each thread
+// keeps a sorted private list over a strided slice; each wave merges its 64 lists with k
+// rounds of shuffle argmax; wave 0 merges the per-wave lists the same way.
 template <int KMAX>
-__global__ __launch_bounds__(SEL_THREADS) void row_topk_kernel(const float* __restrict__ logits, int64_t ld, int V,
-                                                               const int32_t* __restrict__ allowed, int k,
-                                                               int32_t* __restrict__ top_id, float* __restrict__ top_val,
-                                                               float* __restrict__ lse) {
-  __shared__ float sv[SEL_THREADS / WAVE];
-  __shared__ int si[SEL_THREADS / WAVE];
-  __shared__ int st[SEL_THREADS / WAVE];
-  __shared__ float smx[SEL_THREADS / WAVE], ssum[SEL_THREADS / WAVE];
+__global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __restrict__ logits, int64_t ld, int V,
+                                                                const int32_t* __restrict__ allowed, int k,
+                                                                int32_t* __restrict__ top_id,
+                                                                float* __restrict__ top_val, float* __restrict__ lse) {
+  __shared__ float wv[TOPK_WAVES][KMAX];
+  __shared__ int wi[TOPK_WAVES][KMAX];
+  __shared__ float smx[TOPK_WAVES], ssum[TOPK_WAVES];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
   const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
   const float* x = logits + (int64_t)row * ld;
@@ -39,7 +58,7 @@ __global__ __launch_bounds__(SEL_THREADS) void row_topk_kernel(const float* __re
     id[j] = 0x7FFFFFFF;
   }
   float m = -INFINITY, s = 0.f;
-  for (int i = lo + tid; i < hi; i += SEL_THREADS) {
+  for (int i = lo + tid; i < hi; i += TOPK_THREADS) {
     const float xi = x[i];
     if (xi > m) {
       s = s * expf(m - xi) + 1.f;
@@ -63,25 +82,15 @@ __global__ __launch_bounds__(SEL_THREADS) void row_topk_kernel(const float* __re
       }
     }
   }
-  // log-sum-exp across the block
-  float M = wave_max(m);
-  float S = wave_sum(m == -INFINITY ? 0.f : s * expf(m - M));
+  const float M = wave_max(m);
+  const float S = wave_sum(m == -INFINITY ? 0.f : s * expf(m - M));
   if (lane == 0) {
     smx[wave] = M;
     ssum[wave] = S;
   }
-  __syncthreads();
-  if (tid == 0) {
-    float gm = -INFINITY;
-    for (int w = 0; w < SEL_THREADS / WAVE; ++w) gm = fmaxf(gm, smx[w]);
-    float gs = 0.f;
-    for (int w = 0; w < SEL_THREADS / WAVE; ++w)
-      if (smx[w] != -INFINITY) gs += ssum[w] * expf(smx[w] - gm);
-    lse[row] = gm + logf(gs);
-  }
-  // k rounds of block argmax over the heads of the private lists
-  int head = 0;
   const int kk = min(k, hi - lo);
+  // wave-level merge of the private lists
+  int head = 0;
   for (int r = 0; r < kk; ++r) {
     float hv = -INFINITY;
     int hid = 0x7FFFFFFF;
@@ -91,37 +100,39 @@ __global__ __launch_bounds__(SEL_THREADS) void row_topk_kernel(const float* __re
         hv = v[j];
         hid = id[j];
       }
-    float bv = hv;
-    int bi = hid, bt = tid;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, WAVE);
-      const int oi = __shfl_xor(bi, o, WAVE), ot = __shfl_xor(bt, o, WAVE);
-      if (better(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
-        bt = ot;
-      }
-    }
-    __syncthreads();
+    int bl = lane;
+    wave_best(hv, hid, bl);
+    if (lane == bl) ++head;
     if (lane == 0) {
-      sv[wave] = bv;
-      si[wave] = bi;
-      st[wave] = bt;
+      wv[wave][r] = hv;
+      wi[wave][r] = hid;
     }
-    __syncthreads();
-    float wv = sv[0];
-    int wi = si[0], wt = st[0];
-    for (int w = 1; w < SEL_THREADS / WAVE; ++w)
-      if (better(sv[w], si[w], wv, wi)) {
-        wv = sv[w];
-        wi = si[w];
-        wt = st[w];
-      }
-    if (tid == wt) ++head;
-    if (tid == 0) {
-      top_id[row * KMAX + r] = wi;
-      top_val[row * KMAX + r] = wv;
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  if (lane == 0) {
+    float gm = -INFINITY;
+    for (int w = 0; w < TOPK_WAVES; ++w) gm = fmaxf(gm, smx[w]);
+    float gs = 0.f;
+    for (int w = 0; w < TOPK_WAVES; ++w)
+      if (smx[w] != -INFINITY) gs += ssum[w] * expf(smx[w] - gm);
+    lse[row] = gm + logf(gs);
+  }
+  // block-level merge: lane w (< TOPK_WAVES) walks wave w's sorted list
+  int h2 = 0;
+  for (int r = 0; r < kk; ++r) {
+    float hv = -INFINITY;
+    int hid = 0x7FFFFFFF;
+    if (lane < TOPK_WAVES && h2 < kk) {
+      hv = wv[lane][h2];
+      hid = wi[lane][h2];
+    }
+    int bl = lane;
+    wave_best(hv, hid, bl);
+    if (lane == bl) ++h2;
+    if (lane == 0) {
+      top_id[row * KMAX + r] = hid;
+      top_val[row * KMAX + r] = hv;
     }
   }
 }
@@ -295,9 +306,9 @@ adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t
                            int32_t* top_id, float* top_val, float* lse, hipStream_t st) {
   ADT_CHECK_ARG(k >= 1 && k <= kmax && (kmax == 1 || kmax == 16), ADT_E_UNSUPPORTED, "row_topk: k=%d kmax=%d", k, kmax);
   if (kmax == 1)
-    row_topk_kernel<1><<<rows, SEL_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
+    row_topk_kernel<1><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
   else
-    row_topk_kernel<16><<<rows, SEL_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
+    row_topk_kernel<16><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -27,8 +27,10 @@ adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* 
                               int M, int d, void* x, int dtype, hipStream_t st);
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
                            int dtype, hipStream_t st);
-adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos, int slot0,
-                           double theta, void* qout, void* kc, void* vc, int64_t stride_h, int dtype, hipStream_t st);
+adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, hipStream_t st);
+adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos,
+                           const int32_t* slot0, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
+                           int dtype, hipStream_t st);
 adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st);
 adt_status launch_reduce_store(const float* part, int splits, int M, int N, float* out, int64_t ldo, hipStream_t st);
 adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,

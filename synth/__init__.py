@@ -310,3 +310,16 @@ def compaction_paths(rng: np.random.Generator, n_nodes: np.ndarray, a_max: int =
         path[b, 1:ab + 1] = sel
         a[b] = ab
     return path, a
+
+
+def random_knn_table(rows: int, k: int, seed: int = 0) -> np.ndarray:
+    """A neighbour table for acceptance tests: row x lists x first, then k-1 other ids in a
+    seeded random order (no similarity computation)."""
+    rng = np.random.default_rng([seed, 30_000])
+    out = np.zeros((rows, k), dtype=np.int32)
+    for x in range(rows):
+        others = rng.choice(rows - 1, size=k - 1, replace=False)
+        others = others + (others >= x)
+        out[x, 0] = x
+        out[x, 1:] = others
+    return out

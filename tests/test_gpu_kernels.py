@@ -183,3 +183,75 @@ def test_accept_greedy_planted(rt):
                                               t(np.array([n], dtype=np.int32)), cfg, 0)
         a = int(n_acc.item())
         assert a == len(ref_path) and path[1:a + 1].cpu().tolist() == ref_path and int(bonus.item()) == ref_bonus
+
+
+def _random_tree_tokens(rng, n, V, lo, hi):
+    parent = synth.random_parents(rng, n, max_children=6, max_depth=9)
+    token = np.zeros(n, dtype=np.int32)
+    for u in range(n):
+        kids = [c for c in range(n) if parent[c] == u]
+        token[kids] = rng.choice(np.arange(lo, hi), size=len(kids), replace=False)
+    return parent.astype(np.int32), token
+
+
+@pytest.mark.parametrize("mode,top_k,T", [("exact", 2000, 1.0), ("exact", 0, 0.7), ("exact", 3, 1.0),
+                                          ("relaxed", 2000, 1.0), ("relaxed", 50, 1.3)])
+def test_accept_sampling_bit_exact(rt, mode, top_k, T):
+    """Exact / relaxed acceptance on the same fp32 logits: identical path and bonus for every
+    (seed, step).  Logits are sharpened on planted chains so long paths get accepted too."""
+    from oracle.accept import accept_sampling
+    rng = np.random.default_rng(21)
+    V, lo, hi = 8448, 0, 8192
+    knn = synth.random_knn_table(hi, 100, seed=4)
+    tk = torch.from_numpy(knn).cuda()
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    agree = total_acc = 0
+    for trial in range(24):
+        n = int(rng.integers(1, 62))
+        parent, token = _random_tree_tokens(rng, n, V, lo, hi)
+        logits = (rng.standard_normal((n, V)) * 1.5).astype(np.float32)
+        for u in range(n):
+            kids = [c for c in range(n) if parent[c] == u]
+            if kids and rng.random() < 0.7:
+                logits[u, token[kids[0]]] += 7.0
+        allowed = np.tile([lo, hi], (n, 1)).astype(np.int32)
+        for step in range(3):
+            seed = 1000 + trial
+            kw = dict(temperature=T, top_k=top_k, seed=seed, step=step, mode=mode)
+            if mode == "relaxed":
+                kw.update(delta=0.1, knn=knn, knn_k=100)
+            ref_path, ref_bonus = accept_sampling(logits, parent, token, allowed, **kw)
+            cfg = rt.accept_cfg(mode, T, top_k, 0.1 if mode == "relaxed" else 0.0, tk if mode == "relaxed" else None,
+                                100 if mode == "relaxed" else 1, seed)
+            path, n_acc, bonus = rt.verify_accept(t(logits), t(parent), t(token), t(allowed),
+                                                  t(np.array([n], dtype=np.int32)), cfg, step)
+            a = int(n_acc.item())
+            assert path[1:a + 1].cpu().tolist() == ref_path and int(bonus.item()) == ref_bonus, \
+                f"trial {trial} step {step}"
+            agree += 1
+            total_acc += a
+    assert agree == 72 and total_acc > 0
+
+
+def test_accept_sampling_law_on_gpu(rt):
+    """Committed first token over 4000 steps on the GPU follows p (chi-square), root with 3 children."""
+    V = 16
+    rng = np.random.default_rng(3)
+    root = rng.standard_normal(V).astype(np.float32)
+    parent = np.array([-1, 0, 0, 0], dtype=np.int32)
+    token = np.array([0, 5, 2, 9], dtype=np.int32)
+    logits = np.vstack([root, rng.standard_normal((3, V)).astype(np.float32)])
+    allowed = np.tile([0, V], (4, 1)).astype(np.int32)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    tl, tp, tt, ta, tn = t(logits), t(parent), t(token), t(allowed), t(np.array([4], dtype=np.int32))
+    cfg = rt.accept_cfg("exact", 1.0, 0, 0.0, None, 1, 77)
+    trials = 4000
+    counts = np.zeros(V)
+    for s in range(trials):
+        path, n_acc, bonus = rt.verify_accept(tl, tp, tt, ta, tn, cfg, s)
+        a = int(n_acc.item())
+        counts[token[int(path[1].item())] if a > 0 else int(bonus.item())] += 1
+    p = np.exp(root.astype(np.float64) - root.max())
+    p /= p.sum()
+    chi2 = float(np.sum((counts - trials * p) ** 2 / (trials * p)))
+    assert chi2 < 45.0          # 15 dof
