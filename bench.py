@@ -35,6 +35,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-microbench", action="store_true")
+    ap.add_argument("--no-fixed", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
 
 
@@ -157,6 +160,12 @@ def main():
     from paper_2512_21857_amd import abi, runtime as rt
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
+    if args.copy_calibration:
+        src = torch.ones(128 * 1024 * 1024, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = synth.get_config("llamagen_xl")
     print(f"[bench] generating weights for {cfg.name}", file=sys.stderr, flush=True)
     w = synth.model_weights(cfg, threads=min(16, os.cpu_count() or 8))
@@ -175,9 +184,11 @@ def main():
     value = nodes / dt
     prof = profile_pass(rt, abi, sess, args.profile_steps)
     # fixed max tree (depth 6, width 10, 60 nodes) for comparison
-    sfix = fresh(fixed=True)
-    run_steps(sfix, 3)
-    fdt, fnodes, ftokens, _ = timed(sfix, min(args.steps, 50))
+    fdt, fnodes = 1.0, 0
+    if not args.no_fixed:
+        sfix = fresh(fixed=True)
+        run_steps(sfix, 3)
+        fdt, fnodes, ftokens, _ = timed(sfix, min(args.steps, 50))
     g = prof["gemm"]
     gemm_avg_s = g["ms"] / max(g["launches"], 1) * 1e-3
     gemm_bytes = g["bytes"] / max(g["launches"], 1)

@@ -141,6 +141,15 @@ adt_status adt_verify_accept(const float* logits, int64_t ld, int32_t V, const i
                              uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* workspace,
                              size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ c3 support: neighbours
+ * Neighbour table of a VQ codebook for relaxed acceptance: out[x][0] = x, then the k-1
+ * other codes of highest cosine similarity to code x (fp32, ties to the lower id).
+ * codebook: [n][dim] fp32; out: [n][k] int32 (k <= 256); workspace:
+ * adt_codebook_knn_workspace_size(n) bytes.  Set-up work, run once per codebook. */
+size_t adt_codebook_knn_workspace_size(int32_t n);
+adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t dim, int32_t k, int32_t* out, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------ weights
  * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM
  * kernels stream.  srcs/rows: [host] arrays of n_src device pointers and their row counts;
@@ -211,6 +220,9 @@ typedef struct {
    * expansion (a2, a3) with known logits; NULL = run the draft head. */
   const float* draft_table;
   int32_t draft_table_rows;
+  /* 1: capture the verify and draft forwards as HIP graphs (one per tree shape, built on
+   * first use on a private stream, replayed on the caller's stream); 0: plain launches. */
+  int32_t use_graphs;
   void* workspace;
   size_t workspace_bytes;
 } adt_session_desc;
@@ -238,6 +250,9 @@ typedef struct {
   int32_t* allowed_rows;        /* [ADT_MAX_NODES][2] allowed range of each row's successor */
   int32_t* path; int32_t* n_acc; int32_t* bonus;  /* last acceptance */
   const int32_t* tokens_host;   /* [host] committed ids */
+  /* scratch of the last forward (last layer run): rotated queries [rows][d] dtype, attention
+   * output [rows][d] dtype, normed activations [rows][d] dtype, residual stream [rows][d] fp32 */
+  void* q; void* att; void* act; float* resid;
 } adt_session_view;
 
 size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* desc);
@@ -254,7 +269,11 @@ adt_status adt_session_get_view(const adt_session* s, adt_session_view* v);
  * tree size (root included). */
 adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_hat, int32_t n_budget, int32_t* n_nodes_out,
                            void* stream);
-/* Replaces the session's current tree with a caller tree: parent/token [host] n ids. */
+/* Replaces the session's current tree with a caller tree: parent/token [host] n ids, BFS
+ * ordered (parent[i] < i, parent[0] = -1), token[0] = the last committed token, 1 <= n <=
+ * ADT_MAX_NODES.  Called right after adt_tree_expand it keeps that expansion's draft-cache
+ * state (the root's draft row stays valid); otherwise the draft cache is left as it was.
+ * Synchronises.  ADT_E_ARG on a malformed tree, ADT_E_CAPACITY past the cache capacity. */
 adt_status adt_session_set_tree(adt_session* s, const int32_t* parent, const int32_t* token, int32_t n,
                                 void* stream);
 /* b1-b3: the target forward of the session's current tree at the committed length L:

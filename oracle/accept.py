@@ -40,6 +40,24 @@ from .numerics import draw_below, uniform_u64
 DELTA_FRAC_BITS = 16
 
 
+def codebook_knn(codebook: np.ndarray, k: int) -> np.ndarray:
+    """Neighbourhood of the relaxed mode: row x = x itself, then the k-1 other codes with the
+    highest cosine similarity to code x (float64; ties to the lower id)."""
+    c = np.asarray(codebook, dtype=np.float64)
+    c = c / np.linalg.norm(c, axis=1, keepdims=True)
+    sims = c @ c.T
+    n = len(c)
+    ids = np.arange(n)
+    out = np.zeros((n, k), dtype=np.int32)
+    for x in range(n):
+        row = sims[x].copy()
+        row[x] = -np.inf
+        order = np.lexsort((ids, -row))[: k - 1]
+        out[x, 0] = x
+        out[x, 1:] = order
+    return out
+
+
 def greedy_targets(logits: np.ndarray, allowed: np.ndarray) -> np.ndarray:
     """t_u = argmax over [lo_u, hi_u) (np.argmax returns the lowest index among ties)."""
     out = np.zeros(len(logits), dtype=np.int64)

@@ -115,6 +115,7 @@ class Decoder:
         par = np.stack([self._feat_before(p) for p in range(P)])
         self.model.draft_rows(self.tokens, par, pos, pos, causal, self.dcache)
         lo, hi = self.allowed_pos(P)
+        self.prefill_logits = logits[P - 1]
         _, first = self._pick(logits[P - 1:P], [-1], [self.tokens[-1]], np.array([[lo, hi]]), 0)
         self.tokens.append(first)
         self.L = P

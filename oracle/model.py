@@ -38,6 +38,7 @@ class OracleModel:
         self.cache_f64 = (total < 1_200_000_000) if cache_f64 is None else cache_f64
         self._f64: Dict[str, np.ndarray] = {}
         self.scale = 1.0 / np.sqrt(self.m.head_dim)
+        self.trace: Optional[Dict[str, np.ndarray]] = None   # set to {} to keep per-layer values
 
     # -- weights -------------------------------------------------------------------------
     def w(self, name: str) -> np.ndarray:
@@ -78,7 +79,11 @@ class OracleModel:
         h = h + o.reshape(rows, H * Dh) @ self.w(pre + ".wo").T
         b = self.rnd(rmsnorm(h))
         s = self.rnd(silu(b @ self.w(pre + ".wg").T) * (b @ self.w(pre + ".wu").T))
-        return h + s @ self.w(pre + ".wd").T
+        out = h + s @ self.w(pre + ".wd").T
+        if self.trace is not None:
+            self.trace.update({pre + ".q": q.reshape(rows, -1), pre + ".o": o.reshape(rows, -1),
+                               pre + ".h_attn": h, pre + ".b": b, pre + ".s": s, pre + ".h": out})
+        return out
 
     # -- full forwards ---------------------------------------------------------------------
     def target_rows(self, tokens, pos, slots, key_slots, cache: KVCache):

@@ -50,7 +50,7 @@ class SessionDesc(C.Structure):
     _fields_ = [("prefix_len", i32), ("n_image", i32), ("s_cap", i32), ("k_cache", p), ("v_cache", p),
                 ("dk_cache", p), ("dv_cache", p), ("allowed", ip), ("sched", SchedCfg), ("accept", AcceptCfg),
                 ("poisson", ip), ("fixed_tree", i32), ("draft_table", p), ("draft_table_rows", i32),
-                ("workspace", p), ("workspace_bytes", sz)]
+                ("use_graphs", i32), ("workspace", p), ("workspace_bytes", sz)]
 
 
 class StepOut(C.Structure):
@@ -62,7 +62,7 @@ class SessionView(C.Structure):
     _fields_ = [("L", i32), ("Ld", i32), ("step", i32), ("n_tokens", i32), ("n_nodes", i32),
                 ("logits", p), ("feat", p), ("draft_logits", p), ("parent", p), ("token", p), ("depth", p),
                 ("score", p), ("mask", p), ("allowed_rows", p), ("path", p), ("n_acc", p), ("bonus", p),
-                ("tokens_host", ip)]
+                ("tokens_host", ip), ("q", p), ("att", p), ("act", p), ("resid", p)]
 
 
 _SIGS = {
@@ -74,6 +74,8 @@ _SIGS = {
     "adt_kv_compact": (i32, [p, p, i32, i32, i32, i64, i64, p, p, i32, p, i32, i32, p]),
     "adt_accept_workspace_size": (sz, [i32]),
     "adt_verify_accept": (i32, [p, i64, i32, p, p, p, p, i32, C.POINTER(AcceptCfg), u64, p, p, p, p, sz, p]),
+    "adt_codebook_knn_workspace_size": (sz, [i32]),
+    "adt_codebook_knn": (i32, [p, i32, i32, i32, p, p, sz, p]),
     "adt_packed_bytes": (sz, [i32, i32, i32]),
     "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, p, p]),
     "adt_schedule_next": (i32, [C.POINTER(SchedCfg), i32, i32, i32, i32, i32, i32, i32, ip, ip]),

@@ -23,6 +23,7 @@ SOURCES = [
     "kernels/select.hip",
     "kernels/small.hip",
     "kernels/accept_sample.hip",
+    "kernels/knn.hip",
 ]
 
 # Packed fp32 VALU instructions are disabled for the device code.

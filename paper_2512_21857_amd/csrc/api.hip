@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <vector>
 
@@ -66,6 +67,16 @@ static void prof_end(int e, int cls, double bytes, double flops, hipStream_t st)
   if (e < 0) return;
   (void)hipEventRecord(g_prof.ev[e + 1], st);
   g_prof.pending.push_back({cls, e, e + 1, bytes, flops});
+}
+// An event pair for a launch that records its own start and end (hipExtLaunchKernelGGL).
+static int prof_pair() {
+  if (!g_prof.on || g_prof.next + 2 > (int)g_prof.ev.size()) return -1;
+  const int e = g_prof.next;
+  g_prof.next += 2;
+  return e;
+}
+static void prof_done(int e, int cls, double bytes, double flops) {
+  if (e >= 0) g_prof.pending.push_back({cls, e, e + 1, bytes, flops});
 }
 static void prof_collect() {
   if (!g_prof.on) return;
@@ -225,6 +236,14 @@ extern "C" adt_status adt_verify_accept(const float* logits, int64_t ld, int32_t
                      workspace_bytes, (hipStream_t)stream);
 }
 
+extern "C" size_t adt_codebook_knn_workspace_size(int32_t n) { return n > 0 ? knn_ws_bytes(n) : 0; }
+
+extern "C" adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t dim, int32_t k, int32_t* out,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+  ADT_CHECK_ARG(codebook && out && n >= 1 && dim >= 1, ADT_E_ARG, "codebook_knn: bad arguments");
+  return launch_codebook_knn(codebook, n, dim, k, out, workspace, workspace_bytes, (hipStream_t)stream);
+}
+
 extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype) {
   return packed_bytes(total_rows, K, dtype);
 }
@@ -348,6 +367,15 @@ struct adt_session_s {
   size_t attn_ws_bytes;
   void* acc_ws;
   size_t acc_ws_bytes;
+  // HIP graphs of the forwards, keyed by shape; captured on a private stream, replayed on
+  // the caller's stream.
+  bool graphs = true;
+  hipStream_t cap = nullptr;
+  std::map<int64_t, hipGraphExec_t> gexec;
+  ~adt_session_s() {
+    for (auto& kv : gexec) (void)hipGraphExecDestroy(kv.second);
+    if (cap) (void)hipStreamDestroy(cap);
+  }
 };
 
 static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_session_desc* d) {
@@ -486,6 +514,7 @@ extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_d
     return ADT_E_CAPACITY;
   }
   session_layout(s, (char*)d->workspace);
+  s->graphs = d->use_graphs != 0;
   s->allowed_h.assign(d->allowed, d->allowed + 2 * d->n_image);
   if (d->poisson) s->poisson.assign(d->poisson, d->poisson + d->n_image);
   s->rec_d.assign(d->n_image, 0);
@@ -525,13 +554,46 @@ static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, i
   return launch_set_i32(s->scal, small_of(v, 4), 4, st);
 }
 
+// Runs body(stream) through a cached graph (captured on first use for this key).  Eager
+// when graphs are off or the profiling hook is on (events cannot be recorded per kernel
+// inside a replayed graph).
+template <typename F>
+static adt_status run_graph(adt_session_s* s, int64_t key, hipStream_t st, F&& body) {
+  if (!s->graphs || g_prof.on) return body(st);
+  auto it = s->gexec.find(key);
+  if (it == s->gexec.end()) {
+    if (!s->cap) ADT_HIP(hipStreamCreateWithFlags(&s->cap, hipStreamNonBlocking));
+    ADT_HIP(hipStreamBeginCapture(s->cap, hipStreamCaptureModeThreadLocal));
+    const adt_status e = body(s->cap);
+    hipGraph_t g = nullptr;
+    const hipError_t he = hipStreamEndCapture(s->cap, &g);
+    if (e != ADT_OK) {
+      if (he == hipSuccess && g) (void)hipGraphDestroy(g);
+      return e;
+    }
+    ADT_HIP(he);
+    hipGraphExec_t ex = nullptr;
+    const hipError_t ie = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    ADT_HIP(ie);
+    it = s->gexec.emplace(key, ex).first;
+  }
+  ADT_HIP(hipGraphLaunch(it->second, st));
+  return ADT_OK;
+}
+
+static int64_t gkey(int kind, int a, int b, int c) {
+  return ((int64_t)kind << 48) | ((int64_t)a << 32) | ((int64_t)b << 16) | (int64_t)c;
+}
+
 // Algorithmic HBM bytes of a projection: weights once, the input rows, fp32 output rows.
 static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, int K, int S, int dt, float* part,
                          hipStream_t st) {
-  const int e = prof_begin(st);
-  adt_status r = launch_gemm(X, ldx, W, M, N, K, S, dt, part, st);
-  prof_end(e, ADT_PROF_GEMM, (double)N * K * esize(dt) + (double)M * K * esize(dt) + (double)M * N * 4.0,
-           2.0 * M * N * K, st);
+  const int e = prof_pair();
+  adt_status r = launch_gemm(X, ldx, W, M, N, K, S, dt, part, st, e >= 0 ? g_prof.ev[e] : nullptr,
+                             e >= 0 ? g_prof.ev[e + 1] : nullptr);
+  prof_done(e, ADT_PROF_GEMM, (double)N * K * esize(dt) + (double)M * K * esize(dt) + (double)M * N * 4.0,
+            2.0 * M * N * K);
   return r;
 }
 
@@ -544,19 +606,19 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   const int64_t stride_h = (int64_t)s->d.s_cap * Dh;
   const float eps = m->d.norm_eps;
   const float scale = 1.f / std::sqrt((float)Dh);
-  TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
+  (void)slot0;
   const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
   for (int l = l0; l < l1; ++l) {
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
     int S = gemm_splits(M, 3 * dm, dm, dt);
     TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
-    TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
     {
       // K1 + K1c: the prefix K/V once, tree Q/K/V in and O out, the masks.
       const int e = prof_begin(st);
+      TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
       TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M,
-                           L_pre + n_tail, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
+                           s->d.s_cap, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
       prof_end(e, ADT_PROF_ATTN, 2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es + 16.0 * M,
                4.0 * M * (L_pre + n_tail) * H * Dh, st);
     }
@@ -582,27 +644,36 @@ static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float*
 // Target forward of M rows with tokens tok; features into s->feat; logits of rows
 // [lm_row0, lm_row0 + lm_rows) into s->logits.
 static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, const int32_t* pos, int slot0, int L_pre,
-                                 int n_tail, const uint64_t* mask, int lm_row0, int lm_rows, hipStream_t st) {
-  TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, st));
-  TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, st));
-  if (lm_rows > 0)
-    TRY(lm_head(s, (const char*)s->feat + (size_t)lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits, st));
-  return ADT_OK;
+                                 int n_tail, const uint64_t* mask, int lm_row0, int lm_rows, hipStream_t st,
+                                 int64_t key = -1) {
+  TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
+  auto body = [&](hipStream_t cs) -> adt_status {
+    TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, cs));
+    TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
+    if (lm_rows > 0)
+      TRY(lm_head(s, (const char*)s->feat + (size_t)lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits, cs));
+    return ADT_OK;
+  };
+  return key < 0 ? body(st) : run_graph(s, key, st, body);
 }
 
 // Draft-head forward: FC over [embedding ; parent feature], one decoder layer, final norm
 // into feature rows fout (may be null), target LM head for rows [lm_row0, +lm_rows) into out.
 static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int32_t* fsrc, const void* fa, int M,
                                 const int32_t* pos, int slot0, int L_pre, int n_tail, const uint64_t* mask, void* fout,
-                                int lm_row0, int lm_rows, float* lout, hipStream_t st) {
+                                int lm_row0, int lm_rows, float* lout, hipStream_t st, int64_t key = -1) {
   const int dm = s->dm, dt = s->dt;
-  TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, st));
-  const int S = gemm_splits(M, dm, 2 * dm, dt);
-  TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, st));
-  TRY(launch_add_norm(s->part, S, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, st));
-  TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, st));
-  if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, st));
-  return ADT_OK;
+  TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
+  auto body = [&](hipStream_t cs) -> adt_status {
+    TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, cs));
+    const int S = gemm_splits(M, dm, 2 * dm, dt);
+    TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, cs));
+    TRY(launch_add_norm(s->part, S, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
+    TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, cs));
+    if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, cs));
+    return ADT_OK;
+  };
+  return key < 0 ? body(st) : run_graph(s, key, st, body);
 }
 
 static adt_status sync_stream(hipStream_t st) {
@@ -697,7 +768,7 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     TRY(launch_iota(s->cpos, cu, Ld, 1, st));
     TRY(launch_chain_masks(s->cmask, cu, st));
     TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
-                      s->dlogits, st));
+                      s->dlogits, st, gkey(2, 0, 0, cu)));
   }
   // layer 1: the root's top-k children
   int lo, hi;
@@ -717,7 +788,7 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
       TRY(launch_gather_rows(s->d.draft_table, s->idx, nf, V, lrows, ADT_F32, st));
     } else {
       TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1,
-                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, st));
+                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, st, gkey(3, lvl, nf, drow)));
     }
     cell_range(s, L + lvl - P, lo, hi);
     TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
@@ -766,7 +837,8 @@ extern "C" adt_status adt_session_set_tree(adt_session* s, const int32_t* parent
                        s->tr.score, st));
   TRY(sync_stream(st));
   s->n_nodes = n;
-  s->expanded = false;
+  // s->expanded is kept: after adt_tree_expand the draft cache covers the root whichever tree
+  // is verified next, and the node rows past it are rewritten by the next catch-up.
   return ADT_OK;
 }
 
@@ -775,7 +847,8 @@ extern "C" adt_status adt_verify_forward(adt_session* s, void* stream) {
   ADT_CHECK_ARG(s->prefilled && s->n_nodes >= 1, ADT_E_STATE, "verify: no tree");
   ADT_CHECK_ARG(s->L + s->n_nodes <= s->d.s_cap, ADT_E_CAPACITY, "verify: cache capacity");
   const int n = s->n_nodes;
-  return target_forward(s, s->tr.token, n, s->tr.pos, s->L, s->L, n, s->tr.mask, 0, n, (hipStream_t)stream);
+  return target_forward(s, s->tr.token, n, s->tr.pos, s->L, s->L, n, s->tr.mask, 0, n, (hipStream_t)stream,
+                        gkey(1, 0, 0, n));
 }
 
 extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_hat, adt_step_out* out,
@@ -900,5 +973,9 @@ extern "C" adt_status adt_session_get_view(const adt_session* s, adt_session_vie
   v->n_acc = s->tr.nacc;
   v->bonus = s->tr.bonus;
   v->tokens_host = s->tokens.data();
+  v->q = s->q;
+  v->att = s->att;
+  v->act = s->act;
+  v->resid = s->h;
   return ADT_OK;
 }

@@ -7,12 +7,15 @@
 //   S^T[key][q] = K[key][:] . Q[q][:]        (A = K rows, B = Q^T)
 //   O^T[d][q]  += V^T[d][key] . P^T[key][q]  (A = V^T rows, B = P^T)
 // so each lane owns one query column and the online-softmax rescale is a per-lane scalar.
+// Probabilities enter the second product as three bf16 parts (three MFMAs), so the result
+// is as accurate as fp32 accumulation of the bf16 inputs.
 // Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
 #include "../launch.h"
 
 namespace adt {
 
 constexpr int ATT_KT = 64;      // keys per LDS tile
+constexpr int ATT_MAX_SPLITS = 64;
 constexpr int ATT_THREADS = 256;
 
 __device__ __forceinline__ bool tail_visible(uint64_t w0, uint64_t w1, int j) {
@@ -78,21 +81,38 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
     }
   }
 
-  for (int kb = k_begin; kb < k_end; kb += ATT_KT) {
-    __syncthreads();
-    for (int p = tid; p < ATT_KT * DH / 8; p += ATT_THREADS) {
+  // Each thread moves PP pieces (16 bytes of K and of V) per tile.  The next tile's pieces
+  // are loaded into registers before the current tile is computed, so HBM latency overlaps
+  // the MFMA work.
+  constexpr int PP = ATT_KT * DH / 8 / ATT_THREADS;
+  u16x8 kn[PP], vn[PP];
+  auto load_tile = [&](int kb) {
+#pragma unroll
+    for (int j = 0; j < PP; ++j) {
+      const int p = tid + j * ATT_THREADS;
       const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
       const int key = kb + r;
-      u16x8 kv = u16x8{0, 0, 0, 0, 0, 0, 0, 0}, vv = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      kn[j] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      vn[j] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
       if (key < k_end) {
-        kv = *reinterpret_cast<const u16x8*>(kbase + (int64_t)key * DH + c);
-        vv = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + c);
+        kn[j] = *reinterpret_cast<const u16x8*>(kbase + (int64_t)key * DH + c);
+        vn[j] = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + c);
       }
-      *reinterpret_cast<u16x8*>(&Ks[r][c]) = kv;
+    }
+  };
+  if (k_begin < k_end) load_tile(k_begin);
+  for (int kb = k_begin; kb < k_end; kb += ATT_KT) {
+    __syncthreads();
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vv[e];
+    for (int j = 0; j < PP; ++j) {
+      const int p = tid + j * ATT_THREADS;
+      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
+      *reinterpret_cast<u16x8*>(&Ks[r][c]) = kn[j];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vn[j][e];
     }
     __syncthreads();
+    if (kb + ATT_KT < k_end) load_tile(kb + ATT_KT);
 
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
@@ -143,18 +163,27 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
       for (int d = 0; d < DT; ++d) o[i][d] *= alpha;
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
-        bf16x8 pb;
+        // P = P1 + P2 + P3, each part in bf16 (three MFMAs): the probabilities enter the
+        // product with about 24 bits, so it is as accurate as fp32 accumulation.
+        bf16x8 p1, p2, p3;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          pb[r] = __builtin_bit_cast(__bf16, f2bf(st[2 * h2][r]));
-          pb[4 + r] = __builtin_bit_cast(__bf16, f2bf(st[2 * h2 + 1][r]));
+        for (int r = 0; r < 8; ++r) {
+          const float pv = r < 4 ? st[2 * h2][r] : st[2 * h2 + 1][r - 4];
+          const uint16_t b1 = f2bf(pv);
+          const float r1 = pv - bf2f(b1);
+          const uint16_t b2 = f2bf(r1);
+          p1[r] = __builtin_bit_cast(__bf16, b1);
+          p2[r] = __builtin_bit_cast(__bf16, b2);
+          p3[r] = __builtin_bit_cast(__bf16, f2bf(r1 - bf2f(b2)));
         }
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
           const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 4 * g]);
           const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 16 + 4 * g]);
           const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[i][d], 0, 0, 0);
+          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[i][d], 0, 0, 0);
+          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p2, o[i][d], 0, 0, 0);
+          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p3, o[i][d], 0, 0, 0);
         }
       }
     }
@@ -182,25 +211,48 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
 }
 
 // Log-sum-exp merge of the split partials; one block of DH threads per (query, head, seq).
+// Every split's (m, l) is loaded at once (one lane per split), then the weighted sum of
+// the O partials is taken in split order.
 template <typename OutT>
 __global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const float* __restrict__ part_ml,
                                          const int32_t* __restrict__ n_q, int H, int nq_max, int splits, int DH,
                                          OutT* __restrict__ out) {
+  __shared__ float wsh[ATT_MAX_SPLITS];
+  __shared__ float red[4];
   const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
   if (qr >= min(n_q[b], nq_max)) return;
   const int64_t base = (((int64_t)b * H + h) * splits) * nq_max;
-  float M = -INFINITY;
-  for (int s = 0; s < splits; ++s) M = fmaxf(M, part_ml[(base + (int64_t)s * nq_max + qr) * 2]);
-  float lsum = 0.f, acc = 0.f;
-  for (int s = 0; s < splits; ++s) {
-    const int64_t row = base + (int64_t)s * nq_max + qr;
-    const float m = part_ml[row * 2];
-    if (m == -INFINITY) continue;
-    const float w = exp2f(m - M);
-    lsum += w * part_ml[row * 2 + 1];
-    acc += w * part_o[row * DH + d];
+  float m = -INFINITY, l = 0.f;
+  if (d < splits) {
+    m = part_ml[(base + (int64_t)d * nq_max + qr) * 2];
+    l = part_ml[(base + (int64_t)d * nq_max + qr) * 2 + 1];
   }
-  Elem<OutT>::store(out, (((int64_t)b * nq_max + qr) * H + h) * DH + d, lsum > 0.f ? acc / lsum : 0.f);
+  float M = wave_max(m);
+  const int nw = (int)(blockDim.x + WAVE - 1) / WAVE;
+  if (nw > 1) {
+    if (d % WAVE == 0) red[d / WAVE] = M;
+    __syncthreads();
+    M = red[0];
+    for (int i = 1; i < nw; ++i) M = fmaxf(M, red[i]);
+    __syncthreads();
+  }
+  const float w = (m == -INFINITY) ? 0.f : exp2f(m - M);
+  if (d < splits) wsh[d] = w;
+  float ls = wave_sum(w * l);
+  if (nw > 1) {
+    if (d % WAVE == 0) red[d / WAVE] = ls;
+    __syncthreads();
+    ls = 0.f;
+    for (int i = 0; i < nw; ++i) ls += red[i];
+  }
+  __syncthreads();
+  float acc = 0.f;
+#pragma unroll 8
+  for (int s = 0; s < splits; ++s) {
+    const float ws = wsh[s];
+    if (ws != 0.f) acc += ws * part_o[(base + (int64_t)s * nq_max + qr) * DH + d];
+  }
+  Elem<OutT>::store(out, (((int64_t)b * nq_max + qr) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
 }
 
 // fp32 path: one block per (query, head, sequence); scores staged in LDS.
@@ -262,9 +314,10 @@ struct AttnPlan {
 };
 
 static AttnPlan attn_plan(int B, int H, int kv_cap) {
-  // Aim for about two workgroups per CU (256 CUs); at least 128 keys per split.
-  const int want = (512 + B * H - 1) / (B * H);
-  const int max_splits = (kv_cap + 127) / 128;
+  // Aim for about four workgroups per CU (256 CUs); at least two 64-key tiles per split.
+  int want = (1024 + B * H - 1) / (B * H);
+  if (want > ATT_MAX_SPLITS) want = ATT_MAX_SPLITS;
+  const int max_splits = (kv_cap + 2 * ATT_KT - 1) / (2 * ATT_KT);
   int splits = want < 1 ? 1 : want;
   if (splits > max_splits) splits = max_splits;
   if (splits < 1) splits = 1;
@@ -274,12 +327,45 @@ static AttnPlan attn_plan(int B, int H, int kv_cap) {
   return {splits, chunk};
 }
 
-// Upper bound over every kv_cap: a plan never uses more than ceil(512 / (B*H)) splits.
+// Upper bound over every kv_cap: a plan never uses more than ceil(1024 / (B*H)) splits.
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
   (void)kv_cap;
   if (dtype == ADT_F32) return 0;
-  const int max_splits = (512 + B * H - 1) / (B * H);
+  int max_splits = (1024 + B * H - 1) / (B * H);
+  if (max_splits > ATT_MAX_SPLITS) max_splits = ATT_MAX_SPLITS;
   return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
+}
+
+static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
+                            int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+  const AttnPlan p = attn_plan(B, H, kv_cap);
+  const size_t need = (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
+  ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
+                need);
+  float* part_o = (float*)ws;
+  float* part_ml = part_o + (size_t)B * H * p.splits * nq_max * Dh;
+  dim3 grid(p.splits, H, B);
+  const float sl2 = scale * LOG2E;
+#define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
+  tree_attn_bf16_kernel<DHV, TPWV><<<grid, ATT_THREADS, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
+                                                                 (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail, \
+                                                                 mask, H, nq_max, kv_cap, p.chunk, p.splits, sl2, \
+                                                                 part_o, part_ml)
+  if (Dh == 128) {
+    if (nq_max > 64) ADT_ATTN_LAUNCH(128, 2);
+    else ADT_ATTN_LAUNCH(128, 1);
+  } else {
+    if (nq_max > 64) ADT_ATTN_LAUNCH(64, 2);
+    else ADT_ATTN_LAUNCH(64, 1);
+  }
+#undef ADT_ATTN_LAUNCH
+  ADT_LAUNCH_CHECK();
+  dim3 g2(nq_max, H, B);
+  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, H, nq_max, p.splits, Dh,
+                                                         (uint16_t*)out);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
 }
 
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
@@ -295,34 +381,7 @@ adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t
     ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
-  const AttnPlan p = attn_plan(B, H, kv_cap);
-  const size_t need = (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
-  ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
-                need);
-  float* part_o = (float*)ws;
-  float* part_ml = part_o + (size_t)B * H * p.splits * nq_max * Dh;
-  dim3 grid(p.splits, H, B);
-  const float sl2 = scale * LOG2E;
-#define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
-  tree_attn_bf16_kernel<DHV, TPWV><<<grid, ATT_THREADS, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,            \
-                                                                 (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,    \
-                                                                 mask, H, nq_max, kv_cap, p.chunk, p.splits, sl2,    \
-                                                                 part_o, part_ml)
-  const bool wide = nq_max > 64;
-  if (Dh == 128) {
-    if (wide) ADT_ATTN_LAUNCH(128, 2);
-    else ADT_ATTN_LAUNCH(128, 1);
-  } else {
-    if (wide) ADT_ATTN_LAUNCH(64, 2);
-    else ADT_ATTN_LAUNCH(64, 1);
-  }
-#undef ADT_ATTN_LAUNCH
-  ADT_LAUNCH_CHECK();
-  dim3 g2(nq_max, H, B);
-  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, H, nq_max, p.splits, Dh,
-                                                         (uint16_t*)out);
-  ADT_LAUNCH_CHECK();
-  return ADT_OK;
+  return attn_bf16(q, k, v, sb, sh, kv_len, n_q, n_tail, mask, B, H, Dh, nq_max, kv_cap, scale, out, ws, ws_bytes, st);
 }
 
 }  // namespace adt

@@ -8,6 +8,8 @@
 // hundreds of workgroups in flight; each split writes fp32 partials [split][M][N] that the
 // consuming kernel (residual add + norm, RoPE + cache append, SwiGLU, logits) sums in a
 // fixed order, which keeps results deterministic.
+#include <hip/hip_ext.h>
+
 #include "../launch.h"
 
 namespace adt {
@@ -66,7 +68,19 @@ __global__ void pack_f32_kernel(PackSrc s, int N, int K, float* __restrict__ dst
 // ----------------------------------------------------------------------------- bf16 MFMA
 constexpr int GEMM_THREADS = 256;
 
+// lane (lq, g) holds Y[m = mt*16 + lq][n = nt*16 + 4g + r], r = 0..3: one 16-byte store per row.
+template <int MT>
+__device__ __forceinline__ void store_partials(const f32x4 (&acc)[MT], float* __restrict__ part, int s, int M, int N,
+                                               int nt, int lq, int g) {
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int row = m * 16 + lq;
+    if (row < M) *reinterpret_cast<f32x4*>(part + ((int64_t)s * M + row) * N + nt * 16 + 4 * g) = acc[m];
+  }
+}
+
 // MT = 16-row tiles of M; KC = k-tiles (of 32) staged per LDS round (LDS stays < 64 KB).
+// X chunks are staged in LDS and shared by the workgroup's four waves (one n-tile each).
 template <int MT, int KC = (MT > 6 ? 4 : 8)>
 __global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_kernel(const uint16_t* __restrict__ X, int ldx,
                                                                  const uint16_t* __restrict__ Wp, int M, int N,
@@ -117,13 +131,51 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_kernel(const uint16_t*
       }
     }
   }
-  if (!active) return;
-  // lane (lq, g) holds Y[m = mt*16 + lq][n = nt*16 + 4g + r]
+  if (active) store_partials<MT>(acc, part, s, M, N, nt, lq, g);
+}
+
+// Few tree rows (M <= 32): each wave reads its X fragments straight from global memory (the
+// rows are a few KB and L2-resident), so weights and inputs of a whole chunk are in flight
+// together and no workgroup barrier is needed.
+template <int MT, int KC = 8>
+__global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_direct_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                                        const uint16_t* __restrict__ Wp, int M,
+                                                                        int N, int K, int splits,
+                                                                        float* __restrict__ part) {
+  const int NT = N / 16, KT = K / 32;
+  const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
+  const int nt = blockIdx.x * 4 + threadIdx.x / WAVE;
+  const int s = blockIdx.y;
+  if (nt >= NT) return;
+  const int kt0 = (int)((int64_t)KT * s / splits), kt1 = (int)((int64_t)KT * (s + 1) / splits);
+  f32x4 acc[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    const int row = m * 16 + lq;
-    if (row < M) *reinterpret_cast<f32x4*>(part + ((int64_t)s * M + row) * N + nt * 16 + 4 * g) = acc[m];
+  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8* wp = reinterpret_cast<const bf16x8*>(Wp) + ((int64_t)nt * KT) * 64 + lane;
+  for (int c = kt0; c < kt1; c += KC) {
+    const int nk = min(KC, kt1 - c);
+    bf16x8 wf[KC], xf[KC][MT];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+      wf[j] = bf16x8{};
+#pragma unroll
+      for (int m = 0; m < MT; ++m) xf[j][m] = bf16x8{};
+      if (j < nk) {
+        wf[j] = wp[(int64_t)(c + j) * 64];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const int row = m * 16 + lq;
+          if (row < M) xf[j][m] = *reinterpret_cast<const bf16x8*>(X + (int64_t)row * ldx + (c + j) * 32 + g * 8);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+      if (j < nk)
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], xf[j][m], acc[m], 0, 0, 0);
   }
+  store_partials<MT>(acc, part, s, M, N, nt, lq, g);
 }
 
 // ----------------------------------------------------------------------------- fp32 (vector)
@@ -183,39 +235,46 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
   return ADT_OK;
 }
 
+// Split-K factor: enough workgroups to keep HBM busy (about two per CU) but at least
+// eight k-tiles (8 KB of weights per wave) per split, since the consumers sum the splits.
 int gemm_splits(int M, int N, int K, int dtype) {
   if (dtype == ADT_F32) return 1;
   const int NB = (N / 16 + 3) / 4;
   const int KT = K / 32;
-  int s = (512 + NB - 1) / NB;        // about two workgroups per CU
-  if (s > KT / 2) s = KT / 2;         // keep >= 2 k-tiles per split
+  int s = (512 + NB - 1) / NB;
+  if (s > KT / 8) s = KT / 8;
   if (s < 1) s = 1;
   (void)M;
   return s;
 }
 
+// With ev0/ev1 set, the dispatch itself records the events at the kernel's start and end
+// (kernel duration, not host-side markers).
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int splits, int dtype, float* part,
-                       hipStream_t st) {
+                       hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   ADT_CHECK_ARG(M >= 1 && M <= 128, ADT_E_CAPACITY, "gemm: M=%d outside [1,128]", M);
   if (dtype == ADT_F32) {
-    gemm_f32_kernel<<<(N + 3) / 4, 256, 0, st>>>((const float*)X, ldx, (const float*)Wp, M, N, K, part);
+    hipExtLaunchKernelGGL(gemm_f32_kernel, dim3((N + 3) / 4), dim3(256), 0, st, ev0, ev1, 0, (const float*)X, ldx,
+                          (const float*)Wp, M, N, K, part);
     ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
   ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0 && ldx % 8 == 0, ADT_E_SHAPE, "gemm: N=%d K=%d ldx=%d misaligned", N, K, ldx);
-  dim3 grid((N / 16 + 3) / 4, splits);
+  const dim3 grid((N / 16 + 3) / 4, splits), block(GEMM_THREADS);
   const int mt = (M + 15) / 16;
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)Wp;
+#define ADT_GEMM(KERNEL) hipExtLaunchKernelGGL(KERNEL, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, splits, part)
   switch (mt) {
-    case 1: gemm_bf16_kernel<1><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
-    case 2: gemm_bf16_kernel<2><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
-    case 3: gemm_bf16_kernel<3><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
-    case 4: gemm_bf16_kernel<4><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
+    case 1: ADT_GEMM(gemm_bf16_direct_kernel<1>); break;
+    case 2: ADT_GEMM(gemm_bf16_direct_kernel<2>); break;
+    case 3: ADT_GEMM(gemm_bf16_kernel<3>); break;
+    case 4: ADT_GEMM(gemm_bf16_kernel<4>); break;
     case 5:
-    case 6: gemm_bf16_kernel<6><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
-    default: gemm_bf16_kernel<8><<<grid, GEMM_THREADS, 0, st>>>(x, ldx, w, M, N, K, splits, part); break;
+    case 6: ADT_GEMM(gemm_bf16_kernel<6>); break;
+    default: ADT_GEMM(gemm_bf16_kernel<8>); break;
   }
+#undef ADT_GEMM
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -46,10 +46,24 @@ __global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __res
 }
 
 // Sum of the split-K partials of four consecutive columns.
+// Summed in split order so results do not depend on the launch shape; loads are issued
+// eight at a time.
 __device__ __forceinline__ float4 sum_parts4(const float* __restrict__ part, int splits, int64_t stride, int64_t off) {
   float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 4
-  for (int s = 0; s < splits; ++s) {
+  int s = 0;
+  for (; s + 8 <= splits; s += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const float4*>(part + (s + j) * stride + off);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      y.x += v[j].x;
+      y.y += v[j].y;
+      y.z += v[j].z;
+      y.w += v[j].w;
+    }
+  }
+  for (; s < splits; ++s) {
     const float4 v = *reinterpret_cast<const float4*>(part + s * stride + off);
     y.x += v.x;
     y.y += v.y;
@@ -284,7 +298,8 @@ adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* 
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
                            int dtype, hipStream_t st) {
   ADT_CHECK_ARG(d % 4 == 0 && d <= 16 * 1024, ADT_E_SHAPE, "add_norm: d=%d", d);
-  int threads = ((d / 4 + 3) / 4 + 63) / 64 * 64;
+  int threads = (d / 4 + 63) / 64 * 64;   // one float4 column group per thread when d <= 4096
+  if (threads > 1024) threads = 1024;
   if (threads < 64) threads = 64;
   ADT_DISPATCH_T(dtype, add_norm_kernel<T><<<M, threads, 0, st>>>(part, splits, M, d, assign, eps, h, (T*)a));
   ADT_LAUNCH_CHECK();

@@ -35,10 +35,11 @@ __device__ __forceinline__ void wave_best(float& v, int& id, int& lane) {
   }
 }
 
-// Per row: top-k ids by (logit desc, id asc) over [lo, hi) and the log-sum-exp.  Each thread
-// keeps a sorted private list over a strided slice; each wave merges its 64 lists with k
-// rounds of shuffle argmax; wave 0 merges the per-wave lists the same way.
-template <int KMAX>
+// Per row: top-k ids by (logit desc, id asc) over [lo, hi) and the log-sum-exp.  The
+// thread's slice of the row (float4 j*4*T + 4*tid + {0..3}) is loaded into registers in one
+// go, so the loads overlap; then each wave takes k rounds of "best remaining element of
+// each lane" + shuffle argmax, and wave 0 merges the per-wave lists the same way.
+template <int KMAX, int E4>
 __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __restrict__ logits, int64_t ld, int V,
                                                                 const int32_t* __restrict__ allowed, int k,
                                                                 int32_t* __restrict__ top_id,
@@ -49,63 +50,73 @@ __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __r
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
   const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
   const float* x = logits + (int64_t)row * ld;
-
-  float v[KMAX];
-  int id[KMAX];
+  const bool vec = ((ld & 3) == 0);
+  float r[E4 * 4];
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
-    v[j] = -INFINITY;
-    id[j] = 0x7FFFFFFF;
-  }
-  float m = -INFINITY, s = 0.f;
-  for (int i = lo + tid; i < hi; i += TOPK_THREADS) {
-    const float xi = x[i];
-    if (xi > m) {
-      s = s * expf(m - xi) + 1.f;
-      m = xi;
+  for (int j = 0; j < E4; ++j) {
+    const int base = j * 4 * TOPK_THREADS + 4 * tid;
+    if (vec && base + 3 < V) {
+      const float4 q = *reinterpret_cast<const float4*>(x + base);
+      r[4 * j] = q.x;
+      r[4 * j + 1] = q.y;
+      r[4 * j + 2] = q.z;
+      r[4 * j + 3] = q.w;
     } else {
-      s += expf(xi - m);
-    }
-    if (better(xi, i, v[KMAX - 1], id[KMAX - 1])) {
-      v[KMAX - 1] = xi;
-      id[KMAX - 1] = i;
 #pragma unroll
-      for (int j = KMAX - 1; j > 0; --j) {
-        if (better(v[j], id[j], v[j - 1], id[j - 1])) {
-          const float tv = v[j];
-          v[j] = v[j - 1];
-          v[j - 1] = tv;
-          const int ti = id[j];
-          id[j] = id[j - 1];
-          id[j - 1] = ti;
-        }
-      }
+      for (int e = 0; e < 4; ++e) r[4 * j + e] = (base + e < V) ? x[base + e] : -INFINITY;
     }
   }
+  // mask to the allowed range
+#pragma unroll
+  for (int j = 0; j < E4; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = j * 4 * TOPK_THREADS + 4 * tid + e;
+      if (i < lo || i >= hi) r[4 * j + e] = -INFINITY;
+    }
+  // log-sum-exp
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < E4 * 4; ++j) m = fmaxf(m, r[j]);
   const float M = wave_max(m);
-  const float S = wave_sum(m == -INFINITY ? 0.f : s * expf(m - M));
+  float sacc = 0.f;
+  if (M != -INFINITY) {
+#pragma unroll
+    for (int j = 0; j < E4 * 4; ++j) sacc += (r[j] == -INFINITY) ? 0.f : expf(r[j] - M);
+  }
+  const float S = wave_sum(sacc);
   if (lane == 0) {
     smx[wave] = M;
     ssum[wave] = S;
   }
   const int kk = min(k, hi - lo);
-  // wave-level merge of the private lists
-  int head = 0;
-  for (int r = 0; r < kk; ++r) {
-    float hv = -INFINITY;
-    int hid = 0x7FFFFFFF;
+  // wave-level selection
+  for (int q = 0; q < kk; ++q) {
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
 #pragma unroll
-    for (int j = 0; j < KMAX; ++j)
-      if (j == head) {
-        hv = v[j];
-        hid = id[j];
+    for (int j = 0; j < E4 * 4; ++j) {
+      const int i = (j / 4) * 4 * TOPK_THREADS + 4 * tid + (j % 4);
+      if (better(r[j], i, bv, bi)) {
+        bv = r[j];
+        bi = i;
       }
+    }
+    if (bv == -INFINITY) bi = 0x7FFFFFFF;
     int bl = lane;
-    wave_best(hv, hid, bl);
-    if (lane == bl) ++head;
+    float wvv = bv;
+    int wii = bi;
+    wave_best(wvv, wii, bl);
+    if (lane == bl && wii != 0x7FFFFFFF) {
+#pragma unroll
+      for (int j = 0; j < E4 * 4; ++j) {
+        const int i = (j / 4) * 4 * TOPK_THREADS + 4 * tid + (j % 4);
+        if (i == wii) r[j] = -INFINITY;
+      }
+    }
     if (lane == 0) {
-      wv[wave][r] = hv;
-      wi[wave][r] = hid;
+      wv[wave][q] = wvv;
+      wi[wave][q] = wii;
     }
   }
   __syncthreads();
@@ -118,9 +129,8 @@ __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __r
       if (smx[w] != -INFINITY) gs += ssum[w] * expf(smx[w] - gm);
     lse[row] = gm + logf(gs);
   }
-  // block-level merge: lane w (< TOPK_WAVES) walks wave w's sorted list
   int h2 = 0;
-  for (int r = 0; r < kk; ++r) {
+  for (int q = 0; q < kk; ++q) {
     float hv = -INFINITY;
     int hid = 0x7FFFFFFF;
     if (lane < TOPK_WAVES && h2 < kk) {
@@ -131,8 +141,8 @@ __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __r
     wave_best(hv, hid, bl);
     if (lane == bl) ++h2;
     if (lane == 0) {
-      top_id[row * KMAX + r] = hid;
-      top_val[row * KMAX + r] = hv;
+      top_id[row * KMAX + q] = hid;
+      top_val[row * KMAX + q] = hv;
     }
   }
 }
@@ -305,10 +315,23 @@ __global__ void accept_greedy_kernel(const int32_t* __restrict__ argmax, int kma
 adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
                            int32_t* top_id, float* top_val, float* lse, hipStream_t st) {
   ADT_CHECK_ARG(k >= 1 && k <= kmax && (kmax == 1 || kmax == 16), ADT_E_UNSUPPORTED, "row_topk: k=%d kmax=%d", k, kmax);
-  if (kmax == 1)
-    row_topk_kernel<1><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
-  else
-    row_topk_kernel<16><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse);
+  const int e4 = (V + 4 * TOPK_THREADS - 1) / (4 * TOPK_THREADS);
+  ADT_CHECK_ARG(e4 <= 16, ADT_E_UNSUPPORTED, "row_topk: vocab %d above 65536", V);
+#define ADT_TOPK(KM, E)                                                                                        \
+  row_topk_kernel<KM, E><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse)
+#define ADT_TOPK_E(KM)            \
+  if (e4 <= 1) ADT_TOPK(KM, 1);   \
+  else if (e4 <= 2) ADT_TOPK(KM, 2); \
+  else if (e4 <= 4) ADT_TOPK(KM, 4); \
+  else if (e4 <= 8) ADT_TOPK(KM, 8); \
+  else ADT_TOPK(KM, 16)
+  if (kmax == 1) {
+    ADT_TOPK_E(1);
+  } else {
+    ADT_TOPK_E(16);
+  }
+#undef ADT_TOPK_E
+#undef ADT_TOPK
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

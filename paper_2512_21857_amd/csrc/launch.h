@@ -18,7 +18,7 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
                        hipStream_t st);
 int gemm_splits(int M, int N, int K, int dtype);
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int splits, int dtype, float* part,
-                       hipStream_t st);
+                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // rows.hip
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
@@ -90,5 +90,10 @@ adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const in
                                 const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
                                 uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
                                 hipStream_t st);
+
+// knn.hip
+size_t knn_ws_bytes(int n);
+adt_status launch_codebook_knn(const float* cb, int n, int dim, int k, int32_t* out, void* ws, size_t ws_bytes,
+                               hipStream_t st);
 
 }  // namespace adt

@@ -103,6 +103,16 @@ def verify_accept(logits: torch.Tensor, parent: torch.Tensor, token: torch.Tenso
     return path, n_acc, bonus
 
 
+def codebook_knn(codebook: torch.Tensor, k: int) -> torch.Tensor:
+    """codebook fp32 [n][dim] -> int32 [n][k]: each code, then its k-1 most cosine-similar codes."""
+    _require_cuda(codebook)
+    n, dim = codebook.shape
+    out = torch.empty(n, k, dtype=torch.int32, device=codebook.device)
+    ws = torch.empty(lib().adt_codebook_knn_workspace_size(n), dtype=torch.uint8, device=codebook.device)
+    check(lib().adt_codebook_knn(_p(codebook), n, dim, k, _p(out), _p(ws), ws.numel(), _stream()))
+    return out
+
+
 def schedule_next(sched: abi.SchedCfg, left, prev, remaining: int):
     """Host-only schedule: left = (d, k) or None, prev = (a, d) or None."""
     d = C.c_int32()
@@ -176,7 +186,8 @@ class DeviceSession:
 
     def __init__(self, model: DeviceModel, cfg, poisson: Optional[np.ndarray] = None,
                  knn: Optional[torch.Tensor] = None, accept_seed: Optional[int] = None, fixed_tree: bool = False,
-                 accept_mode: Optional[str] = None, draft_table: Optional[torch.Tensor] = None):
+                 accept_mode: Optional[str] = None, draft_table: Optional[torch.Tensor] = None,
+                 use_graphs: bool = True):
         m = cfg.model
         self.model = model
         self.cfg = cfg
@@ -202,7 +213,7 @@ class DeviceSession:
                                C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched), self.accept,
                                C.cast(self._poisson, C.POINTER(C.c_int32)) if self._poisson is not None else None,
                                1 if fixed_tree else 0, _p(draft_table),
-                               0 if draft_table is None else draft_table.shape[0], None, 0)
+                               0 if draft_table is None else draft_table.shape[0], 1 if use_graphs else 0, None, 0)
         self.draft_table = draft_table
         need = lib().adt_session_workspace_size(model.handle, C.byref(desc))
         if need == 0:

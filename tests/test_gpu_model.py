@@ -214,12 +214,14 @@ def test_planted_path_bf16_small(rt):
     _planted(rt, _small_bf16(), 5, extra_rng=9)
 
 
-def test_determinism(rt):
+@pytest.mark.parametrize("graphs", [(True, True), (True, False)])
+def test_determinism(rt, graphs):
+    """Two runs are bitwise identical; so are the graph-replayed and the plainly launched path."""
     cfg = _small_bf16()
     outs = []
-    for _ in range(2):
+    for g in graphs:
         _, _, dm, pre = _setup(rt, cfg)
-        sess = rt.DeviceSession(dm, cfg, fixed_tree=True)
+        sess = rt.DeviceSession(dm, cfg, fixed_tree=True, use_graphs=g)
         sess.prefill(pre)
         toks = [sess.step()["tokens"] for _ in range(4)]
         outs.append((toks, sess.tensors()["logits"].cpu().numpy().copy()))

@@ -170,3 +170,14 @@ def test_relaxed_single_candidate_total_variation():
     nz = law > 0
     chi2 = float(np.sum((counts[nz] - trials * law[nz]) ** 2 / (trials * law[nz])))
     assert chi2 < 30.0
+
+
+def test_codebook_knn_by_angle():
+    """Unit vectors at known angles on a circle: cosine order is angular distance."""
+    theta = np.array([0.0, 0.1, 0.35, 1.0, 2.0, -0.05, 3.1])
+    cb = np.stack([np.cos(theta), np.sin(theta)], axis=1) * np.array([[1.0], [2.0], [0.5], [3.0], [1.0], [1.5], [1.0]])
+    knn = acc.codebook_knn(cb, 4)
+    for x in range(len(theta)):
+        d = np.abs((theta - theta[x] + np.pi) % (2 * np.pi) - np.pi)
+        d[x] = np.inf
+        assert knn[x, 0] == x and list(knn[x, 1:]) == list(np.argsort(d, kind="stable")[:3])
