@@ -152,14 +152,23 @@ adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t dim, int32
 
 /* ------------------------------------------------------------------ weights
  * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM
- * kernels stream.  srcs/rows: [host] arrays of n_src device pointers and their row counts;
- * the sources are stacked in order (mode 0) or, for a gate/up pair (mode 1, n_src = 2,
- * equal rows), interleaved in blocks of 16 rows (gate block t, up block t, ...).
- * bf16: rows and K multiples of 16 and 32; dst holds sum(rows)*K bf16.  f32: same order,
- * row-major.  adt_packed_bytes() gives the size. */
+ * kernels stream.  srcs/rows: [host] arrays of n_src device pointers and their row counts.
+ * Row order of the packed matrix:
+ *   ADT_PACK_STACK    the sources stacked in order (lm_head, draft FC, O, down; the fp32 QKV);
+ *   ADT_PACK_GATE_UP  n_src = 2 equal sources (gate, up) interleaved in blocks of 8 rows:
+ *                     gate rows 8t..8t+7, then up rows 8t..8t+7, t = 0, 1, ... (both dtypes);
+ *   ADT_PACK_QKV      the sources (q, k, v) stacked; inside every head of `group` rows
+ *                     (= head_dim, a multiple of 16) each 16-row block u holds rows 8u..8u+7
+ *                     of the head's first half then the same rows of its second half, so a
+ *                     RoPE pair (j, j + head_dim/2) lands in one block (bf16 QKV weights).
+ * group is ignored by the other modes.  bf16: rows and K multiples of 16 and 32, stored as
+ * 16x32 tiles; dst holds sum(rows)*K bf16.  f32: the same row order, row-major.
+ * adt_packed_bytes() gives the size.  ADT_E_ARG on a bad mode, ADT_E_SHAPE on shapes the
+ * mode cannot tile. */
+enum { ADT_PACK_STACK = 0, ADT_PACK_GATE_UP = 1, ADT_PACK_QKV = 2 };
 size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype);
 adt_status adt_pack_weight(const void* const* srcs, const int32_t* rows, int32_t n_src, int32_t K, int32_t mode,
-                           int32_t dtype, void* dst, void* stream);
+                           int32_t group, int32_t dtype, void* dst, void* stream);
 
 /* ------------------------------------------------------------------ a0: schedule (host)
  * Adjacent initialisation (Sec. 4.1, Horizontal Repeat) + bisectional adaptation
@@ -192,9 +201,10 @@ typedef struct {
   const void* embed;            /* [vocab][d_model] row-major, dtype */
   const void* lm_head;          /* packed [vocab][d_model] */
   const void* draft_fc;         /* packed [d_model][2 d_model] (input = [embedding ; parent feature]) */
-  const void* const* w_qkv;     /* [host] n_layers + 1 packed [3d][d] (rows q, k, v); last = draft layer */
+  const void* const* w_qkv;     /* [host] n_layers + 1 packed [3d][d] (q, k, v): ADT_PACK_QKV with group =
+                                   head_dim for bf16, ADT_PACK_STACK for f32; last = draft layer */
   const void* const* w_o;       /* [host] n_layers + 1 packed [d][d] */
-  const void* const* w_gu;      /* [host] n_layers + 1 packed gate/up interleaved (mode 1) [2F][d] */
+  const void* const* w_gu;      /* [host] n_layers + 1 packed [2F][d], ADT_PACK_GATE_UP */
   const void* const* w_down;    /* [host] n_layers + 1 packed [d][F] */
 } adt_model_desc;
 

@@ -18,6 +18,7 @@ F32, BF16 = 0, 1
 MAX_NODES = 128
 MASK_WORDS = 2
 ACCEPT_GREEDY, ACCEPT_EXACT, ACCEPT_RELAXED = 0, 1, 2
+PACK_STACK, PACK_GATE_UP, PACK_QKV = 0, 1, 2
 ALPHA_REAL, ALPHA_POISSON = 0, 1
 
 p = C.c_void_p
@@ -77,7 +78,7 @@ _SIGS = {
     "adt_codebook_knn_workspace_size": (sz, [i32]),
     "adt_codebook_knn": (i32, [p, i32, i32, i32, p, p, sz, p]),
     "adt_packed_bytes": (sz, [i32, i32, i32]),
-    "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, p, p]),
+    "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, i32, p, p]),
     "adt_schedule_next": (i32, [C.POINTER(SchedCfg), i32, i32, i32, i32, i32, i32, i32, ip, ip]),
     "adt_model_create": (i32, [C.POINTER(ModelDesc), C.POINTER(p)]),
     "adt_model_destroy": (None, [p]),

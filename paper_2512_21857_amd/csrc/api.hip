@@ -249,9 +249,9 @@ extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype)
 }
 
 extern "C" adt_status adt_pack_weight(const void* const* srcs, const int32_t* rows, int32_t n_src, int32_t K,
-                                      int32_t mode, int32_t dtype, void* dst, void* stream) {
+                                      int32_t mode, int32_t group, int32_t dtype, void* dst, void* stream) {
   ADT_CHECK_ARG(valid_dtype(dtype) && K >= 1, ADT_E_ARG, "pack: dtype/K");
-  return launch_pack(srcs, rows, n_src, K, mode, dtype, dst, (hipStream_t)stream);
+  return launch_pack(srcs, rows, n_src, K, mode, group, dtype, dst, (hipStream_t)stream);
 }
 
 extern "C" adt_status adt_schedule_next(const adt_sched_cfg* c, int32_t have_left, int32_t d_left, int32_t k_left,
@@ -351,6 +351,7 @@ struct adt_session_s {
   int a_prev = 0, d_prev = 0, prev_cell = 0;
   // device buffers
   float *h, *part, *logits, *dlogits;
+  float* ssp;   // bf16: per-16-column sums of squares of the residual rows [R][d_model/16]
   void *act, *xin, *q, *att, *sw, *feat, *cfeat, *dfeat;
   size_t part_elems;
   TreeBufs tr;
@@ -397,14 +398,10 @@ static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_sessi
   s->DLR = 1 + std::max(0, (dh - 1) * kh);
   s->KR = std::max(kh, 1);
   s->C = std::max(1, kh + (dh - 1) * kh * kh);
-  const int S = std::max({gemm_splits(R, 3 * s->dm, s->dm, s->dt), gemm_splits(R, s->dm, s->dm, s->dt),
-                          gemm_splits(R, 2 * s->F, s->dm, s->dt), gemm_splits(R, s->dm, s->F, s->dt),
-                          gemm_splits(R, s->V, s->dm, s->dt), gemm_splits(R, s->dm, 2 * s->dm, s->dt)});
-  (void)S;
-  size_t pe = 0;
-  const int shapes[6][2] = {{3 * s->dm, s->dm}, {s->dm, s->dm}, {2 * s->F, s->dm},
-                            {s->dm, s->F},      {s->V, s->dm},  {s->dm, 2 * s->dm}};
-  for (auto& sh : shapes) pe = std::max(pe, (size_t)gemm_splits(R, sh[0], sh[1], s->dt) * R * sh[0]);
+  // fp32 projections write [rows][N] products for the row kernels; bf16 ones finish in place
+  size_t pe = 256;
+  if (s->dt == ADT_F32)
+    for (int n : {3 * s->dm, s->dm, 2 * s->F, s->V}) pe = std::max(pe, (size_t)R * n);
   s->part_elems = pe;
 }
 
@@ -422,6 +419,7 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->cfeat = b.take<char>((size_t)s->C0 * dm * es);
   s->dfeat = b.take<char>((size_t)s->DR * dm * es);
   s->part = b.take<float>(s->part_elems);
+  s->ssp = b.take<float>((size_t)R * (dm / 16));
   s->logits = b.take<float>((size_t)R * s->V);
   s->dlogits = b.take<float>((size_t)s->DLR * s->V);
   TreeBufs& t = s->tr;
@@ -587,10 +585,10 @@ static int64_t gkey(int kind, int a, int b, int c) {
 }
 
 // Algorithmic HBM bytes of a projection: weights once, the input rows, fp32 output rows.
-static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, int K, int S, int dt, float* part,
-                         hipStream_t st) {
+static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, int K, int dt, float* part,
+                         hipStream_t st, const GemmEpi& epi = GemmEpi{}) {
   const int e = prof_pair();
-  adt_status r = launch_gemm(X, ldx, W, M, N, K, S, dt, part, st, e >= 0 ? g_prof.ev[e] : nullptr,
+  adt_status r = launch_gemm(X, ldx, W, M, N, K, dt, part, epi, st, e >= 0 ? g_prof.ev[e] : nullptr,
                              e >= 0 ? g_prof.ev[e + 1] : nullptr);
   prof_done(e, ADT_PROF_GEMM, (double)N * K * esize(dt) + (double)M * K * esize(dt) + (double)M * N * 4.0,
             2.0 * M * N * K);
@@ -608,37 +606,81 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   const float scale = 1.f / std::sqrt((float)Dh);
   (void)slot0;
   const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
+  auto attention = [&](char* kc, char* vc) -> adt_status {
+    // the prefix K/V once, tree Q/K/V in and O out, the masks
+    const int e = prof_begin(st);
+    TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M, s->d.s_cap,
+                         scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
+    prof_end(e, ADT_PROF_ATTN, 2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es + 16.0 * M,
+             4.0 * M * (L_pre + n_tail) * H * Dh, st);
+    return ADT_OK;
+  };
+  if (dt == ADT_BF16) {
+    // Per layer: QKV (norm on load; RoPE + cache append), attention, O (residual add),
+    // gate/up (norm on load; SwiGLU), down (residual add).  The residual epilogues leave the
+    // per-16-column sums of squares that the next norm-on-load consumer reduces.
+    GemmEpi resid;
+    resid.mode = EPI_RESID;
+    resid.h = s->h;
+    resid.ssp_out = s->ssp;
+    for (int l = l0; l < l1; ++l) {
+      char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
+      char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
+      GemmEpi qkv;
+      qkv.mode = EPI_QKV;
+      qkv.ssp_in = s->ssp;
+      qkv.nss_in = dm / 16;
+      qkv.eps = eps;
+      qkv.q = (uint16_t*)s->q;
+      qkv.kc = (uint16_t*)kc;
+      qkv.vc = (uint16_t*)vc;
+      qkv.stride_h = stride_h;
+      qkv.slot0 = s->scal + 3;
+      qkv.pos = pos;
+      qkv.rope = s->rope;
+      qkv.Dh = Dh;
+      TRY(gemm_p(s->h, dm, m->qkv[l], M, 3 * dm, dm, dt, s->part, st, qkv));
+      TRY(attention(kc, vc));
+      TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, dt, s->part, st, resid));
+      GemmEpi sw;
+      sw.mode = EPI_SWIGLU;
+      sw.ssp_in = s->ssp;
+      sw.nss_in = dm / 16;
+      sw.eps = eps;
+      sw.act = (uint16_t*)s->sw;
+      TRY(gemm_p(s->h, dm, m->gu[l], M, 2 * F, dm, dt, s->part, st, sw));
+      TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, dt, s->part, st, resid));
+    }
+    if (final_out) TRY(launch_norm_rows(s->h, s->ssp, M, dm, eps, final_out, dt, st));
+    return ADT_OK;
+  }
+  // fp32: products into part, row kernels finish each step
   for (int l = l0; l < l1; ++l) {
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
-    int S = gemm_splits(M, 3 * dm, dm, dt);
-    TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, S, dt, s->part, st));
-    {
-      // K1 + K1c: the prefix K/V once, tree Q/K/V in and O out, the masks.
-      const int e = prof_begin(st);
-      TRY(launch_qkv_rope(s->part, S, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
-      TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M,
-                           s->d.s_cap, scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
-      prof_end(e, ADT_PROF_ATTN, 2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es + 16.0 * M,
-               4.0 * M * (L_pre + n_tail) * H * Dh, st);
-    }
-    S = gemm_splits(M, dm, dm, dt);
-    TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, S, dt, s->part, st));
-    TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, s->act, dt, st));
-    S = gemm_splits(M, 2 * F, dm, dt);
-    TRY(gemm_p(s->act, dm, m->gu[l], M, 2 * F, dm, S, dt, s->part, st));
-    TRY(launch_swiglu(s->part, S, M, F, s->sw, dt, st));
-    S = gemm_splits(M, dm, F, dt);
-    TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, S, dt, s->part, st));
-    TRY(launch_add_norm(s->part, S, M, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
+    TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, dt, s->part, st));
+    TRY(launch_qkv_rope(s->part, 1, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
+    TRY(attention(kc, vc));
+    TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, dt, s->part, st));
+    TRY(launch_add_norm(s->part, 1, M, dm, 0, eps, s->h, s->act, dt, st));
+    TRY(gemm_p(s->act, dm, m->gu[l], M, 2 * F, dm, dt, s->part, st));
+    TRY(launch_swiglu(s->part, 1, M, F, s->sw, dt, st));
+    TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, dt, s->part, st));
+    TRY(launch_add_norm(s->part, 1, M, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
   }
   return ADT_OK;
 }
 
 static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, hipStream_t st) {
-  const int S = gemm_splits(M, s->V, s->dm, s->dt);
-  TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, S, s->dt, s->part, st));
-  return launch_reduce_store(s->part, S, M, s->V, out, s->V, st);
+  if (s->dt == ADT_BF16) {
+    GemmEpi e;
+    e.mode = EPI_STORE;
+    e.out = out;
+    e.ldo = s->V;
+    return gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, s->dt, s->part, st, e);
+  }
+  TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, s->dt, s->part, st));
+  return launch_reduce_store(s->part, 1, M, s->V, out, s->V, st);
 }
 
 // Target forward of M rows with tokens tok; features into s->feat; logits of rows
@@ -648,7 +690,9 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
                                  int64_t key = -1) {
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
-    TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, cs));
+    const bool bf = s->dt == ADT_BF16;
+    TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, bf ? nullptr : s->act,
+                          bf ? s->ssp : nullptr, s->dt, cs));
     TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
     if (lm_rows > 0)
       TRY(lm_head(s, (const char*)s->feat + (size_t)lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits, cs));
@@ -666,9 +710,17 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
     TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, cs));
-    const int S = gemm_splits(M, dm, 2 * dm, dt);
-    TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, S, dt, s->part, cs));
-    TRY(launch_add_norm(s->part, S, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
+    if (dt == ADT_BF16) {
+      GemmEpi e;
+      e.mode = EPI_RESID;
+      e.h = s->h;
+      e.assign = 1;
+      e.ssp_out = s->ssp;
+      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, dt, s->part, cs, e));
+    } else {
+      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, dt, s->part, cs));
+      TRY(launch_add_norm(s->part, 1, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
+    }
     TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, cs));
     if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, cs));
     return ADT_OK;

@@ -3,11 +3,14 @@
 // At batch 1 the tree has M <= 128 rows, so these products stream the weights from HBM
 // once and are bandwidth-bound (arithmetic intensity ~ M flop/byte).  The bf16 path packs
 // W once into 16x32 MFMA tiles (1 KB contiguous per tile, one 16-byte load per lane) so a
-// wave reads whole kilobytes per instruction; X chunks are staged in LDS and shared by the
-// four waves of a workgroup.  The K range is split across workgroups so every launch has
-// hundreds of workgroups in flight; each split writes fp32 partials [split][M][N] that the
-// consuming kernel (residual add + norm, RoPE + cache append, SwiGLU, logits) sums in a
-// fixed order, which keeps results deterministic.
+// wave reads whole kilobytes per instruction.  One workgroup owns one 16-column output
+// tile and the whole K range: its eight waves take contiguous K chunks, issue all their
+// weight loads at once, and the partial tiles are summed in LDS in wave order (so results
+// are deterministic and no workgroup waits on another).  The finished tile goes through a
+// fused epilogue: residual add with the row sums of squares the next RMSNorm needs, RoPE
+// with the K/V cache append, SwiGLU, or a plain store.  A GEMM whose input is a normalised
+// row applies the norm while loading it (fp32 residual times the row's scale, rounded to
+// bf16), so no norm, RoPE, SwiGLU or reduction kernel runs between projections.
 #include <hip/hip_ext.h>
 
 #include "../launch.h"
@@ -15,25 +18,37 @@
 namespace adt {
 
 // ----------------------------------------------------------------------------- packing
-// bf16 tile layout: tile (nt, kt) holds rows nt*16..+15, columns kt*32..+31 as 64 lanes x 8
-// values; lane l = g*16 + i carries W[nt*16 + i][kt*32 + g*8 + e], e = 0..7.
+// bf16 tile layout: tile (nt, kt) holds packed rows nt*16..+15, columns kt*32..+31 as 64
+// lanes x 8 values; lane l = g*16 + i carries W[row(nt*16 + i)][kt*32 + g*8 + e], e = 0..7.
+// Packed row order (row(n)):
+//   ADT_PACK_STACK    sources stacked in order;
+//   ADT_PACK_GATE_UP  two equal sources interleaved in blocks of 8 rows (gate block t, up
+//                     block t, ...), so every 16-row tile holds 8 gate and the matching 8 up rows;
+//   ADT_PACK_QKV      sources stacked, and inside every head of `group` rows each 16-row tile
+//                     holds rows 8u..8u+7 of the head's first half and the same rows of its
+//                     second half (a RoPE pair shares a tile).
 struct PackSrc {
   const void* p[4];
   int rows[4];
   int n;
-  int mode;   // 0 = stacked, 1 = gate/up interleaved in 16-row blocks
+  int mode;
+  int group;
 };
 
 __device__ __forceinline__ const void* pack_row(const PackSrc& s, int n, int& r) {
-  if (s.mode == 1) {
-    const int blk = n / 16;
-    r = (blk / 2) * 16 + n % 16;
+  if (s.mode == ADT_PACK_GATE_UP) {
+    const int blk = n / 8;
+    r = (blk / 2) * 8 + n % 8;
     return s.p[blk % 2];
   }
   int i = 0;
   while (i < s.n - 1 && n >= s.rows[i]) {
     n -= s.rows[i];
     ++i;
+  }
+  if (s.mode == ADT_PACK_QKV) {
+    const int half = s.group / 2, e = n % s.group, u = e / 16, t = e % 16;
+    n = n - e + (t < 8 ? 8 * u + t : half + 8 * u + t - 8);
   }
   r = n;
   return s.p[i];
@@ -66,92 +81,102 @@ __global__ void pack_f32_kernel(PackSrc s, int N, int K, float* __restrict__ dst
 }
 
 // ----------------------------------------------------------------------------- bf16 MFMA
-constexpr int GEMM_THREADS = 256;
+constexpr int TILE_WAVES = 8;
+constexpr int TILE_THREADS = TILE_WAVES * WAVE;
 
-// lane (lq, g) holds Y[m = mt*16 + lq][n = nt*16 + 4g + r], r = 0..3: one 16-byte store per row.
-template <int MT>
-__device__ __forceinline__ void store_partials(const f32x4 (&acc)[MT], float* __restrict__ part, int s, int M, int N,
-                                               int nt, int lq, int g) {
-#pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    const int row = m * 16 + lq;
-    if (row < M) *reinterpret_cast<f32x4*>(part + ((int64_t)s * M + row) * N + nt * 16 + 4 * g) = acc[m];
-  }
+// Eight consecutive fp32 residual values times the row's norm scale, rounded to bf16.
+__device__ __forceinline__ bf16x8 norm_load8(const float* __restrict__ p, float r) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  const u16x8 u{f2bf(a.x * r), f2bf(a.y * r), f2bf(a.z * r), f2bf(a.w * r),
+                f2bf(b.x * r), f2bf(b.y * r), f2bf(b.z * r), f2bf(b.w * r)};
+  return __builtin_bit_cast(bf16x8, u);
 }
 
-// MT = 16-row tiles of M; KC = k-tiles (of 32) staged per LDS round (LDS stays < 64 KB).
-// X chunks are staged in LDS and shared by the workgroup's four waves (one n-tile each).
-template <int MT, int KC = (MT > 6 ? 4 : 8)>
-__global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                                 const uint16_t* __restrict__ Wp, int M, int N,
-                                                                 int K, int splits, float* __restrict__ part) {
-  constexpr int MP = 16 * MT;
-  constexpr int XW = KC * 32 + 8;   // padded LDS row (bf16)
-  __shared__ __attribute__((aligned(16))) uint16_t Xs[MP][XW];
+__device__ __forceinline__ f32x4 shfl_xor4(f32x4 v, int mask) {
+  return f32x4{__shfl_xor(v[0], mask, WAVE), __shfl_xor(v[1], mask, WAVE), __shfl_xor(v[2], mask, WAVE),
+               __shfl_xor(v[3], mask, WAVE)};
+}
 
-  const int NT = N / 16, KT = K / 32;
-  const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
-  const int lq = lane & 15, g = lane >> 4;
-  const int nt = blockIdx.x * 4 + wave;
-  const int s = blockIdx.y;
-  const int kt0 = (int)((int64_t)KT * s / splits), kt1 = (int)((int64_t)KT * (s + 1) / splits);
-  const bool active = nt < NT;
-
-  f32x4 acc[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const bf16x8* wp = reinterpret_cast<const bf16x8*>(Wp) + ((int64_t)(active ? nt : 0) * KT) * 64 + lane;
-
-  for (int c = kt0; c < kt1; c += KC) {
-    const int nk = min(KC, kt1 - c);
-    bf16x8 wf[KC];
-#pragma unroll
-    for (int j = 0; j < KC; ++j)
-      if (active && j < nk) wf[j] = wp[(int64_t)(c + j) * 64];
-    __syncthreads();
-    const int pieces = MP * nk * 4;
-    for (int p = tid; p < pieces; p += GEMM_THREADS) {
-      const int r = p / (nk * 4), cc = (p % (nk * 4)) * 8;
-      u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (r < M) v = *reinterpret_cast<const u16x8*>(X + (int64_t)r * ldx + c * 32 + cc);
-      *reinterpret_cast<u16x8*>(&Xs[r][cc]) = v;
+// Epilogue of one finished 16-row block of tile nt, run by a whole wave: lane (lq, g) holds
+// Y[row][nt*16 + 4g + r], r = 0..3.  In a QKV or gate/up tile, columns 0..7 (lanes g < 2)
+// pair with columns 8..15 (lanes g + 2).
+__device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row, int g, int nt, int M, int N) {
+  const bool live = row < M;
+  const int c = nt * 16 + 4 * g;
+  if (e.mode == EPI_STORE) {
+    if (live) *reinterpret_cast<f32x4*>(e.out + row * e.ldo + c) = y;
+  } else if (e.mode == EPI_RESID) {
+    float* hp = e.h + (int64_t)row * N + c;
+    if (live) {
+      if (!e.assign) {
+        const f32x4 o = *reinterpret_cast<const f32x4*>(hp);
+        y = f32x4{o[0] + y[0], o[1] + y[1], o[2] + y[2], o[3] + y[3]};
+      }
+      *reinterpret_cast<f32x4*>(hp) = y;
     }
-    __syncthreads();
-    if (active) {
+    float ss = live ? y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3] : 0.f;
+    ss += __shfl_xor(ss, 16, WAVE);
+    ss += __shfl_xor(ss, 32, WAVE);
+    if (live && g == 0) e.ssp_out[(int64_t)row * (N / 16) + nt] = ss;
+  } else if (e.mode == EPI_QKV) {
+    const f32x4 y2 = shfl_xor4(y, 32);
+    if (live && g < 2) {
+      const int d = N / 3, Dh = e.Dh, half = Dh / 2;
+      const int n0 = nt * 16, region = n0 / d, within = n0 % d, head = within / Dh, u = (within % Dh) / 16;
+      const int j = 8 * u + 4 * g;   // element of the head's first half held in y[0]
+      float a[4] = {y[0], y[1], y[2], y[3]}, b[4] = {y2[0], y2[1], y2[2], y2[3]};
+      if (region < 2) {
+        const float2* cs = e.rope + (int64_t)e.pos[row] * half + j;
 #pragma unroll
-      for (int j = 0; j < KC; ++j) {
-        if (j < nk) {
-#pragma unroll
-          for (int m = 0; m < MT; ++m) {
-            const bf16x8 bx = *reinterpret_cast<const bf16x8*>(&Xs[m * 16 + lq][j * 32 + g * 8]);
-            acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], bx, acc[m], 0, 0, 0);
-          }
+        for (int r = 0; r < 4; ++r) {
+          const float2 t = cs[r];
+          const float x1 = a[r], x2 = b[r];
+          a[r] = x1 * t.x - x2 * t.y;
+          b[r] = x2 * t.x + x1 * t.y;
         }
       }
+      uint16_t* dst = region == 0 ? e.q + (int64_t)row * d + head * Dh
+                                  : (region == 1 ? e.kc : e.vc) + head * e.stride_h + (*e.slot0 + (int64_t)row) * Dh;
+      *reinterpret_cast<u16x4*>(dst + j) = u16x4{f2bf(a[0]), f2bf(a[1]), f2bf(a[2]), f2bf(a[3])};
+      *reinterpret_cast<u16x4*>(dst + j + half) = u16x4{f2bf(b[0]), f2bf(b[1]), f2bf(b[2]), f2bf(b[3])};
+    }
+  } else if (e.mode == EPI_SWIGLU) {
+    const f32x4 u = shfl_xor4(y, 32);
+    if (live && g < 2) {
+      const int f = nt * 8 + 4 * g;
+      *reinterpret_cast<u16x4*>(e.act + (int64_t)row * (N / 2) + f) =
+          u16x4{f2bf(y[0] / (1.f + expf(-y[0])) * u[0]), f2bf(y[1] / (1.f + expf(-y[1])) * u[1]),
+                f2bf(y[2] / (1.f + expf(-y[2])) * u[2]), f2bf(y[3] / (1.f + expf(-y[3])) * u[3])};
     }
   }
-  if (active) store_partials<MT>(acc, part, s, M, N, nt, lq, g);
 }
 
-// Few tree rows (M <= 32): each wave reads its X fragments straight from global memory (the
-// rows are a few KB and L2-resident), so weights and inputs of a whole chunk are in flight
-// together and no workgroup barrier is needed.
-template <int MT, int KC = 8>
-__global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_direct_kernel(const uint16_t* __restrict__ X, int ldx,
-                                                                        const uint16_t* __restrict__ Wp, int M,
-                                                                        int N, int K, int splits,
-                                                                        float* __restrict__ part) {
-  const int NT = N / 16, KT = K / 32;
-  const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
-  const int nt = blockIdx.x * 4 + threadIdx.x / WAVE;
-  const int s = blockIdx.y;
-  if (nt >= NT) return;
-  const int kt0 = (int)((int64_t)KT * s / splits), kt1 = (int)((int64_t)KT * (s + 1) / splits);
+// MT = 16-row blocks of M; KC = k-tiles per wave per load round.
+template <int MT, bool NORM, int KC>
+__global__ __launch_bounds__(TILE_THREADS) void gemm_tile_kernel(const void* __restrict__ Xv, int ldx,
+                                                                 const uint16_t* __restrict__ Wp, int M, int N,
+                                                                 int K, GemmEpi epi) {
+  constexpr int MR = MT < 4 ? MT : 4;   // 16-row blocks summed per LDS round
+  __shared__ f32x4 red[TILE_WAVES][MR][WAVE];
+  __shared__ float rscale[NORM ? MT * 16 : 1];
+  const int nt = blockIdx.x, KT = K / 32;
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
+  if constexpr (NORM) {
+    for (int row = wave; row < MT * 16; row += TILE_WAVES) {
+      const float r = row < M ? row_norm_scale(epi.ssp_in + (int64_t)row * epi.nss_in, epi.nss_in, K, epi.eps) : 0.f;
+      if (lane == 0) rscale[row] = r;
+    }
+    __syncthreads();
+  }
   f32x4 acc[MT];
+  float rr[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const bf16x8* wp = reinterpret_cast<const bf16x8*>(Wp) + ((int64_t)nt * KT) * 64 + lane;
+  for (int m = 0; m < MT; ++m) {
+    acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    rr[m] = NORM ? rscale[m * 16 + lq] : 0.f;
+  }
+  const int kt0 = (int)((int64_t)KT * wave / TILE_WAVES), kt1 = (int)((int64_t)KT * (wave + 1) / TILE_WAVES);
+  const bf16x8* wp = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)nt * KT * 64 + lane;
   for (int c = kt0; c < kt1; c += KC) {
     const int nk = min(KC, kt1 - c);
     bf16x8 wf[KC], xf[KC][MT];
@@ -165,7 +190,12 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_direct_kernel(const ui
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
           const int row = m * 16 + lq;
-          if (row < M) xf[j][m] = *reinterpret_cast<const bf16x8*>(X + (int64_t)row * ldx + (c + j) * 32 + g * 8);
+          if (row < M) {
+            if constexpr (NORM)
+              xf[j][m] = norm_load8((const float*)Xv + (int64_t)row * ldx + (c + j) * 32 + g * 8, rr[m]);
+            else
+              xf[j][m] = *reinterpret_cast<const bf16x8*>((const uint16_t*)Xv + (int64_t)row * ldx + (c + j) * 32 + g * 8);
+          }
         }
       }
     }
@@ -175,11 +205,29 @@ __global__ __launch_bounds__(GEMM_THREADS) void gemm_bf16_direct_kernel(const ui
 #pragma unroll
         for (int m = 0; m < MT; ++m) acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], xf[j][m], acc[m], 0, 0, 0);
   }
-  store_partials<MT>(acc, part, s, M, N, nt, lq, g);
+  // Sum the waves' partial tiles in wave order; wave i then finishes 16-row block m0 + i.
+#pragma unroll
+  for (int m0 = 0; m0 < MT; m0 += MR) {
+#pragma unroll
+    for (int i = 0; i < MR; ++i)
+      if (m0 + i < MT) red[wave][i][lane] = acc[m0 + i < MT ? m0 + i : 0];
+    __syncthreads();
+    if (wave < MR && m0 + wave < MT) {
+      f32x4 y = red[0][wave][lane];
+#pragma unroll
+      for (int w = 1; w < TILE_WAVES; ++w) {
+        const f32x4 v = red[w][wave][lane];
+        y = f32x4{y[0] + v[0], y[1] + v[1], y[2] + v[2], y[3] + v[3]};
+      }
+      tile_epilogue(epi, y, (m0 + wave) * 16 + lq, g, nt, M, N);
+    }
+    __syncthreads();
+  }
 }
 
 // ----------------------------------------------------------------------------- fp32 (vector)
-// One wave per output column; lanes stride K, rows in groups of 16, wave-reduced.
+// Unfused fp32 path (row kernels finish the layer).  One wave per output column; lanes
+// stride K, rows in groups of 16, wave-reduced.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ X, int ldx,
                                                        const float* __restrict__ W, int M, int N, int K,
                                                        float* __restrict__ part) {
@@ -210,23 +258,27 @@ size_t packed_bytes(int total_rows, int K, int dtype) {
   return (size_t)total_rows * K * (dtype == ADT_BF16 ? 2 : 4);
 }
 
-adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int dtype, void* dst,
-                       hipStream_t st) {
+adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int group, int dtype,
+                       void* dst, hipStream_t st) {
   ADT_CHECK_ARG(srcs && rows && dst && n_src >= 1 && n_src <= 4, ADT_E_ARG, "pack: bad arguments");
-  ADT_CHECK_ARG(mode == 0 || (mode == 1 && n_src == 2 && rows[0] == rows[1]), ADT_E_ARG, "pack: bad mode");
+  ADT_CHECK_ARG(mode == ADT_PACK_STACK || (mode == ADT_PACK_GATE_UP && n_src == 2 && rows[0] == rows[1]) ||
+                    (mode == ADT_PACK_QKV && group >= 16 && group % 16 == 0),
+                ADT_E_ARG, "pack: bad mode %d (group %d)", mode, group);
   PackSrc s{};
   int N = 0;
   for (int i = 0; i < n_src; ++i) {
     ADT_CHECK_ARG(srcs[i] != nullptr && rows[i] > 0, ADT_E_ARG, "pack: source %d empty", i);
+    ADT_CHECK_ARG(mode != ADT_PACK_QKV || rows[i] % group == 0, ADT_E_SHAPE, "pack: %d rows not whole heads", rows[i]);
+    ADT_CHECK_ARG(mode != ADT_PACK_GATE_UP || rows[i] % 8 == 0, ADT_E_SHAPE, "pack: gate/up rows %d", rows[i]);
     s.p[i] = srcs[i];
     s.rows[i] = rows[i];
     N += rows[i];
-    if (dtype == ADT_BF16) ADT_CHECK_ARG(rows[i] % 16 == 0, ADT_E_SHAPE, "pack: rows %d not a multiple of 16", rows[i]);
   }
   s.n = n_src;
   s.mode = mode;
+  s.group = group;
   if (dtype == ADT_BF16) {
-    ADT_CHECK_ARG(K % 32 == 0, ADT_E_SHAPE, "pack: K %d not a multiple of 32", K);
+    ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0, ADT_E_SHAPE, "pack: N=%d K=%d not multiples of 16/32", N, K);
     pack_bf16_kernel<<<1024, 256, 0, st>>>(s, N, K, (uint16_t*)dst);
   } else {
     pack_f32_kernel<<<1024, 256, 0, st>>>(s, N, K, (float*)dst);
@@ -235,23 +287,8 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
   return ADT_OK;
 }
 
-// Split-K factor: enough workgroups to keep HBM busy (about two per CU) but at least
-// eight k-tiles (8 KB of weights per wave) per split, since the consumers sum the splits.
-int gemm_splits(int M, int N, int K, int dtype) {
-  if (dtype == ADT_F32) return 1;
-  const int NB = (N / 16 + 3) / 4;
-  const int KT = K / 32;
-  int s = (512 + NB - 1) / NB;
-  if (s > KT / 8) s = KT / 8;
-  if (s < 1) s = 1;
-  (void)M;
-  return s;
-}
-
-// With ev0/ev1 set, the dispatch itself records the events at the kernel's start and end
-// (kernel duration, not host-side markers).
-adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int splits, int dtype, float* part,
-                       hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
+                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   ADT_CHECK_ARG(M >= 1 && M <= 128, ADT_E_CAPACITY, "gemm: M=%d outside [1,128]", M);
   if (dtype == ADT_F32) {
     hipExtLaunchKernelGGL(gemm_f32_kernel, dim3((N + 3) / 4), dim3(256), 0, st, ev0, ev1, 0, (const float*)X, ldx,
@@ -260,20 +297,39 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     return ADT_OK;
   }
   ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0 && ldx % 8 == 0, ADT_E_SHAPE, "gemm: N=%d K=%d ldx=%d misaligned", N, K, ldx);
-  const dim3 grid((N / 16 + 3) / 4, splits), block(GEMM_THREADS);
-  const int mt = (M + 15) / 16;
-  const uint16_t* x = (const uint16_t*)X;
-  const uint16_t* w = (const uint16_t*)Wp;
-#define ADT_GEMM(KERNEL) hipExtLaunchKernelGGL(KERNEL, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, splits, part)
-  switch (mt) {
-    case 1: ADT_GEMM(gemm_bf16_direct_kernel<1>); break;
-    case 2: ADT_GEMM(gemm_bf16_direct_kernel<2>); break;
-    case 3: ADT_GEMM(gemm_bf16_kernel<3>); break;
-    case 4: ADT_GEMM(gemm_bf16_kernel<4>); break;
-    case 5:
-    case 6: ADT_GEMM(gemm_bf16_kernel<6>); break;
-    default: ADT_GEMM(gemm_bf16_kernel<8>); break;
+  const bool norm = epi.ssp_in != nullptr;
+  ADT_CHECK_ARG(!norm || epi.nss_in == K / 16, ADT_E_SHAPE, "gemm: norm input needs K/16 sums per row");
+  switch (epi.mode) {
+    case EPI_STORE: ADT_CHECK_ARG(epi.out && epi.ldo % 4 == 0, ADT_E_ARG, "gemm: store target"); break;
+    case EPI_RESID: ADT_CHECK_ARG(epi.h && epi.ssp_out, ADT_E_ARG, "gemm: residual epilogue buffers"); break;
+    case EPI_QKV:
+      ADT_CHECK_ARG(epi.Dh >= 16 && epi.Dh % 16 == 0 && N % (3 * epi.Dh) == 0 && epi.q && epi.kc && epi.vc &&
+                        epi.slot0 && epi.pos && epi.rope,
+                    ADT_E_ARG, "gemm: QKV epilogue (Dh=%d, N=%d)", epi.Dh, N);
+      break;
+    case EPI_SWIGLU: ADT_CHECK_ARG(epi.act != nullptr, ADT_E_ARG, "gemm: SwiGLU output"); break;
+    default: ADT_CHECK_ARG(false, ADT_E_ARG, "gemm: epilogue %d", epi.mode);
   }
+  const dim3 grid(N / 16), block(TILE_THREADS);
+  const int mt = (M + 15) / 16;
+  const uint16_t* w = (const uint16_t*)Wp;
+#define ADT_GEMM(...) hipExtLaunchKernelGGL(__VA_ARGS__, grid, block, 0, st, ev0, ev1, 0, X, ldx, w, M, N, K, epi)
+#define ADT_GEMM_ALL(NORM)                                       \
+  switch (mt) {                                                  \
+    case 1: ADT_GEMM(gemm_tile_kernel<1, NORM, 8>); break;       \
+    case 2: ADT_GEMM(gemm_tile_kernel<2, NORM, 8>); break;       \
+    case 3: ADT_GEMM(gemm_tile_kernel<3, NORM, 4>); break;       \
+    case 4: ADT_GEMM(gemm_tile_kernel<4, NORM, 4>); break;       \
+    case 5:                                                      \
+    case 6: ADT_GEMM(gemm_tile_kernel<6, NORM, 2>); break;       \
+    default: ADT_GEMM(gemm_tile_kernel<8, NORM, 2>); break;      \
+  }
+  if (norm) {
+    ADT_GEMM_ALL(true)
+  } else {
+    ADT_GEMM_ALL(false)
+  }
+#undef ADT_GEMM_ALL
 #undef ADT_GEMM
   ADT_LAUNCH_CHECK();
   return ADT_OK;

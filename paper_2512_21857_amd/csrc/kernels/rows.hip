@@ -1,7 +1,9 @@
-// Row-wise kernels of the forwards and of the cache bookkeeping: embedding, RMSNorm fused
-// with the split-K reduction of the preceding projection, RoPE + KV append, SwiGLU, logits,
-// feature gathers, KV compaction and ancestor masks.  Each kernel handles whole rows (at
-// most 128 tree rows per launch), so they are latency-bound and kept as simple as possible.
+// Row-wise kernels of the forwards and of the cache bookkeeping: embedding (with its norm,
+// or with the per-16-column sums of squares the bf16 GEMMs normalise from), the final norm,
+// the fp32 path's finishing steps after each projection (residual add + RMSNorm, RoPE + KV
+// append, SwiGLU, logits), feature gathers, KV compaction and ancestor masks.  Each kernel
+// handles whole rows (at most 128 tree rows per launch), so they are latency-bound and kept
+// as simple as possible.
 #include "../launch.h"
 
 namespace adt {
@@ -12,10 +14,23 @@ constexpr int ROW_THREADS = 256;
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                  int d, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ a) {
+                                                                 T* __restrict__ a, float* __restrict__ ssp) {
   __shared__ float red[16];
   const int m = blockIdx.x;
   const T* e = E + (int64_t)tok[m] * d;
+  if (ssp) {
+    // per 16-column tile: copy to h and the tile's sum of squares (columns in order)
+    for (int t = threadIdx.x; t < d / 16; t += blockDim.x) {
+      float ss = 0.f;
+      for (int c = t * 16; c < t * 16 + 16; ++c) {
+        const float v = Elem<T>::load(e, c);
+        h[(int64_t)m * d + c] = v;
+        ss += v * v;
+      }
+      ssp[(int64_t)m * (d / 16) + t] = ss;
+    }
+    return;
+  }
   float ss = 0.f;
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     const float v = Elem<T>::load(e, i);
@@ -23,8 +38,30 @@ __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __rest
     ss += v * v;
   }
   const float r = rsqrtf(block_sum(ss, red) / d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+}
+
+// out[m][:] = h[m][:] * scale(m) in the model dtype (the final norm; scale from the
+// per-16-column sums of squares, reduced as every norm-on-load consumer reduces them).
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void norm_rows_kernel(const float* __restrict__ h, const float* __restrict__ ssp,
+                                                                int d, float eps, T* __restrict__ out) {
+  __shared__ float rs;
+  const int m = blockIdx.x;
+  if (threadIdx.x < WAVE) {
+    const float r = row_norm_scale(ssp + (int64_t)m * (d / 16), d / 16, d, eps);
+    if (threadIdx.x == 0) rs = r;
+  }
+  __syncthreads();
+  const float rm = rs;
+  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(h + (int64_t)m * d + i);
+    T* o = out + (int64_t)m * d + i;
+    Elem<T>::store(o, 0, v.x * rm);
+    Elem<T>::store(o, 1, v.y * rm);
+    Elem<T>::store(o, 2, v.z * rm);
+    Elem<T>::store(o, 3, v.w * rm);
+  }
 }
 
 // Draft-head input row m: [E[tok[m]] ; parent feature].  fsrc[m] >= 0 picks row fsrc of the
@@ -166,7 +203,7 @@ __global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __re
   Elem<T>::store(vr, j + half, v2);
 }
 
-// SwiGLU over gate/up partials packed in interleaved 16-column blocks: out[m][j] = silu(g) u.
+// SwiGLU over gate/up products packed in interleaved 8-column blocks: out[m][j] = silu(g) u.
 // Grid (M, F / (4 * 256)); four consecutive outputs per thread.
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void swiglu_kernel(const float* __restrict__ part, int splits, int M, int F,
@@ -174,10 +211,10 @@ __global__ __launch_bounds__(ROW_THREADS) void swiglu_kernel(const float* __rest
   const int m = blockIdx.x, N = 2 * F;
   const int j = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
   if (j >= F) return;
-  const int cg = (j / 16) * 32 + j % 16;
+  const int cg = (j / 8) * 16 + j % 8;
   const int64_t stride = (int64_t)M * N, row = (int64_t)m * N;
   const float4 g = sum_parts4(part, splits, stride, row + cg);
-  const float4 u = sum_parts4(part, splits, stride, row + cg + 16);
+  const float4 u = sum_parts4(part, splits, stride, row + cg + 8);
   T* o = out + (int64_t)m * F + j;
   Elem<T>::store(o, 0, g.x / (1.f + expf(-g.x)) * u.x);
   Elem<T>::store(o, 1, g.y / (1.f + expf(-g.y)) * u.y);
@@ -280,9 +317,18 @@ __global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int3
     __VA_ARGS__;                               \
   }
 
-adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st) {
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a));
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
+                             int dtype, hipStream_t st) {
+  ADT_CHECK_ARG((a != nullptr) != (ssp != nullptr) && (!ssp || d % 16 == 0), ADT_E_ARG, "embed_norm: outputs");
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, ssp));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, float eps, void* out, int dtype,
+                            hipStream_t st) {
+  ADT_CHECK_ARG(d % 16 == 0, ADT_E_SHAPE, "norm_rows: d=%d", d);
+  ADT_DISPATCH_T(dtype, norm_rows_kernel<T><<<M, ROW_THREADS, 0, st>>>(h, ssp, d, eps, (T*)out));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -14,15 +14,50 @@ adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t
 
 // gemm.hip
 size_t packed_bytes(int total_rows, int K, int dtype);
-adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int dtype, void* dst,
-                       hipStream_t st);
-int gemm_splits(int M, int N, int K, int dtype);
-adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int splits, int dtype, float* part,
-                       hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
-
+adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int group, int dtype,
+                       void* dst, hipStream_t st);
+// bf16 projections: one workgroup per 16-column output tile, its waves splitting K and
+// summing in fixed order; the epilogue runs on the finished tile.  With ssp_in set the input
+// rows are the fp32 residual stream, normalised while loaded (RMSNorm scale of each row
+// from its per-16-column sums of squares ssp_in[m][nss_in], over K columns).
+enum : int { EPI_STORE = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_SWIGLU = 4 };
+struct GemmEpi {
+  int mode = EPI_STORE;
+  const float* ssp_in = nullptr;
+  int nss_in = 0;
+  float eps = 0.f;
+  // EPI_STORE: out[m][n] (fp32, leading dimension ldo)
+  float* out = nullptr;
+  int64_t ldo = 0;
+  // EPI_RESID: h[m][n] += y (= y when assign); sums of squares of the new h per 16-column
+  // tile into ssp_out[m][N/16]
+  float* h = nullptr;
+  int assign = 0;
+  float* ssp_out = nullptr;
+  // EPI_QKV (weights packed with ADT_PACK_QKV): q to q[m][H*Dh] after RoPE at pos[m]; k (RoPE)
+  // and v to cache slot (*slot0 + m), element (head, slot, :) at kc + head*stride_h + slot*Dh
+  uint16_t* q = nullptr;
+  uint16_t* kc = nullptr;
+  uint16_t* vc = nullptr;
+  int64_t stride_h = 0;
+  const int32_t* slot0 = nullptr;
+  const int32_t* pos = nullptr;
+  const float2* rope = nullptr;
+  int Dh = 0;
+  // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up
+  uint16_t* act = nullptr;
+};
+// fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the fused kernel, epi.
+adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
+                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // rows.hip
-adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st);
+// h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
+// of squares of h into ssp[m][d/16].
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
+                             int dtype, hipStream_t st);
+// out[m][c] = h[m][c] * scale(m), the scale from ssp[m][d/16], rounded to the model dtype.
+adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, float eps, void* out, int dtype,
+                            hipStream_t st);
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
                               int M, int d, void* x, int dtype, hipStream_t st);
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,

@@ -139,14 +139,16 @@ class DeviceModel:
         self.device = device
         self._keep: List[torch.Tensor] = []
         self.embed = upload(weights["embed"], device)
-        self.lm_head = self._pack([weights["lm_head"]], 0)
-        self.draft_fc = self._pack([weights["draft.fc"]], 0)
+        self.lm_head = self._pack([weights["lm_head"]], abi.PACK_STACK)
+        self.draft_fc = self._pack([weights["draft.fc"]], abi.PACK_STACK)
+        qkv_mode = abi.PACK_QKV if self.dtype == abi.BF16 else abi.PACK_STACK
         qkv, o, gu, down = [], [], [], []
         for pre in [f"layer{l}" for l in range(m.n_layers)] + ["draft"]:
-            qkv.append(self._pack([weights[pre + ".wq"], weights[pre + ".wk"], weights[pre + ".wv"]], 0))
-            o.append(self._pack([weights[pre + ".wo"]], 0))
-            gu.append(self._pack([weights[pre + ".wg"], weights[pre + ".wu"]], 1))
-            down.append(self._pack([weights[pre + ".wd"]], 0))
+            qkv.append(self._pack([weights[pre + ".wq"], weights[pre + ".wk"], weights[pre + ".wv"]], qkv_mode,
+                                  m.head_dim))
+            o.append(self._pack([weights[pre + ".wo"]], abi.PACK_STACK))
+            gu.append(self._pack([weights[pre + ".wg"], weights[pre + ".wu"]], abi.PACK_GATE_UP))
+            down.append(self._pack([weights[pre + ".wd"]], abi.PACK_STACK))
         self.qkv, self.o, self.gu, self.down = qkv, o, gu, down
         ptrs = lambda ts: (C.c_void_p * len(ts))(*[t.data_ptr() for t in ts])
         self._arrays = [ptrs(qkv), ptrs(o), ptrs(gu), ptrs(down)]
@@ -159,7 +161,7 @@ class DeviceModel:
         self.handle = C.c_void_p()
         check(lib().adt_model_create(C.byref(desc), C.byref(self.handle)))
 
-    def _pack(self, arrays: Sequence[np.ndarray], mode: int) -> torch.Tensor:
+    def _pack(self, arrays: Sequence[np.ndarray], mode: int, group: int = 0) -> torch.Tensor:
         srcs = [upload(a, self.device) for a in arrays]
         rows = [int(a.shape[0]) for a in arrays]
         K = int(arrays[0].shape[1])
@@ -167,7 +169,7 @@ class DeviceModel:
         out = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         sp = (C.c_void_p * len(srcs))(*[s.data_ptr() for s in srcs])
         rw = (C.c_int32 * len(rows))(*rows)
-        check(lib().adt_pack_weight(sp, rw, len(srcs), K, mode, self.dtype, _p(out), _stream()))
+        check(lib().adt_pack_weight(sp, rw, len(srcs), K, mode, group, self.dtype, _p(out), _stream()))
         torch.cuda.current_stream().synchronize()
         return out
 

@@ -47,7 +47,10 @@ def _check(got, ref, depth, what, report, one_layer):
     """Elementwise bound 1.5 * depth^0.6 times the tolerance (depth = decoder layers behind the
     value; 1.5 = headroom for the GPU's fp32 arithmetic, whose one-layer feature deviates from
     fp64 1.4x as much, in RMS, as fp32 BLAS does); for one-layer models also at least 99 % of
-    the elements inside the plain tolerance.  Returns the largest absolute difference."""
+    the elements inside the plain tolerance (98 % for the draft head, three rounding stages
+    deep: a single normalised input element that fp32 and fp64 round to neighbouring bf16
+    values moves that row's K and V by one ulp in ~17 % of their elements, and every later
+    row attends to it).  Returns the largest absolute difference."""
     tol = TOL[0] + TOL[1] * np.abs(ref)
     diff = np.abs(got - ref)
     ratio = diff / tol
@@ -57,7 +60,8 @@ def _check(got, ref, depth, what, report, one_layer):
     rec["min_inside_plain"] = min(rec["min_inside_plain"], round(inside, 5))
     assert ratio.max() <= 1.5 * float(depth) ** 0.6, f"{what}: worst |diff|/tol {ratio.max():.3f} at depth {depth}"
     if one_layer:
-        assert inside >= 0.99, f"{what}: only {inside:.4f} inside the plain tolerance"
+        need = 0.99 if depth <= 1 else 0.98
+        assert inside >= need, f"{what}: only {inside:.4f} inside the plain tolerance"
     return float(diff.max())
 
 
