@@ -151,75 +151,152 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
   }
 }
 
-// MT = 16-row blocks of M; KC = k-tiles per wave per load round.
-template <int MT, bool NORM, int KC>
+// k-tiles per wave per load round: as many as fit about 160 VGPRs of loaded operands (a
+// workgroup of 8 waves holds 2 waves per SIMD, so 256 VGPRs per lane are available).
+template <int MT, int NTW, bool NORM>
+constexpr int tile_kc() {
+  constexpr int per = MT * (NORM ? 8 : 4) + NTW * 4;
+  constexpr int kc = (MT >= 6 ? 120 : 160) / per;   // the widest row blocks keep room for accumulators
+  return kc < 1 ? 1 : (kc > 16 ? 16 : kc);
+}
+
+// MT = 16-row blocks of M, NTW = 16-column tiles per workgroup.  Every load of a round is
+// issued before any is used (indices clamped instead of branched on, so the loads form one
+// batch); rounds past the wave's K range and rows past M only feed discarded results.
+template <int MT, int NTW, bool NORM>
 __global__ __launch_bounds__(TILE_THREADS) void gemm_tile_kernel(const void* __restrict__ Xv, int ldx,
                                                                  const uint16_t* __restrict__ Wp, int M, int N,
                                                                  int K, GemmEpi epi) {
-  constexpr int MR = MT < 4 ? MT : 4;   // 16-row blocks summed per LDS round
-  __shared__ f32x4 red[TILE_WAVES][MR][WAVE];
+  constexpr int KC = tile_kc<MT, NTW, NORM>();
+  constexpr int TT = MT * NTW;               // 16x16 output blocks per workgroup
+  constexpr int TR = TT < 4 ? TT : 4;        // blocks summed per LDS round
+  __shared__ f32x4 red[TILE_WAVES][TR][WAVE];
   __shared__ float rscale[NORM ? MT * 16 : 1];
-  const int nt = blockIdx.x, KT = K / 32;
-  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
-  if constexpr (NORM) {
-    for (int row = wave; row < MT * 16; row += TILE_WAVES) {
-      const float r = row < M ? row_norm_scale(epi.ssp_in + (int64_t)row * epi.nss_in, epi.nss_in, K, epi.eps) : 0.f;
-      if (lane == 0) rscale[row] = r;
-    }
-    __syncthreads();
-  }
-  f32x4 acc[MT];
-  float rr[MT];
+  const int KT = K / 32;
+  // the wave index is made scalar, so the K range and the round bounds below are uniform
+  // branches that do not split the batch of loads
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+  const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
+  const int kt0 = (int)((int64_t)KT * wave / TILE_WAVES), kt1 = (int)((int64_t)KT * (wave + 1) / TILE_WAVES);
+  const bf16x8* wp[NTW];
+#pragma unroll
+  for (int t = 0; t < NTW; ++t)
+    wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(blockIdx.x * NTW + t) * KT * 64 + lane;
+
+  bf16x8 wf[KC][NTW];
+  auto load_w = [&](int c) {
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+      if (c + j < kt1)
+#pragma unroll
+        for (int t = 0; t < NTW; ++t) wf[j][t] = wp[t][(int64_t)(c + j) * 64];
+  };
+  const float* xf32[MT];
+  const uint16_t* xb16[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) {
-    acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    rr[m] = NORM ? rscale[m * 16 + lq] : 0.f;
+    const int row = min(m * 16 + lq, M - 1);
+    xf32[m] = (const float*)Xv + (int64_t)row * ldx + g * 8;
+    xb16[m] = (const uint16_t*)Xv + (int64_t)row * ldx + g * 8;
   }
-  const int kt0 = (int)((int64_t)KT * wave / TILE_WAVES), kt1 = (int)((int64_t)KT * (wave + 1) / TILE_WAVES);
-  const bf16x8* wp = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)nt * KT * 64 + lane;
-  for (int c = kt0; c < kt1; c += KC) {
-    const int nk = min(KC, kt1 - c);
-    bf16x8 wf[KC], xf[KC][MT];
+  float4 xa[KC][MT][NORM ? 2 : 1];
+  bf16x8 xb[KC][MT];
+  auto load_x = [&](int c) {
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
-      wf[j] = bf16x8{};
+      if (c + j >= kt1) continue;
+      const int kk = c + j;
 #pragma unroll
-      for (int m = 0; m < MT; ++m) xf[j][m] = bf16x8{};
-      if (j < nk) {
-        wf[j] = wp[(int64_t)(c + j) * 64];
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          const int row = m * 16 + lq;
-          if (row < M) {
-            if constexpr (NORM)
-              xf[j][m] = norm_load8((const float*)Xv + (int64_t)row * ldx + (c + j) * 32 + g * 8, rr[m]);
-            else
-              xf[j][m] = *reinterpret_cast<const bf16x8*>((const uint16_t*)Xv + (int64_t)row * ldx + (c + j) * 32 + g * 8);
-          }
+      for (int m = 0; m < MT; ++m) {
+        if constexpr (NORM) {
+          xa[j][m][0] = *reinterpret_cast<const float4*>(xf32[m] + kk * 32);
+          xa[j][m][NORM ? 1 : 0] = *reinterpret_cast<const float4*>(xf32[m] + kk * 32 + 4);
+        } else {
+          xb[j][m] = *reinterpret_cast<const bf16x8*>(xb16[m] + kk * 32);
         }
       }
     }
+  };
+  // the first round's weights and inputs are in flight while the norm scales are formed
+  load_w(kt0);
+  load_x(kt0);
+
+  float rr[MT];
+  if constexpr (NORM) {
+    // Row scales from the per-16-column sums of squares: LPR consecutive lanes per row
+    // each sum a strided subset in order, then a fixed butterfly across the LPR lanes.
+    constexpr int ROWS = MT * 16;
+    constexpr int LPR = TILE_THREADS / ROWS >= 32 ? 32 : (TILE_THREADS / ROWS >= 16 ? 16 : (TILE_THREADS / ROWS >= 8 ? 8 : 4));
+    const int row = threadIdx.x / LPR, part = threadIdx.x % LPR;
+    float t = 0.f;
+    if (row < ROWS) {
+      const float* sp = epi.ssp_in + (int64_t)min(row, M - 1) * epi.nss_in;
+      const int nss = epi.nss_in;
+      for (int i0 = part; i0 < nss; i0 += 8 * LPR) {
+        float v[8];
 #pragma unroll
-    for (int j = 0; j < KC; ++j)
-      if (j < nk)
+        for (int j = 0; j < 8; ++j) v[j] = sp[min(i0 + j * LPR, nss - 1)];   // one batch of loads
 #pragma unroll
-        for (int m = 0; m < MT; ++m) acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], xf[j][m], acc[m], 0, 0, 0);
-  }
-  // Sum the waves' partial tiles in wave order; wave i then finishes 16-row block m0 + i.
+        for (int j = 0; j < 8; ++j)
+          if (i0 + j * LPR < nss) t += v[j];
+      }
+    }
 #pragma unroll
-  for (int m0 = 0; m0 < MT; m0 += MR) {
-#pragma unroll
-    for (int i = 0; i < MR; ++i)
-      if (m0 + i < MT) red[wave][i][lane] = acc[m0 + i < MT ? m0 + i : 0];
+    for (int o = LPR / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, WAVE);
+    if (row < ROWS && part == 0) rscale[row] = row < M ? rsqrtf(t / K + epi.eps) : 0.f;
     __syncthreads();
-    if (wave < MR && m0 + wave < MT) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) rr[m] = rscale[m * 16 + lq];
+  }
+
+  f32x4 acc[NTW][MT];
+#pragma unroll
+  for (int t = 0; t < NTW; ++t)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[t][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c = kt0; c < kt1; c += KC) {
+    const int nk = min(KC, kt1 - c);
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+      if (j < nk) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          bf16x8 x;
+          if constexpr (NORM) {
+            const float4 a = xa[j][m][0], b = xa[j][m][NORM ? 1 : 0];
+            const float r = rr[m];
+            x = __builtin_bit_cast(bf16x8, u16x8{f2bf(a.x * r), f2bf(a.y * r), f2bf(a.z * r), f2bf(a.w * r),
+                                                 f2bf(b.x * r), f2bf(b.y * r), f2bf(b.z * r), f2bf(b.w * r)});
+          } else {
+            x = xb[j][m];
+          }
+#pragma unroll
+          for (int t = 0; t < NTW; ++t) acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j][t], x, acc[t][m], 0, 0, 0);
+        }
+      }
+    }
+    if (c + KC < kt1) {
+      load_w(c + KC);
+      load_x(c + KC);
+    }
+  }
+  // Sum the waves' partial blocks in wave order; wave i then finishes block q0 + i.
+#pragma unroll
+  for (int q0 = 0; q0 < TT; q0 += TR) {
+#pragma unroll
+    for (int i = 0; i < TR; ++i)
+      if (q0 + i < TT) red[wave][i][lane] = acc[(q0 + i) / MT % NTW][(q0 + i) % MT];
+    __syncthreads();
+    if (wave < TR && q0 + wave < TT) {
       f32x4 y = red[0][wave][lane];
 #pragma unroll
       for (int w = 1; w < TILE_WAVES; ++w) {
         const f32x4 v = red[w][wave][lane];
         y = f32x4{y[0] + v[0], y[1] + v[1], y[2] + v[2], y[3] + v[3]};
       }
-      tile_epilogue(epi, y, (m0 + wave) * 16 + lq, g, nt, M, N);
+      const int q = q0 + wave;
+      tile_epilogue(epi, y, (q % MT) * 16 + lq, g, blockIdx.x * NTW + q / MT, M, N);
     }
     __syncthreads();
   }
@@ -310,19 +387,41 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     case EPI_SWIGLU: ADT_CHECK_ARG(epi.act != nullptr, ADT_E_ARG, "gemm: SwiGLU output"); break;
     default: ADT_CHECK_ARG(false, ADT_E_ARG, "gemm: epilogue %d", epi.mode);
   }
-  const dim3 grid(N / 16), block(TILE_THREADS);
   const int mt = (M + 15) / 16;
+  // 16-column tiles per workgroup: each wave's input fragments feed all of them, so more
+  // tiles cut the re-reads of the input rows, but fewer workgroups leave CUs idle.  The
+  // largest of 4, 2, 1 that keeps at least 160 workgroups (measured best on the 36-layer
+  // d = 1280 cycle among 96, 160, 256 and always 1; at most 2 from 81 rows on, for registers)
+  const int tiles = N / 16;
+  int ntw = 1;
+  if (tiles % 4 == 0 && tiles / 4 >= 160 && mt <= 4) ntw = 4;
+  else if (tiles % 2 == 0 && tiles / 2 >= 160) ntw = 2;
+  const dim3 grid(tiles / ntw), block(TILE_THREADS);
   const uint16_t* w = (const uint16_t*)Wp;
 #define ADT_GEMM(...) hipExtLaunchKernelGGL(__VA_ARGS__, grid, block, 0, st, ev0, ev1, 0, X, ldx, w, M, N, K, epi)
-#define ADT_GEMM_ALL(NORM)                                       \
-  switch (mt) {                                                  \
-    case 1: ADT_GEMM(gemm_tile_kernel<1, NORM, 8>); break;       \
-    case 2: ADT_GEMM(gemm_tile_kernel<2, NORM, 8>); break;       \
-    case 3: ADT_GEMM(gemm_tile_kernel<3, NORM, 4>); break;       \
-    case 4: ADT_GEMM(gemm_tile_kernel<4, NORM, 4>); break;       \
-    case 5:                                                      \
-    case 6: ADT_GEMM(gemm_tile_kernel<6, NORM, 2>); break;       \
-    default: ADT_GEMM(gemm_tile_kernel<8, NORM, 2>); break;      \
+#define ADT_GEMM_MT(MT, NORM)                          \
+  if (ntw == 4) {                                      \
+    ADT_GEMM(gemm_tile_kernel<MT, 4, NORM>);           \
+  } else if (ntw == 2) {                               \
+    ADT_GEMM(gemm_tile_kernel<MT, 2, NORM>);           \
+  } else {                                             \
+    ADT_GEMM(gemm_tile_kernel<MT, 1, NORM>);           \
+  }
+#define ADT_GEMM_MT2(MT, NORM)                         \
+  if (ntw >= 2) {                                      \
+    ADT_GEMM(gemm_tile_kernel<MT, 2, NORM>);           \
+  } else {                                             \
+    ADT_GEMM(gemm_tile_kernel<MT, 1, NORM>);           \
+  }
+#define ADT_GEMM_ALL(NORM)             \
+  switch (mt) {                        \
+    case 1: ADT_GEMM_MT(1, NORM) break; \
+    case 2: ADT_GEMM_MT(2, NORM) break; \
+    case 3: ADT_GEMM_MT(3, NORM) break; \
+    case 4: ADT_GEMM_MT(4, NORM) break; \
+    case 5:                            \
+    case 6: ADT_GEMM_MT2(6, NORM) break; \
+    default: ADT_GEMM_MT2(8, NORM) break; \
   }
   if (norm) {
     ADT_GEMM_ALL(true)
@@ -330,6 +429,8 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     ADT_GEMM_ALL(false)
   }
 #undef ADT_GEMM_ALL
+#undef ADT_GEMM_MT2
+#undef ADT_GEMM_MT
 #undef ADT_GEMM
   ADT_LAUNCH_CHECK();
   return ADT_OK;
