@@ -24,6 +24,25 @@ import time
 import numpy as np
 
 HBM_PEAK_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+GEMM_SRC = os.path.join(ROOT, "paper_2512_21857_amd", "csrc", "kernels", "gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_tile_llamagen_xl_traffic.md")
+
+
+def gemm_traffic():
+    """HBM bytes per GEMM launch from the committed FETCH_SIZE / WRITE_SIZE counter summary,
+    or None when the kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+        src = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    keys = ("source_sha256:", "traffic_bytes_per_launch:")
+    fields = dict(line.split(":", 1) for line in text.splitlines() if line.startswith(keys))
+    if fields.get("source_sha256", "").strip() != src:
+        return None
+    return int(fields["traffic_bytes_per_launch"].strip())
 
 
 def parse():
@@ -215,9 +234,9 @@ def main():
                    "tree": "ADT schedule (adjacent init + bisection)",
                    "mean_depth": round(depth / args.steps, 3), "tokens_per_step": round(tokens / args.steps, 3),
                    "nodes_per_step": round(nodes / args.steps, 2)},
-        "roofline": {"bound": "hbm", "kernel": "gemm_bf16 (weight-streaming projections)",
+        "roofline": {"bound": "hbm", "kernel": "gemm_tile_kernel (bf16 projections with fused epilogues)",
                      "achieved": round(gemm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gemm_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(gemm_gbs / HBM_PEAK_GBS, 4), "traffic": gemm_traffic(),
                      "launches": g["launches"], "avg_us": round(gemm_avg_s * 1e6, 3),
                      "bytes_per_launch": round(gemm_bytes)},
         "tree_attn": {"in_cycle_GB_s": round(attn_gbs, 1), "in_cycle_frac": round(attn_gbs / HBM_PEAK_GBS, 4),
