@@ -1,15 +1,18 @@
 // Tree attention (Sec. 3.1): every tree node attends to the committed prefix and to the
 // nodes on its own root-to-node path (the ancestor bitmask).
 //
-// bf16 path: one workgroup per (split of the key range, head, sequence).  K and V tiles of
-// 64 keys are streamed from HBM once per workgroup and staged in LDS (V transposed), all
-// query rows of the tree are held in registers, and both products run on MFMA 16x16x32:
+// bf16 path, many (sequence, head) pairs (the microbenchmark batch): one workgroup per
+// (split of the key range, head, sequence).  K and V tiles of 64 keys are streamed from HBM
+// once per workgroup and staged in LDS (V transposed), all query rows of the tree are held
+// in registers, and both products run on MFMA 16x16x32:
 //   S^T[key][q] = K[key][:] . Q[q][:]        (A = K rows, B = Q^T)
 //   O^T[d][q]  += V^T[d][key] . P^T[key][q]  (A = V^T rows, B = P^T)
 // so each lane owns one query column and the online-softmax rescale is a per-lane scalar.
 // Probabilities enter the second product as three bf16 parts (three MFMAs), so the result
 // is as accurate as fp32 accumulation of the bf16 inputs.
 // Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
+// Few pairs (one image's forwards): tree_attn_wg_kernel below, one workgroup per pair whose
+// waves split the keys and merge in LDS.
 #include "../launch.h"
 
 namespace adt {
@@ -210,6 +213,216 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
   }
 }
 
+// Few (sequence, head) pairs (the verify and draft forwards of one image): one workgroup
+// per pair, its waves each taking a contiguous, balanced slice of the keys
+// (computed on the device from kv_len + n_tail, so no wave idles on an empty split).  Each
+// wave runs the online softmax over its slice for every query tile, double-buffering
+// 32-key K/V steps in registers and transposing V through its own LDS area; the waves'
+// (O, m, l) are then merged in LDS in wave order, so no second kernel and no partials in
+// global memory.  QT = 16-row query tiles held per wave; W = waves per workgroup (8: a
+// 16-wave variant measured slower, its merge and LDS cost outweighing the shorter slices).
+constexpr int AWG_KT = 32;
+
+template <int DH, int QT, int W>
+__global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap,
+    float scale_log2, uint16_t* __restrict__ out) {
+  constexpr int DT = DH / 16, KS = DH / 32;
+  constexpr int VTW = AWG_KT + 8;                          // padded row of a transposed V step
+  constexpr int VP = AWG_KT * DH / 8 / WAVE;               // 16-byte V pieces per lane per step
+  constexpr int VT_BYTES = W * DH * VTW * 2;
+  constexpr int MG_BYTES = W * 16 * (DH + 2) * 4;          // one query tile of (O, m, l) per wave
+  __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
+
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+  const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
+  const int L = kv_len[b];
+  const int nq = min(n_q[b], nq_max);
+  const int total = min(L + n_tail[b], kv_cap);
+  int per = (total + W - 1) / W;
+  per = (per + 15) / 16 * 16;
+  const int k0 = min(total, wave * per), k1 = min(total, k0 + per);
+  const uint16_t* kbase = kc + b * stride_b + h * stride_h;
+  const uint16_t* vbase = vc + b * stride_b + h * stride_h;
+  uint16_t(*Vt)[VTW] = reinterpret_cast<uint16_t(*)[VTW]>(smem + (size_t)wave * DH * VTW * 2);
+
+  bf16x8 qf[QT][KS];
+  uint64_t mw0[QT], mw1[QT];
+  f32x4 o[QT][DT];
+  float m_run[QT], l_run[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+    mw0[t] = mw1[t] = 0;
+#pragma unroll
+    for (int d = 0; d < DT; ++d) o[t][d] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
+    const int qr = t * 16 + lq;
+    if (qr < nq) {
+      const uint16_t* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[t][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
+      const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+      mw0[t] = mp[0];
+      mw1[t] = mp[1];
+    }
+  }
+
+  // K fragments (A operand rows = keys) and V pieces of one 32-key step, keys clamped to
+  // the valid range (keys past the slice are masked out below)
+  bf16x8 kf[2][KS], kn[2][KS];
+  u16x8 vf[VP], vn[VP];
+  auto load_step = [&](int kb, bf16x8 (&kd)[2][KS], u16x8 (&vd)[VP]) {
+    const int last = max(total - 1, 0);
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      const int key = min(kb + sub * 16 + lq, last);
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        kd[sub][kk] = *reinterpret_cast<const bf16x8*>(kbase + (int64_t)key * DH + kk * 32 + g * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < VP; ++j) {
+      const int p = lane + j * WAVE;
+      const int key = min(kb + p / (DH / 8), last);
+      vd[j] = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + (p % (DH / 8)) * 8);
+    }
+  };
+  if (k0 < k1) load_step(k0, kf, vf);
+  for (int kb = k0; kb < k1; kb += AWG_KT) {
+    // this step's V, transposed into the wave's LDS area
+#pragma unroll
+    for (int j = 0; j < VP; ++j) {
+      const int p = lane + j * WAVE;
+      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vf[j][e];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    f32x4 st[QT][2];
+#pragma unroll
+    for (int t = 0; t < QT; ++t)
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        st[t][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+          st[t][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[sub][kk], qf[t][kk], st[t][sub], 0, 0, 0);
+      }
+    const bool more = kb + AWG_KT < k1;
+    if (more) load_step(kb + AWG_KT, kn, vn);
+    // lane (lq, g) holds S for query t*16 + lq and keys kb + sub*16 + 4g + r
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = kb + sub * 16 + 4 * g + r;
+          const bool vis = key < k1 && (key < L || tail_visible(mw0[t], mw1[t], key - L));
+          const float v = vis ? st[t][sub][r] * scale_log2 : -INFINITY;
+          st[t][sub][r] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      const float m_new = fmaxf(m_run[t], mx);
+      const bool none = (m_new == -INFINITY);
+      const float alpha = none ? 1.f : exp2f(m_run[t] - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = none ? 0.f : exp2f(st[t][sub][r] - m_new);
+          st[t][sub][r] = p;
+          rs += p;
+        }
+      rs += __shfl_xor(rs, 16, WAVE);
+      rs += __shfl_xor(rs, 32, WAVE);
+      l_run[t] = l_run[t] * alpha + rs;
+      m_run[t] = m_new;
+#pragma unroll
+      for (int d = 0; d < DT; ++d) o[t][d] *= alpha;
+      // P = P1 + P2 + P3 in bf16 parts (three MFMAs), as accurate as fp32 accumulation
+      bf16x8 p1, p2, p3;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const float pv = r < 4 ? st[t][0][r] : st[t][1][r - 4];
+        const uint16_t b1 = f2bf(pv);
+        const float r1 = pv - bf2f(b1);
+        const uint16_t b2 = f2bf(r1);
+        p1[r] = __builtin_bit_cast(__bf16, b1);
+        p2[r] = __builtin_bit_cast(__bf16, b2);
+        p3[r] = __builtin_bit_cast(__bf16, f2bf(r1 - bf2f(b2)));
+      }
+#pragma unroll
+      for (int d = 0; d < DT; ++d) {
+        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][4 * g]);
+        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][16 + 4 * g]);
+        const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[t][d], 0, 0, 0);
+        o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p2, o[t][d], 0, 0, 0);
+        o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p3, o[t][d], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (more) {
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) kf[sub][kk] = kn[sub][kk];
+#pragma unroll
+      for (int j = 0; j < VP; ++j) vf[j] = vn[j];
+    }
+  }
+
+  // merge the waves' partials query tile by query tile, in wave order
+  float* mo = reinterpret_cast<float*>(smem);                      // [wave][16][DH]
+  float* mml = mo + W * 16 * DH;                                   // [wave][16][2]
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mo[((size_t)wave * 16 + lq) * DH + d * 16 + 4 * g + r] = o[t][d][r];
+    if (g == 0) {
+      mml[((size_t)wave * 16 + lq) * 2] = m_run[t];
+      mml[((size_t)wave * 16 + lq) * 2 + 1] = l_run[t];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 16 * DH; idx += W * WAVE) {
+      const int row = idx / DH, d = idx % DH, qr = t * 16 + row;
+      if (qr >= nq) continue;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < W; ++w) M = fmaxf(M, mml[(w * 16 + row) * 2]);
+      float ls = 0.f, acc = 0.f;
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        const float mw = mml[(w * 16 + row) * 2];
+        if (mw == -INFINITY) continue;
+        const float wt = exp2f(mw - M);
+        ls += wt * mml[(w * 16 + row) * 2 + 1];
+        acc += wt * mo[((size_t)w * 16 + row) * DH + d];
+      }
+      out[(((int64_t)b * nq_max + qr) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
+    }
+    __syncthreads();
+  }
+}
+
 // Log-sum-exp merge of the split partials; one block of DH threads per (query, head, seq).
 // Every split's (m, l) is loaded at once (one lane per split), then the weighted sum of
 // the O partials is taken in split order.
@@ -327,10 +540,16 @@ static AttnPlan attn_plan(int B, int H, int kv_cap) {
   return {splits, chunk};
 }
 
+// The one-workgroup-per-pair kernel serves few (sequence, head) pairs with up to 4 query
+// tiles (2 at head size 128, for registers); larger batches split keys across workgroups.
+static bool attn_use_wg(int B, int H, int Dh, int nq_max) {
+  return B * H <= 64 && nq_max <= (Dh == 64 ? 64 : 32);
+}
+
 // Upper bound over every kv_cap: a plan never uses more than ceil(1024 / (B*H)) splits.
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
   (void)kv_cap;
-  if (dtype == ADT_F32) return 0;
+  if (dtype == ADT_F32 || attn_use_wg(B, H, Dh, nq_max)) return 0;
   int max_splits = (1024 + B * H - 1) / (B * H);
   if (max_splits > ATT_MAX_SPLITS) max_splits = ATT_MAX_SPLITS;
   return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
@@ -339,6 +558,26 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+  if (attn_use_wg(B, H, Dh, nq_max)) {
+    const dim3 grid(H, B);
+    const float sl2 = scale * LOG2E;
+    const int qt = (nq_max + 15) / 16;
+#define ADT_ATTN_WG(DHV, QTV, WV)                                                                                  \
+  tree_attn_wg_kernel<DHV, QTV, WV><<<grid, WV * WAVE, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,             \
+                                                                (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,    \
+                                                                mask, H, nq_max, kv_cap, sl2, (uint16_t*)out)
+    if (Dh == 128) {
+      if (qt <= 1) ADT_ATTN_WG(128, 1, 8);
+      else ADT_ATTN_WG(128, 2, 8);
+    } else {
+      if (qt <= 1) ADT_ATTN_WG(64, 1, 8);
+      else if (qt <= 2) ADT_ATTN_WG(64, 2, 8);
+      else ADT_ATTN_WG(64, 4, 8);
+    }
+#undef ADT_ATTN_WG
+    ADT_LAUNCH_CHECK();
+    return ADT_OK;
+  }
   const AttnPlan p = attn_plan(B, H, kv_cap);
   const size_t need = (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
   ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
