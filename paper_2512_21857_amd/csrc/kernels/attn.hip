@@ -213,48 +213,50 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
   }
 }
 
-// Few (sequence, head) pairs (the verify and draft forwards of one image): one workgroup
-// per pair, its waves each taking a contiguous, balanced slice of the keys
-// (computed on the device from kv_len + n_tail, so no wave idles on an empty split).  Each
-// wave runs the online softmax over its slice for every query tile, double-buffering
-// 32-key K/V steps in registers and transposing V through its own LDS area; the waves'
-// (O, m, l) are then merged in LDS in wave order, so no second kernel and no partials in
-// global memory.  QT = 16-row query tiles held per wave; W = waves per workgroup (8: a
-// 16-wave variant measured slower, its merge and LDS cost outweighing the shorter slices).
+// One workgroup per (sequence, head): its W = QG x KG waves form QG query groups of QTW
+// 16-row query tiles, and each group's KG waves take contiguous, balanced slices of the
+// keys (computed on the device from kv_len + n_tail, so no wave idles on an empty split).
+// Each wave runs the online softmax over its slice for its query tiles, double-buffering
+// 32-key K/V steps in registers; V is transposed through the wave's own LDS area with one
+// 8-byte store per 4 keys of a dimension.  The KG waves of a group are then merged in LDS
+// in wave order, so there is no second kernel and no partials in global memory.
 constexpr int AWG_KT = 32;
+constexpr int AWG_W = 8;
 
-template <int DH, int QT, int W>
-__global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
+template <int DH, int QTW, int QG>
+__global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap,
     float scale_log2, uint16_t* __restrict__ out) {
+  constexpr int KG = AWG_W / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
-  constexpr int VTW = AWG_KT + 8;                          // padded row of a transposed V step
-  constexpr int VP = AWG_KT * DH / 8 / WAVE;               // 16-byte V pieces per lane per step
-  constexpr int VT_BYTES = W * DH * VTW * 2;
-  constexpr int MG_BYTES = W * 16 * (DH + 2) * 4;          // one query tile of (O, m, l) per wave
+  constexpr int VTW = AWG_KT + 4;                          // padded row of a transposed V step (8-byte aligned)
+  constexpr int VG = (AWG_KT / 4) * (DH / 8) / WAVE;       // (4 keys x 8 dims) groups per lane per step
+  constexpr int VT_BYTES = AWG_W * DH * VTW * 2;
+  constexpr int MG_BYTES = AWG_W * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
   const int h = blockIdx.x, b = blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+  const int qg = wave / KG, kg = wave % KG;
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
   const int L = kv_len[b];
   const int nq = min(n_q[b], nq_max);
   const int total = min(L + n_tail[b], kv_cap);
-  int per = (total + W - 1) / W;
+  int per = (total + KG - 1) / KG;
   per = (per + 15) / 16 * 16;
-  const int k0 = min(total, wave * per), k1 = min(total, k0 + per);
+  const int k0 = min(total, kg * per), k1 = min(total, k0 + per);
   const uint16_t* kbase = kc + b * stride_b + h * stride_h;
   const uint16_t* vbase = vc + b * stride_b + h * stride_h;
   uint16_t(*Vt)[VTW] = reinterpret_cast<uint16_t(*)[VTW]>(smem + (size_t)wave * DH * VTW * 2);
 
-  bf16x8 qf[QT][KS];
-  uint64_t mw0[QT], mw1[QT];
-  f32x4 o[QT][DT];
-  float m_run[QT], l_run[QT];
+  bf16x8 qf[QTW][KS];
+  uint64_t mw0[QTW], mw1[QTW];
+  f32x4 o[QTW][DT];
+  float m_run[QTW], l_run[QTW];
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
+  for (int t = 0; t < QTW; ++t) {
     m_run[t] = -INFINITY;
     l_run[t] = 0.f;
     mw0[t] = mw1[t] = 0;
@@ -262,7 +264,7 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
     for (int d = 0; d < DT; ++d) o[t][d] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
-    const int qr = t * 16 + lq;
+    const int qr = (qg * QTW + t) * 16 + lq;
     if (qr < nq) {
       const uint16_t* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
 #pragma unroll
@@ -273,11 +275,11 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
     }
   }
 
-  // K fragments (A operand rows = keys) and V pieces of one 32-key step, keys clamped to
-  // the valid range (keys past the slice are masked out below)
+  // K fragments (A operand rows = keys) and, per lane, VG groups of 4 consecutive keys x 8
+  // dims of V for one 32-key step; keys clamped to the valid range (masked out below)
   bf16x8 kf[2][KS], kn[2][KS];
-  u16x8 vf[VP], vn[VP];
-  auto load_step = [&](int kb, bf16x8 (&kd)[2][KS], u16x8 (&vd)[VP]) {
+  u16x8 vf[VG][4], vn[VG][4];
+  auto load_step = [&](int kb, bf16x8 (&kd)[2][KS], u16x8 (&vd)[VG][4]) {
     const int last = max(total - 1, 0);
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
@@ -287,28 +289,33 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
         kd[sub][kk] = *reinterpret_cast<const bf16x8*>(kbase + (int64_t)key * DH + kk * 32 + g * 8);
     }
 #pragma unroll
-    for (int j = 0; j < VP; ++j) {
-      const int p = lane + j * WAVE;
-      const int key = min(kb + p / (DH / 8), last);
-      vd[j] = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + (p % (DH / 8)) * 8);
+    for (int j = 0; j < VG; ++j) {
+      const int gi = lane + j * WAVE;                      // group: dims c..c+7 of keys 4*r4..4*r4+3
+      const int c = (gi % (DH / 8)) * 8, r4 = gi / (DH / 8);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int key = min(kb + 4 * r4 + u, last);
+        vd[j][u] = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + c);
+      }
     }
   };
   if (k0 < k1) load_step(k0, kf, vf);
   for (int kb = k0; kb < k1; kb += AWG_KT) {
-    // this step's V, transposed into the wave's LDS area
+    // this step's V, transposed into the wave's LDS area: Vt[dim][key]
 #pragma unroll
-    for (int j = 0; j < VP; ++j) {
-      const int p = lane + j * WAVE;
-      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
+    for (int j = 0; j < VG; ++j) {
+      const int gi = lane + j * WAVE;
+      const int c = (gi % (DH / 8)) * 8, r4 = gi / (DH / 8);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vf[j][e];
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<u16x4*>(&Vt[c + e][4 * r4]) = u16x4{vf[j][0][e], vf[j][1][e], vf[j][2][e], vf[j][3][e]};
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    f32x4 st[QT][2];
+    f32x4 st[QTW][2];
 #pragma unroll
-    for (int t = 0; t < QT; ++t)
+    for (int t = 0; t < QTW; ++t)
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
         st[t][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -318,9 +325,9 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
       }
     const bool more = kb + AWG_KT < k1;
     if (more) load_step(kb + AWG_KT, kn, vn);
-    // lane (lq, g) holds S for query t*16 + lq and keys kb + sub*16 + 4g + r
+    // lane (lq, g) holds S for query tile t, row lq and keys kb + sub*16 + 4g + r
 #pragma unroll
-    for (int t = 0; t < QT; ++t) {
+    for (int t = 0; t < QTW; ++t) {
       float mx = -INFINITY;
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
@@ -383,16 +390,18 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) kf[sub][kk] = kn[sub][kk];
 #pragma unroll
-      for (int j = 0; j < VP; ++j) vf[j] = vn[j];
+      for (int j = 0; j < VG; ++j)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) vf[j][u] = vn[j][u];
     }
   }
 
-  // merge the waves' partials query tile by query tile, in wave order
+  // merge the KG waves of each query group, tile by tile, in wave order
   float* mo = reinterpret_cast<float*>(smem);                      // [wave][16][DH]
-  float* mml = mo + W * 16 * DH;                                   // [wave][16][2]
+  float* mml = mo + AWG_W * 16 * DH;                               // [wave][16][2]
   __syncthreads();
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
+  for (int t = 0; t < QTW; ++t) {
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
@@ -402,20 +411,22 @@ __global__ __launch_bounds__(W * WAVE) void tree_attn_wg_kernel(
       mml[((size_t)wave * 16 + lq) * 2 + 1] = l_run[t];
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < 16 * DH; idx += W * WAVE) {
-      const int row = idx / DH, d = idx % DH, qr = t * 16 + row;
+    for (int idx = threadIdx.x; idx < QG * 16 * DH; idx += AWG_W * WAVE) {
+      const int grp = idx / (16 * DH), row = (idx / DH) % 16, d = idx % DH;
+      const int qr = (grp * QTW + t) * 16 + row;
       if (qr >= nq) continue;
+      const int w0 = grp * KG;
       float M = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < W; ++w) M = fmaxf(M, mml[(w * 16 + row) * 2]);
+      for (int w = 0; w < KG; ++w) M = fmaxf(M, mml[((w0 + w) * 16 + row) * 2]);
       float ls = 0.f, acc = 0.f;
 #pragma unroll
-      for (int w = 0; w < W; ++w) {
-        const float mw = mml[(w * 16 + row) * 2];
+      for (int w = 0; w < KG; ++w) {
+        const float mw = mml[((w0 + w) * 16 + row) * 2];
         if (mw == -INFINITY) continue;
         const float wt = exp2f(mw - M);
-        ls += wt * mml[(w * 16 + row) * 2 + 1];
-        acc += wt * mo[((size_t)w * 16 + row) * DH + d];
+        ls += wt * mml[((w0 + w) * 16 + row) * 2 + 1];
+        acc += wt * mo[((size_t)(w0 + w) * 16 + row) * DH + d];
       }
       out[(((int64_t)b * nq_max + qr) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
     }
@@ -540,16 +551,31 @@ static AttnPlan attn_plan(int B, int H, int kv_cap) {
   return {splits, chunk};
 }
 
-// The one-workgroup-per-pair kernel serves few (sequence, head) pairs with up to 4 query
-// tiles (2 at head size 128, for registers); larger batches split keys across workgroups.
-static bool attn_use_wg(int B, int H, int Dh, int nq_max) {
-  return B * H <= 64 && nq_max <= (Dh == 64 ? 64 : 32);
+// Query tiles per wave and query groups of the one-workgroup-per-pair kernel (registers
+// allow 4 tiles of head size 64, 2 of 128); returns false when nq_max does not fit.
+static bool attn_wg_shape(int Dh, int nq_max, int& qtw, int& qg) {
+  const int qt = (nq_max + 15) / 16;
+  const int cap = Dh == 64 ? 4 : 2;
+  qtw = qt < cap ? qt : cap;
+  const int groups = (qt + qtw - 1) / qtw;
+  qg = groups <= 1 ? 1 : (groups <= 2 ? 2 : 4);   // a power of two dividing the 8 waves
+  return groups <= 4;
+}
+
+// One workgroup per (sequence, head) unless there are few pairs and each of their key
+// slices would be long (one image's verify at a long prefix): then the keys are split
+// across workgroups and merged by a second kernel, which brings more CUs to the stream.
+static bool attn_use_wg(int B, int H, int Dh, int nq_max, int kv_cap) {
+  int qtw, qg;
+  if (!attn_wg_shape(Dh, nq_max, qtw, qg)) return false;
+  const int kg = AWG_W / qg;
+  return B * H >= 128 || kv_cap / kg <= 256;
 }
 
 // Upper bound over every kv_cap: a plan never uses more than ceil(1024 / (B*H)) splits.
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
   (void)kv_cap;
-  if (dtype == ADT_F32 || attn_use_wg(B, H, Dh, nq_max)) return 0;
+  if (dtype == ADT_F32) return 0;
   int max_splits = (1024 + B * H - 1) / (B * H);
   if (max_splits > ATT_MAX_SPLITS) max_splits = ATT_MAX_SPLITS;
   return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
@@ -558,21 +584,27 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
-  if (attn_use_wg(B, H, Dh, nq_max)) {
+  if (attn_use_wg(B, H, Dh, nq_max, kv_cap)) {
+    int qtw, qg;
+    attn_wg_shape(Dh, nq_max, qtw, qg);
     const dim3 grid(H, B);
     const float sl2 = scale * LOG2E;
-    const int qt = (nq_max + 15) / 16;
-#define ADT_ATTN_WG(DHV, QTV, WV)                                                                                  \
-  tree_attn_wg_kernel<DHV, QTV, WV><<<grid, WV * WAVE, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,             \
-                                                                (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,    \
-                                                                mask, H, nq_max, kv_cap, sl2, (uint16_t*)out)
+#define ADT_ATTN_WG(DHV, QTWV, QGV)                                                                                \
+  tree_attn_wg_kernel<DHV, QTWV, QGV><<<grid, AWG_W * WAVE, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
+                                                                     (const uint16_t*)v, sb, sh, kv_len, n_q,      \
+                                                                     n_tail, mask, H, nq_max, kv_cap, sl2,         \
+                                                                     (uint16_t*)out)
     if (Dh == 128) {
-      if (qt <= 1) ADT_ATTN_WG(128, 1, 8);
-      else ADT_ATTN_WG(128, 2, 8);
+      if (qtw == 1) ADT_ATTN_WG(128, 1, 1);
+      else if (qg == 1) ADT_ATTN_WG(128, 2, 1);
+      else if (qg == 2) ADT_ATTN_WG(128, 2, 2);
+      else ADT_ATTN_WG(128, 2, 4);
     } else {
-      if (qt <= 1) ADT_ATTN_WG(64, 1, 8);
-      else if (qt <= 2) ADT_ATTN_WG(64, 2, 8);
-      else ADT_ATTN_WG(64, 4, 8);
+      if (qtw == 1) ADT_ATTN_WG(64, 1, 1);
+      else if (qtw == 2) ADT_ATTN_WG(64, 2, 1);
+      else if (qtw == 3) ADT_ATTN_WG(64, 3, 1);
+      else if (qg == 1) ADT_ATTN_WG(64, 4, 1);
+      else ADT_ATTN_WG(64, 4, 2);
     }
 #undef ADT_ATTN_WG
     ADT_LAUNCH_CHECK();

@@ -80,6 +80,14 @@ def test_tree_attn_bf16_head64_ragged_batch(rt):
     assert _attn_case(rt, B=5, H=3, Dh=64, n=61, l_lo=1, l_hi=700, seed=12, vary_n=True) > 0
 
 
+@pytest.mark.parametrize("n", [20, 40, 61])
+def test_tree_attn_bf16_long_prefix_split_keys(rt, n):
+    """Few (sequence, head) pairs over long prefixes (L in [1500, 2000], head size 128): the keys
+    are split across workgroups and merged by the second kernel."""
+    print(f"tree_attn bf16 long prefix n={n}", flush=True)
+    assert _attn_case(rt, B=2, H=4, Dh=128, n=n, l_lo=1500, l_hi=2000, seed=13) == 2 * n
+
+
 def test_tree_attn_bf16_full_microbench_sampled(rt):
     """The 16 x 32 x 128 microbenchmark at its real size (L in [512, 2400], 128 nodes), checked
     on sampled rows including the root, the last node and a deep node of every sequence."""
