@@ -55,6 +55,7 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-microbench", action="store_true")
     ap.add_argument("--no-fixed", action="store_true")
+    ap.add_argument("--no-mfma", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -140,6 +141,42 @@ def attn_microbench(rt, sizes=(8, 16, 32, 64, 128), iters=30, sets=3):
     return out
 
 
+MFMA_PEAK_TFLOPS = 2500.0
+BATCHED_SHAPES = ((4096, 12288), (4096, 4096), (4096, 22016), (11008, 4096), (4096, 65536))
+
+
+def mfma_benchmark(rt, M=976, iters=10):
+    """The verify projections of 16 trees of 61 rows at once (M = 976) with the 7B-shaped
+    layer dimensions (K, N): QKV, O, gate/up, down, LM head.  MFMA-bound (AI >> 315 flop/B)."""
+    import torch
+    torch.manual_seed(5)
+    out, tot_fl, tot_ms = {}, 0.0, 0.0
+    for K, N in BATCHED_SHAPES:
+        x = torch.randn(M, K, device="cuda").bfloat16()
+        w = torch.randn(N, K, device="cuda").bfloat16()
+        c = torch.empty(M, N, dtype=torch.float32, device="cuda")
+        for _ in range(2):
+            rt.gemm_bf16(x, w, out=c)
+        st = torch.cuda.current_stream()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(iters):
+            rt.gemm_bf16(x, w, out=c)
+        e1.record(st)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1) / iters
+        fl = 2.0 * M * N * K
+        tot_fl += fl
+        tot_ms += ms
+        out[f"{K}x{N}"] = {"us": round(ms * 1e3, 1), "TFLOP_s": round(fl / ms / 1e9, 1)}
+        del x, w, c
+    torch.cuda.empty_cache()
+    tf = tot_fl / tot_ms / 1e9
+    return {"M": M, "shapes_KxN": out, "total_us": round(tot_ms * 1e3, 1), "TFLOP_s": round(tf, 1),
+            "peak_TFLOP_s": MFMA_PEAK_TFLOPS, "frac": round(tf / MFMA_PEAK_TFLOPS, 4),
+            "kernel": "gemm_nt_kernel (bf16 MFMA 32x32x16, fp32 out)"}
+
+
 def cpu_baseline(cfg, weights, budget_s):
     """The oracle as it stands, on this host's cores, over the first cycles of the same
     workload (prefill untimed, then as many cycles as fit in the budget)."""
@@ -215,6 +252,7 @@ def main():
     a = prof["attn"]
     attn_gbs = a["bytes"] / (a["ms"] * 1e-3) / 1e9 if a["ms"] > 0 else 0.0
     micro = {} if args.no_microbench else attn_microbench(rt)
+    mfma = None if args.no_mfma else mfma_benchmark(rt)
     line = {
         "metric": "verified draft-tree nodes/sec + tree-attn HBM GB/s (% peak), 1xMI355X",
         "value": round(value, 2),
@@ -242,6 +280,7 @@ def main():
         "tree_attn": {"in_cycle_GB_s": round(attn_gbs, 1), "in_cycle_frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                       "in_cycle_avg_us": round(a["ms"] / max(a["launches"], 1) * 1e3, 3),
                       "microbench_16x32x128": micro},
+        "batched_verify_gemm": mfma,
         "fixed_tree": {"nodes_per_s": round(fnodes / fdt, 2), "ms_per_step": round(fdt / min(args.steps, 50) * 1e3, 4),
                        "nodes_per_step": round(fnodes / min(args.steps, 50), 2), "tree": "depth 6, width 10, top-60"},
     }

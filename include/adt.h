@@ -150,6 +150,17 @@ size_t adt_codebook_knn_workspace_size(int32_t n);
 adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t dim, int32_t k, int32_t* out, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ b3 for a batch of trees
+ * The dense projections of the verification forward (Sec. 3.1) when the rows of several
+ * trees are multiplied together (M = their total, in the hundreds), where the product is
+ * bound by the matrix cores rather than by the weight stream: C[M][N] = X[M][K] . W[N][K]^T.
+ * X, W: device bf16, row-major with K contiguous (leading dimensions ldx, ldw >= K,
+ * multiples of 8 elements); C: device fp32 [M][ldc] (ldc >= N, a multiple of 4).  N must be
+ * a multiple of 128 and K of 64; M >= 1.  Asynchronous on `stream`.  ADT_E_ARG on null
+ * pointers, ADT_E_SHAPE on other shapes; nothing is enqueued on error. */
+adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw, int32_t M, int32_t N, int32_t K,
+                         float* C, int64_t ldc, void* stream);
+
 /* ------------------------------------------------------------------ weights
  * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM
  * kernels stream.  srcs/rows: [host] arrays of n_src device pointers and their row counts.

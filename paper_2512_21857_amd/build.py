@@ -19,6 +19,7 @@ SOURCES = [
     "api.hip",
     "kernels/attn.hip",
     "kernels/gemm.hip",
+    "kernels/gemm_nt.hip",
     "kernels/rows.hip",
     "kernels/select.hip",
     "kernels/small.hip",

@@ -244,6 +244,11 @@ extern "C" adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t
   return launch_codebook_knn(codebook, n, dim, k, out, workspace, workspace_bytes, (hipStream_t)stream);
 }
 
+extern "C" adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw, int32_t M, int32_t N,
+                                    int32_t K, float* C, int64_t ldc, void* stream) {
+  return launch_gemm_nt(X, ldx, W, ldw, M, N, K, C, ldc, (hipStream_t)stream);
+}
+
 extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype) {
   return packed_bytes(total_rows, K, dtype);
 }

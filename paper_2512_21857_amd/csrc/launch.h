@@ -50,6 +50,9 @@ struct GemmEpi {
 // fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the fused kernel, epi.
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
                        const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// gemm_nt.hip: C[M][N] fp32 = X[M][K] . W[N][K]^T, bf16 row-major operands (MFMA-bound batches)
+adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
+                          int64_t ldc, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // rows.hip
 // h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
 // of squares of h into ssp[m][d/16].

@@ -103,6 +103,17 @@ def verify_accept(logits: torch.Tensor, parent: torch.Tensor, token: torch.Tenso
     return path, n_acc, bonus
 
 
+def gemm_bf16(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """x bf16 [M][K], w bf16 [N][K] (rows K-contiguous) -> fp32 [M][N] = x . w^T."""
+    _require_cuda(x, w)
+    assert x.dtype == torch.bfloat16 and w.dtype == torch.bfloat16 and x.stride(1) == 1 and w.stride(1) == 1
+    M, K = x.shape
+    N = w.shape[0]
+    out = torch.empty(M, N, dtype=torch.float32, device=x.device) if out is None else out
+    check(lib().adt_gemm_bf16(_p(x), x.stride(0), _p(w), w.stride(0), M, N, K, _p(out), out.stride(0), _stream()))
+    return out
+
+
 def codebook_knn(codebook: torch.Tensor, k: int) -> torch.Tensor:
     """codebook fp32 [n][dim] -> int32 [n][k]: each code, then its k-1 most cosine-similar codes."""
     _require_cuda(codebook)

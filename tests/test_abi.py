@@ -49,6 +49,11 @@ def test_argument_errors_return_codes_without_launching(L):
     import ctypes as C
     assert L.adt_verify_accept(fake, 16, 16, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake, fake, 1 << 20,
                                None) == abi.E_ARG
+    # batched projection: null operands; N not a multiple of 128, K not of 64, short leading dimension
+    assert L.adt_gemm_bf16(None, 64, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_ARG
+    assert L.adt_gemm_bf16(fake, 64, fake, 64, 8, 100, 64, fake, 128, None) == abi.E_SHAPE
+    assert L.adt_gemm_bf16(fake, 96, fake, 96, 8, 128, 96, fake, 128, None) == abi.E_SHAPE
+    assert L.adt_gemm_bf16(fake, 32, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_SHAPE
     sess = C.c_void_p()
     assert L.adt_session_create(None, None, C.byref(sess)) == abi.E_ARG
     assert L.adt_step(None, None, None) == abi.E_ARG

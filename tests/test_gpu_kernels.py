@@ -263,3 +263,37 @@ def test_accept_sampling_law_on_gpu(rt):
     p /= p.sum()
     chi2 = float(np.sum((counts - trials * p) ** 2 / (trials * p)))
     assert chi2 < 45.0          # 15 dof
+
+
+def _gemm_ref_check(got, x, w, rows):
+    """got[rows] against the fp64 product of the bf16 inputs, within the fp32 accumulation bound
+    2 K eps sum|x_k w_k| per element (eps = 2^-24)."""
+    xf, wf = x[rows].astype(np.float64), w.astype(np.float64)
+    ref = xf @ wf.T
+    bound = 2.0 * x.shape[1] * 2.0 ** -24 * (np.abs(xf) @ np.abs(wf).T) + 1e-30
+    err = np.abs(got[rows] - ref)
+    assert (err <= bound).all(), f"max err {err.max()} (bound there {bound.flat[err.argmax()]})"
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 128, 64), (100, 256, 128), (300, 512, 192), (250, 32768, 128),
+                                   (200, 65536, 64)])
+def test_gemm_bf16_batched(rt, M, N, K):
+    """All three tile shapes (128x128, 256x128, 256x256) and partial row blocks, every element."""
+    print(f"gemm_bf16 M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + N + K)
+    xb = rng.standard_normal((M, K)).astype(np.float32)
+    wb = rng.standard_normal((N, K)).astype(np.float32)
+    xt = torch.from_numpy(xb).cuda().bfloat16()
+    wt = torch.from_numpy(wb).cuda().bfloat16()
+    got = rt.gemm_bf16(xt, wt).cpu().numpy()
+    _gemm_ref_check(got, xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
+
+
+def test_gemm_bf16_batched_verify_shape_sampled(rt):
+    """M = 976 (16 trees of 61 rows) against a 4096 x 4096 projection, on sampled rows."""
+    rng = np.random.default_rng(976)
+    xt = torch.from_numpy(rng.standard_normal((976, 4096)).astype(np.float32)).cuda().bfloat16()
+    wt = torch.from_numpy(rng.standard_normal((4096, 4096)).astype(np.float32)).cuda().bfloat16()
+    got = rt.gemm_bf16(xt, wt).cpu().numpy()
+    rows = np.array([0, 1, 31, 32, 255, 256, 511, 767, 768, 900, 975])
+    _gemm_ref_check(got, xt.float().cpu().numpy(), wt.float().cpu().numpy(), rows)
