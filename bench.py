@@ -119,7 +119,7 @@ def attn_microbench(rt, sizes=(8, 16, 32, 64, 128), iters=30, sets=3):
         ws = torch.empty(2 * rt.lib().adt_tree_attn_workspace_size(16, 32, 128, n, 4096) + 256, dtype=torch.uint8,
                          device="cuda")
         outs = [torch.empty_like(b[0]) for b in bufs]
-        for i in range(3):
+        for i in range(10):
             b = bufs[i % sets]
             rt.tree_attn(b[0], b[1], b[2], b[3], b[4], b[4], b[5], b[6], out=outs[i % sets], workspace=ws)
         st = torch.cuda.current_stream()
