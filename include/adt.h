@@ -56,6 +56,18 @@ typedef int32_t adt_status;
 #define ADT_ALPHA_REAL 0
 #define ADT_ALPHA_POISSON 1
 
+/* Initial tree attributes (d~, k~) of a cycle (Sec. 4.1 and the alternatives of Sec. 5.3) */
+#define ADT_INIT_HORIZONTAL 0   /* the record of the left cell (i, j-1) */
+#define ADT_INIT_VERTICAL 1     /* the record of the cell above (i-1, j) */
+#define ADT_INIT_RANDOM 2       /* uniform over the depth and width bounds */
+#define ADT_INIT_TOKENFLOCK 3   /* weighted mean over recorded cells within radius delta (Eqs. 6-8) */
+
+/* Width bounds after Eq. 2 (Sec. 4.2) */
+#define ADT_KCLAMP_ALWAYS 0     /* k_hat always clamped to [k_lo, k_hi] */
+#define ADT_KCLAMP_DEEP 1       /* clamped only when the adapted depth d~ +- l_d exceeds 1; a
+                                   one-layer tree keeps k_hat in [1, ADT_MAX_WIDTH] */
+#define ADT_MAX_WIDTH 16        /* widest top-k of one expansion layer */
+
 int32_t adt_version(void);
 /* Copies the last error message of this thread into buf (NUL-terminated, truncated to cap);
  * returns its full length. */
@@ -182,12 +194,25 @@ adt_status adt_pack_weight(const void* const* srcs, const int32_t* rows, int32_t
                            int32_t group, int32_t dtype, void* dst, void* stream);
 
 /* ------------------------------------------------------------------ a0: schedule (host)
- * Adjacent initialisation (Sec. 4.1, Horizontal Repeat) + bisectional adaptation
- * (Sec. 4.2, Eq. 2) + the bounds of Sec. 4.2, as inclusive ranges.
- * have_left: whether the left neighbour cell has a recorded (d, k); have_prev: whether a
- * previous tree exists, with a_prev accepted draft tokens at depth d_prev; remaining =
- * image tokens still to commit including this cycle's bonus.  Writes (d_hat, k_hat);
- * d_hat = 0 means a plain AR step. */
+ * A cycle's tree shape is found in two phases (Sec. 4): an initial (d~, k~) from the records
+ * of committed cells (adt_schedule_init, Sec. 4.1 and Sec. 5.3), then the bisectional
+ * adaptation of Eq. 2 and the bounds of Sec. 4.2 (adt_schedule_next).
+ *
+ * The record of an image cell is the (d_hat, k_hat) of the tree whose cycle committed it;
+ * cells are numbered in raster order, cell = i * grid_w + j.  Rules (init_mode):
+ *   HORIZONTAL: the record of cell - 1 (the raster predecessor at j = 0).
+ *   VERTICAL:   the record of cell - grid_w; in the first row, or where that cell has no
+ *               record, the HORIZONTAL value.
+ *   RANDOM:     d~ = d_lo + floor(U0 * (d_hi - d_lo + 1) / 2^64),
+ *               k~ = k_lo + floor(U1 * (k_hi - k_lo + 1) / 2^64), where (x0..x3) =
+ *               Philox4x32-10(key = seed, counter = (cell, 0, 0, 1)), U0 = x1 << 32 | x0 and
+ *               U1 = x3 << 32 | x2; every cycle, the first included.
+ *   TOKENFLOCK: over the recorded cells c < cell with (dx^2 + dy^2) <= delta^2 (x = column,
+ *               y = row), weights w = delta + 1 - dy normalised to sum 1; d~ and k~ are the
+ *               weighted means rounded half up.
+ * With no source (no record yet, or an empty TOKENFLOCK set) the tree starts from (d0, k0)
+ * and skips Eq. 2.  fix_d / fix_k > 0 replace d~ / k~ by that constant (the fixed-base
+ * ablations of Table V), the first tree included. */
 typedef struct {
   int32_t d_lo, d_hi, k_lo, k_hi; /* inclusive bounds */
   int32_t l_d, l_k;               /* adjustment steps of Eq. 2 */
@@ -195,8 +220,28 @@ typedef struct {
   int32_t n_budget;               /* draft nodes kept by the top-N rerank (Eq. 3) */
   int32_t d0, k0;                 /* first tree */
   int32_t alpha_source;           /* ADT_ALPHA_REAL or ADT_ALPHA_POISSON */
+  int32_t init_mode;              /* ADT_INIT_* */
+  int32_t grid_w;                 /* cells per grid row; >= 1 for VERTICAL and TOKENFLOCK */
+  int32_t flock_delta;            /* TOKENFLOCK radius, >= 1 */
+  int32_t fix_d, fix_k;           /* fixed initial depth / width, 0 = none */
+  int32_t k_clamp;                /* ADT_KCLAMP_ALWAYS or ADT_KCLAMP_DEEP (needs d_lo = 1) */
+  uint64_t seed;                  /* RANDOM key */
 } adt_sched_cfg;
 
+/* Initial (d~, k~) of the cycle whose first drafted token is image cell `cell`.
+ * rec_d, rec_k, has_rec: [host] [n_cells] records (only entries below `cell` are read).
+ * Writes have_init = 0 (start from (d0, k0) without adaptation) or 1 with (d_init, k_init).
+ * ADT_E_ARG on null pointers, a cell outside [0, n_cells) or an invalid rule setting. */
+adt_status adt_schedule_init(const adt_sched_cfg* cfg, int32_t cell, int32_t n_cells, const int32_t* rec_d,
+                             const int32_t* rec_k, const int32_t* has_rec, int32_t* have_init, int32_t* d_init,
+                             int32_t* k_init);
+
+/* Eq. 2 and the bounds.  have_left: whether an initial value (d_left, k_left) exists (from
+ * adt_schedule_init; 0 = start from (d0, k0) and skip Eq. 2); have_prev: whether a previous
+ * tree exists, with a_prev accepted draft tokens at depth d_prev (alpha = a_prev / d_prev,
+ * positive iff alpha >= beta); remaining = image tokens still to commit including this
+ * cycle's bonus.  The depth is clamped to [d_lo, d_hi] and then cut to remaining - 1; the
+ * width per k_clamp.  Writes (d_hat, k_hat); d_hat = 0 means a plain AR step. */
 adt_status adt_schedule_next(const adt_sched_cfg* cfg, int32_t have_left, int32_t d_left, int32_t k_left,
                              int32_t have_prev, int32_t a_prev, int32_t d_prev, int32_t remaining, int32_t* d_hat,
                              int32_t* k_hat);

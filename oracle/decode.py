@@ -31,7 +31,7 @@ from .attention import tree_key_slots
 from .expand import Tree, build_tree, expand
 from .model import OracleModel
 from .numerics import draw_below, masked_logits, uniform_u64
-from .schedule import schedule
+from .schedule import initial, schedule
 from .tree import ancestors_and_self
 
 
@@ -183,7 +183,8 @@ class Decoder:
         prev = self.prev
         if prev is not None and self.cfg.sched.alpha_source == "poisson" and self.poisson is not None:
             prev = (min(int(self.poisson[self.prev_cell]), prev[1]), prev[1])
-        return schedule(self.cfg.sched, self.records.get(cell - 1), prev, remaining)
+        init = initial(self.cfg.sched, cell, self.records, self.cfg.grid_w)
+        return schedule(self.cfg.sched, init, prev, remaining)
 
     def compact(self, path: List[int]):
         compact_cache(self.tcache.k, self.tcache.v, self.L, path)

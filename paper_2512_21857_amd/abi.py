@@ -20,6 +20,9 @@ MASK_WORDS = 2
 ACCEPT_GREEDY, ACCEPT_EXACT, ACCEPT_RELAXED = 0, 1, 2
 PACK_STACK, PACK_GATE_UP, PACK_QKV = 0, 1, 2
 ALPHA_REAL, ALPHA_POISSON = 0, 1
+INIT_HORIZONTAL, INIT_VERTICAL, INIT_RANDOM, INIT_TOKENFLOCK = 0, 1, 2, 3
+KCLAMP_ALWAYS, KCLAMP_DEEP = 0, 1
+MAX_WIDTH = 16
 
 p = C.c_void_p
 i32 = C.c_int32
@@ -37,7 +40,9 @@ class AcceptCfg(C.Structure):
 
 class SchedCfg(C.Structure):
     _fields_ = [("d_lo", i32), ("d_hi", i32), ("k_lo", i32), ("k_hi", i32), ("l_d", i32), ("l_k", i32),
-                ("beta", f32), ("n_budget", i32), ("d0", i32), ("k0", i32), ("alpha_source", i32)]
+                ("beta", f32), ("n_budget", i32), ("d0", i32), ("k0", i32), ("alpha_source", i32),
+                ("init_mode", i32), ("grid_w", i32), ("flock_delta", i32), ("fix_d", i32), ("fix_k", i32),
+                ("k_clamp", i32), ("seed", u64)]
 
 
 class ModelDesc(C.Structure):
@@ -81,6 +86,7 @@ _SIGS = {
     "adt_packed_bytes": (sz, [i32, i32, i32]),
     "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, i32, p, p]),
     "adt_schedule_next": (i32, [C.POINTER(SchedCfg), i32, i32, i32, i32, i32, i32, i32, ip, ip]),
+    "adt_schedule_init": (i32, [C.POINTER(SchedCfg), i32, i32, ip, ip, ip, ip, ip, ip]),
     "adt_model_create": (i32, [C.POINTER(ModelDesc), C.POINTER(p)]),
     "adt_model_destroy": (None, [p]),
     "adt_session_workspace_size": (sz, [p, C.POINTER(SessionDesc)]),

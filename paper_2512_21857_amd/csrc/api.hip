@@ -22,6 +22,12 @@ void set_error(const char* fmt, ...) {
   va_end(ap);
 }
 
+#define TRY(x)                \
+  do {                        \
+    adt_status e__ = (x);     \
+    if (e__ != ADT_OK) return e__; \
+  } while (0)
+
 static inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct Bump {
@@ -259,12 +265,100 @@ extern "C" adt_status adt_pack_weight(const void* const* srcs, const int32_t* ro
   return launch_pack(srcs, rows, n_src, K, mode, group, dtype, dst, (hipStream_t)stream);
 }
 
+static adt_status check_sched_cfg(const adt_sched_cfg* c) {
+  ADT_CHECK_ARG(c->d_lo >= 1 && c->d_lo <= c->d_hi && c->k_lo >= 1 && c->k_lo <= c->k_hi, ADT_E_ARG,
+                "schedule: bad bounds");
+  ADT_CHECK_ARG(c->init_mode >= ADT_INIT_HORIZONTAL && c->init_mode <= ADT_INIT_TOKENFLOCK, ADT_E_ARG,
+                "schedule: init_mode %d", c->init_mode);
+  ADT_CHECK_ARG(c->grid_w >= 1 || (c->init_mode != ADT_INIT_VERTICAL && c->init_mode != ADT_INIT_TOKENFLOCK),
+                ADT_E_ARG, "schedule: grid_w %d", c->grid_w);
+  ADT_CHECK_ARG(c->flock_delta >= 1 || c->init_mode != ADT_INIT_TOKENFLOCK, ADT_E_ARG, "schedule: flock_delta %d",
+                c->flock_delta);
+  ADT_CHECK_ARG(c->fix_d >= 0 && c->fix_k >= 0, ADT_E_ARG, "schedule: fixed bases");
+  ADT_CHECK_ARG(c->k_clamp == ADT_KCLAMP_ALWAYS || (c->k_clamp == ADT_KCLAMP_DEEP && c->d_lo == 1), ADT_E_ARG,
+                "schedule: k_clamp %d (the deep-only rule needs d_lo = 1)", c->k_clamp);
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_schedule_init(const adt_sched_cfg* c, int32_t cell, int32_t n_cells, const int32_t* rec_d,
+                                        const int32_t* rec_k, const int32_t* has_rec, int32_t* have_init,
+                                        int32_t* d_init, int32_t* k_init) {
+  ADT_CHECK_ARG(c && rec_d && rec_k && has_rec && have_init && d_init && k_init, ADT_E_ARG,
+                "schedule_init: null pointer");
+  ADT_CHECK_ARG(cell >= 0 && cell < n_cells, ADT_E_ARG, "schedule_init: cell %d of %d", cell, n_cells);
+  TRY(check_sched_cfg(c));
+  int have = 0, d = 0, k = 0;
+  auto take = [&](int g) {
+    if (g >= 0 && g < cell && has_rec[g]) {
+      have = 1;
+      d = rec_d[g];
+      k = rec_k[g];
+    }
+  };
+  switch (c->init_mode) {
+    case ADT_INIT_HORIZONTAL:
+      take(cell - 1);
+      break;
+    case ADT_INIT_VERTICAL:
+      take(cell - c->grid_w);
+      if (!have) take(cell - 1);
+      break;
+    case ADT_INIT_RANDOM: {
+      // two 64-bit draws from one Philox block; floor(U * span / 2^64) as a 128-bit product
+      uint32_t x[4] = {(uint32_t)cell, 0u, 0u, 1u};
+      philox4x32_10(x, (uint32_t)c->seed, (uint32_t)(c->seed >> 32));
+      const uint64_t u0 = ((uint64_t)x[1] << 32) | x[0], u1 = ((uint64_t)x[3] << 32) | x[2];
+      const uint64_t sd = (uint64_t)(c->d_hi - c->d_lo + 1), sk = (uint64_t)(c->k_hi - c->k_lo + 1);
+      d = c->d_lo + (int)(((unsigned __int128)u0 * sd) >> 64);
+      k = c->k_lo + (int)(((unsigned __int128)u1 * sk) >> 64);
+      have = 1;
+      break;
+    }
+    case ADT_INIT_TOKENFLOCK: {
+      // Eqs. 6-8: only rows y - delta .. y and columns x - delta .. x + delta can lie within
+      // the radius; the 1/delta of the weights cancels in the normalisation.
+      const int W = c->grid_w, R2 = c->flock_delta * c->flock_delta;
+      const int y = cell / W, x = cell % W;
+      int64_t sw = 0, swd = 0, swk = 0;
+      for (int dy = 0; dy <= c->flock_delta && dy <= y; ++dy)
+        for (int dx = -c->flock_delta; dx <= c->flock_delta; ++dx) {
+          const int xx = x + dx;
+          if (xx < 0 || xx >= W || dx * dx + dy * dy > R2) continue;
+          const int g = (y - dy) * W + xx;
+          if (g >= cell || !has_rec[g]) continue;
+          const int64_t w = c->flock_delta + 1 - dy;
+          sw += w;
+          swd += w * rec_d[g];
+          swk += w * rec_k[g];
+        }
+      if (sw > 0) {
+        have = 1;
+        d = (int)((2 * swd + sw) / (2 * sw));   // round half up of swd / sw (all terms >= 0)
+        k = (int)((2 * swk + sw) / (2 * sw));
+      }
+      break;
+    }
+  }
+  if (c->fix_d > 0 || c->fix_k > 0) {
+    if (!have) {
+      d = c->d0;
+      k = c->k0;
+      have = 1;
+    }
+    if (c->fix_d > 0) d = c->fix_d;
+    if (c->fix_k > 0) k = c->fix_k;
+  }
+  *have_init = have;
+  *d_init = have ? d : 0;
+  *k_init = have ? k : 0;
+  return ADT_OK;
+}
+
 extern "C" adt_status adt_schedule_next(const adt_sched_cfg* c, int32_t have_left, int32_t d_left, int32_t k_left,
                                         int32_t have_prev, int32_t a_prev, int32_t d_prev, int32_t remaining,
                                         int32_t* d_hat, int32_t* k_hat) {
   ADT_CHECK_ARG(c && d_hat && k_hat, ADT_E_ARG, "schedule: null pointer");
-  ADT_CHECK_ARG(c->d_lo >= 1 && c->d_lo <= c->d_hi && c->k_lo >= 1 && c->k_lo <= c->k_hi, ADT_E_ARG,
-                "schedule: bad bounds");
+  TRY(check_sched_cfg(c));
   ADT_CHECK_ARG(remaining >= 1, ADT_E_ARG, "schedule: nothing remains");
   int d, k;
   if (!have_left) {
@@ -284,8 +378,11 @@ extern "C" adt_status adt_schedule_next(const adt_sched_cfg* c, int32_t have_lef
       }
     }
   }
+  if (c->k_clamp == ADT_KCLAMP_DEEP && d <= 1)
+    k = std::max(1, std::min(ADT_MAX_WIDTH, k));
+  else
+    k = std::max(c->k_lo, std::min(c->k_hi, k));
   d = std::max(c->d_lo, std::min(c->d_hi, d));
-  k = std::max(c->k_lo, std::min(c->k_hi, k));
   d = std::min(d, remaining - 1);
   *d_hat = d;
   *k_hat = k;
@@ -401,8 +498,10 @@ static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_sessi
   s->C0 = dh + 2;
   s->DR = s->C0 + std::max(1, (dh - 1) * kh);
   s->DLR = 1 + std::max(0, (dh - 1) * kh);
+  // a one-layer tree may be as wide as ADT_MAX_WIDTH under the deep-only width clamp
+  const int kw = d->sched.k_clamp == ADT_KCLAMP_DEEP ? ADT_MAX_WIDTH : kh;
   s->KR = std::max(kh, 1);
-  s->C = std::max(1, kh + (dh - 1) * kh * kh);
+  s->C = std::max(kw, kh + (dh - 1) * kh * kh);
   // fp32 projections write [rows][N] products for the row kernels; bf16 ones finish in place
   size_t pe = 256;
   if (s->dt == ADT_F32)
@@ -482,7 +581,7 @@ static adt_status check_session_desc(const adt_model* m, const adt_session_desc*
   ADT_CHECK_ARG(d->k_cache && d->v_cache && d->dk_cache && d->dv_cache && d->allowed, ADT_E_ARG,
                 "session: caches / allowed table missing");
   const adt_sched_cfg& c = d->sched;
-  ADT_CHECK_ARG(c.d_lo >= 1 && c.d_lo <= c.d_hi && c.k_lo >= 1 && c.k_lo <= c.k_hi, ADT_E_ARG, "session: bounds");
+  TRY(check_sched_cfg(&c));
   ADT_CHECK_ARG(c.d_hi <= 30 && c.k_hi <= 16, ADT_E_UNSUPPORTED, "session: d_hi <= 30 and k_hi <= 16 supported");
   ADT_CHECK_ARG(c.n_budget >= 1 && c.n_budget <= R - 1, ADT_E_CAPACITY, "session: n_budget %d", c.n_budget);
   ADT_CHECK_ARG((c.d_hi - 1) * c.k_hi <= R, ADT_E_CAPACITY, "session: draft tree rows exceed %d", R);
@@ -538,12 +637,6 @@ extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_d
 }
 
 extern "C" void adt_session_destroy(adt_session* s) { delete s; }
-
-#define TRY(x)                \
-  do {                        \
-    adt_status e__ = (x);     \
-    if (e__ != ADT_OK) return e__; \
-  } while (0)
 
 static SmallI32 small_of(const int32_t* v, int n) {
   SmallI32 s{};
@@ -802,7 +895,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "tree_expand: null session");
   ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "tree_expand: session not prefilled");
   const adt_sched_cfg& c = s->d.sched;
-  ADT_CHECK_ARG(d_hat >= 1 && d_hat <= c.d_hi && k_hat >= 1 && k_hat <= c.k_hi, ADT_E_ARG,
+  const int k_top = (c.k_clamp == ADT_KCLAMP_DEEP && d_hat == 1) ? ADT_MAX_WIDTH : c.k_hi;
+  ADT_CHECK_ARG(d_hat >= 1 && d_hat <= c.d_hi && k_hat >= 1 && k_hat <= k_top, ADT_E_ARG,
                 "tree_expand: (d,k)=(%d,%d) outside the session bounds", d_hat, k_hat);
   ADT_CHECK_ARG(n_budget >= 1 && n_budget <= R - 1, ADT_E_CAPACITY, "tree_expand: n_budget %d", n_budget);
   const int L = s->L, Ld = s->Ld, P = s->P;
@@ -972,20 +1066,20 @@ extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, i
   return ADT_OK;
 }
 
-static void schedule_for(adt_session_s* s, int& d_hat, int& k_hat) {
+static adt_status schedule_for(adt_session_s* s, int& d_hat, int& k_hat) {
   const adt_sched_cfg& c = s->d.sched;
   const int cell = s->L + 1 - s->P;
   const int remaining = s->T - cell;
   if (s->d.fixed_tree) {
     d_hat = std::min(c.d_hi, remaining - 1);
     k_hat = c.k_hi;
-    return;
+    return ADT_OK;
   }
-  const int have_left = (cell >= 1 && s->has_rec[cell - 1]) ? 1 : 0;
+  int have = 0, d0 = 0, k0 = 0;
+  TRY(adt_schedule_init(&c, cell, s->T, s->rec_d.data(), s->rec_k.data(), s->has_rec.data(), &have, &d0, &k0));
   int a_prev = s->a_prev;
   if (c.alpha_source == ADT_ALPHA_POISSON && s->have_prev) a_prev = std::min(s->poisson[s->prev_cell], s->d_prev);
-  adt_schedule_next(&c, have_left, have_left ? s->rec_d[cell - 1] : 0, have_left ? s->rec_k[cell - 1] : 0,
-                    s->have_prev ? 1 : 0, a_prev, s->d_prev, remaining, &d_hat, &k_hat);
+  return adt_schedule_next(&c, have, d0, k0, s->have_prev ? 1 : 0, a_prev, s->d_prev, remaining, &d_hat, &k_hat);
 }
 
 extern "C" adt_status adt_step(adt_session* s, adt_step_out* out, void* stream) {
@@ -1000,7 +1094,7 @@ extern "C" adt_status adt_step(adt_session* s, adt_step_out* out, void* stream) 
     return ADT_OK;
   }
   int d_hat = 0, k_hat = 0;
-  schedule_for(s, d_hat, k_hat);
+  TRY(schedule_for(s, d_hat, k_hat));
   if (d_hat >= 1) {
     TRY(adt_tree_expand(s, d_hat, k_hat, s->d.sched.n_budget, nullptr, st));
   } else {

@@ -35,6 +35,24 @@ template <> struct Elem<uint16_t> {
   __device__ static __forceinline__ void store(uint16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
 };
 
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds over counter (c0..c3) with key (k0, k1);
+// host and device share it (acceptance draws on the GPU, the Random tree initialisation on
+// the host).
+__host__ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0, n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = (uint32_t)p1;
+    c[2] = n2;
+    c[3] = (uint32_t)p0;
+    k0 += W0;
+    k1 += W1;
+  }
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);

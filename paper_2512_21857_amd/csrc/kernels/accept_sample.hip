@@ -20,23 +20,6 @@ namespace adt {
 constexpr int AS_THREADS = 1024;
 constexpr int AS_DELTA_BITS = 16;
 
-// Philox4x32-10 (Salmon et al., SC'11): counter (c0..c3), key (k0, k1).
-__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
-  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
-    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
-    const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-    c[0] = n0;
-    c[1] = lo1;
-    c[2] = n2;
-    c[3] = lo0;
-    k0 += W0;
-    k1 += W1;
-  }
-}
-
 __device__ __forceinline__ uint64_t draw_below(uint64_t seed, uint32_t step, uint32_t node, uint32_t trial,
                                                uint64_t W) {
   uint32_t c[4] = {step, node, trial, 0u};

@@ -134,9 +134,29 @@ def schedule_next(sched: abi.SchedCfg, left, prev, remaining: int):
     return d.value, k.value
 
 
-def sched_struct(s) -> abi.SchedCfg:
+INIT_MODES = {"horizontal": abi.INIT_HORIZONTAL, "vertical": abi.INIT_VERTICAL, "random": abi.INIT_RANDOM,
+              "tokenflock": abi.INIT_TOKENFLOCK}
+K_CLAMPS = {"always": abi.KCLAMP_ALWAYS, "deep": abi.KCLAMP_DEEP}
+
+
+def schedule_init(sched: abi.SchedCfg, cell: int, records: dict, n_cells: int):
+    """Host-only initial (d~, k~) of the cycle starting at `cell` from records {cell: (d, k)};
+    None = no source (the first tree's (d0, k0) without adaptation)."""
+    rd = (C.c_int32 * n_cells)()
+    rk = (C.c_int32 * n_cells)()
+    hr = (C.c_int32 * n_cells)()
+    for g, (d, k) in records.items():
+        rd[g], rk[g], hr[g] = d, k, 1
+    have, d, k = C.c_int32(), C.c_int32(), C.c_int32()
+    check(lib().adt_schedule_init(C.byref(sched), cell, n_cells, rd, rk, hr, C.byref(have), C.byref(d), C.byref(k)))
+    return (d.value, k.value) if have.value else None
+
+
+def sched_struct(s, grid_w: int = 0) -> abi.SchedCfg:
     src = abi.ALPHA_POISSON if getattr(s, "alpha_source", "real") == "poisson" else abi.ALPHA_REAL
-    return abi.SchedCfg(s.d_lo, s.d_hi, s.k_lo, s.k_hi, s.l_d, s.l_k, s.beta, s.n_budget, s.d0, s.k0, src)
+    return abi.SchedCfg(s.d_lo, s.d_hi, s.k_lo, s.k_hi, s.l_d, s.l_k, s.beta, s.n_budget, s.d0, s.k0, src,
+                        INIT_MODES[s.init], grid_w, s.flock_delta, s.fix_d, s.fix_k, K_CLAMPS[s.k_clamp],
+                        s.seed & (2 ** 64 - 1))
 
 
 # ============================================================================ model + session
@@ -223,7 +243,7 @@ class DeviceSession:
                                  cfg.seed if accept_seed is None else accept_seed)
         desc = abi.SessionDesc(cfg.prefix_len, cfg.n_image, self.s_cap, _p(self.k_cache), _p(self.v_cache),
                                _p(self.dk_cache), _p(self.dv_cache),
-                               C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched), self.accept,
+                               C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched, cfg.grid_w), self.accept,
                                C.cast(self._poisson, C.POINTER(C.c_int32)) if self._poisson is not None else None,
                                1 if fixed_tree else 0, _p(draft_table),
                                0 if draft_table is None else draft_table.shape[0], 1 if use_graphs else 0, None, 0)

@@ -53,6 +53,12 @@ class SchedCfg:
     d0: int                # tree of the first step (no neighbour yet)
     k0: int
     alpha_source: str = "real"   # "real" | "poisson"
+    init: str = "horizontal"     # initial (d~, k~): "horizontal" | "vertical" | "random" | "tokenflock"
+    flock_delta: int = 2         # TokenFlock radius in grid cells
+    fix_d: int = 0               # fixed initial depth (Table V ablations), 0 = none
+    fix_k: int = 0               # fixed initial width, 0 = none
+    k_clamp: str = "always"      # "always" | "deep": width bounds only when the adapted depth exceeds 1
+    seed: int = 0                # key of the Random initialisation
 
 
 @dataclasses.dataclass(frozen=True)

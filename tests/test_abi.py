@@ -1,10 +1,12 @@
 """The C ABI on the CPU: libadt.so loads, exports every entry point declared in
 include/adt.h, validates arguments before launching anything, and its host-only schedule
 matches the oracle's (Sec. 4.1-4.2, Eq. 2)."""
+import ctypes as C
 import json
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -80,3 +82,48 @@ def test_schedule_matches_oracle(L):
                 if left is None and prev is not None:
                     continue
                 assert runtime.schedule_next(s, left, prev, rem) == schedule(sc, left, prev, rem)
+
+
+@pytest.mark.parametrize("rule", ["horizontal", "vertical", "random", "tokenflock", "fixed", "deep"])
+def test_schedule_init_rules_match_oracle(L, rule):
+    """adt_schedule_init + adt_schedule_next against the oracle's initial() + schedule() over
+    random record tables (Sec. 4.1, Sec. 5.3 Eqs. 6-8, Table V, Sec. 4.2)."""
+    import dataclasses
+    from paper_2512_21857_amd import runtime
+    from synth import SchedCfg
+    from oracle.schedule import initial, schedule
+    rng = np.random.default_rng(5)
+    W, n = 7, 70
+    base = SchedCfg(1, 6, 4, 10, 1, 10, 1.0, 60, 5, 10)
+    kw = {"fixed": dict(fix_d=1, fix_k=25), "deep": dict(k_clamp="deep", init="vertical")}.get(rule, {"init": rule})
+    for delta in ((1, 2, 3) if rule == "tokenflock" else (2,)):
+        sc = dataclasses.replace(base, flock_delta=delta, seed=99, **kw)
+        s = runtime.sched_struct(sc, W)
+        for trial in range(40):
+            cell = int(rng.integers(0, n))
+            recs = {g: (int(rng.integers(0, 12)), int(rng.integers(0, 20)))
+                    for g in range(1, n) if rng.random() < 0.8}
+            init = runtime.schedule_init(s, cell, recs, n)
+            assert init == initial(sc, cell, {g: r for g, r in recs.items() if g < cell}, W), (rule, cell)
+            for prev in (None, (0, 2), (3, 3), (1, 1)):
+                for rem in (1, 3, 50):
+                    assert runtime.schedule_next(s, init, prev, rem) == schedule(sc, init, prev, rem)
+
+
+def test_schedule_init_rejects_bad_settings(L):
+    import dataclasses
+    from paper_2512_21857_amd import runtime, abi
+    from synth import SchedCfg
+    base = SchedCfg(1, 6, 4, 10, 1, 10, 1.0, 60, 5, 10)
+    rd = (C.c_int32 * 4)()
+    out = [C.c_int32() for _ in range(3)]
+    for kw, w in ((dict(init="vertical"), 0), (dict(init="tokenflock", flock_delta=0), 4),
+                  (dict(k_clamp="deep", d_lo=2), 4), (dict(fix_d=-1), 4)):
+        s = runtime.sched_struct(dataclasses.replace(base, **kw), w)
+        assert L.adt_schedule_init(C.byref(s), 1, 4, rd, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG
+    s = runtime.sched_struct(base, 4)
+    s.init_mode = 7
+    assert L.adt_schedule_init(C.byref(s), 1, 4, rd, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG
+    s.init_mode = abi.INIT_HORIZONTAL
+    assert L.adt_schedule_init(C.byref(s), 4, 4, rd, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG
+    assert L.adt_schedule_init(C.byref(s), 0, 4, None, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG

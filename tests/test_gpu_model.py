@@ -48,8 +48,9 @@ def _greedy_margin(row, lo, hi):
     return seg[-1] - seg[-2] if len(seg) > 1 else np.inf
 
 
-def _compare_run(rt, cfg, n_steps, fixed_tree=False, label=""):
-    """Runs GPU adt_step and the oracle decoder side by side; returns (steps matched, flag)."""
+def _compare_run(rt, cfg, n_steps, fixed_tree=False, label="", shapes=None):
+    """Runs GPU adt_step and the oracle decoder side by side; returns (steps matched, flag).
+    shapes, if a list, receives every compared (d_hat, k_hat)."""
     _, om, dm, pre = _setup(rt, cfg)
     sess = rt.DeviceSession(dm, cfg, fixed_tree=fixed_tree)
     dec = Decoder(cfg, om, pre)
@@ -68,6 +69,8 @@ def _compare_run(rt, cfg, n_steps, fixed_tree=False, label=""):
         t = sess.tensors()
         print(f"{label} step {o.step}: d={o.d_hat} k={o.k_hat} n={o.tree.n} a={len(o.path)}", flush=True)
         assert (g["d_hat"], g["k_hat"]) == (o.d_hat, o.k_hat), "schedule differs"
+        if shapes is not None:
+            shapes.append((o.d_hat, o.k_hat))
         if o.draft_root_logits is not None:
             gd = t["draft_logits"][0].cpu().numpy()
             assert _tol_ok(gd, o.draft_root_logits, tol).all(), \
@@ -96,6 +99,28 @@ def test_tiny_full_image_adt_schedule(rt):
     matched, flag = _compare_run(rt, cfg, 10_000, label="tiny")
     print("tiny matched", matched, flag)
     assert flag is None and matched >= 1
+
+
+INIT_RULES = {"vertical": dict(init="vertical"), "random": dict(init="random", seed=11),
+              "tokenflock": dict(init="tokenflock", flock_delta=2), "fixed_d1": dict(fix_d=1),
+              "fixed_d1_k3": dict(fix_d=1, fix_k=3), "deep_width": dict(k_clamp="deep", l_k=4)}
+
+
+@pytest.mark.parametrize("rule", list(INIT_RULES))
+def test_tiny_full_image_init_rules(rt, rule):
+    """The other initialisation rules (Sec. 4.1, Sec. 5.3 Eqs. 6-8, Table V) and the
+    deep-only width bound (Sec. 4.2) through adt_step over a whole image: every schedule
+    decision, tree and committed token equal to the oracle's."""
+    cfg = synth.get_config("tiny")
+    cfg = dataclasses.replace(cfg, sched=dataclasses.replace(cfg.sched, **INIT_RULES[rule]))
+    shapes = []
+    matched, flag = _compare_run(rt, cfg, 10_000, label="tiny-" + rule, shapes=shapes)
+    print(rule, "matched", matched, flag, "shapes", sorted(set(shapes)))
+    assert flag is None and matched >= 1
+    if rule == "deep_width":
+        assert any(k > cfg.sched.k_hi for _, k in shapes)     # one-layer trees wider than k_hi ran
+    if rule == "random":
+        assert len(set(shapes)) >= 6
 
 
 def test_tiny_fixed_deep_tree(rt):
