@@ -58,19 +58,42 @@ def compact_cache(k: np.ndarray, v: np.ndarray, L: int, path: List[int]) -> None
         v[..., L + m, :] = v[..., L + node, :]
 
 
+class Branch:
+    """One guidance branch (Sec. 3.1, CFG): its own prompt, target and draft caches and
+    target features; the image tokens are shared by all branches."""
+
+    def __init__(self, model: OracleModel, prefix, s_cap: int):
+        self.prefix = [int(t) for t in prefix]
+        self.tcache, self.dcache = model.new_caches(s_cap)
+        self.feat: Dict[int, np.ndarray] = {}          # target feature per committed position
+
+
+def guide(rows: List[np.ndarray], scale: Optional[float]) -> np.ndarray:
+    """Classifier-free guidance (Ho & Salimans) on logits: l_u + s (l_c - l_u); one branch
+    passes through."""
+    if scale is None:
+        return rows[0]
+    cond, uncond = rows
+    return uncond + scale * (cond - uncond)
+
+
 class Decoder:
     """Oracle decode state for one image."""
 
     def __init__(self, cfg: DecodeCfg, model: OracleModel, prefix: np.ndarray,
                  poisson: Optional[np.ndarray] = None, knn: Optional[np.ndarray] = None,
-                 accept_seed: Optional[int] = None):
+                 accept_seed: Optional[int] = None, uncond_prefix: Optional[np.ndarray] = None):
         self.cfg = cfg
         self.model = model
         self.P = len(prefix)
         self.tokens: List[int] = [int(t) for t in prefix]
         s_cap = self.P + cfg.n_image + 256
-        self.tcache, self.dcache = model.new_caches(s_cap)
-        self.feat: Dict[int, np.ndarray] = {}          # target feature per committed position
+        self.guidance = cfg.guidance
+        prompts = [prefix]
+        if cfg.guidance is not None:
+            assert uncond_prefix is not None and len(uncond_prefix) == self.P
+            prompts.append(uncond_prefix)
+        self.branches = [Branch(model, pr, s_cap) for pr in prompts]
         self.records: Dict[int, Tuple[int, int]] = {}  # cell -> (d, k) of the committing tree
         self.prev: Optional[Tuple[int, int]] = None    # (a, d) of the previous tree
         self.prev_cell: Optional[int] = None
@@ -80,6 +103,19 @@ class Decoder:
         self.poisson = poisson
         self.knn = knn
         self.accept_seed = cfg.seed if accept_seed is None else accept_seed
+
+    # the conditional (or only) branch's state
+    @property
+    def tcache(self):
+        return self.branches[0].tcache
+
+    @property
+    def dcache(self):
+        return self.branches[0].dcache
+
+    @property
+    def feat(self):
+        return self.branches[0].feat
 
     # ---------------------------------------------------------------- helpers
     def allowed_pos(self, p: int) -> Tuple[int, int]:
@@ -100,23 +136,28 @@ class Decoder:
                                    top_k=a.top_k, seed=self.accept_seed, step=step, mode=a.mode,
                                    delta=a.delta, knn=self.knn, knn_k=a.knn_k)
 
-    def _feat_before(self, p: int) -> np.ndarray:
-        return self.feat[p - 1] if p > 0 else np.zeros(self.cfg.model.d_model)
+    def _feat_before(self, br: Branch, p: int) -> np.ndarray:
+        return br.feat[p - 1] if p > 0 else np.zeros(self.cfg.model.d_model)
 
     # ---------------------------------------------------------------- prefill
     def prefill(self) -> int:
-        """Target and draft over the prefix, then the first image token by one AR step."""
+        """Target and draft over each branch's prompt, then the first image token by one AR
+        step on the (guided) logits of the last prompt row."""
         P = self.P
         pos = list(range(P))
         causal = [list(range(r + 1)) for r in range(P)]
-        logits, f = self.model.target_rows(self.tokens, pos, pos, causal, self.tcache)
-        for p in range(P):
-            self.feat[p] = f[p]
-        par = np.stack([self._feat_before(p) for p in range(P)])
-        self.model.draft_rows(self.tokens, par, pos, pos, causal, self.dcache)
+        last = []
+        for br in self.branches:
+            logits, f = self.model.target_rows(br.prefix, pos, pos, causal, br.tcache)
+            for p in range(P):
+                br.feat[p] = f[p]
+            par = np.stack([self._feat_before(br, p) for p in range(P)])
+            self.model.draft_rows(br.prefix, par, pos, pos, causal, br.dcache)
+            last.append(logits[P - 1])
         lo, hi = self.allowed_pos(P)
-        self.prefill_logits = logits[P - 1]
-        _, first = self._pick(logits[P - 1:P], [-1], [self.tokens[-1]], np.array([[lo, hi]]), 0)
+        self.prefill_branch_logits = last
+        self.prefill_logits = guide(last, self.guidance)
+        _, first = self._pick(self.prefill_logits[None], [-1], [self.tokens[-1]], np.array([[lo, hi]]), 0)
         self.tokens.append(first)
         self.L = P
         self.Ld = P
@@ -125,28 +166,31 @@ class Decoder:
 
     # ---------------------------------------------------------------- draft side
     def _draft_catch_up(self):
-        """Draft rows for committed positions Ld..L (the root last).  Returns the root row's
-        (logits, draft feature)."""
+        """Draft rows for committed positions Ld..L (the root last), every branch.  Returns
+        the root row's guided logits and its draft feature per branch."""
         ps = list(range(self.Ld, self.L + 1))
         toks = [self.tokens[p] for p in ps]
-        par = np.stack([self._feat_before(p) for p in ps])
         keys = [list(range(p + 1)) for p in ps]
-        lg, fd = self.model.draft_rows(toks, par, ps, ps, keys, self.dcache)
-        return lg[-1], fd[-1]
+        lgs, feats = [], []
+        for br in self.branches:
+            par = np.stack([self._feat_before(br, p) for p in ps])
+            lg, fd = self.model.draft_rows(toks, par, ps, ps, keys, br.dcache)
+            lgs.append(lg[-1])
+            feats.append(fd[-1])
+        return guide(lgs, self.guidance), feats
 
     def expand_tree(self, d_hat: int, k_hat: int):
         L = self.L
         root_logits, root_feat = self._draft_catch_up()
         row_slot: Dict[int, int] = {}       # pool index -> draft cache slot of its row
-        row_feat: Dict[int, np.ndarray] = {}
+        row_feat: Dict[int, List[np.ndarray]] = {}   # pool index -> draft feature per branch
         next_slot = [L + 1]
 
         def level_fn(frontier, pool):
-            toks, feats, pos, slots, keys = [], [], [], [], []
+            toks, pos, slots, keys = [], [], [], []
             for u in frontier:
                 node = pool[u]
                 toks.append(node.token)
-                feats.append(root_feat if node.parent == -1 else row_feat[node.parent])
                 pos.append(L + node.depth)
                 slot = next_slot[0]
                 next_slot[0] += 1
@@ -158,10 +202,14 @@ class Decoder:
                     anc.append(row_slot[v])
                     v = pool[v].parent
                 keys.append(list(range(L + 1)) + sorted(anc) + [slot])
-            lg, fd = self.model.draft_rows(toks, np.stack(feats), pos, slots, keys, self.dcache)
-            for u, frow in zip(frontier, fd):
-                row_feat[u] = frow
-            return lg
+            lgs = []
+            for b, br in enumerate(self.branches):
+                feats = [root_feat[b] if pool[u].parent == -1 else row_feat[pool[u].parent][b] for u in frontier]
+                lg, fd = self.model.draft_rows(toks, np.stack(feats), pos, slots, keys, br.dcache)
+                for u, frow in zip(frontier, fd):
+                    row_feat.setdefault(u, []).append(frow)
+                lgs.append(lg)
+            return guide(lgs, self.guidance)
 
         pool, sel = expand(root_logits, level_fn, d_hat, k_hat, self.cfg.sched.n_budget,
                            lambda depth: self.allowed_pos(L + depth))
@@ -169,13 +217,21 @@ class Decoder:
 
     # ---------------------------------------------------------------- one cycle
     def verify(self, tree: Tree):
+        """Target forward of every tree node in each branch.  Returns (guided logits,
+        features per branch, allowed ranges); the per-branch logits stay in
+        self.verify_branch_logits."""
         L = self.L
         anc = ancestors_and_self(tree.parent)
         pos = [L + int(dp) for dp in tree.depth]
         slots = [L + i for i in range(tree.n)]
-        logits, f = self.model.target_rows(tree.token, pos, slots, tree_key_slots(L, anc), self.tcache)
+        lgs, fs = [], []
+        for br in self.branches:
+            logits, f = self.model.target_rows(tree.token, pos, slots, tree_key_slots(L, anc), br.tcache)
+            lgs.append(logits)
+            fs.append(f)
+        self.verify_branch_logits = lgs
         allowed = np.array([self.allowed_pos(L + int(dp) + 1) for dp in tree.depth], dtype=np.int64)
-        return logits, f, allowed
+        return guide(lgs, self.guidance), fs, allowed
 
     def schedule_next(self) -> Tuple[int, int]:
         cell = self.L + 1 - self.P                   # cell of the first drafted token
@@ -187,7 +243,8 @@ class Decoder:
         return schedule(self.cfg.sched, init, prev, remaining)
 
     def compact(self, path: List[int]):
-        compact_cache(self.tcache.k, self.tcache.v, self.L, path)
+        for br in self.branches:
+            compact_cache(br.tcache.k, br.tcache.v, self.L, path)
 
     def step(self) -> StepInfo:
         d_hat, k_hat = self.schedule_next()
@@ -201,14 +258,15 @@ class Decoder:
         """Verify a tree, accept along it, compact and commit.  Without a preceding expansion
         (expanded=False) the draft cache was not advanced, so its valid length stays."""
         L = self.L
-        logits, f, allowed = self.verify(tree)
+        logits, fs, allowed = self.verify(tree)
         masked = np.stack([masked_logits(logits[i], *allowed[i]) for i in range(tree.n)])
         path, bonus = self._pick(masked, tree.parent, tree.token, allowed, self.step_no)
         committed = [int(tree.token[v]) for v in path] + [int(bonus)]
         self.compact(path)
-        self.feat[L] = f[0]
-        for m, v in enumerate(path, start=1):
-            self.feat[L + m] = f[v]
+        for br, f in zip(self.branches, fs):
+            br.feat[L] = f[0]
+            for m, v in enumerate(path, start=1):
+                br.feat[L + m] = f[v]
         cell0 = L + 1 - self.P
         for c in range(cell0, cell0 + len(committed)):
             self.records[c] = (d_hat, k_hat)
@@ -230,23 +288,28 @@ class Decoder:
         return out
 
 
-def ar_decode(cfg: DecodeCfg, model: OracleModel, prefix: np.ndarray, n_tokens: Optional[int] = None):
-    """Plain greedy AR reference: prefill, then one target row per token.  Returns
-    (image tokens, per-token logits of the row that predicted each token after the first)."""
+def ar_decode(cfg: DecodeCfg, model: OracleModel, prefix: np.ndarray, n_tokens: Optional[int] = None,
+              uncond_prefix: Optional[np.ndarray] = None):
+    """Plain greedy AR reference: prefill, then one target row per token (per guidance
+    branch, the logits combined by CFG).  Returns (image tokens, per-token guided logits of
+    the row that predicted each token after the first)."""
     assert cfg.accept.mode == "greedy"
-    dec = Decoder(cfg, model, prefix)
-    P = dec.P
+    prompts = [prefix] if cfg.guidance is None else [prefix, uncond_prefix]
+    P = len(prefix)
     n_tokens = cfg.n_image if n_tokens is None else n_tokens
+    caches = [model.new_caches(P + n_tokens + 1)[0] for _ in prompts]
     pos = list(range(P))
     causal = [list(range(r + 1)) for r in range(P)]
-    logits, _ = model.target_rows(dec.tokens, pos, pos, causal, dec.tcache)
+    last = [model.target_rows([int(t) for t in pr], pos, pos, causal, c)[0][P - 1] for pr, c in zip(prompts, caches)]
+    g = guide(last, cfg.guidance)
     lo, hi = cfg.allowed(0)
-    toks = [lo + int(np.argmax(logits[P - 1][lo:hi]))]
+    toks = [lo + int(np.argmax(g[lo:hi]))]
     rows = []
     for i in range(1, n_tokens):
         p = P + i - 1                                  # position of the latest token
-        lg, _ = model.target_rows([toks[-1]], [p], [p], [list(range(p + 1))], dec.tcache)
-        rows.append(lg[0])
+        g = guide([model.target_rows([toks[-1]], [p], [p], [list(range(p + 1))], c)[0][0] for c in caches],
+                  cfg.guidance)
+        rows.append(g)
         lo, hi = cfg.allowed(i)
-        toks.append(lo + int(np.argmax(lg[0][lo:hi])))
+        toks.append(lo + int(np.argmax(g[lo:hi])))
     return toks, rows

@@ -87,6 +87,7 @@ class DecodeCfg:
     sched: SchedCfg
     accept: AcceptCfg
     codebook: Optional[Tuple[int, int]] = None   # (entries, dim) for relaxed mode
+    guidance: Optional[float] = None   # classifier-free guidance scale (two branches), None = off
 
     @property
     def n_image(self) -> int:
@@ -235,6 +236,12 @@ def model_weights(cfg: DecodeCfg, threads: int = 8, names: Optional[List[str]] =
 def prefix_ids(cfg: DecodeCfg) -> np.ndarray:
     r = np.random.default_rng([cfg.seed, 10_000])
     return r.integers(cfg.prefix_lo, cfg.prefix_hi, size=cfg.prefix_len, dtype=np.int64).astype(np.int32)
+
+
+def null_prefix_ids(cfg: DecodeCfg) -> np.ndarray:
+    """The unconditional prompt of a guided configuration: as long as the prompt, every
+    position holding one reserved id (the last id of the prompt range)."""
+    return np.full(cfg.prefix_len, cfg.prefix_hi - 1, dtype=np.int32)
 
 
 def poisson_table(cfg: DecodeCfg) -> np.ndarray:

@@ -118,3 +118,46 @@ def test_bf16_rounding_points_bound_error():
     lx, _ = m_x.target_rows(pre, pos, pos, causal, m_x.new_caches(64)[0])
     assert np.all(np.abs(lr - lx) <= 2e-2 + 1e-2 * np.abs(lx))
     assert np.abs(lr - lx).max() > 0
+
+
+# ---------------------------------------------------------------- classifier-free guidance
+# Sec. 3.1: p and q are both computed with CFG (conditional and unconditional branches per
+# position, Fig. 5 caption); the combination is l_u + s (l_c - l_u) on logits.
+def _guided(cfg, s):
+    return dataclasses.replace(cfg, guidance=s)
+
+
+@pytest.mark.parametrize("planted", [False, True])
+def test_guided_tree_decode_equals_guided_ar(tiny, planted):
+    cfg0, w, _, pre, _, _ = tiny
+    cfg = _guided(cfg0, 3.0)
+    null = synth.null_prefix_ids(cfg)
+    model = OracleModel(cfg, w)
+    ar, _ = ar_decode(cfg, model, pre, uncond_prefix=null)
+    assert ar != tiny[4]                          # guidance changes the image
+    if planted:
+        _plant_draft(model, list(pre) + list(ar), cfg.model.vocab)
+    dec = Decoder(cfg, model, pre, uncond_prefix=null)
+    dec.prefill()
+    infos = dec.run()
+    assert dec.tokens[len(pre):] == ar
+    if planted:
+        assert np.mean([len(i.path) for i in infos]) > 2.0
+
+
+def test_guidance_scale_one_and_zero_reduce_to_one_branch(tiny):
+    """s = 1 gives the conditional model's logits, s = 0 the unconditional one's: the guided
+    decode then equals a plain decode with that branch's prompt, cycle for cycle."""
+    cfg0, w, model, pre, _, _ = tiny
+    null = synth.null_prefix_ids(cfg0)
+    for s, prompt in ((1.0, pre), (0.0, null)):
+        g = Decoder(_guided(cfg0, s), model, pre, uncond_prefix=null)
+        p = Decoder(cfg0, model, prompt)
+        assert g.prefill() == p.prefill()
+        np.testing.assert_allclose(g.prefill_logits, p.prefill_logits, rtol=1e-12, atol=1e-12)
+        for _ in range(12):
+            gi, pi = g.step(), p.step()
+            assert (gi.d_hat, gi.k_hat, gi.committed) == (pi.d_hat, pi.k_hat, pi.committed)
+            assert gi.tree.token.tolist() == pi.tree.token.tolist()
+            np.testing.assert_allclose(gi.logits, pi.logits, rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(gi.draft_root_logits, pi.draft_root_logits, rtol=1e-12, atol=1e-12)
