@@ -9,7 +9,8 @@ N(0, 0.02) weights), a 120-token seeded prompt and a 32 x 32 image grid, trees o
 60 draft nodes, width <= 10, depth <= 6.  The metric is verified draft-tree nodes per
 second; the line also carries the roofline of the dominant kernel (the weight-streaming
 projections), tree-attention bandwidth (in the cycle and in the 16 x 32 x 128 tree-attention
-microbenchmark) and the CPU oracle timed on this host.
+microbenchmark), the batched verify projections, the same cycle under classifier-free
+guidance (scale 3.0: both branches in every forward) and the CPU oracle timed on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -56,6 +57,7 @@ def parse():
     ap.add_argument("--no-microbench", action="store_true")
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-mfma", action="store_true")
+    ap.add_argument("--no-guided", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -233,6 +235,20 @@ def main():
         s.prefill(pre)
         return s
 
+    def guided_run(k):
+        """The same cycle with classifier-free guidance (scale 3.0, conditional and
+        unconditional branches in every forward)."""
+        import dataclasses
+        gcfg = dataclasses.replace(cfg, guidance=3.0)
+        gs = rt.DeviceSession(dm, gcfg)
+        gs.prefill(pre, synth.null_prefix_ids(gcfg))
+        run_steps(gs, 3)
+        gdt, gnodes, gtokens, gdepth = timed(gs, k)
+        del gs
+        return {"scale": 3.0, "nodes_per_s": round(gnodes / gdt, 2), "ms_per_step": round(gdt / k * 1e3, 4),
+                "nodes_per_step": round(gnodes / k, 2), "tokens_per_step": round(gtokens / k, 3),
+                "mean_depth": round(gdepth / k, 3), "steps": k}
+
     sess = fresh()
     run_steps(sess, args.warmup)
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
@@ -253,6 +269,7 @@ def main():
     attn_gbs = a["bytes"] / (a["ms"] * 1e-3) / 1e9 if a["ms"] > 0 else 0.0
     micro = {} if args.no_microbench else attn_microbench(rt)
     mfma = None if args.no_mfma else mfma_benchmark(rt)
+    guided = None if args.no_guided else guided_run(min(args.steps, 50))
     line = {
         "metric": "verified draft-tree nodes/sec + tree-attn HBM GB/s (% peak), 1xMI355X",
         "value": round(value, 2),
@@ -281,6 +298,7 @@ def main():
                       "in_cycle_avg_us": round(a["ms"] / max(a["launches"], 1) * 1e3, 3),
                       "microbench_16x32x128": micro},
         "batched_verify_gemm": mfma,
+        "guided": guided,
         "fixed_tree": {"nodes_per_s": round(fnodes / fdt, 2), "ms_per_step": round(fdt / min(args.steps, 50) * 1e3, 4),
                        "nodes_per_step": round(fnodes / min(args.steps, 50), 2), "tree": "depth 6, width 10, top-60"},
     }

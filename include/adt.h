@@ -289,6 +289,15 @@ typedef struct {
   /* 1: capture the verify and draft forwards as HIP graphs (one per tree shape, built on
    * first use on a private stream, replayed on the caller's stream); 0: plain launches. */
   int32_t use_graphs;
+  /* Classifier-free guidance in target and draft (Sec. 3.1; Fig. 5 caption): guided = 1 runs
+   * every forward over a conditional and an unconditional branch and uses the logits
+   * l_u + guidance_scale (l_c - l_u) for drafting and acceptance.  Then the caches hold both
+   * branches, branch 1 after branch 0 (k_cache / v_cache [2][n_layers][n_heads][s_cap]
+   * [head_dim], dk_cache / dv_cache [2][n_heads][s_cap][head_dim]), the prompt passed to
+   * adt_session_prefill is both prompts ([2][prefix_len]: conditional, then unconditional,
+   * equally long), and a tree holds at most ADT_MAX_NODES / 2 nodes (n_budget <= 63). */
+  int32_t guided;
+  float guidance_scale;
   void* workspace;
   size_t workspace_bytes;
 } adt_session_desc;
@@ -319,13 +328,20 @@ typedef struct {
   /* scratch of the last forward (last layer run): rotated queries [rows][d] dtype, attention
    * output [rows][d] dtype, normed activations [rows][d] dtype, residual stream [rows][d] fp32 */
   void* q; void* att; void* act; float* resid;
+  /* guidance: rows of the last forwards hold node i's branches at rows nb i + b (b = 0
+   * conditional); feat is then [ADT_MAX_NODES / 2][2][d_model] and logits / draft_logits are
+   * the guided ones */
+  int32_t n_branches;
+  float* branch_logits;         /* guided: [n][2][vocab] per-branch verify logits, else NULL */
+  float* draft_branch_logits;   /* guided: [2][vocab] per-branch logits of the draft root row, else NULL */
 } adt_session_view;
 
 size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* desc);
 adt_status adt_session_create(const adt_model* m, const adt_session_desc* desc, adt_session** out);
 void adt_session_destroy(adt_session* s);
 /* Target and draft over the prompt, then the first image token by one AR step (greedy or a
- * draw at step 0).  prefix: [host] prefix_len ids.  Synchronises. */
+ * draw at step 0).  prefix: [host] prefix_len ids (guided: 2 * prefix_len, the conditional
+ * prompt then the unconditional one).  Synchronises. */
 adt_status adt_session_prefill(adt_session* s, const int32_t* prefix, int32_t* first_token, void* stream);
 adt_status adt_session_get_view(const adt_session* s, adt_session_view* v);
 

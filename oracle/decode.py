@@ -177,6 +177,7 @@ class Decoder:
             lg, fd = self.model.draft_rows(toks, par, ps, ps, keys, br.dcache)
             lgs.append(lg[-1])
             feats.append(fd[-1])
+        self.draft_root_branch_logits = lgs
         return guide(lgs, self.guidance), feats
 
     def expand_tree(self, d_hat: int, k_hat: int):

@@ -56,7 +56,8 @@ class SessionDesc(C.Structure):
     _fields_ = [("prefix_len", i32), ("n_image", i32), ("s_cap", i32), ("k_cache", p), ("v_cache", p),
                 ("dk_cache", p), ("dv_cache", p), ("allowed", ip), ("sched", SchedCfg), ("accept", AcceptCfg),
                 ("poisson", ip), ("fixed_tree", i32), ("draft_table", p), ("draft_table_rows", i32),
-                ("use_graphs", i32), ("workspace", p), ("workspace_bytes", sz)]
+                ("use_graphs", i32), ("guided", i32), ("guidance_scale", f32), ("workspace", p),
+                ("workspace_bytes", sz)]
 
 
 class StepOut(C.Structure):
@@ -68,7 +69,8 @@ class SessionView(C.Structure):
     _fields_ = [("L", i32), ("Ld", i32), ("step", i32), ("n_tokens", i32), ("n_nodes", i32),
                 ("logits", p), ("feat", p), ("draft_logits", p), ("parent", p), ("token", p), ("depth", p),
                 ("score", p), ("mask", p), ("allowed_rows", p), ("path", p), ("n_acc", p), ("bonus", p),
-                ("tokens_host", ip), ("q", p), ("att", p), ("act", p), ("resid", p)]
+                ("tokens_host", ip), ("q", p), ("att", p), ("act", p), ("resid", p), ("n_branches", i32),
+                ("branch_logits", p), ("draft_branch_logits", p)]
 
 
 _SIGS = {

@@ -164,8 +164,9 @@ extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const vo
                 (long long)stride_h);
   ADT_CHECK_ARG(B == 1 || stride_b >= (int64_t)H * stride_h, ADT_E_SHAPE, "tree_attn: stride_b too small");
   ADT_CHECK_ARG(std::isfinite(scale) && scale > 0.f, ADT_E_ARG, "tree_attn: scale");
-  return launch_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask, B, H, Dh, nq_max,
-                          kv_cap, scale, dtype, out, workspace, workspace_bytes, (hipStream_t)stream);
+  return launch_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask,
+                          AttnRows{nq_max, 1, nq_max}, B, H, Dh, nq_max, kv_cap, scale, dtype, out, workspace,
+                          workspace_bytes, (hipStream_t)stream);
 }
 
 extern "C" adt_status adt_tree_masks(const int32_t* parent, const int32_t* n_nodes, int32_t B, int32_t n_max,
@@ -184,8 +185,8 @@ extern "C" adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, in
   ADT_CHECK_ARG(a_max >= 0 && a_max < ADT_MAX_NODES && path_stride >= a_max + 1, ADT_E_CAPACITY,
                 "kv_compact: a_max %d path_stride %d", a_max, path_stride);
   if (a_max == 0) return ADT_OK;
-  return launch_kv_compact(k_cache, v_cache, B, slices, Dh, stride_b, stride_slice, kv_len, path, path_stride, n_acc,
-                           a_max, dtype, (hipStream_t)stream);
+  return launch_kv_compact(k_cache, v_cache, B, slices, Dh, stride_b, stride_slice, kv_len, 1, path, path_stride, n_acc,
+                           1, a_max, dtype, (hipStream_t)stream);
 }
 
 extern "C" size_t adt_accept_workspace_size(int32_t V) {
@@ -443,6 +444,13 @@ struct adt_session_s {
   int DLR;      // draft logits rows
   int KR;       // frontier rows capacity
   int C;        // pool capacity
+  // guidance: nb = 2 branches (conditional, unconditional) interleaved node by node in every
+  // forward's rows; caches of branch 1 sit tcache_sb / dcache_sb elements after branch 0
+  int nb = 1;
+  float gscale = 1.f;
+  int64_t tcache_sb = 0, dcache_sb = 0;
+  float* rawlog = nullptr;   // [R][V] per-branch verify logits (guided)
+  float* draw = nullptr;     // [nb (1 + KR)][V] per-branch draft logits: root rows, then a level's rows
   // host state
   bool prefilled = false;
   bool expanded = false;   // the current tree came from adt_tree_expand (draft root row written)
@@ -494,6 +502,10 @@ static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_sessi
   s->V = md.vocab;
   s->P = d->prefix_len;
   s->T = d->n_image;
+  s->nb = d->guided ? 2 : 1;
+  s->gscale = d->guidance_scale;
+  s->tcache_sb = (int64_t)md.n_layers * md.n_heads * d->s_cap * md.head_dim;
+  s->dcache_sb = (int64_t)md.n_heads * d->s_cap * md.head_dim;
   const int dh = d->sched.d_hi, kh = d->sched.k_hi;
   s->C0 = dh + 2;
   s->DR = s->C0 + std::max(1, (dh - 1) * kh);
@@ -520,12 +532,16 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->att = b.take<char>((size_t)R * dm * es);
   s->sw = b.take<char>((size_t)R * s->F * es);
   s->feat = b.take<char>((size_t)R * dm * es);
-  s->cfeat = b.take<char>((size_t)s->C0 * dm * es);
-  s->dfeat = b.take<char>((size_t)s->DR * dm * es);
+  s->cfeat = b.take<char>((size_t)s->nb * s->C0 * dm * es);
+  s->dfeat = b.take<char>((size_t)s->nb * s->DR * dm * es);
   s->part = b.take<float>(s->part_elems);
   s->ssp = b.take<float>((size_t)R * (dm / 16));
   s->logits = b.take<float>((size_t)R * s->V);
   s->dlogits = b.take<float>((size_t)s->DLR * s->V);
+  if (s->nb > 1) {
+    s->rawlog = b.take<float>((size_t)R * s->V);
+    s->draw = b.take<float>((size_t)s->nb * (1 + s->KR) * s->V);
+  }
   TreeBufs& t = s->tr;
   t.parent = b.take<int32_t>(R);
   t.token = b.take<int32_t>(R);
@@ -554,7 +570,7 @@ static size_t session_layout(adt_session_s* s, char* base) {
     s->nx[i].mask = b.take<uint64_t>(2 * s->KR);
     s->nx[i].frontier = b.take<int32_t>(s->KR);
   }
-  s->ctok = b.take<int32_t>(R);
+  s->ctok = b.take<int32_t>(2 * R);
   s->cfsrc = b.take<int32_t>(R);
   s->cpos = b.take<int32_t>(R);
   s->idx = b.take<int32_t>(R);
@@ -565,7 +581,7 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->allowed_lvl = b.take<int32_t>(2 * R);
   s->scal = b.take<int32_t>(16);
   s->rope = b.take<float2>((size_t)s->d.s_cap * (s->Dh / 2));
-  s->attn_ws_bytes = tree_attn_ws_bytes(1, s->H, s->Dh, R, s->d.s_cap, s->dt);
+  s->attn_ws_bytes = tree_attn_ws_bytes(s->nb, s->H, s->Dh, R / s->nb, s->d.s_cap, s->dt);
   s->attn_ws = b.take<char>(std::max<size_t>(s->attn_ws_bytes, 256));
   s->acc_ws_bytes = adt_accept_workspace_size(s->V);
   s->acc_ws = b.take<char>(s->acc_ws_bytes);
@@ -583,7 +599,10 @@ static adt_status check_session_desc(const adt_model* m, const adt_session_desc*
   const adt_sched_cfg& c = d->sched;
   TRY(check_sched_cfg(&c));
   ADT_CHECK_ARG(c.d_hi <= 30 && c.k_hi <= 16, ADT_E_UNSUPPORTED, "session: d_hi <= 30 and k_hi <= 16 supported");
-  ADT_CHECK_ARG(c.n_budget >= 1 && c.n_budget <= R - 1, ADT_E_CAPACITY, "session: n_budget %d", c.n_budget);
+  const int nb = d->guided ? 2 : 1;
+  ADT_CHECK_ARG(d->guided == 0 || d->guided == 1, ADT_E_ARG, "session: guided %d", d->guided);
+  ADT_CHECK_ARG(!d->guided || std::isfinite(d->guidance_scale), ADT_E_ARG, "session: guidance scale");
+  ADT_CHECK_ARG(c.n_budget >= 1 && c.n_budget <= R / nb - 1, ADT_E_CAPACITY, "session: n_budget %d", c.n_budget);
   ADT_CHECK_ARG((c.d_hi - 1) * c.k_hi <= R, ADT_E_CAPACITY, "session: draft tree rows exceed %d", R);
   ADT_CHECK_ARG(c.alpha_source == ADT_ALPHA_REAL || (c.alpha_source == ADT_ALPHA_POISSON && d->poisson), ADT_E_ARG,
                 "session: alpha source");
@@ -644,10 +663,13 @@ static SmallI32 small_of(const int32_t* v, int n) {
   return s;
 }
 
-// scal[0..3] = attention prefix length, query rows, tail rows, first cache slot of the rows.
+// Device scalars of a forward, one copy per guidance branch: scal[0..1] attention prefix
+// length, [2..3] query rows, [4..5] tail rows; scal[6] first cache slot of the rows;
+// scal[8..9] the committed length for compaction.
+enum { SC_KV = 0, SC_NQ = 2, SC_TAIL = 4, SC_SLOT = 6, SC_CL = 8 };
 static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, int slot0, hipStream_t st) {
-  int32_t v[4] = {kv_len, nq, ntail, slot0};
-  return launch_set_i32(s->scal, small_of(v, 4), 4, st);
+  int32_t v[7] = {kv_len, kv_len, nq, nq, ntail, ntail, slot0};
+  return launch_set_i32(s->scal, small_of(v, 7), 7, st);
 }
 
 // Runs body(stream) through a cached graph (captured on first use for this key).  Eager
@@ -693,11 +715,13 @@ static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, in
   return r;
 }
 
-// Decoder layers over M rows.  Cache stack `kc/vc` has stride_layer between layers.
+// Decoder layers over the nb * M rows of M tree nodes (branches interleaved node by node).
 static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
                              const uint64_t* mask, void* final_out, hipStream_t st) {
   const adt_model_s* m = s->m;
-  const int dm = s->dm, H = s->H, Dh = s->Dh, F = s->F, dt = s->dt;
+  const int dm = s->dm, H = s->H, Dh = s->Dh, F = s->F, dt = s->dt, nb = s->nb, rows = nb * M;
+  const int64_t cache_sb = draft ? s->dcache_sb : s->tcache_sb;
+  const Branches br{nb, 0, cache_sb};
   const size_t es = esize(dt);
   const int64_t stride_h = (int64_t)s->d.s_cap * Dh;
   const float eps = m->d.norm_eps;
@@ -707,10 +731,11 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   auto attention = [&](char* kc, char* vc) -> adt_status {
     // the prefix K/V once, tree Q/K/V in and O out, the masks
     const int e = prof_begin(st);
-    TRY(launch_tree_attn(s->q, kc, vc, 0, stride_h, s->scal, s->scal + 1, s->scal + 2, mask, 1, H, Dh, M, s->d.s_cap,
-                         scale, dt, s->att, s->attn_ws, s->attn_ws_bytes, st));
-    prof_end(e, ADT_PROF_ATTN, 2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es + 16.0 * M,
-             4.0 * M * (L_pre + n_tail) * H * Dh, st);
+    TRY(launch_tree_attn(s->q, kc, vc, cache_sb, stride_h, s->scal + SC_KV, s->scal + SC_NQ, s->scal + SC_TAIL, mask,
+                         AttnRows{1, nb, 0}, nb, H, Dh, M, s->d.s_cap, scale, dt, s->att, s->attn_ws,
+                         s->attn_ws_bytes, st));
+    prof_end(e, ADT_PROF_ATTN, nb * (2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es) + 16.0 * M,
+             4.0 * rows * (L_pre + n_tail) * H * Dh, st);
     return ADT_OK;
   };
   if (dt == ADT_BF16) {
@@ -733,67 +758,78 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       qkv.kc = (uint16_t*)kc;
       qkv.vc = (uint16_t*)vc;
       qkv.stride_h = stride_h;
-      qkv.slot0 = s->scal + 3;
+      qkv.slot0 = s->scal + SC_SLOT;
       qkv.pos = pos;
       qkv.rope = s->rope;
       qkv.Dh = Dh;
-      TRY(gemm_p(s->h, dm, m->qkv[l], M, 3 * dm, dm, dt, s->part, st, qkv));
+      qkv.nb = nb;
+      qkv.cache_sb = cache_sb;
+      TRY(gemm_p(s->h, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
-      TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, dt, s->part, st, resid));
+      TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st, resid));
       GemmEpi sw;
       sw.mode = EPI_SWIGLU;
       sw.ssp_in = s->ssp;
       sw.nss_in = dm / 16;
       sw.eps = eps;
       sw.act = (uint16_t*)s->sw;
-      TRY(gemm_p(s->h, dm, m->gu[l], M, 2 * F, dm, dt, s->part, st, sw));
-      TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, dt, s->part, st, resid));
+      TRY(gemm_p(s->h, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
+      TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st, resid));
     }
-    if (final_out) TRY(launch_norm_rows(s->h, s->ssp, M, dm, eps, final_out, dt, st));
+    if (final_out) TRY(launch_norm_rows(s->h, s->ssp, rows, dm, eps, final_out, dt, st));
     return ADT_OK;
   }
   // fp32: products into part, row kernels finish each step
   for (int l = l0; l < l1; ++l) {
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
-    TRY(gemm_p(s->act, dm, m->qkv[l], M, 3 * dm, dm, dt, s->part, st));
-    TRY(launch_qkv_rope(s->part, 1, M, H, Dh, pos, s->scal + 3, s->rope, s->q, kc, vc, stride_h, dt, st));
+    TRY(gemm_p(s->act, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st));
+    TRY(launch_qkv_rope(s->part, 1, rows, H, Dh, pos, s->scal + SC_SLOT, s->rope, s->q, kc, vc, stride_h, dt, st, br));
     TRY(attention(kc, vc));
-    TRY(gemm_p(s->att, dm, m->o[l], M, dm, dm, dt, s->part, st));
-    TRY(launch_add_norm(s->part, 1, M, dm, 0, eps, s->h, s->act, dt, st));
-    TRY(gemm_p(s->act, dm, m->gu[l], M, 2 * F, dm, dt, s->part, st));
-    TRY(launch_swiglu(s->part, 1, M, F, s->sw, dt, st));
-    TRY(gemm_p(s->sw, F, m->down[l], M, dm, F, dt, s->part, st));
-    TRY(launch_add_norm(s->part, 1, M, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
+    TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st));
+    TRY(launch_add_norm(s->part, 1, rows, dm, 0, eps, s->h, s->act, dt, st));
+    TRY(gemm_p(s->act, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st));
+    TRY(launch_swiglu(s->part, 1, rows, F, s->sw, dt, st));
+    TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st));
+    TRY(launch_add_norm(s->part, 1, rows, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
   }
   return ADT_OK;
 }
 
-static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, hipStream_t st) {
+// Logits of M nodes (nb rows each) into out [M][V]; with guidance the per-branch rows go to
+// raw [nb M][V] and out gets their combination.
+static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, float* raw, hipStream_t st) {
+  const int rows = s->nb * M;
+  float* dst = s->nb > 1 ? raw : out;
   if (s->dt == ADT_BF16) {
     GemmEpi e;
     e.mode = EPI_STORE;
-    e.out = out;
+    e.out = dst;
     e.ldo = s->V;
-    return gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, s->dt, s->part, st, e);
+    TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st, e));
+  } else {
+    TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st));
+    TRY(launch_reduce_store(s->part, 1, rows, s->V, dst, s->V, st));
   }
-  TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, M, s->V, s->dm, s->dt, s->part, st));
-  return launch_reduce_store(s->part, 1, M, s->V, out, s->V, st);
+  if (s->nb > 1) TRY(launch_guide_rows(raw, M, s->V, s->gscale, out, s->V, st));
+  return ADT_OK;
 }
 
 // Target forward of M rows with tokens tok; features into s->feat; logits of rows
 // [lm_row0, lm_row0 + lm_rows) into s->logits.
+// (M nodes, nb rows each; tok_boff as in Branches: 0 = the branches share the tokens.)
 static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, const int32_t* pos, int slot0, int L_pre,
                                  int n_tail, const uint64_t* mask, int lm_row0, int lm_rows, hipStream_t st,
-                                 int64_t key = -1) {
+                                 int64_t key = -1, int tok_boff = 0) {
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
     const bool bf = s->dt == ADT_BF16;
-    TRY(launch_embed_norm(s->m->d.embed, tok, M, s->dm, s->m->d.norm_eps, s->h, bf ? nullptr : s->act,
-                          bf ? s->ssp : nullptr, s->dt, cs));
+    TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, bf ? nullptr : s->act,
+                          bf ? s->ssp : nullptr, s->dt, cs, Branches{s->nb, tok_boff, 0}));
     TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
     if (lm_rows > 0)
-      TRY(lm_head(s, (const char*)s->feat + (size_t)lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits, cs));
+      TRY(lm_head(s, (const char*)s->feat + (size_t)s->nb * lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits,
+                  s->rawlog, cs));
     return ADT_OK;
   };
   return key < 0 ? body(st) : run_graph(s, key, st, body);
@@ -801,26 +837,30 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
 
 // Draft-head forward: FC over [embedding ; parent feature], one decoder layer, final norm
 // into feature rows fout (may be null), target LM head for rows [lm_row0, +lm_rows) into out.
+// (M nodes, nb rows each; lraw takes the per-branch logits under guidance.)
 static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int32_t* fsrc, const void* fa, int M,
                                 const int32_t* pos, int slot0, int L_pre, int n_tail, const uint64_t* mask, void* fout,
-                                int lm_row0, int lm_rows, float* lout, hipStream_t st, int64_t key = -1) {
-  const int dm = s->dm, dt = s->dt;
+                                int lm_row0, int lm_rows, float* lout, float* lraw, hipStream_t st, int64_t key = -1,
+                                int tok_boff = 0) {
+  const int dm = s->dm, dt = s->dt, rows = s->nb * M;
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
-    TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, M, dm, s->xin, dt, cs));
+    TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, rows, dm, s->xin, dt, cs,
+                           Branches{s->nb, tok_boff, 0}));
     if (dt == ADT_BF16) {
       GemmEpi e;
       e.mode = EPI_RESID;
       e.h = s->h;
       e.assign = 1;
       e.ssp_out = s->ssp;
-      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, dt, s->part, cs, e));
+      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e));
     } else {
-      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, M, dm, 2 * dm, dt, s->part, cs));
-      TRY(launch_add_norm(s->part, 1, M, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
+      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs));
+      TRY(launch_add_norm(s->part, 1, rows, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
     }
     TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, cs));
-    if (lm_rows > 0) TRY(lm_head(s, (const char*)fout + (size_t)lm_row0 * dm * esize(dt), lm_rows, lout, cs));
+    if (lm_rows > 0)
+      TRY(lm_head(s, (const char*)fout + (size_t)s->nb * lm_row0 * dm * esize(dt), lm_rows, lout, lraw, cs));
     return ADT_OK;
   };
   return key < 0 ? body(st) : run_graph(s, key, st, body);
@@ -851,25 +891,38 @@ extern "C" adt_status adt_session_prefill(adt_session* s, const int32_t* prefix,
   ADT_CHECK_ARG(s && prefix, ADT_E_ARG, "prefill: null pointer");
   ADT_CHECK_ARG(!s->prefilled, ADT_E_STATE, "prefill: already prefilled");
   hipStream_t st = (hipStream_t)stream;
-  const int P = s->P;
-  for (int i = 0; i < P; ++i) ADT_CHECK_ARG(prefix[i] >= 0 && prefix[i] < s->V, ADT_E_ARG, "prefill: id %d", prefix[i]);
-  ADT_HIP(hipMemcpyAsync(s->ctok, prefix, sizeof(int32_t) * P, hipMemcpyHostToDevice, st));
+  const int P = s->P, nb = s->nb;
+  for (int i = 0; i < nb * P; ++i)
+    ADT_CHECK_ARG(prefix[i] >= 0 && prefix[i] < s->V, ADT_E_ARG, "prefill: id %d", prefix[i]);
+  // ctok = the prompts of all branches, branch after branch
+  ADT_HIP(hipMemcpyAsync(s->ctok, prefix, sizeof(int32_t) * nb * P, hipMemcpyHostToDevice, st));
   TRY(sync_stream(st));
   TRY(launch_iota(s->cpos, P, 0, 1, st));
   TRY(launch_chain_masks(s->cmask, P, st));
-  // target over the prompt; logits of the last row predict the first image token
-  TRY(target_forward(s, s->ctok, P, s->cpos, 0, 0, P, s->cmask, P - 1, 1, st));
+  // Target and draft over the prompt in chunks of at most R rows (R / nb nodes).  Row p of the
+  // draft takes the target feature of p - 1 (zeros for p = 0); the feature of the node before
+  // a chunk is carried in draft-feature node 0.
+  const int CH = R / nb;
+  for (int c0 = 0; c0 < P; c0 += CH) {
+    const int cn = std::min(CH, P - c0);
+    const bool last = c0 + cn == P;
+    TRY(target_forward(s, s->ctok + c0, cn, s->cpos + c0, c0, c0, cn, s->cmask, cn - 1, last ? 1 : 0, st, -1, P));
+    TRY(launch_iota(s->cfsrc, cn, -1, 1, st));
+    if (c0 > 0) {
+      int32_t carry[1] = {-2};
+      TRY(launch_set_i32(s->cfsrc, small_of(carry, 1), 1, st));
+    }
+    TRY(draft_forward(s, s->ctok + c0, s->cfsrc, s->feat, cn, s->cpos + c0, c0, c0, cn, s->cmask, nullptr, 0, 0,
+                      nullptr, nullptr, st, -1, P));
+    int32_t li[1] = {cn - 1};
+    TRY(launch_set_i32(s->idx, small_of(li, 1), 1, st));
+    TRY(launch_gather_rows(s->feat, s->idx, 1, nb * s->dm, last ? s->cfeat : s->dfeat, s->dt, st));
+  }
   TRY(set_root_only_tree(s, prefix[P - 1], P - 1, st));
   // the root-only tree's successor is image cell 0
   TRY(launch_fill_pairs(s->tr.allowed_rows, 1, s->allowed_h[0], s->allowed_h[1], st));
   TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, 1, s->d.accept, 0,
                   s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
-  // draft head over the prompt: row p takes the target feature of p-1 (zeros for p = 0)
-  TRY(launch_iota(s->cfsrc, P, -1, 1, st));
-  TRY(draft_forward(s, s->ctok, s->cfsrc, s->feat, P, s->cpos, 0, 0, P, s->cmask, nullptr, 0, 0, nullptr, st));
-  int32_t li[1] = {P - 1};
-  TRY(launch_set_i32(s->idx, small_of(li, 1), 1, st));
-  TRY(launch_gather_rows(s->feat, s->idx, 1, s->dm, s->cfeat, s->dt, st));
   int32_t first = 0;
   ADT_HIP(hipMemcpyAsync(&first, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
   TRY(sync_stream(st));
@@ -898,7 +951,7 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   const int k_top = (c.k_clamp == ADT_KCLAMP_DEEP && d_hat == 1) ? ADT_MAX_WIDTH : c.k_hi;
   ADT_CHECK_ARG(d_hat >= 1 && d_hat <= c.d_hi && k_hat >= 1 && k_hat <= k_top, ADT_E_ARG,
                 "tree_expand: (d,k)=(%d,%d) outside the session bounds", d_hat, k_hat);
-  ADT_CHECK_ARG(n_budget >= 1 && n_budget <= R - 1, ADT_E_CAPACITY, "tree_expand: n_budget %d", n_budget);
+  ADT_CHECK_ARG(n_budget >= 1 && n_budget <= R / s->nb - 1, ADT_E_CAPACITY, "tree_expand: n_budget %d", n_budget);
   const int L = s->L, Ld = s->Ld, P = s->P;
   ADT_CHECK_ARG(L + 1 + d_hat - P <= s->T, ADT_E_ARG, "tree_expand: depth %d runs past the image", d_hat);
   hipStream_t st = (hipStream_t)stream;
@@ -919,7 +972,7 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     TRY(launch_iota(s->cpos, cu, Ld, 1, st));
     TRY(launch_chain_masks(s->cmask, cu, st));
     TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
-                      s->dlogits, st, gkey(2, 0, 0, cu)));
+                      s->dlogits, s->draw, st, gkey(2, 0, 0, cu)));
   }
   // layer 1: the root's top-k children
   int lo, hi;
@@ -933,13 +986,14 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   for (int lvl = 2; lvl <= d_hat; ++lvl) {
     const int dl_row = 1 + (lvl - 2) * c.k_hi;
     float* lrows = s->dlogits + (size_t)dl_row * V;
-    void* fout = (char*)s->dfeat + (size_t)(s->C0 + drow) * s->dm * esize(s->dt);
+    void* fout = (char*)s->dfeat + (size_t)s->nb * (s->C0 + drow) * s->dm * esize(s->dt);
     if (table) {
       TRY(launch_table_rows(s->nx[cur].tok, nf, lvl - 1, trows, s->idx, st));
       TRY(launch_gather_rows(s->d.draft_table, s->idx, nf, V, lrows, ADT_F32, st));
     } else {
       TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1,
-                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, st, gkey(3, lvl, nf, drow)));
+                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, s->draw ? s->draw + (size_t)s->nb * s->V : nullptr,
+                        st, gkey(3, lvl, nf, drow)));
     }
     cell_range(s, L + lvl - P, lo, hi);
     TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
@@ -965,7 +1019,7 @@ extern "C" adt_status adt_session_set_tree(adt_session* s, const int32_t* parent
                                            void* stream) {
   ADT_CHECK_ARG(s && parent && token, ADT_E_ARG, "set_tree: null pointer");
   ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "set_tree: session not prefilled");
-  ADT_CHECK_ARG(n >= 1 && n <= R, ADT_E_CAPACITY, "set_tree: n %d", n);
+  ADT_CHECK_ARG(n >= 1 && n <= R / s->nb, ADT_E_CAPACITY, "set_tree: n %d (at most %d)", n, R / s->nb);
   ADT_CHECK_ARG(parent[0] == -1, ADT_E_ARG, "set_tree: node 0 must be the root");
   std::vector<int> dep(n, 0);
   for (int i = 1; i < n; ++i) {
@@ -1026,14 +1080,15 @@ extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, i
                 "accept_commit: %d catch-up rows exceed %d (too many cycles without expansion)", frow0 + a + 1, s->C0);
   if (a > 0) {
     int32_t lv[1] = {L};
-    TRY(launch_set_i32(s->scal + 8, small_of(lv, 1), 1, st));
+    TRY(launch_set_i32(s->scal + SC_CL, small_of(lv, 1), 1, st));
     const int e = prof_begin(st);
-    TRY(launch_kv_compact(s->d.k_cache, s->d.v_cache, 1, s->Lr * s->H, s->Dh, 0, (int64_t)s->d.s_cap * s->Dh,
-                          s->scal + 8, s->tr.path, R, s->tr.nacc, a, s->dt, st));
-    prof_end(e, ADT_PROF_COMPACT, 4.0 * a * s->Lr * s->H * s->Dh * esize(s->dt), 0.0, st);
+    // every guidance branch moves the same accepted nodes
+    TRY(launch_kv_compact(s->d.k_cache, s->d.v_cache, s->nb, s->Lr * s->H, s->Dh, s->tcache_sb,
+                          (int64_t)s->d.s_cap * s->Dh, s->scal + SC_CL, 0, s->tr.path, 0, s->tr.nacc, 0, a, s->dt, st));
+    prof_end(e, ADT_PROF_COMPACT, 4.0 * s->nb * a * s->Lr * s->H * s->Dh * esize(s->dt), 0.0, st);
   }
-  TRY(launch_gather_rows(s->feat, s->tr.path, a + 1, s->dm,
-                         (char*)s->cfeat + (size_t)frow0 * s->dm * esize(s->dt), s->dt, st));
+  TRY(launch_gather_rows(s->feat, s->tr.path, a + 1, s->nb * s->dm,
+                         (char*)s->cfeat + (size_t)s->nb * frow0 * s->dm * esize(s->dt), s->dt, st));
   const int cell0 = L + 1 - P;
   std::vector<int32_t> committed;
   for (int m = 1; m <= a; ++m) committed.push_back(tok[path[m]]);
@@ -1128,5 +1183,8 @@ extern "C" adt_status adt_session_get_view(const adt_session* s, adt_session_vie
   v->att = s->att;
   v->act = s->act;
   v->resid = s->h;
+  v->n_branches = s->nb;
+  v->branch_logits = s->rawlog;
+  v->draft_branch_logits = s->draw;
   return ADT_OK;
 }

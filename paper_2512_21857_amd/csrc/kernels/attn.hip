@@ -31,8 +31,8 @@ template <int DH, int TPW>
 __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
-    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap,
-    int chunk, int splits, float scale_log2, float* __restrict__ part_o, float* __restrict__ part_ml) {
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
+    int kv_cap, int chunk, int splits, float scale_log2, float* __restrict__ part_o, float* __restrict__ part_ml) {
   constexpr int DT = DH / 16;   // 16-wide dimension tiles of O
   constexpr int KS = DH / 32;   // 32-deep k-steps of Q.K
   __shared__ __attribute__((aligned(16))) uint16_t Ks[ATT_KT][DH + 8];
@@ -74,10 +74,10 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
     if (i < n_my) {
       const int qr = (wave + 4 * i) * 16 + lq;
       if (qr < nq) {
-        const uint16_t* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+        const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
 #pragma unroll
         for (int t = 0; t < KS; ++t) qf[i][t] = *reinterpret_cast<const bf16x8*>(qp + t * 32 + g * 8);
-        const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+        const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
         mw0[i] = mp[0];
         mw1[i] = mp[1];
       }
@@ -227,8 +227,8 @@ template <int DH, int QTW, int QG>
 __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
-    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap,
-    float scale_log2, uint16_t* __restrict__ out) {
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
   constexpr int KG = AWG_W / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
   constexpr int VTW = AWG_KT + 4;                          // padded row of a transposed V step (8-byte aligned)
@@ -266,10 +266,10 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
     const int qr = (qg * QTW + t) * 16 + lq;
     if (qr < nq) {
-      const uint16_t* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+      const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[t][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
-      const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+      const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
       mw0[t] = mp[0];
       mw1[t] = mp[1];
     }
@@ -428,7 +428,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
         ls += wt * mml[((w0 + w) * 16 + row) * 2 + 1];
         acc += wt * mo[((size_t)(w0 + w) * 16 + row) * DH + d];
       }
-      out[(((int64_t)b * nq_max + qr) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
+      out[(((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
     }
     __syncthreads();
   }
@@ -439,8 +439,8 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 // the O partials is taken in split order.
 template <typename OutT>
 __global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const float* __restrict__ part_ml,
-                                         const int32_t* __restrict__ n_q, int H, int nq_max, int splits, int DH,
-                                         OutT* __restrict__ out) {
+                                         const int32_t* __restrict__ n_q, AttnRows rl, int H, int nq_max, int splits,
+                                         int DH, OutT* __restrict__ out) {
   __shared__ float wsh[ATT_MAX_SPLITS];
   __shared__ float red[4];
   const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
@@ -476,26 +476,26 @@ __global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const
     const float ws = wsh[s];
     if (ws != 0.f) acc += ws * part_o[(base + (int64_t)s * nq_max + qr) * DH + d];
   }
-  Elem<OutT>::store(out, (((int64_t)b * nq_max + qr) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
+  Elem<OutT>::store(out, (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
 }
 
 // fp32 path: one block per (query, head, sequence); scores staged in LDS.
 __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ kc, const float* __restrict__ vc, int64_t stride_b,
     int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
-    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, int H, int nq_max, int kv_cap, int DH,
-    float scale, float* __restrict__ out) {
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
+    int kv_cap, int DH, float scale, float* __restrict__ out) {
   extern __shared__ float smem[];      // DH query values, then kv_cap scores
   __shared__ float red[16];
   const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, tid = threadIdx.x;
   if (qr >= min(n_q[b], nq_max)) return;
   const int L = kv_len[b];
   const int total = min(L + n_tail[b], kv_cap);
-  const uint64_t* mp = mask + ((int64_t)b * nq_max + qr) * ADT_MASK_WORDS;
+  const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
   const uint64_t w0 = mp[0], w1 = mp[1];
   float* qs = smem;
   float* sc = smem + DH;
-  const float* qp = q + (((int64_t)b * nq_max + qr) * H + h) * DH;
+  const float* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
   for (int d = tid; d < DH; d += blockDim.x) qs[d] = qp[d];
   __syncthreads();
   const float* kb = kc + b * stride_b + h * stride_h;
@@ -528,7 +528,7 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
   for (int d = tid; d < DH; d += blockDim.x) {
     float acc = 0.f;
     for (int k = 0; k < total; ++k) acc += sc[k] * vb[(int64_t)k * DH + d];
-    out[(((int64_t)b * nq_max + qr) * H + h) * DH + d] = acc / sum;
+    out[(((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d] = acc / sum;
   }
 }
 
@@ -582,7 +582,7 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
 }
 
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
-                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
   if (attn_use_wg(B, H, Dh, nq_max, kv_cap)) {
     int qtw, qg;
@@ -592,7 +592,7 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
 #define ADT_ATTN_WG(DHV, QTWV, QGV)                                                                                \
   tree_attn_wg_kernel<DHV, QTWV, QGV><<<grid, AWG_W * WAVE, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
                                                                      (const uint16_t*)v, sb, sh, kv_len, n_q,      \
-                                                                     n_tail, mask, H, nq_max, kv_cap, sl2,         \
+                                                                     n_tail, mask, rl, H, nq_max, kv_cap, sl2,     \
                                                                      (uint16_t*)out)
     if (Dh == 128) {
       if (qtw == 1) ADT_ATTN_WG(128, 1, 1);
@@ -621,7 +621,8 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
 #define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
   tree_attn_bf16_kernel<DHV, TPWV><<<grid, ATT_THREADS, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
                                                                  (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail, \
-                                                                 mask, H, nq_max, kv_cap, p.chunk, p.splits, sl2, \
+                                                                 mask, rl, H, nq_max, kv_cap, p.chunk, p.splits,  \
+                                                                 sl2,                                             \
                                                                  part_o, part_ml)
   if (Dh == 128) {
     if (nq_max > 64) ADT_ATTN_LAUNCH(128, 2);
@@ -633,14 +634,14 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
 #undef ADT_ATTN_LAUNCH
   ADT_LAUNCH_CHECK();
   dim3 g2(nq_max, H, B);
-  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, H, nq_max, p.splits, Dh,
+  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, rl, H, nq_max, p.splits, Dh,
                                                          (uint16_t*)out);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
-                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
                             hipStream_t st) {
   if (dtype == ADT_F32) {
@@ -648,11 +649,12 @@ adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t
     ADT_CHECK_ARG(sm <= 60 * 1024, ADT_E_CAPACITY, "tree_attn f32: kv_cap %d too large for LDS scores", kv_cap);
     dim3 grid(nq_max, H, B);
     tree_attn_f32_kernel<<<grid, 128, sm, st>>>((const float*)q, (const float*)k, (const float*)v, sb, sh, kv_len,
-                                                n_q, n_tail, mask, H, nq_max, kv_cap, Dh, scale, (float*)out);
+                                                n_q, n_tail, mask, rl, H, nq_max, kv_cap, Dh, scale, (float*)out);
     ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
-  return attn_bf16(q, k, v, sb, sh, kv_len, n_q, n_tail, mask, B, H, Dh, nq_max, kv_cap, scale, out, ws, ws_bytes, st);
+  return attn_bf16(q, k, v, sb, sh, kv_len, n_q, n_tail, mask, rl, B, H, Dh, nq_max, kv_cap, scale, out, ws, ws_bytes,
+                   st);
 }
 
 }  // namespace adt

@@ -125,8 +125,9 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
       const int n0 = nt * 16, region = n0 / d, within = n0 % d, head = within / Dh, u = (within % Dh) / 16;
       const int j = 8 * u + 4 * g;   // element of the head's first half held in y[0]
       float a[4] = {y[0], y[1], y[2], y[3]}, b[4] = {y2[0], y2[1], y2[2], y2[3]};
+      const int node = e.nb == 1 ? row : row >> 1, branch = row - node * e.nb;
       if (region < 2) {
-        const float2* cs = e.rope + (int64_t)e.pos[row] * half + j;
+        const float2* cs = e.rope + (int64_t)e.pos[node] * half + j;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float2 t = cs[r];
@@ -136,7 +137,8 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
         }
       }
       uint16_t* dst = region == 0 ? e.q + (int64_t)row * d + head * Dh
-                                  : (region == 1 ? e.kc : e.vc) + head * e.stride_h + (*e.slot0 + (int64_t)row) * Dh;
+                                  : (region == 1 ? e.kc : e.vc) + branch * e.cache_sb + head * e.stride_h +
+                                        (*e.slot0 + (int64_t)node) * Dh;
       *reinterpret_cast<u16x4*>(dst + j) = u16x4{f2bf(a[0]), f2bf(a[1]), f2bf(a[2]), f2bf(a[3])};
       *reinterpret_cast<u16x4*>(dst + j + half) = u16x4{f2bf(b[0]), f2bf(b[1]), f2bf(b[2]), f2bf(b[3])};
     }
@@ -380,6 +382,7 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     case EPI_STORE: ADT_CHECK_ARG(epi.out && epi.ldo % 4 == 0, ADT_E_ARG, "gemm: store target"); break;
     case EPI_RESID: ADT_CHECK_ARG(epi.h && epi.ssp_out, ADT_E_ARG, "gemm: residual epilogue buffers"); break;
     case EPI_QKV:
+      ADT_CHECK_ARG(epi.nb == 1 || epi.nb == 2, ADT_E_ARG, "gemm: QKV epilogue branches %d", epi.nb);
       ADT_CHECK_ARG(epi.Dh >= 16 && epi.Dh % 16 == 0 && N % (3 * epi.Dh) == 0 && epi.q && epi.kc && epi.vc &&
                         epi.slot0 && epi.pos && epi.rope,
                     ADT_E_ARG, "gemm: QKV epilogue (Dh=%d, N=%d)", epi.Dh, N);

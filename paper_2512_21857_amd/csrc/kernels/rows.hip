@@ -14,10 +14,11 @@ constexpr int ROW_THREADS = 256;
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                  int d, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ a, float* __restrict__ ssp) {
+                                                                 T* __restrict__ a, float* __restrict__ ssp,
+                                                                 Branches br) {
   __shared__ float red[16];
   const int m = blockIdx.x;
-  const T* e = E + (int64_t)tok[m] * d;
+  const T* e = E + (int64_t)tok[m / br.nb + (m % br.nb) * br.tok_boff] * d;
   if (ssp) {
     // per 16-column tile: copy to h and the tile's sum of squares (columns in order)
     for (int t = threadIdx.x; t < d / 16; t += blockDim.x) {
@@ -70,11 +71,14 @@ __global__ __launch_bounds__(ROW_THREADS) void norm_rows_kernel(const float* __r
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                   const int32_t* __restrict__ fsrc, const T* __restrict__ fa,
-                                                                  const T* __restrict__ fb, int d, T* __restrict__ x) {
-  const int m = blockIdx.x;
-  const T* e = E + (int64_t)tok[m] * d;
-  const int s = fsrc[m];
-  const T* f = s >= 0 ? fa + (int64_t)s * d : (s <= -2 ? fb + (int64_t)(-s - 2) * d : nullptr);
+                                                                  const T* __restrict__ fb, int d, T* __restrict__ x,
+                                                                  Branches br) {
+  const int m = blockIdx.x, node = m / br.nb, b = m % br.nb;
+  const T* e = E + (int64_t)tok[node + b * br.tok_boff] * d;
+  const int s = fsrc[node];
+  // feature sources hold the branches of one node in consecutive rows
+  const T* f = s >= 0 ? fa + ((int64_t)s * br.nb + b) * d
+                      : (s <= -2 ? fb + ((int64_t)(-s - 2) * br.nb + b) * d : nullptr);
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     x[(int64_t)m * 2 * d + i] = e[i];
     if (f) x[(int64_t)m * 2 * d + d + i] = f[i];
@@ -172,8 +176,8 @@ __global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __re
                                                                const int32_t* __restrict__ slot0,
                                                                const float2* __restrict__ rope, T* __restrict__ qout,
                                                                T* __restrict__ kc, T* __restrict__ vc,
-                                                               int64_t stride_h) {
-  const int m = blockIdx.x;
+                                                               int64_t stride_h, Branches br) {
+  const int m = blockIdx.x, node = m / br.nb;
   const int d = H * Dh, N = 3 * d, half = Dh / 2;
   const int i = blockIdx.y * blockDim.x + threadIdx.x;
   if (i >= H * half) return;
@@ -191,8 +195,10 @@ __global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __re
     v1 += p[2 * d + c1];
     v2 += p[2 * d + c2];
   }
-  const float2 cs = rope[(int64_t)pos[m] * half + j];
-  const int64_t slot = *slot0 + m;
+  const float2 cs = rope[(int64_t)pos[node] * half + j];
+  const int64_t slot = *slot0 + node;
+  kc += (m % br.nb) * br.cache_sb;
+  vc += (m % br.nb) * br.cache_sb;
   Elem<T>::store(qout, (int64_t)m * d + c1, q1 * cs.x - q2 * cs.y);
   Elem<T>::store(qout, (int64_t)m * d + c2, q2 * cs.x + q1 * cs.y);
   T* kr = kc + hh * stride_h + slot * Dh;
@@ -247,12 +253,13 @@ __global__ void gather_rows_kernel(const T* __restrict__ src, const int32_t* __r
 template <typename T, int ROWS_MAX>
 __global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__ kc, T* __restrict__ vc, int Dh,
                                                                  int64_t stride_b, int64_t stride_s,
-                                                                 const int32_t* __restrict__ kv_len,
+                                                                 const int32_t* __restrict__ kv_len, int kv_stride,
                                                                  const int32_t* __restrict__ path, int path_stride,
-                                                                 const int32_t* __restrict__ n_acc, int a_max) {
+                                                                 const int32_t* __restrict__ n_acc, int acc_stride,
+                                                                 int a_max) {
   const int sl = blockIdx.x, b = blockIdx.y;
-  const int a = min(n_acc[b], a_max);
-  const int L = kv_len[b];
+  const int a = min(n_acc[b * acc_stride], a_max);
+  const int L = kv_len[b * kv_stride];
   const int per_row = Dh * (int)sizeof(T) / 16;        // 16-byte pieces per row
   const int pieces = a * per_row;
   u16x8 kr[ROWS_MAX], vr[ROWS_MAX];
@@ -277,6 +284,25 @@ __global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__
       reinterpret_cast<u16x8*>(kb + (int64_t)(L + m) * Dh)[c] = kr[it];
       reinterpret_cast<u16x8*>(vb + (int64_t)(L + m) * Dh)[c] = vr[it];
     }
+  }
+}
+
+// Classifier-free guidance on logits: out[i][v] = u + s (c - u) with c = raw[2i][v] (the
+// conditional branch) and u = raw[2i + 1][v].  Grid (V / 4 / 256 rounded up, rows).
+__global__ void guide_rows_kernel(const float* __restrict__ raw, int V, float scale, float* __restrict__ out,
+                                  int64_t ldo) {
+  const int i = blockIdx.y;
+  const float* c = raw + (int64_t)2 * i * V;
+  const float* u = c + V;
+  float* o = out + (int64_t)i * ldo;
+  const int v = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (v + 4 <= V) {
+    const float4 a = *reinterpret_cast<const float4*>(c + v), b = *reinterpret_cast<const float4*>(u + v);
+    *reinterpret_cast<float4*>(o + v) =
+        make_float4(b.x + scale * (a.x - b.x), b.y + scale * (a.y - b.y), b.z + scale * (a.z - b.z),
+                    b.w + scale * (a.w - b.w));
+  } else {
+    for (int j = v; j < V; ++j) o[j] = u[j] + scale * (c[j] - u[j]);
   }
 }
 
@@ -318,9 +344,9 @@ __global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int3
   }
 
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
-                             int dtype, hipStream_t st) {
+                             int dtype, hipStream_t st, const Branches& br) {
   ADT_CHECK_ARG((a != nullptr) != (ssp != nullptr) && (!ssp || d % 16 == 0), ADT_E_ARG, "embed_norm: outputs");
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, ssp));
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, ssp, br));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -334,9 +360,9 @@ adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, floa
 }
 
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
-                              int M, int d, void* x, int dtype, hipStream_t st) {
+                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br) {
   ADT_DISPATCH_T(dtype, draft_input_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, fsrc, (const T*)fa,
-                                                                          (const T*)fb, d, (T*)x));
+                                                                          (const T*)fb, d, (T*)x, br));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -360,10 +386,10 @@ adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, h
 
 adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos,
                            const int32_t* slot0, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
-                           int dtype, hipStream_t st) {
+                           int dtype, hipStream_t st, const Branches& br) {
   dim3 grid(M, (H * Dh / 2 + ROW_THREADS - 1) / ROW_THREADS);
   ADT_DISPATCH_T(dtype, qkv_rope_kernel<T><<<grid, ROW_THREADS, 0, st>>>(part, splits, M, H, Dh, pos, slot0, rope,
-                                                                          (T*)qout, (T*)kc, (T*)vc, stride_h));
+                                                                          (T*)qout, (T*)kc, (T*)vc, stride_h, br));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -392,27 +418,31 @@ adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int 
 }
 
 adt_status launch_kv_compact(void* k, void* v, int B, int slices, int Dh, int64_t sb, int64_t ss, const int32_t* kv_len,
-                             const int32_t* path, int path_stride, const int32_t* n_acc, int a_max, int dtype,
-                             hipStream_t st) {
+                             int kv_stride, const int32_t* path, int path_stride, const int32_t* n_acc, int acc_stride,
+                             int a_max, int dtype, hipStream_t st) {
   const int bytes_row = Dh * (dtype == ADT_BF16 ? 2 : 4);
   ADT_CHECK_ARG(bytes_row % 16 == 0, ADT_E_SHAPE, "kv_compact: row of %d bytes not a multiple of 16", bytes_row);
   const int pieces = a_max * bytes_row / 16;
   dim3 grid(slices, B);
+#define ADT_COMPACT(T, RM)                                                                                        \
+  kv_compact_kernel<T, RM><<<grid, ROW_THREADS, 0, st>>>((T*)k, (T*)v, Dh, sb, ss, kv_len, kv_stride, path,       \
+                                                         path_stride, n_acc, acc_stride, a_max)
   if (dtype == ADT_BF16) {
-    if (pieces <= 4 * ROW_THREADS)
-      kv_compact_kernel<uint16_t, 4><<<grid, ROW_THREADS, 0, st>>>((uint16_t*)k, (uint16_t*)v, Dh, sb, ss, kv_len, path,
-                                                                  path_stride, n_acc, a_max);
-    else
-      kv_compact_kernel<uint16_t, 16><<<grid, ROW_THREADS, 0, st>>>((uint16_t*)k, (uint16_t*)v, Dh, sb, ss, kv_len,
-                                                                   path, path_stride, n_acc, a_max);
+    if (pieces <= 4 * ROW_THREADS) ADT_COMPACT(uint16_t, 4);
+    else ADT_COMPACT(uint16_t, 16);
   } else {
-    if (pieces <= 4 * ROW_THREADS)
-      kv_compact_kernel<float, 4><<<grid, ROW_THREADS, 0, st>>>((float*)k, (float*)v, Dh, sb, ss, kv_len, path,
-                                                               path_stride, n_acc, a_max);
-    else
-      kv_compact_kernel<float, 16><<<grid, ROW_THREADS, 0, st>>>((float*)k, (float*)v, Dh, sb, ss, kv_len, path,
-                                                                path_stride, n_acc, a_max);
+    if (pieces <= 4 * ROW_THREADS) ADT_COMPACT(float, 4);
+    else ADT_COMPACT(float, 16);
   }
+#undef ADT_COMPACT
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_guide_rows(const float* raw, int rows, int V, float scale, float* out, int64_t ldo, hipStream_t st) {
+  if (rows <= 0) return ADT_OK;
+  dim3 grid((V / 4 + ROW_THREADS) / ROW_THREADS, rows);
+  guide_rows_kernel<<<grid, ROW_THREADS, 0, st>>>(raw, V, scale, out, ldo);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -5,12 +5,28 @@
 
 namespace adt {
 
+// Guidance branches of a forward (classifier-free guidance): row r is node r / nb of branch
+// r % nb (branch 0 conditional, 1 unconditional; nb = 1 without guidance).  The token of row
+// r is tok[node + branch * tok_boff] (tok_boff = 0: the branches share one token list); the
+// caches of branch b start cache_sb elements after those of branch 0.
+struct Branches {
+  int nb = 1;
+  int tok_boff = 0;
+  int64_t cache_sb = 0;
+};
+
 // attn.hip
+// Row of query qr of sequence b in q and out: b * rs_b + qr * rs_i (rows of H * Dh); its mask
+// row: b * ms_b + qr.  Separate sequences: (nq_max, 1, nq_max).  Guidance branches of one
+// tree interleaved node by node: (1, B, 0), one mask per node.
+struct AttnRows {
+  int rs_b, rs_i, ms_b;
+};
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype);
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
-                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, int B, int H, int Dh,
-                            int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
-                            hipStream_t st);
+                            const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H,
+                            int Dh, int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws,
+                            size_t ws_bytes, hipStream_t st);
 
 // gemm.hip
 size_t packed_bytes(int total_rows, int K, int dtype);
@@ -44,6 +60,8 @@ struct GemmEpi {
   const int32_t* pos = nullptr;
   const float2* rope = nullptr;
   int Dh = 0;
+  int nb = 1;              // guidance branches: row m is node m / nb of branch m % nb, whose
+  int64_t cache_sb = 0;    // caches sit cache_sb elements further; q keeps row m
   // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up
   uint16_t* act = nullptr;
 };
@@ -57,25 +75,29 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
 // h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
 // of squares of h into ssp[m][d/16].
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
-                             int dtype, hipStream_t st);
+                             int dtype, hipStream_t st, const Branches& br = Branches{});
 // out[m][c] = h[m][c] * scale(m), the scale from ssp[m][d/16], rounded to the model dtype.
 adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, float eps, void* out, int dtype,
                             hipStream_t st);
+// x[m] = [E[token] ; parent feature]: fsrc >= 0 is a node of fa, -1 zeros, <= -2 node
+// (-2 - fsrc) of fb; fa and fb hold the nb branch rows of a node consecutively.
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
-                              int M, int d, void* x, int dtype, hipStream_t st);
+                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br = Branches{});
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
                            int dtype, hipStream_t st);
 adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, hipStream_t st);
 adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos,
                            const int32_t* slot0, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
-                           int dtype, hipStream_t st);
+                           int dtype, hipStream_t st, const Branches& br = Branches{});
 adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st);
 adt_status launch_reduce_store(const float* part, int splits, int M, int N, float* out, int64_t ldo, hipStream_t st);
 adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,
                               hipStream_t st);
 adt_status launch_kv_compact(void* k, void* v, int B, int slices, int Dh, int64_t sb, int64_t ss, const int32_t* kv_len,
-                             const int32_t* path, int path_stride, const int32_t* n_acc, int a_max, int dtype,
-                             hipStream_t st);
+                             int kv_stride, const int32_t* path, int path_stride, const int32_t* n_acc, int acc_stride,
+                             int a_max, int dtype, hipStream_t st);
+// out[i] = u + scale (c - u) over V logits, c = raw[2i], u = raw[2i + 1] (rows of V floats).
+adt_status launch_guide_rows(const float* raw, int rows, int V, float scale, float* out, int64_t ldo, hipStream_t st);
 adt_status launch_tree_masks(const int32_t* parent, const int32_t* n_nodes, int B, int n_max, uint64_t* mask,
                              int32_t* depth, hipStream_t st);
 

@@ -227,9 +227,12 @@ class DeviceSession:
         dev = model.device
         self.s_cap = ((cfg.prefix_len + cfg.n_image + abi.MAX_NODES + 63) // 64) * 64
         tdt = TORCH_DT[model.dtype]
-        self.k_cache = torch.zeros(m.n_layers, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
+        guided = getattr(cfg, "guidance", None) is not None
+        self.nb = 2 if guided else 1
+        br = (2,) if guided else ()       # guidance: conditional and unconditional caches
+        self.k_cache = torch.zeros(*br, m.n_layers, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
         self.v_cache = torch.zeros_like(self.k_cache)
-        self.dk_cache = torch.zeros(m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
+        self.dk_cache = torch.zeros(*br, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
         self.dv_cache = torch.zeros_like(self.dk_cache)
         allowed = np.ascontiguousarray(cfg.allowed_table().reshape(-1), dtype=np.int32)
         self._allowed = (C.c_int32 * allowed.size)(*allowed.tolist())
@@ -246,7 +249,8 @@ class DeviceSession:
                                C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched, cfg.grid_w), self.accept,
                                C.cast(self._poisson, C.POINTER(C.c_int32)) if self._poisson is not None else None,
                                1 if fixed_tree else 0, _p(draft_table),
-                               0 if draft_table is None else draft_table.shape[0], 1 if use_graphs else 0, None, 0)
+                               0 if draft_table is None else draft_table.shape[0], 1 if use_graphs else 0,
+                               1 if guided else 0, float(cfg.guidance) if guided else 0.0, None, 0)
         self.draft_table = draft_table
         need = lib().adt_session_workspace_size(model.handle, C.byref(desc))
         if need == 0:
@@ -264,8 +268,12 @@ class DeviceSession:
             self.handle = None
 
     # -- cycle pieces ----------------------------------------------------------------------
-    def prefill(self, prefix: np.ndarray) -> int:
-        arr = (C.c_int32 * len(prefix))(*[int(x) for x in prefix])
+    def prefill(self, prefix: np.ndarray, uncond_prefix: Optional[np.ndarray] = None) -> int:
+        """prefix: the prompt ids; with guidance also the unconditional prompt (same length)."""
+        ids = list(prefix) + (list(uncond_prefix) if self.nb == 2 else [])
+        if (self.nb == 2) != (uncond_prefix is not None):
+            raise ValueError("an unconditional prompt is needed exactly when the session is guided")
+        arr = (C.c_int32 * len(ids))(*[int(x) for x in ids])
         first = C.c_int32()
         check(lib().adt_session_prefill(self.handle, arr, C.byref(first), _stream()))
         return first.value
@@ -312,10 +320,11 @@ class DeviceSession:
         n = v.n_nodes
         tdt = TORCH_DT[self.model.dtype]
         s = self.cfg.sched
-        return {
+        nb = v.n_branches
+        out = {
             "L": v.L, "Ld": v.Ld, "n": n, "step": v.step,
             "logits": self._ws(v.logits, n * m.vocab, torch.float32).view(n, m.vocab),
-            "feat": self._ws(v.feat, n * m.d_model, tdt).view(n, m.d_model),
+            "feat": self._ws(v.feat, n * nb * m.d_model, tdt).view(n, nb, m.d_model).squeeze(1),
             "draft_logits": self._ws(v.draft_logits, (1 + (s.d_hi - 1) * s.k_hi) * m.vocab,
                                      torch.float32).view(-1, m.vocab),
             "parent": self._ws(v.parent, n, torch.int32), "token": self._ws(v.token, n, torch.int32),
@@ -326,6 +335,10 @@ class DeviceSession:
             "bonus": self._ws(v.bonus, 1, torch.int32),
             "tokens": [v.tokens_host[i] for i in range(v.n_tokens)],
         }
+        if nb == 2:
+            out["branch_logits"] = self._ws(v.branch_logits, n * 2 * m.vocab, torch.float32).view(n, 2, m.vocab)
+            out["draft_branch_logits"] = self._ws(v.draft_branch_logits, 2 * m.vocab, torch.float32).view(2, m.vocab)
+        return out
 
 
 def _step_dict(o: abi.StepOut) -> dict:

@@ -48,18 +48,32 @@ def _greedy_margin(row, lo, hi):
     return seg[-1] - seg[-2] if len(seg) > 1 else np.inf
 
 
+def _guided_ok(got, ref, branch_refs, s, tol):
+    """Guided logits u + s (c - u): each branch within tol moves them by at most
+    (|1 - s| + s) (atol + rtol max(|c|, |u|))."""
+    k = abs(1.0 - s) + s
+    scale = np.maximum(np.abs(branch_refs[0]), np.abs(branch_refs[1]))
+    return np.abs(got - ref) <= k * (tol[0] + tol[1] * scale)
+
+
 def _compare_run(rt, cfg, n_steps, fixed_tree=False, label="", shapes=None):
     """Runs GPU adt_step and the oracle decoder side by side; returns (steps matched, flag).
     shapes, if a list, receives every compared (d_hat, k_hat)."""
     _, om, dm, pre = _setup(rt, cfg)
     sess = rt.DeviceSession(dm, cfg, fixed_tree=fixed_tree)
-    dec = Decoder(cfg, om, pre)
+    guided = cfg.guidance is not None
+    null = synth.null_prefix_ids(cfg) if guided else None
+    dec = Decoder(cfg, om, pre, uncond_prefix=null)
     if fixed_tree:
         s = cfg.sched
         dec.schedule_next = lambda: (min(s.d_hi, cfg.n_image - (dec.L + 1 - dec.P) - 1), s.k_hi)
     tol = TOL[cfg.model.dtype]
-    g_first = sess.prefill(pre)
+    g_first = sess.prefill(pre, null)
     o_first = dec.prefill()
+    if guided:
+        gl = sess.tensors()["logits"][0].cpu().numpy()
+        assert _guided_ok(gl, dec.prefill_logits, dec.prefill_branch_logits, cfg.guidance, tol).all(), \
+            f"guided prefill logits outside tolerance: {np.abs(gl - dec.prefill_logits).max()}"
     if g_first != o_first:
         return 0, "first token differs (near-tie)"
     matched = 0
@@ -73,7 +87,15 @@ def _compare_run(rt, cfg, n_steps, fixed_tree=False, label="", shapes=None):
             shapes.append((o.d_hat, o.k_hat))
         if o.draft_root_logits is not None:
             gd = t["draft_logits"][0].cpu().numpy()
-            assert _tol_ok(gd, o.draft_root_logits, tol).all(), \
+            if guided:
+                gb = t["draft_branch_logits"].cpu().numpy()
+                for b in range(2):
+                    assert _tol_ok(gb[b], dec.draft_root_branch_logits[b], tol).all(), \
+                        f"draft root logits of branch {b} outside tolerance at step {o.step}"
+                ok = _guided_ok(gd, o.draft_root_logits, dec.draft_root_branch_logits, cfg.guidance, tol)
+            else:
+                ok = _tol_ok(gd, o.draft_root_logits, tol)
+            assert ok.all(), \
                 f"draft root logits outside tolerance at step {o.step}: {np.abs(gd - o.draft_root_logits).max()}"
         same_tree = (t["n"] == o.tree.n and t["parent"].cpu().tolist() == o.tree.parent.tolist()
                      and t["token"].cpu().tolist() == o.tree.token.tolist())
@@ -81,7 +103,14 @@ def _compare_run(rt, cfg, n_steps, fixed_tree=False, label="", shapes=None):
             return matched, f"tree differs at step {o.step}"
         assert t["depth"].cpu().tolist() == o.tree.depth.tolist()
         glog = t["logits"].cpu().numpy()
-        ok = _tol_ok(glog, o.logits, tol)
+        if guided:
+            gb = t["branch_logits"].cpu().numpy()
+            for b in range(2):
+                assert _tol_ok(gb[:, b], dec.verify_branch_logits[b], tol).all(), \
+                    f"verify logits of branch {b} outside tolerance at step {o.step}"
+            ok = _guided_ok(glog, o.logits, dec.verify_branch_logits, cfg.guidance, tol)
+        else:
+            ok = _tol_ok(glog, o.logits, tol)
         assert ok.all(), f"verify logits outside tolerance at step {o.step}: max err {np.abs(glog - o.logits).max()}"
         if g["tokens"] != o.committed:
             # near-tie rule: some decision on the oracle's walk had a margin below tolerance
@@ -121,6 +150,26 @@ def test_tiny_full_image_init_rules(rt, rule):
         assert any(k > cfg.sched.k_hi for _, k in shapes)     # one-layer trees wider than k_hi ran
     if rule == "random":
         assert len(set(shapes)) >= 6
+
+
+@pytest.mark.parametrize("scale,prefix_len", [(3.0, 100), (1.5, 40)])
+def test_tiny_full_image_guided(rt, scale, prefix_len):
+    """Classifier-free guidance in target and draft (Sec. 3.1, Fig. 5 caption) over the whole
+    image: both branches' logits within tolerance, guided logits within the propagated bound,
+    schedule, trees and committed tokens bit-exact.  A 100-id prompt is prefilled in two
+    chunks (64 nodes = 128 rows, then 36)."""
+    cfg = synth.get_config("tiny")
+    cfg = dataclasses.replace(cfg, guidance=scale, prefix_len=prefix_len)
+    matched, flag = _compare_run(rt, cfg, 10_000, label=f"tiny-guided-{scale}")
+    print("guided", scale, "matched", matched, flag)
+    assert flag is None and matched >= 1
+
+
+def test_bf16_small_guided(rt):
+    cfg = dataclasses.replace(_small_bf16(), guidance=3.0)
+    matched, flag = _compare_run(rt, cfg, 30, label="bf16-small-guided")
+    print("bf16 small guided matched", matched, flag)
+    assert flag is None or "tree differs" in flag or "near-tie" in flag
 
 
 def test_tiny_fixed_deep_tree(rt):
@@ -189,7 +238,9 @@ def _planted(rt, cfg, m, extra_rng=0):
     ranks plus distractors.  Verify + accept + compact must give a = m, bonus = AR token m+1
     and a compacted cache equal to the oracle's."""
     w, om, dm, pre = _setup(rt, cfg)
-    ar, _ = ar_decode(cfg, om, pre, n_tokens=m + 2)
+    guided = cfg.guidance is not None
+    null = synth.null_prefix_ids(cfg) if guided else None
+    ar, _ = ar_decode(cfg, om, pre, n_tokens=m + 2, uncond_prefix=null)
     rng = np.random.default_rng(extra_rng)
     V = cfg.model.vocab
     lo, hi = cfg.img_lo, cfg.img_hi
@@ -207,8 +258,8 @@ def _planted(rt, cfg, m, extra_rng=0):
         cur = base + kids.index(ar[j])
     # BFS order already holds: each level's children are appended after the previous level
     sess = rt.DeviceSession(dm, cfg)
-    first = sess.prefill(pre)
-    dec = Decoder(cfg, om, pre)
+    first = sess.prefill(pre, null)
+    dec = Decoder(cfg, om, pre, uncond_prefix=null)
     assert dec.prefill() == first == ar[0]
     sess.set_tree(parent, token)
     sess.verify()
@@ -218,16 +269,28 @@ def _planted(rt, cfg, m, extra_rng=0):
     info = dec.verify_commit(tree, m, 1)
     glog = t["logits"].cpu().numpy()
     tol = TOL[cfg.model.dtype]
-    assert _tol_ok(glog, info.logits, tol).all(), f"max err {np.abs(glog - info.logits).max()}"
+    if guided:
+        ok = _guided_ok(glog, info.logits, dec.verify_branch_logits, cfg.guidance, tol)
+    else:
+        ok = _tol_ok(glog, info.logits, tol)
+    assert ok.all(), f"max err {np.abs(glog - info.logits).max()}"
     out = sess.accept_commit(m, 1)
     assert out["n_accepted"] == m and out["tokens"] == ar[1:m + 2]
     assert info.committed == out["tokens"]
     L0 = len(pre)
     n_keep = L0 + m + 1
-    gk = sess.k_cache.float().cpu().numpy()[:, :, :n_keep]
-    gv = sess.v_cache.float().cpu().numpy()[:, :, :n_keep]
-    assert _tol_ok(gk, dec.tcache.k[:, :, :n_keep], tol).all()
-    assert _tol_ok(gv, dec.tcache.v[:, :, :n_keep], tol).all()
+    for b, br in enumerate(dec.branches):
+        gk = (sess.k_cache[b] if guided else sess.k_cache).float().cpu().numpy()[:, :, :n_keep]
+        gv = (sess.v_cache[b] if guided else sess.v_cache).float().cpu().numpy()[:, :, :n_keep]
+        assert _tol_ok(gk, br.tcache.k[:, :, :n_keep], tol).all(), f"compacted K of branch {b}"
+        assert _tol_ok(gv, br.tcache.v[:, :, :n_keep], tol).all(), f"compacted V of branch {b}"
+    if guided and not dec.done():
+        # the next cycle's draft catch-up reads the committed features of both branches
+        o, g = dec.step(), sess.step()
+        assert (g["d_hat"], g["k_hat"]) == (o.d_hat, o.k_hat)
+        gb = sess.tensors()["draft_branch_logits"].cpu().numpy()
+        for b in range(2):
+            assert _tol_ok(gb[b], dec.draft_root_branch_logits[b], tol).all(), f"draft root of branch {b}"
 
 
 @pytest.mark.parametrize("m", [0, 1, 3, 4])
@@ -237,6 +300,15 @@ def test_planted_path_tiny(rt, m):
 
 def test_planted_path_bf16_small(rt):
     _planted(rt, _small_bf16(), 5, extra_rng=9)
+
+
+@pytest.mark.parametrize("m", [0, 3])
+def test_planted_path_tiny_guided(rt, m):
+    _planted(rt, dataclasses.replace(synth.get_config("tiny"), guidance=3.0), m, extra_rng=m)
+
+
+def test_planted_path_bf16_small_guided(rt):
+    _planted(rt, dataclasses.replace(_small_bf16(), guidance=3.0), 5, extra_rng=9)
 
 
 @pytest.mark.parametrize("graphs", [(True, True), (True, False)])
