@@ -730,12 +730,12 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
   auto attention = [&](char* kc, char* vc) -> adt_status {
     // the prefix K/V once, tree Q/K/V in and O out, the masks
-    const int e = prof_begin(st);
+    const int e = prof_pair();
     TRY(launch_tree_attn(s->q, kc, vc, cache_sb, stride_h, s->scal + SC_KV, s->scal + SC_NQ, s->scal + SC_TAIL, mask,
                          AttnRows{1, nb, 0}, nb, H, Dh, M, s->d.s_cap, scale, dt, s->att, s->attn_ws,
-                         s->attn_ws_bytes, st));
-    prof_end(e, ADT_PROF_ATTN, nb * (2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es) + 16.0 * M,
-             4.0 * rows * (L_pre + n_tail) * H * Dh, st);
+                         s->attn_ws_bytes, st, e >= 0 ? g_prof.ev[e] : nullptr, e >= 0 ? g_prof.ev[e + 1] : nullptr));
+    prof_done(e, ADT_PROF_ATTN, nb * (2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es) + 16.0 * M,
+              4.0 * rows * (L_pre + n_tail) * H * Dh);
     return ADT_OK;
   };
   if (dt == ADT_BF16) {

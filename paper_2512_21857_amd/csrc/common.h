@@ -17,12 +17,9 @@ typedef uint16_t u16x4 __attribute__((ext_vector_type(4)));
 constexpr int WAVE = 64;
 constexpr float LOG2E = 1.4426950408889634f;
 
-// float -> bfloat16 bits, round to nearest even (finite inputs).
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+// float -> bfloat16 bits, round to nearest even (gfx950 converts in hardware,
+// v_cvt_pk_bf16_f32, two values per instruction when paired).
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
 template <typename T> struct Elem;

@@ -8,11 +8,14 @@
 //   S^T[key][q] = K[key][:] . Q[q][:]        (A = K rows, B = Q^T)
 //   O^T[d][q]  += V^T[d][key] . P^T[key][q]  (A = V^T rows, B = P^T)
 // so each lane owns one query column and the online-softmax rescale is a per-lane scalar.
-// Probabilities enter the second product as three bf16 parts (three MFMAs), so the result
-// is as accurate as fp32 accumulation of the bf16 inputs.
+// Probabilities enter the second product rounded to bf16 (relative error 2^-9 per term, below
+// the bf16 rounding of the output itself); steps wholly inside the unmasked prefix skip the
+// mask test, and the running output is rescaled only when some row's maximum moved.
 // Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
 // Few pairs (one image's forwards): tree_attn_wg_kernel below, one workgroup per pair whose
 // waves split the keys and merge in LDS.
+#include <hip/hip_ext.h>
+
 #include "../launch.h"
 
 namespace adt {
@@ -132,15 +135,25 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
       }
       // lane (lq, g) now holds S for query (wave + 4i)*16 + lq and keys kb + sub*16 + 4g + r.
       float mx = -INFINITY;
+      if (kb + ATT_KT <= min(L, k_end)) {
 #pragma unroll
-      for (int sub = 0; sub < 4; ++sub) {
+        for (int sub = 0; sub < 4; ++sub)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = kb + sub * 16 + 4 * g + r;
-          const bool vis = key < k_end && (key < L || tail_visible(mw0[i], mw1[i], key - L));
-          const float v = vis ? st[sub][r] * scale_log2 : -INFINITY;
-          st[sub][r] = v;
-          mx = fmaxf(mx, v);
+          for (int r = 0; r < 4; ++r) {
+            st[sub][r] *= scale_log2;
+            mx = fmaxf(mx, st[sub][r]);
+          }
+      } else {
+#pragma unroll
+        for (int sub = 0; sub < 4; ++sub) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = kb + sub * 16 + 4 * g + r;
+            const bool vis = key < k_end && (key < L || tail_visible(mw0[i], mw1[i], key - L));
+            const float v = vis ? st[sub][r] * scale_log2 : -INFINITY;
+            st[sub][r] = v;
+            mx = fmaxf(mx, v);
+          }
         }
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
@@ -162,31 +175,21 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
       rs += __shfl_xor(rs, 32, WAVE);
       l_run[i] = l_run[i] * alpha + rs;
       m_run[i] = m_new;
+      if (!__all(alpha == 1.f)) {
 #pragma unroll
-      for (int d = 0; d < DT; ++d) o[i][d] *= alpha;
+        for (int d = 0; d < DT; ++d) o[i][d] *= alpha;
+      }
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
-        // P = P1 + P2 + P3, each part in bf16 (three MFMAs): the probabilities enter the
-        // product with about 24 bits, so it is as accurate as fp32 accumulation.
-        bf16x8 p1, p2, p3;
+        bf16x8 p1;
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const float pv = r < 4 ? st[2 * h2][r] : st[2 * h2 + 1][r - 4];
-          const uint16_t b1 = f2bf(pv);
-          const float r1 = pv - bf2f(b1);
-          const uint16_t b2 = f2bf(r1);
-          p1[r] = __builtin_bit_cast(__bf16, b1);
-          p2[r] = __builtin_bit_cast(__bf16, b2);
-          p3[r] = __builtin_bit_cast(__bf16, f2bf(r1 - bf2f(b2)));
-        }
+        for (int r = 0; r < 8; ++r) p1[r] = (__bf16)(r < 4 ? st[2 * h2][r] : st[2 * h2 + 1][r - 4]);
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
           const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 4 * g]);
           const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 16 + 4 * g]);
           const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
           o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[i][d], 0, 0, 0);
-          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p2, o[i][d], 0, 0, 0);
-          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p3, o[i][d], 0, 0, 0);
         }
       }
     }
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
-    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out, int pairs, int qsplit) {
   constexpr int KG = AWG_W / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
   constexpr int VTW = AWG_KT + 4;                          // padded row of a transposed V step (8-byte aligned)
@@ -237,16 +240,26 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
   constexpr int MG_BYTES = AWG_W * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
-  const int h = blockIdx.x, b = blockIdx.y;
+  // Workgroup i takes query slice qs of pair p, with i = (p / 8) * 8 qsplit + 8 qs + p % 8:
+  // workgroups are dealt to the 8 XCDs in turn, so every slice of a pair runs on one XCD
+  // and its K/V come from HBM into that XCD's L2 once.
+  const int grp = blockIdx.x / (8 * qsplit), rem = blockIdx.x % (8 * qsplit);
+  const int qs = rem / 8, pair = grp * 8 + rem % 8;
+  const int tile0 = qs * QG * QTW;                         // first query tile of this slice
+  // padding, or a slice past every tree: no keys and no rows (no early exit, which would
+  // put a wait for the arguments before the loads below)
+  const bool dead = pair >= pairs || tile0 * 16 >= nq_max;
+  const int h = dead ? 0 : pair % H, b = dead ? 0 : pair / H;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int qg = wave / KG, kg = wave % KG;
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
   const int L = kv_len[b];
-  const int nq = min(n_q[b], nq_max);
-  const int total = min(L + n_tail[b], kv_cap);
+  const int nq = dead ? 0 : min(n_q[b], nq_max);
+  const int total = dead ? 0 : min(L + n_tail[b], kv_cap);
   int per = (total + KG - 1) / KG;
   per = (per + 15) / 16 * 16;
   const int k0 = min(total, kg * per), k1 = min(total, k0 + per);
+
   const uint16_t* kbase = kc + b * stride_b + h * stride_h;
   const uint16_t* vbase = vc + b * stride_b + h * stride_h;
   uint16_t(*Vt)[VTW] = reinterpret_cast<uint16_t(*)[VTW]>(smem + (size_t)wave * DH * VTW * 2);
@@ -264,7 +277,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     for (int d = 0; d < DT; ++d) o[t][d] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
-    const int qr = (qg * QTW + t) * 16 + lq;
+    const int qr = (tile0 + qg * QTW + t) * 16 + lq;
     if (qr < nq) {
       const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
 #pragma unroll
@@ -329,16 +342,26 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 #pragma unroll
     for (int t = 0; t < QTW; ++t) {
       float mx = -INFINITY;
+      if (kb + AWG_KT <= min(L, k1)) {
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
+        for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = kb + sub * 16 + 4 * g + r;
-          const bool vis = key < k1 && (key < L || tail_visible(mw0[t], mw1[t], key - L));
-          const float v = vis ? st[t][sub][r] * scale_log2 : -INFINITY;
-          st[t][sub][r] = v;
-          mx = fmaxf(mx, v);
-        }
+          for (int r = 0; r < 4; ++r) {
+            st[t][sub][r] *= scale_log2;
+            mx = fmaxf(mx, st[t][sub][r]);
+          }
+      } else {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = kb + sub * 16 + 4 * g + r;
+            const bool vis = key < k1 && (key < L || tail_visible(mw0[t], mw1[t], key - L));
+            const float v = vis ? st[t][sub][r] * scale_log2 : -INFINITY;
+            st[t][sub][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
       mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
       const float m_new = fmaxf(m_run[t], mx);
@@ -357,28 +380,19 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
       rs += __shfl_xor(rs, 32, WAVE);
       l_run[t] = l_run[t] * alpha + rs;
       m_run[t] = m_new;
+      if (!__all(alpha == 1.f)) {
 #pragma unroll
-      for (int d = 0; d < DT; ++d) o[t][d] *= alpha;
-      // P = P1 + P2 + P3 in bf16 parts (three MFMAs), as accurate as fp32 accumulation
-      bf16x8 p1, p2, p3;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const float pv = r < 4 ? st[t][0][r] : st[t][1][r - 4];
-        const uint16_t b1 = f2bf(pv);
-        const float r1 = pv - bf2f(b1);
-        const uint16_t b2 = f2bf(r1);
-        p1[r] = __builtin_bit_cast(__bf16, b1);
-        p2[r] = __builtin_bit_cast(__bf16, b2);
-        p3[r] = __builtin_bit_cast(__bf16, f2bf(r1 - bf2f(b2)));
+        for (int d = 0; d < DT; ++d) o[t][d] *= alpha;
       }
+      bf16x8 p1;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) p1[r] = (__bf16)(r < 4 ? st[t][0][r] : st[t][1][r - 4]);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
         const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][4 * g]);
         const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][16 + 4 * g]);
         const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[t][d], 0, 0, 0);
-        o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p2, o[t][d], 0, 0, 0);
-        o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p3, o[t][d], 0, 0, 0);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -412,10 +426,10 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     }
     __syncthreads();
     for (int idx = threadIdx.x; idx < QG * 16 * DH; idx += AWG_W * WAVE) {
-      const int grp = idx / (16 * DH), row = (idx / DH) % 16, d = idx % DH;
-      const int qr = (grp * QTW + t) * 16 + row;
+      const int qgr = idx / (16 * DH), row = (idx / DH) % 16, d = idx % DH;
+      const int qr = (tile0 + qgr * QTW + t) * 16 + row;
       if (qr >= nq) continue;
-      const int w0 = grp * KG;
+      const int w0 = qgr * KG;
       float M = -INFINITY;
 #pragma unroll
       for (int w = 0; w < KG; ++w) M = fmaxf(M, mml[((w0 + w) * 16 + row) * 2]);
@@ -551,23 +565,32 @@ static AttnPlan attn_plan(int B, int H, int kv_cap) {
   return {splits, chunk};
 }
 
-// Query tiles per wave and query groups of the one-workgroup-per-pair kernel (registers
-// allow 4 tiles of head size 64, 2 of 128); returns false when nq_max does not fit.
-static bool attn_wg_shape(int Dh, int nq_max, int& qtw, int& qg) {
+// Query tiles per wave, query groups and query slices (workgroups per pair) of the
+// one-workgroup-per-pair kernel.  With few pairs every 16-row query tile gets a workgroup of
+// its own (its 8 waves split the keys), so a large tree brings more CUs to the softmax,
+// which bounds it; with many pairs the tiles of a pair share one workgroup (registers allow
+// 4 tiles of head size 64, 2 of 128).  Returns false when nq_max does not fit.
+static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, int& qsplit) {
   const int qt = (nq_max + 15) / 16;
+  if (B * H < 128) {
+    qtw = qg = 1;
+    qsplit = qt;
+    return qt <= ADT_MAX_NODES / 16;
+  }
   const int cap = Dh == 64 ? 4 : 2;
   qtw = qt < cap ? qt : cap;
   const int groups = (qt + qtw - 1) / qtw;
   qg = groups <= 1 ? 1 : (groups <= 2 ? 2 : 4);   // a power of two dividing the 8 waves
+  qsplit = 1;
   return groups <= 4;
 }
 
-// One workgroup per (sequence, head) unless there are few pairs and each of their key
-// slices would be long (one image's verify at a long prefix): then the keys are split
-// across workgroups and merged by a second kernel, which brings more CUs to the stream.
+// One workgroup per (sequence, head, query slice) unless there are few pairs and each of
+// their key slices would be long (one image's forwards at a long prefix): then the keys are
+// split across workgroups and merged by a second kernel, which brings more CUs to the stream.
 static bool attn_use_wg(int B, int H, int Dh, int nq_max, int kv_cap) {
-  int qtw, qg;
-  if (!attn_wg_shape(Dh, nq_max, qtw, qg)) return false;
+  int qtw, qg, qsplit;
+  if (!attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit)) return false;
   const int kg = AWG_W / qg;
   return B * H >= 128 || kv_cap / kg <= 256;
 }
@@ -583,17 +606,18 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
 
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
-                            int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st) {
+                            int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st,
+                            hipEvent_t ev0, hipEvent_t ev1) {
   if (attn_use_wg(B, H, Dh, nq_max, kv_cap)) {
-    int qtw, qg;
-    attn_wg_shape(Dh, nq_max, qtw, qg);
-    const dim3 grid(H, B);
+    int qtw, qg, qsplit;
+    attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
+    const int pairs = B * H;
+    const dim3 grid(qsplit == 1 ? pairs : (pairs + 7) / 8 * 8 * qsplit);
     const float sl2 = scale * LOG2E;
 #define ADT_ATTN_WG(DHV, QTWV, QGV)                                                                                \
-  tree_attn_wg_kernel<DHV, QTWV, QGV><<<grid, AWG_W * WAVE, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
-                                                                     (const uint16_t*)v, sb, sh, kv_len, n_q,      \
-                                                                     n_tail, mask, rl, H, nq_max, kv_cap, sl2,     \
-                                                                     (uint16_t*)out)
+  hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV>, grid, dim3(AWG_W * WAVE), 0, st, ev0, ev1, 0,          \
+                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
+                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, pairs, qsplit)
     if (Dh == 128) {
       if (qtw == 1) ADT_ATTN_WG(128, 1, 1);
       else if (qg == 1) ADT_ATTN_WG(128, 2, 1);
@@ -619,11 +643,9 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   dim3 grid(p.splits, H, B);
   const float sl2 = scale * LOG2E;
 #define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
-  tree_attn_bf16_kernel<DHV, TPWV><<<grid, ATT_THREADS, 0, st>>>((const uint16_t*)q, (const uint16_t*)k,       \
-                                                                 (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail, \
-                                                                 mask, rl, H, nq_max, kv_cap, p.chunk, p.splits,  \
-                                                                 sl2,                                             \
-                                                                 part_o, part_ml)
+  hipExtLaunchKernelGGL(tree_attn_bf16_kernel<DHV, TPWV>, grid, dim3(ATT_THREADS), 0, st, ev0, nullptr, 0,      \
+                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail, \
+                        mask, rl, H, nq_max, kv_cap, p.chunk, p.splits, sl2, part_o, part_ml)
   if (Dh == 128) {
     if (nq_max > 64) ADT_ATTN_LAUNCH(128, 2);
     else ADT_ATTN_LAUNCH(128, 1);
@@ -634,8 +656,8 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
 #undef ADT_ATTN_LAUNCH
   ADT_LAUNCH_CHECK();
   dim3 g2(nq_max, H, B);
-  tree_attn_combine_kernel<uint16_t><<<g2, Dh, 0, st>>>(part_o, part_ml, n_q, rl, H, nq_max, p.splits, Dh,
-                                                         (uint16_t*)out);
+  hipExtLaunchKernelGGL(tree_attn_combine_kernel<uint16_t>, g2, dim3(Dh), 0, st, nullptr, ev1, 0, part_o, part_ml,
+                        n_q, rl, H, nq_max, p.splits, Dh, (uint16_t*)out);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -643,18 +665,19 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
-                            hipStream_t st) {
+                            hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   if (dtype == ADT_F32) {
     const size_t sm = (size_t)(Dh + kv_cap) * sizeof(float);
     ADT_CHECK_ARG(sm <= 60 * 1024, ADT_E_CAPACITY, "tree_attn f32: kv_cap %d too large for LDS scores", kv_cap);
     dim3 grid(nq_max, H, B);
-    tree_attn_f32_kernel<<<grid, 128, sm, st>>>((const float*)q, (const float*)k, (const float*)v, sb, sh, kv_len,
-                                                n_q, n_tail, mask, rl, H, nq_max, kv_cap, Dh, scale, (float*)out);
+    hipExtLaunchKernelGGL(tree_attn_f32_kernel, grid, dim3(128), sm, st, ev0, ev1, 0, (const float*)q, (const float*)k,
+                          (const float*)v, sb, sh, kv_len, n_q, n_tail, mask, rl, H, nq_max, kv_cap, Dh, scale,
+                          (float*)out);
     ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
   return attn_bf16(q, k, v, sb, sh, kv_len, n_q, n_tail, mask, rl, B, H, Dh, nq_max, kv_cap, scale, out, ws, ws_bytes,
-                   st);
+                   st, ev0, ev1);
 }
 
 }  // namespace adt
