@@ -26,17 +26,23 @@ import numpy as np
 
 HBM_PEAK_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
-GEMM_SRC = os.path.join(ROOT, "paper_2512_21857_amd", "csrc", "kernels", "gemm.hip")
+# the sources the GEMM kernel is compiled from (kernel, shared helpers, epilogue struct)
+GEMM_SRCS = [os.path.join(ROOT, "paper_2512_21857_amd", "csrc", *parts)
+             for parts in (("kernels", "gemm.hip"), ("common.h",), ("launch.h",))]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_tile_llamagen_xl_traffic.md")
 
 
 def gemm_traffic():
     """HBM bytes per GEMM launch from the committed FETCH_SIZE / WRITE_SIZE counter summary,
-    or None when the kernel source changed since the counters were taken."""
+    or None when the kernel's sources changed since the counters were taken (sha256 over
+    gemm.hip, common.h and launch.h, in that order)."""
     import hashlib
     try:
         text = open(TRAFFIC_FILE).read()
-        src = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+        h = hashlib.sha256()
+        for path in GEMM_SRCS:
+            h.update(open(path, "rb").read())
+        src = h.hexdigest()
     except OSError:
         return None
     keys = ("source_sha256:", "traffic_bytes_per_launch:")
