@@ -29,6 +29,19 @@ __device__ __forceinline__ bool tail_visible(uint64_t w0, uint64_t w1, int j) {
   return (w >> (j & 63)) & 1ull;
 }
 
+// Whether key `key` is visible to a row with ancestor mask (w0, w1): inside [0, k_end) and
+// either in the prefix [0, L) or a marked tree row.  Written without short-circuits, so it
+// compiles to selects rather than a branch per element.
+__device__ __forceinline__ bool key_visible(int key, int k_end, int L, uint64_t w0, uint64_t w1) {
+  const int j = key - L;
+  const uint64_t w = j < 64 ? w0 : w1;
+  return (key < k_end) & ((key < L) | (bool)((w >> (j & 63)) & 1ull));
+}
+
+// 2^x on the transcendental unit alone (no denormal fix-up: softmax weights that small
+// are zero for every purpose here).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // TPW = query tiles (of 16) per wave: 1 covers up to 64 queries, 2 up to 128.
 template <int DH, int TPW>
 __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
@@ -149,7 +162,7 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int key = kb + sub * 16 + 4 * g + r;
-            const bool vis = key < k_end && (key < L || tail_visible(mw0[i], mw1[i], key - L));
+            const bool vis = key_visible(key, k_end, L, mw0[i], mw1[i]);
             const float v = vis ? st[sub][r] * scale_log2 : -INFINITY;
             st[sub][r] = v;
             mx = fmaxf(mx, v);
@@ -160,13 +173,13 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
       mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
       const float m_new = fmaxf(m_run[i], mx);
       const bool none = (m_new == -INFINITY);
-      const float alpha = none ? 1.f : exp2f(m_run[i] - m_new);
+      const float alpha = none ? 1.f : fast_exp2(m_run[i] - m_new);
       float rs = 0.f;
 #pragma unroll
       for (int sub = 0; sub < 4; ++sub) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = none ? 0.f : exp2f(st[sub][r] - m_new);
+          const float p = none ? 0.f : fast_exp2(st[sub][r] - m_new);
           st[sub][r] = p;
           rs += p;
         }
@@ -220,8 +233,8 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
 // 16-row query tiles, and each group's KG waves take contiguous, balanced slices of the
 // keys (computed on the device from kv_len + n_tail, so no wave idles on an empty split).
 // Each wave runs the online softmax over its slice for its query tiles, double-buffering
-// 32-key K/V steps in registers; V is transposed through the wave's own LDS area with one
-// 8-byte store per 4 keys of a dimension.  The KG waves of a group are then merged in LDS
+// 32-key K/V steps in registers; V rows go to the wave's own LDS area as they are and come
+// back transposed through gfx950's LDS transpose load.  The KG waves of a group are then merged in LDS
 // in wave order, so there is no second kernel and no partials in global memory.
 constexpr int AWG_KT = 32;
 constexpr int AWG_W = 8;
@@ -234,9 +247,11 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     int kv_cap, float scale_log2, uint16_t* __restrict__ out, int pairs, int qsplit) {
   constexpr int KG = AWG_W / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
-  constexpr int VTW = AWG_KT + 4;                          // padded row of a transposed V step (8-byte aligned)
+  // V rows of a step, padded by 32 bytes so that the 8 rows a transpose load touches per
+  // pair of 16-lane groups fall on distinct banks
+  constexpr int VRW = DH + 16;
   constexpr int VG = (AWG_KT / 4) * (DH / 8) / WAVE;       // (4 keys x 8 dims) groups per lane per step
-  constexpr int VT_BYTES = AWG_W * DH * VTW * 2;
+  constexpr int VT_BYTES = AWG_W * AWG_KT * VRW * 2;
   constexpr int MG_BYTES = AWG_W * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
@@ -262,7 +277,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 
   const uint16_t* kbase = kc + b * stride_b + h * stride_h;
   const uint16_t* vbase = vc + b * stride_b + h * stride_h;
-  uint16_t(*Vt)[VTW] = reinterpret_cast<uint16_t(*)[VTW]>(smem + (size_t)wave * DH * VTW * 2);
+  uint16_t(*Vr)[VRW] = reinterpret_cast<uint16_t(*)[VRW]>(smem + (size_t)wave * AWG_KT * VRW * 2);
 
   bf16x8 qf[QTW][KS];
   uint64_t mw0[QTW], mw1[QTW];
@@ -290,8 +305,6 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 
   // K fragments (A operand rows = keys) and, per lane, VG groups of 4 consecutive keys x 8
   // dims of V for one 32-key step; keys clamped to the valid range (masked out below)
-  bf16x8 kf[2][KS], kn[2][KS];
-  u16x8 vf[VG][4], vn[VG][4];
   auto load_step = [&](int kb, bf16x8 (&kd)[2][KS], u16x8 (&vd)[VG][4]) {
     const int last = max(total - 1, 0);
 #pragma unroll
@@ -312,16 +325,19 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
       }
     }
   };
-  if (k0 < k1) load_step(k0, kf, vf);
-  for (int kb = k0; kb < k1; kb += AWG_KT) {
-    // this step's V, transposed into the wave's LDS area: Vt[dim][key]
+  // One 32-key step: this step's V rows into the wave's LDS area (row-major, padded rows),
+  // S^T = K Q^T, the next step's loads, the online softmax, then O^T += V^T P^T with the V^T
+  // operand read back by the LDS transpose load: lane (i, g) of ds_read_b64_tr_b16 returns,
+  // over slots s = 0..3, element i of the row read by lane 4s + i/4 of its 16-lane group, so
+  // lane j addressing row k0 + j/4, columns d0 + 4(j%4)..+3 yields V[k0 + s][d0 + i].
+  auto step = [&](int kb, const bf16x8 (&kf)[2][KS], const u16x8 (&vf)[VG][4], bool more, bf16x8 (&kn)[2][KS],
+                  u16x8 (&vn)[VG][4]) {
 #pragma unroll
     for (int j = 0; j < VG; ++j) {
       const int gi = lane + j * WAVE;
       const int c = (gi % (DH / 8)) * 8, r4 = gi / (DH / 8);
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        *reinterpret_cast<u16x4*>(&Vt[c + e][4 * r4]) = u16x4{vf[j][0][e], vf[j][1][e], vf[j][2][e], vf[j][3][e]};
+      for (int u = 0; u < 4; ++u) *reinterpret_cast<u16x8*>(&Vr[4 * r4 + u][c]) = vf[j][u];
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -336,13 +352,13 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
         for (int kk = 0; kk < KS; ++kk)
           st[t][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[sub][kk], qf[t][kk], st[t][sub], 0, 0, 0);
       }
-    const bool more = kb + AWG_KT < k1;
     if (more) load_step(kb + AWG_KT, kn, vn);
     // lane (lq, g) holds S for query tile t, row lq and keys kb + sub*16 + 4g + r
+    const bool prefix_only = kb + AWG_KT <= min(L, k1);
 #pragma unroll
     for (int t = 0; t < QTW; ++t) {
       float mx = -INFINITY;
-      if (kb + AWG_KT <= min(L, k1)) {
+      if (prefix_only) {
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
@@ -356,7 +372,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int key = kb + sub * 16 + 4 * g + r;
-            const bool vis = key < k1 && (key < L || tail_visible(mw0[t], mw1[t], key - L));
+            const bool vis = key_visible(key, k1, L, mw0[t], mw1[t]);
             const float v = vis ? st[t][sub][r] * scale_log2 : -INFINITY;
             st[t][sub][r] = v;
             mx = fmaxf(mx, v);
@@ -366,13 +382,13 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
       mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
       const float m_new = fmaxf(m_run[t], mx);
       const bool none = (m_new == -INFINITY);
-      const float alpha = none ? 1.f : exp2f(m_run[t] - m_new);
+      const float alpha = none ? 1.f : fast_exp2(m_run[t] - m_new);
       float rs = 0.f;
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = none ? 0.f : exp2f(st[t][sub][r] - m_new);
+          const float p = none ? 0.f : fast_exp2(st[t][sub][r] - m_new);
           st[t][sub][r] = p;
           rs += p;
         }
@@ -389,15 +405,23 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
       for (int r = 0; r < 8; ++r) p1[r] = (__bf16)(r < 4 ? st[t][0][r] : st[t][1][r - 4]);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][4 * g]);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][16 + 4 * g]);
-        const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const int col = d * 16 + 4 * (lq & 3), row = lq >> 2;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)&Vr[4 * g + row][col]);
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)&Vr[16 + 4 * g + row][col]);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, v8i16{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
         o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[t][d], 0, 0, 0);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  bf16x8 kf[2][KS], kn[2][KS];
+  u16x8 vf[VG][4], vn[VG][4];
+  if (k0 < k1) load_step(k0, kf, vf);
+  for (int kb = k0; kb < k1; kb += AWG_KT) {
+    const bool more = kb + AWG_KT < k1;
+    step(kb, kf, vf, more, kn, vn);
     if (more) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
@@ -547,6 +571,214 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
 }
 
 // ----------------------------------------------------------------------------- host
+// Large trees over many pairs: one workgroup of eight waves per (sequence, head).  64-key
+// blocks of K and V come into LDS once per workgroup (each thread fetches its share of the
+// next block into registers while the current one is computed, then stores it; double
+// buffered, one barrier per block), and every wave reads them: wave w owns query tile
+// w % QT and, when the tree has at most four tiles (KH = 2), one half of every block's keys
+// (w / QT); the halves are merged in LDS at the end.  K and V rows are stored with their
+// 16-byte chunks XOR-swizzled by row, so the K operand reads (16 rows of one chunk column)
+// and the V^T reads through the transpose load (8 rows of two chunk columns) each touch
+// distinct banks.
+constexpr int BLK_KT = 64;
+
+template <int DH>
+__device__ __forceinline__ int blk_swz_k(int row) { return DH == 128 ? (row & 15) : ((row >> 1) & 7); }
+template <int DH>
+__device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
+
+template <int DH, int KH>
+__global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
+    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
+  constexpr int CH = DH / 8;                     // 16-byte chunks per row
+  constexpr int DT = DH / 16, KS = DH / 32;
+  constexpr int BLK_BYTES = BLK_KT * DH * 2;     // one block of K or of V
+  constexpr int LOADS = BLK_BYTES / (AWG_W * WAVE * 16);   // direct loads per thread per block and operand
+  constexpr int SUBS = BLK_KT / KH / 16;         // 16-key sub-blocks per wave per block
+  static_assert(LOADS >= 1 && SUBS % 2 == 0, "block shape");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[4 * BLK_BYTES];   // [buffer][K, V]
+
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+  const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
+  const int QT = (nq_max + 15) / 16;
+  const int tile = wave % QT, kpart = wave / QT;
+  const bool active = kpart < KH;                // the remaining waves only load
+  const int L = kv_len[b];
+  const int nq = min(n_q[b], nq_max);
+  const int total = min(L + n_tail[b], kv_cap);
+  const int nblk = (total + BLK_KT - 1) / BLK_KT;
+  const uint16_t* kbase = kc + b * stride_b + h * stride_h;
+  const uint16_t* vbase = vc + b * stride_b + h * stride_h;
+
+  const int qr = tile * 16 + lq;
+  bf16x8 qf[KS];
+  uint64_t mw0 = 0, mw1 = 0;
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) qf[kk] = bf16x8{};
+  if (active && qr < nq) {
+    const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
+    const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
+    mw0 = mp[0];
+    mw1 = mp[1];
+  }
+
+  // Slot s (16 bytes) of a block holds row s / CH, chunk (s % CH) ^ swizzle(row); thread t
+  // fills slots r * 512 + t.  Keys past the live range repeat the last key (masked below).
+  u16x8 kr[LOADS], vr[LOADS];
+  auto fetch_block = [&](int blk) {
+    const int last = max(total - 1, 0);
+#pragma unroll
+    for (int r = 0; r < LOADS; ++r) {
+      const int slot = r * AWG_W * WAVE + threadIdx.x, row = slot / CH, phys = slot % CH;
+      const int64_t key = min(blk * BLK_KT + row, last);
+      kr[r] = *reinterpret_cast<const u16x8*>(kbase + key * DH + (phys ^ blk_swz_k<DH>(row)) * 8);
+      vr[r] = *reinterpret_cast<const u16x8*>(vbase + key * DH + (phys ^ blk_swz_v<DH>(row)) * 8);
+    }
+  };
+  auto store_block = [&](int buf) {
+    unsigned char* kb = smem + buf * 2 * BLK_BYTES;
+#pragma unroll
+    for (int r = 0; r < LOADS; ++r) {
+      const int slot = r * AWG_W * WAVE + threadIdx.x;
+      *reinterpret_cast<u16x8*>(kb + slot * 16) = kr[r];
+      *reinterpret_cast<u16x8*>(kb + BLK_BYTES + slot * 16) = vr[r];
+    }
+  };
+
+  f32x4 o[DT];
+#pragma unroll
+  for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  if (nblk > 0) fetch_block(0);
+  for (int blk = 0; blk < nblk; ++blk) {
+    // the buffer written here was last read two blocks ago, before the previous barrier
+    store_block(blk & 1);
+    __syncthreads();
+    if (blk + 1 < nblk) fetch_block(blk + 1);
+    if (!active) continue;
+    const unsigned char* kb = smem + (blk & 1) * 2 * BLK_BYTES;
+    const unsigned char* vb = kb + BLK_BYTES;
+    // this wave's keys of the block, 32 at a time: S^T = K Q^T (lane (lq, g) gets keys
+    // key0 + sub*16 + 4g + r for query column lq), the online softmax, O^T += V^T P^T
+#pragma unroll
+    for (int hf = 0; hf < SUBS / 2; ++hf) {
+      const int kw0 = kpart * (BLK_KT / KH) + hf * 32;   // first key within the block
+      const int key0 = blk * BLK_KT + kw0;
+      f32x4 st[2];
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int row = kw0 + sub * 16 + lq;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          const int phys = (kk * 4 + g) ^ blk_swz_k<DH>(row);
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(kb + row * DH * 2 + phys * 16);
+          st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[sub], 0, 0, 0);
+        }
+      }
+      float mx = -INFINITY;
+      if (key0 + 32 <= min(L, total)) {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            st[sub][r] *= scale_log2;
+            mx = fmaxf(mx, st[sub][r]);
+          }
+      } else {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = key0 + sub * 16 + 4 * g + r;
+            const float v = key_visible(key, total, L, mw0, mw1) ? st[sub][r] * scale_log2 : -INFINITY;
+            st[sub][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
+      const float m_new = fmaxf(m_run, mx);
+      const bool none = (m_new == -INFINITY);
+      const float alpha = none ? 1.f : fast_exp2(m_run - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = none ? 0.f : fast_exp2(st[sub][r] - m_new);
+          st[sub][r] = p;
+          rs += p;
+        }
+      rs += __shfl_xor(rs, 16, WAVE);
+      rs += __shfl_xor(rs, 32, WAVE);
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+      if (!__all(alpha == 1.f)) {
+#pragma unroll
+        for (int d = 0; d < DT; ++d) o[d] *= alpha;
+      }
+      // the transpose load of lane j of a 16-lane group addresses row j / 4 and dims
+      // 4 (j % 4)..+3 of a 4-row, 16-dim window
+      bf16x8 pb;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) pb[r] = (__bf16)(r < 4 ? st[0][r] : st[1][r - 4]);
+      const int r_lo = kw0 + 4 * g + (lq >> 2), r_hi = r_lo + 16;
+#pragma unroll
+      for (int d = 0; d < DT; ++d) {
+        const int c = 2 * d + ((lq & 3) >> 1), half = lq & 1;
+        const int off_lo = r_lo * DH * 2 + ((c ^ blk_swz_v<DH>(r_lo)) * 16) + half * 8;
+        const int off_hi = r_hi * DH * 2 + ((c ^ blk_swz_v<DH>(r_hi)) * 16) + half * 8;
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vb + off_lo));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vb + off_hi));
+        const bf16x8 a = __builtin_bit_cast(bf16x8, v8i16{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[d], 0, 0, 0);
+      }
+    }
+  }
+
+  // KH = 2: the second half's state goes through LDS to its partner wave, which merges
+  float* mo = reinterpret_cast<float*>(smem);          // [tile][DT * 4 + 2][WAVE]
+  if (KH == 2) {
+    __syncthreads();
+    if (active && kpart == 1) {
+      float* t = mo + (size_t)tile * (DT * 4 + 2) * WAVE;
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) t[(d * 4 + r) * WAVE + lane] = o[d][r];
+      t[(DT * 4) * WAVE + lane] = m_run;
+      t[(DT * 4 + 1) * WAVE + lane] = l_run;
+    }
+    __syncthreads();
+    if (active && kpart == 0) {
+      const float* t = mo + (size_t)tile * (DT * 4 + 2) * WAVE;
+      const float m1 = t[(DT * 4) * WAVE + lane], l1 = t[(DT * 4 + 1) * WAVE + lane];
+      const float M = fmaxf(m_run, m1);
+      const float w0 = M == -INFINITY ? 0.f : fast_exp2(m_run - M), w1 = M == -INFINITY ? 0.f : fast_exp2(m1 - M);
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[d][r] = o[d][r] * w0 + t[(d * 4 + r) * WAVE + lane] * w1;
+      l_run = l_run * w0 + l1 * w1;
+    }
+  }
+  if (active && kpart == 0 && qr < nq) {
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    uint16_t* op = out + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+      *reinterpret_cast<u16x4*>(op + d * 16 + 4 * g) =
+          u16x4{f2bf(o[d][0] * inv), f2bf(o[d][1] * inv), f2bf(o[d][2] * inv), f2bf(o[d][3] * inv)};
+  }
+}
+
 struct AttnPlan {
   int splits, chunk;
 };
@@ -585,6 +817,10 @@ static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, i
   return groups <= 4;
 }
 
+// Many pairs with trees of 33-128 rows: the shared-block kernel (one K/V stream per pair,
+// read by every query tile from LDS).
+static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 32 && nq_max <= 128; }
+
 // One workgroup per (sequence, head, query slice) unless there are few pairs and each of
 // their key slices would be long (one image's forwards at a long prefix): then the keys are
 // split across workgroups and merged by a second kernel, which brings more CUs to the stream.
@@ -608,6 +844,25 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st,
                             hipEvent_t ev0, hipEvent_t ev1) {
+  if (attn_use_blk(B, H, nq_max)) {
+    const dim3 grid(H, B);
+    const float sl2 = scale * LOG2E;
+    const bool kh2 = (nq_max + 15) / 16 <= 4;
+#define ADT_ATTN_BLK(DHV, KHV)                                                                                     \
+  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV>, grid, dim3(AWG_W * WAVE), 0, st, ev0, ev1, 0,              \
+                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
+                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
+    if (Dh == 128) {
+      if (kh2) ADT_ATTN_BLK(128, 2);
+      else ADT_ATTN_BLK(128, 1);
+    } else {
+      if (kh2) ADT_ATTN_BLK(64, 2);
+      else ADT_ATTN_BLK(64, 1);
+    }
+#undef ADT_ATTN_BLK
+    ADT_LAUNCH_CHECK();
+    return ADT_OK;
+  }
   if (attn_use_wg(B, H, Dh, nq_max, kv_cap)) {
     int qtw, qg, qsplit;
     attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);

@@ -88,6 +88,18 @@ def test_tree_attn_bf16_long_prefix_split_keys(rt, n):
     assert _attn_case(rt, B=2, H=4, Dh=128, n=n, l_lo=1500, l_hi=2000, seed=13) == 2 * n
 
 
+@pytest.mark.parametrize("B,H,Dh,n,l_lo,l_hi,vary", [
+    (8, 16, 64, 40, 0, 300, True),      # shared 64-key blocks, 3 query tiles, keys split in two halves
+    (4, 32, 128, 64, 1, 130, False),    # 4 tiles, prefixes shorter than two blocks
+    (16, 8, 64, 100, 60, 200, True),    # 7 tiles (one wave only loads), ragged trees
+    (2, 64, 128, 128, 0, 70, False),    # 8 tiles, almost no prefix: nearly every block is masked
+    (8, 16, 128, 33, 500, 700, False),  # the smallest tree of the shared-block path
+])
+def test_tree_attn_bf16_many_pairs_blocks(rt, B, H, Dh, n, l_lo, l_hi, vary):
+    """Many (sequence, head) pairs with trees of 33-128 rows take the shared-block kernel."""
+    assert _attn_case(rt, B=B, H=H, Dh=Dh, n=n, l_lo=l_lo, l_hi=l_hi, seed=B * 1000 + n, vary_n=vary) > 0
+
+
 def test_tree_attn_bf16_full_microbench_sampled(rt):
     """The 16 x 32 x 128 microbenchmark at its real size (L in [512, 2400], 128 nodes), checked
     on sampled rows including the root, the last node and a deep node of every sequence."""
