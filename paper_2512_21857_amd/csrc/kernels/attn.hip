@@ -575,12 +575,12 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
 // blocks of K and V come into LDS once per workgroup (each thread fetches its share of the
 // next block into registers while the current one is computed, then stores it; double
 // buffered, one barrier per block), and every wave reads them: wave w owns query tile
-// w % QT and, when the tree has at most four tiles (KH = 2), one half of every block's keys
-// (w / QT); the halves are merged in LDS at the end.  K and V rows are stored with their
+// w % QT and one of the KH parts of every block's keys (w / QT): KH = 1 for 5-8 tiles,
+// 2 for 3-4 tiles (64-key blocks) and 4 for 2 tiles (128-key blocks); the parts of a tile
+// are merged in LDS at the end, in part order.  K and V rows are stored with their
 // 16-byte chunks XOR-swizzled by row, so the K operand reads (16 rows of one chunk column)
 // and the V^T reads through the transpose load (8 rows of two chunk columns) each touch
 // distinct banks.
-constexpr int BLK_KT = 64;
 
 template <int DH>
 __device__ __forceinline__ int blk_swz_k(int row) { return DH == 128 ? (row & 15) : ((row >> 1) & 7); }
@@ -593,12 +593,14 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
     int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
+  constexpr int BLK_KT = KH == 4 ? 128 : 64;      // keys per block: 32 per wave and half-step
   constexpr int CH = DH / 8;                     // 16-byte chunks per row
   constexpr int DT = DH / 16, KS = DH / 32;
   constexpr int BLK_BYTES = BLK_KT * DH * 2;     // one block of K or of V
   constexpr int LOADS = BLK_BYTES / (AWG_W * WAVE * 16);   // direct loads per thread per block and operand
   constexpr int SUBS = BLK_KT / KH / 16;         // 16-key sub-blocks per wave per block
   static_assert(LOADS >= 1 && SUBS % 2 == 0, "block shape");
+  static_assert((KH - 1) * (8 / KH) * (DT * 4 + 2) * WAVE * 4 <= 4 * BLK_BYTES, "merge area");
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * BLK_BYTES];   // [buffer][K, V]
 
   const int h = blockIdx.x, b = blockIdx.y;
@@ -743,12 +745,12 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
     }
   }
 
-  // KH = 2: the second half's state goes through LDS to its partner wave, which merges
-  float* mo = reinterpret_cast<float*>(smem);          // [tile][DT * 4 + 2][WAVE]
-  if (KH == 2) {
+  // KH > 1: parts 1.. of a tile pass their state through LDS to part 0, which merges them
+  float* mo = reinterpret_cast<float*>(smem);          // [tile][part - 1][DT * 4 + 2][WAVE]
+  if (KH > 1) {
     __syncthreads();
-    if (active && kpart == 1) {
-      float* t = mo + (size_t)tile * (DT * 4 + 2) * WAVE;
+    if (active && kpart >= 1) {
+      float* t = mo + (size_t)(tile * (KH - 1) + kpart - 1) * (DT * 4 + 2) * WAVE;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
@@ -758,15 +760,20 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
     }
     __syncthreads();
     if (active && kpart == 0) {
-      const float* t = mo + (size_t)tile * (DT * 4 + 2) * WAVE;
-      const float m1 = t[(DT * 4) * WAVE + lane], l1 = t[(DT * 4 + 1) * WAVE + lane];
-      const float M = fmaxf(m_run, m1);
-      const float w0 = M == -INFINITY ? 0.f : fast_exp2(m_run - M), w1 = M == -INFINITY ? 0.f : fast_exp2(m1 - M);
 #pragma unroll
-      for (int d = 0; d < DT; ++d)
+      for (int kp = 1; kp < KH; ++kp) {
+        const float* t = mo + (size_t)(tile * (KH - 1) + kp - 1) * (DT * 4 + 2) * WAVE;
+        const float m1 = t[(DT * 4) * WAVE + lane], l1 = t[(DT * 4 + 1) * WAVE + lane];
+        const float M = fmaxf(m_run, m1);
+        const float w0 = M == -INFINITY ? 0.f : fast_exp2(m_run - M);
+        const float w1 = M == -INFINITY ? 0.f : fast_exp2(m1 - M);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o[d][r] = o[d][r] * w0 + t[(d * 4 + r) * WAVE + lane] * w1;
-      l_run = l_run * w0 + l1 * w1;
+        for (int d = 0; d < DT; ++d)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[d][r] = o[d][r] * w0 + t[(d * 4 + r) * WAVE + lane] * w1;
+        l_run = l_run * w0 + l1 * w1;
+        m_run = M;
+      }
     }
   }
   if (active && kpart == 0 && qr < nq) {
@@ -817,9 +824,9 @@ static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, i
   return groups <= 4;
 }
 
-// Many pairs with trees of 33-128 rows: the shared-block kernel (one K/V stream per pair,
+// Many pairs with trees of 17-128 rows: the shared-block kernel (one K/V stream per pair,
 // read by every query tile from LDS).
-static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 32 && nq_max <= 128; }
+static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 16 && nq_max <= 128; }
 
 // One workgroup per (sequence, head, query slice) unless there are few pairs and each of
 // their key slices would be long (one image's forwards at a long prefix): then the keys are
@@ -847,16 +854,18 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   if (attn_use_blk(B, H, nq_max)) {
     const dim3 grid(H, B);
     const float sl2 = scale * LOG2E;
-    const bool kh2 = (nq_max + 15) / 16 <= 4;
+    const int qt = (nq_max + 15) / 16;
 #define ADT_ATTN_BLK(DHV, KHV)                                                                                     \
   hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV>, grid, dim3(AWG_W * WAVE), 0, st, ev0, ev1, 0,              \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
     if (Dh == 128) {
-      if (kh2) ADT_ATTN_BLK(128, 2);
+      if (qt <= 2) ADT_ATTN_BLK(128, 4);
+      else if (qt <= 4) ADT_ATTN_BLK(128, 2);
       else ADT_ATTN_BLK(128, 1);
     } else {
-      if (kh2) ADT_ATTN_BLK(64, 2);
+      if (qt <= 2) ADT_ATTN_BLK(64, 4);
+      else if (qt <= 4) ADT_ATTN_BLK(64, 2);
       else ADT_ATTN_BLK(64, 1);
     }
 #undef ADT_ATTN_BLK
