@@ -10,7 +10,8 @@ N(0, 0.02) weights), a 120-token seeded prompt and a 32 x 32 image grid, trees o
 second; the line also carries the roofline of the dominant kernel (the weight-streaming
 projections), tree-attention bandwidth (in the cycle and in the 16 x 32 x 128 tree-attention
 microbenchmark), the batched verify projections, the same cycle under classifier-free
-guidance (scale 3.0: both branches in every forward) and the CPU oracle timed on this host.
+guidance (scale 3.0: both branches in every forward), 16 images decoded together (one verify
+forward over all their trees per step) and the CPU oracle timed on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -64,6 +65,7 @@ def parse():
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-mfma", action="store_true")
     ap.add_argument("--no-guided", action="store_true")
+    ap.add_argument("--no-batch", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -255,6 +257,34 @@ def main():
                 "nodes_per_step": round(gnodes / k, 2), "tokens_per_step": round(gtokens / k, 3),
                 "mean_depth": round(gdepth / k, 3), "steps": k}
 
+    def batched_run(B, fixed, k):
+        """B images decoded together: per image its own schedule and draft tree, one verify
+        forward over the packed rows of all B trees per step (packed-weight MFMA GEMMs)."""
+        import dataclasses
+        prompts = [synth.prefix_ids(dataclasses.replace(cfg, seed=cfg.seed + 101 * b)) for b in range(B)]
+        bt = rt.DeviceBatch(dm, [cfg] * B, fixed_tree=fixed)
+        bt.prefill(prompts)
+
+        def go(n):
+            nodes = tokens = 0
+            for _ in range(n):
+                for o in bt.step():
+                    nodes += max(o["n_nodes"] - 1, 0)
+                    tokens += o["n_committed"]
+            torch.cuda.synchronize()
+            return nodes, tokens
+        go(3)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        nodes, tokens = go(k)
+        bdt = time.perf_counter() - t0
+        del bt
+        torch.cuda.empty_cache()
+        return {"batch": B, "tree": "depth 6, width 10, top-60" if fixed else "ADT schedule per image",
+                "nodes_per_s": round(nodes / bdt, 2), "ms_per_step": round(bdt / k * 1e3, 4),
+                "rows_per_step": round((nodes + B * k) / k, 1), "tokens_per_step": round(tokens / k, 3),
+                "steps": k}
+
     sess = fresh()
     run_steps(sess, args.warmup)
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
@@ -276,6 +306,8 @@ def main():
     micro = {} if args.no_microbench else attn_microbench(rt)
     mfma = None if args.no_mfma else mfma_benchmark(rt)
     guided = None if args.no_guided else guided_run(min(args.steps, 50))
+    batched = None if args.no_batch else [batched_run(16, True, min(args.steps, 30)),
+                                          batched_run(16, False, min(args.steps, 30))]
     line = {
         "metric": "verified draft-tree nodes/sec + tree-attn HBM GB/s (% peak), 1xMI355X",
         "value": round(value, 2),
@@ -305,6 +337,7 @@ def main():
                       "microbench_16x32x128": micro},
         "batched_verify_gemm": mfma,
         "guided": guided,
+        "batched": batched,
         "fixed_tree": {"nodes_per_s": round(fnodes / fdt, 2), "ms_per_step": round(fdt / min(args.steps, 50) * 1e3, 4),
                        "nodes_per_step": round(fnodes / min(args.steps, 50), 2), "tree": "depth 6, width 10, top-60"},
     }

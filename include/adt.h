@@ -366,6 +366,29 @@ adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_ha
 /* One full cycle: a0 + a1-a3 + b + c + d1.  Synchronises once (the accepted path). */
 adt_status adt_step(adt_session* s, adt_step_out* out, void* stream);
 
+/* ------------------------------------------------------------------ batched cycle
+ * Several images decoded together (Sec. 3.1 verification applied to a batch of trees): each
+ * session schedules and drafts its own tree as in adt_step, then ONE target forward verifies
+ * every tree, its rows packed one tree after another (M = sum of tree sizes; the projections
+ * run on the MFMA-tiled batched GEMM reading the packed weights, attention takes each tree
+ * against its own cache), and each session accepts and commits from its rows.  Results equal
+ * adt_step on each session up to floating-point order.
+ * sessions: [host] B prefilled sessions of one bf16 model, unguided, equal s_cap, whose
+ *   target caches are equally spaced: k_cache of session b = k_cache of session 0 +
+ *   b * stride (the same stride for v_cache, at least n_layers*n_heads*s_cap*head_dim
+ *   elements), i.e. one [B][n_layers][n_heads][s_cap][head_dim] allocation.  The batch
+ *   keeps the pointers; the sessions must outlive it and not be stepped on their own while
+ *   it is used.
+ * workspace: device memory of adt_batch_workspace_size() bytes, owned by the caller.
+ * adt_batch_step writes outs[b] for every session (done sessions report done = 1 and are
+ * not verified).  ADT_E_ARG / ADT_E_SHAPE when the sessions do not satisfy the above. */
+typedef struct adt_batch_s adt_batch;
+size_t adt_batch_workspace_size(adt_session* const* sessions, int32_t B);
+adt_status adt_batch_create(adt_session* const* sessions, int32_t B, void* workspace, size_t workspace_bytes,
+                            adt_batch** out);
+void adt_batch_destroy(adt_batch* b);
+adt_status adt_batch_step(adt_batch* b, adt_step_out* outs, void* stream);
+
 /* ------------------------------------------------------------------ profiling
  * Optional timing of the session's kernels by class, with HIP events recorded on the
  * caller's stream around each launch (adds a little host overhead while enabled).  Read

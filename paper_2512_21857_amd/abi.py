@@ -101,6 +101,10 @@ _SIGS = {
     "adt_verify_forward": (i32, [p, p]),
     "adt_session_accept_commit": (i32, [p, i32, i32, C.POINTER(StepOut), p]),
     "adt_step": (i32, [p, C.POINTER(StepOut), p]),
+    "adt_batch_workspace_size": (sz, [C.POINTER(p), i32]),
+    "adt_batch_create": (i32, [C.POINTER(p), i32, p, sz, C.POINTER(p)]),
+    "adt_batch_destroy": (None, [p]),
+    "adt_batch_step": (i32, [p, C.POINTER(StepOut), p]),
     "adt_profile_enable": (i32, [i32]),
     "adt_profile_read": (i32, [i32, C.POINTER(i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                C.POINTER(C.c_double), i32]),

@@ -1159,6 +1159,210 @@ extern "C" adt_status adt_step(adt_session* s, adt_step_out* out, void* stream) 
   return adt_session_accept_commit(s, d_hat, k_hat, out, st);
 }
 
+// ============================================================================ batched cycle
+struct adt_batch_s {
+  std::vector<adt_session_s*> ss;
+  int B = 0, Mmax = 0, Nmax = 0;
+  int64_t cache_sb = 0;        // elements between consecutive sessions' target caches
+  float *h = nullptr, *C = nullptr;
+  void *a = nullptr, *q = nullptr, *att = nullptr, *sw = nullptr, *feat = nullptr;
+  int32_t *tok, *pos, *slot, *seq, *row_off, *kv_len, *nq;
+  uint64_t* mask;
+  void* attn_ws = nullptr;
+  size_t attn_ws_bytes = 0;
+};
+
+static adt_status check_batch(adt_session* const* ss, int B, int64_t& cache_sb) {
+  ADT_CHECK_ARG(ss && B >= 1 && B <= 256, ADT_E_ARG, "batch: %d sessions", B);
+  for (int b = 0; b < B; ++b) ADT_CHECK_ARG(ss[b] != nullptr, ADT_E_ARG, "batch: session %d is null", b);
+  const adt_session_s* s0 = ss[0];
+  const int64_t per = (int64_t)s0->Lr * s0->H * s0->d.s_cap * s0->Dh;
+  cache_sb = B > 1 ? ((const char*)ss[1]->d.k_cache - (const char*)s0->d.k_cache) / (int64_t)esize(s0->dt) : per;
+  ADT_CHECK_ARG(cache_sb >= per, ADT_E_SHAPE, "batch: target caches closer than one session's size");
+  for (int b = 0; b < B; ++b) {
+    const adt_session_s* s = ss[b];
+    ADT_CHECK_ARG(s->m == s0->m && s->dt == ADT_BF16 && s->nb == 1, ADT_E_ARG,
+                  "batch: session %d is not an unguided bf16 session of the first one's model", b);
+    ADT_CHECK_ARG(s->prefilled && s->d.s_cap == s0->d.s_cap, ADT_E_ARG, "batch: session %d not prefilled or s_cap", b);
+    ADT_CHECK_ARG((const char*)s->d.k_cache == (const char*)s0->d.k_cache + b * cache_sb * esize(s->dt) &&
+                      (const char*)s->d.v_cache == (const char*)s0->d.v_cache + b * cache_sb * esize(s->dt),
+                  ADT_E_SHAPE, "batch: caches of session %d not at the common stride", b);
+  }
+  const int dm = s0->dm, F = s0->F, V = s0->V;
+  ADT_CHECK_ARG(dm % 128 == 0 && F % 128 == 0 && V % 128 == 0 && F % 64 == 0, ADT_E_SHAPE,
+                "batch: d_model, ffn and vocab must be multiples of 128");
+  return ADT_OK;
+}
+
+static size_t batch_layout(adt_batch_s* bt, const adt_session_s* s0, char* base) {
+  Bump b{base};
+  const int M = bt->Mmax, dm = s0->dm;
+  bt->h = b.take<float>((size_t)M * dm);
+  bt->C = b.take<float>((size_t)M * bt->Nmax);
+  bt->a = b.take<uint16_t>((size_t)M * dm);
+  bt->q = b.take<uint16_t>((size_t)M * dm);
+  bt->att = b.take<uint16_t>((size_t)M * dm);
+  bt->sw = b.take<uint16_t>((size_t)M * s0->F);
+  bt->feat = b.take<uint16_t>((size_t)M * dm);
+  bt->tok = b.take<int32_t>(M);
+  bt->pos = b.take<int32_t>(M);
+  bt->slot = b.take<int32_t>(M);
+  bt->seq = b.take<int32_t>(M);
+  bt->row_off = b.take<int32_t>(bt->B + 1);
+  bt->kv_len = b.take<int32_t>(bt->B);
+  bt->nq = b.take<int32_t>(bt->B);
+  bt->mask = b.take<uint64_t>((size_t)M * ADT_MASK_WORDS);
+  bt->attn_ws_bytes = tree_attn_ws_bytes(bt->B, s0->H, s0->Dh, R, s0->d.s_cap, s0->dt);
+  bt->attn_ws = b.take<char>(std::max<size_t>(bt->attn_ws_bytes, 256));
+  return align_up(b.off, 256);
+}
+
+static void batch_dims(adt_batch_s* bt, adt_session* const* ss, int B) {
+  const adt_session_s* s0 = ss[0];
+  bt->B = B;
+  bt->Mmax = B * R;
+  bt->Nmax = std::max({3 * s0->dm, 2 * s0->F, s0->V});
+}
+
+extern "C" size_t adt_batch_workspace_size(adt_session* const* sessions, int32_t B) {
+  int64_t sb = 0;
+  if (check_batch(sessions, B, sb)) return 0;
+  adt_batch_s bt;
+  batch_dims(&bt, sessions, B);
+  return batch_layout(&bt, sessions[0], nullptr);
+}
+
+extern "C" adt_status adt_batch_create(adt_session* const* sessions, int32_t B, void* workspace,
+                                       size_t workspace_bytes, adt_batch** out) {
+  ADT_CHECK_ARG(out != nullptr, ADT_E_ARG, "batch_create: null out");
+  int64_t sb = 0;
+  TRY(check_batch(sessions, B, sb));
+  adt_batch_s* bt = new (std::nothrow) adt_batch_s();
+  ADT_CHECK_ARG(bt != nullptr, ADT_E_ARG, "batch_create: out of host memory");
+  batch_dims(bt, sessions, B);
+  const size_t need = batch_layout(bt, sessions[0], nullptr);
+  if (!workspace || workspace_bytes < need) {
+    delete bt;
+    set_error("batch_create: workspace %zu < %zu bytes", workspace_bytes, need);
+    return ADT_E_CAPACITY;
+  }
+  batch_layout(bt, sessions[0], (char*)workspace);
+  bt->ss.assign(sessions, sessions + B);
+  bt->cache_sb = sb;
+  *out = bt;
+  return ADT_OK;
+}
+
+extern "C" void adt_batch_destroy(adt_batch* b) { delete b; }
+
+// The batched GEMM over packed weights, timed like the single-tree projections.
+static adt_status gemm_b(const void* X, int ldx, const void* W, int M, int N, int K, float* C, hipStream_t st) {
+  const int e = prof_pair();
+  adt_status r = launch_gemm_nt(X, ldx, W, 0, M, N, K, C, N, st, e >= 0 ? g_prof.ev[e] : nullptr,
+                                e >= 0 ? g_prof.ev[e + 1] : nullptr, true);
+  prof_done(e, ADT_PROF_GEMM, (double)N * K * 2.0 + (double)M * K * 2.0 + (double)M * N * 4.0, 2.0 * M * N * K);
+  return r;
+}
+
+// One target forward over the packed rows of every tree: embedding + norm, per layer the
+// QKV projection with RoPE and cache append, tree attention per sequence, the output
+// projection with residual add and norm, gate/up with SwiGLU, down with residual add and
+// norm, then the LM head.  Norm outputs, Q/K/V, attention output and SwiGLU product are
+// rounded to bf16 where the single-tree path rounds them; the residual stays fp32.
+static adt_status batch_forward(adt_batch_s* bt, int M, int nq_max, hipStream_t st) {
+  const adt_session_s* s0 = bt->ss[0];
+  const adt_model_s* m = s0->m;
+  const int dm = s0->dm, H = s0->H, Dh = s0->Dh, F = s0->F, V = s0->V, dt = s0->dt;
+  const float eps = m->d.norm_eps, scale = 1.f / std::sqrt((float)Dh);
+  const int64_t stride_h = (int64_t)s0->d.s_cap * Dh;
+  TRY(launch_embed_norm(m->d.embed, bt->tok, M, dm, eps, bt->h, bt->a, nullptr, dt, st));
+  for (int l = 0; l < s0->Lr; ++l) {
+    char* kc = (char*)s0->d.k_cache + (size_t)l * H * stride_h * 2;
+    char* vc = (char*)s0->d.v_cache + (size_t)l * H * stride_h * 2;
+    TRY(gemm_b(bt->a, dm, m->qkv[l], M, 3 * dm, dm, bt->C, st));
+    TRY(launch_qkv_rows(bt->C, M, H, Dh, bt->pos, bt->slot, bt->seq, s0->rope, bt->q, kc, vc, stride_h, bt->cache_sb,
+                        dt, st));
+    const int e = prof_pair();
+    TRY(launch_tree_attn(bt->q, kc, vc, bt->cache_sb, stride_h, bt->kv_len, bt->nq, bt->nq, bt->mask,
+                         AttnRows{0, 1, 0, bt->row_off}, bt->B, H, Dh, nq_max, s0->d.s_cap, scale, dt, bt->att,
+                         bt->attn_ws, bt->attn_ws_bytes, st, e >= 0 ? g_prof.ev[e] : nullptr,
+                         e >= 0 ? g_prof.ev[e + 1] : nullptr));
+    prof_done(e, ADT_PROF_ATTN, 0.0, 0.0);
+    TRY(gemm_b(bt->att, dm, m->o[l], M, dm, dm, bt->C, st));
+    TRY(launch_add_norm(bt->C, 1, M, dm, 0, eps, bt->h, bt->a, dt, st));
+    TRY(gemm_b(bt->a, dm, m->gu[l], M, 2 * F, dm, bt->C, st));
+    TRY(launch_swiglu(bt->C, 1, M, F, bt->sw, dt, st));
+    TRY(gemm_b(bt->sw, F, m->down[l], M, dm, F, bt->C, st));
+    TRY(launch_add_norm(bt->C, 1, M, dm, 0, eps, bt->h, l + 1 == s0->Lr ? bt->feat : bt->a, dt, st));
+  }
+  return gemm_b(bt->feat, dm, m->d.lm_head, M, V, dm, bt->C, st);
+}
+
+extern "C" adt_status adt_batch_step(adt_batch* bt, adt_step_out* outs, void* stream) {
+  ADT_CHECK_ARG(bt != nullptr && outs != nullptr, ADT_E_ARG, "batch_step: null pointer");
+  hipStream_t st = (hipStream_t)stream;
+  const int B = bt->B;
+  std::vector<int> dh(B, 0), kh(B, 0), n(B, 0), active(B, 0);
+  // each session's schedule and draft tree, as in adt_step
+  for (int b = 0; b < B; ++b) {
+    adt_session_s* s = bt->ss[b];
+    if ((int)s->tokens.size() - s->P >= s->T) continue;
+    active[b] = 1;
+    TRY(schedule_for(s, dh[b], kh[b]));
+    if (dh[b] >= 1) {
+      TRY(adt_tree_expand(s, dh[b], kh[b], s->d.sched.n_budget, nullptr, st));
+    } else {
+      TRY(set_root_only_tree(s, s->tokens[s->L], s->L, st));
+    }
+    n[b] = s->n_nodes;
+  }
+  // packed rows: tree b at rows [off_b, off_b + n_b); node i at cache slot L_b + i
+  std::vector<int32_t> off(B + 1, 0), kv(B, 0), slot, seq;
+  int nq_max = 1;
+  for (int b = 0; b < B; ++b) {
+    off[b + 1] = off[b] + n[b];
+    kv[b] = bt->ss[b]->L;
+    nq_max = std::max(nq_max, n[b]);
+    for (int i = 0; i < n[b]; ++i) {
+      slot.push_back(bt->ss[b]->L + i);
+      seq.push_back(b);
+    }
+  }
+  const int M = off[B];
+  if (M > 0) {
+    for (int b = 0; b < B; ++b) {
+      if (!n[b]) continue;
+      const adt_session_s* s = bt->ss[b];
+      ADT_CHECK_ARG(s->L + n[b] <= s->d.s_cap, ADT_E_CAPACITY, "batch_step: cache capacity of session %d", b);
+      ADT_HIP(hipMemcpyAsync(bt->tok + off[b], s->tr.token, sizeof(int32_t) * n[b], hipMemcpyDeviceToDevice, st));
+      ADT_HIP(hipMemcpyAsync(bt->pos + off[b], s->tr.pos, sizeof(int32_t) * n[b], hipMemcpyDeviceToDevice, st));
+      ADT_HIP(hipMemcpyAsync(bt->mask + (size_t)off[b] * ADT_MASK_WORDS, s->tr.mask,
+                             sizeof(uint64_t) * ADT_MASK_WORDS * n[b], hipMemcpyDeviceToDevice, st));
+    }
+    ADT_HIP(hipMemcpyAsync(bt->slot, slot.data(), sizeof(int32_t) * M, hipMemcpyHostToDevice, st));
+    ADT_HIP(hipMemcpyAsync(bt->seq, seq.data(), sizeof(int32_t) * M, hipMemcpyHostToDevice, st));
+    ADT_HIP(hipMemcpyAsync(bt->row_off, off.data(), sizeof(int32_t) * (B + 1), hipMemcpyHostToDevice, st));
+    ADT_HIP(hipMemcpyAsync(bt->kv_len, kv.data(), sizeof(int32_t) * B, hipMemcpyHostToDevice, st));
+    ADT_HIP(hipMemcpyAsync(bt->nq, n.data(), sizeof(int32_t) * B, hipMemcpyHostToDevice, st));
+    TRY(batch_forward(bt, M, nq_max, st));
+  }
+  // each session accepts and commits from its own rows
+  for (int b = 0; b < B; ++b) {
+    adt_session_s* s = bt->ss[b];
+    if (!active[b]) {
+      memset(&outs[b], 0, sizeof(outs[b]));
+      outs[b].done = 1;
+      continue;
+    }
+    ADT_HIP(hipMemcpyAsync(s->logits, bt->C + (size_t)off[b] * s->V, sizeof(float) * s->V * n[b],
+                           hipMemcpyDeviceToDevice, st));
+    ADT_HIP(hipMemcpyAsync(s->feat, (char*)bt->feat + (size_t)off[b] * s->dm * 2, (size_t)s->dm * 2 * n[b],
+                           hipMemcpyDeviceToDevice, st));
+    TRY(adt_session_accept_commit(s, dh[b], kh[b], &outs[b], st));
+  }
+  return ADT_OK;
+}
+
 extern "C" adt_status adt_session_get_view(const adt_session* s, adt_session_view* v) {
   ADT_CHECK_ARG(s && v, ADT_E_ARG, "get_view: null pointer");
   v->L = s->L;

@@ -90,10 +90,10 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
     if (i < n_my) {
       const int qr = (wave + 4 * i) * 16 + lq;
       if (qr < nq) {
-        const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+        const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
         for (int t = 0; t < KS; ++t) qf[i][t] = *reinterpret_cast<const bf16x8*>(qp + t * 32 + g * 8);
-        const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
+        const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
         mw0[i] = mp[0];
         mw1[i] = mp[1];
       }
@@ -294,10 +294,10 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
     for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
     const int qr = (tile0 + qg * QTW + t) * 16 + lq;
     if (qr < nq) {
-      const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+      const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) qf[t][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
-      const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
+      const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
       mw0[t] = mp[0];
       mw1[t] = mp[1];
     }
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
         ls += wt * mml[((w0 + w) * 16 + row) * 2 + 1];
         acc += wt * mo[((size_t)(w0 + w) * 16 + row) * DH + d];
       }
-      out[(((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
+      out[(rl.q_row(b, qr) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
     }
     __syncthreads();
   }
@@ -514,7 +514,7 @@ __global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const
     const float ws = wsh[s];
     if (ws != 0.f) acc += ws * part_o[(base + (int64_t)s * nq_max + qr) * DH + d];
   }
-  Elem<OutT>::store(out, (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
+  Elem<OutT>::store(out, (rl.q_row(b, qr) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
 }
 
 // fp32 path: one block per (query, head, sequence); scores staged in LDS.
@@ -529,11 +529,11 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
   if (qr >= min(n_q[b], nq_max)) return;
   const int L = kv_len[b];
   const int total = min(L + n_tail[b], kv_cap);
-  const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
+  const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
   const uint64_t w0 = mp[0], w1 = mp[1];
   float* qs = smem;
   float* sc = smem + DH;
-  const float* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+  const float* qp = q + (rl.q_row(b, qr) * H + h) * DH;
   for (int d = tid; d < DH; d += blockDim.x) qs[d] = qp[d];
   __syncthreads();
   const float* kb = kc + b * stride_b + h * stride_h;
@@ -566,7 +566,7 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
   for (int d = tid; d < DH; d += blockDim.x) {
     float acc = 0.f;
     for (int k = 0; k < total; ++k) acc += sc[k] * vb[(int64_t)k * DH + d];
-    out[(((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH + d] = acc / sum;
+    out[(rl.q_row(b, qr) * H + h) * DH + d] = acc / sum;
   }
 }
 
@@ -622,10 +622,10 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
 #pragma unroll
   for (int kk = 0; kk < KS; ++kk) qf[kk] = bf16x8{};
   if (active && qr < nq) {
-    const uint16_t* qp = q + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+    const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
-    const uint64_t* mp = mask + ((int64_t)b * rl.ms_b + qr) * ADT_MASK_WORDS;
+    const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
     mw0 = mp[0];
     mw1 = mp[1];
   }
@@ -778,7 +778,7 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
   }
   if (active && kpart == 0 && qr < nq) {
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    uint16_t* op = out + (((int64_t)b * rl.rs_b + (int64_t)qr * rl.rs_i) * H + h) * DH;
+    uint16_t* op = out + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
     for (int d = 0; d < DT; ++d)
       *reinterpret_cast<u16x4*>(op + d * 16 + 4 * g) =

@@ -12,6 +12,10 @@
 //   B operand (X rows):  lane l holds X[m0 + l%32][k0 + 8*(l/32) .. +7]
 //   D (C^T block):       lane l, register v holds C[m0 + l%32][n0 + 8*(v/4) + 4*(l/32) + v%4]
 // so each lane stores four consecutive columns of a C row per register group.
+// W is either row-major (ldw) or in the library's packed weight layout (16 x 32 tiles of
+// 1 KB, tile (n/16, k/32) at ((n/16) K/32 + k/32) * 512 elements, the 8 elements k..k+7 of
+// row n at ((k%32)/8 * 16 + n%16) * 8 within it), so the forwards' packed weights serve the
+// batched path too.
 #include <hip/hip_ext.h>
 
 #include "../launch.h"
@@ -25,7 +29,7 @@ constexpr int NT_THREADS = NT_WAVES_N * NT_WAVES_M * WAVE;
 constexpr int NT_BK = 64;
 constexpr int NT_ROW = NT_BK + 8;   // padded LDS row, bf16 (144 B: 16-byte reads of 16 lanes hit distinct banks)
 
-template <int BN, int BM>
+template <int BN, int BM, bool PACKED>
 __global__ __launch_bounds__(NT_THREADS) void gemm_nt_kernel(const uint16_t* __restrict__ X, int64_t ldx,
                                                              const uint16_t* __restrict__ W, int64_t ldw, int M,
                                                              int K, float* __restrict__ C, int64_t ldc) {
@@ -49,13 +53,18 @@ __global__ __launch_bounds__(NT_THREADS) void gemm_nt_kernel(const uint16_t* __r
 #pragma unroll
   for (int i = 0; i < CH; ++i) {
     const int row = crow + RPP * i;
-    gsrc[i] = i < WCH ? W + (int64_t)(n0 + row) * ldw + ccol
+    const int n = n0 + row;
+    const int64_t wofs = PACKED ? ((int64_t)(n / 16) * (K / 32) + ccol / 32) * 512 + (((ccol % 32) / 8) * 16 + n % 16) * 8
+                                : (int64_t)n * ldw + ccol;
+    gsrc[i] = i < WCH ? W + wofs
                       : X + (int64_t)min(m0 + row - BN, M - 1) * ldx + ccol;   // rows past M feed discarded columns
   }
+  // per stage: 64 columns of X; of W 64 columns, or two packed tiles
+  constexpr int WSTEP = PACKED ? 1024 : NT_BK;
   u16x8 stg[CH];
   auto gload = [&](int kt) {
 #pragma unroll
-    for (int i = 0; i < CH; ++i) stg[i] = *reinterpret_cast<const u16x8*>(gsrc[i] + kt * NT_BK);
+    for (int i = 0; i < CH; ++i) stg[i] = *reinterpret_cast<const u16x8*>(gsrc[i] + kt * (i < WCH ? WSTEP : NT_BK));
   };
   auto lstore = [&](int buf) {
     uint16_t* base = lds + buf * STAGE;
@@ -119,25 +128,29 @@ __global__ __launch_bounds__(NT_THREADS) void gemm_nt_kernel(const uint16_t* __r
 }
 
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
-                          int64_t ldc, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+                          int64_t ldc, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, bool packed) {
   ADT_CHECK_ARG(X && W && C, ADT_E_ARG, "gemm_nt: null pointer");
   ADT_CHECK_ARG(M >= 1 && N >= 128 && K >= 64 && N % 128 == 0 && K % 64 == 0, ADT_E_SHAPE,
                 "gemm_nt: M=%d N=%d K=%d (N a multiple of 128, K of 64)", M, N, K);
-  ADT_CHECK_ARG(ldx >= K && ldw >= K && ldc >= N && ldx % 8 == 0 && ldw % 8 == 0 && ldc % 4 == 0, ADT_E_SHAPE,
-                "gemm_nt: leading dimensions");
+  ADT_CHECK_ARG(ldx >= K && (packed || ldw >= K) && ldc >= N && ldx % 8 == 0 && ldw % 8 == 0 && ldc % 4 == 0,
+                ADT_E_SHAPE, "gemm_nt: leading dimensions");
   // Tile choice (measured on the M = 976 projections of the 7B layer shapes): 256 x 256
   // when it still gives every CU a workgroup, else 128 x 128 (two workgroups per CU by LDS);
   // 256 x 128 was never the fastest.
   const int best = (N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 256) ? 0 : 2;
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)W;
+#define ADT_NT(BNV, BMV, PK)                                                                                    \
+  hipExtLaunchKernelGGL(gemm_nt_kernel<BNV, BMV, PK>, dim3((M + BMV - 1) / BMV, N / BNV), dim3(NT_THREADS), 0, st, \
+                        ev0, ev1, 0, x, ldx, w, ldw, M, K, C, ldc)
   if (best == 0) {
-    hipExtLaunchKernelGGL(gemm_nt_kernel<256, 256>, dim3((M + 255) / 256, N / 256), dim3(NT_THREADS), 0, st, ev0,
-                          ev1, 0, x, ldx, w, ldw, M, K, C, ldc);
+    if (packed) ADT_NT(256, 256, true);
+    else ADT_NT(256, 256, false);
   } else {
-    hipExtLaunchKernelGGL(gemm_nt_kernel<128, 128>, dim3((M + 127) / 128, N / 128), dim3(NT_THREADS), 0, st, ev0,
-                          ev1, 0, x, ldx, w, ldw, M, K, C, ldc);
+    if (packed) ADT_NT(128, 128, true);
+    else ADT_NT(128, 128, false);
   }
+#undef ADT_NT
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

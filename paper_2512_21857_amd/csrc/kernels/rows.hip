@@ -209,6 +209,39 @@ __global__ __launch_bounds__(ROW_THREADS) void qkv_rope_kernel(const float* __re
   Elem<T>::store(vr, j + half, v2);
 }
 
+// Batched verify, after the QKV projection of packed-order weights: C[m][3d] fp32 whose
+// columns follow the ADT_PACK_QKV row order (within a head, 16-column tile u holds dims
+// 8u..8u+7 of the head's first half, then the same dims of its second half: RoPE pairs
+// sit 8 columns apart).  Row m belongs to sequence seq[m], position pos[m], cache slot
+// slot[m]; q row m gets the rotated query, the caches of its sequence (base + seq *
+// cache_sb) the rotated key and the value, all in the head's natural dim order.
+// Grid (M, pairs / 256 rounded up); one RoPE pair per thread.
+template <typename T>
+__global__ __launch_bounds__(ROW_THREADS) void qkv_rows_kernel(const float* __restrict__ C, int H, int Dh,
+                                                               const int32_t* __restrict__ pos,
+                                                               const int32_t* __restrict__ slot,
+                                                               const int32_t* __restrict__ seq,
+                                                               const float2* __restrict__ rope, T* __restrict__ qout,
+                                                               T* __restrict__ kc, T* __restrict__ vc, int64_t stride_h,
+                                                               int64_t cache_sb) {
+  const int m = blockIdx.x;
+  const int d = H * Dh, half = Dh / 2;
+  const int i = blockIdx.y * blockDim.x + threadIdx.x;
+  if (i >= H * half) return;
+  const int hh = i / half, j = i % half;
+  const int c1 = hh * Dh + (j / 8) * 16 + j % 8, c2 = c1 + 8;     // packed columns of dims j, j + half
+  const float* row = C + (int64_t)m * 3 * d;
+  const float2 cs = rope[(int64_t)pos[m] * half + j];
+  const float q1 = row[c1], q2 = row[c2], k1 = row[d + c1], k2 = row[d + c2];
+  Elem<T>::store(qout, (int64_t)m * d + hh * Dh + j, q1 * cs.x - q2 * cs.y);
+  Elem<T>::store(qout, (int64_t)m * d + hh * Dh + j + half, q2 * cs.x + q1 * cs.y);
+  const int64_t off = (int64_t)seq[m] * cache_sb + hh * stride_h + (int64_t)slot[m] * Dh;
+  Elem<T>::store(kc + off, j, k1 * cs.x - k2 * cs.y);
+  Elem<T>::store(kc + off, j + half, k2 * cs.x + k1 * cs.y);
+  Elem<T>::store(vc + off, j, row[2 * d + c1]);
+  Elem<T>::store(vc + off, j + half, row[2 * d + c2]);
+}
+
 // SwiGLU over gate/up products packed in interleaved 8-column blocks: out[m][j] = silu(g) u.
 // Grid (M, F / (4 * 256)); four consecutive outputs per thread.
 template <typename T>
@@ -390,6 +423,18 @@ adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, 
   dim3 grid(M, (H * Dh / 2 + ROW_THREADS - 1) / ROW_THREADS);
   ADT_DISPATCH_T(dtype, qkv_rope_kernel<T><<<grid, ROW_THREADS, 0, st>>>(part, splits, M, H, Dh, pos, slot0, rope,
                                                                           (T*)qout, (T*)kc, (T*)vc, stride_h, br));
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_qkv_rows(const float* C, int M, int H, int Dh, const int32_t* pos, const int32_t* slot,
+                           const int32_t* seq, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
+                           int64_t cache_sb, int dtype, hipStream_t st) {
+  ADT_CHECK_ARG(Dh % 16 == 0, ADT_E_SHAPE, "qkv_rows: head_dim %d", Dh);
+  if (M <= 0) return ADT_OK;
+  dim3 grid(M, (H * Dh / 2 + ROW_THREADS - 1) / ROW_THREADS);
+  ADT_DISPATCH_T(dtype, qkv_rows_kernel<T><<<grid, ROW_THREADS, 0, st>>>(C, H, Dh, pos, slot, seq, rope, (T*)qout,
+                                                                          (T*)kc, (T*)vc, stride_h, cache_sb));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

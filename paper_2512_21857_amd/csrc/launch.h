@@ -18,9 +18,18 @@ struct Branches {
 // attn.hip
 // Row of query qr of sequence b in q and out: b * rs_b + qr * rs_i (rows of H * Dh); its mask
 // row: b * ms_b + qr.  Separate sequences: (nq_max, 1, nq_max).  Guidance branches of one
-// tree interleaved node by node: (1, B, 0), one mask per node.
+// tree interleaved node by node: (1, B, 0), one mask per node.  With row_off (device, [B])
+// the rows of sequence b start at row_off[b] instead (packed trees of different sizes), for
+// q, out and masks alike.
 struct AttnRows {
   int rs_b, rs_i, ms_b;
+  const int32_t* row_off = nullptr;
+  __device__ __forceinline__ int64_t q_row(int b, int qr) const {
+    return (row_off ? (int64_t)row_off[b] : (int64_t)b * rs_b) + (int64_t)qr * rs_i;
+  }
+  __device__ __forceinline__ int64_t m_row(int b, int qr) const {
+    return (row_off ? (int64_t)row_off[b] : (int64_t)b * ms_b) + qr;
+  }
 };
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype);
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
@@ -69,8 +78,10 @@ struct GemmEpi {
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
                        const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // gemm_nt.hip: C[M][N] fp32 = X[M][K] . W[N][K]^T, bf16 row-major operands (MFMA-bound batches)
+// (packed: W in the adt_pack_weight layout, ldw unused; rows in the packed order)
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
-                          int64_t ldc, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                          int64_t ldc, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                          bool packed = false);
 // rows.hip
 // h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
 // of squares of h into ssp[m][d/16].
@@ -89,6 +100,11 @@ adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, h
 adt_status launch_qkv_rope(const float* part, int splits, int M, int H, int Dh, const int32_t* pos,
                            const int32_t* slot0, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
                            int dtype, hipStream_t st, const Branches& br = Branches{});
+// Batched verify: RoPE and cache append from fp32 QKV products in ADT_PACK_QKV column order;
+// row m belongs to sequence seq[m] (caches cache_sb elements apart), position pos[m], slot slot[m].
+adt_status launch_qkv_rows(const float* C, int M, int H, int Dh, const int32_t* pos, const int32_t* slot,
+                           const int32_t* seq, const float2* rope, void* qout, void* kc, void* vc, int64_t stride_h,
+                           int64_t cache_sb, int dtype, hipStream_t st);
 adt_status launch_swiglu(const float* part, int splits, int M, int F, void* out, int dtype, hipStream_t st);
 adt_status launch_reduce_store(const float* part, int splits, int M, int N, float* out, int64_t ldo, hipStream_t st);
 adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,

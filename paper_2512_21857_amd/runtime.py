@@ -220,7 +220,9 @@ class DeviceSession:
     def __init__(self, model: DeviceModel, cfg, poisson: Optional[np.ndarray] = None,
                  knn: Optional[torch.Tensor] = None, accept_seed: Optional[int] = None, fixed_tree: bool = False,
                  accept_mode: Optional[str] = None, draft_table: Optional[torch.Tensor] = None,
-                 use_graphs: bool = True):
+                 use_graphs: bool = True, caches: Optional[tuple] = None):
+        """caches: optional (k_cache, v_cache) views to use as the target caches (a batch
+        passes slices of one allocation); otherwise they are allocated here."""
         m = cfg.model
         self.model = model
         self.cfg = cfg
@@ -230,8 +232,11 @@ class DeviceSession:
         guided = getattr(cfg, "guidance", None) is not None
         self.nb = 2 if guided else 1
         br = (2,) if guided else ()       # guidance: conditional and unconditional caches
-        self.k_cache = torch.zeros(*br, m.n_layers, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
-        self.v_cache = torch.zeros_like(self.k_cache)
+        if caches is not None:
+            self.k_cache, self.v_cache = caches
+        else:
+            self.k_cache = torch.zeros(*br, m.n_layers, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
+            self.v_cache = torch.zeros_like(self.k_cache)
         self.dk_cache = torch.zeros(*br, m.n_heads, self.s_cap, m.head_dim, dtype=tdt, device=dev)
         self.dv_cache = torch.zeros_like(self.dk_cache)
         allowed = np.ascontiguousarray(cfg.allowed_table().reshape(-1), dtype=np.int32)
@@ -339,6 +344,45 @@ class DeviceSession:
             out["branch_logits"] = self._ws(v.branch_logits, n * 2 * m.vocab, torch.float32).view(n, 2, m.vocab)
             out["draft_branch_logits"] = self._ws(v.draft_branch_logits, 2 * m.vocab, torch.float32).view(2, m.vocab)
         return out
+
+
+class DeviceBatch:
+    """Several images decoded together: B sessions of one model whose target caches are
+    slices of one [B][layers][heads][s_cap][head_dim] allocation, verified by one forward
+    per cycle (adt_batch_step)."""
+
+    def __init__(self, model: DeviceModel, cfgs: Sequence, fixed_tree: bool = False):
+        m = cfgs[0].model
+        B = len(cfgs)
+        s_cap = ((cfgs[0].prefix_len + cfgs[0].n_image + abi.MAX_NODES + 63) // 64) * 64
+        tdt = TORCH_DT[model.dtype]
+        self.k_cache = torch.zeros(B, m.n_layers, m.n_heads, s_cap, m.head_dim, dtype=tdt, device=model.device)
+        self.v_cache = torch.zeros_like(self.k_cache)
+        self.sessions = [DeviceSession(model, c, fixed_tree=fixed_tree, use_graphs=False,
+                                       caches=(self.k_cache[b], self.v_cache[b])) for b, c in enumerate(cfgs)]
+        self._handles = (C.c_void_p * B)(*[s.handle.value for s in self.sessions])
+        self.handle = None
+
+    def prefill(self, prefixes: Sequence[np.ndarray]) -> List[int]:
+        firsts = [s.prefill(p) for s, p in zip(self.sessions, prefixes)]
+        B = len(self.sessions)
+        need = lib().adt_batch_workspace_size(self._handles, B)
+        if need == 0:
+            check(lib().adt_batch_create(self._handles, B, None, 0, C.byref(C.c_void_p())))
+        self.workspace = torch.empty(need, dtype=torch.uint8, device=self.k_cache.device)
+        self.handle = C.c_void_p()
+        check(lib().adt_batch_create(self._handles, B, _p(self.workspace), need, C.byref(self.handle)))
+        return firsts
+
+    def step(self) -> List[dict]:
+        outs = (abi.StepOut * len(self.sessions))()
+        check(lib().adt_batch_step(self.handle, outs, _stream()))
+        return [_step_dict(o) for o in outs]
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib_loaded():
+            lib().adt_batch_destroy(self.handle)
+            self.handle = None
 
 
 def _step_dict(o: abi.StepOut) -> dict:

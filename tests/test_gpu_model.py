@@ -323,3 +323,100 @@ def test_determinism(rt, graphs):
         toks = [sess.step()["tokens"] for _ in range(4)]
         outs.append((toks, sess.tensors()["logits"].cpu().numpy().copy()))
     assert outs[0][0] == outs[1][0] and np.array_equal(outs[0][1], outs[1][1])
+
+
+# ---------------------------------------------------------------- batched cycle
+def _batch_prompts(cfg, B):
+    return [synth.prefix_ids(dataclasses.replace(cfg, seed=cfg.seed + 101 * b)) for b in range(B)]
+
+
+@pytest.mark.parametrize("B,fixed", [(4, False), (5, True), (16, True)])
+def test_batch_cycle_matches_single_sessions(rt, B, fixed):
+    """adt_batch_step (one verify forward over the packed rows of B trees, MFMA-tiled GEMMs on
+    the packed weights, per-sequence attention) against B sessions stepped alone, in lockstep:
+    each cycle the single session expands with the batch's (d, k) (root draft logits within
+    the bf16 tolerance; its tree equal to the batch's unless the single session's own root
+    top-k margin lies inside the observed draft error, or the difference is deeper, where the
+    draft inputs already carry the previous verify's rounding), then verifies the batch's tree
+    (verify logits within the tolerance) and accepts (committed tokens equal unless the single
+    session's argmax margin on the path is inside the observed error; that sequence then
+    stops).  The single path itself is checked against the oracle by the tests above.  Fixed
+    6-deep, 10-wide trees give 61 rows per tree (M up to 976)."""
+    cfg = _small_bf16()
+    w, om, dm, _ = _setup(rt, cfg)
+    prompts = _batch_prompts(cfg, B)
+    batch = rt.DeviceBatch(dm, [cfg] * B, fixed_tree=fixed)
+    singles = [rt.DeviceSession(dm, cfg, fixed_tree=fixed, use_graphs=False) for _ in range(B)]
+    firsts = batch.prefill(prompts)
+    assert firsts == [s.prefill(p) for s, p in zip(singles, prompts)]
+    live = [True] * B
+    tol = TOL["bf16"]
+    stats = {"cycles": 0, "rows": 0, "tree_equal": 0, "tree_level1_ties": 0, "deeper_tree_differs": 0,
+             "commit_ties": 0, "oracle_cycles": 0}
+    # sequence 0 also against the oracle: its schedule, and its verify of the batch's tree
+    dec = Decoder(cfg, om, prompts[0])
+    if fixed:
+        sc = cfg.sched
+        dec.schedule_next = lambda: (min(sc.d_hi, cfg.n_image - (dec.L + 1 - dec.P) - 1), sc.k_hi)
+    oracle_live = dec.prefill() == firsts[0]
+    for step in range(8):
+        outs = batch.step()
+        for b in range(B):
+            if not live[b]:
+                continue
+            g, s = outs[b], singles[b]
+            if g["n_committed"] == 0:
+                live[b] = False
+                continue
+            d, k = g["d_hat"], g["k_hat"]
+            t = batch.sessions[b].tensors()
+            bpar, btok = t["parent"].cpu().tolist(), t["token"].cpu().tolist()
+            if d >= 1:
+                n = s.expand(d, k, cfg.sched.n_budget)
+                ts = s.tensors()
+                gz, sz = t["draft_logits"][0].cpu().numpy(), ts["draft_logits"][0].cpu().numpy()
+                assert _tol_ok(gz, sz, tol).all(), f"sequence {b}: root draft logits"
+                if ts["parent"].cpu().tolist() == bpar and ts["token"].cpu().tolist() == btok:
+                    stats["tree_equal"] += 1
+                else:
+                    l1 = lambda par, tok: [tok[i] for i in range(len(par)) if par[i] == 0]
+                    if l1(bpar, btok) != l1(ts["parent"].cpu().tolist()[:n], ts["token"].cpu().tolist()[:n]):
+                        lo, hi = ts["allowed"].cpu().numpy()[0]
+                        z = np.sort(sz[lo:hi].astype(np.float64))[::-1][: k + 1]
+                        err = float(np.abs(gz - sz).max())
+                        assert np.min(z[:-1] - z[1:]) < 2 * err + tol[0], f"sequence {b}: first level differs"
+                        stats["tree_level1_ties"] += 1
+                    else:
+                        stats["deeper_tree_differs"] += 1
+            s.set_tree(bpar, btok)
+            s.verify()
+            ts = s.tensors()
+            glog, slog = t["logits"].cpu().numpy(), ts["logits"].cpu().numpy()
+            assert glog.shape == slog.shape
+            assert _tol_ok(glog, slog, tol).all(), f"sequence {b}: verify logits max diff {np.abs(glog - slog).max()}"
+            if b == 0 and oracle_live and not dec.done():
+                assert dec.schedule_next() == (d, k), "schedule differs from the oracle"
+                tree = Tree(np.asarray(bpar, np.int32), np.asarray(btok, np.int32), depths(bpar).astype(np.int32),
+                            np.zeros(len(bpar)), np.full(len(bpar), -1))
+                info = dec.verify_commit(tree, d, k, expanded=d >= 1)
+                assert _tol_ok(glog, info.logits, tol).all(), \
+                    f"verify logits vs oracle: max diff {np.abs(glog - info.logits).max()}"
+                stats["oracle_cycles"] += 1
+                if info.committed != g["tokens"]:
+                    err = float(np.abs(glog - info.logits).max())
+                    margins = [_greedy_margin(info.logits[u], *info.allowed[u]) for u in [0] + info.path]
+                    assert min(margins) < 2 * err + tol[0], "tokens differ from the oracle without a near-tie"
+                    oracle_live = False
+            o = s.accept_commit(d, k)
+            stats["cycles"] += 1
+            stats["rows"] += len(bpar)
+            if g["tokens"] != o["tokens"]:
+                err = float(np.abs(glog - slog).max())
+                allowed = ts["allowed"].cpu().numpy()
+                path = ts["path"].cpu().numpy()[: o["n_accepted"] + 1]
+                margins = [_greedy_margin(slog[u], *allowed[u]) for u in path]
+                assert min(margins) < 2 * err + tol[0], f"sequence {b}: tokens differ without a near-tie"
+                stats["commit_ties"] += 1
+                live[b] = False
+    print("batch", B, "fixed", fixed, stats)
+    assert stats["cycles"] >= B * 6 and stats["oracle_cycles"] >= 4
