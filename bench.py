@@ -11,7 +11,8 @@ second; the line also carries the roofline of the dominant kernel (the weight-st
 projections), tree-attention bandwidth (in the cycle and in the 16 x 32 x 128 tree-attention
 microbenchmark), the batched verify projections, the same cycle under classifier-free
 guidance (scale 3.0: both branches in every forward), 16 images decoded together (one verify
-forward over all their trees per step) and the CPU oracle timed on this host.
+forward over all their trees per step), the cycle with stochastic children (drawn from q,
+verified by Eq. 1 as printed) and the CPU oracle timed on this host.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -66,6 +67,7 @@ def parse():
     ap.add_argument("--no-mfma", action="store_true")
     ap.add_argument("--no-guided", action="store_true")
     ap.add_argument("--no-batch", action="store_true")
+    ap.add_argument("--no-stochastic", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -157,34 +159,50 @@ BATCHED_SHAPES = ((4096, 12288), (4096, 4096), (4096, 22016), (11008, 4096), (40
 
 def mfma_benchmark(rt, M=976, iters=10):
     """The verify projections of 16 trees of 61 rows at once (M = 976) with the 7B-shaped
-    layer dimensions (K, N): QKV, O, gate/up, down, LM head.  MFMA-bound (AI >> 315 flop/B)."""
+    layer dimensions (K, N): QKV, O, gate/up, down, LM head, weights in the library's packed
+    layout (as every model weight is kept).  MFMA-bound (AI >> 315 flop/B).  The vendor BLAS
+    (torch.mm, bf16 out) on the same operands is timed beside it for context."""
     import torch
     torch.manual_seed(5)
-    out, tot_fl, tot_ms = {}, 0.0, 0.0
-    for K, N in BATCHED_SHAPES:
-        x = torch.randn(M, K, device="cuda").bfloat16()
-        w = torch.randn(N, K, device="cuda").bfloat16()
-        c = torch.empty(M, N, dtype=torch.float32, device="cuda")
+    out, tot_fl, tot_ms, tot_ref = {}, 0.0, 0.0, 0.0
+
+    def ev_time(f):
         for _ in range(2):
-            rt.gemm_bf16(x, w, out=c)
+            f()
         st = torch.cuda.current_stream()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(st)
         for _ in range(iters):
-            rt.gemm_bf16(x, w, out=c)
+            f()
         e1.record(st)
         e1.synchronize()
-        ms = e0.elapsed_time(e1) / iters
+        return e0.elapsed_time(e1) / iters
+
+    for K, N in BATCHED_SHAPES:
+        x = torch.randn(M, K, device="cuda").bfloat16()
+        w = torch.randn(N, K, device="cuda").bfloat16()
+        wp = rt.pack_bf16(w)
+        c = torch.empty(M, N, dtype=torch.float32, device="cuda")
+        ms = ev_time(lambda: rt.gemm_bf16_packed(x, wp, N, out=c))
+        cb = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+        wt = w.t()
+        ref_ms = ev_time(lambda: torch.mm(x, wt, out=cb))
         fl = 2.0 * M * N * K
         tot_fl += fl
         tot_ms += ms
-        out[f"{K}x{N}"] = {"us": round(ms * 1e3, 1), "TFLOP_s": round(fl / ms / 1e9, 1)}
-        del x, w, c
+        tot_ref += ref_ms
+        out[f"{K}x{N}"] = {"us": round(ms * 1e3, 1), "TFLOP_s": round(fl / ms / 1e9, 1),
+                           "vendor_blas_TFLOP_s": round(fl / ref_ms / 1e9, 1)}
+        del x, w, wp, c, cb, wt
     torch.cuda.empty_cache()
     tf = tot_fl / tot_ms / 1e9
+    ref_tf = tot_fl / tot_ref / 1e9
     return {"M": M, "shapes_KxN": out, "total_us": round(tot_ms * 1e3, 1), "TFLOP_s": round(tf, 1),
             "peak_TFLOP_s": MFMA_PEAK_TFLOPS, "frac": round(tf / MFMA_PEAK_TFLOPS, 4),
-            "kernel": "gemm_nt_kernel (bf16 MFMA 32x32x16, fp32 out)"}
+            "vendor_blas": {"TFLOP_s": round(ref_tf, 1), "frac": round(ref_tf / MFMA_PEAK_TFLOPS, 4),
+                            "call": "torch.mm bf16 -> bf16 (hipBLASLt), same operands"},
+            "kernel": "gemm_nt_dma_kernel (>= 128 blocks of 256x256: global->LDS DMA ring) / gemm_nt_kernel "
+                      "(bf16 MFMA 32x32x16, fp32 out)"}
 
 
 def cpu_baseline(cfg, weights, budget_s):
@@ -257,6 +275,21 @@ def main():
                 "nodes_per_step": round(gnodes / k, 2), "tokens_per_step": round(gtokens / k, 3),
                 "mean_depth": round(gdepth / k, 3), "steps": k}
 
+    def stochastic_run(k, children=3):
+        """The same cycle with stochastic children (children drawn from q at T = 1, every drawn
+        child kept, Eq. 1 acceptance with the residual norm(max(0, p - q)))."""
+        import dataclasses
+        scfg = dataclasses.replace(cfg, accept=synth.AcceptCfg(mode="mss", temperature=1.0, top_k=0,
+                                                                children=children))
+        ss = rt.DeviceSession(dm, scfg)
+        ss.prefill(pre)
+        run_steps(ss, 3)
+        sdt, snodes, stokens, sdepth = timed(ss, k)
+        del ss
+        return {"children": children, "temperature": 1.0, "nodes_per_s": round(snodes / sdt, 2),
+                "ms_per_step": round(sdt / k * 1e3, 4), "nodes_per_step": round(snodes / k, 2),
+                "tokens_per_step": round(stokens / k, 3), "mean_depth": round(sdepth / k, 3), "steps": k}
+
     def batched_run(B, fixed, k):
         """B images decoded together: per image its own schedule and draft tree, one verify
         forward over the packed rows of all B trees per step (packed-weight MFMA GEMMs)."""
@@ -306,6 +339,7 @@ def main():
     micro = {} if args.no_microbench else attn_microbench(rt)
     mfma = None if args.no_mfma else mfma_benchmark(rt)
     guided = None if args.no_guided else guided_run(min(args.steps, 50))
+    stochastic = None if args.no_stochastic else stochastic_run(min(args.steps, 50))
     batched = None if args.no_batch else [batched_run(16, True, min(args.steps, 30)),
                                           batched_run(16, False, min(args.steps, 30))]
     line = {
@@ -338,6 +372,7 @@ def main():
         "batched_verify_gemm": mfma,
         "guided": guided,
         "batched": batched,
+        "stochastic_children": stochastic,
         "fixed_tree": {"nodes_per_s": round(fnodes / fdt, 2), "ms_per_step": round(fdt / min(args.steps, 50) * 1e3, 4),
                        "nodes_per_step": round(fnodes / min(args.steps, 50), 2), "tree": "depth 6, width 10, top-60"},
     }

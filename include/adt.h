@@ -52,6 +52,7 @@ typedef int32_t adt_status;
 #define ADT_ACCEPT_GREEDY 0
 #define ADT_ACCEPT_EXACT 1
 #define ADT_ACCEPT_RELAXED 2
+#define ADT_ACCEPT_MSS 3
 
 #define ADT_ALPHA_REAL 0
 #define ADT_ALPHA_POISSON 1
@@ -127,6 +128,16 @@ adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, int32_t slice
  *  RELAXED: as EXACT but x is credited with the weights of its nearest codebook neighbours
  *    knn[x][1..knn_k-1] taken in order while their sum stays <= delta * (remaining total);
  *    on rejection the credited set is removed.
+ *  MSS: Eq. 1 as printed, for trees whose children are i.i.d. draws from q (stochastic
+ *    children, Sec. 3.1: each selected node generates its children by sampling from the
+ *    draft distribution; a session in this mode expands that way, see adt_tree_expand).
+ *    At node u the children are tried in node order: child x is accepted iff
+ *    u32 * qw(x) * Wp < 2^32 * pw(x) * Wq (probability min(1, p(x) / q(x))), u32 = U >> 32
+ *    of the draw at (step, u, trial, 0); after a rejection pw(y) <- max(0, pw(y) Wq -
+ *    qw(y) Wp) >> s with s the least shift leaving every weight below 2^32 (the residual
+ *    norm(max(0, p - q)) of multi-step speculative sampling); with all rejected the bonus
+ *    is drawn from the residual, at a leaf from p.  qw, Wq: the weights (same temperature
+ *    and top_k as p) of row q_row[u] of q_logits, the draft row that drew u's children.
  *  Draws: r = floor(U * W / 2^64), U = Philox4x32-10(key = seed, counter = (step, node,
  *    trial, 0)) words (x1 << 32 | x0), W = remaining total weight.
  * logits: [n][ld] fp32 (row u gives the target distribution of u's successor)
@@ -144,6 +155,12 @@ typedef struct {
   int32_t knn_stride;  /* int32 per knn row */
   const int32_t* knn;  /* device [knn_rows][knn_stride] */
   uint64_t seed;
+  int32_t children;    /* MSS sessions: children drawn per expanded node, in [1, 16] and <= n_budget */
+  const float* q_logits;   /* MSS, adt_verify_accept: device [rows][q_ld] draft logits (sessions set their own) */
+  int64_t q_ld;
+  const int32_t* q_row;    /* MSS, adt_verify_accept: device [n] row of q_logits that drew node u's children;
+                              an entry outside [0, q_rows) stops the walk at u (bonus drawn from p) */
+  int32_t q_rows;          /* MSS, adt_verify_accept: rows of q_logits */
 } adt_accept_cfg;
 
 size_t adt_accept_workspace_size(int32_t V);
@@ -172,6 +189,13 @@ adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t dim, int32
  * pointers, ADT_E_SHAPE on other shapes; nothing is enqueued on error. */
 adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw, int32_t M, int32_t N, int32_t K,
                          float* C, int64_t ldc, void* stream);
+
+/* The same product with W in the packed layout of adt_pack_weight (ADT_PACK_STACK, bf16;
+ * the layout every model weight is kept in), as the batched verification forward multiplies
+ * it.  Wp: device, adt_packed_bytes(N, K, ADT_BF16) bytes, W's rows in their packed
+ * order (C's columns follow that order).  Shapes, errors and asynchrony as adt_gemm_bf16. */
+adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K, float* C,
+                                int64_t ldc, void* stream);
 
 /* ------------------------------------------------------------------ weights
  * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM
@@ -348,7 +372,14 @@ adt_status adt_session_get_view(const adt_session* s, adt_session_view* v);
 /* a1-a3: the draft head's catch-up rows then d_hat - 1 frontier forwards (Sec. 4.2, Eq. 4),
  * top-k children scored by summed log-probability (Eq. 3), frontier select, top-N rerank and
  * the BFS tree arrays + masks of the session's current tree.  n_nodes_out [host] gets the
- * tree size (root included). */
+ * tree size (root included).
+ * Sessions in ADT_ACCEPT_MSS mode draw the children instead (Sec. 3.1 read literally): every
+ * expanded node takes accept.children i.i.d. draws from q (the acceptance's integer weights
+ * of its draft row), child j of tree node u at r = floor(U W_q / 2^64), U at counter (step,
+ * u, j, 2), the id the smallest with prefix weight > r.  All drawn children stay in the tree
+ * (no rerank: the siblings must remain an i.i.d. sample of q); each later layer expands the
+ * k_hat best nodes of the previous one by path confidence, as many as keep the tree within
+ * n_budget draft nodes; nodes are in creation order (siblings in draw order). */
 adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_hat, int32_t n_budget, int32_t* n_nodes_out,
                            void* stream);
 /* Replaces the session's current tree with a caller tree: parent/token [host] n ids, BFS

@@ -27,6 +27,17 @@ kernel decides in); all later arithmetic is exact integer.  A draw is
 r = floor(U * W / 2^64) with U the 64 bits of Philox4x32-10 at key = seed and
 counter = (step, node, trial, 0), and W the remaining total weight.
 
+Literal Eq. 1 with stochastic children (accept_mss): the children of a node are i.i.d.
+draws from q, so Eq. 1's ratio applies as printed.  Siblings are tried in draw order:
+child x is accepted with probability min(1, p(x) / q(x)); after a rejection p becomes the
+residual norm(max(0, p - q)) (the multi-step rule of SpecInfer, which the paper builds on)
+and the next sibling is tried against it; if all are rejected the bonus is drawn from the
+last residual, and at a leaf from p.  The committed token's law is exactly p.  Numbers: p
+and q are the same integer weights as above (q from the draft row that drew the children),
+with totals W_p, W_q; the test u < p(x)/q(x) with a 32-bit uniform u = U >> 32 is the
+integer comparison u * q_w(x) * W_p < 2^32 * p_w(x) * W_q; the residual weights are
+max(0, p_w(y) W_q - q_w(y) W_p) shifted right until the largest fits in 32 bits.
+
 Test infrastructure only; see the package docstring.
 """
 from __future__ import annotations
@@ -165,5 +176,46 @@ def accept_sampling(logits: np.ndarray, parent, token, allowed, *, temperature: 
                 return path, top1_id(logits[u], lo, hi, temperature)
             r = draw_below(uniform_u64(seed, step, u, trial), W)
             return path, inverse_cdf(w, r)
+        path.append(accepted)
+        u = accepted
+
+
+MSS_WEIGHT_BITS = 32
+
+
+def accept_mss(logits: np.ndarray, q_rows: dict, parent, token, allowed, *, temperature: float, top_k: int,
+               seed: int, step: int) -> Tuple[List[int], int]:
+    """Multi-step acceptance of a tree with stochastic children (Eq. 1 with the residual
+    norm(max(0, p - q))).  q_rows[u]: the draft logit row whose q drew node u's children.
+    Returns (path, bonus)."""
+    ch = children_of(parent)
+    path: List[int] = []
+    u = 0
+    while True:
+        lo, hi = int(allowed[u][0]), int(allowed[u][1])
+        wp = [int(v) for v in quantised_weights(logits[u], lo, hi, temperature, top_k)]
+        Wp = sum(wp)
+        trial = 0
+        accepted = None
+        if ch[u]:
+            wq = [int(v) for v in quantised_weights(q_rows[u], lo, hi, temperature, top_k)]
+            Wq = sum(wq)
+            for c in ch[u]:
+                x = int(token[c])
+                u32 = uniform_u64(seed, step, u, trial) >> 32
+                trial += 1
+                if u32 * wq[x] * Wp < (wp[x] * Wq) << 32:
+                    accepted = c
+                    break
+                res = [max(0, wp[y] * Wq - wq[y] * Wp) for y in range(len(wp))]
+                shift = max(0, max(res).bit_length() - MSS_WEIGHT_BITS)
+                wp = [v >> shift for v in res]
+                Wp = sum(wp)
+                if Wp == 0:
+                    # p == q on the support: a rejection has probability zero; kept for safety
+                    return path, top1_id(logits[u], lo, hi, temperature)
+        if accepted is None:
+            r = draw_below(uniform_u64(seed, step, u, trial), Wp)
+            return path, inverse_cdf(np.asarray(wp, dtype=object), r)
         path.append(accepted)
         u = accepted

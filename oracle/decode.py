@@ -28,7 +28,7 @@ import numpy as np
 from synth import DecodeCfg
 from . import accept as acc
 from .attention import tree_key_slots
-from .expand import Tree, build_tree, expand
+from .expand import Tree, build_tree, expand, expand_sampled
 from .model import OracleModel
 from .numerics import draw_below, masked_logits, uniform_u64
 from .schedule import initial, schedule
@@ -103,6 +103,7 @@ class Decoder:
         self.poisson = poisson
         self.knn = knn
         self.accept_seed = cfg.seed if accept_seed is None else accept_seed
+        self.q_rows: Dict[int, np.ndarray] = {}   # stochastic children: tree index -> draft row of its children
 
     # the conditional (or only) branch's state
     @property
@@ -132,6 +133,9 @@ class Decoder:
         a = self.cfg.accept
         if a.mode == "greedy":
             return acc.accept_greedy(logit_rows, parent, token, allowed)
+        if a.mode == "mss":
+            return acc.accept_mss(logit_rows, self.q_rows, parent, token, allowed, temperature=a.temperature,
+                                  top_k=a.top_k, seed=self.accept_seed, step=step)
         return acc.accept_sampling(logit_rows, parent, token, allowed, temperature=a.temperature,
                                    top_k=a.top_k, seed=self.accept_seed, step=step, mode=a.mode,
                                    delta=a.delta, knn=self.knn, knn_k=a.knn_k)
@@ -212,8 +216,24 @@ class Decoder:
                 lgs.append(lg)
             return guide(lgs, self.guidance)
 
-        pool, sel = expand(root_logits, level_fn, d_hat, k_hat, self.cfg.sched.n_budget,
-                           lambda depth: self.allowed_pos(L + depth))
+        a = self.cfg.accept
+        allowed_at = lambda depth: self.allowed_pos(L + depth)
+        if a.mode == "mss":
+            # stochastic children: q of every expanded node is kept for the acceptance, keyed by
+            # the node's tree index (pool index + 1; the root is 0)
+            self.q_rows = {0: root_logits}
+
+            def sampled_level(frontier, pool):
+                rows = level_fn(frontier, pool)
+                for u, row in zip(frontier, rows):
+                    self.q_rows[u + 1] = row
+                return rows
+
+            pool, sel = expand_sampled(root_logits, sampled_level, d_hat, k_hat, a.children, self.cfg.sched.n_budget,
+                                       allowed_at, temperature=a.temperature, top_k=a.top_k, seed=self.accept_seed,
+                                       step=self.step_no)
+            return build_tree(self.tokens[-1], pool, sel, by_creation=True), root_logits
+        pool, sel = expand(root_logits, level_fn, d_hat, k_hat, self.cfg.sched.n_budget, allowed_at)
         return build_tree(self.tokens[-1], pool, sel), root_logits
 
     # ---------------------------------------------------------------- one cycle

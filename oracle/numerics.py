@@ -79,6 +79,13 @@ def uniform_u64(seed: int, step: int, node: int, trial: int) -> int:
     return (x[1] << 32) | x[0]
 
 
+def uniform_u64_tagged(seed: int, step: int, node: int, index: int, tag: int) -> int:
+    """64 random bits at key = seed, counter = (step, node, index, tag); tag 0 is the
+    acceptance draw above, tag 2 a drafted child (stochastic children)."""
+    x = philox4x32_10((step, node, index, tag), (seed & MASK32, (seed >> 32) & MASK32))
+    return (x[1] << 32) | x[0]
+
+
 def draw_below(u64: int, w_total: int) -> int:
     """Uniform integer in [0, w_total): the high 64 bits of the 128-bit product u64 * w_total."""
     return (int(u64) * int(w_total)) >> 64

@@ -17,7 +17,7 @@ E_ARG, E_SHAPE, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_STATE = -1, -2, -3, -4, -5, 
 F32, BF16 = 0, 1
 MAX_NODES = 128
 MASK_WORDS = 2
-ACCEPT_GREEDY, ACCEPT_EXACT, ACCEPT_RELAXED = 0, 1, 2
+ACCEPT_GREEDY, ACCEPT_EXACT, ACCEPT_RELAXED, ACCEPT_MSS = 0, 1, 2, 3
 PACK_STACK, PACK_GATE_UP, PACK_QKV = 0, 1, 2
 ALPHA_REAL, ALPHA_POISSON = 0, 1
 INIT_HORIZONTAL, INIT_VERTICAL, INIT_RANDOM, INIT_TOKENFLOCK = 0, 1, 2, 3
@@ -35,7 +35,8 @@ ip = C.POINTER(C.c_int32)
 
 class AcceptCfg(C.Structure):
     _fields_ = [("mode", i32), ("temperature", f32), ("top_k", i32), ("delta", f32), ("knn_k", i32),
-                ("knn_rows", i32), ("knn_stride", i32), ("knn", p), ("seed", u64)]
+                ("knn_rows", i32), ("knn_stride", i32), ("knn", p), ("seed", u64), ("children", i32),
+                ("q_logits", p), ("q_ld", i64), ("q_row", p), ("q_rows", i32)]
 
 
 class SchedCfg(C.Structure):
@@ -85,6 +86,7 @@ _SIGS = {
     "adt_codebook_knn_workspace_size": (sz, [i32]),
     "adt_codebook_knn": (i32, [p, i32, i32, i32, p, p, sz, p]),
     "adt_gemm_bf16": (i32, [p, i64, p, i64, i32, i32, i32, p, i64, p]),
+    "adt_gemm_bf16_packed": (i32, [p, i64, p, i32, i32, i32, p, i64, p]),
     "adt_packed_bytes": (sz, [i32, i32, i32]),
     "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, i32, p, p]),
     "adt_schedule_next": (i32, [C.POINTER(SchedCfg), i32, i32, i32, i32, i32, i32, i32, ip, ip]),

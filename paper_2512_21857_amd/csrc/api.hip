@@ -208,13 +208,16 @@ static adt_status accept_impl(const float* logits, int64_t ld, int V, const int3
     if (e) return e;
     return launch_accept_greedy(top_id, 1, parent, token, n_nodes, n_max, path, n_acc, bonus, st);
   }
+  if (cfg.mode == ADT_ACCEPT_MSS)
+    return launch_accept_mss(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg, step, path, n_acc, bonus, rest,
+                             accept_ws_bytes(V), st);
   return launch_accept_sample(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg, step, path, n_acc, bonus,
                               rest, accept_ws_bytes(V), st);
 }
 
 static adt_status check_accept_cfg(const adt_accept_cfg* cfg) {
   ADT_CHECK_ARG(cfg != nullptr, ADT_E_ARG, "accept: null cfg");
-  ADT_CHECK_ARG(cfg->mode >= ADT_ACCEPT_GREEDY && cfg->mode <= ADT_ACCEPT_RELAXED, ADT_E_ARG, "accept: mode %d",
+  ADT_CHECK_ARG(cfg->mode >= ADT_ACCEPT_GREEDY && cfg->mode <= ADT_ACCEPT_MSS, ADT_E_ARG, "accept: mode %d",
                 cfg->mode);
   if (cfg->mode != ADT_ACCEPT_GREEDY) {
     ADT_CHECK_ARG(cfg->temperature > 0.f && std::isfinite(cfg->temperature), ADT_E_ARG, "accept: temperature");
@@ -239,6 +242,8 @@ extern "C" adt_status adt_verify_accept(const float* logits, int64_t ld, int32_t
   ADT_CHECK_ARG(n_max >= 1 && n_max <= ADT_MAX_NODES, ADT_E_CAPACITY, "verify_accept: n_max %d", n_max);
   adt_status e = check_accept_cfg(cfg);
   if (e) return e;
+  ADT_CHECK_ARG(cfg->mode != ADT_ACCEPT_MSS || (cfg->q_logits && cfg->q_row && cfg->q_ld >= V && cfg->q_rows >= 1),
+                ADT_E_ARG, "verify_accept: MSS needs q_logits, q_row, q_ld >= V and q_rows >= 1");
   return accept_impl(logits, ld, V, parent, token, allowed, n_nodes, n_max, *cfg, step, path, n_acc, bonus, workspace,
                      workspace_bytes, (hipStream_t)stream);
 }
@@ -254,6 +259,11 @@ extern "C" adt_status adt_codebook_knn(const float* codebook, int32_t n, int32_t
 extern "C" adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw, int32_t M, int32_t N,
                                     int32_t K, float* C, int64_t ldc, void* stream) {
   return launch_gemm_nt(X, ldx, W, ldw, M, N, K, C, ldc, (hipStream_t)stream);
+}
+
+extern "C" adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K,
+                                           float* C, int64_t ldc, void* stream) {
+  return launch_gemm_nt(X, ldx, Wp, K, M, N, K, C, ldc, (hipStream_t)stream, nullptr, nullptr, true);
 }
 
 extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype) {
@@ -431,6 +441,7 @@ extern "C" void adt_model_destroy(adt_model* m) { delete m; }
 // ============================================================================ session
 struct TreeBufs {
   int32_t *parent, *token, *depth, *pos, *allowed_rows, *n, *path, *nacc, *bonus;
+  int32_t* qrow;   // draft-logit row that drew each node's children (stochastic children)
   float* score;
   uint64_t* mask;
 };
@@ -478,6 +489,7 @@ struct adt_session_s {
   size_t attn_ws_bytes;
   void* acc_ws;
   size_t acc_ws_bytes;
+  uint64_t* samp_w = nullptr;   // stochastic children: [KR][V] q weights of a level's rows
   // HIP graphs of the forwards, keyed by shape; captured on a private stream, replayed on
   // the caller's stream.
   bool graphs = true;
@@ -514,6 +526,7 @@ static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_sessi
   const int kw = d->sched.k_clamp == ADT_KCLAMP_DEEP ? ADT_MAX_WIDTH : kh;
   s->KR = std::max(kh, 1);
   s->C = std::max(kw, kh + (dh - 1) * kh * kh);
+  if (d->accept.mode == ADT_ACCEPT_MSS) s->C = std::max(s->C, R);   // every drawn child is kept
   // fp32 projections write [rows][N] products for the row kernels; bf16 ones finish in place
   size_t pe = 256;
   if (s->dt == ADT_F32)
@@ -554,12 +567,14 @@ static size_t session_layout(adt_session_s* s, char* base) {
   t.bonus = b.take<int32_t>(4);
   t.score = b.take<float>(R);
   t.mask = b.take<uint64_t>(2 * R);
+  t.qrow = b.take<int32_t>(R);
   s->allowed_img = b.take<int32_t>((size_t)2 * s->T);
   s->pool.token = b.take<int32_t>(s->C);
   s->pool.score = b.take<float>(s->C);
   s->pool.depth = b.take<int32_t>(s->C);
   s->pool.parent = b.take<int32_t>(s->C);
   s->pool.drow = b.take<int32_t>(s->C);
+  s->pool.qrow = b.take<int32_t>(s->C);
   s->pool.rmask = b.take<uint64_t>((size_t)2 * std::max(1, s->DR - s->C0));
   s->sel_rank = b.take<int32_t>(s->C);
   s->bfs_of = b.take<int32_t>(s->C);
@@ -585,6 +600,7 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->attn_ws = b.take<char>(std::max<size_t>(s->attn_ws_bytes, 256));
   s->acc_ws_bytes = adt_accept_workspace_size(s->V);
   s->acc_ws = b.take<char>(s->acc_ws_bytes);
+  if (s->d.accept.mode == ADT_ACCEPT_MSS) s->samp_w = b.take<uint64_t>((size_t)s->KR * s->V);
   return align_up(b.off, 256);
 }
 
@@ -611,7 +627,11 @@ static adt_status check_session_desc(const adt_model* m, const adt_session_desc*
     const int lo = d->allowed[2 * g], hi = d->allowed[2 * g + 1];
     ADT_CHECK_ARG(0 <= lo && lo < hi && hi <= m->d.vocab, ADT_E_ARG, "session: allowed range of cell %d", g);
   }
-  return check_accept_cfg(&d->accept);
+  TRY(check_accept_cfg(&d->accept));
+  ADT_CHECK_ARG(d->accept.mode != ADT_ACCEPT_MSS ||
+                    (d->accept.children >= 1 && d->accept.children <= 16 && d->accept.children <= c.n_budget),
+                ADT_E_ARG, "session: MSS children %d (in [1, 16] and <= n_budget)", d->accept.children);
+  return ADT_OK;
 }
 
 extern "C" size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* d) {
@@ -887,6 +907,17 @@ static adt_status set_root_only_tree(adt_session_s* s, int root_token, int L, hi
   return ADT_OK;
 }
 
+// The session's acceptance settings; stochastic children read q from the session's own draft
+// logit rows through the map its last expansion wrote.
+static adt_accept_cfg session_accept_cfg(const adt_session_s* s) {
+  adt_accept_cfg c = s->d.accept;
+  c.q_logits = s->dlogits;
+  c.q_ld = s->V;
+  c.q_row = s->tr.qrow;
+  c.q_rows = s->DLR;
+  return c;
+}
+
 extern "C" adt_status adt_session_prefill(adt_session* s, const int32_t* prefix, int32_t* first_token, void* stream) {
   ADT_CHECK_ARG(s && prefix, ADT_E_ARG, "prefill: null pointer");
   ADT_CHECK_ARG(!s->prefilled, ADT_E_STATE, "prefill: already prefilled");
@@ -921,7 +952,7 @@ extern "C" adt_status adt_session_prefill(adt_session* s, const int32_t* prefix,
   TRY(set_root_only_tree(s, prefix[P - 1], P - 1, st));
   // the root-only tree's successor is image cell 0
   TRY(launch_fill_pairs(s->tr.allowed_rows, 1, s->allowed_h[0], s->allowed_h[1], st));
-  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, 1, s->d.accept, 0,
+  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, 1, session_accept_cfg(s), 0,
                   s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
   int32_t first = 0;
   ADT_HIP(hipMemcpyAsync(&first, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
@@ -941,6 +972,59 @@ static void cell_range(const adt_session_s* s, int cell, int& lo, int& hi) {
   cell = std::max(0, std::min(s->T - 1, cell));
   lo = s->allowed_h[2 * cell];
   hi = s->allowed_h[2 * cell + 1];
+}
+
+// Stochastic children (the session's acceptance is ADT_ACCEPT_MSS): the root's draft row is in
+// dlogits row 0 and its allowed range in allowed_lvl[0].  Every expanded node draws ch children
+// from q; level lvl expands the best nf nodes of the previous layer (nf <= k_hat, whole
+// expansions within n_budget); the tree keeps every drawn child in creation order.
+static adt_status expand_sampled(adt_session_s* s, int d_hat, int k_hat, int n_budget, int cu, bool table,
+                                 int32_t* n_nodes_out, hipStream_t st) {
+  const adt_sched_cfg& c = s->d.sched;
+  const adt_accept_cfg& a = s->d.accept;
+  const int V = s->V, L = s->L, P = s->P, ch = a.children;
+  const uint32_t step = (uint32_t)s->step;
+  TRY(launch_row_sample(s->dlogits, V, V, s->allowed_lvl, 1, nullptr, ch, a.temperature, a.top_k, a.seed, step,
+                        s->samp_w, s->top_id, s->top_val, s->lse, 16, st));
+  int pool_n = ch;
+  int nf = d_hat > 1 ? std::min({k_hat, ch, (n_budget - pool_n) / ch}) : 0;
+  TRY(launch_expand_level(s->pool, nullptr, 1, ch, 0, 1, std::max(nf, 1), s->top_id, s->top_val, s->lse, 16,
+                          nf > 0 ? 1 : 0, L, 0, cu - 1, s->C0, 1, s->nx[0], st));
+  int drow = 0, cur = 0;
+  for (int lvl = 2; lvl <= d_hat && nf > 0; ++lvl) {
+    const int dl_row = 1 + (lvl - 2) * c.k_hi;
+    float* lrows = s->dlogits + (size_t)dl_row * V;
+    void* fout = (char*)s->dfeat + (size_t)s->nb * (s->C0 + drow) * s->dm * esize(s->dt);
+    if (table) {
+      TRY(launch_table_rows(s->nx[cur].tok, nf, lvl - 1, s->d.draft_table_rows, s->idx, st));
+      TRY(launch_gather_rows(s->d.draft_table, s->idx, nf, V, lrows, ADT_F32, st));
+    } else {
+      TRY(draft_forward(s, s->nx[cur].tok, s->nx[cur].fsrc, s->cfeat, nf, s->nx[cur].pos, L + 1 + drow, L + 1,
+                        drow + nf, s->nx[cur].mask, fout, 0, nf, lrows, s->draw ? s->draw + (size_t)s->nb * s->V : nullptr,
+                        st, gkey(3, lvl, nf, drow)));
+    }
+    int lo, hi;
+    cell_range(s, L + lvl - P, lo, hi);
+    TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
+    TRY(launch_row_sample(lrows, V, V, s->allowed_lvl, nf, s->nx[cur].frontier, ch, a.temperature, a.top_k, a.seed,
+                          step, s->samp_w, s->top_id, s->top_val, s->lse, 16, st));
+    const int made = nf * ch;
+    const int nf_next = lvl < d_hat ? std::min({k_hat, made, (n_budget - pool_n - made) / ch}) : 0;
+    TRY(launch_expand_level(s->pool, s->nx[cur].frontier, nf, ch, pool_n, lvl, std::max(nf_next, 1), s->top_id,
+                            s->top_val, s->lse, 16, nf_next > 0 ? 1 : 0, L, drow + nf, cu - 1, s->C0,
+                            1 + (lvl - 1) * c.k_hi, s->nx[cur ^ 1], st));
+    pool_n += made;
+    drow += nf;
+    nf = nf_next;
+    cur ^= 1;
+  }
+  TRY(launch_expand_finalize(s->pool, pool_n, pool_n, s->tokens[L], L, P, s->T, s->allowed_img, s->sel_rank,
+                             s->bfs_of, s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
+                             s->tr.allowed_rows, s->tr.qrow, s->tr.n, true, st));
+  s->n_nodes = pool_n + 1;
+  s->expanded = true;
+  if (n_nodes_out) *n_nodes_out = s->n_nodes;
+  return ADT_OK;
 }
 
 extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_hat, int32_t n_budget,
@@ -974,14 +1058,19 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
                       s->dlogits, s->draw, st, gkey(2, 0, 0, cu)));
   }
-  // layer 1: the root's top-k children
   int lo, hi;
   cell_range(s, L + 1 - P, lo, hi);
   TRY(launch_fill_pairs(s->allowed_lvl, 1, lo, hi, st));
+  if (s->d.accept.mode == ADT_ACCEPT_MSS) {
+    ADT_CHECK_ARG(n_budget >= s->d.accept.children, ADT_E_ARG, "tree_expand: n_budget %d below the %d children of one node",
+                  n_budget, s->d.accept.children);
+    return expand_sampled(s, d_hat, k_hat, n_budget, cu, table, n_nodes_out, st);
+  }
+  // layer 1: the root's top-k children
   TRY(launch_row_topk(s->dlogits, V, V, s->allowed_lvl, 1, k_hat, 16, s->top_id, s->top_val, s->lse, st));
   int cnt = std::min(k_hat, hi - lo);
   TRY(launch_expand_level(s->pool, nullptr, 1, cnt, 0, 1, k_hat, s->top_id, s->top_val, s->lse, 16, d_hat > 1 ? 1 : 0,
-                          L, 0, cu - 1, s->C0, s->nx[0], st));
+                          L, 0, cu - 1, s->C0, 1, s->nx[0], st));
   int pool_n = cnt, nf = std::min(k_hat, cnt), drow = 0, cur = 0;
   for (int lvl = 2; lvl <= d_hat; ++lvl) {
     const int dl_row = 1 + (lvl - 2) * c.k_hi;
@@ -1000,7 +1089,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, st));
     cnt = std::min(k_hat, hi - lo);
     TRY(launch_expand_level(s->pool, s->nx[cur].frontier, nf, cnt, pool_n, lvl, k_hat, s->top_id, s->top_val, s->lse,
-                            16, lvl < d_hat ? 1 : 0, L, drow + nf, cu - 1, s->C0, s->nx[cur ^ 1], st));
+                            16, lvl < d_hat ? 1 : 0, L, drow + nf, cu - 1, s->C0, 1 + (lvl - 1) * c.k_hi,
+                            s->nx[cur ^ 1], st));
     pool_n += nf * cnt;
     drow += nf;
     nf = std::min(k_hat, nf * cnt);
@@ -1008,7 +1098,7 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   }
   TRY(launch_expand_finalize(s->pool, pool_n, n_budget, s->tokens[L], L, P, s->T, s->allowed_img, s->sel_rank,
                              s->bfs_of, s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
-                             s->tr.allowed_rows, s->tr.n, st));
+                             s->tr.allowed_rows, s->tr.qrow, s->tr.n, false, st));
   s->n_nodes = std::min(n_budget, pool_n) + 1;
   s->expanded = true;
   if (n_nodes_out) *n_nodes_out = s->n_nodes;
@@ -1021,6 +1111,9 @@ extern "C" adt_status adt_session_set_tree(adt_session* s, const int32_t* parent
   ADT_CHECK_ARG(s->prefilled, ADT_E_STATE, "set_tree: session not prefilled");
   ADT_CHECK_ARG(n >= 1 && n <= R / s->nb, ADT_E_CAPACITY, "set_tree: n %d (at most %d)", n, R / s->nb);
   ADT_CHECK_ARG(parent[0] == -1, ADT_E_ARG, "set_tree: node 0 must be the root");
+  ADT_CHECK_ARG(s->d.accept.mode != ADT_ACCEPT_MSS, ADT_E_UNSUPPORTED,
+                "set_tree: stochastic-children sessions verify their own expansions (the q rows of a given tree "
+                "are unknown); use adt_verify_accept with q rows");
   std::vector<int> dep(n, 0);
   for (int i = 1; i < n; ++i) {
     ADT_CHECK_ARG(parent[i] >= 0 && parent[i] < i, ADT_E_ARG, "set_tree: parent[%d]=%d not BFS ordered", i, parent[i]);
@@ -1062,7 +1155,7 @@ extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, i
   ADT_CHECK_ARG(s->prefilled && s->n_nodes >= 1, ADT_E_STATE, "accept_commit: no verified tree");
   hipStream_t st = (hipStream_t)stream;
   const int n = s->n_nodes, L = s->L, P = s->P;
-  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, s->d.accept,
+  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, session_accept_cfg(s),
                   (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
   std::vector<int32_t> path(R), tok(R);
   int32_t a = 0, bonus = 0;

@@ -20,12 +20,18 @@ namespace adt {
 constexpr int AS_THREADS = 1024;
 constexpr int AS_DELTA_BITS = 16;
 
+// 64 random bits at key = seed, counter = (step, node, index, tag): words (x1 << 32 | x0).
+// tag 0: acceptance draws; tag 2: drafted children (stochastic children).
+__device__ __forceinline__ uint64_t philox_u64(uint64_t seed, uint32_t step, uint32_t node, uint32_t index,
+                                               uint32_t tag) {
+  uint32_t c[4] = {step, node, index, tag};
+  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
+  return ((uint64_t)c[1] << 32) | c[0];
+}
+
 __device__ __forceinline__ uint64_t draw_below(uint64_t seed, uint32_t step, uint32_t node, uint32_t trial,
                                                uint64_t W) {
-  uint32_t c[4] = {step, node, trial, 0u};
-  philox4x32_10(c, (uint32_t)seed, (uint32_t)(seed >> 32));
-  const uint64_t U = ((uint64_t)c[1] << 32) | c[0];
-  return __umul64hi(U, W);
+  return __umul64hi(philox_u64(seed, step, node, trial, 0u), W);
 }
 
 // Order-preserving 64-bit key: larger z first, then lower id first.
@@ -103,6 +109,110 @@ __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T,
   return prefix;
 }
 
+// Integer weights w[i] = rint(exp(z_i - max z) * 2^32), z = x[i] / T, over the top_k ids of
+// [lo, hi) by (z desc, id asc) (all of them when top_k is 0 or covers the range), zero
+// elsewhere in [0, V); returns their total.  Every thread must call it.
+__device__ uint64_t build_weights(const float* x, int lo, int hi, int V, float T, int top_k, uint64_t* w,
+                                  SampleShared& sh) {
+  const int tid = threadIdx.x;
+  const int cnt = hi - lo;
+  uint64_t thr = 0;
+  if (top_k > 0 && top_k < cnt) thr = radix_select(x, lo, hi, top_k, T, sh);
+  float zm = -INFINITY;
+  for (int i = lo + tid; i < hi; i += AS_THREADS) {
+    const float z = x[i] / T;
+    if (zkey(z, i) >= thr) zm = fmaxf(zm, z);
+  }
+  zm = block_max_f32(zm, sh);
+  uint64_t part = 0;
+  for (int i = tid; i < V; i += AS_THREADS) {
+    uint64_t wi = 0;
+    if (i >= lo && i < hi) {
+      const float z = x[i] / T;
+      if (zkey(z, i) >= thr) {
+        const float e = expf(z - zm);
+        wi = (uint64_t)rint((double)e * 4294967296.0);
+      }
+    }
+    w[i] = wi;
+    part += wi;
+  }
+  const uint64_t total = block_sum_u64(part, sh);
+  __threadfence_block();
+  __syncthreads();
+  return total;
+}
+
+// The top-1 id of softmax(x / T) over [lo, hi): largest z, lowest id.  Every thread calls it.
+__device__ int block_top1(const float* x, int lo, int hi, float T, SampleShared& sh) {
+  const int tid = threadIdx.x;
+  float bz = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int i = lo + tid; i < hi; i += AS_THREADS) {
+    const float z = x[i] / T;
+    if (z > bz || (z == bz && i < bi)) {
+      bz = z;
+      bi = i;
+    }
+  }
+  sh.scan[tid] = ((uint64_t)__float_as_uint(bz) << 32) | (uint32_t)bi;
+  __syncthreads();
+  if (tid == 0) {
+    float best = -INFINITY;
+    int bid = lo;
+    for (int t = 0; t < AS_THREADS; ++t) {
+      const float z = __uint_as_float((uint32_t)(sh.scan[t] >> 32));
+      const int id = (int)(uint32_t)sh.scan[t];
+      if (id == 0x7FFFFFFF) continue;
+      if (z > best || (z == best && id < bid)) {
+        best = z;
+        bid = id;
+      }
+    }
+    sh.bonus = bid;
+  }
+  __syncthreads();
+  const int r = sh.bonus;
+  __syncthreads();
+  return r;
+}
+
+// Per-thread chunks of [lo, hi) for inverse-CDF lookups: thread t owns ids [b0, b1) and
+// sh.scan[t] = the total weight of the ids before its chunk.  Every thread calls it.
+__device__ void chunk_scan(const uint64_t* w, int lo, int hi, int& b0, int& b1, uint64_t& own, SampleShared& sh) {
+  const int tid = threadIdx.x;
+  const int per = (hi - lo + AS_THREADS - 1) / AS_THREADS;
+  b0 = lo + tid * per;
+  b1 = min(hi, b0 + per);
+  uint64_t s = 0;
+  for (int i = b0; i < b1; ++i) s += w[i];
+  own = s;
+  sh.scan[tid] = s;
+  __syncthreads();
+  if (tid == 0) {   // exclusive scan of the per-thread sums
+    uint64_t run = 0;
+    for (int t = 0; t < AS_THREADS; ++t) {
+      const uint64_t v = sh.scan[t];
+      sh.scan[t] = run;
+      run += v;
+    }
+  }
+  __syncthreads();
+}
+
+// Smallest id with prefix weight > r, if it lies in this thread's chunk (else -1).
+__device__ __forceinline__ int chunk_find(const uint64_t* w, int b0, int b1, uint64_t own, uint64_t r,
+                                          const SampleShared& sh) {
+  uint64_t run = sh.scan[threadIdx.x];
+  if (b0 < b1 && run <= r && r < run + own) {
+    for (int i = b0; i < b1; ++i) {
+      run += w[i];
+      if (run > r) return i;
+    }
+  }
+  return -1;
+}
+
 __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const float* __restrict__ logits, int64_t ld, int V, const int32_t* __restrict__ parent,
     const int32_t* __restrict__ token, const int32_t* __restrict__ allowed, const int32_t* __restrict__ n_nodes,
@@ -124,33 +234,7 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const int u = sh.node;
     const int lo = max(0, min(allowed[u * 2], V)), hi = max(lo, min(allowed[u * 2 + 1], V));
     const float* x = logits + (int64_t)u * ld;
-    const int cnt = hi - lo;
-    // --- top-k threshold over (z desc, id asc)
-    uint64_t thr = 0;
-    if (top_k > 0 && top_k < cnt) thr = radix_select(x, lo, hi, top_k, T, sh);
-    // --- max z of the kept set, weights, total
-    float zm = -INFINITY;
-    for (int i = lo + tid; i < hi; i += AS_THREADS) {
-      const float z = x[i] / T;
-      if (zkey(z, i) >= thr) zm = fmaxf(zm, z);
-    }
-    zm = block_max_f32(zm, sh);
-    uint64_t part = 0;
-    for (int i = tid; i < V; i += AS_THREADS) {
-      uint64_t wi = 0;
-      if (i >= lo && i < hi) {
-        const float z = x[i] / T;
-        if (zkey(z, i) >= thr) {
-          const float e = expf(z - zm);
-          wi = (uint64_t)rint((double)e * 4294967296.0);
-        }
-      }
-      w[i] = wi;
-      part += wi;
-    }
-    const uint64_t total = block_sum_u64(part, sh);
-    __threadfence_block();
-    __syncthreads();
+    const uint64_t total = build_weights(x, lo, hi, V, T, top_k, w, sh);
     // --- sibling walk (one lane; w lives in global memory and is only touched by this lane)
     if (tid == 0) {
       uint64_t W = total;
@@ -208,60 +292,17 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const uint64_t W = sh.total;
     if (W == 0) {
       // residual empty: the top-1 id of p (largest z, lowest id)
-      float bz = -INFINITY;
-      int bi = 0x7FFFFFFF;
-      for (int i = lo + tid; i < hi; i += AS_THREADS) {
-        const float z = x[i] / T;
-        if (z > bz || (z == bz && i < bi)) {
-          bz = z;
-          bi = i;
-        }
-      }
-      sh.scan[tid] = ((uint64_t)__float_as_uint(bz) << 32) | (uint32_t)bi;
-      __syncthreads();
-      if (tid == 0) {
-        float best = -INFINITY;
-        int bid = lo;
-        for (int t = 0; t < AS_THREADS; ++t) {
-          const float z = __uint_as_float((uint32_t)(sh.scan[t] >> 32));
-          const int id = (int)(uint32_t)sh.scan[t];
-          if (id == 0x7FFFFFFF) continue;
-          if (z > best || (z == best && id < bid)) {
-            best = z;
-            bid = id;
-          }
-        }
-        sh.bonus = bid;
-      }
+      const int b = block_top1(x, lo, hi, T, sh);
+      if (tid == 0) sh.bonus = b;
       __syncthreads();
       break;
     }
     const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)sh.trial, W);
-    const int per = (cnt + AS_THREADS - 1) / AS_THREADS;
-    const int b0 = lo + tid * per, b1 = min(hi, b0 + per);
-    uint64_t s = 0;
-    for (int i = b0; i < b1; ++i) s += w[i];
-    sh.scan[tid] = s;
-    __syncthreads();
-    if (tid == 0) {   // exclusive scan of the per-thread sums
-      uint64_t run = 0;
-      for (int t = 0; t < AS_THREADS; ++t) {
-        const uint64_t v = sh.scan[t];
-        sh.scan[t] = run;
-        run += v;
-      }
-    }
-    __syncthreads();
-    uint64_t run = sh.scan[tid];
-    if (b0 < b1 && run <= r && r < run + s) {
-      for (int i = b0; i < b1; ++i) {
-        run += w[i];
-        if (run > r) {
-          sh.bonus = i;
-          break;
-        }
-      }
-    }
+    int b0, b1;
+    uint64_t own;
+    chunk_scan(w, lo, hi, b0, b1, own, sh);
+    const int f = chunk_find(w, b0, b1, own, r, sh);
+    if (f >= 0) sh.bonus = f;
     __syncthreads();
     break;
   }
@@ -271,7 +312,207 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
   }
 }
 
-size_t accept_ws_bytes(int V) { return (size_t)V * 8 + 4096; }
+__device__ float block_sum_f32(float v, SampleShared& sh) {
+  v = wave_sum(v);
+  __syncthreads();
+  if (threadIdx.x % WAVE == 0) sh.f32[threadIdx.x / WAVE] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < AS_THREADS / WAVE; ++i) s += sh.f32[i];
+  __syncthreads();
+  return s;
+}
+
+__device__ int block_max_i32(int v, SampleShared& sh) {
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, WAVE));
+  __syncthreads();
+  if (threadIdx.x % WAVE == 0) sh.u64[threadIdx.x / WAVE] = (uint64_t)(uint32_t)v;
+  __syncthreads();
+  int m = 0;
+  for (int i = 0; i < AS_THREADS / WAVE; ++i) m = max(m, (int)(uint32_t)sh.u64[i]);
+  __syncthreads();
+  return m;
+}
+
+__device__ __forceinline__ int bitlen128(unsigned __int128 v) {
+  const uint64_t hi = (uint64_t)(v >> 64), lo = (uint64_t)v;
+  return hi ? 128 - __clzll(hi) : (lo ? 64 - __clzll(lo) : 0);
+}
+
+// ---------------------------------------------------------------------------- stochastic children
+// One workgroup per frontier row: q's integer weights (as p's above), the log-sum-exp of the
+// row at T = 1 over its allowed ids (the confidences that rank the frontier), then cnt draws
+// r_j = floor(U_j W / 2^64), U_j at counter (step, parent tree index, j, 2), each resolved to
+// the smallest id with prefix weight > r_j.
+__global__ __launch_bounds__(AS_THREADS) void row_sample_kernel(const float* __restrict__ logits, int64_t ld, int V,
+                                                                const int32_t* __restrict__ allowed,
+                                                                const int32_t* __restrict__ front, int cnt, float T,
+                                                                int top_k, uint64_t seed, uint32_t step,
+                                                                uint64_t* __restrict__ wbuf, int32_t* __restrict__ top_id,
+                                                                float* __restrict__ top_val, float* __restrict__ lse,
+                                                                int kmax) {
+  __shared__ SampleShared sh;
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const float* x = logits + (int64_t)r * ld;
+  uint64_t* w = wbuf + (int64_t)r * V;
+  const int lo = max(0, min(allowed[2 * r], V)), hi = max(lo, min(allowed[2 * r + 1], V));
+  const uint64_t W = build_weights(x, lo, hi, V, T, top_k, w, sh);
+  float m1 = -INFINITY;
+  for (int i = lo + tid; i < hi; i += AS_THREADS) m1 = fmaxf(m1, x[i]);
+  m1 = block_max_f32(m1, sh);
+  float e1 = 0.f;
+  for (int i = lo + tid; i < hi; i += AS_THREADS) e1 += expf(x[i] - m1);
+  e1 = block_sum_f32(e1, sh);
+  int b0, b1;
+  uint64_t own;
+  chunk_scan(w, lo, hi, b0, b1, own, sh);
+  const uint32_t node = front ? (uint32_t)(front[r] + 1) : 0u;
+  for (int j = 0; j < cnt; ++j) {
+    const uint64_t rj = __umul64hi(philox_u64(seed, step, node, (uint32_t)j, 2u), W);
+    const int id = chunk_find(w, b0, b1, own, rj, sh);
+    if (id >= 0) {
+      top_id[r * kmax + j] = id;
+      top_val[r * kmax + j] = x[id];
+    }
+  }
+  if (tid == 0) lse[r] = m1 + logf(e1);
+}
+
+adt_status launch_row_sample(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows,
+                             const int32_t* front, int cnt, float T, int top_k, uint64_t seed, uint32_t step,
+                             uint64_t* w, int32_t* top_id, float* top_val, float* lse, int kmax, hipStream_t st) {
+  ADT_CHECK_ARG(rows >= 1 && cnt >= 1 && cnt <= kmax, ADT_E_ARG, "row_sample: rows %d cnt %d", rows, cnt);
+  row_sample_kernel<<<rows, AS_THREADS, 0, st>>>(logits, ld, V, allowed, front, cnt, T, top_k, seed, step, w, top_id,
+                                                 top_val, lse, kmax);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+// ---------------------------------------------------------------------------- literal Eq. 1
+// Multi-step acceptance for children drawn i.i.d. from q: at node u the children are tried in
+// node order; child x is accepted iff u32 * q_w(x) * W_p < 2^32 * p_w(x) * W_q (u32 = the high
+// half of the draw at counter (step, u, trial, 0)), i.e. with probability min(1, p(x) / q(x));
+// after a rejection p_w(y) <- max(0, p_w(y) W_q - q_w(y) W_p) >> s, s the least shift leaving
+// every weight below 2^32 (products in 128 bits); with all rejected the bonus is drawn from
+// the residual, at a leaf from p.  q_w: the weights of draft-logit row q_row[u].
+__global__ __launch_bounds__(AS_THREADS) void accept_mss_kernel(
+    const float* __restrict__ logits, int64_t ld, int V, const int32_t* __restrict__ parent,
+    const int32_t* __restrict__ token, const int32_t* __restrict__ allowed, const int32_t* __restrict__ n_nodes,
+    int n_max, float T, int top_k, const float* __restrict__ q_logits, int64_t q_ld, const int32_t* __restrict__ q_row,
+    int q_rows, uint64_t seed, uint32_t step, uint64_t* __restrict__ w, uint64_t* __restrict__ wq, int32_t* __restrict__ path,
+    int32_t* __restrict__ n_acc, int32_t* __restrict__ bonus) {
+  __shared__ SampleShared sh;
+  const int tid = threadIdx.x;
+  const int n = min(*n_nodes, n_max);
+  if (tid == 0) {
+    sh.node = 0;
+    sh.a = 0;
+    sh.bonus = 0;
+    path[0] = 0;
+  }
+  __syncthreads();
+  for (int guard = 0; guard < ADT_MAX_NODES; ++guard) {
+    const int u = sh.node;
+    const int lo = max(0, min(allowed[u * 2], V)), hi = max(lo, min(allowed[u * 2 + 1], V));
+    const float* x = logits + (int64_t)u * ld;
+    uint64_t Wp = build_weights(x, lo, hi, V, T, top_k, w, sh);
+    int first = -1;
+    for (int c = u + 1; c < n; ++c)
+      if (parent[c] == u) {
+        first = c;
+        break;
+      }
+    const int qr = first >= 0 ? q_row[u] : -1;
+    int trial = 0, accepted = -1;
+    bool empty = false;
+    if (qr >= 0 && qr < q_rows) {   // a node without a valid q row ends the walk (bonus from p)
+      const uint64_t Wq = build_weights(q_logits + (int64_t)qr * q_ld, lo, hi, V, T, top_k, wq, sh);
+      for (int c = first; c < n; ++c) {
+        if (parent[c] != u) continue;
+        const int xt = min(max(token[c], 0), V - 1);
+        if (tid == 0) {
+          const uint32_t u32 = (uint32_t)(philox_u64(seed, step, (uint32_t)u, (uint32_t)trial, 0u) >> 32);
+          const unsigned __int128 lhs = (unsigned __int128)((uint64_t)u32 * wq[xt]) * Wp;
+          const unsigned __int128 rhs = ((unsigned __int128)w[xt] * Wq) << 32;
+          sh.accepted = lhs < rhs ? 1 : 0;
+        }
+        __syncthreads();
+        ++trial;
+        const int acc = sh.accepted;
+        __syncthreads();
+        if (acc) {
+          accepted = c;
+          break;
+        }
+        int bl = 0;
+        for (int y = lo + tid; y < hi; y += AS_THREADS) {
+          const unsigned __int128 a = (unsigned __int128)w[y] * Wq, b = (unsigned __int128)wq[y] * Wp;
+          if (a > b) bl = max(bl, bitlen128(a - b));
+        }
+        bl = block_max_i32(bl, sh);
+        const int shift = max(0, bl - 32);
+        uint64_t part = 0;
+        for (int y = lo + tid; y < hi; y += AS_THREADS) {
+          const unsigned __int128 a = (unsigned __int128)w[y] * Wq, b = (unsigned __int128)wq[y] * Wp;
+          const uint64_t v = a > b ? (uint64_t)((a - b) >> shift) : 0;
+          w[y] = v;
+          part += v;
+        }
+        Wp = block_sum_u64(part, sh);
+        __threadfence_block();
+        __syncthreads();
+        if (Wp == 0) {   // p == q on the support: a rejection has probability zero; kept for safety
+          empty = true;
+          break;
+        }
+      }
+    }
+    if (accepted >= 0) {
+      if (tid == 0) {
+        sh.a += 1;
+        path[sh.a] = accepted;
+        sh.node = accepted;
+      }
+      __syncthreads();
+      continue;
+    }
+    if (empty) {
+      const int b = block_top1(x, lo, hi, T, sh);
+      if (tid == 0) sh.bonus = b;
+      __syncthreads();
+      break;
+    }
+    const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)trial, Wp);
+    int b0, b1;
+    uint64_t own;
+    chunk_scan(w, lo, hi, b0, b1, own, sh);
+    const int f = chunk_find(w, b0, b1, own, r, sh);
+    if (f >= 0) sh.bonus = f;
+    __syncthreads();
+    break;
+  }
+  if (tid == 0) {
+    *n_acc = sh.a;
+    *bonus = sh.bonus;
+  }
+}
+
+size_t accept_ws_bytes(int V) { return (size_t)V * 16 + 4096; }
+
+adt_status launch_accept_mss(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
+                             const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
+                             uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
+                             hipStream_t st) {
+  ADT_CHECK_ARG(ws_bytes >= (size_t)V * 16, ADT_E_CAPACITY, "accept_mss: workspace");
+  ADT_CHECK_ARG(cfg.q_logits && cfg.q_row && cfg.q_ld >= V && cfg.q_rows >= 1, ADT_E_ARG, "accept_mss: q rows");
+  uint64_t* w = (uint64_t*)ws;
+  accept_mss_kernel<<<1, AS_THREADS, 0, st>>>(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg.temperature,
+                                              cfg.top_k, cfg.q_logits, cfg.q_ld, cfg.q_row, cfg.q_rows, cfg.seed,
+                                              (uint32_t)step,
+                                              w, w + V, path, n_acc, bonus);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
 
 adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
                                 const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,

@@ -127,6 +127,138 @@ __global__ __launch_bounds__(NT_THREADS) void gemm_nt_kernel(const uint16_t* __r
     }
 }
 
+// ---------------------------------------------------------------------------------------------
+// Packed weights with many tiles: the operands reach LDS by direct global->LDS DMA
+// (global_load_lds_dwordx4: a wave instruction moves 1 KB, lane l's 16 bytes landing at byte
+// 16 l), so no registers stage them and no wave spends issue slots storing them.  A workgroup
+// of eight waves owns a 256 x 256 block of C^T; K advances in 32-wide stages held in a ring of
+// NSTAGE slots of 32 KB, each slot 32 tiles of 1 KB in the packed order (16 rows x 32 columns,
+// lane l = 16 g + i holding row i, columns 8g..8g+7): tiles 0-15 the block's W rows, 16-31 its
+// X rows.  A packed W tile is copied as stored (1 KB contiguous); an X tile is gathered from
+// row-major rows (16 rows x 64 bytes).  The MFMA operand reads of a 16-lane group then cover
+// 256 contiguous bytes (no bank conflicts, no padding).
+// Pipeline, per stage kt: the fragments of the stage's second half are read while the first
+// half's eight MFMAs run; each wave waits for its own DMA of stage kt+1 (the NSTAGE-3 newer
+// stages stay in flight) and one barrier publishes it; the DMA of stage kt+NSTAGE-1 then
+// refills the slot of stage kt-1, whose fragments every wave consumed before that barrier;
+// the next stage's first fragments are read while the second half's MFMAs run.  The DMA and
+// the waits are inline assembly because the compiler, which cannot tell LDS slots apart,
+// would otherwise wait for every DMA in flight before each LDS read.
+constexpr int DMA_THREADS = 512, DMA_TILES = 32, DMA_SLOT = DMA_TILES * 1024, DMA_NSTAGE = 5;
+
+// M0 is written with s_mov only: an SCC-writing instruction here would corrupt a compare the
+// compiler keeps live across the statement.
+#define ADT_DMA4(g0, g1, g2, g3, d)                                                                         \
+  asm volatile("s_mov_b32 m0, %4\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off\n\t"                          \
+               "s_mov_b32 m0, %5\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off\n\t"                          \
+               "s_mov_b32 m0, %6\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, off\n\t"                          \
+               "s_mov_b32 m0, %7\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %3, off" ::"v"(g0),                      \
+               "v"(g1), "v"(g2), "v"(g3), "s"(d), "s"((d) + 1024), "s"((d) + 2048), "s"((d) + 3072)          \
+               : "memory", "m0")
+
+template <int NSTAGE>
+__global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t* __restrict__ X, int64_t ldx,
+                                                                  const uint16_t* __restrict__ W, int M, int K,
+                                                                  float* __restrict__ C, int64_t ldc) {
+  static_assert(NSTAGE == 4 || NSTAGE == 5, "the wait counts below assume four or five slots");
+  constexpr int D = NSTAGE - 1;   // stages in flight ahead of the one being multiplied
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[NSTAGE * DMA_SLOT / 2];
+  // XCD-aware order: workgroup b runs on XCD b % 8; each XCD takes a contiguous range of
+  // tiles (row blocks fastest), so the row blocks that share a W block meet in one L2
+  const int MT = (M + 255) / 256, G = gridDim.x;
+  const int b = blockIdx.x, xcd = b % 8, q = G / 8, r = G % 8;
+  const int t = xcd * q + min(xcd, r) + b / 8;
+  const int m0 = (t % MT) * 256, n0 = (t / MT) * 256;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / WAVE), lane = tid % WAVE;
+  const int wn = wave / 4, wm = wave % 4;
+
+  // DMA sources: wave w fills tiles 4w..4w+3 of every stage (W tiles for w < 4, X tiles after)
+  const uint16_t* src[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int T = 4 * wave + i;
+    if (wave < 4) {
+      src[i] = W + ((int64_t)(n0 / 16 + T) * (K / 32)) * 512 + lane * 8;
+    } else {
+      const int m = min(m0 + 16 * (T - 16) + lane % 16, M - 1);   // rows past M feed discarded columns
+      src[i] = X + (int64_t)m * ldx + 8 * (lane / 16);
+    }
+  }
+  const int64_t step = wave < 4 ? 512 : 32;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)lds;
+  const uint32_t wdst = lds0 + 4 * wave * 1024;
+  const int KT = K / 32;
+  auto issue = [&](int kt) {   // past the last stage: the last stage again, into a slot never read
+    const int64_t ks = min(kt, KT - 1) * step;
+    const uint32_t d = wdst + (kt % NSTAGE) * DMA_SLOT;
+    ADT_DMA4(src[0] + ks, src[1] + ks, src[2] + ks, src[3] + ks, d);
+  };
+  // fragment offsets (bytes) inside a slot: A = W rows wn*128 + 32 nb + lane%32, B = X rows
+  // wm*64 + 32 mb + lane%32, columns 16 s + 8 (lane/32) of the stage
+  const int sub = ((lane / 32) * 16 + lane % 16) * 16;
+  const int aoff = (wn * 8 + (lane % 32) / 16) * 1024 + sub;
+  const int boff = (16 + wm * 4 + (lane % 32) / 16) * 1024 + sub;
+  const char* lbase = (const char*)lds;
+  auto frags = [&](int kt, int s, bf16x8* a, bf16x8* bb) {
+    const char* p = lbase + (kt % NSTAGE) * DMA_SLOT + s * 512;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) a[nb] = *reinterpret_cast<const bf16x8*>(p + aoff + nb * 2048);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) bb[mb] = *reinterpret_cast<const bf16x8*>(p + boff + mb * 2048);
+  };
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
+  auto mma = [&](const bf16x8* a, const bf16x8* bb) {
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], bb[mb], acc[nb][mb], 0, 0, 0);
+  };
+
+#pragma unroll
+  for (int s = 0; s < D; ++s) issue(s);
+  if constexpr (D == 3) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
+  bf16x8 a0[4], b0[2], a1[4], b1[2];
+  frags(0, 0, a0, b0);
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the loop starts with no LDS read pending
+  for (int kt = 0; kt < KT; ++kt) {
+    frags(kt, 1, a1, b1);
+    mma(a0, b0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);   // the six reads first, then the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    if constexpr (D == 3) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
+    issue(kt + D);
+    frags(kt + 1, 0, a0, b0);   // past the last stage: a stale slot, never used
+    mma(a1, b1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+  }
+  // no DMA may still be writing this workgroup's LDS when it exits
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  const int l32 = lane % 32, hi = lane / 32;
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int m = m0 + wm * 64 + mb * 32 + l32;
+      if (m >= M) continue;
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const int n = n0 + wn * 128 + nb * 32 + 8 * grp + 4 * hi;
+        *reinterpret_cast<f32x4*>(C + (int64_t)m * ldc + n) =
+            f32x4{acc[nb][mb][4 * grp], acc[nb][mb][4 * grp + 1], acc[nb][mb][4 * grp + 2], acc[nb][mb][4 * grp + 3]};
+      }
+    }
+}
+#undef ADT_DMA4
+
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
                           int64_t ldc, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, bool packed) {
   ADT_CHECK_ARG(X && W && C, ADT_E_ARG, "gemm_nt: null pointer");
@@ -140,6 +272,14 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
   const int best = (N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 256) ? 0 : 2;
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)W;
+  // Packed weights in 256 x 256 blocks when that still gives at least 128 workgroups (half
+  // the CUs; measured faster than the 128 x 128 blocks down to there): the DMA pipeline.
+  if (packed && N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 128) {
+    hipExtLaunchKernelGGL(gemm_nt_dma_kernel<DMA_NSTAGE>, dim3((M + 255) / 256 * (N / 256)), dim3(DMA_THREADS), 0, st,
+                          ev0, ev1, 0, x, ldx, w, M, K, C, ldc);
+    ADT_LAUNCH_CHECK();
+    return ADT_OK;
+  }
 #define ADT_NT(BNV, BMV, PK)                                                                                    \
   hipExtLaunchKernelGGL(gemm_nt_kernel<BNV, BMV, PK>, dim3((M + BMV - 1) / BMV, N / BNV), dim3(NT_THREADS), 0, st, \
                         ev0, ev1, 0, x, ldx, w, ldw, M, K, C, ldc)

@@ -157,7 +157,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __r
 __global__ __launch_bounds__(SEL_THREADS) void expand_level_kernel(
     Pool pool, const int32_t* __restrict__ front, int nf, int cnt, int base, int depth, int k_hat,
     const int32_t* __restrict__ top_id, const float* __restrict__ top_val, const float* __restrict__ lse, int kmax,
-    int make_next, int L, int drow_base, int root_frow, int tree_frow0, NextRows nx) {
+    int make_next, int L, int drow_base, int root_frow, int tree_frow0, int qrow_base, NextRows nx) {
   const int C = nf * cnt;
   const int tid = threadIdx.x;
   for (int i = tid; i < C; i += SEL_THREADS) {
@@ -170,6 +170,7 @@ __global__ __launch_bounds__(SEL_THREADS) void expand_level_kernel(
     pool.depth[idx] = depth;
     pool.parent[idx] = par;
     pool.drow[idx] = -1;
+    pool.qrow[idx] = -1;
   }
   __syncthreads();
   __threadfence_block();
@@ -187,6 +188,7 @@ __global__ __launch_bounds__(SEL_THREADS) void expand_level_kernel(
       const int par = pool.parent[ci];
       const int jrow = drow_base + rank;
       pool.drow[ci] = jrow;
+      pool.qrow[ci] = qrow_base + rank;
       nx.frontier[rank] = ci;
       nx.tok[rank] = pool.token[ci];
       nx.pos[rank] = L + depth;
@@ -215,10 +217,12 @@ __global__ __launch_bounds__(SEL_THREADS) void expand_finalize_kernel(
     Pool pool, int C, int n_budget, int root_token, int L, int P, int n_image, const int32_t* __restrict__ allowed_img,
     int32_t* __restrict__ sel_rank, int32_t* __restrict__ bfs_of, int32_t* __restrict__ parent,
     int32_t* __restrict__ token, int32_t* __restrict__ depth, float* __restrict__ score, int32_t* __restrict__ pos,
-    uint64_t* __restrict__ mask, int32_t* __restrict__ allowed_rows, int32_t* __restrict__ n_out) {
+    uint64_t* __restrict__ mask, int32_t* __restrict__ allowed_rows, int32_t* __restrict__ qrow,
+    int32_t* __restrict__ n_out, int keep_all) {
   const int tid = threadIdx.x;
-  const int N = min(n_budget, C);
-  for (int i = tid; i < C; i += SEL_THREADS) {
+  const int N = keep_all ? C : min(n_budget, C);
+  for (int i = tid; i < C && keep_all; i += SEL_THREADS) bfs_of[i] = i + 1;   // creation order is BFS
+  for (int i = tid; i < C && !keep_all; i += SEL_THREADS) {
     const float si = pool.score[i];
     const int di = pool.depth[i];
     int rank = 0;
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(SEL_THREADS) void expand_finalize_kernel(
     sel_rank[i] = rank;
   }
   __syncthreads();
-  for (int i = tid; i < C; i += SEL_THREADS) {
+  for (int i = tid; i < C && !keep_all; i += SEL_THREADS) {
     int b = -1;
     if (sel_rank[i] < N) {
       const float si = pool.score[i];
@@ -254,12 +258,14 @@ __global__ __launch_bounds__(SEL_THREADS) void expand_finalize_kernel(
     token[b] = pool.token[i];
     depth[b] = pool.depth[i];
     score[b] = pool.score[i];
+    qrow[b] = pool.qrow[i];
   }
   if (tid == 0) {
     parent[0] = -1;
     token[0] = root_token;
     depth[0] = 0;
     score[0] = 0.f;
+    qrow[0] = 0;   // the root's children come from draft-logit row 0
     *n_out = N + 1;
   }
   __syncthreads();
@@ -338,10 +344,10 @@ adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t
 
 adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
                                const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
-                               int L, int drow_base, int root_frow, int tree_frow0, const NextRows& nx,
+                               int L, int drow_base, int root_frow, int tree_frow0, int qrow_base, const NextRows& nx,
                                hipStream_t st) {
   expand_level_kernel<<<1, SEL_THREADS, 0, st>>>(pool, front, nf, cnt, base, depth, k_hat, top_id, top_val, lse, kmax,
-                                                 make_next, L, drow_base, root_frow, tree_frow0, nx);
+                                                 make_next, L, drow_base, root_frow, tree_frow0, qrow_base, nx);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -349,10 +355,11 @@ adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, i
 adt_status launch_expand_finalize(const Pool& pool, int C, int n_budget, int root_token, int L, int P, int n_image,
                                   const int32_t* allowed_img, int32_t* sel_rank, int32_t* bfs_of, int32_t* parent,
                                   int32_t* token, int32_t* depth, float* score, int32_t* pos, uint64_t* mask,
-                                  int32_t* allowed_rows, int32_t* n_out, hipStream_t st) {
+                                  int32_t* allowed_rows, int32_t* qrow, int32_t* n_out, bool keep_all,
+                                  hipStream_t st) {
   expand_finalize_kernel<<<1, SEL_THREADS, 0, st>>>(pool, C, n_budget, root_token, L, P, n_image, allowed_img,
                                                     sel_rank, bfs_of, parent, token, depth, score, pos, mask,
-                                                    allowed_rows, n_out);
+                                                    allowed_rows, qrow, n_out, keep_all ? 1 : 0);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -124,6 +124,7 @@ struct Pool {
   int32_t* depth;
   int32_t* parent;
   int32_t* drow;
+  int32_t* qrow;   // draft-logit row that drew an expanded node's children (-1 otherwise)
   uint64_t* rmask;
 };
 struct NextRows {
@@ -137,12 +138,13 @@ adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t
                            int32_t* top_id, float* top_val, float* lse, hipStream_t st);
 adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
                                const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
-                               int L, int drow_base, int root_frow, int tree_frow0, const NextRows& nx,
+                               int L, int drow_base, int root_frow, int tree_frow0, int qrow_base, const NextRows& nx,
                                hipStream_t st);
+// keep_all: every pool node in creation order (stochastic children), else the top-N rerank
 adt_status launch_expand_finalize(const Pool& pool, int C, int n_budget, int root_token, int L, int P, int n_image,
                                   const int32_t* allowed_img, int32_t* sel_rank, int32_t* bfs_of, int32_t* parent,
                                   int32_t* token, int32_t* depth, float* score, int32_t* pos, uint64_t* mask,
-                                  int32_t* allowed_rows, int32_t* n_out, hipStream_t st);
+                                  int32_t* allowed_rows, int32_t* qrow, int32_t* n_out, bool keep_all, hipStream_t st);
 adt_status launch_accept_greedy(const int32_t* argmax, int kmax, const int32_t* parent, const int32_t* token,
                                 const int32_t* n_nodes, int n_max, int32_t* path, int32_t* n_acc, int32_t* bonus,
                                 hipStream_t st);
@@ -161,11 +163,23 @@ adt_status launch_tree_rows(const int32_t* depth, const int32_t* n_nodes, int n_
                             hipStream_t st);
 
 // accept_sample.hip
+// Stochastic children: per frontier row r (pool index front[r], the root when front is null),
+// cnt i.i.d. draws from q (the acceptance's integer weights at temperature T, top_k) with
+// Philox counter (step, parent tree index, j, 2); top_id/top_val [rows][kmax] receive the ids
+// and their logits, lse [rows] the log-sum-exp at T = 1 over the allowed ids.  w: rows * V
+// uint64 of scratch.
+adt_status launch_row_sample(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows,
+                             const int32_t* front, int cnt, float T, int top_k, uint64_t seed, uint32_t step,
+                             uint64_t* w, int32_t* top_id, float* top_val, float* lse, int kmax, hipStream_t st);
 size_t accept_ws_bytes(int V);
 adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
                                 const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
                                 uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
                                 hipStream_t st);
+adt_status launch_accept_mss(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
+                             const int32_t* allowed, const int32_t* n_nodes, int n_max, const adt_accept_cfg& cfg,
+                             uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
+                             hipStream_t st);
 
 // knn.hip
 size_t knn_ws_bytes(int n);

@@ -80,10 +80,20 @@ def kv_compact(k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tenso
 
 
 def accept_cfg(mode: str = "greedy", temperature: float = 1.0, top_k: int = 0, delta: float = 0.0,
-               knn: Optional[torch.Tensor] = None, knn_k: int = 1, seed: int = 0) -> abi.AcceptCfg:
-    m = {"greedy": abi.ACCEPT_GREEDY, "exact": abi.ACCEPT_EXACT, "relaxed": abi.ACCEPT_RELAXED}[mode]
+               knn: Optional[torch.Tensor] = None, knn_k: int = 1, seed: int = 0, children: int = 0,
+               q_logits: Optional[torch.Tensor] = None, q_row: Optional[torch.Tensor] = None) -> abi.AcceptCfg:
+    """mode 'mss': Eq. 1 with stochastic children (children per expanded node in a session;
+    for adt_verify_accept the draft logit rows q_logits [rows][V] and the row q_row[u] that
+    drew node u's children)."""
+    m = {"greedy": abi.ACCEPT_GREEDY, "exact": abi.ACCEPT_EXACT, "relaxed": abi.ACCEPT_RELAXED,
+         "mss": abi.ACCEPT_MSS}[mode]
     rows, stride = (knn.shape[0], knn.shape[1]) if knn is not None else (0, 0)
-    return abi.AcceptCfg(m, temperature, top_k, delta, knn_k, rows, stride, _p(knn), seed)
+    q_ld, q_rows = (q_logits.stride(0), q_logits.shape[0]) if q_logits is not None else (0, 0)
+    cfg = abi.AcceptCfg(m, temperature, top_k, delta, knn_k, rows, stride, _p(knn), seed, children, _p(q_logits),
+                        q_ld, _p(q_row), q_rows)
+    # the struct holds raw device pointers: keep their tensors alive as long as the struct
+    cfg._tensors = (knn, q_logits, q_row)
+    return cfg
 
 
 def verify_accept(logits: torch.Tensor, parent: torch.Tensor, token: torch.Tensor, allowed: torch.Tensor,
@@ -111,6 +121,28 @@ def gemm_bf16(x: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = No
     N = w.shape[0]
     out = torch.empty(M, N, dtype=torch.float32, device=x.device) if out is None else out
     check(lib().adt_gemm_bf16(_p(x), x.stride(0), _p(w), w.stride(0), M, N, K, _p(out), out.stride(0), _stream()))
+    return out
+
+
+def pack_bf16(w: torch.Tensor) -> torch.Tensor:
+    """w bf16 [N][K] (row-major, K contiguous) -> the library's packed tile layout (uint8 bytes)."""
+    _require_cuda(w)
+    assert w.dtype == torch.bfloat16 and w.is_contiguous()
+    N, K = w.shape
+    out = torch.empty(lib().adt_packed_bytes(N, K, abi.BF16), dtype=torch.uint8, device=w.device)
+    srcs = (C.c_void_p * 1)(w.data_ptr())
+    rows = (C.c_int32 * 1)(N)
+    check(lib().adt_pack_weight(srcs, rows, 1, K, abi.PACK_STACK, 0, abi.BF16, _p(out), _stream()))
+    return out
+
+
+def gemm_bf16_packed(x: torch.Tensor, wp: torch.Tensor, N: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """x bf16 [M][K], wp = pack_bf16(w) for w [N][K] -> fp32 [M][N] = x . w^T."""
+    _require_cuda(x, wp)
+    assert x.dtype == torch.bfloat16 and x.stride(1) == 1
+    M, K = x.shape
+    out = torch.empty(M, N, dtype=torch.float32, device=x.device) if out is None else out
+    check(lib().adt_gemm_bf16_packed(_p(x), x.stride(0), _p(wp), M, N, K, _p(out), out.stride(0), _stream()))
     return out
 
 
@@ -248,7 +280,7 @@ class DeviceSession:
         mode = accept_mode or a.mode
         self.knn = knn
         self.accept = accept_cfg(mode, a.temperature, a.top_k, a.delta, knn, a.knn_k,
-                                 cfg.seed if accept_seed is None else accept_seed)
+                                 cfg.seed if accept_seed is None else accept_seed, children=a.children)
         desc = abi.SessionDesc(cfg.prefix_len, cfg.n_image, self.s_cap, _p(self.k_cache), _p(self.v_cache),
                                _p(self.dk_cache), _p(self.dv_cache),
                                C.cast(self._allowed, C.POINTER(C.c_int32)), sched_struct(cfg.sched, cfg.grid_w), self.accept,

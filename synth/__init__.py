@@ -63,11 +63,12 @@ class SchedCfg:
 
 @dataclasses.dataclass(frozen=True)
 class AcceptCfg:
-    mode: str = "greedy"   # "greedy" | "exact" | "relaxed"
+    mode: str = "greedy"   # "greedy" | "exact" | "relaxed" | "mss" (stochastic children, Eq. 1 as printed)
     temperature: float = 1.0
     top_k: int = 0         # 0 = untruncated
     delta: float = 0.0
     knn_k: int = 1
+    children: int = 0      # mss: children drawn per expanded node
 
 
 @dataclasses.dataclass(frozen=True)

@@ -51,8 +51,17 @@ def test_argument_errors_return_codes_without_launching(L):
     import ctypes as C
     assert L.adt_verify_accept(fake, 16, 16, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake, fake, 1 << 20,
                                None) == abi.E_ARG
+    # stochastic-children acceptance without its q rows (null, short row stride, no rows)
+    for q_logits, q_ld, q_row, q_rows in ((None, 16, fake, 4), (fake, 8, fake, 4), (fake, 16, None, 4),
+                                          (fake, 16, fake, 0)):
+        cfg = abi.AcceptCfg(abi.ACCEPT_MSS, 1.0, 0, 0.0, 1, 0, 0, None, 0, 2, q_logits, q_ld, q_row, q_rows)
+        assert L.adt_verify_accept(fake, 16, 16, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake, fake,
+                                   1 << 20, None) == abi.E_ARG
     # batched projection: null operands; N not a multiple of 128, K not of 64, short leading dimension
     assert L.adt_gemm_bf16(None, 64, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_ARG
+    assert L.adt_gemm_bf16_packed(fake, 64, None, 8, 128, 64, fake, 128, None) == abi.E_ARG
+    assert L.adt_gemm_bf16_packed(fake, 64, fake, 8, 384, 96, fake, 384, None) == abi.E_SHAPE
+    assert L.adt_gemm_bf16_packed(fake, 64, fake, 0, 256, 64, fake, 256, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 64, fake, 64, 8, 100, 64, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 96, fake, 96, 8, 128, 96, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 32, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_SHAPE
@@ -127,3 +136,19 @@ def test_schedule_init_rejects_bad_settings(L):
     s.init_mode = abi.INIT_HORIZONTAL
     assert L.adt_schedule_init(C.byref(s), 4, 4, rd, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG
     assert L.adt_schedule_init(C.byref(s), 0, 4, None, rd, rd, *[C.byref(o) for o in out]) == abi.E_ARG
+
+
+def test_accept_cfg_keeps_its_tensors_alive():
+    """The config struct holds raw device pointers; the binding keeps the tensors they point
+    to alive with it, so temporaries passed in cannot be freed (and their memory reused)
+    before a kernel reads them."""
+    import gc
+    import torch
+    from paper_2512_21857_amd import runtime as rt
+    cfg = rt.accept_cfg("mss", 1.0, 0, seed=1, children=2, q_logits=torch.arange(12.0).view(3, 4),
+                        q_row=torch.tensor([0, 2], dtype=torch.int32))
+    gc.collect()
+    q_logits, q_row = cfg._tensors[1], cfg._tensors[2]
+    assert cfg.q_logits == q_logits.data_ptr() and cfg.q_row == q_row.data_ptr()
+    assert (cfg.q_ld, cfg.q_rows, cfg.children) == (4, 3, 2)
+    assert q_logits[2, 3].item() == 11.0

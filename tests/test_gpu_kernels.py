@@ -255,6 +255,54 @@ def test_accept_sampling_bit_exact(rt, mode, top_k, T):
     assert agree == 72 and total_acc > 0
 
 
+@pytest.mark.parametrize("top_k,T", [(0, 1.0), (2000, 1.0), (3, 0.7), (50, 1.3)])
+def test_accept_mss_bit_exact(rt, top_k, T):
+    """Eq. 1 as printed with stochastic children (min(1, p/q), residual norm(max(0, p - q)) in
+    128-bit integer arithmetic): identical path and bonus to the oracle for every (seed, step)
+    on the same fp32 target and draft rows.  q rows are p rows plus noise, so p/q is near 1
+    and long paths are accepted; some nodes get an unrelated q (many rejections, residuals)."""
+    from oracle.accept import accept_mss
+    rng = np.random.default_rng(31)
+    V, lo, hi = 8448, 0, 8192
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    agree = total_acc = rejections = 0
+    for trial in range(16):
+        n = int(rng.integers(1, 62))
+        parent, token = _random_tree_tokens(rng, n, V, lo, hi)
+        logits = (rng.standard_normal((n, V)) * 1.5).astype(np.float32)
+        q_logits = np.zeros((n + 1, V), dtype=np.float32)
+        q_row = np.full(n, -1, dtype=np.int32)
+        for u in range(n):
+            kids = [c for c in range(n) if parent[c] == u]
+            if not kids:
+                continue
+            q_row[u] = u + 1
+            if rng.random() < 0.75:
+                q_logits[u + 1] = logits[u] + (rng.standard_normal(V) * 0.3).astype(np.float32)
+                logits[u, token[kids[0]]] += 8.0
+                q_logits[u + 1, token[kids[0]]] += 8.0
+            else:
+                q_logits[u + 1] = (rng.standard_normal(V) * 1.5).astype(np.float32)
+        allowed = np.tile([lo, hi], (n, 1)).astype(np.int32)
+        q_map = {u: q_logits[q_row[u]] for u in range(n) if q_row[u] >= 0}
+        tq, tr = t(q_logits), t(q_row)
+        for step in range(3):
+            seed = 2000 + trial
+            ref_path, ref_bonus = accept_mss(logits, q_map, parent, token, allowed, temperature=T, top_k=top_k,
+                                             seed=seed, step=step)
+            cfg = rt.accept_cfg("mss", T, top_k, seed=seed, q_logits=tq, q_row=tr)
+            path, n_acc, bonus = rt.verify_accept(t(logits), t(parent), t(token), t(allowed),
+                                                  t(np.array([n], dtype=np.int32)), cfg, step)
+            a = int(n_acc.item())
+            assert path[1:a + 1].cpu().tolist() == ref_path and int(bonus.item()) == ref_bonus, \
+                f"trial {trial} step {step}"
+            agree += 1
+            total_acc += a
+            u = ref_path[-1] if ref_path else 0
+            rejections += any(parent[c] == u for c in range(n))
+    assert agree == 48 and total_acc > 20 and rejections >= 3
+
+
 def test_accept_sampling_law_on_gpu(rt):
     """Committed first token over 4000 steps on the GPU follows p (chi-square), root with 3 children."""
     V = 16
@@ -301,6 +349,39 @@ def test_gemm_bf16_batched(rt, M, N, K):
     wt = torch.from_numpy(wb).cuda().bfloat16()
     got = rt.gemm_bf16(xt, wt).cpu().numpy()
     _gemm_ref_check(got, xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192)])
+def test_gemm_bf16_packed(rt, M, N, K):
+    """Packed weights: the DMA pipeline (256 x 256 blocks, >= 128 of them; K below and above the
+    stages it keeps in flight; one row; partial row blocks) and the register-staged kernel (few
+    blocks), every element; equal bit for bit to the row-major kernel (same summation order)."""
+    print(f"gemm_bf16_packed M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M * 7 + N + K)
+    xt = torch.from_numpy(rng.standard_normal((M, K)).astype(np.float32)).cuda().bfloat16()
+    wt = torch.from_numpy(rng.standard_normal((N, K)).astype(np.float32)).cuda().bfloat16()
+    wp = rt.pack_bf16(wt)
+    got = rt.gemm_bf16_packed(xt, wp, N)
+    _gemm_ref_check(got.cpu().numpy(), xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
+    assert torch.equal(got, rt.gemm_bf16(xt, wt))
+
+
+def test_gemm_bf16_packed_verify_shapes_sampled(rt):
+    """M = 976 (16 trees of 61 rows) with the 7B-shaped projections the benchmark times, on
+    sampled rows: QKV 4096 x 12288 and the LM head 4096 x 65536 (DMA pipeline), down 11008 x
+    4096 (register-staged)."""
+    rng = np.random.default_rng(977)
+    rows = np.array([0, 1, 31, 32, 255, 256, 511, 767, 768, 900, 975])
+    for K, N in ((4096, 12288), (4096, 65536), (11008, 4096)):
+        print(f"gemm_bf16_packed M=976 N={N} K={K}", flush=True)
+        xt = torch.from_numpy(rng.standard_normal((976, K)).astype(np.float32)).cuda().bfloat16()
+        wt = torch.from_numpy(rng.standard_normal((N, K)).astype(np.float32)).cuda().bfloat16()
+        got = rt.gemm_bf16_packed(xt, rt.pack_bf16(wt), N)
+        xs, ws = xt.float().cpu().numpy(), wt.float().cpu().numpy()
+        _gemm_ref_check(got.cpu().numpy(), xs, ws, rows)
+        assert torch.equal(got, rt.gemm_bf16(xt, wt))
+        del xt, wt, got
+        torch.cuda.empty_cache()
 
 
 def test_gemm_bf16_batched_verify_shape_sampled(rt):

@@ -233,6 +233,91 @@ def test_expand_from_table_bit_exact(rt, d_hat, k_hat, n_budget):
     assert np.array_equal(t["mask"].cpu().numpy().view(np.uint64), packed_mask(ref.parent, 2))
 
 
+@pytest.mark.parametrize("d_hat,k_hat,children,n_budget,top_k,T", [(1, 4, 3, 16, 0, 1.0), (3, 4, 3, 16, 0, 1.0),
+                                                                    (6, 10, 4, 60, 50, 0.8), (9, 13, 2, 127, 0, 1.3),
+                                                                    (4, 2, 16, 60, 0, 1.0)])
+def test_expand_sampled_from_table_bit_exact(rt, d_hat, k_hat, children, n_budget, top_k, T):
+    """Stochastic children (every expanded node draws its children from q; all drawn children
+    kept in creation order; whole expansions within the budget) driven by a caller-supplied
+    draft-logit table: the GPU tree equals the oracle's sampled expansion of the same table."""
+    from oracle.expand import build_tree, expand_sampled
+    cfg = synth.get_config("tiny")
+    cfg = dataclasses.replace(cfg, sched=dataclasses.replace(cfg.sched, d_hi=9, k_hi=13, n_budget=127),
+                              accept=synth.AcceptCfg(mode="mss", temperature=T, top_k=top_k, children=children))
+    _, om, dm, pre = _setup(rt, cfg)
+    rows = 97
+    table = synth.draw_tensor(78, 5, (rows, cfg.model.vocab), False, std=np.float32(2.0))
+    sess = rt.DeviceSession(dm, cfg, draft_table=torch.from_numpy(table).cuda())
+    root = sess.prefill(pre)
+    n = sess.expand(d_hat, k_hat, n_budget)
+    t = sess.tensors()
+    tab = table.astype(np.float64)
+    L = len(pre)
+    level_fn = lambda frontier, pool: np.stack([tab[_table_row(pool[u].depth, pool[u].token, rows)] for u in frontier])
+    pool, sel = expand_sampled(tab[_table_row(0, root, rows)], level_fn, d_hat, k_hat, children, n_budget,
+                               lambda dp: cfg.allowed(L + dp - len(pre)), temperature=T, top_k=top_k, seed=cfg.seed,
+                               step=t["step"])
+    ref = build_tree(root, pool, sel, by_creation=True)
+    print(f"sampled tree d={d_hat} k={k_hat} c={children}: {ref.n} nodes", flush=True)
+    assert n == ref.n
+    assert t["parent"].cpu().tolist() == ref.parent.tolist()
+    assert t["token"].cpu().tolist() == ref.token.tolist()
+    assert t["depth"].cpu().tolist() == ref.depth.tolist()
+    np.testing.assert_allclose(t["score"].cpu().numpy(), ref.score, atol=2e-5, rtol=1e-6)
+
+
+@pytest.mark.parametrize("children,top_k,T", [(3, 0, 1.0), (2, 40, 0.8)])
+def test_tiny_cycles_stochastic_children(rt, children, top_k, T):
+    """Whole cycles with stochastic children and Eq. 1 as printed (tiny fp32 model, ADT
+    schedule): schedule, sampled trees and committed tokens equal the oracle's cycle by
+    cycle; every cycle the session's acceptance kernel re-decides the oracle's logits, q rows
+    and tree bit for bit (the precision both decide in).  A difference of the sessions' own
+    commits is accepted only where that re-decision agrees with the oracle (a draw within the
+    fp32 logit error of a boundary); the run then stops."""
+    from oracle.accept import accept_mss
+    cfg = synth.get_config("tiny")
+    cfg = dataclasses.replace(cfg, accept=synth.AcceptCfg(mode="mss", temperature=T, top_k=top_k, children=children))
+    _, om, dm, pre = _setup(rt, cfg)
+    sess = rt.DeviceSession(dm, cfg)
+    dec = Decoder(cfg, om, pre)
+    assert sess.prefill(pre) == dec.prefill()
+    t_ = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    matched = accepted = 0
+    while not dec.done() and matched < 60:
+        o = dec.step()
+        g = sess.step()
+        t = sess.tensors()
+        assert (g["d_hat"], g["k_hat"]) == (o.d_hat, o.k_hat), f"schedule at step {o.step}"
+        assert t["parent"].cpu().tolist() == o.tree.parent.tolist(), f"tree parents at step {o.step}"
+        assert t["token"].cpu().tolist() == o.tree.token.tolist(), f"tree tokens at step {o.step}"
+        glog = t["logits"].cpu().numpy()
+        assert _tol_ok(glog, o.logits, TOL["f32"]).all()
+        # the kernel on the oracle's numbers
+        n = o.tree.n
+        q_nodes = sorted(dec.q_rows)
+        q_logits = np.stack([dec.q_rows[u] for u in q_nodes]).astype(np.float32) if q_nodes else \
+            np.zeros((1, cfg.model.vocab), np.float32)
+        q_row = np.full(n, -1, dtype=np.int32)
+        for i, u in enumerate(q_nodes):
+            if u < n:
+                q_row[u] = i
+        tq, tr_ = t_(q_logits), t_(q_row)
+        acfg = rt.accept_cfg("mss", T, top_k, seed=cfg.seed, q_logits=tq, q_row=tr_)
+        args = [t_(o.logits.astype(np.float32)), t_(o.tree.parent.astype(np.int32)), t_(o.tree.token.astype(np.int32)),
+                t_(o.allowed.astype(np.int32)), t_(np.array([n], dtype=np.int32))]
+        path, n_acc, bonus = rt.verify_accept(*args, acfg, o.step)
+        a = int(n_acc.item())
+        assert path[1:a + 1].cpu().tolist() == list(o.path) and int(bonus.item()) == o.bonus, \
+            f"shared-number acceptance differs at step {o.step}"
+        if g["tokens"] != o.committed:
+            print(f"stochastic children: commits differ at step {o.step} (fp32 draw boundary)", flush=True)
+            break
+        matched += 1
+        accepted += len(o.path)
+    print(f"stochastic children c={children}: {matched} cycles matched, {accepted} draft tokens accepted", flush=True)
+    assert matched >= 30 and accepted > 0
+
+
 def _planted(rt, cfg, m, extra_rng=0):
     """Planted tree: the oracle's own greedy AR continuation as one chain at random sibling
     ranks plus distractors.  Verify + accept + compact must give a = m, bonus = AR token m+1
