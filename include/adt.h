@@ -193,9 +193,15 @@ adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw,
 /* The same product with W in the packed layout of adt_pack_weight (ADT_PACK_STACK, bf16;
  * the layout every model weight is kept in), as the batched verification forward multiplies
  * it.  Wp: device, adt_packed_bytes(N, K, ADT_BF16) bytes, W's rows in their packed
- * order (C's columns follow that order).  Shapes, errors and asynchrony as adt_gemm_bf16. */
+ * order (C's columns follow that order).  workspace: NULL, or device scratch of
+ * adt_gemm_bf16_packed_workspace_size(M, N, K) bytes, with which a product of few output
+ * blocks and long K (K >= 2048) splits K across 2 or 4 workgroups per block and adds the fp32
+ * partials to C in a fixed order (deterministic; rounding then differs from the unsplit
+ * product by the reassociation of the K sum).  Shapes, errors and asynchrony as
+ * adt_gemm_bf16. */
+size_t adt_gemm_bf16_packed_workspace_size(int32_t M, int32_t N, int32_t K);
 adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K, float* C,
-                                int64_t ldc, void* stream);
+                                int64_t ldc, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ weights
  * Repacks row-major [rows][K] matrices (rows = output features) into the layout the GEMM

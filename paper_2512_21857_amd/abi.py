@@ -86,7 +86,8 @@ _SIGS = {
     "adt_codebook_knn_workspace_size": (sz, [i32]),
     "adt_codebook_knn": (i32, [p, i32, i32, i32, p, p, sz, p]),
     "adt_gemm_bf16": (i32, [p, i64, p, i64, i32, i32, i32, p, i64, p]),
-    "adt_gemm_bf16_packed": (i32, [p, i64, p, i32, i32, i32, p, i64, p]),
+    "adt_gemm_bf16_packed": (i32, [p, i64, p, i32, i32, i32, p, i64, p, sz, p]),
+    "adt_gemm_bf16_packed_workspace_size": (sz, [i32, i32, i32]),
     "adt_packed_bytes": (sz, [i32, i32, i32]),
     "adt_pack_weight": (i32, [C.POINTER(p), ip, i32, i32, i32, i32, i32, p, p]),
     "adt_schedule_next": (i32, [C.POINTER(SchedCfg), i32, i32, i32, i32, i32, i32, i32, ip, ip]),

@@ -261,9 +261,16 @@ extern "C" adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, i
   return launch_gemm_nt(X, ldx, W, ldw, M, N, K, C, ldc, (hipStream_t)stream);
 }
 
+extern "C" size_t adt_gemm_bf16_packed_workspace_size(int32_t M, int32_t N, int32_t K) {
+  if (M < 1 || N < 256 || N % 256 != 0 || K < 64) return 0;
+  return (size_t)(gemm_nt_ksplit(M, N, K, SIZE_MAX) - 1) * M * N * sizeof(float);
+}
+
 extern "C" adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K,
-                                           float* C, int64_t ldc, void* stream) {
-  return launch_gemm_nt(X, ldx, Wp, K, M, N, K, C, ldc, (hipStream_t)stream, nullptr, nullptr, true);
+                                           float* C, int64_t ldc, void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+  return launch_gemm_nt(X, ldx, Wp, K, M, N, K, C, ldc, (hipStream_t)stream, nullptr, nullptr, true, (float*)workspace,
+                        workspace ? workspace_bytes / sizeof(float) : 0);
 }
 
 extern "C" size_t adt_packed_bytes(int32_t total_rows, int32_t K, int32_t dtype) {

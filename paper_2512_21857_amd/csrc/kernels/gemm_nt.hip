@@ -18,6 +18,9 @@
 // batched path too.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+#include <cstdint>
+
 #include "../launch.h"
 
 namespace adt {
@@ -156,10 +159,14 @@ constexpr int DMA_THREADS = 512, DMA_TILES = 32, DMA_SLOT = DMA_TILES * 1024, DM
                "v"(g1), "v"(g2), "v"(g3), "s"(d), "s"((d) + 1024), "s"((d) + 2048), "s"((d) + 3072)          \
                : "memory", "m0")
 
+// With ksplit > 1 the K stages of a block are split into ksplit contiguous ranges, one per
+// workgroup: range 0 writes C, range s > 0 writes the fp32 partial P[s-1] ([M][N], row stride
+// N), and gemm_nt_reduce_kernel adds them to C in range order (deterministic).
 template <int NSTAGE>
 __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t* __restrict__ X, int64_t ldx,
-                                                                  const uint16_t* __restrict__ W, int M, int K,
-                                                                  float* __restrict__ C, int64_t ldc) {
+                                                                  const uint16_t* __restrict__ W, int M, int N, int K,
+                                                                  float* __restrict__ C, int64_t ldc, int ksplit,
+                                                                  float* __restrict__ P) {
   static_assert(NSTAGE == 4 || NSTAGE == 5, "the wait counts below assume four or five slots");
   constexpr int D = NSTAGE - 1;   // stages in flight ahead of the one being multiplied
   __shared__ __attribute__((aligned(1024))) uint16_t lds[NSTAGE * DMA_SLOT / 2];
@@ -167,10 +174,12 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
   // tiles (row blocks fastest), so the row blocks that share a W block meet in one L2
   const int MT = (M + 255) / 256, G = gridDim.x;
   const int b = blockIdx.x, xcd = b % 8, q = G / 8, r = G % 8;
-  const int t = xcd * q + min(xcd, r) + b / 8;
+  const int tk = xcd * q + min(xcd, r) + b / 8;
+  const int ks = tk % ksplit, t = tk / ksplit;
   const int m0 = (t % MT) * 256, n0 = (t / MT) * 256;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / WAVE), lane = tid % WAVE;
   const int wn = wave / 4, wm = wave % 4;
+  const int KTall = K / 32, kt0 = (int)((int64_t)KTall * ks / ksplit), kt1 = (int)((int64_t)KTall * (ks + 1) / ksplit);
 
   // DMA sources: wave w fills tiles 4w..4w+3 of every stage (W tiles for w < 4, X tiles after)
   const uint16_t* src[4];
@@ -185,9 +194,11 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
     }
   }
   const int64_t step = wave < 4 ? 512 : 32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) src[i] += kt0 * step;   // this workgroup's K range
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)lds;
   const uint32_t wdst = lds0 + 4 * wave * 1024;
-  const int KT = K / 32;
+  const int KT = kt1 - kt0;
   auto issue = [&](int kt) {   // past the last stage: the last stage again, into a slot never read
     const int64_t ks = min(kt, KT - 1) * step;
     const uint32_t d = wdst + (kt % NSTAGE) * DMA_SLOT;
@@ -242,6 +253,8 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
   }
   // no DMA may still be writing this workgroup's LDS when it exits
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  float* out = ks == 0 ? C : P + (int64_t)(ks - 1) * M * N;
+  const int64_t ldo = ks == 0 ? ldc : N;
   const int l32 = lane % 32, hi = lane / 32;
 #pragma unroll
   for (int nb = 0; nb < 4; ++nb)
@@ -252,15 +265,42 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
         const int n = n0 + wn * 128 + nb * 32 + 8 * grp + 4 * hi;
-        *reinterpret_cast<f32x4*>(C + (int64_t)m * ldc + n) =
+        *reinterpret_cast<f32x4*>(out + (int64_t)m * ldo + n) =
             f32x4{acc[nb][mb][4 * grp], acc[nb][mb][4 * grp + 1], acc[nb][mb][4 * grp + 2], acc[nb][mb][4 * grp + 3]};
       }
     }
 }
 #undef ADT_DMA4
 
+// C += P[0] + P[1] + ... in that order, four columns per thread.
+__global__ void gemm_nt_reduce_kernel(float* __restrict__ C, int64_t ldc, const float* __restrict__ P, int M, int N,
+                                      int nparts) {
+  const int64_t quads = (int64_t)M * (N / 4);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < quads; i += (int64_t)gridDim.x * blockDim.x) {
+    const int m = (int)(i / (N / 4)), n = (int)(i % (N / 4)) * 4;
+    f32x4 c = *reinterpret_cast<const f32x4*>(C + (int64_t)m * ldc + n);
+    for (int s = 0; s < nparts; ++s) {
+      const f32x4 p = *reinterpret_cast<const f32x4*>(P + (int64_t)s * M * N + (int64_t)m * N + n);
+      c = f32x4{c[0] + p[0], c[1] + p[1], c[2] + p[2], c[3] + p[3]};
+    }
+    *reinterpret_cast<f32x4*>(C + (int64_t)m * ldc + n) = c;
+  }
+}
+
+// K ranges per 256 x 256 block for the DMA pipeline: 1, or (blocks under 128, K >= 2048 so
+// the partials' traffic stays small beside the product) 4, else 2, as far as part_elems holds
+// the extra ranges' partials.
+int gemm_nt_ksplit(int M, int N, int K, size_t part_elems) {
+  const int64_t tiles = (int64_t)((M + 255) / 256) * (N / 256);
+  if (tiles >= 128 || K < 2048) return 1;
+  for (int ks = 4; ks >= 2; ks /= 2)
+    if ((size_t)(ks - 1) * M * N <= part_elems && K / 32 >= 4 * ks) return ks;
+  return 1;
+}
+
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
-                          int64_t ldc, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, bool packed) {
+                          int64_t ldc, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, bool packed, float* part,
+                          size_t part_elems) {
   ADT_CHECK_ARG(X && W && C, ADT_E_ARG, "gemm_nt: null pointer");
   ADT_CHECK_ARG(M >= 1 && N >= 128 && K >= 64 && N % 128 == 0 && K % 64 == 0, ADT_E_SHAPE,
                 "gemm_nt: M=%d N=%d K=%d (N a multiple of 128, K of 64)", M, N, K);
@@ -272,12 +312,22 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
   const int best = (N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 256) ? 0 : 2;
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)W;
-  // Packed weights in 256 x 256 blocks when that still gives at least 128 workgroups (half
-  // the CUs; measured faster than the 128 x 128 blocks down to there): the DMA pipeline.
-  if (packed && N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 128) {
-    hipExtLaunchKernelGGL(gemm_nt_dma_kernel<DMA_NSTAGE>, dim3((M + 255) / 256 * (N / 256)), dim3(DMA_THREADS), 0, st,
-                          ev0, ev1, 0, x, ldx, w, M, K, C, ldc);
+  // Packed weights in 256 x 256 blocks when that gives at least 128 workgroups (half the CUs;
+  // measured faster than the 128 x 128 blocks down to there), if need be with K split across
+  // workgroups: the DMA pipeline.
+  const int ksplit = (packed && N % 256 == 0 && part) ? gemm_nt_ksplit(M, N, K, part_elems) : 1;
+  if (packed && N % 256 == 0 && (ksplit > 1 || (int64_t)(N / 256) * ((M + 255) / 256) >= 128)) {
+    hipExtLaunchKernelGGL(gemm_nt_dma_kernel<DMA_NSTAGE>, dim3((M + 255) / 256 * (N / 256) * ksplit),
+                          dim3(DMA_THREADS), 0, st, ev0, ksplit > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc,
+                          ksplit, part);
     ADT_LAUNCH_CHECK();
+    if (ksplit > 1) {
+      const int64_t quads = (int64_t)M * (N / 4);
+      const int blocks = (int)std::min<int64_t>((quads + 255) / 256, 4096);
+      hipExtLaunchKernelGGL(gemm_nt_reduce_kernel, dim3(blocks), dim3(256), 0, st, nullptr, ev1, 0, C, ldc,
+                            (const float*)part, M, N, ksplit - 1);
+      ADT_LAUNCH_CHECK();
+    }
     return ADT_OK;
   }
 #define ADT_NT(BNV, BMV, PK)                                                                                    \

@@ -136,13 +136,20 @@ def pack_bf16(w: torch.Tensor) -> torch.Tensor:
     return out
 
 
-def gemm_bf16_packed(x: torch.Tensor, wp: torch.Tensor, N: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """x bf16 [M][K], wp = pack_bf16(w) for w [N][K] -> fp32 [M][N] = x . w^T."""
+def gemm_bf16_packed(x: torch.Tensor, wp: torch.Tensor, N: int, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, split: bool = True) -> torch.Tensor:
+    """x bf16 [M][K], wp = pack_bf16(w) for w [N][K] -> fp32 [M][N] = x . w^T.  With split the
+    K-split scratch is allocated here unless a workspace is given; without, no K split."""
     _require_cuda(x, wp)
     assert x.dtype == torch.bfloat16 and x.stride(1) == 1
     M, K = x.shape
     out = torch.empty(M, N, dtype=torch.float32, device=x.device) if out is None else out
-    check(lib().adt_gemm_bf16_packed(_p(x), x.stride(0), _p(wp), M, N, K, _p(out), out.stride(0), _stream()))
+    if split and workspace is None:
+        need = lib().adt_gemm_bf16_packed_workspace_size(M, N, K)
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device) if need else None
+    ws, nbytes = (workspace, workspace.numel()) if split and workspace is not None else (None, 0)
+    check(lib().adt_gemm_bf16_packed(_p(x), x.stride(0), _p(wp), M, N, K, _p(out), out.stride(0), _p(ws), nbytes,
+                                     _stream()))
     return out
 
 

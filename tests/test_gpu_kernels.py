@@ -351,11 +351,15 @@ def test_gemm_bf16_batched(rt, M, N, K):
     _gemm_ref_check(got, xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
 
 
-@pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192)])
+@pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192),
+                                   (300, 512, 4096), (40, 1024, 2112)])
 def test_gemm_bf16_packed(rt, M, N, K):
     """Packed weights: the DMA pipeline (256 x 256 blocks, >= 128 of them; K below and above the
-    stages it keeps in flight; one row; partial row blocks) and the register-staged kernel (few
-    blocks), every element; equal bit for bit to the row-major kernel (same summation order)."""
+    stages it keeps in flight; one row; partial row blocks), the DMA pipeline with K split over
+    4 workgroups per block (few blocks, long K; uneven ranges at K = 2112) and the
+    register-staged kernel, every element.  Without a K split the result equals the row-major
+    kernel bit for bit (same summation order); the split result is checked against the bound
+    and, with the workspace withheld, the unsplit result is the row-major one again."""
     print(f"gemm_bf16_packed M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M * 7 + N + K)
     xt = torch.from_numpy(rng.standard_normal((M, K)).astype(np.float32)).cuda().bfloat16()
@@ -363,23 +367,31 @@ def test_gemm_bf16_packed(rt, M, N, K):
     wp = rt.pack_bf16(wt)
     got = rt.gemm_bf16_packed(xt, wp, N)
     _gemm_ref_check(got.cpu().numpy(), xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
-    assert torch.equal(got, rt.gemm_bf16(xt, wt))
+    split = rt.lib().adt_gemm_bf16_packed_workspace_size(M, N, K) > 0
+    assert split == (K >= 2048)
+    ref = rt.gemm_bf16(xt, wt)
+    if split:
+        assert torch.equal(rt.gemm_bf16_packed(xt, wp, N, split=False), ref)
+        assert torch.equal(rt.gemm_bf16_packed(xt, wp, N), got)   # deterministic
+    else:
+        assert torch.equal(got, ref)
 
 
 def test_gemm_bf16_packed_verify_shapes_sampled(rt):
     """M = 976 (16 trees of 61 rows) with the 7B-shaped projections the benchmark times, on
-    sampled rows: QKV 4096 x 12288 and the LM head 4096 x 65536 (DMA pipeline), down 11008 x
-    4096 (register-staged)."""
+    sampled rows: QKV 4096 x 12288 and the LM head 4096 x 65536 (DMA pipeline), O 4096 x 4096
+    and down 11008 x 4096 (DMA pipeline with K split in four)."""
     rng = np.random.default_rng(977)
     rows = np.array([0, 1, 31, 32, 255, 256, 511, 767, 768, 900, 975])
-    for K, N in ((4096, 12288), (4096, 65536), (11008, 4096)):
+    for K, N in ((4096, 12288), (4096, 65536), (4096, 4096), (11008, 4096)):
         print(f"gemm_bf16_packed M=976 N={N} K={K}", flush=True)
         xt = torch.from_numpy(rng.standard_normal((976, K)).astype(np.float32)).cuda().bfloat16()
         wt = torch.from_numpy(rng.standard_normal((N, K)).astype(np.float32)).cuda().bfloat16()
         got = rt.gemm_bf16_packed(xt, rt.pack_bf16(wt), N)
         xs, ws = xt.float().cpu().numpy(), wt.float().cpu().numpy()
         _gemm_ref_check(got.cpu().numpy(), xs, ws, rows)
-        assert torch.equal(got, rt.gemm_bf16(xt, wt))
+        if rt.lib().adt_gemm_bf16_packed_workspace_size(976, N, K) == 0:
+            assert torch.equal(got, rt.gemm_bf16(xt, wt))
         del xt, wt, got
         torch.cuda.empty_cache()
 
