@@ -1270,7 +1270,30 @@ struct adt_batch_s {
   uint64_t* mask;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+  // The sessions' draft expansions are independent chains of small kernels; they run on
+  // BATCH_STREAMS streams of their own (default priority), joined to the caller's stream by
+  // events, so several overlap on the GPU.
+  static constexpr int BATCH_STREAMS = 4;
+  hipStream_t aux[BATCH_STREAMS] = {};
+  hipEvent_t ev_fork = nullptr, ev_join[BATCH_STREAMS] = {};
+  ~adt_batch_s() {
+    for (int j = 0; j < BATCH_STREAMS; ++j) {
+      if (aux[j]) (void)hipStreamDestroy(aux[j]);
+      if (ev_join[j]) (void)hipEventDestroy(ev_join[j]);
+    }
+    if (ev_fork) (void)hipEventDestroy(ev_fork);
+  }
 };
+
+static adt_status batch_streams(adt_batch_s* bt) {
+  if (bt->ev_fork) return ADT_OK;
+  for (int j = 0; j < adt_batch_s::BATCH_STREAMS; ++j) {
+    ADT_HIP(hipStreamCreateWithFlags(&bt->aux[j], hipStreamNonBlocking));
+    ADT_HIP(hipEventCreateWithFlags(&bt->ev_join[j], hipEventDisableTiming));
+  }
+  ADT_HIP(hipEventCreateWithFlags(&bt->ev_fork, hipEventDisableTiming));
+  return ADT_OK;
+}
 
 static adt_status check_batch(adt_session* const* ss, int B, int64_t& cache_sb) {
   ADT_CHECK_ARG(ss && B >= 1 && B <= 256, ADT_E_ARG, "batch: %d sessions", B);
@@ -1403,19 +1426,30 @@ extern "C" adt_status adt_batch_step(adt_batch* bt, adt_step_out* outs, void* st
   hipStream_t st = (hipStream_t)stream;
   const int B = bt->B;
   std::vector<int> dh(B, 0), kh(B, 0), n(B, 0), active(B, 0);
-  // each session's schedule and draft tree, as in adt_step
-  for (int b = 0; b < B; ++b) {
+  // each session's schedule and draft tree, as in adt_step; the expansions of different
+  // sessions run on the auxiliary streams, after everything already on the caller's stream
+  TRY(batch_streams(bt));
+  constexpr int NS = adt_batch_s::BATCH_STREAMS;
+  ADT_HIP(hipEventRecord(bt->ev_fork, st));
+  for (int j = 0; j < NS; ++j) ADT_HIP(hipStreamWaitEvent(bt->aux[j], bt->ev_fork, 0));
+  adt_status fail = ADT_OK;
+  for (int b = 0; b < B && fail == ADT_OK; ++b) {
     adt_session_s* s = bt->ss[b];
     if ((int)s->tokens.size() - s->P >= s->T) continue;
     active[b] = 1;
-    TRY(schedule_for(s, dh[b], kh[b]));
-    if (dh[b] >= 1) {
-      TRY(adt_tree_expand(s, dh[b], kh[b], s->d.sched.n_budget, nullptr, st));
-    } else {
-      TRY(set_root_only_tree(s, s->tokens[s->L], s->L, st));
-    }
+    hipStream_t sb = bt->aux[b % NS];
+    fail = schedule_for(s, dh[b], kh[b]);
+    if (fail == ADT_OK)
+      fail = dh[b] >= 1 ? adt_tree_expand(s, dh[b], kh[b], s->d.sched.n_budget, nullptr, sb)
+                        : set_root_only_tree(s, s->tokens[s->L], s->L, sb);
     n[b] = s->n_nodes;
   }
+  // join before anything else (also on failure, so no stream is left ahead of the caller's)
+  for (int j = 0; j < NS; ++j) {
+    ADT_HIP(hipEventRecord(bt->ev_join[j], bt->aux[j]));
+    ADT_HIP(hipStreamWaitEvent(st, bt->ev_join[j], 0));
+  }
+  if (fail != ADT_OK) return fail;
   // packed rows: tree b at rows [off_b, off_b + n_b); node i at cache slot L_b + i
   std::vector<int32_t> off(B + 1, 0), kv(B, 0), slot, seq;
   int nq_max = 1;
