@@ -147,7 +147,7 @@ __global__ __launch_bounds__(NT_THREADS) void gemm_nt_kernel(const uint16_t* __r
 // the next stage's first fragments are read while the second half's MFMAs run.  The DMA and
 // the waits are inline assembly because the compiler, which cannot tell LDS slots apart,
 // would otherwise wait for every DMA in flight before each LDS read.
-constexpr int DMA_THREADS = 512, DMA_TILES = 32, DMA_SLOT = DMA_TILES * 1024, DMA_NSTAGE = 5;
+constexpr int DMA_NSTAGE = 5;
 
 // M0 is written with s_mov only: an SCC-writing instruction here would corrupt a compare the
 // compiler keeps live across the statement.
@@ -162,38 +162,45 @@ constexpr int DMA_THREADS = 512, DMA_TILES = 32, DMA_SLOT = DMA_TILES * 1024, DM
 // With ksplit > 1 the K stages of a block are split into ksplit contiguous ranges, one per
 // workgroup: range 0 writes C, range s > 0 writes the fp32 partial P[s-1] ([M][N], row stride
 // N), and gemm_nt_reduce_kernel adds them to C in range order (deterministic).
-template <int NSTAGE>
-__global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t* __restrict__ X, int64_t ldx,
-                                                                  const uint16_t* __restrict__ W, int M, int N, int K,
-                                                                  float* __restrict__ C, int64_t ldc, int ksplit,
-                                                                  float* __restrict__ P) {
+// BN x BM block of C^T per workgroup of WN x WM waves (each a (BN/WN) x (BM/WM) part of 32x32
+// MFMA blocks); a stage slot holds (BN + BM) / 16 tiles, four per wave: 256 x 256 with 2 x 4
+// waves, or 128 x 128 with 2 x 2 (two workgroups per CU).
+template <int BN, int BM, int WN, int WM, int NSTAGE>
+__global__ __launch_bounds__(WN * WM * WAVE) void gemm_nt_dma_kernel(const uint16_t* __restrict__ X, int64_t ldx,
+                                                                     const uint16_t* __restrict__ W, int M, int N,
+                                                                     int K, float* __restrict__ C, int64_t ldc,
+                                                                     int ksplit, float* __restrict__ P) {
   static_assert(NSTAGE == 4 || NSTAGE == 5, "the wait counts below assume four or five slots");
+  constexpr int WAVES = WN * WM, TILES = (BN + BM) / 16, SLOT = TILES * 1024;
+  constexpr int WTN = BN / WN, WTM = BM / WM, NB = WTN / 32, MB = WTM / 32;
+  static_assert(TILES == 4 * WAVES && (BN / 16) % 4 == 0 && NB >= 1 && MB >= 1, "four DMA tiles per wave");
   constexpr int D = NSTAGE - 1;   // stages in flight ahead of the one being multiplied
-  __shared__ __attribute__((aligned(1024))) uint16_t lds[NSTAGE * DMA_SLOT / 2];
+  __shared__ __attribute__((aligned(1024))) uint16_t lds[NSTAGE * SLOT / 2];
   // XCD-aware order: workgroup b runs on XCD b % 8; each XCD takes a contiguous range of
   // tiles (row blocks fastest), so the row blocks that share a W block meet in one L2
-  const int MT = (M + 255) / 256, G = gridDim.x;
+  const int MT = (M + BM - 1) / BM, G = gridDim.x;
   const int b = blockIdx.x, xcd = b % 8, q = G / 8, r = G % 8;
   const int tk = xcd * q + min(xcd, r) + b / 8;
   const int ks = tk % ksplit, t = tk / ksplit;
-  const int m0 = (t % MT) * 256, n0 = (t / MT) * 256;
+  const int m0 = (t % MT) * BM, n0 = (t / MT) * BN;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / WAVE), lane = tid % WAVE;
-  const int wn = wave / 4, wm = wave % 4;
+  const int wn = wave / WM, wm = wave % WM;
+  constexpr int WAVES_W = (BN / 16) / 4;   // waves that load W tiles
   const int KTall = K / 32, kt0 = (int)((int64_t)KTall * ks / ksplit), kt1 = (int)((int64_t)KTall * (ks + 1) / ksplit);
 
-  // DMA sources: wave w fills tiles 4w..4w+3 of every stage (W tiles for w < 4, X tiles after)
+  // DMA sources: wave w fills tiles 4w..4w+3 of every stage (W tiles first, then X tiles)
   const uint16_t* src[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int T = 4 * wave + i;
-    if (wave < 4) {
+    if (wave < WAVES_W) {
       src[i] = W + ((int64_t)(n0 / 16 + T) * (K / 32)) * 512 + lane * 8;
     } else {
-      const int m = min(m0 + 16 * (T - 16) + lane % 16, M - 1);   // rows past M feed discarded columns
+      const int m = min(m0 + 16 * (T - BN / 16) + lane % 16, M - 1);   // rows past M feed discarded columns
       src[i] = X + (int64_t)m * ldx + 8 * (lane / 16);
     }
   }
-  const int64_t step = wave < 4 ? 512 : 32;
+  const int64_t step = wave < WAVES_W ? 512 : 32;
 #pragma unroll
   for (int i = 0; i < 4; ++i) src[i] += kt0 * step;   // this workgroup's K range
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint16_t*)lds;
@@ -201,55 +208,56 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
   const int KT = kt1 - kt0;
   auto issue = [&](int kt) {   // past the last stage: the last stage again, into a slot never read
     const int64_t ks = min(kt, KT - 1) * step;
-    const uint32_t d = wdst + (kt % NSTAGE) * DMA_SLOT;
+    const uint32_t d = wdst + (kt % NSTAGE) * SLOT;
     ADT_DMA4(src[0] + ks, src[1] + ks, src[2] + ks, src[3] + ks, d);
   };
-  // fragment offsets (bytes) inside a slot: A = W rows wn*128 + 32 nb + lane%32, B = X rows
-  // wm*64 + 32 mb + lane%32, columns 16 s + 8 (lane/32) of the stage
+  // fragment offsets (bytes) inside a slot: A = W rows wn*WTN + 32 nb + lane%32, B = X rows
+  // wm*WTM + 32 mb + lane%32, columns 16 s + 8 (lane/32) of the stage
   const int sub = ((lane / 32) * 16 + lane % 16) * 16;
-  const int aoff = (wn * 8 + (lane % 32) / 16) * 1024 + sub;
-  const int boff = (16 + wm * 4 + (lane % 32) / 16) * 1024 + sub;
+  const int aoff = (wn * (WTN / 16) + (lane % 32) / 16) * 1024 + sub;
+  const int boff = (BN / 16 + wm * (WTM / 16) + (lane % 32) / 16) * 1024 + sub;
   const char* lbase = (const char*)lds;
   auto frags = [&](int kt, int s, bf16x8* a, bf16x8* bb) {
-    const char* p = lbase + (kt % NSTAGE) * DMA_SLOT + s * 512;
+    const char* p = lbase + (kt % NSTAGE) * SLOT + s * 512;
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb) a[nb] = *reinterpret_cast<const bf16x8*>(p + aoff + nb * 2048);
+    for (int nb = 0; nb < NB; ++nb) a[nb] = *reinterpret_cast<const bf16x8*>(p + aoff + nb * 2048);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) bb[mb] = *reinterpret_cast<const bf16x8*>(p + boff + mb * 2048);
+    for (int mb = 0; mb < MB; ++mb) bb[mb] = *reinterpret_cast<const bf16x8*>(p + boff + mb * 2048);
   };
-  f32x16 acc[4][2];
+  f32x16 acc[NB][MB];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < NB; ++a)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < MB; ++c)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.f;
   auto mma = [&](const bf16x8* a, const bf16x8* bb) {
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], bb[mb], acc[nb][mb], 0, 0, 0);
+      for (int mb = 0; mb < MB; ++mb)
+        acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], bb[mb], acc[nb][mb], 0, 0, 0);
   };
 
 #pragma unroll
   for (int s = 0; s < D; ++s) issue(s);
   if constexpr (D == 3) asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
   else asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
-  bf16x8 a0[4], b0[2], a1[4], b1[2];
+  bf16x8 a0[NB], b0[MB], a1[NB], b1[MB];
   frags(0, 0, a0, b0);
   __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the loop starts with no LDS read pending
   for (int kt = 0; kt < KT; ++kt) {
     frags(kt, 1, a1, b1);
     mma(a0, b0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);   // the six reads first, then the MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NB + MB, 0);   // the reads first, then the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x008, NB * MB, 0);
     if constexpr (D == 3) asm volatile("s_waitcnt vmcnt(4)\n\ts_barrier" ::: "memory");
     else asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
     issue(kt + D);
     frags(kt + 1, 0, a0, b0);   // past the last stage: a stale slot, never used
     mma(a1, b1);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NB + MB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NB * MB, 0);
   }
   // no DMA may still be writing this workgroup's LDS when it exits
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -257,14 +265,14 @@ __global__ __launch_bounds__(DMA_THREADS) void gemm_nt_dma_kernel(const uint16_t
   const int64_t ldo = ks == 0 ? ldc : N;
   const int l32 = lane % 32, hi = lane / 32;
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb)
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      const int m = m0 + wm * 64 + mb * 32 + l32;
+    for (int mb = 0; mb < MB; ++mb) {
+      const int m = m0 + wm * WTM + mb * 32 + l32;
       if (m >= M) continue;
 #pragma unroll
       for (int grp = 0; grp < 4; ++grp) {
-        const int n = n0 + wn * 128 + nb * 32 + 8 * grp + 4 * hi;
+        const int n = n0 + wn * WTN + nb * 32 + 8 * grp + 4 * hi;
         *reinterpret_cast<f32x4*>(out + (int64_t)m * ldo + n) =
             f32x4{acc[nb][mb][4 * grp], acc[nb][mb][4 * grp + 1], acc[nb][mb][4 * grp + 2], acc[nb][mb][4 * grp + 3]};
       }
@@ -317,9 +325,9 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
   // workgroups: the DMA pipeline.
   const int ksplit = (packed && N % 256 == 0 && part) ? gemm_nt_ksplit(M, N, K, part_elems) : 1;
   if (packed && N % 256 == 0 && (ksplit > 1 || (int64_t)(N / 256) * ((M + 255) / 256) >= 128)) {
-    hipExtLaunchKernelGGL(gemm_nt_dma_kernel<DMA_NSTAGE>, dim3((M + 255) / 256 * (N / 256) * ksplit),
-                          dim3(DMA_THREADS), 0, st, ev0, ksplit > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc,
-                          ksplit, part);
+    hipExtLaunchKernelGGL((gemm_nt_dma_kernel<256, 256, 2, 4, DMA_NSTAGE>),
+                          dim3((M + 255) / 256 * (N / 256) * ksplit), dim3(8 * WAVE), 0, st, ev0,
+                          ksplit > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc, ksplit, part);
     ADT_LAUNCH_CHECK();
     if (ksplit > 1) {
       const int64_t quads = (int64_t)M * (N / 4);
@@ -328,6 +336,14 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
                             (const float*)part, M, N, ksplit - 1);
       ADT_LAUNCH_CHECK();
     }
+    return ADT_OK;
+  }
+  // Packed weights with fewer blocks (the narrow projections of a batch of trees): 128 x 128
+  // blocks of four waves through the same DMA pipeline, two workgroups per CU.
+  if (packed) {
+    hipExtLaunchKernelGGL((gemm_nt_dma_kernel<128, 128, 2, 2, DMA_NSTAGE>), dim3((M + 127) / 128 * (N / 128)),
+                          dim3(4 * WAVE), 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, C, ldc, 1, nullptr);
+    ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
 #define ADT_NT(BNV, BMV, PK)                                                                                    \

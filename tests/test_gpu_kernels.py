@@ -352,12 +352,13 @@ def test_gemm_bf16_batched(rt, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192),
-                                   (300, 512, 4096), (40, 1024, 2112)])
+                                   (300, 512, 4096), (40, 1024, 2112), (130, 384, 320), (976, 3840, 1280)])
 def test_gemm_bf16_packed(rt, M, N, K):
-    """Packed weights: the DMA pipeline (256 x 256 blocks, >= 128 of them; K below and above the
-    stages it keeps in flight; one row; partial row blocks), the DMA pipeline with K split over
-    4 workgroups per block (few blocks, long K; uneven ranges at K = 2112) and the
-    register-staged kernel, every element.  Without a K split the result equals the row-major
+    """Packed weights: the DMA pipeline in 256 x 256 blocks (>= 128 of them; K below and above
+    the stages it keeps in flight; one row; partial row blocks), with K split over 4
+    workgroups per block (few blocks, long K; uneven ranges at K = 2112), and in 128 x 128
+    blocks of four waves (few blocks, short K: the narrow projections of a batch of trees),
+    every element.  Without a K split the result equals the row-major
     kernel bit for bit (same summation order); the split result is checked against the bound
     and, with the workspace withheld, the unsplit result is the row-major one again."""
     print(f"gemm_bf16_packed M={M} N={N} K={K}", flush=True)
