@@ -195,7 +195,7 @@ adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw,
  * it.  Wp: device, adt_packed_bytes(N, K, ADT_BF16) bytes, W's rows in their packed
  * order (C's columns follow that order).  workspace: NULL, or device scratch of
  * adt_gemm_bf16_packed_workspace_size(M, N, K) bytes, with which a product of few output
- * blocks and long K (K >= 2048) splits K across 2 or 4 workgroups per block and adds the fp32
+ * blocks and long K (K >= 8192) splits K across 2 or 4 workgroups per block and adds the fp32
  * partials to C in a fixed order (deterministic; rounding then differs from the unsplit
  * product by the reassociation of the K sum).  Shapes, errors and asynchrony as
  * adt_gemm_bf16. */

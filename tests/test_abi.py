@@ -62,11 +62,11 @@ def test_argument_errors_return_codes_without_launching(L):
     assert L.adt_gemm_bf16_packed(fake, 64, None, 8, 128, 64, fake, 128, None, 0, None) == abi.E_ARG
     assert L.adt_gemm_bf16_packed(fake, 64, fake, 8, 384, 96, fake, 384, None, 0, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16_packed(fake, 64, fake, 0, 256, 64, fake, 256, None, 0, None) == abi.E_SHAPE
-    # K split only for few blocks and long K: 4 ranges of the 64-block 4096 x 4096 product,
-    # none for the 256-block LM head or short K
-    assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 4096) == 3 * 976 * 4096 * 4
-    assert L.adt_gemm_bf16_packed_workspace_size(976, 65536, 4096) == 0
-    assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 1024) == 0
+    # K split only for few blocks and long K: 4 ranges of the 64-block 4096 x 11008 product,
+    # none for the 256-block LM head or shorter K
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 11008) == 3 * 976 * 4096 * 4
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 65536, 11008) == 0
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 4096) == 0
     assert L.adt_gemm_bf16(fake, 64, fake, 64, 8, 100, 64, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 96, fake, 96, 8, 128, 96, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 32, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_SHAPE

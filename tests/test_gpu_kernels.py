@@ -352,11 +352,11 @@ def test_gemm_bf16_batched(rt, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192),
-                                   (300, 512, 4096), (40, 1024, 2112), (130, 384, 320), (976, 3840, 1280)])
+                                   (300, 512, 8192), (40, 1024, 8256), (130, 384, 320), (976, 3840, 1280)])
 def test_gemm_bf16_packed(rt, M, N, K):
     """Packed weights: the DMA pipeline in 256 x 256 blocks (>= 128 of them; K below and above
     the stages it keeps in flight; one row; partial row blocks), with K split over 4
-    workgroups per block (few blocks, long K; uneven ranges at K = 2112), and in 128 x 128
+    workgroups per block (few blocks, long K; uneven ranges at K = 8256), and in 128 x 128
     blocks of four waves (few blocks, short K: the narrow projections of a batch of trees),
     every element.  Without a K split the result equals the row-major
     kernel bit for bit (same summation order); the split result is checked against the bound
@@ -369,7 +369,7 @@ def test_gemm_bf16_packed(rt, M, N, K):
     got = rt.gemm_bf16_packed(xt, wp, N)
     _gemm_ref_check(got.cpu().numpy(), xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
     split = rt.lib().adt_gemm_bf16_packed_workspace_size(M, N, K) > 0
-    assert split == (K >= 2048)
+    assert split == (K >= 8192)
     ref = rt.gemm_bf16(xt, wt)
     if split:
         assert torch.equal(rt.gemm_bf16_packed(xt, wp, N, split=False), ref)
@@ -380,8 +380,8 @@ def test_gemm_bf16_packed(rt, M, N, K):
 
 def test_gemm_bf16_packed_verify_shapes_sampled(rt):
     """M = 976 (16 trees of 61 rows) with the 7B-shaped projections the benchmark times, on
-    sampled rows: QKV 4096 x 12288 and the LM head 4096 x 65536 (DMA pipeline), O 4096 x 4096
-    and down 11008 x 4096 (DMA pipeline with K split in four)."""
+    sampled rows: QKV 4096 x 12288 and the LM head 4096 x 65536 (DMA pipeline, 256 x 256), O
+    4096 x 4096 (128 x 128) and down 11008 x 4096 (256 x 256 with K split in four)."""
     rng = np.random.default_rng(977)
     rows = np.array([0, 1, 31, 32, 255, 256, 511, 767, 768, 900, 975])
     for K, N in ((4096, 12288), (4096, 65536), (4096, 4096), (11008, 4096)):
