@@ -497,6 +497,8 @@ struct adt_session_s {
   void* acc_ws;
   size_t acc_ws_bytes;
   uint64_t* samp_w = nullptr;   // stochastic children: [KR][V] q weights of a level's rows
+  // pinned host staging of an acceptance's readback: path [R], tokens [R], a, bonus
+  int32_t* h_acc = nullptr;
   // HIP graphs of the forwards, keyed by shape; captured on a private stream, replayed on
   // the caller's stream.
   bool graphs = true;
@@ -505,6 +507,7 @@ struct adt_session_s {
   ~adt_session_s() {
     for (auto& kv : gexec) (void)hipGraphExecDestroy(kv.second);
     if (cap) (void)hipStreamDestroy(cap);
+    if (h_acc) (void)hipHostFree(h_acc);
   }
 };
 
@@ -1156,21 +1159,38 @@ extern "C" adt_status adt_verify_forward(adt_session* s, void* stream) {
                         gkey(1, 0, 0, n));
 }
 
+// Acceptance on the last verify and the readback of its result into the session's pinned
+// staging (asynchronous on st); accept_finish commits once st has been synchronised.
+static adt_status accept_launch(adt_session_s* s, hipStream_t st) {
+  const int n = s->n_nodes;
+  if (!s->h_acc) ADT_HIP(hipHostMalloc((void**)&s->h_acc, sizeof(int32_t) * (2 * R + 2), hipHostMallocDefault));
+  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, session_accept_cfg(s),
+                  (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
+  ADT_HIP(hipMemcpyAsync(s->h_acc, s->tr.path, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(s->h_acc + R, s->tr.token, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(s->h_acc + 2 * R, s->tr.nacc, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(s->h_acc + 2 * R + 1, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  return ADT_OK;
+}
+
+static adt_status accept_finish(adt_session_s* s, int32_t d_hat, int32_t k_hat, adt_step_out* out, hipStream_t st);
+
 extern "C" adt_status adt_session_accept_commit(adt_session* s, int32_t d_hat, int32_t k_hat, adt_step_out* out,
                                                 void* stream) {
   ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "accept_commit: null session");
   ADT_CHECK_ARG(s->prefilled && s->n_nodes >= 1, ADT_E_STATE, "accept_commit: no verified tree");
   hipStream_t st = (hipStream_t)stream;
-  const int n = s->n_nodes, L = s->L, P = s->P;
-  TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, session_accept_cfg(s),
-                  (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
-  std::vector<int32_t> path(R), tok(R);
-  int32_t a = 0, bonus = 0;
-  ADT_HIP(hipMemcpyAsync(path.data(), s->tr.path, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(tok.data(), s->tr.token, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(&a, s->tr.nacc, sizeof(int32_t), hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(&bonus, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  TRY(accept_launch(s, st));
   TRY(sync_stream(st));
+  return accept_finish(s, d_hat, k_hat, out, st);
+}
+
+// c + d1 after the acceptance's readback has landed: compaction, catch-up features, records
+static adt_status accept_finish(adt_session_s* s, int32_t d_hat, int32_t k_hat, adt_step_out* out, hipStream_t st) {
+  const int n = s->n_nodes, L = s->L, P = s->P;
+  const int32_t* path = s->h_acc;
+  const int32_t* tok = s->h_acc + R;
+  const int32_t a = s->h_acc[2 * R], bonus = s->h_acc[2 * R + 1];
   ADT_CHECK_ARG(a >= 0 && a < n, ADT_E_STATE, "accept_commit: accepted length %d out of range", a);
   // Catch-up features are kept for committed positions Ld-1 .. L_new-1.  After an expansion
   // the draft cache covers the root, so the next catch-up starts at L + 1.
@@ -1480,19 +1500,33 @@ extern "C" adt_status adt_batch_step(adt_batch* bt, adt_step_out* outs, void* st
     ADT_HIP(hipMemcpyAsync(bt->nq, n.data(), sizeof(int32_t) * B, hipMemcpyHostToDevice, st));
     TRY(batch_forward(bt, M, nq_max, st));
   }
-  // each session accepts and commits from its own rows
+  // each session accepts from its own rows: every acceptance first (on the auxiliary streams,
+  // after the forward), one synchronisation, then each session commits
   for (int b = 0; b < B; ++b) {
     adt_session_s* s = bt->ss[b];
+    if (!active[b]) continue;
+    ADT_HIP(hipMemcpyAsync(s->logits, bt->C + (size_t)off[b] * s->V, sizeof(float) * s->V * n[b],
+                           hipMemcpyDeviceToDevice, st));
+    ADT_HIP(hipMemcpyAsync(s->feat, (char*)bt->feat + (size_t)off[b] * s->dm * 2, (size_t)s->dm * 2 * n[b],
+                           hipMemcpyDeviceToDevice, st));
+  }
+  ADT_HIP(hipEventRecord(bt->ev_fork, st));
+  for (int j = 0; j < NS; ++j) ADT_HIP(hipStreamWaitEvent(bt->aux[j], bt->ev_fork, 0));
+  for (int b = 0; b < B && fail == ADT_OK; ++b)
+    if (active[b]) fail = accept_launch(bt->ss[b], bt->aux[b % NS]);
+  for (int j = 0; j < NS; ++j) {
+    ADT_HIP(hipEventRecord(bt->ev_join[j], bt->aux[j]));
+    ADT_HIP(hipStreamWaitEvent(st, bt->ev_join[j], 0));
+  }
+  if (fail != ADT_OK) return fail;
+  TRY(sync_stream(st));
+  for (int b = 0; b < B; ++b) {
     if (!active[b]) {
       memset(&outs[b], 0, sizeof(outs[b]));
       outs[b].done = 1;
       continue;
     }
-    ADT_HIP(hipMemcpyAsync(s->logits, bt->C + (size_t)off[b] * s->V, sizeof(float) * s->V * n[b],
-                           hipMemcpyDeviceToDevice, st));
-    ADT_HIP(hipMemcpyAsync(s->feat, (char*)bt->feat + (size_t)off[b] * s->dm * 2, (size_t)s->dm * 2 * n[b],
-                           hipMemcpyDeviceToDevice, st));
-    TRY(adt_session_accept_commit(s, dh[b], kh[b], &outs[b], st));
+    TRY(accept_finish(bt->ss[b], dh[b], kh[b], &outs[b], st));
   }
   return ADT_OK;
 }
