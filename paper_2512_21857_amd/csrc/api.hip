@@ -263,7 +263,7 @@ extern "C" adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, i
 
 extern "C" size_t adt_gemm_bf16_packed_workspace_size(int32_t M, int32_t N, int32_t K) {
   if (M < 1 || N < 256 || N % 256 != 0 || K < 64) return 0;
-  return (size_t)(gemm_nt_ksplit(M, N, K, SIZE_MAX) - 1) * M * N * sizeof(float);
+  return gemm_nt_part_elems(M, N, K) * sizeof(float);
 }
 
 extern "C" adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K,

@@ -163,8 +163,8 @@ constexpr int DMA_NSTAGE = 5;
 // workgroup: range 0 writes C, range s > 0 writes the fp32 partial P[s-1] ([M][N], row stride
 // N), and gemm_nt_reduce_kernel adds them to C in range order (deterministic).
 // BN x BM block of C^T per workgroup of WN x WM waves (each a (BN/WN) x (BM/WM) part of 32x32
-// MFMA blocks); a stage slot holds (BN + BM) / 16 tiles, four per wave: 256 x 256 with 2 x 4
-// waves, or 128 x 128 with 2 x 2 (two workgroups per CU).
+// MFMA blocks); a stage slot holds (BN + BM) / 16 tiles, four per wave: 256 x 256 or
+// 384 x 128 with 2 x 4 or 4 x 2 waves, or 128 x 128 with 2 x 2 (two workgroups per CU).
 template <int BN, int BM, int WN, int WM, int NSTAGE>
 __global__ __launch_bounds__(WN * WM * WAVE) void gemm_nt_dma_kernel(const uint16_t* __restrict__ X, int64_t ldx,
                                                                      const uint16_t* __restrict__ W, int M, int N,
@@ -295,16 +295,71 @@ __global__ void gemm_nt_reduce_kernel(float* __restrict__ C, int64_t ldc, const 
   }
 }
 
-// K ranges per 256 x 256 block for the DMA pipeline: 1, or (blocks under 128, K >= 8192 so
-// the partials' traffic stays small beside the product; shorter K runs faster in 128 x 128
-// blocks, measured at 976 x 4096 x 4096) 4, else 2, as far as part_elems holds the extra
-// ranges' partials.
-int gemm_nt_ksplit(int M, int N, int K, size_t part_elems) {
-  const int64_t tiles = (int64_t)((M + 255) / 256) * (N / 256);
-  if (tiles >= 128 || K < 8192) return 1;
-  for (int ks = 4; ks >= 2; ks /= 2)
-    if ((size_t)(ks - 1) * M * N <= part_elems && K / 32 >= 4 * ks) return ks;
-  return 1;
+// Plan of the packed path on the DMA pipeline.  A 256 x 256 (or 384 x 128) workgroup takes
+// a whole CU by LDS, so the blocks run in rounds of DMA_SLOTS.
+//  * few 256 x 256 blocks (under 128) with K >= 8192: K split over ksplit = 4 (else 2)
+//    workgroups per block, as far as the partials fit (the partials' traffic stays small
+//    beside the product; shorter K runs faster in 128 x 128 blocks, measured at
+//    976 x 4096 x 4096);
+//  * one partial round of 256 x 256 blocks that 384 x 128 blocks fill further (N a multiple
+//    of 384): those, at three quarters of the work per block;
+//  * more than one round whose last is at most half full: the columns of the full rounds in
+//    one launch, the rest in a second launch with K split over as many workgroups per block
+//    as one round holds (at most 4), then the fixed-order reduce of their partials.
+constexpr int DMA_SLOTS = 256;
+struct NtPlan {
+  int bn = 256;      // 256 (256 x 256 blocks) or 384 (384 x 128)
+  int ksplit = 1;    // K ranges per block of the (first) launch
+  int n_tail = 0;    // columns run by the second launch
+  int tail_ks = 1;   // K ranges per block of the second launch
+  size_t part = 0;   // fp32 partials used
+};
+static NtPlan gemm_nt_plan(int M, int N, int K, size_t part_elems) {
+  NtPlan p;
+  const int mt = (M + 255) / 256, nb = N / 256, kt = K / 32;
+  const int64_t tiles = (int64_t)mt * nb;
+  if (tiles < 128 && K >= 8192) {
+    for (int ks = 4; ks >= 2; ks /= 2)
+      if ((size_t)(ks - 1) * M * N <= part_elems && kt >= 4 * ks) {
+        p.ksplit = ks;
+        p.part = (size_t)(ks - 1) * M * N;
+        return p;
+      }
+    return p;
+  }
+  if (N % 384 == 0 && tiles >= 128 && tiles < DMA_SLOTS) {
+    const int64_t t384 = (int64_t)((M + 127) / 128) * (N / 384);
+    if (t384 > tiles && t384 <= DMA_SLOTS) p.bn = 384;
+    return p;
+  }
+  if (tiles > DMA_SLOTS && tiles % DMA_SLOTS != 0 && tiles % DMA_SLOTS <= DMA_SLOTS / 2) {
+    const int nb_main = (int)(tiles / DMA_SLOTS * DMA_SLOTS / mt);
+    const int tail_tiles = mt * (nb - nb_main);
+    const int ks = std::min(4, DMA_SLOTS / tail_tiles);
+    const size_t need = (size_t)(ks - 1) * M * (nb - nb_main) * 256;
+    if (ks >= 2 && kt >= 4 * ks && need <= part_elems) {
+      p.n_tail = (nb - nb_main) * 256;
+      p.tail_ks = ks;
+      p.part = need;
+    }
+  }
+  return p;
+}
+
+size_t gemm_nt_part_elems(int M, int N, int K) { return gemm_nt_plan(M, N, K, SIZE_MAX).part; }
+
+// One launch of 256 x 256 DMA blocks over columns [0, N) of the operands given (W already
+// offset to the first column's packed tile), K split ks ways with the partials reduced.
+static void launch_dma256(const uint16_t* x, int64_t ldx, const uint16_t* w, int M, int N, int K, float* C,
+                          int64_t ldc, int ks, float* part, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  hipExtLaunchKernelGGL((gemm_nt_dma_kernel<256, 256, 2, 4, DMA_NSTAGE>), dim3((M + 255) / 256 * (N / 256) * ks),
+                        dim3(8 * WAVE), 0, st, ev0, ks > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc, ks, part);
+  if (ks > 1) {
+    const int64_t quads = (int64_t)M * (N / 4);
+    const int blocks = (int)std::min<int64_t>((quads + 255) / 256, 4096);
+    hipExtLaunchKernelGGL(gemm_nt_reduce_kernel, dim3(blocks), dim3(256), 0, st, nullptr, ev1, 0, C, ldc,
+                          (const float*)part, M, N, ks - 1);
+  }
 }
 
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
@@ -321,23 +376,29 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
   const int best = (N % 256 == 0 && (int64_t)(N / 256) * ((M + 255) / 256) >= 256) ? 0 : 2;
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)W;
-  // Packed weights in 256 x 256 blocks when that gives at least 128 workgroups (half the CUs;
-  // measured faster than the 128 x 128 blocks down to there), if need be with K split across
-  // workgroups: the DMA pipeline.
-  const int ksplit = (packed && N % 256 == 0 && part) ? gemm_nt_ksplit(M, N, K, part_elems) : 1;
-  if (packed && N % 256 == 0 && (ksplit > 1 || (int64_t)(N / 256) * ((M + 255) / 256) >= 128)) {
-    hipExtLaunchKernelGGL((gemm_nt_dma_kernel<256, 256, 2, 4, DMA_NSTAGE>),
-                          dim3((M + 255) / 256 * (N / 256) * ksplit), dim3(8 * WAVE), 0, st, ev0,
-                          ksplit > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc, ksplit, part);
-    ADT_LAUNCH_CHECK();
-    if (ksplit > 1) {
-      const int64_t quads = (int64_t)M * (N / 4);
-      const int blocks = (int)std::min<int64_t>((quads + 255) / 256, 4096);
-      hipExtLaunchKernelGGL(gemm_nt_reduce_kernel, dim3(blocks), dim3(256), 0, st, nullptr, ev1, 0, C, ldc,
-                            (const float*)part, M, N, ksplit - 1);
+  // Packed weights in 256 x 256 (or 384 x 128) blocks when that gives at least 128
+  // workgroups (half the CUs; measured faster than the 128 x 128 blocks down to there), or
+  // with K split across workgroups: the DMA pipeline, as planned above.
+  if (packed && N % 256 == 0) {
+    const NtPlan p = gemm_nt_plan(M, N, K, part ? part_elems : 0);
+    if (p.bn == 384) {
+      hipExtLaunchKernelGGL((gemm_nt_dma_kernel<384, 128, 4, 2, DMA_NSTAGE>),
+                            dim3((M + 127) / 128 * (N / 384)), dim3(8 * WAVE), 0, st, ev0, ev1, 0, x, ldx, w, M, N, K,
+                            C, ldc, 1, nullptr);
       ADT_LAUNCH_CHECK();
+      return ADT_OK;
     }
-    return ADT_OK;
+    if (p.ksplit > 1 || (int64_t)(N / 256) * ((M + 255) / 256) >= 128) {
+      const int n_main = N - p.n_tail;
+      launch_dma256(x, ldx, w, M, n_main, K, C, ldc, p.ksplit, part, st, ev0, p.n_tail ? nullptr : ev1);
+      ADT_LAUNCH_CHECK();
+      if (p.n_tail) {
+        launch_dma256(x, ldx, w + (int64_t)(n_main / 16) * (K / 32) * 512, M, p.n_tail, K, C + n_main, ldc, p.tail_ks,
+                      part, st, nullptr, ev1);
+        ADT_LAUNCH_CHECK();
+      }
+      return ADT_OK;
+    }
   }
   // Packed weights with fewer blocks (the narrow projections of a batch of trees): 128 x 128
   // blocks of four waves through the same DMA pipeline, two workgroups per CU.

@@ -80,11 +80,11 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
 // gemm_nt.hip: C[M][N] fp32 = X[M][K] . W[N][K]^T, bf16 row-major operands (MFMA-bound batches)
 // (packed: W in the adt_pack_weight layout, ldw unused; rows in the packed order)
 // part: fp32 scratch of part_elems for K-split partials of the packed path (null: no split);
-// gemm_nt_ksplit gives the split it uses.
+// gemm_nt_part_elems gives what the packed path's plan uses with unlimited scratch.
 adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw, int M, int N, int K, float* C,
                           int64_t ldc, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
                           bool packed = false, float* part = nullptr, size_t part_elems = 0);
-int gemm_nt_ksplit(int M, int N, int K, size_t part_elems);
+size_t gemm_nt_part_elems(int M, int N, int K);
 // rows.hip
 // h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
 // of squares of h into ssp[m][d/16].

@@ -67,6 +67,11 @@ def test_argument_errors_return_codes_without_launching(L):
     assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 11008) == 3 * 976 * 4096 * 4
     assert L.adt_gemm_bf16_packed_workspace_size(976, 65536, 11008) == 0
     assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 4096) == 0
+    # 344 blocks of 256 x 256: the last 22 column blocks (88 blocks) split two ways
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 22016, 4096) == 976 * 22 * 256 * 4
+    # 192 blocks of 256 x 256 become 256 of 384 x 128: no partials
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 12288, 4096) == 0
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 32000, 4096) == 0
     assert L.adt_gemm_bf16(fake, 64, fake, 64, 8, 100, 64, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 96, fake, 96, 8, 128, 96, fake, 128, None) == abi.E_SHAPE
     assert L.adt_gemm_bf16(fake, 32, fake, 64, 8, 128, 64, fake, 128, None) == abi.E_SHAPE

@@ -352,15 +352,20 @@ def test_gemm_bf16_batched(rt, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192),
-                                   (300, 512, 8192), (40, 1024, 8256), (130, 384, 320), (976, 3840, 1280)])
+                                   (300, 512, 8192), (40, 1024, 8256), (130, 384, 320), (976, 3840, 1280),
+                                   (976, 12288, 512), (300, 35840, 512), (976, 22016, 320)])
 def test_gemm_bf16_packed(rt, M, N, K):
     """Packed weights: the DMA pipeline in 256 x 256 blocks (>= 128 of them; K below and above
     the stages it keeps in flight; one row; partial row blocks), with K split over 4
     workgroups per block (few blocks, long K; uneven ranges at K = 8256), and in 128 x 128
     blocks of four waves (few blocks, short K: the narrow projections of a batch of trees),
-    every element.  Without a K split the result equals the row-major
-    kernel bit for bit (same summation order); the split result is checked against the bound
-    and, with the workspace withheld, the unsplit result is the row-major one again."""
+    in 384 x 128 blocks (976 x 12288: 256 of them against 192 of 256 x 256), and with a last
+    round of blocks at most half full moved to a second launch with K split (35840 columns
+    over 2 row blocks: 256 + 24 blocks, the 24 split four ways; 22016 over 4: 256 + 88, split
+    two ways), every element.  Without a K split the result
+    equals the row-major kernel bit for bit (same summation order); the split result is
+    checked against the bound and, with the workspace withheld, the unsplit result is the
+    row-major one again."""
     print(f"gemm_bf16_packed M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M * 7 + N + K)
     xt = torch.from_numpy(rng.standard_normal((M, K)).astype(np.float32)).cuda().bfloat16()
@@ -369,7 +374,7 @@ def test_gemm_bf16_packed(rt, M, N, K):
     got = rt.gemm_bf16_packed(xt, wp, N)
     _gemm_ref_check(got.cpu().numpy(), xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
     split = rt.lib().adt_gemm_bf16_packed_workspace_size(M, N, K) > 0
-    assert split == (K >= 8192)
+    assert split == (K >= 8192 or N in (35840, 22016))
     ref = rt.gemm_bf16(xt, wt)
     if split:
         assert torch.equal(rt.gemm_bf16_packed(xt, wp, N, split=False), ref)
