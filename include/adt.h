@@ -198,8 +198,9 @@ adt_status adt_gemm_bf16(const void* X, int64_t ldx, const void* W, int64_t ldw,
  * which K is split across 2-4 workgroups per output block for a product of few blocks and
  * long K (K >= 8192), or for the columns of a last, at most half-full round of blocks, and
  * the fp32 partials are added to C in a fixed order (deterministic; rounding then differs
- * from the unsplit product by the reassociation of the K sum).  With a NULL or smaller
- * workspace nothing is split.  Shapes, errors and asynchrony as adt_gemm_bf16. */
+ * from the unsplit product by the reassociation of the K sum).  A NULL workspace splits
+ * nothing; a smaller one splits only as far as it holds the partials.  Shapes, errors and
+ * asynchrony as adt_gemm_bf16. */
 size_t adt_gemm_bf16_packed_workspace_size(int32_t M, int32_t N, int32_t K);
 adt_status adt_gemm_bf16_packed(const void* X, int64_t ldx, const void* Wp, int32_t M, int32_t N, int32_t K, float* C,
                                 int64_t ldc, void* workspace, size_t workspace_bytes, void* stream);
