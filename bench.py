@@ -153,6 +153,45 @@ def attn_microbench(rt, sizes=(8, 16, 32, 64, 128), iters=30, sets=3):
     return out
 
 
+def compact_microbench(rt, B=16, layers=36, heads=20, Dh=64, a=6, nodes=61, iters=30):
+    """KV compaction alone at the LlamaGen-XL cache shape (16 sequences x 36 layers x 20
+    heads, head size 64, bf16), every sequence committing a = 6 accepted nodes of a 61-node
+    tree (path[m] an increasing draw from the tree's slots).  Call i moves its rows at prefix
+    lengths shifted by i trees, so the rows it touches are not in the last-level cache."""
+    import torch
+    slices, step = layers * heads, nodes + 8
+    rng = np.random.default_rng(17)
+    base = rng.integers(256, 513, size=B)
+    S_cap = int(base.max()) + step * (iters + 3) + nodes
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(17)
+    k = torch.randn((B, slices, S_cap, Dh), generator=gen, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn((B, slices, S_cap, Dh), generator=gen, device="cuda", dtype=torch.bfloat16)
+    path = np.zeros((B, a + 1), np.int32)
+    for b in range(B):
+        path[b, 1:] = np.sort(rng.choice(np.arange(1, nodes), size=a, replace=False))
+    path_t = torch.from_numpy(path).cuda()
+    n_acc = torch.full((B,), a, dtype=torch.int32, device="cuda")
+    lens = [torch.from_numpy((base + step * i).astype(np.int32)).cuda() for i in range(iters + 3)]
+    for i in range(3):
+        rt.kv_compact(k, v, lens[iters + i], path_t, n_acc, a)
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for i in range(iters):
+        rt.kv_compact(k, v, lens[i], path_t, n_acc, a)
+    e1.record(st)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    byts = 2.0 * 2 * B * slices * a * Dh * 2   # K and V rows, each read once and written once
+    gbs = byts / (ms * 1e-3) / 1e9
+    del k, v
+    torch.cuda.empty_cache()
+    return {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "bytes": int(byts), "workload": f"{B} sequences x {layers} layers x {heads} heads x {Dh}, "
+            f"{a} accepted nodes of {nodes} per sequence, bf16"}
+
+
 MFMA_PEAK_TFLOPS = 2500.0
 BATCHED_SHAPES = ((4096, 12288), (4096, 4096), (4096, 22016), (11008, 4096), (4096, 65536))
 
@@ -337,6 +376,7 @@ def main():
     a = prof["attn"]
     attn_gbs = a["bytes"] / (a["ms"] * 1e-3) / 1e9 if a["ms"] > 0 else 0.0
     micro = {} if args.no_microbench else attn_microbench(rt)
+    compact = None if args.no_microbench else compact_microbench(rt)
     mfma = None if args.no_mfma else mfma_benchmark(rt)
     guided = None if args.no_guided else guided_run(min(args.steps, 50))
     stochastic = None if args.no_stochastic else stochastic_run(min(args.steps, 50))
@@ -369,6 +409,7 @@ def main():
         "tree_attn": {"in_cycle_GB_s": round(attn_gbs, 1), "in_cycle_frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                       "in_cycle_avg_us": round(a["ms"] / max(a["launches"], 1) * 1e3, 3),
                       "microbench_16x32x128": micro},
+        "kv_compact": compact,
         "batched_verify_gemm": mfma,
         "guided": guided,
         "batched": batched,

@@ -111,7 +111,8 @@ adt_status adt_tree_masks(const int32_t* parent, const int32_t* n_nodes, int32_t
  * (BFS order of an accepted chain) so every source is at or after its destination; all
  * reads of a slice happen before its writes.  Both K and V caches are compacted.
  * Slice s of sequence b starts at base + b*stride_b + s*stride_slice; rows are Dh long.
- * n_acc[b] <= a_max <= ADT_MAX_NODES - 1. */
+ * n_acc[b] <= a_max <= ADT_MAX_NODES - 1, and a_max rows of one slice at most 64 KB
+ * (a_max * Dh * element size <= 65536; ADT_E_UNSUPPORTED otherwise). */
 adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, int32_t slices, int32_t Dh, int64_t stride_b,
                           int64_t stride_slice, const int32_t* kv_len, const int32_t* path, int32_t path_stride,
                           const int32_t* n_acc, int32_t a_max, int32_t dtype, void* stream);

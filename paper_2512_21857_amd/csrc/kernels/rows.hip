@@ -4,6 +4,8 @@
 // append, SwiGLU, logits), feature gathers, KV compaction and ancestor masks.  Each kernel
 // handles whole rows (at most 128 tree rows per launch), so they are latency-bound and kept
 // as simple as possible.
+#include <algorithm>
+
 #include "../launch.h"
 
 namespace adt {
@@ -281,41 +283,48 @@ __global__ void gather_rows_kernel(const T* __restrict__ src, const int32_t* __r
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[(int64_t)i * d + c] = s[c];
 }
 
-// KV compaction: one block per (slice, sequence).  Reads every moved row into registers,
-// then writes them, so in-place moves never read a row already overwritten.
+// KV compaction: one block per (group of G slices, sequence); piece p of a block is 16
+// bytes of row m of slice p / pps of the group (pps = a_max rows of 16-byte pieces).  Every
+// moved row of a slice is read into registers before any is written (one barrier), so
+// in-place moves never read a row already overwritten; a slice never spans two blocks.
 template <typename T, int ROWS_MAX>
 __global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__ kc, T* __restrict__ vc, int Dh,
                                                                  int64_t stride_b, int64_t stride_s,
                                                                  const int32_t* __restrict__ kv_len, int kv_stride,
                                                                  const int32_t* __restrict__ path, int path_stride,
                                                                  const int32_t* __restrict__ n_acc, int acc_stride,
-                                                                 int a_max) {
-  const int sl = blockIdx.x, b = blockIdx.y;
+                                                                 int a_max, int slices, int G) {
+  const int b = blockIdx.y, s0 = blockIdx.x * G;
   const int a = min(n_acc[b * acc_stride], a_max);
   const int L = kv_len[b * kv_stride];
   const int per_row = Dh * (int)sizeof(T) / 16;        // 16-byte pieces per row
-  const int pieces = a * per_row;
+  const int pps = a_max * per_row;                     // pieces per slice
+  const int total = G * pps;
   u16x8 kr[ROWS_MAX], vr[ROWS_MAX];
-  T* kb = kc + b * stride_b + sl * stride_s;
-  T* vb = vc + b * stride_b + sl * stride_s;
 #pragma unroll
   for (int it = 0; it < ROWS_MAX; ++it) {
     const int p = threadIdx.x + it * ROW_THREADS;
-    if (p < pieces) {
-      const int m = p / per_row + 1, c = p % per_row;
-      const int src = path[(int64_t)b * path_stride + m];
-      kr[it] = reinterpret_cast<const u16x8*>(kb + (int64_t)(L + src) * Dh)[c];
-      vr[it] = reinterpret_cast<const u16x8*>(vb + (int64_t)(L + src) * Dh)[c];
+    if (p < total) {
+      const int sl = s0 + p / pps, w = p % pps, m = w / per_row + 1, c = w % per_row;
+      if (sl < slices && m <= a) {
+        const int src = path[(int64_t)b * path_stride + m];
+        const int64_t off = b * stride_b + sl * stride_s + (int64_t)(L + src) * Dh;
+        kr[it] = reinterpret_cast<const u16x8*>(kc + off)[c];
+        vr[it] = reinterpret_cast<const u16x8*>(vc + off)[c];
+      }
     }
   }
   __syncthreads();
 #pragma unroll
   for (int it = 0; it < ROWS_MAX; ++it) {
     const int p = threadIdx.x + it * ROW_THREADS;
-    if (p < pieces) {
-      const int m = p / per_row + 1, c = p % per_row;
-      reinterpret_cast<u16x8*>(kb + (int64_t)(L + m) * Dh)[c] = kr[it];
-      reinterpret_cast<u16x8*>(vb + (int64_t)(L + m) * Dh)[c] = vr[it];
+    if (p < total) {
+      const int sl = s0 + p / pps, w = p % pps, m = w / per_row + 1, c = w % per_row;
+      if (sl < slices && m <= a) {
+        const int64_t off = b * stride_b + sl * stride_s + (int64_t)(L + m) * Dh;
+        reinterpret_cast<u16x8*>(kc + off)[c] = kr[it];
+        reinterpret_cast<u16x8*>(vc + off)[c] = vr[it];
+      }
     }
   }
 }
@@ -467,16 +476,22 @@ adt_status launch_kv_compact(void* k, void* v, int B, int slices, int Dh, int64_
                              int a_max, int dtype, hipStream_t st) {
   const int bytes_row = Dh * (dtype == ADT_BF16 ? 2 : 4);
   ADT_CHECK_ARG(bytes_row % 16 == 0, ADT_E_SHAPE, "kv_compact: row of %d bytes not a multiple of 16", bytes_row);
-  const int pieces = a_max * bytes_row / 16;
-  dim3 grid(slices, B);
+  const int pieces = a_max * bytes_row / 16;   // per slice
+  ADT_CHECK_ARG(pieces <= 16 * ROW_THREADS, ADT_E_UNSUPPORTED,
+                "kv_compact: %d accepted rows of %d bytes exceed one block's %d-byte staging", a_max, bytes_row,
+                16 * ROW_THREADS * 16);
+  // as many whole slices per block as its registers hold (one slice when a slice fills them)
+  const int rm = pieces <= 4 * ROW_THREADS ? 4 : 16;
+  const int G = std::max(1, std::min(slices, rm * ROW_THREADS / std::max(pieces, 1)));
+  dim3 grid((slices + G - 1) / G, B);
 #define ADT_COMPACT(T, RM)                                                                                        \
   kv_compact_kernel<T, RM><<<grid, ROW_THREADS, 0, st>>>((T*)k, (T*)v, Dh, sb, ss, kv_len, kv_stride, path,       \
-                                                         path_stride, n_acc, acc_stride, a_max)
+                                                         path_stride, n_acc, acc_stride, a_max, slices, G)
   if (dtype == ADT_BF16) {
-    if (pieces <= 4 * ROW_THREADS) ADT_COMPACT(uint16_t, 4);
+    if (rm == 4) ADT_COMPACT(uint16_t, 4);
     else ADT_COMPACT(uint16_t, 16);
   } else {
-    if (pieces <= 4 * ROW_THREADS) ADT_COMPACT(float, 4);
+    if (rm == 4) ADT_COMPACT(float, 4);
     else ADT_COMPACT(float, 16);
   }
 #undef ADT_COMPACT

@@ -46,6 +46,8 @@ def test_argument_errors_return_codes_without_launching(L):
     assert L.adt_tree_attn(fake, fake, fake, 0, 64 * 10, fake, fake, fake, fake, 1, 1, 64, 129, 10, 1.0, 1, fake, fake,
                            0, None) == abi.E_CAPACITY
     assert L.adt_kv_compact(fake, fake, 1, 1, 64, 0, 64, fake, fake, 4, fake, 200, 1, None) == abi.E_CAPACITY
+    # 100 accepted fp32 rows of 1024 (400 KB per slice) exceed one block's staging
+    assert L.adt_kv_compact(fake, fake, 1, 1, 1024, 0, 1024, fake, fake, 101, fake, 100, 0, None) == abi.E_UNSUPPORTED
     assert L.adt_tree_masks(fake, fake, 1, 300, fake, None, None) == abi.E_CAPACITY
     cfg = abi.AcceptCfg(7, 1.0, 0, 0.0, 1, 0, 0, None, 0)
     import ctypes as C
