@@ -1290,6 +1290,8 @@ struct adt_batch_s {
   uint64_t* mask;
   void* attn_ws = nullptr;
   size_t attn_ws_bytes = 0;
+  float* gemm_part = nullptr;   // fp32 partials of the projections' K splits
+  size_t gemm_part_elems = 0;
   // The sessions' draft expansions are independent chains of small kernels; they run on
   // BATCH_STREAMS streams of their own (default priority), joined to the caller's stream by
   // events, so several overlap on the GPU.
@@ -1357,6 +1359,14 @@ static size_t batch_layout(adt_batch_s* bt, const adt_session_s* s0, char* base)
   bt->mask = b.take<uint64_t>((size_t)M * ADT_MASK_WORDS);
   bt->attn_ws_bytes = tree_attn_ws_bytes(bt->B, s0->H, s0->Dh, R, s0->d.s_cap, s0->dt);
   bt->attn_ws = b.take<char>(std::max<size_t>(bt->attn_ws_bytes, 256));
+  // scratch for the K splits the packed-GEMM plan takes, at the most any row count needs
+  const int F = s0->F;
+  const int shapes[5][2] = {{3 * dm, dm}, {dm, dm}, {2 * F, dm}, {dm, F}, {s0->V, dm}};
+  size_t part = 0;
+  for (int m = 1; m <= M; ++m)
+    for (const auto& sh : shapes) part = std::max(part, gemm_nt_part_elems(m, sh[0], sh[1]));
+  bt->gemm_part_elems = part;
+  bt->gemm_part = part ? b.take<float>(part) : nullptr;
   return align_up(b.off, 256);
 }
 
@@ -1399,10 +1409,11 @@ extern "C" adt_status adt_batch_create(adt_session* const* sessions, int32_t B, 
 extern "C" void adt_batch_destroy(adt_batch* b) { delete b; }
 
 // The batched GEMM over packed weights, timed like the single-tree projections.
-static adt_status gemm_b(const void* X, int ldx, const void* W, int M, int N, int K, float* C, hipStream_t st) {
+static adt_status gemm_b(const adt_batch_s* bt, const void* X, int ldx, const void* W, int M, int N, int K,
+                         hipStream_t st) {
   const int e = prof_pair();
-  adt_status r = launch_gemm_nt(X, ldx, W, 0, M, N, K, C, N, st, e >= 0 ? g_prof.ev[e] : nullptr,
-                                e >= 0 ? g_prof.ev[e + 1] : nullptr, true);
+  adt_status r = launch_gemm_nt(X, ldx, W, 0, M, N, K, bt->C, N, st, e >= 0 ? g_prof.ev[e] : nullptr,
+                                e >= 0 ? g_prof.ev[e + 1] : nullptr, true, bt->gemm_part, bt->gemm_part_elems);
   prof_done(e, ADT_PROF_GEMM, (double)N * K * 2.0 + (double)M * K * 2.0 + (double)M * N * 4.0, 2.0 * M * N * K);
   return r;
 }
@@ -1422,7 +1433,7 @@ static adt_status batch_forward(adt_batch_s* bt, int M, int nq_max, hipStream_t 
   for (int l = 0; l < s0->Lr; ++l) {
     char* kc = (char*)s0->d.k_cache + (size_t)l * H * stride_h * 2;
     char* vc = (char*)s0->d.v_cache + (size_t)l * H * stride_h * 2;
-    TRY(gemm_b(bt->a, dm, m->qkv[l], M, 3 * dm, dm, bt->C, st));
+    TRY(gemm_b(bt, bt->a, dm, m->qkv[l], M, 3 * dm, dm, st));
     TRY(launch_qkv_rows(bt->C, M, H, Dh, bt->pos, bt->slot, bt->seq, s0->rope, bt->q, kc, vc, stride_h, bt->cache_sb,
                         dt, st));
     const int e = prof_pair();
@@ -1431,14 +1442,14 @@ static adt_status batch_forward(adt_batch_s* bt, int M, int nq_max, hipStream_t 
                          bt->attn_ws, bt->attn_ws_bytes, st, e >= 0 ? g_prof.ev[e] : nullptr,
                          e >= 0 ? g_prof.ev[e + 1] : nullptr));
     prof_done(e, ADT_PROF_ATTN, 0.0, 0.0);
-    TRY(gemm_b(bt->att, dm, m->o[l], M, dm, dm, bt->C, st));
+    TRY(gemm_b(bt, bt->att, dm, m->o[l], M, dm, dm, st));
     TRY(launch_add_norm(bt->C, 1, M, dm, 0, eps, bt->h, bt->a, dt, st));
-    TRY(gemm_b(bt->a, dm, m->gu[l], M, 2 * F, dm, bt->C, st));
+    TRY(gemm_b(bt, bt->a, dm, m->gu[l], M, 2 * F, dm, st));
     TRY(launch_swiglu(bt->C, 1, M, F, bt->sw, dt, st));
-    TRY(gemm_b(bt->sw, F, m->down[l], M, dm, F, bt->C, st));
+    TRY(gemm_b(bt, bt->sw, F, m->down[l], M, dm, F, st));
     TRY(launch_add_norm(bt->C, 1, M, dm, 0, eps, bt->h, l + 1 == s0->Lr ? bt->feat : bt->a, dt, st));
   }
-  return gemm_b(bt->feat, dm, m->d.lm_head, M, V, dm, bt->C, st);
+  return gemm_b(bt, bt->feat, dm, m->d.lm_head, M, V, dm, st);
 }
 
 extern "C" adt_status adt_batch_step(adt_batch* bt, adt_step_out* outs, void* stream) {
