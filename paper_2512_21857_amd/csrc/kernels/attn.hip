@@ -239,20 +239,20 @@ __global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
 constexpr int AWG_KT = 32;
 constexpr int AWG_W = 8;
 
-template <int DH, int QTW, int QG>
-__global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
+template <int DH, int QTW, int QG, int NW>
+__global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
     int kv_cap, float scale_log2, uint16_t* __restrict__ out, int pairs, int qsplit) {
-  constexpr int KG = AWG_W / QG;                           // key slices per query group
+  constexpr int KG = NW / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
   // V rows of a step, padded by 32 bytes so that the 8 rows a transpose load touches per
   // pair of 16-lane groups fall on distinct banks
   constexpr int VRW = DH + 16;
   constexpr int VG = (AWG_KT / 4) * (DH / 8) / WAVE;       // (4 keys x 8 dims) groups per lane per step
-  constexpr int VT_BYTES = AWG_W * AWG_KT * VRW * 2;
-  constexpr int MG_BYTES = AWG_W * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
+  constexpr int VT_BYTES = NW * AWG_KT * VRW * 2;
+  constexpr int MG_BYTES = NW * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
   // Workgroup i takes query slice qs of pair p, with i = (p / 8) * 8 qsplit + 8 qs + p % 8:
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
 
   // merge the KG waves of each query group, tile by tile, in wave order
   float* mo = reinterpret_cast<float*>(smem);                      // [wave][16][DH]
-  float* mml = mo + AWG_W * 16 * DH;                               // [wave][16][2]
+  float* mml = mo + NW * 16 * DH;                               // [wave][16][2]
   __syncthreads();
 #pragma unroll
   for (int t = 0; t < QTW; ++t) {
@@ -449,7 +449,7 @@ __global__ __launch_bounds__(AWG_W * WAVE) void tree_attn_wg_kernel(
       mml[((size_t)wave * 16 + lq) * 2 + 1] = l_run[t];
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < QG * 16 * DH; idx += AWG_W * WAVE) {
+    for (int idx = threadIdx.x; idx < QG * 16 * DH; idx += NW * WAVE) {
       const int qgr = idx / (16 * DH), row = (idx / DH) % 16, d = idx % DH;
       const int qr = (tile0 + qgr * QTW + t) * 16 + row;
       if (qr >= nq) continue;
@@ -824,6 +824,15 @@ static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, i
   return groups <= 4;
 }
 
+// Waves per workgroup of the one-workgroup-per-pair kernel.  Many pairs at head size 128
+// with trees of 9-16 rows (about 160 VGPRs a wave, so one eight-wave workgroup per CU): four
+// waves, so that three workgroups share a CU and every pair of a 512-pair launch is resident
+// at once (measured: 16 rows 61 % of 8 TB/s against 59.5 %; at 8 rows eight waves stay
+// ahead, 60.7 % against 60.2 %).
+static int attn_wg_waves(int B, int H, int Dh, int nq_max) {
+  return (B * H >= 128 && Dh == 128 && nq_max > 8) ? 4 : AWG_W;
+}
+
 // Many pairs with trees of 17-128 rows: the shared-block kernel (one K/V stream per pair,
 // read by every query tile from LDS).
 static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 16 && nq_max <= 128; }
@@ -834,7 +843,7 @@ static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_m
 static bool attn_use_wg(int B, int H, int Dh, int nq_max, int kv_cap) {
   int qtw, qg, qsplit;
   if (!attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit)) return false;
-  const int kg = AWG_W / qg;
+  const int kg = attn_wg_waves(B, H, Dh, nq_max) / qg;
   return B * H >= 128 || kv_cap / kg <= 256;
 }
 
@@ -878,21 +887,22 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
     const int pairs = B * H;
     const dim3 grid(qsplit == 1 ? pairs : (pairs + 7) / 8 * 8 * qsplit);
     const float sl2 = scale * LOG2E;
-#define ADT_ATTN_WG(DHV, QTWV, QGV)                                                                                \
-  hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV>, grid, dim3(AWG_W * WAVE), 0, st, ev0, ev1, 0,          \
+#define ADT_ATTN_WG(DHV, QTWV, QGV, NWV)                                                                           \
+  hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,       \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, pairs, qsplit)
     if (Dh == 128) {
-      if (qtw == 1) ADT_ATTN_WG(128, 1, 1);
-      else if (qg == 1) ADT_ATTN_WG(128, 2, 1);
-      else if (qg == 2) ADT_ATTN_WG(128, 2, 2);
-      else ADT_ATTN_WG(128, 2, 4);
+      if (qtw == 1 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4);
+      else if (qtw == 1) ADT_ATTN_WG(128, 1, 1, AWG_W);
+      else if (qg == 1) ADT_ATTN_WG(128, 2, 1, AWG_W);
+      else if (qg == 2) ADT_ATTN_WG(128, 2, 2, AWG_W);
+      else ADT_ATTN_WG(128, 2, 4, AWG_W);
     } else {
-      if (qtw == 1) ADT_ATTN_WG(64, 1, 1);
-      else if (qtw == 2) ADT_ATTN_WG(64, 2, 1);
-      else if (qtw == 3) ADT_ATTN_WG(64, 3, 1);
-      else if (qg == 1) ADT_ATTN_WG(64, 4, 1);
-      else ADT_ATTN_WG(64, 4, 2);
+      if (qtw == 1) ADT_ATTN_WG(64, 1, 1, AWG_W);
+      else if (qtw == 2) ADT_ATTN_WG(64, 2, 1, AWG_W);
+      else if (qtw == 3) ADT_ATTN_WG(64, 3, 1, AWG_W);
+      else if (qg == 1) ADT_ATTN_WG(64, 4, 1, AWG_W);
+      else ADT_ATTN_WG(64, 4, 2, AWG_W);
     }
 #undef ADT_ATTN_WG
     ADT_LAUNCH_CHECK();

@@ -102,6 +102,15 @@ def test_tree_attn_bf16_many_pairs_blocks(rt, B, H, Dh, n, l_lo, l_hi, vary):
     assert _attn_case(rt, B=B, H=H, Dh=Dh, n=n, l_lo=l_lo, l_hi=l_hi, seed=B * 1000 + n, vary_n=vary) > 0
 
 
+@pytest.mark.parametrize("n", [7, 16])
+def test_tree_attn_bf16_many_pairs_one_tile(rt, n):
+    """Many (sequence, head) pairs with trees of at most 16 rows at head size 128: one
+    workgroup per pair whose waves split the keys (eight waves up to 8 rows, four above),
+    ragged trees and prefixes from empty to several hundred keys."""
+    print(f"tree_attn bf16 many pairs one tile n={n}", flush=True)
+    assert _attn_case(rt, B=8, H=16, Dh=128, n=n, l_lo=0, l_hi=700, seed=8000 + n, vary_n=True) > 0
+
+
 def test_tree_attn_bf16_full_microbench_sampled(rt):
     """The 16 x 32 x 128 microbenchmark at its real size (L in [512, 2400], 128 nodes), checked
     on sampled rows including the root, the last node and a deep node of every sequence."""
