@@ -587,8 +587,8 @@ __device__ __forceinline__ int blk_swz_k(int row) { return DH == 128 ? (row & 15
 template <int DH>
 __device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
 
-template <int DH, int KH>
-__global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
+template <int DH, int KH, int NW>
+__global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
@@ -597,10 +597,10 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
   constexpr int CH = DH / 8;                     // 16-byte chunks per row
   constexpr int DT = DH / 16, KS = DH / 32;
   constexpr int BLK_BYTES = BLK_KT * DH * 2;     // one block of K or of V
-  constexpr int LOADS = BLK_BYTES / (AWG_W * WAVE * 16);   // direct loads per thread per block and operand
+  constexpr int LOADS = BLK_BYTES / (NW * WAVE * 16);   // direct loads per thread per block and operand
   constexpr int SUBS = BLK_KT / KH / 16;         // 16-key sub-blocks per wave per block
   static_assert(LOADS >= 1 && SUBS % 2 == 0, "block shape");
-  static_assert((KH - 1) * (8 / KH) * (DT * 4 + 2) * WAVE * 4 <= 4 * BLK_BYTES, "merge area");
+  static_assert((KH - 1) * (NW / KH) * (DT * 4 + 2) * WAVE * 4 <= 4 * BLK_BYTES, "merge area");
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * BLK_BYTES];   // [buffer][K, V]
 
   const int h = blockIdx.x, b = blockIdx.y;
@@ -637,7 +637,7 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
     const int last = max(total - 1, 0);
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
-      const int slot = r * AWG_W * WAVE + threadIdx.x, row = slot / CH, phys = slot % CH;
+      const int slot = r * NW * WAVE + threadIdx.x, row = slot / CH, phys = slot % CH;
       const int64_t key = min(blk * BLK_KT + row, last);
       kr[r] = *reinterpret_cast<const u16x8*>(kbase + key * DH + (phys ^ blk_swz_k<DH>(row)) * 8);
       vr[r] = *reinterpret_cast<const u16x8*>(vbase + key * DH + (phys ^ blk_swz_v<DH>(row)) * 8);
@@ -647,7 +647,7 @@ __global__ __launch_bounds__(AWG_W * WAVE, 4) void tree_attn_blk_kernel(
     unsigned char* kb = smem + buf * 2 * BLK_BYTES;
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
-      const int slot = r * AWG_W * WAVE + threadIdx.x;
+      const int slot = r * NW * WAVE + threadIdx.x;
       *reinterpret_cast<u16x8*>(kb + slot * 16) = kr[r];
       *reinterpret_cast<u16x8*>(kb + BLK_BYTES + slot * 16) = vr[r];
     }
@@ -825,10 +825,10 @@ static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, i
 }
 
 // Waves per workgroup of the one-workgroup-per-pair kernel.  Many pairs at head size 128
-// with trees of 9-16 rows (about 160 VGPRs a wave, so one eight-wave workgroup per CU): four
-// waves, so that three workgroups share a CU and every pair of a 512-pair launch is resident
-// at once (measured: 16 rows 61 % of 8 TB/s against 59.5 %; at 8 rows eight waves stay
-// ahead, 60.7 % against 60.2 %).
+// with trees of 9-16 rows (about 160-190 VGPRs a wave, so one eight-wave workgroup per CU):
+// four waves, so that two workgroups share a CU and every pair of a 512-pair launch is
+// resident at once (measured: 16 rows 61 % of 8 TB/s against 59.5 %; at 8 rows eight waves
+// stay ahead, 60.7 % against 60.2 %).
 static int attn_wg_waves(int B, int H, int Dh, int nq_max) {
   return (B * H >= 128 && Dh == 128 && nq_max > 8) ? 4 : AWG_W;
 }
@@ -864,18 +864,21 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
     const dim3 grid(H, B);
     const float sl2 = scale * LOG2E;
     const int qt = (nq_max + 15) / 16;
-#define ADT_ATTN_BLK(DHV, KHV)                                                                                     \
-  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV>, grid, dim3(AWG_W * WAVE), 0, st, ev0, ev1, 0,              \
+#define ADT_ATTN_BLK(DHV, KHV, NWV)                                                                                \
+  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,           \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
+    // two tiles at head size 128: four waves (two tiles x two key halves, ~190 VGPRs), so two
+    // workgroups share a CU and a 512-pair launch is resident at once (32 nodes: 61 % of
+    // 8 TB/s against 58 % with eight waves in 128-key blocks, one workgroup per CU)
     if (Dh == 128) {
-      if (qt <= 2) ADT_ATTN_BLK(128, 4);
-      else if (qt <= 4) ADT_ATTN_BLK(128, 2);
-      else ADT_ATTN_BLK(128, 1);
+      if (qt <= 2) ADT_ATTN_BLK(128, 2, 4);
+      else if (qt <= 4) ADT_ATTN_BLK(128, 2, AWG_W);
+      else ADT_ATTN_BLK(128, 1, AWG_W);
     } else {
-      if (qt <= 2) ADT_ATTN_BLK(64, 4);
-      else if (qt <= 4) ADT_ATTN_BLK(64, 2);
-      else ADT_ATTN_BLK(64, 1);
+      if (qt <= 2) ADT_ATTN_BLK(64, 4, AWG_W);
+      else if (qt <= 4) ADT_ATTN_BLK(64, 2, AWG_W);
+      else ADT_ATTN_BLK(64, 1, AWG_W);
     }
 #undef ADT_ATTN_BLK
     ADT_LAUNCH_CHECK();

@@ -94,7 +94,7 @@ def test_tree_attn_bf16_long_prefix_split_keys(rt, n):
     (16, 8, 64, 100, 60, 200, True),    # 7 tiles (one wave only loads), ragged trees
     (2, 64, 128, 128, 0, 70, False),    # 8 tiles, almost no prefix: nearly every block is masked
     (8, 16, 128, 33, 500, 700, False),  # 3 tiles at the smallest row count of that shape
-    (8, 16, 128, 32, 100, 400, True),   # 2 tiles: 128-key blocks, keys split in four parts
+    (8, 16, 128, 32, 100, 400, True),   # 2 tiles at head size 128: four waves, keys split in two halves
     (16, 8, 64, 20, 0, 200, False),     # 2 tiles at head size 64, the smallest tree of the path
 ])
 def test_tree_attn_bf16_many_pairs_blocks(rt, B, H, Dh, n, l_lo, l_hi, vary):
