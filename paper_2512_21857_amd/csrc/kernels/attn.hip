@@ -12,8 +12,10 @@
 // the bf16 rounding of the output itself); steps wholly inside the unmasked prefix skip the
 // mask test, and the running output is rescaled only when some row's maximum moved.
 // Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
-// Few pairs (one image's forwards): tree_attn_wg_kernel below, one workgroup per pair whose
-// waves split the keys and merge in LDS.
+// Few pairs (one image's forwards), and many pairs with trees of at most 16 rows:
+// tree_attn_wg_kernel below, one workgroup per pair (or query slice) whose waves split the
+// keys and merge in LDS; many pairs with 17-128 rows: tree_attn_blk_kernel, one workgroup per
+// pair sharing each K/V block through LDS.
 #include <hip/hip_ext.h>
 
 #include "../launch.h"
@@ -576,8 +578,9 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
 // next block into registers while the current one is computed, then stores it; double
 // buffered, one barrier per block), and every wave reads them: wave w owns query tile
 // w % QT and one of the KH parts of every block's keys (w / QT): KH = 1 for 5-8 tiles,
-// 2 for 3-4 tiles (64-key blocks) and 4 for 2 tiles (128-key blocks); the parts of a tile
-// are merged in LDS at the end, in part order.  K and V rows are stored with their
+// 2 for 3-4 tiles (64-key blocks) and, with eight waves, 4 for 2 tiles (128-key blocks);
+// a workgroup of NW = 4 waves takes 2 tiles with KH = 2; the parts of a tile are merged in
+// LDS at the end, in part order.  K and V rows are stored with their
 // 16-byte chunks XOR-swizzled by row, so the K operand reads (16 rows of one chunk column)
 // and the V^T reads through the transpose load (8 rows of two chunk columns) each touch
 // distinct banks.
