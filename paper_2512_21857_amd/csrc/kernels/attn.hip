@@ -573,7 +573,7 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
 }
 
 // ----------------------------------------------------------------------------- host
-// Large trees over many pairs: one workgroup of eight waves per (sequence, head).  64-key
+// Large trees over many pairs: one workgroup of NW waves per (sequence, head).  64-key
 // blocks of K and V come into LDS once per workgroup (each thread fetches its share of the
 // next block into registers while the current one is computed, then stores it; double
 // buffered, one barrier per block), and every wave reads them: wave w owns query tile
