@@ -346,7 +346,19 @@ static NtPlan gemm_nt_plan(int M, int N, int K, size_t part_elems) {
   return p;
 }
 
-size_t gemm_nt_part_elems(int M, int N, int K) { return gemm_nt_plan(M, N, K, SIZE_MAX).part; }
+// 128 x 128 blocks: with at most half as many blocks as CUs and K >= 2048 the K range is
+// split in two, so that twice the CUs work (measured slower at a full round of blocks).
+static int gemm_nt_ks128(int M, int N, int K, size_t part_elems) {
+  const int64_t blocks = (int64_t)((M + 127) / 128) * (N / 128);
+  return (blocks <= DMA_SLOTS / 2 && K >= 2048 && (size_t)M * N <= part_elems) ? 2 : 1;
+}
+
+size_t gemm_nt_part_elems(int M, int N, int K) {
+  const NtPlan p = gemm_nt_plan(M, N, K, SIZE_MAX);
+  const bool dma256 = N % 256 == 0 && (p.bn == 384 || p.ksplit > 1 || (int64_t)(N / 256) * ((M + 255) / 256) >= 128);
+  if (dma256) return p.part;
+  return gemm_nt_ks128(M, N, K, SIZE_MAX) > 1 ? (size_t)M * N : 0;
+}
 
 // One launch of 256 x 256 DMA blocks over columns [0, N) of the operands given (W already
 // offset to the first column's packed tile), K split ks ways with the partials reduced.
@@ -403,9 +415,17 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
   // Packed weights with fewer blocks (the narrow projections of a batch of trees): 128 x 128
   // blocks of four waves through the same DMA pipeline, two workgroups per CU.
   if (packed) {
-    hipExtLaunchKernelGGL((gemm_nt_dma_kernel<128, 128, 2, 2, DMA_NSTAGE>), dim3((M + 127) / 128 * (N / 128)),
-                          dim3(4 * WAVE), 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, C, ldc, 1, nullptr);
+    const int ks = gemm_nt_ks128(M, N, K, part ? part_elems : 0);
+    hipExtLaunchKernelGGL((gemm_nt_dma_kernel<128, 128, 2, 2, DMA_NSTAGE>), dim3((M + 127) / 128 * (N / 128) * ks),
+                          dim3(4 * WAVE), 0, st, ev0, ks > 1 ? nullptr : ev1, 0, x, ldx, w, M, N, K, C, ldc, ks, part);
     ADT_LAUNCH_CHECK();
+    if (ks > 1) {
+      const int64_t quads = (int64_t)M * (N / 4);
+      const int blocks = (int)std::min<int64_t>((quads + 255) / 256, 4096);
+      hipExtLaunchKernelGGL(gemm_nt_reduce_kernel, dim3(blocks), dim3(256), 0, st, nullptr, ev1, 0, C, ldc,
+                            (const float*)part, M, N, ks - 1);
+      ADT_LAUNCH_CHECK();
+    }
     return ADT_OK;
   }
 #define ADT_NT(BNV, BMV, PK)                                                                                    \

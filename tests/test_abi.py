@@ -68,7 +68,10 @@ def test_argument_errors_return_codes_without_launching(L):
     # none for the 256-block LM head or shorter K
     assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 11008) == 3 * 976 * 4096 * 4
     assert L.adt_gemm_bf16_packed_workspace_size(976, 65536, 11008) == 0
+    # 256 blocks of 128 x 128 fill the CUs: no split
     assert L.adt_gemm_bf16_packed_workspace_size(976, 4096, 4096) == 0
+    # 80 blocks of 128 x 128 with K >= 2048: K split in two, one partial
+    assert L.adt_gemm_bf16_packed_workspace_size(976, 1280, 3584) == 976 * 1280 * 4
     # 344 blocks of 256 x 256: the last 22 column blocks (88 blocks) split two ways
     assert L.adt_gemm_bf16_packed_workspace_size(976, 22016, 4096) == 976 * 22 * 256 * 4
     # 192 blocks of 256 x 256 become 256 of 384 x 128: no partials

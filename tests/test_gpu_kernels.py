@@ -362,7 +362,7 @@ def test_gemm_bf16_batched(rt, M, N, K):
 
 @pytest.mark.parametrize("M,N,K", [(300, 32768, 128), (1, 65536, 64), (100, 256, 128), (520, 16384, 192),
                                    (300, 512, 8192), (40, 1024, 8256), (130, 384, 320), (976, 3840, 1280),
-                                   (976, 12288, 512), (300, 35840, 512), (976, 22016, 320)])
+                                   (976, 12288, 512), (300, 35840, 512), (976, 22016, 320), (500, 1280, 2048)])
 def test_gemm_bf16_packed(rt, M, N, K):
     """Packed weights: the DMA pipeline in 256 x 256 blocks (>= 128 of them; K below and above
     the stages it keeps in flight; one row; partial row blocks), with K split over 4
@@ -383,7 +383,8 @@ def test_gemm_bf16_packed(rt, M, N, K):
     got = rt.gemm_bf16_packed(xt, wp, N)
     _gemm_ref_check(got.cpu().numpy(), xt.float().cpu().numpy(), wt.float().cpu().numpy(), np.arange(M))
     split = rt.lib().adt_gemm_bf16_packed_workspace_size(M, N, K) > 0
-    assert split == (K >= 8192 or N in (35840, 22016))
+    # 500 x 1280 x 2048: 40 blocks of 128 x 128 with K >= 2048, K split in two
+    assert split == (K >= 8192 or N in (35840, 22016) or (M, N, K) == (500, 1280, 2048))
     ref = rt.gemm_bf16(xt, wt)
     if split:
         assert torch.equal(rt.gemm_bf16_packed(xt, wp, N, split=False), ref)
