@@ -58,10 +58,11 @@ class OracleModel:
         return self.w("embed")[np.asarray(tokens, dtype=np.int64)]
 
     # -- one decoder layer over a set of rows ---------------------------------------------
-    def layer(self, pre: str, h: np.ndarray, pos: Sequence[int], slots: Sequence[int],
-              key_slots: Sequence[Sequence[int]], cache: KVCache, li: int) -> np.ndarray:
-        """h: [rows][d] residual stream.  Row r sits at position pos[r]; its K/V are written
-        to cache slot slots[r] before attention, and it attends to key_slots[r]."""
+    def attn_block(self, pre: str, h: np.ndarray, pos: Sequence[int], slots: Sequence[int],
+                   key_slots: Sequence[Sequence[int]], cache: KVCache, li: int):
+        """First half of a pre-norm layer: h + Attn(RMSNorm(h)) W_o.  Row r sits at position
+        pos[r]; its K/V are written to cache slot slots[r] before attention, and it attends to
+        key_slots[r].  Returns (new residual, q, o)."""
         m = self.m
         rows = h.shape[0]
         H, Dh = m.n_heads, m.head_dim
@@ -76,13 +77,23 @@ class OracleModel:
         cache.k[li][:, sl, :] = k.transpose(1, 0, 2)
         cache.v[li][:, sl, :] = v.transpose(1, 0, 2)
         o = self.rnd(attend_rows(q, cache.k[li], cache.v[li], key_slots, self.scale))
-        h = h + o.reshape(rows, H * Dh) @ self.w(pre + ".wo").T
+        return h + o.reshape(rows, H * Dh) @ self.w(pre + ".wo").T, q, o
+
+    def mlp_block(self, pre: str, h: np.ndarray):
+        """Second half: h + SwiGLU(RMSNorm(h)) W_down.  Returns (new residual, b, s)."""
         b = self.rnd(rmsnorm(h))
         s = self.rnd(silu(b @ self.w(pre + ".wg").T) * (b @ self.w(pre + ".wu").T))
-        out = h + s @ self.w(pre + ".wd").T
+        return h + s @ self.w(pre + ".wd").T, b, s
+
+    def layer(self, pre: str, h: np.ndarray, pos: Sequence[int], slots: Sequence[int],
+              key_slots: Sequence[Sequence[int]], cache: KVCache, li: int) -> np.ndarray:
+        """h: [rows][d] residual stream through both halves of the layer."""
+        rows = h.shape[0]
+        h_attn, q, o = self.attn_block(pre, h, pos, slots, key_slots, cache, li)
+        out, b, s = self.mlp_block(pre, h_attn)
         if self.trace is not None:
             self.trace.update({pre + ".q": q.reshape(rows, -1), pre + ".o": o.reshape(rows, -1),
-                               pre + ".h_attn": h, pre + ".b": b, pre + ".s": s, pre + ".h": out})
+                               pre + ".h_attn": h_attn, pre + ".b": b, pre + ".s": s, pre + ".h": out})
         return out
 
     # -- full forwards ---------------------------------------------------------------------
