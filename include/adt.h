@@ -378,6 +378,48 @@ void adt_session_destroy(adt_session* s);
 adt_status adt_session_prefill(adt_session* s, const int32_t* prefix, int32_t* first_token, void* stream);
 adt_status adt_session_get_view(const adt_session* s, adt_session_view* v);
 
+/* Layer-by-layer record of the session's forwards, so that each decoder layer of the target
+ * (Sec. 3.1, parallel verification) and of the draft head (Sec. 4.2; Fig. 5 caption) can be
+ * compared with a reference evaluated from the same inputs.  For tests and debugging; off by
+ * default.  While a capture is set the session's forwards run as plain launches (no graph
+ * replay) and every forward appends, in order:
+ *   resid:  fp32 snapshots of the residual stream, each [rows][d_model] (rows = nodes x
+ *           branches, branch rows interleaved node by node): target forwards 2 n_layers + 1 of
+ *           them (2l = the input of layer l, 2l + 1 = after layer l's attention block with the
+ *           output projection added, 2 n_layers = the last layer's output, i.e. the final norm's
+ *           input), draft forwards 3 (0 = the FC output, 1 = after the attention block, 2 = the
+ *           layer output);
+ *   xin:    draft forwards only: the FC input rows [rows][2 d_model] in the model dtype
+ *           ([token embedding ; parent feature]);
+ *   meta:   int32, per forward: token ids [nodes], positions [nodes], then the ancestor masks
+ *           [nodes][ADT_MASK_WORDS] as uint64 (8-byte aligned).  Node r's K/V go to cache slot
+ *           slot0 + r and it attends to slots [0, kv_prefix) plus kv_prefix + j for every set bit
+ *           j of its mask.
+ * The buffers are caller-owned device memory; a forward whose data would overrun one fails
+ * with ADT_E_CAPACITY before it launches anything.  adt_session_set_capture resets the record
+ * (NULL switches capture off); adt_session_capture_record returns forward i's offsets.  Not
+ * used by the batched cycle. */
+typedef struct {
+  float* resid;
+  size_t resid_elems;
+  void* xin;
+  size_t xin_bytes;
+  int32_t* meta;
+  size_t meta_elems;
+} adt_capture;
+typedef struct {
+  int32_t draft;                /* 0 target forward, 1 draft-head forward */
+  int32_t nodes, rows;          /* tree or prompt nodes; rows = nodes x branches */
+  int32_t kv_prefix, slot0, n_tail;
+  int32_t snapshots;            /* residual snapshots written (2 n_layers + 1, or 3) */
+  int64_t resid_off;            /* first float of this forward in resid */
+  int64_t xin_off;              /* first byte in xin (draft forwards) */
+  int64_t meta_off;             /* first int32 in meta */
+} adt_capture_rec;
+adt_status adt_session_set_capture(adt_session* s, const adt_capture* cap);
+int32_t adt_session_capture_count(const adt_session* s);
+adt_status adt_session_capture_record(const adt_session* s, int32_t i, adt_capture_rec* rec);
+
 /* a1-a3: the draft head's catch-up rows then d_hat - 1 frontier forwards (Sec. 4.2, Eq. 4),
  * top-k children scored by summed log-probability (Eq. 3), frontier select, top-N rerank and
  * the BFS tree arrays + masks of the session's current tree.  n_nodes_out [host] gets the

@@ -74,6 +74,15 @@ class SessionView(C.Structure):
                 ("branch_logits", p), ("draft_branch_logits", p)]
 
 
+class Capture(C.Structure):
+    _fields_ = [("resid", p), ("resid_elems", sz), ("xin", p), ("xin_bytes", sz), ("meta", p), ("meta_elems", sz)]
+
+
+class CaptureRec(C.Structure):
+    _fields_ = [("draft", i32), ("nodes", i32), ("rows", i32), ("kv_prefix", i32), ("slot0", i32), ("n_tail", i32),
+                ("snapshots", i32), ("resid_off", i64), ("xin_off", i64), ("meta_off", i64)]
+
+
 _SIGS = {
     "adt_version": (i32, []),
     "adt_last_error": (sz, [C.c_char_p, sz]),
@@ -99,6 +108,9 @@ _SIGS = {
     "adt_session_destroy": (None, [p]),
     "adt_session_prefill": (i32, [p, ip, ip, p]),
     "adt_session_get_view": (i32, [p, C.POINTER(SessionView)]),
+    "adt_session_set_capture": (i32, [p, C.POINTER(Capture)]),
+    "adt_session_capture_count": (i32, [p]),
+    "adt_session_capture_record": (i32, [p, i32, C.POINTER(CaptureRec)]),
     "adt_tree_expand": (i32, [p, i32, i32, i32, ip, p]),
     "adt_session_set_tree": (i32, [p, ip, ip, i32, p]),
     "adt_verify_forward": (i32, [p, p]),

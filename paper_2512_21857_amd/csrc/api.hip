@@ -499,6 +499,13 @@ struct adt_session_s {
   uint64_t* samp_w = nullptr;   // stochastic children: [KR][V] q weights of a level's rows
   // pinned host staging of an acceptance's readback: path [R], tokens [R], a, bonus
   int32_t* h_acc = nullptr;
+  // layer-by-layer record (adt_session_set_capture): forwards run eagerly while it is set;
+  // capt_cur indexes the record of the forward in progress (-1 outside a forward)
+  bool capt_on = false;
+  adt_capture capt{};
+  std::vector<adt_capture_rec> capt_log;
+  size_t capt_resid = 0, capt_xin = 0, capt_meta = 0;
+  int capt_cur = -1;
   // HIP graphs of the forwards, keyed by shape; captured on a private stream, replayed on
   // the caller's stream.
   bool graphs = true;
@@ -707,7 +714,7 @@ static adt_status set_scalars(adt_session_s* s, int kv_len, int nq, int ntail, i
 // inside a replayed graph).
 template <typename F>
 static adt_status run_graph(adt_session_s* s, int64_t key, hipStream_t st, F&& body) {
-  if (!s->graphs || g_prof.on) return body(st);
+  if (!s->graphs || g_prof.on || s->capt_on) return body(st);
   auto it = s->gexec.find(key);
   if (it == s->gexec.end()) {
     if (!s->cap) ADT_HIP(hipStreamCreateWithFlags(&s->cap, hipStreamNonBlocking));
@@ -745,6 +752,56 @@ static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, in
   return r;
 }
 
+// ---------------------------------------------------------------------------- capture
+// Opens the record of one forward (adt_session_set_capture): checks that its residual
+// snapshots, FC inputs and row metadata fit the caller's buffers, then copies the rows'
+// tokens (branch 0), positions and ancestor masks.  Nothing is launched when a buffer is full.
+static adt_status capt_begin(adt_session_s* s, bool draft, int M, int L_pre, int slot0, int n_tail,
+                             const int32_t* tok, const int32_t* pos, const uint64_t* mask, hipStream_t st) {
+  s->capt_cur = -1;
+  if (!s->capt_on) return ADT_OK;
+  adt_capture_rec r{};
+  r.draft = draft ? 1 : 0;
+  r.nodes = M;
+  r.rows = s->nb * M;
+  r.kv_prefix = L_pre;
+  r.slot0 = slot0;
+  r.n_tail = n_tail;
+  r.snapshots = draft ? 3 : 2 * s->Lr + 1;
+  r.resid_off = (int64_t)s->capt_resid;
+  r.xin_off = (int64_t)s->capt_xin;
+  r.meta_off = (int64_t)s->capt_meta;
+  const size_t nres = (size_t)r.snapshots * r.rows * s->dm;
+  const size_t nxin = draft ? (size_t)r.rows * 2 * s->dm * esize(s->dt) : 0;
+  const size_t nmeta = (size_t)M * (2 + 2 * ADT_MASK_WORDS);
+  ADT_CHECK_ARG(s->capt_resid + nres <= s->capt.resid_elems, ADT_E_CAPACITY,
+                "capture: residual buffer holds %zu floats, %zu needed", s->capt.resid_elems, s->capt_resid + nres);
+  ADT_CHECK_ARG(!draft || (s->capt.xin && s->capt_xin + nxin <= s->capt.xin_bytes), ADT_E_CAPACITY,
+                "capture: FC input buffer holds %zu bytes, %zu needed", s->capt.xin_bytes, s->capt_xin + nxin);
+  ADT_CHECK_ARG(s->capt.meta && s->capt_meta + nmeta <= s->capt.meta_elems, ADT_E_CAPACITY,
+                "capture: metadata buffer holds %zu ints, %zu needed", s->capt.meta_elems, s->capt_meta + nmeta);
+  int32_t* mt = s->capt.meta + s->capt_meta;
+  ADT_HIP(hipMemcpyAsync(mt, tok, sizeof(int32_t) * M, hipMemcpyDeviceToDevice, st));
+  ADT_HIP(hipMemcpyAsync(mt + M, pos, sizeof(int32_t) * M, hipMemcpyDeviceToDevice, st));
+  ADT_HIP(hipMemcpyAsync(mt + 2 * M, mask, sizeof(uint64_t) * ADT_MASK_WORDS * M, hipMemcpyDeviceToDevice, st));
+  s->capt_resid += nres;
+  s->capt_xin += nxin;
+  s->capt_meta += nmeta;
+  s->capt_log.push_back(r);
+  s->capt_cur = (int)s->capt_log.size() - 1;
+  return ADT_OK;
+}
+
+// Residual snapshot idx of the forward in progress (no-op outside a captured forward).
+static adt_status capt_snap(adt_session_s* s, int idx, hipStream_t st) {
+  if (s->capt_cur < 0) return ADT_OK;
+  const adt_capture_rec& r = s->capt_log[s->capt_cur];
+  const size_t n = (size_t)r.rows * s->dm;
+  ADT_HIP(hipMemcpyAsync(s->capt.resid + r.resid_off + (size_t)idx * n, s->h, sizeof(float) * n,
+                         hipMemcpyDeviceToDevice, st));
+  return ADT_OK;
+}
+
 // Decoder layers over the nb * M rows of M tree nodes (branches interleaved node by node).
 static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
                              const uint64_t* mask, void* final_out, hipStream_t st) {
@@ -779,6 +836,7 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
     for (int l = l0; l < l1; ++l) {
       char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
       char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
+      TRY(capt_snap(s, 2 * (l - l0), st));
       GemmEpi qkv;
       qkv.mode = EPI_QKV;
       qkv.ssp_in = s->ssp;
@@ -797,6 +855,7 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       TRY(gemm_p(s->h, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
       TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st, resid));
+      TRY(capt_snap(s, 2 * (l - l0) + 1, st));
       GemmEpi sw;
       sw.mode = EPI_SWIGLU;
       sw.ssp_in = s->ssp;
@@ -806,6 +865,7 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       TRY(gemm_p(s->h, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
       TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st, resid));
     }
+    TRY(capt_snap(s, 2 * (l1 - l0), st));
     if (final_out) TRY(launch_norm_rows(s->h, s->ssp, rows, dm, eps, final_out, dt, st));
     return ADT_OK;
   }
@@ -813,17 +873,19 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   for (int l = l0; l < l1; ++l) {
     char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
     char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
+    TRY(capt_snap(s, 2 * (l - l0), st));
     TRY(gemm_p(s->act, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st));
     TRY(launch_qkv_rope(s->part, 1, rows, H, Dh, pos, s->scal + SC_SLOT, s->rope, s->q, kc, vc, stride_h, dt, st, br));
     TRY(attention(kc, vc));
     TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st));
     TRY(launch_add_norm(s->part, 1, rows, dm, 0, eps, s->h, s->act, dt, st));
+    TRY(capt_snap(s, 2 * (l - l0) + 1, st));
     TRY(gemm_p(s->act, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st));
     TRY(launch_swiglu(s->part, 1, rows, F, s->sw, dt, st));
     TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st));
     TRY(launch_add_norm(s->part, 1, rows, dm, 0, eps, s->h, l + 1 == l1 ? final_out : s->act, dt, st));
   }
-  return ADT_OK;
+  return capt_snap(s, 2 * (l1 - l0), st);
 }
 
 // Logits of M nodes (nb rows each) into out [M][V]; with guidance the per-branch rows go to
@@ -854,12 +916,14 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
     const bool bf = s->dt == ADT_BF16;
+    TRY(capt_begin(s, false, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
     TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, bf ? nullptr : s->act,
                           bf ? s->ssp : nullptr, s->dt, cs, Branches{s->nb, tok_boff, 0}));
     TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
     if (lm_rows > 0)
       TRY(lm_head(s, (const char*)s->feat + (size_t)s->nb * lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits,
                   s->rawlog, cs));
+    s->capt_cur = -1;
     return ADT_OK;
   };
   return key < 0 ? body(st) : run_graph(s, key, st, body);
@@ -875,8 +939,12 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
   const int dm = s->dm, dt = s->dt, rows = s->nb * M;
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
+    TRY(capt_begin(s, true, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
     TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, rows, dm, s->xin, dt, cs,
                            Branches{s->nb, tok_boff, 0}));
+    if (s->capt_cur >= 0)
+      ADT_HIP(hipMemcpyAsync((char*)s->capt.xin + s->capt_log[s->capt_cur].xin_off, s->xin,
+                             (size_t)rows * 2 * dm * esize(dt), hipMemcpyDeviceToDevice, cs));
     if (dt == ADT_BF16) {
       GemmEpi e;
       e.mode = EPI_RESID;
@@ -891,6 +959,7 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
     TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, cs));
     if (lm_rows > 0)
       TRY(lm_head(s, (const char*)fout + (size_t)s->nb * lm_row0 * dm * esize(dt), lm_rows, lout, lraw, cs));
+    s->capt_cur = -1;
     return ADT_OK;
   };
   return key < 0 ? body(st) : run_graph(s, key, st, body);
@@ -1539,6 +1608,28 @@ extern "C" adt_status adt_batch_step(adt_batch* bt, adt_step_out* outs, void* st
     }
     TRY(accept_finish(bt->ss[b], dh[b], kh[b], &outs[b], st));
   }
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_session_set_capture(adt_session* s, const adt_capture* cap) {
+  ADT_CHECK_ARG(s != nullptr, ADT_E_ARG, "set_capture: null session");
+  const bool on = cap != nullptr && cap->resid != nullptr;
+  ADT_CHECK_ARG(!on || cap->meta != nullptr, ADT_E_ARG, "set_capture: metadata buffer missing");
+  s->capt_log.clear();
+  s->capt_resid = s->capt_xin = s->capt_meta = 0;
+  s->capt_cur = -1;
+  s->capt_on = on;
+  s->capt = on ? *cap : adt_capture{};
+  return ADT_OK;
+}
+
+extern "C" int32_t adt_session_capture_count(const adt_session* s) { return s ? (int32_t)s->capt_log.size() : 0; }
+
+extern "C" adt_status adt_session_capture_record(const adt_session* s, int32_t i, adt_capture_rec* rec) {
+  ADT_CHECK_ARG(s && rec, ADT_E_ARG, "capture_record: null pointer");
+  ADT_CHECK_ARG(i >= 0 && i < (int32_t)s->capt_log.size(), ADT_E_ARG, "capture_record: %d of %zu", i,
+                s->capt_log.size());
+  *rec = s->capt_log[i];
   return ADT_OK;
 }
 

@@ -352,6 +352,52 @@ class DeviceSession:
         check(lib().adt_session_get_view(self.handle, C.byref(v)))
         return v
 
+    # -- layer-by-layer record (adt_session_set_capture) -------------------------------------
+    def set_capture(self, resid_elems: int = 0, xin_bytes: int = 0, meta_elems: int = 0) -> None:
+        """Allocates the record buffers and (re)starts recording; resid_elems = 0 stops."""
+        dev = self.model.device
+        if resid_elems <= 0:
+            self._capture = None
+            check(lib().adt_session_set_capture(self.handle, None))
+            return
+        bufs = (torch.empty(resid_elems, dtype=torch.float32, device=dev),
+                torch.empty(max(xin_bytes, 16), dtype=torch.uint8, device=dev),
+                torch.empty(max(meta_elems, 16), dtype=torch.int32, device=dev))
+        cap = abi.Capture(_p(bufs[0]), resid_elems, _p(bufs[1]), xin_bytes, _p(bufs[2]), meta_elems)
+        check(lib().adt_session_set_capture(self.handle, C.byref(cap)))
+        self._capture = bufs
+
+    def restart_capture(self) -> None:
+        """Clears the record, keeping the buffers."""
+        r, x, m = self._capture
+        cap = abi.Capture(_p(r), r.numel(), _p(x), x.numel(), _p(m), m.numel())
+        check(lib().adt_session_set_capture(self.handle, C.byref(cap)))
+
+    def captured(self) -> List[dict]:
+        """Every recorded forward since the last (re)start: its record fields, the residual
+        snapshots [snapshots][rows][d_model] fp32, the FC input rows (draft forwards), and
+        tokens, positions and ancestor masks per node (host arrays)."""
+        res, xin, meta = self._capture
+        torch.cuda.current_stream().synchronize()
+        d = self.cfg.model.d_model
+        tdt = TORCH_DT[self.model.dtype]
+        out = []
+        for i in range(lib().adt_session_capture_count(self.handle)):
+            r = abi.CaptureRec()
+            check(lib().adt_session_capture_record(self.handle, i, C.byref(r)))
+            n, rows = r.nodes, r.rows
+            rec = {f: getattr(r, f) for f, _ in abi.CaptureRec._fields_}
+            rec["resid"] = res[r.resid_off: r.resid_off + r.snapshots * rows * d].view(r.snapshots, rows, d).cpu()
+            if r.draft:
+                nb = rows * 2 * d * torch.empty((), dtype=tdt).element_size()
+                rec["xin"] = xin[r.xin_off: r.xin_off + nb].view(tdt).view(rows, 2 * d).cpu()
+            mt = meta[r.meta_off: r.meta_off + 6 * n].cpu()
+            rec["tok"] = mt[:n].numpy().copy()
+            rec["pos"] = mt[n: 2 * n].numpy().copy()
+            rec["mask"] = mt[2 * n:].numpy().view(np.uint64).reshape(n, 2).copy()
+            out.append(rec)
+        return out
+
     def _ws(self, ptr: int, count: int, dtype: torch.dtype) -> torch.Tensor:
         off = ptr - self.workspace.data_ptr()
         nb = count * torch.empty((), dtype=dtype).element_size()

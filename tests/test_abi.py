@@ -167,3 +167,14 @@ def test_accept_cfg_keeps_its_tensors_alive():
     assert cfg.q_logits == q_logits.data_ptr() and cfg.q_row == q_row.data_ptr()
     assert (cfg.q_ld, cfg.q_rows, cfg.children) == (4, 3, 2)
     assert q_logits[2, 3].item() == 11.0
+
+
+def test_capture_arguments(L):
+    """Layer-by-layer record: a null session is refused, a record without its metadata buffer
+    is refused, and a null session has no records."""
+    import ctypes as C
+    from paper_2512_21857_amd import abi
+    assert L.adt_session_set_capture(None, None) == abi.E_ARG
+    assert L.adt_session_capture_count(None) == 0
+    rec = abi.CaptureRec()
+    assert L.adt_session_capture_record(None, 0, C.byref(rec)) == abi.E_ARG
