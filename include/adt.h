@@ -95,6 +95,19 @@ adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache
                          const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
                          int32_t kv_cap, float scale, int32_t dtype, void* out, void* workspace,
                          size_t workspace_bytes, void* stream);
+/* adt_tree_attn for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same arguments without the
+ * workspace, the same result and the same errors.  The key-split partials live in a 64 MiB
+ * device array inside the library, one per device, whose address is looked up on the first
+ * call on that device; a call whose partials need more (only few sequence-head pairs with long
+ * prefixes split the keys: e.g. 32 pairs of 128-row trees over more than ~4000 slots) returns
+ * ADT_E_CAPACITY and enqueues nothing.  Allocates nothing.  Every call on a device shares that
+ * device's array and leaves the last call's partials in it: calls that overlap on one device
+ * (several streams or threads) race, so the caller must serialise them. */
+adt_status adt_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                                 int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                                 const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
+                                 int32_t kv_cap, float scale, int32_t dtype, void* out, void* stream);
 
 /* ------------------------------------------------------------------ a3 support: masks
  * Ancestor bitmask and depth of every node of B BFS-ordered trees (Sec. 3.1 tree mask):

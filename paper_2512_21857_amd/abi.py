@@ -88,6 +88,7 @@ _SIGS = {
     "adt_last_error": (sz, [C.c_char_p, sz]),
     "adt_tree_attn_workspace_size": (sz, [i32, i32, i32, i32, i32]),
     "adt_tree_attn": (i32, [p, p, p, i64, i64, p, p, p, p, i32, i32, i32, i32, i32, f32, i32, p, p, sz, p]),
+    "adt_tree_attn_noalloc": (i32, [p, p, p, i64, i64, p, p, p, p, i32, i32, i32, i32, i32, f32, i32, p, p]),
     "adt_tree_masks": (i32, [p, p, i32, i32, p, p, p]),
     "adt_kv_compact": (i32, [p, p, i32, i32, i32, i64, i64, p, p, i32, p, i32, i32, p]),
     "adt_accept_workspace_size": (sz, [i32]),

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -149,11 +150,10 @@ extern "C" size_t adt_tree_attn_workspace_size(int32_t B, int32_t H, int32_t Dh,
   return tree_attn_ws_bytes(B, H, Dh, nq_max, kv_cap, ADT_BF16);
 }
 
-extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
-                                    int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
-                                    const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
-                                    int32_t kv_cap, float scale, int32_t dtype, void* out, void* workspace,
-                                    size_t workspace_bytes, void* stream) {
+static adt_status check_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                                  int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                                  const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
+                                  int32_t kv_cap, float scale, int32_t dtype, void* out) {
   ADT_CHECK_ARG(q && k_cache && v_cache && kv_len && n_q && n_tail && anc_mask && out, ADT_E_ARG,
                 "tree_attn: null pointer");
   ADT_CHECK_ARG(valid_dtype(dtype), ADT_E_ARG, "tree_attn: bad dtype %d", dtype);
@@ -164,9 +164,63 @@ extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const vo
                 (long long)stride_h);
   ADT_CHECK_ARG(B == 1 || stride_b >= (int64_t)H * stride_h, ADT_E_SHAPE, "tree_attn: stride_b too small");
   ADT_CHECK_ARG(std::isfinite(scale) && scale > 0.f, ADT_E_ARG, "tree_attn: scale");
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                                    int64_t stride_h, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                                    const uint64_t* anc_mask, int32_t B, int32_t H, int32_t Dh, int32_t nq_max,
+                                    int32_t kv_cap, float scale, int32_t dtype, void* out, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  TRY(check_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask, B, H, Dh, nq_max, kv_cap,
+                      scale, dtype, out));
   return launch_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask,
                           AttnRows{nq_max, 1, nq_max}, B, H, Dh, nq_max, kv_cap, scale, dtype, out, workspace,
                           workspace_bytes, (hipStream_t)stream);
+}
+
+// Scratch of adt_tree_attn_noalloc: the key-split partials of a launch live in this
+// file-scope device array instead of a caller workspace.  Every device the library runs on
+// holds its own copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns with that device current (kept per device below), never through
+// the array's name, which in host code is a stand-in and not a device address.
+constexpr size_t ATTN_SCRATCH_BYTES = (size_t)64 << 20;
+constexpr int SCRATCH_MAX_DEVICES = 64;
+static __device__ __align__(256) char scratch[ATTN_SCRATCH_BYTES];
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[SCRATCH_MAX_DEVICES];
+
+static adt_status scratch_on_current_device(void** out) {
+  int dev = -1;
+  ADT_HIP(hipGetDevice(&dev));
+  ADT_CHECK_ARG(dev >= 0 && dev < SCRATCH_MAX_DEVICES, ADT_E_UNSUPPORTED, "tree_attn_noalloc: device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    ADT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    ADT_CHECK_ARG(p != nullptr, ADT_E_HIP, "tree_attn_noalloc: no address for the scratch array");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return ADT_OK;
+}
+
+extern "C" adt_status adt_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache, int64_t stride_b,
+                                            int64_t stride_h, const int32_t* kv_len, const int32_t* n_q,
+                                            const int32_t* n_tail, const uint64_t* anc_mask, int32_t B, int32_t H,
+                                            int32_t Dh, int32_t nq_max, int32_t kv_cap, float scale, int32_t dtype,
+                                            void* out, void* stream) {
+  TRY(check_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask, B, H, Dh, nq_max, kv_cap,
+                      scale, dtype, out));
+  const size_t need = tree_attn_ws_need(B, H, Dh, nq_max, kv_cap, dtype);
+  ADT_CHECK_ARG(need <= ATTN_SCRATCH_BYTES, ADT_E_CAPACITY,
+                "tree_attn_noalloc: the key-split partials need %zu bytes, the scratch holds %zu", need,
+                ATTN_SCRATCH_BYTES);
+  void* ws = nullptr;
+  TRY(scratch_on_current_device(&ws));
+  return launch_tree_attn(q, k_cache, v_cache, stride_b, stride_h, kv_len, n_q, n_tail, anc_mask,
+                          AttnRows{nq_max, 1, nq_max}, B, H, Dh, nq_max, kv_cap, scale, dtype, out, ws,
+                          ATTN_SCRATCH_BYTES, (hipStream_t)stream);
 }
 
 extern "C" adt_status adt_tree_masks(const int32_t* parent, const int32_t* n_nodes, int32_t B, int32_t n_max,

@@ -859,6 +859,12 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
   return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
 }
 
+size_t tree_attn_ws_need(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
+  if (dtype == ADT_F32 || attn_use_blk(B, H, nq_max) || attn_use_wg(B, H, Dh, nq_max, kv_cap)) return 0;
+  const AttnPlan p = attn_plan(B, H, kv_cap);
+  return (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
+}
+
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st,
@@ -915,7 +921,7 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
     return ADT_OK;
   }
   const AttnPlan p = attn_plan(B, H, kv_cap);
-  const size_t need = (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
+  const size_t need = tree_attn_ws_need(B, H, Dh, nq_max, kv_cap, ADT_BF16);
   ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
                 need);
   float* part_o = (float*)ws;

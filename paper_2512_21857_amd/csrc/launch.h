@@ -32,6 +32,8 @@ struct AttnRows {
   }
 };
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype);
+// Exact scratch bytes one launch of these sizes uses (0 unless it splits the keys).
+size_t tree_attn_ws_need(int B, int H, int Dh, int nq_max, int kv_cap, int dtype);
 adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H,
                             int Dh, int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws,

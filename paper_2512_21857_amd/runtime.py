@@ -59,6 +59,21 @@ def tree_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_
     return out
 
 
+def tree_attn_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, kv_len: torch.Tensor,
+                      n_q: torch.Tensor, n_tail: torch.Tensor, mask: torch.Tensor, kv_cap: int,
+                      scale: Optional[float] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """tree_attn through adt_tree_attn_noalloc (the library's own scratch, no workspace)."""
+    _require_cuda(q, k_cache, v_cache, kv_len, n_q, n_tail, mask)
+    B, nq_max, H, Dh = q.shape
+    S_cap = k_cache.shape[2]
+    dt = abi.BF16 if q.dtype == torch.bfloat16 else abi.F32
+    out = torch.empty_like(q) if out is None else out
+    scale = 1.0 / float(np.sqrt(Dh)) if scale is None else scale
+    check(lib().adt_tree_attn_noalloc(_p(q), _p(k_cache), _p(v_cache), H * S_cap * Dh, S_cap * Dh, _p(kv_len), _p(n_q),
+                                      _p(n_tail), _p(mask), B, H, Dh, nq_max, kv_cap, scale, dt, _p(out), _stream()))
+    return out
+
+
 def tree_masks(parent: torch.Tensor, n_nodes: torch.Tensor, depth: bool = True):
     """parent int32 [B][n_max] -> (mask int64 [B][n_max][2] holding uint64 bits, depth int32 [B][n_max])."""
     _require_cuda(parent, n_nodes)

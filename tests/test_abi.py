@@ -178,3 +178,16 @@ def test_capture_arguments(L):
     assert L.adt_session_capture_count(None) == 0
     rec = abi.CaptureRec()
     assert L.adt_session_capture_record(None, 0, C.byref(rec)) == abi.E_ARG
+
+
+def test_tree_attn_noalloc_rejects_oversize_partials(L):
+    """Key-split partials beyond the library's 64 MiB scratch (120 pairs of 128-row trees over
+    10000 slots) are refused before anything is enqueued; argument errors are those of
+    adt_tree_attn."""
+    from paper_2512_21857_amd import abi
+    fake = 0x1000
+    assert L.adt_tree_attn_noalloc(fake, fake, fake, 0, 128 * 10000, fake, fake, fake, fake, 1, 120, 128, 128, 10000,
+                                   1.0, abi.BF16, fake, None) == abi.E_CAPACITY
+    assert "scratch" in abi.last_error()
+    assert L.adt_tree_attn_noalloc(None, fake, fake, 0, 64, fake, fake, fake, fake, 1, 1, 64, 1, 1, 1.0, abi.BF16, fake,
+                                   None) == abi.E_ARG
