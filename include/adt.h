@@ -495,6 +495,15 @@ adt_status adt_batch_step(adt_batch* b, adt_step_out* outs, void* stream);
 #define ADT_PROF_COMPACT 2  /* KV compaction */
 #define ADT_PROF_CLASSES 3
 adt_status adt_profile_enable(int32_t on);
+/* Probes of what the device sustains, to report beside the nominal peaks (HBM 8 TB/s, dense
+ * bf16 MFMA 2.5 PFLOP/s).  adt_probe_hbm_read streams `bytes` (a multiple of 16, 16-byte
+ * aligned device buffer) with 16-byte loads and folds them into `sink`; adt_probe_mfma runs
+ * `iters` rounds of back-to-back 32x32x16 bf16 MFMAs on register operands (no memory traffic)
+ * and reports the flops it launched in *flops [host].  sink: device scratch of at least
+ * adt_probe_sink_bytes() bytes.  Asynchronous on `stream`; the caller times them. */
+size_t adt_probe_sink_bytes(void);
+adt_status adt_probe_hbm_read(const void* buf, size_t bytes, void* sink, size_t sink_bytes, void* stream);
+adt_status adt_probe_mfma(int32_t iters, void* sink, size_t sink_bytes, double* flops, void* stream);
 adt_status adt_profile_read(int32_t cls, int64_t* launches, double* ms, double* bytes, double* flops, int32_t reset);
 
 #ifdef __cplusplus

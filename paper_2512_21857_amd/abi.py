@@ -122,6 +122,9 @@ _SIGS = {
     "adt_batch_destroy": (None, [p]),
     "adt_batch_step": (i32, [p, C.POINTER(StepOut), p]),
     "adt_profile_enable": (i32, [i32]),
+    "adt_probe_sink_bytes": (sz, []),
+    "adt_probe_hbm_read": (i32, [p, sz, p, sz, p]),
+    "adt_probe_mfma": (i32, [i32, p, sz, C.POINTER(C.c_double), p]),
     "adt_profile_read": (i32, [i32, C.POINTER(i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                C.POINTER(C.c_double), i32]),
 }

@@ -25,6 +25,7 @@ SOURCES = [
     "kernels/small.hip",
     "kernels/accept_sample.hip",
     "kernels/knn.hip",
+    "kernels/probe.hip",
 ]
 
 # Packed fp32 VALU instructions are disabled for the device code.

@@ -74,6 +74,24 @@ def tree_attn_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Ten
     return out
 
 
+def probe_hbm_read(buf: torch.Tensor, sink: torch.Tensor) -> None:
+    """One streaming read of buf (device, 16-byte multiple) by the library's probe kernel."""
+    _require_cuda(buf, sink)
+    check(lib().adt_probe_hbm_read(_p(buf), buf.numel() * buf.element_size(), _p(sink), sink.numel(), _stream()))
+
+
+def probe_mfma(iters: int, sink: torch.Tensor) -> float:
+    """Launches the MFMA-only probe; returns the flops it performs."""
+    _require_cuda(sink)
+    fl = C.c_double()
+    check(lib().adt_probe_mfma(iters, _p(sink), sink.numel(), C.byref(fl), _stream()))
+    return fl.value
+
+
+def probe_sink() -> torch.Tensor:
+    return torch.empty(lib().adt_probe_sink_bytes(), dtype=torch.uint8, device="cuda")
+
+
 def tree_masks(parent: torch.Tensor, n_nodes: torch.Tensor, depth: bool = True):
     """parent int32 [B][n_max] -> (mask int64 [B][n_max][2] holding uint64 bits, depth int32 [B][n_max])."""
     _require_cuda(parent, n_nodes)
