@@ -128,13 +128,14 @@ def profile_pass(abi, sess, k):
     import ctypes as C
     L = abi.lib()
     abi.check(L.adt_profile_enable(1))
-    for cls in (abi.PROF_GEMM, abi.PROF_ATTN, abi.PROF_COMPACT):
+    for cls in (abi.PROF_GEMM, abi.PROF_ATTN, abi.PROF_COMPACT, abi.PROF_ROWS):
         L.adt_profile_read(cls, None, None, None, None, 1)
     v0 = sess.view()
     run_steps(sess, k)
     v1 = sess.view()
     out = {"L_from": v0.L, "L_to": v1.L}
-    for name, cls in (("gemm", abi.PROF_GEMM), ("attn", abi.PROF_ATTN), ("compact", abi.PROF_COMPACT)):
+    for name, cls in (("gemm", abi.PROF_GEMM), ("attn", abi.PROF_ATTN), ("compact", abi.PROF_COMPACT),
+                      ("rows", abi.PROF_ROWS)):
         n, ms, by, fl = C.c_int64(), C.c_double(), C.c_double(), C.c_double()
         abi.check(L.adt_profile_read(cls, C.byref(n), C.byref(ms), C.byref(by), C.byref(fl), 1))
         out[name] = {"launches": n.value, "ms": ms.value, "bytes": by.value, "flops": fl.value}
@@ -144,12 +145,15 @@ def profile_pass(abi, sess, k):
 
 def roofline_of(prof, workload, kernel):
     g = prof["gemm"]
+    r = prof["rows"]
     avg_s = g["ms"] / max(g["launches"], 1) * 1e-3
     byts = g["bytes"] / max(g["launches"], 1)
     gbs = byts / avg_s / 1e9 if avg_s > 0 else 0.0
     return {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": gemm_traffic(workload), "launches": g["launches"],
-            "avg_us": round(avg_s * 1e6, 3), "bytes_per_launch": round(byts)}
+            "avg_us": round(avg_s * 1e6, 3), "bytes_per_launch": round(byts),
+            "residual_finish": {"launches": r["launches"], "avg_us": round(r["ms"] / max(r["launches"], 1) * 1e3, 3),
+                                "kernel": "resid_norm_kernel (K-range sums + residual add + RMSNorm)"}}
 
 
 def attn_of(prof):
@@ -473,7 +477,7 @@ def main():
                    "timed_from_cell": mid, "tokens_per_step": head["tokens_per_step"],
                    "nodes_per_step": head["nodes_per_step"], "mean_depth": head["mean_depth"],
                    "tokens_per_s": head["tokens_per_s"]},
-        "roofline": roofline_of(prof_mid, "lumina_7b", "gemm_tile_kernel (bf16 projections with fused epilogues)"),
+        "roofline": roofline_of(prof_mid, "lumina_7b", "gemm_rows_kernel (bf16 projections, fused epilogues or K-range sums)"),
         "tree_attn": {"in_cycle_mid_image": attn_of(prof_mid), "in_cycle_end_of_image": attn_of(prof_end)},
         "full_image": full,
     }
@@ -514,7 +518,7 @@ def main():
             del s
             s, fr = workload_run(rt, ldm, lcfg, lpre, min(K, 50), 3, lcfg.n_image // 2, fixed_tree=True)
             del s
-            r["roofline"] = roofline_of(lprof, "llamagen_xl", "gemm_tile_kernel")
+            r["roofline"] = roofline_of(lprof, "llamagen_xl", "gemm_rows_kernel")
             r["tree_attn_in_cycle"] = attn_of(lprof)
             r["fixed_tree_depth6_width10"] = fr
             line["llamagen_xl"] = r

@@ -493,7 +493,8 @@ adt_status adt_batch_step(adt_batch* b, adt_step_out* outs, void* stream);
 #define ADT_PROF_GEMM 0     /* dense projections (bf16 MFMA or fp32) */
 #define ADT_PROF_ATTN 1     /* tree attention + split merge */
 #define ADT_PROF_COMPACT 2  /* KV compaction */
-#define ADT_PROF_CLASSES 3
+#define ADT_PROF_ROWS 3     /* finish of a residual projection: K-range sums, residual add, RMSNorm */
+#define ADT_PROF_CLASSES 4
 adt_status adt_profile_enable(int32_t on);
 /* Probes of what the device sustains, to report beside the nominal peaks (HBM 8 TB/s, dense
  * bf16 MFMA 2.5 PFLOP/s).  adt_probe_hbm_read streams `bytes` (a multiple of 16, 16-byte

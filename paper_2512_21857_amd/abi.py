@@ -129,7 +129,7 @@ _SIGS = {
                                C.POINTER(C.c_double), i32]),
 }
 
-PROF_GEMM, PROF_ATTN, PROF_COMPACT = 0, 1, 2
+PROF_GEMM, PROF_ATTN, PROF_COMPACT, PROF_ROWS = 0, 1, 2, 3
 
 EXPORTED = tuple(_SIGS)
 

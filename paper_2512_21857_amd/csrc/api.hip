@@ -533,7 +533,6 @@ struct adt_session_s {
   int a_prev = 0, d_prev = 0, prev_cell = 0;
   // device buffers
   float *h, *part, *logits, *dlogits;
-  float* ssp;   // bf16: per-16-column sums of squares of the residual rows [R][d_model/16]
   void *act, *xin, *q, *att, *sw, *feat, *cfeat, *dfeat;
   size_t part_elems;
   TreeBufs tr;
@@ -598,8 +597,9 @@ static void session_dims(adt_session_s* s, const adt_model_s* m, const adt_sessi
   s->KR = std::max(kh, 1);
   s->C = std::max(kw, kh + (dh - 1) * kh * kh);
   if (d->accept.mode == ADT_ACCEPT_MSS) s->C = std::max(s->C, R);   // every drawn child is kept
-  // fp32 projections write [rows][N] products for the row kernels; bf16 ones finish in place
-  size_t pe = 256;
+  // fp32 projections write [rows][N] products for the row kernels; bf16 residual projections
+  // (O, down, draft FC) write up to GEMM_MAX_SPLITS K-range sums of [rows][d_model]
+  size_t pe = (size_t)GEMM_MAX_SPLITS * R * s->dm;
   if (s->dt == ADT_F32)
     for (int n : {3 * s->dm, s->dm, 2 * s->F, s->V}) pe = std::max(pe, (size_t)R * n);
   s->part_elems = pe;
@@ -619,7 +619,6 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->cfeat = b.take<char>((size_t)s->nb * s->C0 * dm * es);
   s->dfeat = b.take<char>((size_t)s->nb * s->DR * dm * es);
   s->part = b.take<float>(s->part_elems);
-  s->ssp = b.take<float>((size_t)R * (dm / 16));
   s->logits = b.take<float>((size_t)R * s->V);
   s->dlogits = b.take<float>((size_t)s->DLR * s->V);
   if (s->nb > 1) {
@@ -797,10 +796,10 @@ static int64_t gkey(int kind, int a, int b, int c) {
 
 // Algorithmic HBM bytes of a projection: weights once, the input rows, fp32 output rows.
 static adt_status gemm_p(const void* X, int ldx, const void* W, int M, int N, int K, int dt, float* part,
-                         hipStream_t st, const GemmEpi& epi = GemmEpi{}) {
+                         hipStream_t st, const GemmEpi& epi = GemmEpi{}, int* splits = nullptr) {
   const int e = prof_pair();
   adt_status r = launch_gemm(X, ldx, W, M, N, K, dt, part, epi, st, e >= 0 ? g_prof.ev[e] : nullptr,
-                             e >= 0 ? g_prof.ev[e + 1] : nullptr);
+                             e >= 0 ? g_prof.ev[e + 1] : nullptr, splits);
   prof_done(e, ADT_PROF_GEMM, (double)N * K * esize(dt) + (double)M * K * esize(dt) + (double)M * N * 4.0,
             2.0 * M * N * K);
   return r;
@@ -856,6 +855,15 @@ static adt_status capt_snap(adt_session_s* s, int idx, hipStream_t st) {
   return ADT_OK;
 }
 
+// Finish of a bf16 residual projection: its K-range sums added to the residual rows (or
+// assigned) and the rows' RMSNorm into out.
+static adt_status resid_finish(adt_session_s* s, int splits, int rows, int assign, void* out, hipStream_t st) {
+  const int e = prof_begin(st);
+  TRY(launch_resid_norm(s->part, splits, rows, s->dm, assign, s->m->d.norm_eps, s->h, out, s->dt, st));
+  prof_end(e, ADT_PROF_ROWS, (double)splits * rows * s->dm * 4.0 + rows * s->dm * (8.0 + esize(s->dt)), 0.0, st);
+  return ADT_OK;
+}
+
 // Decoder layers over the nb * M rows of M tree nodes (branches interleaved node by node).
 static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
                              const uint64_t* mask, void* final_out, hipStream_t st) {
@@ -880,22 +888,20 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
     return ADT_OK;
   };
   if (dt == ADT_BF16) {
-    // Per layer: QKV (norm on load; RoPE + cache append), attention, O (residual add),
-    // gate/up (norm on load; SwiGLU), down (residual add).  The residual epilogues leave the
-    // per-16-column sums of squares that the next norm-on-load consumer reduces.
-    GemmEpi resid;
-    resid.mode = EPI_RESID;
-    resid.h = s->h;
-    resid.ssp_out = s->ssp;
+    // Per layer: QKV (RoPE + cache append) from the normalised rows in act, attention, O (K-range
+    // sums) and its finish (residual add, the MLP's RMSNorm into act), gate/up (SwiGLU), down
+    // and its finish (residual add, the next layer's RMSNorm into act, or the final norm into
+    // final_out after the last layer).
+    GemmEpi pe;
+    pe.mode = EPI_PART;
+    pe.part = s->part;
+    pe.part_elems = s->part_elems;
     for (int l = l0; l < l1; ++l) {
       char* kc = draft ? (char*)s->d.dk_cache : (char*)s->d.k_cache + (size_t)l * H * stride_h * es;
       char* vc = draft ? (char*)s->d.dv_cache : (char*)s->d.v_cache + (size_t)l * H * stride_h * es;
       TRY(capt_snap(s, 2 * (l - l0), st));
       GemmEpi qkv;
       qkv.mode = EPI_QKV;
-      qkv.ssp_in = s->ssp;
-      qkv.nss_in = dm / 16;
-      qkv.eps = eps;
       qkv.q = (uint16_t*)s->q;
       qkv.kc = (uint16_t*)kc;
       qkv.vc = (uint16_t*)vc;
@@ -906,21 +912,20 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       qkv.Dh = Dh;
       qkv.nb = nb;
       qkv.cache_sb = cache_sb;
-      TRY(gemm_p(s->h, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
+      TRY(gemm_p(s->act, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
-      TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st, resid));
+      int sp = 1;
+      TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st, pe, &sp));
+      TRY(resid_finish(s, sp, rows, 0, s->act, st));
       TRY(capt_snap(s, 2 * (l - l0) + 1, st));
       GemmEpi sw;
       sw.mode = EPI_SWIGLU;
-      sw.ssp_in = s->ssp;
-      sw.nss_in = dm / 16;
-      sw.eps = eps;
       sw.act = (uint16_t*)s->sw;
-      TRY(gemm_p(s->h, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
-      TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st, resid));
+      TRY(gemm_p(s->act, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
+      TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st, pe, &sp));
+      TRY(resid_finish(s, sp, rows, 0, (l + 1 == l1 && final_out) ? final_out : s->act, st));
     }
     TRY(capt_snap(s, 2 * (l1 - l0), st));
-    if (final_out) TRY(launch_norm_rows(s->h, s->ssp, rows, dm, eps, final_out, dt, st));
     return ADT_OK;
   }
   // fp32: products into part, row kernels finish each step
@@ -969,10 +974,9 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
                                  int64_t key = -1, int tok_boff = 0) {
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
-    const bool bf = s->dt == ADT_BF16;
     TRY(capt_begin(s, false, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
-    TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, bf ? nullptr : s->act,
-                          bf ? s->ssp : nullptr, s->dt, cs, Branches{s->nb, tok_boff, 0}));
+    TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, cs,
+                          Branches{s->nb, tok_boff, 0}));
     TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
     if (lm_rows > 0)
       TRY(lm_head(s, (const char*)s->feat + (size_t)s->nb * lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits,
@@ -1001,11 +1005,12 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
                              (size_t)rows * 2 * dm * esize(dt), hipMemcpyDeviceToDevice, cs));
     if (dt == ADT_BF16) {
       GemmEpi e;
-      e.mode = EPI_RESID;
-      e.h = s->h;
-      e.assign = 1;
-      e.ssp_out = s->ssp;
-      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e));
+      e.mode = EPI_PART;
+      e.part = s->part;
+      e.part_elems = s->part_elems;
+      int sp = 1;
+      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e, &sp));
+      TRY(resid_finish(s, sp, rows, 1, s->act, cs));
     } else {
       TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs));
       TRY(launch_add_norm(s->part, 1, rows, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
@@ -1552,7 +1557,7 @@ static adt_status batch_forward(adt_batch_s* bt, int M, int nq_max, hipStream_t 
   const int dm = s0->dm, H = s0->H, Dh = s0->Dh, F = s0->F, V = s0->V, dt = s0->dt;
   const float eps = m->d.norm_eps, scale = 1.f / std::sqrt((float)Dh);
   const int64_t stride_h = (int64_t)s0->d.s_cap * Dh;
-  TRY(launch_embed_norm(m->d.embed, bt->tok, M, dm, eps, bt->h, bt->a, nullptr, dt, st));
+  TRY(launch_embed_norm(m->d.embed, bt->tok, M, dm, eps, bt->h, bt->a, dt, st));
   for (int l = 0; l < s0->Lr; ++l) {
     char* kc = (char*)s0->d.k_cache + (size_t)l * H * stride_h * 2;
     char* vc = (char*)s0->d.v_cache + (size_t)l * H * stride_h * 2;

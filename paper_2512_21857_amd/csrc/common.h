@@ -64,16 +64,6 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// RMSNorm scale of one row from its per-16-column sums of squares ssp[0..nss): each lane
-// sums a strided subset in order, then a fixed butterfly, so every kernel that needs the
-// scale of a row gets the same bits.  Called by a whole wave.
-__device__ __forceinline__ float row_norm_scale(const float* __restrict__ ssp, int nss, int d, float eps) {
-  float t = 0.f;
-  for (int i = threadIdx.x % WAVE; i < nss; i += WAVE) t += ssp[i];
-  t = wave_sum(t);
-  return rsqrtf(t / d + eps);
-}
-
 // Block-wide sum for blockDim.x a multiple of 64 (<= 1024); `red` holds >= 16 floats.
 __device__ __forceinline__ float block_sum(float v, float* red) {
   v = wave_sum(v);

@@ -3,15 +3,20 @@
 // At batch 1 the tree has M <= 128 rows, so these products stream the weights from HBM
 // once and are bandwidth-bound (arithmetic intensity ~ M flop/byte).  The bf16 path packs
 // W once into 16x32 MFMA tiles (1 KB contiguous per tile, one 16-byte load per lane) so a
-// wave reads whole kilobytes per instruction.  One workgroup owns one 16-column output
-// tile and the whole K range: its eight waves take contiguous K chunks, issue all their
-// weight loads at once, and the partial tiles are summed in LDS in wave order (so results
-// are deterministic and no workgroup waits on another).  The finished tile goes through a
-// fused epilogue: residual add with the row sums of squares the next RMSNorm needs, RoPE
-// with the K/V cache append, SwiGLU, or a plain store.  A GEMM whose input is a normalised
-// row applies the norm while loading it (fp32 residual times the row's scale, rounded to
-// bf16), so no norm, RoPE, SwiGLU or reduction kernel runs between projections.
+// wave reads whole kilobytes per instruction.  A workgroup owns T adjacent 16-column tiles
+// and one of S contiguous K ranges; its eight waves split that range, keep the next k-tiles'
+// weight and input fragments in flight while multiplying the current ones, and sum their
+// partial tiles in LDS in wave order (deterministic; no workgroup waits on another).  T and
+// S are chosen so that about one workgroup lands on each CU with as many columns as its
+// registers allow: every workgroup reads the M input rows of its K range, so more columns
+// per workgroup mean fewer re-reads of the input per weight byte.  The input rows are the
+// bf16 activations the previous step stored (the residual projections' finish writes the
+// next RMSNorm output).  With S = 1 the finished tile runs a fused epilogue (RoPE with the
+// K/V cache append, SwiGLU, or a plain store); residual projections store their K-range
+// sums, and resid_norm adds them in range order.
 #include <hip/hip_ext.h>
+
+#include <algorithm>
 
 #include "../launch.h"
 
@@ -84,14 +89,6 @@ __global__ void pack_f32_kernel(PackSrc s, int N, int K, float* __restrict__ dst
 constexpr int TILE_WAVES = 8;
 constexpr int TILE_THREADS = TILE_WAVES * WAVE;
 
-// Eight consecutive fp32 residual values times the row's norm scale, rounded to bf16.
-__device__ __forceinline__ bf16x8 norm_load8(const float* __restrict__ p, float r) {
-  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
-  const u16x8 u{f2bf(a.x * r), f2bf(a.y * r), f2bf(a.z * r), f2bf(a.w * r),
-                f2bf(b.x * r), f2bf(b.y * r), f2bf(b.z * r), f2bf(b.w * r)};
-  return __builtin_bit_cast(bf16x8, u);
-}
-
 __device__ __forceinline__ f32x4 shfl_xor4(f32x4 v, int mask) {
   return f32x4{__shfl_xor(v[0], mask, WAVE), __shfl_xor(v[1], mask, WAVE), __shfl_xor(v[2], mask, WAVE),
                __shfl_xor(v[3], mask, WAVE)};
@@ -105,19 +102,6 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
   const int c = nt * 16 + 4 * g;
   if (e.mode == EPI_STORE) {
     if (live) *reinterpret_cast<f32x4*>(e.out + row * e.ldo + c) = y;
-  } else if (e.mode == EPI_RESID) {
-    float* hp = e.h + (int64_t)row * N + c;
-    if (live) {
-      if (!e.assign) {
-        const f32x4 o = *reinterpret_cast<const f32x4*>(hp);
-        y = f32x4{o[0] + y[0], o[1] + y[1], o[2] + y[2], o[3] + y[3]};
-      }
-      *reinterpret_cast<f32x4*>(hp) = y;
-    }
-    float ss = live ? y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3] : 0.f;
-    ss += __shfl_xor(ss, 16, WAVE);
-    ss += __shfl_xor(ss, 32, WAVE);
-    if (live && g == 0) e.ssp_out[(int64_t)row * (N / 16) + nt] = ss;
   } else if (e.mode == EPI_QKV) {
     const f32x4 y2 = shfl_xor4(y, 32);
     if (live && g < 2) {
@@ -153,134 +137,80 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
   }
 }
 
-// k-tiles per wave per load round: as many as fit about 160 VGPRs of loaded operands (a
-// workgroup of 8 waves holds 2 waves per SIMD, so 256 VGPRs per lane are available).
-template <int MT, int NTW, bool NORM>
-constexpr int tile_kc() {
-  constexpr int per = MT * (NORM ? 8 : 4) + NTW * 4;
-  constexpr int kc = (MT >= 6 ? 120 : 160) / per;   // the widest row blocks keep room for accumulators
-  return kc < 1 ? 1 : (kc > 16 ? 16 : kc);
-}
-
-// MT = 16-row blocks of M, NTW = 16-column tiles per workgroup.  Every load of a round is
-// issued before any is used (indices clamped instead of branched on, so the loads form one
-// batch); rounds past the wave's K range and rows past M only feed discarded results.
-template <int MT, int NTW, bool NORM>
-__global__ __launch_bounds__(TILE_THREADS) void gemm_tile_kernel(const void* __restrict__ Xv, int ldx,
-                                                                 const uint16_t* __restrict__ Wp, int M, int N,
-                                                                 int K, GemmEpi epi) {
-  constexpr int KC = tile_kc<MT, NTW, NORM>();
-  constexpr int TT = MT * NTW;               // 16x16 output blocks per workgroup
+// MT = 16-row blocks of M, T = 16-column tiles per workgroup, KC = k-tiles per load round.
+// Workgroup b takes column block b / S and K range b % S; wave w takes the w-th eighth of the
+// range.  Rounds are double-buffered: round r + 1's fragments are requested before round r's
+// MFMAs, so one round stays in flight per wave.  With stagger the wave starts its rounds at an
+// offset that depends on the workgroup (wrapping around its chunk), so the waves of different
+// CUs do not read the same input lines at the same time; the sum order stays fixed per tile.
+// Loads past the wave's range are clamped to its last k-tile and their products discarded.
+template <int MT, int T, int KC>
+__global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t* __restrict__ X, int ldx,
+                                                                 const uint16_t* __restrict__ Wp, int M, int N, int K,
+                                                                 int S, int stagger, GemmEpi epi) {
+  constexpr int TT = MT * T;                 // 16x16 output blocks per workgroup
   constexpr int TR = TT < 4 ? TT : 4;        // blocks summed per LDS round
   __shared__ f32x4 red[TILE_WAVES][TR][WAVE];
-  __shared__ float rscale[NORM ? MT * 16 : 1];
   const int KT = K / 32;
-  // the wave index is made scalar, so the K range and the round bounds below are uniform
-  // branches that do not split the batch of loads
+  const int cb = blockIdx.x / S, sp = blockIdx.x % S;
+  // the wave index is made scalar, so the K range and the round bounds are uniform branches
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
-  const int kt0 = (int)((int64_t)KT * wave / TILE_WAVES), kt1 = (int)((int64_t)KT * (wave + 1) / TILE_WAVES);
-  const bf16x8* wp[NTW];
+  const int ks0 = (int)((int64_t)KT * sp / S), ks1 = (int)((int64_t)KT * (sp + 1) / S);
+  const int kt0 = ks0 + (int)((int64_t)(ks1 - ks0) * wave / TILE_WAVES);
+  const int kt1 = ks0 + (int)((int64_t)(ks1 - ks0) * (wave + 1) / TILE_WAVES);
+  const int nk = kt1 - kt0, span = (nk + KC - 1) / KC * KC;
+  const int rot = (stagger && nk > 0) ? (int)((blockIdx.x * 37u) % (unsigned)(span / KC)) * KC : 0;
+  const bf16x8* wp[T];
 #pragma unroll
-  for (int t = 0; t < NTW; ++t)
-    wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(blockIdx.x * NTW + t) * KT * 64 + lane;
-
-  bf16x8 wf[KC][NTW];
-  auto load_w = [&](int c) {
+  for (int t = 0; t < T; ++t) wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(cb * T + t) * KT * 64 + lane;
+  const uint16_t* xp[MT];
 #pragma unroll
-    for (int j = 0; j < KC; ++j)
-      if (c + j < kt1)
-#pragma unroll
-        for (int t = 0; t < NTW; ++t) wf[j][t] = wp[t][(int64_t)(c + j) * 64];
+  for (int m = 0; m < MT; ++m) xp[m] = X + (int64_t)min(m * 16 + lq, M - 1) * ldx + g * 8;
+  // round start of the i-th round (c = kt0 + i * KC) after the rotation
+  auto kmap = [&](int c) {
+    int r = c - kt0 + rot;
+    if (r >= span) r -= span;
+    return kt0 + r;
   };
-  const float* xf32[MT];
-  const uint16_t* xb16[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    const int row = min(m * 16 + lq, M - 1);
-    xf32[m] = (const float*)Xv + (int64_t)row * ldx + g * 8;
-    xb16[m] = (const uint16_t*)Xv + (int64_t)row * ldx + g * 8;
-  }
-  float4 xa[KC][MT][NORM ? 2 : 1];
-  bf16x8 xb[KC][MT];
-  auto load_x = [&](int c) {
+  bf16x8 wa[KC][T], xa[KC][MT], wb[KC][T], xb[KC][MT];
+  auto load = [&](bf16x8(&w)[KC][T], bf16x8(&x)[KC][MT], int c) {
+    const int c0 = kmap(c);
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
-      if (c + j >= kt1) continue;
-      const int kk = c + j;
+      const int kk = min(c0 + j, kt1 - 1);
 #pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        if constexpr (NORM) {
-          xa[j][m][0] = *reinterpret_cast<const float4*>(xf32[m] + kk * 32);
-          xa[j][m][NORM ? 1 : 0] = *reinterpret_cast<const float4*>(xf32[m] + kk * 32 + 4);
-        } else {
-          xb[j][m] = *reinterpret_cast<const bf16x8*>(xb16[m] + kk * 32);
-        }
-      }
+      for (int t = 0; t < T; ++t) w[j][t] = wp[t][(int64_t)kk * 64];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) x[j][m] = *reinterpret_cast<const bf16x8*>(xp[m] + kk * 32);
     }
   };
-  // the first round's weights and inputs are in flight while the norm scales are formed
-  load_w(kt0);
-  load_x(kt0);
-
-  float rr[MT];
-  if constexpr (NORM) {
-    // Row scales from the per-16-column sums of squares: LPR consecutive lanes per row
-    // each sum a strided subset in order, then a fixed butterfly across the LPR lanes.
-    constexpr int ROWS = MT * 16;
-    constexpr int LPR = TILE_THREADS / ROWS >= 32 ? 32 : (TILE_THREADS / ROWS >= 16 ? 16 : (TILE_THREADS / ROWS >= 8 ? 8 : 4));
-    const int row = threadIdx.x / LPR, part = threadIdx.x % LPR;
-    float t = 0.f;
-    if (row < ROWS) {
-      const float* sp = epi.ssp_in + (int64_t)min(row, M - 1) * epi.nss_in;
-      const int nss = epi.nss_in;
-      for (int i0 = part; i0 < nss; i0 += 8 * LPR) {
-        float v[8];
+  f32x4 acc[T][MT];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = sp[min(i0 + j * LPR, nss - 1)];   // one batch of loads
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (i0 + j * LPR < nss) t += v[j];
-      }
-    }
-#pragma unroll
-    for (int o = LPR / 2; o >= 1; o >>= 1) t += __shfl_xor(t, o, WAVE);
-    if (row < ROWS && part == 0) rscale[row] = row < M ? rsqrtf(t / K + epi.eps) : 0.f;
-    __syncthreads();
-#pragma unroll
-    for (int m = 0; m < MT; ++m) rr[m] = rscale[m * 16 + lq];
-  }
-
-  f32x4 acc[NTW][MT];
-#pragma unroll
-  for (int t = 0; t < NTW; ++t)
+  for (int t = 0; t < T; ++t)
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[t][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  for (int c = kt0; c < kt1; c += KC) {
-    const int nk = min(KC, kt1 - c);
+  auto mma = [&](bf16x8(&w)[KC][T], bf16x8(&x)[KC][MT], int c) {
+    const int c0 = kmap(c);
 #pragma unroll
-    for (int j = 0; j < KC; ++j) {
-      if (j < nk) {
+    for (int j = 0; j < KC; ++j)
+      if (c0 + j < kt1)
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-          bf16x8 x;
-          if constexpr (NORM) {
-            const float4 a = xa[j][m][0], b = xa[j][m][NORM ? 1 : 0];
-            const float r = rr[m];
-            x = __builtin_bit_cast(bf16x8, u16x8{f2bf(a.x * r), f2bf(a.y * r), f2bf(a.z * r), f2bf(a.w * r),
-                                                 f2bf(b.x * r), f2bf(b.y * r), f2bf(b.z * r), f2bf(b.w * r)});
-          } else {
-            x = xb[j][m];
-          }
+        for (int m = 0; m < MT; ++m)
 #pragma unroll
-          for (int t = 0; t < NTW; ++t) acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j][t], x, acc[t][m], 0, 0, 0);
-        }
-      }
-    }
-    if (c + KC < kt1) {
-      load_w(c + KC);
-      load_x(c + KC);
+          for (int t = 0; t < T; ++t) acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[j][t], x[j][m], acc[t][m], 0, 0, 0);
+  };
+  if (nk > 0) {
+    load(wa, xa, kt0);
+    for (int c = kt0;;) {
+      if (c + KC < kt1) load(wb, xb, c + KC);
+      mma(wa, xa, c);
+      c += KC;
+      if (c >= kt1) break;
+      if (c + KC < kt1) load(wa, xa, c + KC);
+      mma(wb, xb, c);
+      c += KC;
+      if (c >= kt1) break;
     }
   }
   // Sum the waves' partial blocks in wave order; wave i then finishes block q0 + i.
@@ -288,7 +218,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_tile_kernel(const void* __r
   for (int q0 = 0; q0 < TT; q0 += TR) {
 #pragma unroll
     for (int i = 0; i < TR; ++i)
-      if (q0 + i < TT) red[wave][i][lane] = acc[(q0 + i) / MT % NTW][(q0 + i) % MT];
+      if (q0 + i < TT) red[wave][i][lane] = acc[(q0 + i) / MT % T][(q0 + i) % MT];
     __syncthreads();
     if (wave < TR && q0 + wave < TT) {
       f32x4 y = red[0][wave][lane];
@@ -298,7 +228,12 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_tile_kernel(const void* __r
         y = f32x4{y[0] + v[0], y[1] + v[1], y[2] + v[2], y[3] + v[3]};
       }
       const int q = q0 + wave;
-      tile_epilogue(epi, y, (q % MT) * 16 + lq, g, blockIdx.x * NTW + q / MT, M, N);
+      const int row = (q % MT) * 16 + lq, nt = cb * T + q / MT;
+      if (epi.mode == EPI_PART) {
+        if (row < M) *reinterpret_cast<f32x4*>(epi.part + ((int64_t)sp * M + row) * N + nt * 16 + 4 * g) = y;
+      } else {
+        tile_epilogue(epi, y, row, g, nt, M, N);
+      }
     }
     __syncthreads();
   }
@@ -366,21 +301,55 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
   return ADT_OK;
 }
 
+// Tiles per workgroup T and K ranges S for M rows of an N x K product.  Measured on the 7B
+// layer shapes (K 4096 / 11008, N 4096 - 65536) at 4, 11 and 61 rows: one workgroup per CU
+// (256) with the widest T the registers allow wins; at 61 rows QKV 768 tiles T = 3 (256
+// workgroups) 27 against 48 us, O and down (256 tiles) T = 4 with 4 K ranges 12 / 26 against
+// 20 / 52 us, gate/up T = 4 (344) 62 against 96 us; at <= 16 rows the narrower T = 1-3 that
+// give 256-2048 workgroups (LM head T = 2, 86 against 112 us).  partial: the caller adds the
+// K-range sums (residual projections), so S may exceed 1.
+RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
+  const int mt = (M + 15) / 16, tiles = N / 16, KT = K / 32;
+  const int tmax = mt <= 4 ? 4 : 2;
+  auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
+  if (!partial || (mt == 1 && tiles >= 192)) {
+    // one K range: the widest T that still gives >= 256 workgroups (at one row block, wider
+    // than 2 only if that is exactly one workgroup per CU)
+    int T = 1;
+    for (int t : {4, 3, 2})
+      if (ok(t) && tiles / t >= 256 && (mt > 1 || t <= 2 || tiles / t <= 256)) {
+        T = t;
+        break;
+      }
+    return {T, 1};
+  }
+  // K ranges: each wave keeps at least two k-tiles
+  const int smax = std::max(1, std::min(GEMM_MAX_SPLITS, KT / (2 * TILE_WAVES)));
+  int T = 1;
+  for (int t : {4, 3, 2})
+    if (ok(t) && (tiles / t) * smax >= 192) {
+      T = t;
+      break;
+    }
+  const int blocks = tiles / T;
+  const int S = blocks >= 192 ? 1 : std::max(1, std::min(smax, 256 / blocks));
+  return {T, S};
+}
+
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
-                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, int* splits) {
   ADT_CHECK_ARG(M >= 1 && M <= 128, ADT_E_CAPACITY, "gemm: M=%d outside [1,128]", M);
   if (dtype == ADT_F32) {
     hipExtLaunchKernelGGL(gemm_f32_kernel, dim3((N + 3) / 4), dim3(256), 0, st, ev0, ev1, 0, (const float*)X, ldx,
                           (const float*)Wp, M, N, K, part);
     ADT_LAUNCH_CHECK();
+    if (splits) *splits = 1;
     return ADT_OK;
   }
   ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0 && ldx % 8 == 0, ADT_E_SHAPE, "gemm: N=%d K=%d ldx=%d misaligned", N, K, ldx);
-  const bool norm = epi.ssp_in != nullptr;
-  ADT_CHECK_ARG(!norm || epi.nss_in == K / 16, ADT_E_SHAPE, "gemm: norm input needs K/16 sums per row");
   switch (epi.mode) {
     case EPI_STORE: ADT_CHECK_ARG(epi.out && epi.ldo % 4 == 0, ADT_E_ARG, "gemm: store target"); break;
-    case EPI_RESID: ADT_CHECK_ARG(epi.h && epi.ssp_out, ADT_E_ARG, "gemm: residual epilogue buffers"); break;
+    case EPI_PART: ADT_CHECK_ARG(epi.part != nullptr, ADT_E_ARG, "gemm: partial-sum buffer"); break;
     case EPI_QKV:
       ADT_CHECK_ARG(epi.nb == 1 || epi.nb == 2, ADT_E_ARG, "gemm: QKV epilogue branches %d", epi.nb);
       ADT_CHECK_ARG(epi.Dh >= 16 && epi.Dh % 16 == 0 && N % (3 * epi.Dh) == 0 && epi.q && epi.kc && epi.vc &&
@@ -390,52 +359,44 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     case EPI_SWIGLU: ADT_CHECK_ARG(epi.act != nullptr, ADT_E_ARG, "gemm: SwiGLU output"); break;
     default: ADT_CHECK_ARG(false, ADT_E_ARG, "gemm: epilogue %d", epi.mode);
   }
+  const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART);
+  ADT_CHECK_ARG(epi.mode != EPI_PART || (size_t)p.S * M * N <= epi.part_elems, ADT_E_CAPACITY,
+                "gemm: %d K-range sums of %d x %d exceed the partial buffer", p.S, M, N);
   const int mt = (M + 15) / 16;
-  // 16-column tiles per workgroup: each wave's input fragments feed all of them, so more
-  // tiles cut the re-reads of the input rows, but fewer workgroups leave CUs idle.  The
-  // largest of 4, 2, 1 that keeps at least 160 workgroups (measured best on the 36-layer
-  // d = 1280 cycle among 96, 160, 256 and always 1; at most 2 from 81 rows on, for registers)
-  const int tiles = N / 16;
-  int ntw = 1;
-  if (tiles % 4 == 0 && tiles / 4 >= 160 && mt <= 4) ntw = 4;
-  else if (tiles % 2 == 0 && tiles / 2 >= 160) ntw = 2;
-  const dim3 grid(tiles / ntw), block(TILE_THREADS);
+  const int stagger = 1;
+  const dim3 grid(N / 16 / p.T * p.S), block(TILE_THREADS);
+  const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)Wp;
-#define ADT_GEMM(...) hipExtLaunchKernelGGL(__VA_ARGS__, grid, block, 0, st, ev0, ev1, 0, X, ldx, w, M, N, K, epi)
-#define ADT_GEMM_MT(MT, NORM)                          \
-  if (ntw == 4) {                                      \
-    ADT_GEMM(gemm_tile_kernel<MT, 4, NORM>);           \
-  } else if (ntw == 2) {                               \
-    ADT_GEMM(gemm_tile_kernel<MT, 2, NORM>);           \
-  } else {                                             \
-    ADT_GEMM(gemm_tile_kernel<MT, 1, NORM>);           \
+#define ADT_GR(MTV, TV, KCV)                                                                                  \
+  hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, p.S, \
+                        stagger, epi)
+#define ADT_GR_T4(MTV, KCV)              \
+  switch (p.T) {                         \
+    case 4: ADT_GR(MTV, 4, KCV); break;  \
+    case 3: ADT_GR(MTV, 3, KCV); break;  \
+    case 2: ADT_GR(MTV, 2, KCV); break;  \
+    default: ADT_GR(MTV, 1, KCV); break; \
   }
-#define ADT_GEMM_MT2(MT, NORM)                         \
-  if (ntw >= 2) {                                      \
-    ADT_GEMM(gemm_tile_kernel<MT, 2, NORM>);           \
-  } else {                                             \
-    ADT_GEMM(gemm_tile_kernel<MT, 1, NORM>);           \
+#define ADT_GR_T2(MTV, KCV)              \
+  if (p.T >= 2) {                        \
+    ADT_GR(MTV, 2, KCV);                 \
+  } else {                               \
+    ADT_GR(MTV, 1, KCV);                 \
   }
-#define ADT_GEMM_ALL(NORM)             \
-  switch (mt) {                        \
-    case 1: ADT_GEMM_MT(1, NORM) break; \
-    case 2: ADT_GEMM_MT(2, NORM) break; \
-    case 3: ADT_GEMM_MT(3, NORM) break; \
-    case 4: ADT_GEMM_MT(4, NORM) break; \
-    case 5:                            \
-    case 6: ADT_GEMM_MT2(6, NORM) break; \
-    default: ADT_GEMM_MT2(8, NORM) break; \
+  switch (mt) {
+    case 1: ADT_GR_T4(1, 3) break;
+    case 2: ADT_GR_T4(2, 2) break;
+    case 3: ADT_GR_T4(3, 2) break;
+    case 4: ADT_GR_T4(4, 2) break;
+    case 5:
+    case 6: ADT_GR_T2(6, 2) break;
+    default: ADT_GR_T2(8, 2) break;
   }
-  if (norm) {
-    ADT_GEMM_ALL(true)
-  } else {
-    ADT_GEMM_ALL(false)
-  }
-#undef ADT_GEMM_ALL
-#undef ADT_GEMM_MT2
-#undef ADT_GEMM_MT
-#undef ADT_GEMM
+#undef ADT_GR_T2
+#undef ADT_GR_T4
+#undef ADT_GR
   ADT_LAUNCH_CHECK();
+  if (splits) *splits = p.S;
   return ADT_OK;
 }
 

@@ -1,6 +1,5 @@
-// Row-wise kernels of the forwards and of the cache bookkeeping: embedding (with its norm,
-// or with the per-16-column sums of squares the bf16 GEMMs normalise from), the final norm,
-// the fp32 path's finishing steps after each projection (residual add + RMSNorm, RoPE + KV
+// Row-wise kernels of the forwards and of the cache bookkeeping: embedding with its norm, the
+// finish of a residual projection (K-range sums, residual add, the next norm), the fp32 path's finishing steps after each projection (residual add + RMSNorm, RoPE + KV
 // append, SwiGLU, logits), feature gathers, KV compaction and ancestor masks.  Each kernel
 // handles whole rows (at most 128 tree rows per launch), so they are latency-bound and kept
 // as simple as possible.
@@ -16,24 +15,10 @@ constexpr int ROW_THREADS = 256;
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                  int d, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ a, float* __restrict__ ssp,
-                                                                 Branches br) {
+                                                                 T* __restrict__ a, Branches br) {
   __shared__ float red[16];
   const int m = blockIdx.x;
   const T* e = E + (int64_t)tok[m / br.nb + (m % br.nb) * br.tok_boff] * d;
-  if (ssp) {
-    // per 16-column tile: copy to h and the tile's sum of squares (columns in order)
-    for (int t = threadIdx.x; t < d / 16; t += blockDim.x) {
-      float ss = 0.f;
-      for (int c = t * 16; c < t * 16 + 16; ++c) {
-        const float v = Elem<T>::load(e, c);
-        h[(int64_t)m * d + c] = v;
-        ss += v * v;
-      }
-      ssp[(int64_t)m * (d / 16) + t] = ss;
-    }
-    return;
-  }
   float ss = 0.f;
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
     const float v = Elem<T>::load(e, i);
@@ -44,26 +29,48 @@ __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __rest
   for (int i = threadIdx.x; i < d; i += blockDim.x) Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
 }
 
-// out[m][:] = h[m][:] * scale(m) in the model dtype (the final norm; scale from the
-// per-16-column sums of squares, reduced as every norm-on-load consumer reduces them).
-template <typename T>
-__global__ __launch_bounds__(ROW_THREADS) void norm_rows_kernel(const float* __restrict__ h, const float* __restrict__ ssp,
-                                                                int d, float eps, T* __restrict__ out) {
-  __shared__ float rs;
+// Finish of a residual projection, one row per workgroup: the K-range sums of the row are
+// added in range order, added to (or, with assign, written as) the residual row, and the
+// row's RMSNorm is stored in the model dtype for the next projection.  Each thread keeps its
+// columns (4 at a time) between the two passes, so the norm reads nothing back.
+template <typename T, int VPT>
+__global__ __launch_bounds__(ROW_THREADS) void resid_norm_kernel(const float* __restrict__ part, int S, int M, int d,
+                                                                 int assign, float eps, float* __restrict__ h,
+                                                                 T* __restrict__ out) {
+  __shared__ float red[16];
   const int m = blockIdx.x;
-  if (threadIdx.x < WAVE) {
-    const float r = row_norm_scale(ssp + (int64_t)m * (d / 16), d / 16, d, eps);
-    if (threadIdx.x == 0) rs = r;
+  const int64_t split = (int64_t)M * d;
+  float* hr = h + (int64_t)m * d;
+  const float* pr = part + (int64_t)m * d;
+  float4 y[VPT];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int i = (j * ROW_THREADS + threadIdx.x) * 4;
+    if (i >= d) continue;
+    float4 v = *reinterpret_cast<const float4*>(pr + i);
+    for (int sp = 1; sp < S; ++sp) {
+      const float4 w = *reinterpret_cast<const float4*>(pr + sp * split + i);
+      v = make_float4(v.x + w.x, v.y + w.y, v.z + w.z, v.w + w.w);
+    }
+    if (!assign) {
+      const float4 o = *reinterpret_cast<const float4*>(hr + i);
+      v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+    }
+    *reinterpret_cast<float4*>(hr + i) = v;
+    y[j] = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
-  __syncthreads();
-  const float rm = rs;
-  for (int i = threadIdx.x * 4; i < d; i += blockDim.x * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(h + (int64_t)m * d + i);
-    T* o = out + (int64_t)m * d + i;
-    Elem<T>::store(o, 0, v.x * rm);
-    Elem<T>::store(o, 1, v.y * rm);
-    Elem<T>::store(o, 2, v.z * rm);
-    Elem<T>::store(o, 3, v.w * rm);
+  const float r = rsqrtf(block_sum(ss, red) / d + eps);
+  T* o = out + (int64_t)m * d;
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int i = (j * ROW_THREADS + threadIdx.x) * 4;
+    if (i >= d) continue;
+    Elem<T>::store(o, i, y[j].x * r);
+    Elem<T>::store(o, i + 1, y[j].y * r);
+    Elem<T>::store(o, i + 2, y[j].z * r);
+    Elem<T>::store(o, i + 3, y[j].w * r);
   }
 }
 
@@ -385,18 +392,23 @@ __global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int3
     __VA_ARGS__;                               \
   }
 
-adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
-                             int dtype, hipStream_t st, const Branches& br) {
-  ADT_CHECK_ARG((a != nullptr) != (ssp != nullptr) && (!ssp || d % 16 == 0), ADT_E_ARG, "embed_norm: outputs");
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, ssp, br));
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
+                             hipStream_t st, const Branches& br) {
+  ADT_CHECK_ARG(a != nullptr && h != nullptr, ADT_E_ARG, "embed_norm: outputs");
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
-adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, float eps, void* out, int dtype,
-                            hipStream_t st) {
-  ADT_CHECK_ARG(d % 16 == 0, ADT_E_SHAPE, "norm_rows: d=%d", d);
-  ADT_DISPATCH_T(dtype, norm_rows_kernel<T><<<M, ROW_THREADS, 0, st>>>(h, ssp, d, eps, (T*)out));
+adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign, float eps, float* h, void* out,
+                             int dtype, hipStream_t st) {
+  ADT_CHECK_ARG(part && h && out && S >= 1 && M >= 1, ADT_E_ARG, "resid_norm: bad arguments");
+  ADT_CHECK_ARG(d % 4 == 0 && d <= 8 * 4 * ROW_THREADS, ADT_E_SHAPE, "resid_norm: d=%d (a multiple of 4, <= 8192)", d);
+  const int vpt = (d + 4 * ROW_THREADS - 1) / (4 * ROW_THREADS);
+#define ADT_RN(V) resid_norm_kernel<T, V><<<M, ROW_THREADS, 0, st>>>(part, S, M, d, assign, eps, h, (T*)out)
+  ADT_DISPATCH_T(dtype, if (vpt <= 1) ADT_RN(1); else if (vpt <= 2) ADT_RN(2); else if (vpt <= 4) ADT_RN(4);
+                 else ADT_RN(8));
+#undef ADT_RN
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -43,24 +43,20 @@ adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t
 size_t packed_bytes(int total_rows, int K, int dtype);
 adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, int K, int mode, int group, int dtype,
                        void* dst, hipStream_t st);
-// bf16 projections: one workgroup per 16-column output tile, its waves splitting K and
-// summing in fixed order; the epilogue runs on the finished tile.  With ssp_in set the input
-// rows are the fp32 residual stream, normalised while loaded (RMSNorm scale of each row
-// from its per-16-column sums of squares ssp_in[m][nss_in], over K columns).
-enum : int { EPI_STORE = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_SWIGLU = 4 };
+// bf16 projections at batch 1 (M <= 128 rows of bf16 input, weights packed): each workgroup
+// owns T 16-column tiles and one of S contiguous K ranges; its eight waves split that range
+// and their partial tiles are summed in LDS in wave order.  With S = 1 the finished tile
+// runs the epilogue; EPI_PART stores the S range sums instead, for resid_norm to add in
+// range order.  T and S come from gemm_rows_plan.
+enum : int { EPI_STORE = 1, EPI_PART = 2, EPI_QKV = 3, EPI_SWIGLU = 4 };
 struct GemmEpi {
   int mode = EPI_STORE;
-  const float* ssp_in = nullptr;
-  int nss_in = 0;
-  float eps = 0.f;
   // EPI_STORE: out[m][n] (fp32, leading dimension ldo)
   float* out = nullptr;
   int64_t ldo = 0;
-  // EPI_RESID: h[m][n] += y (= y when assign); sums of squares of the new h per 16-column
-  // tile into ssp_out[m][N/16]
-  float* h = nullptr;
-  int assign = 0;
-  float* ssp_out = nullptr;
+  // EPI_PART: part[s][m][n] (fp32), the sum over K range s of S
+  float* part = nullptr;
+  size_t part_elems = 0;
   // EPI_QKV (weights packed with ADT_PACK_QKV): q to q[m][H*Dh] after RoPE at pos[m]; k (RoPE)
   // and v to cache slot (*slot0 + m), element (head, slot, :) at kc + head*stride_h + slot*Dh
   uint16_t* q = nullptr;
@@ -76,9 +72,16 @@ struct GemmEpi {
   // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up
   uint16_t* act = nullptr;
 };
-// fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the fused kernel, epi.
+struct RowsPlan {
+  int T, S;       // 16-column tiles per workgroup, K ranges
+};
+RowsPlan gemm_rows_plan(int M, int N, int K, bool partial);
+constexpr int GEMM_MAX_SPLITS = 8;
+// fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the kernel above with the
+// epilogue epi; *splits (if given) gets S.
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
-                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                       const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
+                       int* splits = nullptr);
 // gemm_nt.hip: C[M][N] fp32 = X[M][K] . W[N][K]^T, bf16 row-major operands (MFMA-bound batches)
 // (packed: W in the adt_pack_weight layout, ldw unused; rows in the packed order)
 // part: fp32 scratch of part_elems for K-split partials of the packed path (null: no split);
@@ -88,13 +91,14 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
                           bool packed = false, float* part = nullptr, size_t part_elems = 0);
 size_t gemm_nt_part_elems(int M, int N, int K);
 // rows.hip
-// h = embedding rows; with a: a = norm(h) in the model dtype; with ssp: per-16-column sums
-// of squares of h into ssp[m][d/16].
-adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, float* ssp,
-                             int dtype, hipStream_t st, const Branches& br = Branches{});
-// out[m][c] = h[m][c] * scale(m), the scale from ssp[m][d/16], rounded to the model dtype.
-adt_status launch_norm_rows(const float* h, const float* ssp, int M, int d, float eps, void* out, int dtype,
-                            hipStream_t st);
+// h = embedding rows, a = RMSNorm(h) in the model dtype.
+adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
+                             hipStream_t st, const Branches& br = Branches{});
+// The residual projection's finish, one row per workgroup: y = sum over s < S of part[s][m][:]
+// (in s order), h[m] = y (assign) or h[m] + y, then out[m] = RMSNorm(h[m]) in the model dtype
+// (the next projection's input, or the final features).
+adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign, float eps, float* h, void* out,
+                             int dtype, hipStream_t st);
 // x[m] = [E[token] ; parent feature]: fsrc >= 0 is a node of fa, -1 zeros, <= -2 node
 // (-2 - fsrc) of fb; fa and fb hold the nb branch rows of a node consecutively.
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
