@@ -97,10 +97,11 @@ adt_status adt_tree_attn(const void* q, const void* k_cache, const void* v_cache
                          size_t workspace_bytes, void* stream);
 /* adt_tree_attn for callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc): the same arguments without the
- * workspace, the same result and the same errors.  The key-split partials live in a 64 MiB
+ * workspace, the same result and the same errors.  The key-split partials live in a 16 MiB
  * device array inside the library, one per device, whose address is looked up on the first
- * call on that device; a call whose partials need more (only few sequence-head pairs with long
- * prefixes split the keys: e.g. 32 pairs of 128-row trees over more than ~4000 slots) returns
+ * call on that device; a call whose partials need more (only fewer than 128 sequence-head pairs
+ * split the keys, into about 256 / pairs ranges: e.g. 120 pairs of 128-row trees at head size
+ * 128 over 10000 slots need 24 MB; 32 pairs of 61-row trees need 8.1 MB) returns
  * ADT_E_CAPACITY and enqueues nothing.  Allocates nothing.  Every call on a device shares that
  * device's array and leaves the last call's partials in it: calls that overlap on one device
  * (several streams or threads) race, so the caller must serialise them. */

@@ -184,7 +184,7 @@ extern "C" adt_status adt_tree_attn(const void* q, const void* k_cache, const vo
 // holds its own copy until the process ends; host code reaches it only through the address
 // hipGetSymbolAddress returns with that device current (kept per device below), never through
 // the array's name, which in host code is a stand-in and not a device address.
-constexpr size_t ATTN_SCRATCH_BYTES = (size_t)64 << 20;
+constexpr size_t ATTN_SCRATCH_BYTES = (size_t)16 << 20;
 constexpr int SCRATCH_MAX_DEVICES = 64;
 static __device__ __align__(256) char scratch[ATTN_SCRATCH_BYTES];
 static std::mutex g_scratch_mu;

@@ -1,21 +1,19 @@
 // Tree attention (Sec. 3.1): every tree node attends to the committed prefix and to the
 // nodes on its own root-to-node path (the ancestor bitmask).
 //
-// bf16 path, many (sequence, head) pairs (the microbenchmark batch): one workgroup per
-// (split of the key range, head, sequence).  K and V tiles of 64 keys are streamed from HBM
-// once per workgroup and staged in LDS (V transposed), all query rows of the tree are held
-// in registers, and both products run on MFMA 16x16x32:
+// bf16 path: both products run on MFMA 16x16x32 with the keys on the A side,
 //   S^T[key][q] = K[key][:] . Q[q][:]        (A = K rows, B = Q^T)
 //   O^T[d][q]  += V^T[d][key] . P^T[key][q]  (A = V^T rows, B = P^T)
 // so each lane owns one query column and the online-softmax rescale is a per-lane scalar.
 // Probabilities enter the second product rounded to bf16 (relative error 2^-9 per term, below
 // the bf16 rounding of the output itself); steps wholly inside the unmasked prefix skip the
 // mask test, and the running output is rescaled only when some row's maximum moved.
-// Splits write (O, m, l) partials that a second kernel merges with log-sum-exp weights.
-// Few pairs (one image's forwards), and many pairs with trees of at most 16 rows:
-// tree_attn_wg_kernel below, one workgroup per pair (or query slice) whose waves split the
-// keys and merge in LDS; many pairs with 17-128 rows: tree_attn_blk_kernel, one workgroup per
-// pair sharing each K/V block through LDS.
+// Three kernels by shape: tree_attn_blk_kernel (trees of 17-128 rows over many pairs, and
+// every tree over few pairs with long prefixes: one workgroup per pair, or per pair and key
+// split, sharing each K/V block through LDS; splits write (O, m, l) partials that
+// tree_attn_combine_kernel merges with log-sum-exp weights), tree_attn_wg_kernel (trees of
+// at most 16 rows over many pairs, and few pairs over short prefixes: one workgroup per
+// pair or query slice whose waves split the keys and merge in LDS), and tree_attn_f32_kernel.
 #include <hip/hip_ext.h>
 
 #include "../launch.h"
@@ -24,7 +22,6 @@ namespace adt {
 
 constexpr int ATT_KT = 64;      // keys per LDS tile
 constexpr int ATT_MAX_SPLITS = 64;
-constexpr int ATT_THREADS = 256;
 
 __device__ __forceinline__ bool tail_visible(uint64_t w0, uint64_t w1, int j) {
   const uint64_t w = j < 64 ? w0 : w1;
@@ -43,193 +40,6 @@ __device__ __forceinline__ bool key_visible(int key, int k_end, int L, uint64_t 
 // 2^x on the transcendental unit alone (no denormal fix-up: softmax weights that small
 // are zero for every purpose here).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// TPW = query tiles (of 16) per wave: 1 covers up to 64 queries, 2 up to 128.
-template <int DH, int TPW>
-__global__ __launch_bounds__(ATT_THREADS) void tree_attn_bf16_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
-    int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
-    const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
-    int kv_cap, int chunk, int splits, float scale_log2, float* __restrict__ part_o, float* __restrict__ part_ml) {
-  constexpr int DT = DH / 16;   // 16-wide dimension tiles of O
-  constexpr int KS = DH / 32;   // 32-deep k-steps of Q.K
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[ATT_KT][DH + 8];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH][ATT_KT + 8];
-
-  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int L = kv_len[b];
-  const int nq = min(n_q[b], nq_max);
-  const int total = min(L + n_tail[b], kv_cap);
-  const int k_begin = s * chunk;
-  const int k_end = min(total, k_begin + chunk);
-  const int tid = threadIdx.x, wave = tid / WAVE, lane = tid % WAVE;
-  const int lq = lane & 15, g = lane >> 4;
-  const int QT = (nq + 15) / 16;
-
-  const int64_t pbase = (((int64_t)b * H + h) * splits + s) * nq_max;
-  float* po = part_o + pbase * DH;
-  float* pml = part_ml + pbase * 2;
-  const uint16_t* kbase = kc + b * stride_b + h * stride_h;
-  const uint16_t* vbase = vc + b * stride_b + h * stride_h;
-
-  // This wave's query tiles: wave, wave + 4, ...
-  int n_my = 0;
-  for (int t = wave; t < QT && n_my < TPW; t += 4) ++n_my;
-
-  bf16x8 qf[TPW][KS];
-  uint64_t mw0[TPW], mw1[TPW];
-  f32x4 o[TPW][DT];
-  float m_run[TPW], l_run[TPW];
-#pragma unroll
-  for (int i = 0; i < TPW; ++i) {
-    m_run[i] = -INFINITY;
-    l_run[i] = 0.f;
-    mw0[i] = mw1[i] = 0;
-#pragma unroll
-    for (int d = 0; d < DT; ++d) o[i][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int t = 0; t < KS; ++t) qf[i][t] = bf16x8{};
-    if (i < n_my) {
-      const int qr = (wave + 4 * i) * 16 + lq;
-      if (qr < nq) {
-        const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
-#pragma unroll
-        for (int t = 0; t < KS; ++t) qf[i][t] = *reinterpret_cast<const bf16x8*>(qp + t * 32 + g * 8);
-        const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
-        mw0[i] = mp[0];
-        mw1[i] = mp[1];
-      }
-    }
-  }
-
-  // Each thread moves PP pieces (16 bytes of K and of V) per tile.  The next tile's pieces
-  // are loaded into registers before the current tile is computed, so HBM latency overlaps
-  // the MFMA work.
-  constexpr int PP = ATT_KT * DH / 8 / ATT_THREADS;
-  u16x8 kn[PP], vn[PP];
-  auto load_tile = [&](int kb) {
-#pragma unroll
-    for (int j = 0; j < PP; ++j) {
-      const int p = tid + j * ATT_THREADS;
-      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
-      const int key = kb + r;
-      kn[j] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      vn[j] = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (key < k_end) {
-        kn[j] = *reinterpret_cast<const u16x8*>(kbase + (int64_t)key * DH + c);
-        vn[j] = *reinterpret_cast<const u16x8*>(vbase + (int64_t)key * DH + c);
-      }
-    }
-  };
-  if (k_begin < k_end) load_tile(k_begin);
-  for (int kb = k_begin; kb < k_end; kb += ATT_KT) {
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < PP; ++j) {
-      const int p = tid + j * ATT_THREADS;
-      const int r = p / (DH / 8), c = (p % (DH / 8)) * 8;
-      *reinterpret_cast<u16x8*>(&Ks[r][c]) = kn[j];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[c + e][r] = vn[j][e];
-    }
-    __syncthreads();
-    if (kb + ATT_KT < k_end) load_tile(kb + ATT_KT);
-
-#pragma unroll
-    for (int i = 0; i < TPW; ++i) {
-      if (i >= n_my) break;
-      f32x4 st[4];
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub) {
-        st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < KS; ++t) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&Ks[sub * 16 + lq][t * 32 + g * 8]);
-          st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[i][t], st[sub], 0, 0, 0);
-        }
-      }
-      // lane (lq, g) now holds S for query (wave + 4i)*16 + lq and keys kb + sub*16 + 4g + r.
-      float mx = -INFINITY;
-      if (kb + ATT_KT <= min(L, k_end)) {
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            st[sub][r] *= scale_log2;
-            mx = fmaxf(mx, st[sub][r]);
-          }
-      } else {
-#pragma unroll
-        for (int sub = 0; sub < 4; ++sub) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int key = kb + sub * 16 + 4 * g + r;
-            const bool vis = key_visible(key, k_end, L, mw0[i], mw1[i]);
-            const float v = vis ? st[sub][r] * scale_log2 : -INFINITY;
-            st[sub][r] = v;
-            mx = fmaxf(mx, v);
-          }
-        }
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-      const float m_new = fmaxf(m_run[i], mx);
-      const bool none = (m_new == -INFINITY);
-      const float alpha = none ? 1.f : fast_exp2(m_run[i] - m_new);
-      float rs = 0.f;
-#pragma unroll
-      for (int sub = 0; sub < 4; ++sub) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = none ? 0.f : fast_exp2(st[sub][r] - m_new);
-          st[sub][r] = p;
-          rs += p;
-        }
-      }
-      rs += __shfl_xor(rs, 16, WAVE);
-      rs += __shfl_xor(rs, 32, WAVE);
-      l_run[i] = l_run[i] * alpha + rs;
-      m_run[i] = m_new;
-      if (!__all(alpha == 1.f)) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) o[i][d] *= alpha;
-      }
-#pragma unroll
-      for (int h2 = 0; h2 < 2; ++h2) {
-        bf16x8 p1;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) p1[r] = (__bf16)(r < 4 ? st[2 * h2][r] : st[2 * h2 + 1][r - 4]);
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 4 * g]);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vt[d * 16 + lq][32 * h2 + 16 + 4 * g]);
-          const bf16x8 a = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          o[i][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, p1, o[i][d], 0, 0, 0);
-        }
-      }
-    }
-  }
-
-  // lane (lq, g) holds O^T[d = dt*16 + 4g + r][q].
-#pragma unroll
-  for (int i = 0; i < TPW; ++i) {
-    const int qr = (wave + 4 * i) * 16 + lq;
-    if (i >= n_my || qr >= nq) continue;
-#pragma unroll
-    for (int d = 0; d < DT; ++d) *reinterpret_cast<f32x4*>(po + (int64_t)qr * DH + d * 16 + 4 * g) = o[i][d];
-    if (g == 0) {
-      pml[qr * 2] = m_run[i];
-      pml[qr * 2 + 1] = l_run[i];
-    }
-  }
-  // Query rows of idle waves / empty splits still need a neutral partial.
-  if (k_begin >= k_end) {
-    for (int qr = tid; qr < nq; qr += ATT_THREADS) {
-      pml[qr * 2] = -INFINITY;
-      pml[qr * 2 + 1] = 0.f;
-    }
-  }
-}
 
 // One workgroup per (sequence, head): its W = QG x KG waves form QG query groups of QTW
 // 16-row query tiles, and each group's KG waves take contiguous, balanced slices of the
@@ -595,7 +405,8 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
-    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out, int splits, float* __restrict__ part_o,
+    float* __restrict__ part_ml) {
   constexpr int BLK_KT = KH == 4 ? 128 : 64;      // keys per block: 32 per wave and half-step
   constexpr int CH = DH / 8;                     // 16-byte chunks per row
   constexpr int DT = DH / 16, KS = DH / 32;
@@ -606,7 +417,7 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
   static_assert((KH - 1) * (NW / KH) * (DT * 4 + 2) * WAVE * 4 <= 4 * BLK_BYTES, "merge area");
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * BLK_BYTES];   // [buffer][K, V]
 
-  const int h = blockIdx.x, b = blockIdx.y;
+  const int h = blockIdx.x, b = blockIdx.y, sp = blockIdx.z;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
   const int QT = (nq_max + 15) / 16;
@@ -615,7 +426,11 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
   const int L = kv_len[b];
   const int nq = min(n_q[b], nq_max);
   const int total = min(L + n_tail[b], kv_cap);
-  const int nblk = (total + BLK_KT - 1) / BLK_KT;
+  // with splits > 1, split sp takes a contiguous share of the live blocks (balanced on the
+  // device, so a replayed launch follows the growing prefix)
+  const int nblk_all = (total + BLK_KT - 1) / BLK_KT;
+  const int per = (nblk_all + splits - 1) / splits;
+  const int blk0 = min(nblk_all, sp * per), nblk = min(nblk_all, blk0 + per);
   const uint16_t* kbase = kc + b * stride_b + h * stride_h;
   const uint16_t* vbase = vc + b * stride_b + h * stride_h;
 
@@ -660,8 +475,8 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
 #pragma unroll
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  if (nblk > 0) fetch_block(0);
-  for (int blk = 0; blk < nblk; ++blk) {
+  if (blk0 < nblk) fetch_block(blk0);
+  for (int blk = blk0; blk < nblk; ++blk) {
     // the buffer written here was last read two blocks ago, before the previous barrier
     store_block(blk & 1);
     __syncthreads();
@@ -780,45 +595,44 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
     }
   }
   if (active && kpart == 0 && qr < nq) {
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    uint16_t* op = out + (rl.q_row(b, qr) * H + h) * DH;
+    if (splits == 1) {
+      const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+      uint16_t* op = out + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
-      *reinterpret_cast<u16x4*>(op + d * 16 + 4 * g) =
-          u16x4{f2bf(o[d][0] * inv), f2bf(o[d][1] * inv), f2bf(o[d][2] * inv), f2bf(o[d][3] * inv)};
+      for (int d = 0; d < DT; ++d)
+        *reinterpret_cast<u16x4*>(op + d * 16 + 4 * g) =
+            u16x4{f2bf(o[d][0] * inv), f2bf(o[d][1] * inv), f2bf(o[d][2] * inv), f2bf(o[d][3] * inv)};
+    } else {
+      // this split's (O, m, l) for the log-sum-exp merge (m in the log2 domain)
+      const int64_t pr = (((int64_t)b * H + h) * splits + sp) * nq_max + qr;
+#pragma unroll
+      for (int d = 0; d < DT; ++d) *reinterpret_cast<f32x4*>(part_o + pr * DH + d * 16 + 4 * g) = o[d];
+      if (g == 0) {
+        part_ml[pr * 2] = m_run;
+        part_ml[pr * 2 + 1] = l_run;
+      }
+    }
   }
 }
 
-struct AttnPlan {
-  int splits, chunk;
-};
-
-static AttnPlan attn_plan(int B, int H, int kv_cap) {
-  // Aim for about four workgroups per CU (256 CUs); at least two 64-key tiles per split.
-  int want = (1024 + B * H - 1) / (B * H);
-  if (want > ATT_MAX_SPLITS) want = ATT_MAX_SPLITS;
+// Key splits of the shared-block kernel for few (sequence, head) pairs: about one workgroup
+// per CU, and at least two 64-key blocks per split at the cache capacity.  The live blocks
+// are divided among the splits on the device.
+static int attn_splits(int B, int H, int kv_cap) {
+  int want = (256 + B * H - 1) / (B * H);
   const int max_splits = (kv_cap + 2 * ATT_KT - 1) / (2 * ATT_KT);
-  int splits = want < 1 ? 1 : want;
-  if (splits > max_splits) splits = max_splits;
-  if (splits < 1) splits = 1;
-  int chunk = (kv_cap + splits - 1) / splits;
-  chunk = (chunk + ATT_KT - 1) / ATT_KT * ATT_KT;
-  splits = (kv_cap + chunk - 1) / chunk;
-  return {splits, chunk};
+  want = want > max_splits ? max_splits : want;
+  want = want > ATT_MAX_SPLITS ? ATT_MAX_SPLITS : want;
+  return want < 1 ? 1 : want;
 }
 
-// Query tiles per wave, query groups and query slices (workgroups per pair) of the
-// one-workgroup-per-pair kernel.  With few pairs every 16-row query tile gets a workgroup of
-// its own (its 8 waves split the keys), so a large tree brings more CUs to the softmax,
-// which bounds it; with many pairs the tiles of a pair share one workgroup (registers allow
-// 4 tiles of head size 64, 2 of 128).  Returns false when nq_max does not fit.
+// Query tiles per wave and query groups of the one-workgroup-per-pair kernel, used for many
+// pairs: the tiles of a pair share one workgroup (registers allow 4 tiles of head size 64, 2
+// of 128).  Returns false when nq_max does not fit.
 static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, int& qsplit) {
+  (void)B;
+  (void)H;
   const int qt = (nq_max + 15) / 16;
-  if (B * H < 128) {
-    qtw = qg = 1;
-    qsplit = qt;
-    return qt <= ADT_MAX_NODES / 16;
-  }
   const int cap = Dh == 64 ? 4 : 2;
   qtw = qt < cap ? qt : cap;
   const int groups = (qt + qtw - 1) / qtw;
@@ -840,65 +654,38 @@ static int attn_wg_waves(int B, int H, int Dh, int nq_max) {
 // read by every query tile from LDS).
 static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 16 && nq_max <= 128; }
 
-// One workgroup per (sequence, head, query slice) unless there are few pairs and each of
-// their key slices would be long (one image's forwards at a long prefix): then the keys are
-// split across workgroups and merged by a second kernel, which brings more CUs to the stream.
-static bool attn_use_wg(int B, int H, int Dh, int nq_max, int kv_cap) {
+// Many pairs with trees of at most 16 rows: one workgroup per pair.  Few pairs (one image's
+// forwards) take the shared-block kernel with the keys split across workgroups instead.
+static bool attn_use_wg(int B, int H, int Dh, int nq_max) {
   int qtw, qg, qsplit;
-  if (!attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit)) return false;
-  const int kg = attn_wg_waves(B, H, Dh, nq_max) / qg;
-  return B * H >= 128 || kv_cap / kg <= 256;
+  return B * H >= 128 && attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
 }
 
-// Upper bound over every kv_cap: a plan never uses more than ceil(1024 / (B*H)) splits.
+// Upper bound over every kv_cap: the splits never exceed ceil(256 / (B*H)).
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
   (void)kv_cap;
   if (dtype == ADT_F32) return 0;
-  int max_splits = (1024 + B * H - 1) / (B * H);
+  int max_splits = (256 + B * H - 1) / (B * H);
   if (max_splits > ATT_MAX_SPLITS) max_splits = ATT_MAX_SPLITS;
   return (size_t)B * H * max_splits * nq_max * (Dh + 2) * sizeof(float);
 }
 
 size_t tree_attn_ws_need(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
-  if (dtype == ADT_F32 || attn_use_blk(B, H, nq_max) || attn_use_wg(B, H, Dh, nq_max, kv_cap)) return 0;
-  const AttnPlan p = attn_plan(B, H, kv_cap);
-  return (size_t)B * H * p.splits * nq_max * (Dh + 2) * sizeof(float);
+  if (dtype == ADT_F32 || attn_use_blk(B, H, nq_max) || attn_use_wg(B, H, Dh, nq_max)) return 0;
+  const int S = attn_splits(B, H, kv_cap);
+  return S > 1 ? (size_t)B * H * S * nq_max * (Dh + 2) * sizeof(float) : 0;
 }
 
 static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t sb, int64_t sh, const int32_t* kv_len,
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st,
                             hipEvent_t ev0, hipEvent_t ev1) {
-  if (attn_use_blk(B, H, nq_max)) {
-    const dim3 grid(H, B);
-    const float sl2 = scale * LOG2E;
-    const int qt = (nq_max + 15) / 16;
-#define ADT_ATTN_BLK(DHV, KHV, NWV)                                                                                \
-  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,           \
-                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
-                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
-    // two tiles at head size 128: four waves (two tiles x two key halves, ~190 VGPRs), so two
-    // workgroups share a CU and a 512-pair launch is resident at once (32 nodes: 61 % of
-    // 8 TB/s against 58 % with eight waves in 128-key blocks, one workgroup per CU)
-    if (Dh == 128) {
-      if (qt <= 2) ADT_ATTN_BLK(128, 2, 4);
-      else if (qt <= 4) ADT_ATTN_BLK(128, 2, AWG_W);
-      else ADT_ATTN_BLK(128, 1, AWG_W);
-    } else {
-      if (qt <= 2) ADT_ATTN_BLK(64, 4, AWG_W);
-      else if (qt <= 4) ADT_ATTN_BLK(64, 2, AWG_W);
-      else ADT_ATTN_BLK(64, 1, AWG_W);
-    }
-#undef ADT_ATTN_BLK
-    ADT_LAUNCH_CHECK();
-    return ADT_OK;
-  }
-  if (attn_use_wg(B, H, Dh, nq_max, kv_cap)) {
+  const float sl2 = scale * LOG2E;
+  if (attn_use_wg(B, H, Dh, nq_max)) {
     int qtw, qg, qsplit;
     attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
     const int pairs = B * H;
     const dim3 grid(qsplit == 1 ? pairs : (pairs + 7) / 8 * 8 * qsplit);
-    const float sl2 = scale * LOG2E;
 #define ADT_ATTN_WG(DHV, QTWV, QGV, NWV)                                                                           \
   hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,       \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
@@ -920,31 +707,44 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
     ADT_LAUNCH_CHECK();
     return ADT_OK;
   }
-  const AttnPlan p = attn_plan(B, H, kv_cap);
-  const size_t need = tree_attn_ws_need(B, H, Dh, nq_max, kv_cap, ADT_BF16);
-  ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
-                need);
-  float* part_o = (float*)ws;
-  float* part_ml = part_o + (size_t)B * H * p.splits * nq_max * Dh;
-  dim3 grid(p.splits, H, B);
-  const float sl2 = scale * LOG2E;
-#define ADT_ATTN_LAUNCH(DHV, TPWV)                                                                             \
-  hipExtLaunchKernelGGL(tree_attn_bf16_kernel<DHV, TPWV>, grid, dim3(ATT_THREADS), 0, st, ev0, nullptr, 0,      \
-                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail, \
-                        mask, rl, H, nq_max, kv_cap, p.chunk, p.splits, sl2, part_o, part_ml)
-  if (Dh == 128) {
-    if (nq_max > 64) ADT_ATTN_LAUNCH(128, 2);
-    else ADT_ATTN_LAUNCH(128, 1);
-  } else {
-    if (nq_max > 64) ADT_ATTN_LAUNCH(64, 2);
-    else ADT_ATTN_LAUNCH(64, 1);
+  // the shared-block kernel: many pairs with 17-128 rows in one launch, few pairs with the
+  // keys split across workgroups and a log-sum-exp merge
+  const int S = attn_use_blk(B, H, nq_max) ? 1 : attn_splits(B, H, kv_cap);
+  float *part_o = nullptr, *part_ml = nullptr;
+  if (S > 1) {
+    const size_t need = tree_attn_ws_need(B, H, Dh, nq_max, kv_cap, ADT_BF16);
+    ADT_CHECK_ARG(ws != nullptr && ws_bytes >= need, ADT_E_CAPACITY, "tree_attn: workspace %zu < %zu bytes", ws_bytes,
+                  need);
+    part_o = (float*)ws;
+    part_ml = part_o + (size_t)B * H * S * nq_max * Dh;
   }
-#undef ADT_ATTN_LAUNCH
+  const dim3 grid(H, B, S);
+  const int qt = (nq_max + 15) / 16;
+  hipEvent_t e1 = S > 1 ? nullptr : ev1;
+#define ADT_ATTN_BLK(DHV, KHV, NWV)                                                                                \
+  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, e1, 0,            \
+                        (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
+                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, S, part_o, part_ml)
+  // two tiles at head size 128: four waves (two tiles x two key halves, ~190 VGPRs), so two
+  // workgroups share a CU and a 512-pair launch is resident at once (32 nodes: 61 % of
+  // 8 TB/s against 58 % with eight waves in 128-key blocks, one workgroup per CU)
+  if (Dh == 128) {
+    if (qt <= 2) ADT_ATTN_BLK(128, 2, 4);
+    else if (qt <= 4) ADT_ATTN_BLK(128, 2, AWG_W);
+    else ADT_ATTN_BLK(128, 1, AWG_W);
+  } else {
+    if (qt <= 2) ADT_ATTN_BLK(64, 4, AWG_W);
+    else if (qt <= 4) ADT_ATTN_BLK(64, 2, AWG_W);
+    else ADT_ATTN_BLK(64, 1, AWG_W);
+  }
+#undef ADT_ATTN_BLK
   ADT_LAUNCH_CHECK();
-  dim3 g2(nq_max, H, B);
-  hipExtLaunchKernelGGL(tree_attn_combine_kernel<uint16_t>, g2, dim3(Dh), 0, st, nullptr, ev1, 0, part_o, part_ml,
-                        n_q, rl, H, nq_max, p.splits, Dh, (uint16_t*)out);
-  ADT_LAUNCH_CHECK();
+  if (S > 1) {
+    const dim3 g2(nq_max, H, B);
+    hipExtLaunchKernelGGL(tree_attn_combine_kernel<uint16_t>, g2, dim3(Dh), 0, st, nullptr, ev1, 0, part_o, part_ml,
+                          n_q, rl, H, nq_max, S, Dh, (uint16_t*)out);
+    ADT_LAUNCH_CHECK();
+  }
   return ADT_OK;
 }
 

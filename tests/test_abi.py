@@ -181,9 +181,9 @@ def test_capture_arguments(L):
 
 
 def test_tree_attn_noalloc_rejects_oversize_partials(L):
-    """Key-split partials beyond the library's 64 MiB scratch (120 pairs of 128-row trees over
-    10000 slots) are refused before anything is enqueued; argument errors are those of
-    adt_tree_attn."""
+    """Key-split partials beyond the library's 16 MiB scratch (120 pairs of 128-row trees at head
+    size 128 over 10000 slots: 3 key ranges, 24 MB) are refused before anything is enqueued;
+    argument errors are those of adt_tree_attn."""
     from paper_2512_21857_amd import abi
     fake = 0x1000
     assert L.adt_tree_attn_noalloc(fake, fake, fake, 0, 128 * 10000, fake, fake, fake, fake, 1, 120, 128, 128, 10000,
