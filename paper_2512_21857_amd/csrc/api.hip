@@ -538,7 +538,6 @@ struct adt_session_s {
   TreeBufs tr;
   int32_t* allowed_img;
   Pool pool;
-  int32_t *sel_rank, *bfs_of;
   NextRows nx[2];
   int32_t *ctok, *cfsrc, *cpos, *idx;
   uint64_t* cmask;
@@ -646,8 +645,6 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->pool.drow = b.take<int32_t>(s->C);
   s->pool.qrow = b.take<int32_t>(s->C);
   s->pool.rmask = b.take<uint64_t>((size_t)2 * std::max(1, s->DR - s->C0));
-  s->sel_rank = b.take<int32_t>(s->C);
-  s->bfs_of = b.take<int32_t>(s->C);
   for (int i = 0; i < 2; ++i) {
     s->nx[i].tok = b.take<int32_t>(s->KR);
     s->nx[i].fsrc = b.take<int32_t>(s->KR);
@@ -690,6 +687,9 @@ static adt_status check_session_desc(const adt_model* m, const adt_session_desc*
   ADT_CHECK_ARG(!d->guided || std::isfinite(d->guidance_scale), ADT_E_ARG, "session: guidance scale");
   ADT_CHECK_ARG(c.n_budget >= 1 && c.n_budget <= R / nb - 1, ADT_E_CAPACITY, "session: n_budget %d", c.n_budget);
   ADT_CHECK_ARG((c.d_hi - 1) * c.k_hi <= R, ADT_E_CAPACITY, "session: draft tree rows exceed %d", R);
+  ADT_CHECK_ARG(c.k_hi + (c.d_hi - 1) * c.k_hi * c.k_hi <= EXPAND_MAX_POOL, ADT_E_CAPACITY,
+                "session: candidate pool k_hi + (d_hi - 1) k_hi^2 = %d exceeds %d", c.k_hi + (c.d_hi - 1) * c.k_hi * c.k_hi,
+                EXPAND_MAX_POOL);
   ADT_CHECK_ARG(c.alpha_source == ADT_ALPHA_REAL || (c.alpha_source == ADT_ALPHA_POISSON && d->poisson), ADT_E_ARG,
                 "session: alpha source");
   ADT_CHECK_ARG(d->draft_table == nullptr || d->draft_table_rows >= 1, ADT_E_ARG, "session: draft table rows");
@@ -733,7 +733,11 @@ extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_d
   s->has_rec.assign(d->n_image, 0);
   s->d.allowed = nullptr;
   s->d.poisson = nullptr;
-  hipError_t he = hipMemcpy(s->allowed_img, s->allowed_h.data(), sizeof(int32_t) * 2 * s->T, hipMemcpyHostToDevice);
+  // pinned host staging of every acceptance's readback, allocated once here (the cycle
+  // itself allocates nothing)
+  hipError_t he = hipHostMalloc((void**)&s->h_acc, sizeof(int32_t) * (2 * R + 2), hipHostMallocDefault);
+  if (he == hipSuccess)
+    he = hipMemcpy(s->allowed_img, s->allowed_h.data(), sizeof(int32_t) * 2 * s->T, hipMemcpyHostToDevice);
   if (he == hipSuccess && launch_rope_table(s->rope, s->d.s_cap, s->Dh, m->d.rope_theta, nullptr) == ADT_OK)
     he = hipDeviceSynchronize();
   if (he != hipSuccess) {
@@ -1156,8 +1160,8 @@ static adt_status expand_sampled(adt_session_s* s, int d_hat, int k_hat, int n_b
     nf = nf_next;
     cur ^= 1;
   }
-  TRY(launch_expand_finalize(s->pool, pool_n, pool_n, s->tokens[L], L, P, s->T, s->allowed_img, s->sel_rank,
-                             s->bfs_of, s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
+  TRY(launch_expand_finalize(s->pool, pool_n, pool_n, s->tokens[L], L, P, s->T, s->allowed_img,
+                             s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
                              s->tr.allowed_rows, s->tr.qrow, s->tr.n, true, st));
   s->n_nodes = pool_n + 1;
   s->expanded = true;
@@ -1234,8 +1238,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     nf = std::min(k_hat, nf * cnt);
     cur ^= 1;
   }
-  TRY(launch_expand_finalize(s->pool, pool_n, n_budget, s->tokens[L], L, P, s->T, s->allowed_img, s->sel_rank,
-                             s->bfs_of, s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
+  TRY(launch_expand_finalize(s->pool, pool_n, n_budget, s->tokens[L], L, P, s->T, s->allowed_img,
+                             s->tr.parent, s->tr.token, s->tr.depth, s->tr.score, s->tr.pos, s->tr.mask,
                              s->tr.allowed_rows, s->tr.qrow, s->tr.n, false, st));
   s->n_nodes = std::min(n_budget, pool_n) + 1;
   s->expanded = true;
@@ -1291,7 +1295,6 @@ extern "C" adt_status adt_verify_forward(adt_session* s, void* stream) {
 // staging (asynchronous on st); accept_finish commits once st has been synchronised.
 static adt_status accept_launch(adt_session_s* s, hipStream_t st) {
   const int n = s->n_nodes;
-  if (!s->h_acc) ADT_HIP(hipHostMalloc((void**)&s->h_acc, sizeof(int32_t) * (2 * R + 2), hipHostMallocDefault));
   TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, session_accept_cfg(s),
                   (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
   ADT_HIP(hipMemcpyAsync(s->h_acc, s->tr.path, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));

@@ -151,9 +151,11 @@ adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, i
                                hipStream_t st);
 // keep_all: every pool node in creation order (stochastic children), else the top-N rerank
 adt_status launch_expand_finalize(const Pool& pool, int C, int n_budget, int root_token, int L, int P, int n_image,
-                                  const int32_t* allowed_img, int32_t* sel_rank, int32_t* bfs_of, int32_t* parent,
-                                  int32_t* token, int32_t* depth, float* score, int32_t* pos, uint64_t* mask,
-                                  int32_t* allowed_rows, int32_t* qrow, int32_t* n_out, bool keep_all, hipStream_t st);
+                                  const int32_t* allowed_img, int32_t* parent, int32_t* token, int32_t* depth,
+                                  float* score, int32_t* pos, uint64_t* mask, int32_t* allowed_rows, int32_t* qrow,
+                                  int32_t* n_out, bool keep_all, hipStream_t st);
+// Largest candidate pool the rerank holds in LDS.
+constexpr int EXPAND_MAX_POOL = 4096;
 adt_status launch_accept_greedy(const int32_t* argmax, int kmax, const int32_t* parent, const int32_t* token,
                                 const int32_t* n_nodes, int n_max, int32_t* path, int32_t* n_acc, int32_t* bonus,
                                 hipStream_t st);

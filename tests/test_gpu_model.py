@@ -165,13 +165,6 @@ def test_tiny_full_image_guided(rt, scale, prefix_len):
     assert flag is None and matched >= 1
 
 
-def test_bf16_small_guided(rt):
-    cfg = dataclasses.replace(_small_bf16(), guidance=3.0)
-    matched, flag = _compare_run(rt, cfg, 30, label="bf16-small-guided")
-    print("bf16 small guided matched", matched, flag)
-    assert flag is None or "tree differs" in flag or "near-tie" in flag
-
-
 def test_tiny_fixed_deep_tree(rt):
     cfg = synth.get_config("tiny")
     matched, flag = _compare_run(rt, cfg, 40, fixed_tree=True, label="tiny-fixed")
@@ -182,20 +175,6 @@ def test_tiny_fixed_deep_tree(rt):
 def _small_bf16():
     cfg = synth.shrink(synth.get_config("llamagen_xl"), n_layers=2, d_model=256, n_heads=4, ffn=512, vocab=512)
     return dataclasses.replace(cfg, prefix_len=16, img_hi=512, prefix_hi=512, grid_h=8, grid_w=8)
-
-
-def test_bf16_small_fixed_tree(rt):
-    """bf16 with 10-wide, 6-deep trees: draft logits within tolerance every compared step;
-    top-10 orderings of bf16 logits hit near-ties quickly, which ends the comparison."""
-    matched, flag = _compare_run(rt, _small_bf16(), 12, fixed_tree=True, label="bf16-small")
-    print("bf16 small matched", matched, flag)
-    assert flag is None or "tree differs" in flag or "near-tie" in flag
-
-
-def test_bf16_small_adt_schedule(rt):
-    matched, flag = _compare_run(rt, _small_bf16(), 30, label="bf16-small-adt")
-    print("bf16 small adt matched", matched, flag)
-    assert flag is None or "tree differs" in flag or "near-tie" in flag
 
 
 def _table_row(depth, token, rows):

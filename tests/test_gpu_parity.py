@@ -27,6 +27,7 @@ whose fp64 scores are closer than the observed score error, the two orders are b
 such a frontier or rerank boundary is accepted only with that margin, and counted.  Because the
 oracle follows the GPU's trajectory, the comparison never stops at a divergence.
 """
+import dataclasses
 import gc
 import time
 
@@ -116,59 +117,96 @@ def _cache_layer(t: torch.Tensor) -> np.ndarray:
 
 
 # ------------------------------------------------------------------------------ layer-local
-def check_forward(rep, om, sess, rec, what):
-    """The oracle evaluates every half-layer of one recorded forward from the GPU's inputs."""
+def _caches(sess, draft, nb, layers):
+    """[branch][layer] (K, V) device views of the session's caches."""
+    if draft:
+        return [[(sess.dk_cache[b] if nb > 1 else sess.dk_cache, sess.dv_cache[b] if nb > 1 else sess.dv_cache)]
+                for b in range(nb)]
+    return [[((sess.k_cache[b] if nb > 1 else sess.k_cache)[l], (sess.v_cache[b] if nb > 1 else sess.v_cache)[l])
+             for l in range(layers)] for b in range(nb)]
+
+
+def check_forward(rep, om, sess, rec, what, nb=1):
+    """The oracle evaluates every half-layer of one recorded forward from the GPU's inputs,
+    branch by branch (with guidance, node r's branch-b row is row nb r + b).  Returns the
+    oracle's final norm of the GPU's last residual, [branch][rows][d]."""
     m = om.m
     n, d = rec["nodes"], m.d_model
-    assert rec["rows"] == n, "unguided sessions only"
+    assert rec["rows"] == n * nb
     pos = [int(p) for p in rec["pos"]]
     Lp, s0 = rec["kv_prefix"], rec["slot0"]
     slots = [s0 + r for r in range(n)]
     keys = [list(range(Lp)) + [Lp + j for j in _bits(rec["mask"][r])] for r in range(n)]
     for r in range(n):
         assert slots[r] in keys[r], f"{what}: row {r} does not see its own slot"
-    R = f64(rec["resid"])
-    if rec["draft"]:
-        names = ["draft"]
-        caches = [(sess.dk_cache, sess.dv_cache)]
-        xin = f64(rec["xin"])
-        rep.exact(f"{what}: FC input embedding half", np.array_equal(xin[:, :d], om.embed_rows(rec["tok"])),
-                  "embedding rows differ")
-        rep.check("draft FC output", R[0], xin @ om.w("draft.fc").T, what)
-    else:
-        names = [f"layer{l}" for l in range(m.n_layers)]
-        caches = [(sess.k_cache[l], sess.v_cache[l]) for l in range(m.n_layers)]
-        rep.exact(f"{what}: embedding", np.array_equal(R[0], om.embed_rows(rec["tok"])), "embedding rows differ")
-    for li, pre in enumerate(names):
-        kc = _cache_layer(caches[li][0])
-        vc = _cache_layer(caches[li][1])
-        H, S, Dh = kc.shape
-        cache = KVCache(1, H, S, Dh)
-        cache.k[0] = kc
-        cache.v[0] = vc
-        h_in, h_mid, h_out = R[2 * li], R[2 * li + 1], R[2 * li + 2]
-        o_mid, _, _ = om.attn_block(pre, h_in, pos, slots, keys, cache, 0)
-        tag = f"{what} {pre}"
-        rep.check("attention block contribution", h_mid - h_in, o_mid - h_in, tag)
-        rep.check("residual after attention", h_mid, o_mid, tag)
-        rep.check("K rows appended", kc[:, slots, :], cache.k[0][:, slots, :], tag)
-        rep.check("V rows appended", vc[:, slots, :], cache.v[0][:, slots, :], tag)
-        o_out, _, _ = om.mlp_block(pre, h_mid)
-        rep.check("MLP block contribution", h_out - h_mid, o_out - h_mid, tag)
-        rep.check("layer output", h_out, o_out, tag)
-    return om.rnd(rmsnorm(R[-1]))
+    Rall = f64(rec["resid"])
+    names = ["draft"] if rec["draft"] else [f"layer{l}" for l in range(m.n_layers)]
+    caches = _caches(sess, rec["draft"], nb, m.n_layers)
+    out = []
+    for b in range(nb):
+        R = Rall[:, b::nb]
+        tag_b = what + (f" branch {b}" if nb > 1 else "")
+        # the tokens recorded are branch 0's; every branch shares them outside the prompt
+        same_tok = b == 0 or not what.startswith("prefill")
+        if rec["draft"]:
+            xin = f64(rec["xin"])[b::nb]
+            if same_tok:
+                rep.exact(f"{what}: FC input embedding half", np.array_equal(xin[:, :d], om.embed_rows(rec["tok"])),
+                          "embedding rows differ")
+            rep.check("draft FC output", R[0], xin @ om.w("draft.fc").T, tag_b)
+        elif same_tok:
+            rep.exact(f"{what}: embedding", np.array_equal(R[0], om.embed_rows(rec["tok"])), "embedding rows differ")
+        for li, pre in enumerate(names):
+            kc = f64(caches[b][li][0])
+            vc = f64(caches[b][li][1])
+            H, S, Dh = kc.shape
+            cache = KVCache(1, H, S, Dh)
+            cache.k[0] = kc
+            cache.v[0] = vc
+            h_in, h_mid, h_out = R[2 * li], R[2 * li + 1], R[2 * li + 2]
+            o_mid, _, _ = om.attn_block(pre, h_in, pos, slots, keys, cache, 0)
+            tag = f"{tag_b} {pre}"
+            rep.check("attention block contribution", h_mid - h_in, o_mid - h_in, tag)
+            rep.check("residual after attention", h_mid, o_mid, tag)
+            rep.check("K rows appended", kc[:, slots, :], cache.k[0][:, slots, :], tag)
+            rep.check("V rows appended", vc[:, slots, :], cache.v[0][:, slots, :], tag)
+            o_out, _, _ = om.mlp_block(pre, h_mid)
+            rep.check("MLP block contribution", h_out - h_mid, o_out - h_mid, tag)
+            rep.check("layer output", h_out, o_out, tag)
+        out.append(om.rnd(rmsnorm(R[-1])))
+    return out
 
 
-def check_head(rep, om, feat_gpu, logits_gpu, f_ref, what):
-    """Final features against the oracle's norm of the GPU's final residual; logits against the
-    oracle's LM head applied to the GPU's own features."""
-    if feat_gpu is not None:
-        rep.check("final features", feat_gpu, f_ref, what)
-        base = feat_gpu
-    else:
-        base = f_ref
-    if logits_gpu is not None:
-        rep.check("logits", logits_gpu, base @ om.w("lm_head").T, what)
+def check_head(rep, om, feat_gpu, logits_gpu, f_ref, what, scale=None, branch_logits=None):
+    """Final features (per branch) against the oracle's norm of the GPU's final residual;
+    logits against the oracle's LM head applied to the GPU's own features.  With guidance the
+    per-branch logits (when given) are checked, and the guided logits l_u + s (l_c - l_u)
+    against the branch logits' combination within the propagated bound (|1 - s| + s) tol."""
+    nb = len(f_ref)
+    base = []
+    for b in range(nb):
+        if feat_gpu is not None:
+            rep.check("final features", feat_gpu[b], f_ref[b], what)
+            base.append(feat_gpu[b])
+        else:
+            base.append(f_ref[b])
+    if logits_gpu is None:
+        return
+    lb = [x @ om.w("lm_head").T for x in base]
+    if nb == 1:
+        rep.check("logits", logits_gpu, lb[0], what)
+        return
+    if branch_logits is not None:
+        for b in range(nb):
+            rep.check("branch logits", branch_logits[b], lb[b], what)
+    ref = lb[1] + scale * (lb[0] - lb[1])
+    k = abs(1.0 - scale) + scale
+    bound = k * (TOL[0] + TOL[1] * np.maximum(np.abs(lb[0]), np.abs(lb[1])))
+    ratio = float(np.max(np.abs(logits_gpu - ref) / bound))
+    rep.worst["guided logits / propagated bound"] = max(rep.worst.get("guided logits / propagated bound", 0.0),
+                                                       round(ratio, 4))
+    if ratio > 1.0:
+        rep.fail.append(f"guided logits {what}: {ratio:.3f} of the propagated bound")
 
 
 def _ws_rows(sess, ptr, rows, cols, dtype):
@@ -266,39 +304,50 @@ def crossfed_accept(cfg, knn, logits, parent, token, allowed, step):
 
 
 # ------------------------------------------------------------------------------ the run
-def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None):
+def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None, fixed_tree=False):
+    """Layer-local float checks and cross-fed integer checks over n_cycles cycles of the GPU's
+    own trajectory (fixed_tree: every cycle (d_hi, k_hi) instead of the schedule)."""
     m = cfg.model
     d, V, P = m.d_model, m.vocab, cfg.prefix_len
-    rep = Report(cfg.name + ("" if cfg.accept.mode == "greedy" else f"/{cfg.accept.mode}"))
+    guided = cfg.guidance is not None
+    nb = 2 if guided else 1
+    gs = cfg.guidance
+    rep = Report(cfg.name + ("" if cfg.accept.mode == "greedy" else f"/{cfg.accept.mode}") +
+                 (f"/guided {gs}" if guided else "") + ("/fixed" if fixed_tree else ""))
     knn_t = torch.from_numpy(knn).cuda() if knn is not None else None
-    sess = rt.DeviceSession(dm, cfg, poisson=poisson, knn=knn_t)
-    tdt = torch.bfloat16
-    sess.set_capture(resid_elems=(2 * m.n_layers + 1) * 128 * d + 8 * 128 * 3 * d, xin_bytes=4 * 128 * 2 * d * 2,
+    sess = rt.DeviceSession(dm, cfg, poisson=poisson, knn=knn_t, fixed_tree=fixed_tree)
+    tdt = torch.bfloat16 if m.dtype == "bf16" else torch.float32
+    sess.set_capture(resid_elems=(2 * m.n_layers + 1) * 128 * d + 8 * 128 * 3 * d, xin_bytes=4 * 128 * 2 * d * 4,
                      meta_elems=1 << 16)
     pre = synth.prefix_ids(cfg)
-    first = sess.prefill(pre)
+    null = synth.null_prefix_ids(cfg) if guided else None
+    first = sess.prefill(pre, null)
     recs = sess.captured()
     v = sess.view()
-    gfeat = {}     # GPU target feature (bf16 values as float64) per committed position
+    f_ref = None
     for r in recs:
         if r["draft"]:
-            check_forward(rep, om, sess, r, f"prefill draft rows {r['slot0']}..")
+            check_forward(rep, om, sess, r, f"prefill draft rows {r['slot0']}..", nb)
         else:
-            f_ref = check_forward(rep, om, sess, r, f"prefill target rows {r['slot0']}..")
+            f_ref = check_forward(rep, om, sess, r, f"prefill target rows {r['slot0']}..", nb)
     # the last chunk's features and the last prompt row's logits
     last = recs[-2] if recs[-1]["draft"] else recs[-1]
     assert not last["draft"]
     cn = last["nodes"]
-    feat = f64(_ws_rows(sess, v.feat, cn, d, tdt))
+    feat = f64(_ws_rows(sess, v.feat, cn * nb, d, tdt)).reshape(cn, nb, d)
     lg = f64(_ws_rows(sess, v.logits, 1, V, torch.float32))
-    check_head(rep, om, feat, None, f_ref, "prefill")
-    rep.check("logits", lg[0], feat[cn - 1] @ om.w("lm_head").T, "prefill last row")
+    bl = f64(_ws_rows(sess, v.branch_logits, nb, V, torch.float32)) if guided else None
+    check_head(rep, om, [feat[:, b] for b in range(nb)], None, f_ref, "prefill")
+    check_head(rep, om, [feat[cn - 1: cn, b] for b in range(nb)], lg[0:1], [f[cn - 1: cn] for f in f_ref],
+               "prefill last row", gs, None if bl is None else [bl[b: b + 1] for b in range(nb)])
+    gfeat = [{} for _ in range(nb)]   # GPU target features (bf16 values as float64) per committed position
     for r in range(cn):
-        gfeat[last["slot0"] + r] = feat[r]
+        for b in range(nb):
+            gfeat[b][last["slot0"] + r] = feat[r, b]
     lo, hi = cfg.allowed(0)
     op, ob = crossfed_accept(cfg, knn, lg, [-1], [int(pre[-1])], [(lo, hi)], 0)
     rep.exact("first token (cross-fed)", op == [] and ob == first, f"oracle {ob} gpu {first}")
-    log(cfg.name, "prefill checked", {k: v for k, v in rep.worst.items()})
+    log(rep.name, "prefill checked", {k: v for k, v in rep.worst.items()})
     records, prev, prev_cell = {}, None, None
     sched = rt.sched_struct(cfg.sched, cfg.grid_w)
     for cyc in range(1, n_cycles + 1):
@@ -309,19 +358,21 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None):
         remaining = cfg.n_image - cell
         if remaining <= 0:
             break
-        # schedule from the GPU's history: the oracle's and the library's host rule agree
-        pv = prev
-        if pv is not None and cfg.sched.alpha_source == "poisson":
-            pv = (min(int(poisson[prev_cell]), pv[1]), pv[1])
-        init = initial(cfg.sched, cell, records, cfg.grid_w)
-        d_hat, k_hat = schedule(cfg.sched, init, pv, remaining)
-        c_init = rt.schedule_init(sched, cell, records, cfg.n_image)
-        c_dk = rt.schedule_next(sched, c_init, pv, remaining)
-        rep.exact("schedule (oracle = library host rule)", (d_hat, k_hat) == c_dk, f"{(d_hat, k_hat)} vs {c_dk}")
-        t_draft = None
+        if fixed_tree:
+            d_hat, k_hat = min(cfg.sched.d_hi, remaining - 1), cfg.sched.k_hi
+        else:
+            # schedule from the GPU's history: the oracle's and the library's host rule agree
+            pv = prev
+            if pv is not None and cfg.sched.alpha_source == "poisson":
+                pv = (min(int(poisson[prev_cell]), pv[1]), pv[1])
+            init = initial(cfg.sched, cell, records, cfg.grid_w)
+            d_hat, k_hat = schedule(cfg.sched, init, pv, remaining)
+            c_init = rt.schedule_init(sched, cell, records, cfg.n_image)
+            c_dk = rt.schedule_next(sched, c_init, pv, remaining)
+            rep.exact("schedule (oracle = library host rule)", (d_hat, k_hat) == c_dk, f"{(d_hat, k_hat)} vs {c_dk}")
         if d_hat >= 1:
             sess.restart_capture()
-            n = sess.expand(d_hat, k_hat, cfg.sched.n_budget)
+            sess.expand(d_hat, k_hat, cfg.sched.n_budget)
             drecs = sess.captured()
             assert all(r["draft"] for r in drecs)
             t = sess.tensors()
@@ -330,16 +381,19 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None):
             xin = f64(cu["xin"])
             for r, p in enumerate(cu["pos"]):
                 p = int(p)
-                if p - 1 in gfeat:
-                    rep.exact("catch-up FC input feature = committed target feature",
-                              np.array_equal(xin[r, d:], gfeat[p - 1]), f"position {p}")
-            fr = check_forward(rep, om, sess, cu, f"cycle {cyc} draft catch-up")
+                for b in range(nb):
+                    if p - 1 in gfeat[b]:
+                        rep.exact("catch-up FC input feature = committed target feature",
+                                  np.array_equal(xin[nb * r + b, d:], gfeat[b][p - 1]), f"position {p} branch {b}")
+            fr = check_forward(rep, om, sess, cu, f"cycle {cyc} draft catch-up", nb)
             dl = f64(t["draft_logits"])
-            check_head(rep, om, None, dl[0], fr[-1], f"cycle {cyc} draft root")
+            dbl = f64(t["draft_branch_logits"]) if guided else None
+            check_head(rep, om, None, dl[0:1], [f[-1:] for f in fr], f"cycle {cyc} draft root", gs,
+                       None if dbl is None else [dbl[b: b + 1] for b in range(nb)])
             for li, r in enumerate(drecs[1:]):
-                fr = check_forward(rep, om, sess, r, f"cycle {cyc} draft level {li + 2}")
+                fr = check_forward(rep, om, sess, r, f"cycle {cyc} draft level {li + 2}", nb)
                 base = 1 + li * cfg.sched.k_hi
-                check_head(rep, om, None, dl[base: base + r["nodes"]], fr, f"cycle {cyc} draft level {li + 2}")
+                check_head(rep, om, None, dl[base: base + r["nodes"]], fr, f"cycle {cyc} draft level {li + 2}", gs)
             crossfed_expand(rep, cfg, t, drecs[1:], L, tokens[L], d_hat, k_hat, cfg.sched.n_budget, P)
         else:
             sess.set_tree([-1], [tokens[L]])
@@ -349,19 +403,21 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None):
         assert len(vrec) == 1 and not vrec[0]["draft"]
         t = sess.tensors()
         n = t["n"]
-        f_ref = check_forward(rep, om, sess, vrec[0], f"cycle {cyc} verify")
-        feat = f64(t["feat"])
+        f_ref = check_forward(rep, om, sess, vrec[0], f"cycle {cyc} verify", nb)
+        feat = f64(t["feat"]).reshape(n, nb, d)
         logits32 = t["logits"].cpu().numpy()
-        check_head(rep, om, feat, logits32.astype(np.float64), f_ref, f"cycle {cyc} verify")
+        vbl = f64(t["branch_logits"]) if guided else None
+        check_head(rep, om, [feat[:, b] for b in range(nb)], logits32.astype(np.float64), f_ref, f"cycle {cyc} verify",
+                   gs, None if vbl is None else [vbl[:, b] for b in range(nb)])
         parent = t["parent"].cpu().numpy()
         token = t["token"].cpu().numpy()
         depth = t["depth"].cpu().numpy()
         allowed = t["allowed"].cpu().numpy()
         want_allowed = np.array([cfg.allowed(L + int(dp) + 1 - P) for dp in depth])
         rep.exact("allowed ranges of the tree rows", np.array_equal(allowed, want_allowed), "")
-        # pre-commit K/V rows of the tree, every layer
-        pk = f64(sess.k_cache[:, :, L: L + n, :])
-        pvv = f64(sess.v_cache[:, :, L: L + n, :])
+        # pre-commit K/V rows of the tree, every layer (and branch)
+        pk = f64(sess.k_cache[..., L: L + n, :])
+        pvv = f64(sess.v_cache[..., L: L + n, :])
         opath, obonus = crossfed_accept(cfg, knn, logits32, parent, token, allowed, step)
         g = sess.accept_commit(d_hat, k_hat)
         t2 = sess.tensors()
@@ -373,20 +429,20 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None):
         # compaction: slot L + m <- slot L + v_m, bit for bit
         ck, cv = pk.copy(), pvv.copy()
         compact_cache(ck, cv, 0, gpath)
-        post_k = f64(sess.k_cache[:, :, L: L + 1 + a, :])
-        post_v = f64(sess.v_cache[:, :, L: L + 1 + a, :])
-        rep.exact("compacted K/V rows", np.array_equal(post_k, ck[:, :, : a + 1]) and
-                  np.array_equal(post_v, cv[:, :, : a + 1]), f"cycle {cyc}")
+        post_k = f64(sess.k_cache[..., L: L + 1 + a, :])
+        post_v = f64(sess.v_cache[..., L: L + 1 + a, :])
+        rep.exact("compacted K/V rows", np.array_equal(post_k, ck[..., : a + 1, :]) and
+                  np.array_equal(post_v, cv[..., : a + 1, :]), f"cycle {cyc}")
         rep.exact("draft cache length after the cycle", sess.view().Ld == (L + 1 if d_hat >= 1 else Ld), "")
-        gfeat[L] = feat[0]
-        for mm, u in enumerate(gpath, start=1):
-            gfeat[L + mm] = feat[u]
+        for b in range(nb):
+            gfeat[b][L] = feat[0, b]
+            for mm, u in enumerate(gpath, start=1):
+                gfeat[b][L + mm] = feat[u, b]
         for c in range(cell, cell + a + 1):
             records[c] = (d_hat, k_hat)
         prev, prev_cell = (a, d_hat), cell
         rep.bump("cycles")
-        log(cfg.name, f"cycle {cyc}: d={d_hat} k={k_hat} n={n} a={a}", dict(rep.count),
-            {k: v for k, v in rep.worst.items()})
+        log(rep.name, f"cycle {cyc}: d={d_hat} k={k_hat} n={n} a={a}", {k: v for k, v in rep.worst.items()})
     sess.set_capture(0)
     del sess
     gc.collect()
@@ -437,3 +493,24 @@ def test_anole_7b_full_depth_parity_exact_and_relaxed(rt):
     s2 = run_parity(rt, rcfg, dm, om, 8, knn=knn)
     assert not s2["failures"], s2
     assert s["counts"]["cycles"] >= 8 and s2["counts"]["cycles"] >= 8
+
+
+def _small_bf16():
+    cfg = synth.shrink(synth.get_config("llamagen_xl"), n_layers=2, d_model=256, n_heads=4, ffn=512, vocab=512)
+    return dataclasses.replace(cfg, prefix_len=16, img_hi=512, prefix_hi=512, grid_h=8, grid_w=8)
+
+
+@pytest.mark.parametrize("variant", ["adt", "fixed", "guided"])
+def test_bf16_small_parity(rt, variant):
+    """The 2-layer bf16 model (d 256, 4 x 64 heads, V 512, 8 x 8 grid) under the ADT schedule,
+    with fixed 6-deep 10-wide trees, and with classifier-free guidance (scale 3.0): every cycle
+    of the image layer-local within the bf16 tolerance and cross-fed bit-exact."""
+    cfg = _small_bf16()
+    if variant == "guided":
+        cfg = dataclasses.replace(cfg, guidance=3.0)
+    w = synth.model_weights(cfg)
+    dm = rt.DeviceModel(cfg, w)
+    om = OracleModel(cfg, w)
+    s = run_parity(rt, cfg, dm, om, 64, fixed_tree=variant == "fixed")
+    assert not s["failures"], s
+    assert s["counts"]["cycles"] >= 8
