@@ -41,18 +41,19 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # the sources the GEMM kernel is compiled from (kernel, shared helpers, epilogue struct)
 GEMM_SRCS = [os.path.join(ROOT, "paper_2512_21857_amd", "csrc", *parts)
              for parts in (("kernels", "gemm.hip"), ("common.h",), ("launch.h",))]
-TRAFFIC_FILES = {"lumina_7b": os.path.join(ROOT, "profiles", "gemm_tile_lumina_7b_traffic.md"),
-                 "llamagen_xl": os.path.join(ROOT, "profiles", "gemm_tile_llamagen_xl_traffic.md")}
+TRAFFIC_FILES = {"lumina_7b": os.path.join(ROOT, "profiles", "gemm_rows_lumina_7b_traffic.md")}
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def gemm_traffic(workload):
-    """HBM bytes per GEMM launch from the committed FETCH_SIZE / WRITE_SIZE counter summary of
-    this workload, or None when the kernel's sources changed since the counters were taken
-    (sha256 over gemm.hip, common.h and launch.h, in that order) or no summary exists."""
+def gemm_traffic(workload, algorithmic_bytes_per_launch):
+    """HBM bytes per GEMM launch: the counter-measured traffic / algorithmic ratio of the
+    committed FETCH_SIZE / WRITE_SIZE summary of this workload (every projection launch of a
+    --traffic-run) times this run's algorithmic bytes per launch; None when the kernel's
+    sources changed since the counters were taken (sha256 over gemm.hip, common.h and
+    launch.h, in that order) or no summary exists."""
     try:
         text = open(TRAFFIC_FILES[workload]).read()
         h = hashlib.sha256()
@@ -61,11 +62,11 @@ def gemm_traffic(workload):
         src = h.hexdigest()
     except (OSError, KeyError):
         return None
-    keys = ("source_sha256:", "traffic_bytes_per_launch:")
+    keys = ("source_sha256:", "traffic_over_algorithmic:")
     fields = dict(line.split(":", 1) for line in text.splitlines() if line.startswith(keys))
-    if fields.get("source_sha256", "").strip() != src:
+    if fields.get("source_sha256", "").strip() != src or "traffic_over_algorithmic" not in fields:
         return None
-    return int(fields["traffic_bytes_per_launch"].strip())
+    return int(round(float(fields["traffic_over_algorithmic"].strip()) * algorithmic_bytes_per_launch))
 
 
 def parse():
@@ -83,6 +84,10 @@ def parse():
     ap.add_argument("--no-microbench", action="store_true")
     ap.add_argument("--no-mfma", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip guided / stochastic / batched cycles")
+    ap.add_argument("--start-cell", type=int, default=-1, help="first timed image cell (default: mid-image)")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="counter-collection mode: profile every projection launch from the prefill on over the "
+                         "warm-up and timed steps of the headline workload and print their count and algorithmic bytes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -123,15 +128,22 @@ def fast_forward(sess, cfg, cell):
             return
 
 
-def profile_pass(abi, sess, k):
-    """Per-kernel-class HIP-event timing over k further steps of the same session (eager)."""
+def profile_pass(abi, sess, k, tag="profile"):
+    """Per-kernel-class HIP-event timing over k further steps of the same session (eager).
+    The pass's CLOCK_MONOTONIC window goes to stderr, so a kernel trace of the same command
+    (whose timestamps use that clock) can be cut to the same launches."""
     import ctypes as C
+    import torch
     L = abi.lib()
     abi.check(L.adt_profile_enable(1))
     for cls in (abi.PROF_GEMM, abi.PROF_ATTN, abi.PROF_COMPACT, abi.PROF_ROWS):
         L.adt_profile_read(cls, None, None, None, None, 1)
     v0 = sess.view()
+    torch.cuda.synchronize()
+    t0 = time.monotonic_ns()
     run_steps(sess, k)
+    t1 = time.monotonic_ns()
+    log(f"{tag} pass window {t0} {t1}")
     v1 = sess.view()
     out = {"L_from": v0.L, "L_to": v1.L}
     for name, cls in (("gemm", abi.PROF_GEMM), ("attn", abi.PROF_ATTN), ("compact", abi.PROF_COMPACT),
@@ -150,7 +162,7 @@ def roofline_of(prof, workload, kernel):
     byts = g["bytes"] / max(g["launches"], 1)
     gbs = byts / avg_s / 1e9 if avg_s > 0 else 0.0
     return {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": gemm_traffic(workload), "launches": g["launches"],
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": gemm_traffic(workload, byts), "launches": g["launches"],
             "avg_us": round(avg_s * 1e6, 3), "bytes_per_launch": round(byts),
             "residual_finish": {"launches": r["launches"], "avg_us": round(r["ms"] / max(r["launches"], 1) * 1e3, 3),
                                 "kernel": "resid_norm_kernel (K-range sums + residual add + RMSNorm)"}}
@@ -442,12 +454,27 @@ def main():
     dm = rt.DeviceModel(cfg, w)
     pre = synth.prefix_ids(cfg)
     poisson = synth.poisson_table(cfg)
-    mid = cfg.n_image // 2
+    mid = cfg.n_image // 2 if args.start_cell < 0 else args.start_cell
+    if args.traffic_run:
+        import ctypes as C
+        L = abi.lib()
+        abi.check(L.adt_profile_enable(1))
+        L.adt_profile_read(abi.PROF_GEMM, None, None, None, None, 1)
+        sess = rt.DeviceSession(dm, cfg, poisson=poisson)
+        sess.prefill(pre)
+        fast_forward(sess, cfg, mid)
+        run_steps(sess, W + K)
+        n, ms, by, fl = C.c_int64(), C.c_double(), C.c_double(), C.c_double()
+        abi.check(L.adt_profile_read(abi.PROF_GEMM, C.byref(n), C.byref(ms), C.byref(by), C.byref(fl), 1))
+        abi.check(L.adt_profile_enable(0))
+        print(json.dumps({"traffic_run": cfg.name, "gemm_launches": n.value, "gemm_algorithmic_bytes": by.value,
+                          "start_cell": mid, "steps": W + K}), flush=True)
+        return
     log(f"{cfg.name}: fast-forward to cell {mid}, {W} warm-up steps, {K} timed steps")
     sess, head = workload_run(rt, dm, cfg, pre, K, W, mid, poisson=poisson)
-    prof_mid = profile_pass(abi, sess, args.profile_steps)
+    prof_mid = profile_pass(abi, sess, args.profile_steps, "mid-image profile")
     fast_forward(sess, cfg, cfg.n_image - 2 * args.profile_steps)
-    prof_end = profile_pass(abi, sess, args.profile_steps)
+    prof_end = profile_pass(abi, sess, args.profile_steps, "end-of-image profile")
     del sess
     full = None if args.no_full_image else full_image(rt, dm, cfg, pre, poisson=poisson)
     cpu = None
