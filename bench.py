@@ -109,13 +109,19 @@ def run_steps(sess, k):
     return nodes, tokens, depth, steps
 
 
-def timed(sess, k):
+def timed(sess, k, tag=None):
+    """k steps between two synchronisations; with a tag, the CLOCK_MONOTONIC window of the
+    timed region goes to stderr for cutting a kernel trace of the same command."""
     import torch
     torch.cuda.synchronize()
+    w0 = time.monotonic_ns()
     t0 = time.perf_counter()
     nodes, tokens, depth, steps = run_steps(sess, k)
     torch.cuda.synchronize()
-    return time.perf_counter() - t0, nodes, tokens, depth, steps
+    dt = time.perf_counter() - t0
+    if tag:
+        log(f"{tag} pass window {w0} {time.monotonic_ns()}")
+    return dt, nodes, tokens, depth, steps
 
 
 def fast_forward(sess, cfg, cell):
@@ -182,12 +188,12 @@ def steps_line(dt, nodes, tokens, depth, steps):
             "steps": steps}
 
 
-def workload_run(rt, dm, cfg, pre, k, warm, start_cell, **sess_kw):
+def workload_run(rt, dm, cfg, pre, k, warm, start_cell, tag=None, **sess_kw):
     sess = rt.DeviceSession(dm, cfg, **sess_kw)
     sess.prefill(pre)
     fast_forward(sess, cfg, start_cell)
     run_steps(sess, warm)
-    line = steps_line(*timed(sess, k))
+    line = steps_line(*timed(sess, k, tag))
     line["start_cell"] = start_cell
     return sess, line
 
@@ -471,7 +477,7 @@ def main():
                           "start_cell": mid, "steps": W + K}), flush=True)
         return
     log(f"{cfg.name}: fast-forward to cell {mid}, {W} warm-up steps, {K} timed steps")
-    sess, head = workload_run(rt, dm, cfg, pre, K, W, mid, poisson=poisson)
+    sess, head = workload_run(rt, dm, cfg, pre, K, W, mid, tag="timed", poisson=poisson)
     prof_mid = profile_pass(abi, sess, args.profile_steps, "mid-image profile")
     fast_forward(sess, cfg, cfg.n_image - 2 * args.profile_steps)
     prof_end = profile_pass(abi, sess, args.profile_steps, "end-of-image profile")

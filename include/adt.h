@@ -373,7 +373,10 @@ typedef struct {
   int32_t* path; int32_t* n_acc; int32_t* bonus;  /* last acceptance */
   const int32_t* tokens_host;   /* [host] committed ids */
   /* scratch of the last forward (last layer run): rotated queries [rows][d] dtype, attention
-   * output [rows][d] dtype, normed activations [rows][d] dtype, residual stream [rows][d] fp32 */
+   * output [rows][d] dtype, normed activations [rows][d] dtype, residual stream [rows][d] fp32.
+   * In bf16 sessions att and act hold the fragment layout of the projections' inputs: with
+   * B = (rows + 15) / 16 row blocks, element (r, k) sits at
+   * (((k / 32) * B + r / 16) * 64 + r % 16 + 16 * ((k % 32) / 8)) * 8 + k % 8. */
   void* q; void* att; void* act; float* resid;
   /* guidance: rows of the last forwards hold node i's branches at rows nb i + b (b = 0
    * conditional); feat is then [ADT_MAX_NODES / 2][2][d_model] and logits / draft_logits are

@@ -860,17 +860,26 @@ static adt_status capt_snap(adt_session_s* s, int idx, hipStream_t st) {
 }
 
 // Finish of a bf16 residual projection: its K-range sums added to the residual rows (or
-// assigned) and the rows' RMSNorm into out.
-static adt_status resid_finish(adt_session_s* s, int splits, int rows, int assign, void* out, hipStream_t st) {
+// assigned) and the rows' RMSNorm into out (layout out_pk) and, if given, out2 (layout out2_pk).
+static adt_status resid_finish(adt_session_s* s, int splits, int rows, int assign, void* out, int out_pk, void* out2,
+                               int out2_pk, hipStream_t st) {
   const int e = prof_begin(st);
-  TRY(launch_resid_norm(s->part, splits, rows, s->dm, assign, s->m->d.norm_eps, s->h, out, s->dt, st));
-  prof_end(e, ADT_PROF_ROWS, (double)splits * rows * s->dm * 4.0 + rows * s->dm * (8.0 + esize(s->dt)), 0.0, st);
+  TRY(launch_resid_norm(s->part, splits, rows, s->dm, assign, s->m->d.norm_eps, s->h, out, out_pk, out2, out2_pk, s->dt,
+                        st));
+  prof_end(e, ADT_PROF_ROWS,
+           (double)splits * rows * s->dm * 4.0 + rows * s->dm * (8.0 + (out2 ? 2.0 : 1.0) * esize(s->dt)), 0.0, st);
   return ADT_OK;
 }
 
+// bf16 forwards keep the inputs of their projections (act, att, sw, xin) in the fragment layout
+// of this many 16-row blocks; fp32 forwards keep them row-major.
+static int act_blocks(const adt_session_s* s, int rows) { return s->dt == ADT_BF16 ? (rows + 15) / 16 : 0; }
+
 // Decoder layers over the nb * M rows of M tree nodes (branches interleaved node by node).
+// The final norm goes to final_out (row-major; bf16: act if null) and, with act_too (bf16),
+// also to act.
 static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t* pos, int slot0, int L_pre, int n_tail,
-                             const uint64_t* mask, void* final_out, hipStream_t st) {
+                             const uint64_t* mask, void* final_out, bool act_too, hipStream_t st) {
   const adt_model_s* m = s->m;
   const int dm = s->dm, H = s->H, Dh = s->Dh, F = s->F, dt = s->dt, nb = s->nb, rows = nb * M;
   const int64_t cache_sb = draft ? s->dcache_sb : s->tcache_sb;
@@ -879,13 +888,16 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
   const int64_t stride_h = (int64_t)s->d.s_cap * Dh;
   const float eps = m->d.norm_eps;
   const float scale = 1.f / std::sqrt((float)Dh);
+  const int pk = act_blocks(s, rows);
   (void)slot0;
   const int l0 = draft ? s->Lr : 0, l1 = draft ? s->Lr + 1 : s->Lr;
   auto attention = [&](char* kc, char* vc) -> adt_status {
     // the prefix K/V once, tree Q/K/V in and O out, the masks
     const int e = prof_pair();
+    AttnRows rl{1, nb, 0};
+    rl.o_pk = pk;
     TRY(launch_tree_attn(s->q, kc, vc, cache_sb, stride_h, s->scal + SC_KV, s->scal + SC_NQ, s->scal + SC_TAIL, mask,
-                         AttnRows{1, nb, 0}, nb, H, Dh, M, s->d.s_cap, scale, dt, s->att, s->attn_ws,
+                         rl, nb, H, Dh, M, s->d.s_cap, scale, dt, s->att, s->attn_ws,
                          s->attn_ws_bytes, st, e >= 0 ? g_prof.ev[e] : nullptr, e >= 0 ? g_prof.ev[e + 1] : nullptr));
     prof_done(e, ADT_PROF_ATTN, nb * (2.0 * L_pre * H * Dh * es + 4.0 * M * H * Dh * es) + 16.0 * M,
               4.0 * rows * (L_pre + n_tail) * H * Dh);
@@ -916,18 +928,22 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       qkv.Dh = Dh;
       qkv.nb = nb;
       qkv.cache_sb = cache_sb;
-      TRY(gemm_p(s->act, dm, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
+      TRY(gemm_p(s->act, X_FRAG, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
       int sp = 1;
-      TRY(gemm_p(s->att, dm, m->o[l], rows, dm, dm, dt, s->part, st, pe, &sp));
-      TRY(resid_finish(s, sp, rows, 0, s->act, st));
+      TRY(gemm_p(s->att, X_FRAG, m->o[l], rows, dm, dm, dt, s->part, st, pe, &sp));
+      TRY(resid_finish(s, sp, rows, 0, s->act, pk, nullptr, 0, st));
       TRY(capt_snap(s, 2 * (l - l0) + 1, st));
       GemmEpi sw;
       sw.mode = EPI_SWIGLU;
       sw.act = (uint16_t*)s->sw;
-      TRY(gemm_p(s->act, dm, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
-      TRY(gemm_p(s->sw, F, m->down[l], rows, dm, F, dt, s->part, st, pe, &sp));
-      TRY(resid_finish(s, sp, rows, 0, (l + 1 == l1 && final_out) ? final_out : s->act, st));
+      sw.act_pk = pk;
+      TRY(gemm_p(s->act, X_FRAG, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
+      TRY(gemm_p(s->sw, X_FRAG, m->down[l], rows, dm, F, dt, s->part, st, pe, &sp));
+      if (l + 1 == l1 && final_out)
+        TRY(resid_finish(s, sp, rows, 0, final_out, 0, act_too ? s->act : nullptr, pk, st));
+      else
+        TRY(resid_finish(s, sp, rows, 0, s->act, pk, nullptr, 0, st));
     }
     TRY(capt_snap(s, 2 * (l1 - l0), st));
     return ADT_OK;
@@ -952,8 +968,10 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
 }
 
 // Logits of M nodes (nb rows each) into out [M][V]; with guidance the per-branch rows go to
-// raw [nb M][V] and out gets their combination.
-static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float* out, float* raw, hipStream_t st) {
+// raw [nb M][V] and out gets their combination.  feat_rows: row-major with ldx = d_model, or
+// (bf16, ldx == X_FRAG) the fragment layout.
+static adt_status lm_head(adt_session_s* s, const void* feat_rows, int ldx, int M, float* out, float* raw,
+                          hipStream_t st) {
   const int rows = s->nb * M;
   float* dst = s->nb > 1 ? raw : out;
   if (s->dt == ADT_BF16) {
@@ -961,7 +979,7 @@ static adt_status lm_head(adt_session_s* s, const void* feat_rows, int M, float*
     e.mode = EPI_STORE;
     e.out = dst;
     e.ldo = s->V;
-    TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st, e));
+    TRY(gemm_p(feat_rows, ldx, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st, e));
   } else {
     TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st));
     TRY(launch_reduce_store(s->part, 1, rows, s->V, dst, s->V, st));
@@ -979,12 +997,17 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
     TRY(capt_begin(s, false, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
+    const int pk = act_blocks(s, s->nb * M);
     TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, cs,
-                          Branches{s->nb, tok_boff, 0}));
-    TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, cs));
-    if (lm_rows > 0)
-      TRY(lm_head(s, (const char*)s->feat + (size_t)s->nb * lm_row0 * s->dm * esize(s->dt), lm_rows, s->logits,
-                  s->rawlog, cs));
+                          Branches{s->nb, tok_boff, 0}, pk));
+    // logits of every row read the final norm from act in the fragment layout
+    const bool all = pk && lm_row0 == 0 && lm_rows == M;
+    TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, all, cs));
+    if (all)
+      TRY(lm_head(s, s->act, X_FRAG, lm_rows, s->logits, s->rawlog, cs));
+    else if (lm_rows > 0)
+      TRY(lm_head(s, (const char*)s->feat + (size_t)s->nb * lm_row0 * s->dm * esize(s->dt), s->dm, lm_rows,
+                  s->logits, s->rawlog, cs));
     s->capt_cur = -1;
     return ADT_OK;
   };
@@ -1002,26 +1025,31 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
   TRY(set_scalars(s, L_pre, M, n_tail, slot0, st));
   auto body = [&](hipStream_t cs) -> adt_status {
     TRY(capt_begin(s, true, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
+    const int pk = act_blocks(s, rows);
     TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, rows, dm, s->xin, dt, cs,
-                           Branches{s->nb, tok_boff, 0}));
-    if (s->capt_cur >= 0)
-      ADT_HIP(hipMemcpyAsync((char*)s->capt.xin + s->capt_log[s->capt_cur].xin_off, s->xin,
-                             (size_t)rows * 2 * dm * esize(dt), hipMemcpyDeviceToDevice, cs));
+                           Branches{s->nb, tok_boff, 0}, pk));
+    if (s->capt_cur >= 0)   // the captured FC input is row-major
+      TRY(launch_draft_input(s->m->d.embed, tok, fsrc, fa, s->dfeat, rows, dm,
+                             (char*)s->capt.xin + s->capt_log[s->capt_cur].xin_off, dt, cs,
+                             Branches{s->nb, tok_boff, 0}, 0));
     if (dt == ADT_BF16) {
       GemmEpi e;
       e.mode = EPI_PART;
       e.part = s->part;
       e.part_elems = s->part_elems;
       int sp = 1;
-      TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e, &sp));
-      TRY(resid_finish(s, sp, rows, 1, s->act, cs));
+      TRY(gemm_p(s->xin, X_FRAG, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e, &sp));
+      TRY(resid_finish(s, sp, rows, 1, s->act, pk, nullptr, 0, cs));
     } else {
       TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs));
       TRY(launch_add_norm(s->part, 1, rows, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));
     }
-    TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, cs));
-    if (lm_rows > 0)
-      TRY(lm_head(s, (const char*)fout + (size_t)s->nb * lm_row0 * dm * esize(dt), lm_rows, lout, lraw, cs));
+    const bool all = pk && fout && lm_row0 == 0 && lm_rows == M;
+    TRY(run_layers(s, true, M, pos, slot0, L_pre, n_tail, mask, fout, all, cs));
+    if (all)
+      TRY(lm_head(s, s->act, X_FRAG, lm_rows, lout, lraw, cs));
+    else if (lm_rows > 0)
+      TRY(lm_head(s, (const char*)fout + (size_t)s->nb * lm_row0 * dm * esize(dt), dm, lm_rows, lout, lraw, cs));
     s->capt_cur = -1;
     return ADT_OK;
   };

@@ -34,6 +34,28 @@ template <> struct Elem<uint16_t> {
   __device__ static __forceinline__ float load(const uint16_t* p, int64_t i) { return bf2f(p[i]); }
   __device__ static __forceinline__ void store(uint16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
 };
+// Four consecutive values at p (aligned to four elements): one vector store.
+__device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void store4(uint16_t* p, float a, float b, float c, float d) {
+  *reinterpret_cast<u16x4*>(p) = u16x4{f2bf(a), f2bf(b), f2bf(c), f2bf(d)};
+}
+
+// Fragment layout of a bf16 activation matrix (rows r < 16 pk, K columns, K % 32 == 0): the
+// 16 x 32 block (r / 16, k / 32) is 1 KB contiguous in the order a wave hands it to the
+// 16x16x32 MFMA as its B operand (lane (r % 16) + 16 ((k % 32) / 8) holds 8 consecutive
+// columns), and blocks follow each other row block fastest: block (k / 32) pk + r / 16.  A
+// wave then reads a block with one contiguous 16-byte load per lane, where the row-major
+// layout needs sixteen half-used 128-byte lines.  pk = 0 selects row-major with leading
+// dimension ld.  Runs of up to 8 columns starting at a multiple of their length stay
+// contiguous in both layouts.
+__host__ __device__ __forceinline__ int64_t frag_index(int64_t r, int k, int pk) {
+  return (((int64_t)(k >> 5) * pk + (r >> 4)) * 64 + (r & 15) + ((k & 31) >> 3) * 16) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ int64_t act_index(int64_t r, int k, int64_t ld, int pk) {
+  return pk ? frag_index(r, k, pk) : r * ld + k;
+}
 
 // Philox4x32-10 (Salmon et al., SC'11): ten rounds over counter (c0..c3) with key (k0, k1);
 // host and device share it (acceptance draws on the GPU, the Random tree initialisation on

@@ -278,55 +278,58 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
         ls += wt * mml[((w0 + w) * 16 + row) * 2 + 1];
         acc += wt * mo[((size_t)(w0 + w) * 16 + row) * DH + d];
       }
-      out[(rl.q_row(b, qr) * H + h) * DH + d] = f2bf(ls > 0.f ? acc / ls : 0.f);
+      out[rl.o_index(b, qr, H, DH, h, d)] = f2bf(ls > 0.f ? acc / ls : 0.f);
     }
     __syncthreads();
   }
 }
 
-// Log-sum-exp merge of the split partials; one block of DH threads per (query, head, seq).
-// Every split's (m, l) is loaded at once (one lane per split), then the weighted sum of
-// the O partials is taken in split order.
-template <typename OutT>
-__global__ void tree_attn_combine_kernel(const float* __restrict__ part_o, const float* __restrict__ part_ml,
-                                         const int32_t* __restrict__ n_q, AttnRows rl, int H, int nq_max, int splits,
-                                         int DH, OutT* __restrict__ out) {
-  __shared__ float wsh[ATT_MAX_SPLITS];
-  __shared__ float red[4];
-  const int qr = blockIdx.x, h = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
+// Log-sum-exp merge of the key splits: split s holds the unnormalised O and (m, l) of query
+// qr (m in the log2 domain) at row base + s * nq_max + qr.  A thread merges four dims of one
+// query (DH / 4 threads per query, COMB_THREADS / (DH / 4) queries per block); the splits'
+// values are requested eight at a time before any is used, and weights and sums run in
+// split order.
+constexpr int COMB_THREADS = 256;
+__global__ __launch_bounds__(COMB_THREADS) void tree_attn_combine_kernel(
+    const float* __restrict__ part_o, const float* __restrict__ part_ml, const int32_t* __restrict__ n_q, AttnRows rl,
+    int H, int nq_max, int splits, int DH, uint16_t* __restrict__ out) {
+  const int h = blockIdx.y, b = blockIdx.z, per_q = DH / 4;
+  const int qr = blockIdx.x * (COMB_THREADS / per_q) + threadIdx.x / per_q, d = (threadIdx.x % per_q) * 4;
   if (qr >= min(n_q[b], nq_max)) return;
-  const int64_t base = (((int64_t)b * H + h) * splits) * nq_max;
-  float m = -INFINITY, l = 0.f;
-  if (d < splits) {
-    m = part_ml[(base + (int64_t)d * nq_max + qr) * 2];
-    l = part_ml[(base + (int64_t)d * nq_max + qr) * 2 + 1];
+  const int64_t base = (((int64_t)b * H + h) * splits) * nq_max + qr;
+  float M = -INFINITY;
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float mv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mv[j] = s0 + j < splits ? part_ml[(base + (int64_t)(s0 + j) * nq_max) * 2] : -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);
   }
-  float M = wave_max(m);
-  const int nw = (int)(blockDim.x + WAVE - 1) / WAVE;
-  if (nw > 1) {
-    if (d % WAVE == 0) red[d / WAVE] = M;
-    __syncthreads();
-    M = red[0];
-    for (int i = 1; i < nw; ++i) M = fmaxf(M, red[i]);
-    __syncthreads();
+  float ls = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float mv[8], lv[8];
+    float4 ov[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      mv[j] = -INFINITY;
+      if (s0 + j < splits) {
+        const int64_t r = base + (int64_t)(s0 + j) * nq_max;
+        mv[j] = part_ml[r * 2];
+        lv[j] = part_ml[r * 2 + 1];
+        ov[j] = *reinterpret_cast<const float4*>(part_o + r * DH + d);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (mv[j] == -INFINITY) continue;
+      const float w = exp2f(mv[j] - M);
+      ls += w * lv[j];
+      acc = make_float4(acc.x + w * ov[j].x, acc.y + w * ov[j].y, acc.z + w * ov[j].z, acc.w + w * ov[j].w);
+    }
   }
-  const float w = (m == -INFINITY) ? 0.f : exp2f(m - M);
-  if (d < splits) wsh[d] = w;
-  float ls = wave_sum(w * l);
-  if (nw > 1) {
-    if (d % WAVE == 0) red[d / WAVE] = ls;
-    __syncthreads();
-    ls = 0.f;
-    for (int i = 0; i < nw; ++i) ls += red[i];
-  }
-  __syncthreads();
-  float acc = 0.f;
-#pragma unroll 8
-  for (int s = 0; s < splits; ++s) {
-    const float ws = wsh[s];
-    if (ws != 0.f) acc += ws * part_o[(base + (int64_t)s * nq_max + qr) * DH + d];
-  }
-  Elem<OutT>::store(out, (rl.q_row(b, qr) * H + h) * DH + d, ls > 0.f ? acc / ls : 0.f);
+  const float inv = ls > 0.f ? 1.f / ls : 0.f;
+  store4(out + rl.o_index(b, qr, H, DH, h, d), acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
 }
 
 // fp32 path: one block per (query, head, sequence); scores staged in LDS.
@@ -400,8 +403,8 @@ __device__ __forceinline__ int blk_swz_k(int row) { return DH == 128 ? (row & 15
 template <int DH>
 __device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
 
-template <int DH, int KH, int NW>
-__global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
+template <int DH, int KH, int NW, int P>
+__global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
@@ -450,24 +453,25 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
 
   // Slot s (16 bytes) of a block holds row s / CH, chunk (s % CH) ^ swizzle(row); thread t
   // fills slots r * 512 + t.  Keys past the live range repeat the last key (masked below).
-  u16x8 kr[LOADS], vr[LOADS];
-  auto fetch_block = [&](int blk) {
+  // P register stages: block blk + P is requested while block blk is computed
+  u16x8 kr[P][LOADS], vr[P][LOADS];
+  auto fetch_block = [&](int u, int blk) {
     const int last = max(total - 1, 0);
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int slot = r * NW * WAVE + threadIdx.x, row = slot / CH, phys = slot % CH;
       const int64_t key = min(blk * BLK_KT + row, last);
-      kr[r] = *reinterpret_cast<const u16x8*>(kbase + key * DH + (phys ^ blk_swz_k<DH>(row)) * 8);
-      vr[r] = *reinterpret_cast<const u16x8*>(vbase + key * DH + (phys ^ blk_swz_v<DH>(row)) * 8);
+      kr[u][r] = *reinterpret_cast<const u16x8*>(kbase + key * DH + (phys ^ blk_swz_k<DH>(row)) * 8);
+      vr[u][r] = *reinterpret_cast<const u16x8*>(vbase + key * DH + (phys ^ blk_swz_v<DH>(row)) * 8);
     }
   };
-  auto store_block = [&](int buf) {
+  auto store_block = [&](int u, int buf) {
     unsigned char* kb = smem + buf * 2 * BLK_BYTES;
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int slot = r * NW * WAVE + threadIdx.x;
-      *reinterpret_cast<u16x8*>(kb + slot * 16) = kr[r];
-      *reinterpret_cast<u16x8*>(kb + BLK_BYTES + slot * 16) = vr[r];
+      *reinterpret_cast<u16x8*>(kb + slot * 16) = kr[u][r];
+      *reinterpret_cast<u16x8*>(kb + BLK_BYTES + slot * 16) = vr[u][r];
     }
   };
 
@@ -475,13 +479,8 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
 #pragma unroll
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  if (blk0 < nblk) fetch_block(blk0);
-  for (int blk = blk0; blk < nblk; ++blk) {
-    // the buffer written here was last read two blocks ago, before the previous barrier
-    store_block(blk & 1);
-    __syncthreads();
-    if (blk + 1 < nblk) fetch_block(blk + 1);
-    if (!active) continue;
+  // this wave's share of block blk, read from LDS buffer blk & 1
+  auto compute = [&](int blk) {
     const unsigned char* kb = smem + (blk & 1) * 2 * BLK_BYTES;
     const unsigned char* vb = kb + BLK_BYTES;
     // this wave's keys of the block, 32 at a time: S^T = K Q^T (lane (lq, g) gets keys
@@ -561,6 +560,22 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
         o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[d], 0, 0, 0);
       }
     }
+  };
+#pragma unroll
+  for (int u = 0; u < P; ++u)
+    if (blk0 + u < nblk) fetch_block(u, blk0 + u);
+  for (int base = blk0; base < nblk; base += P) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      const int blk = base + u;
+      if (blk < nblk) {
+        // the buffer written here was last read two blocks ago, before the previous barrier
+        store_block(u, blk & 1);
+        __syncthreads();
+        if (blk + P < nblk) fetch_block(u, blk + P);
+        if (active) compute(blk);
+      }
+    }
   }
 
   // KH > 1: parts 1.. of a tile pass their state through LDS to part 0, which merges them
@@ -597,11 +612,10 @@ __global__ __launch_bounds__(NW * WAVE, 4) void tree_attn_blk_kernel(
   if (active && kpart == 0 && qr < nq) {
     if (splits == 1) {
       const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-      uint16_t* op = out + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
-        *reinterpret_cast<u16x4*>(op + d * 16 + 4 * g) =
-            u16x4{f2bf(o[d][0] * inv), f2bf(o[d][1] * inv), f2bf(o[d][2] * inv), f2bf(o[d][3] * inv)};
+        store4(out + rl.o_index(b, qr, H, DH, h, d * 16 + 4 * g), o[d][0] * inv, o[d][1] * inv, o[d][2] * inv,
+               o[d][3] * inv);
     } else {
       // this split's (O, m, l) for the log-sum-exp merge (m in the log2 domain)
       const int64_t pr = (((int64_t)b * H + h) * splits + sp) * nq_max + qr;
@@ -721,27 +735,37 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   const dim3 grid(H, B, S);
   const int qt = (nq_max + 15) / 16;
   hipEvent_t e1 = S > 1 ? nullptr : ev1;
-#define ADT_ATTN_BLK(DHV, KHV, NWV)                                                                                \
-  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, e1, 0,            \
+#define ADT_ATTN_BLK_P(DHV, KHV, NWV, PV)                                                                       \
+  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV, PV>, grid, dim3(NWV * WAVE), 0, st, ev0, e1, 0,        \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, S, part_o, part_ml)
+  // a split workgroup owns the CU and streams a few blocks, so it keeps three in flight; many
+  // pairs without splits keep one (two workgroups share a CU)
+#define ADT_ATTN_BLK(DHV, KHV, NWV)        \
+  if (S > 1) {                             \
+    ADT_ATTN_BLK_P(DHV, KHV, NWV, 3);      \
+  } else {                                 \
+    ADT_ATTN_BLK_P(DHV, KHV, NWV, 1);      \
+  }
   // two tiles at head size 128: four waves (two tiles x two key halves, ~190 VGPRs), so two
   // workgroups share a CU and a 512-pair launch is resident at once (32 nodes: 61 % of
   // 8 TB/s against 58 % with eight waves in 128-key blocks, one workgroup per CU)
   if (Dh == 128) {
-    if (qt <= 2) ADT_ATTN_BLK(128, 2, 4);
-    else if (qt <= 4) ADT_ATTN_BLK(128, 2, AWG_W);
-    else ADT_ATTN_BLK(128, 1, AWG_W);
+    if (qt <= 2) { ADT_ATTN_BLK(128, 2, 4) }
+    else if (qt <= 4) { ADT_ATTN_BLK(128, 2, AWG_W) }
+    else { ADT_ATTN_BLK(128, 1, AWG_W) }
   } else {
-    if (qt <= 2) ADT_ATTN_BLK(64, 4, AWG_W);
-    else if (qt <= 4) ADT_ATTN_BLK(64, 2, AWG_W);
-    else ADT_ATTN_BLK(64, 1, AWG_W);
+    if (qt <= 2) { ADT_ATTN_BLK(64, 4, AWG_W) }
+    else if (qt <= 4) { ADT_ATTN_BLK(64, 2, AWG_W) }
+    else { ADT_ATTN_BLK(64, 1, AWG_W) }
   }
 #undef ADT_ATTN_BLK
+#undef ADT_ATTN_BLK_P
   ADT_LAUNCH_CHECK();
   if (S > 1) {
-    const dim3 g2(nq_max, H, B);
-    hipExtLaunchKernelGGL(tree_attn_combine_kernel<uint16_t>, g2, dim3(Dh), 0, st, nullptr, ev1, 0, part_o, part_ml,
+    const int qpb = COMB_THREADS / (Dh / 4);
+    const dim3 g2((nq_max + qpb - 1) / qpb, H, B);
+    hipExtLaunchKernelGGL(tree_attn_combine_kernel, g2, dim3(COMB_THREADS), 0, st, nullptr, ev1, 0, part_o, part_ml,
                           n_q, rl, H, nq_max, S, Dh, (uint16_t*)out);
     ADT_LAUNCH_CHECK();
   }
@@ -752,6 +776,10 @@ adt_status launch_tree_attn(const void* q, const void* k, const void* v, int64_t
                             const int32_t* n_q, const int32_t* n_tail, const uint64_t* mask, AttnRows rl, int B, int H, int Dh,
                             int nq_max, int kv_cap, float scale, int dtype, void* out, void* ws, size_t ws_bytes,
                             hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  ADT_CHECK_ARG(rl.o_pk == 0 || (dtype == ADT_BF16 && (H * Dh) % 32 == 0 && !rl.row_off &&
+                                  (int64_t)(B - 1) * rl.rs_b + (int64_t)(nq_max - 1) * rl.rs_i < 16LL * rl.o_pk),
+                ADT_E_ARG, "tree_attn: fragment-layout output of %d row blocks (bf16, rows of a multiple of 32 values)",
+                rl.o_pk);
   if (dtype == ADT_F32) {
     const size_t sm = (size_t)(Dh + kv_cap) * sizeof(float);
     ADT_CHECK_ARG(sm <= 60 * 1024, ADT_E_CAPACITY, "tree_attn f32: kv_cap %d too large for LDS scores", kv_cap);

@@ -130,7 +130,7 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
     const f32x4 u = shfl_xor4(y, 32);
     if (live && g < 2) {
       const int f = nt * 8 + 4 * g;
-      *reinterpret_cast<u16x4*>(e.act + (int64_t)row * (N / 2) + f) =
+      *reinterpret_cast<u16x4*>(e.act + act_index(row, f, N / 2, e.act_pk)) =
           u16x4{f2bf(y[0] / (1.f + expf(-y[0])) * u[0]), f2bf(y[1] / (1.f + expf(-y[1])) * u[1]),
                 f2bf(y[2] / (1.f + expf(-y[2])) * u[2]), f2bf(y[3] / (1.f + expf(-y[3])) * u[3])};
     }
@@ -164,9 +164,15 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
   const bf16x8* wp[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(cb * T + t) * KT * 64 + lane;
+  // input fragment m of k-tile kk at xp[m] + kk * xks: row-major rows (clamped to M - 1), or
+  // the fragment layout's 1 KB blocks (row blocks past the last clamped to it)
+  const int mt = (M + 15) / 16;
   const uint16_t* xp[MT];
 #pragma unroll
-  for (int m = 0; m < MT; ++m) xp[m] = X + (int64_t)min(m * 16 + lq, M - 1) * ldx + g * 8;
+  for (int m = 0; m < MT; ++m)
+    xp[m] = ldx == X_FRAG ? X + ((int64_t)min(m, mt - 1) * WAVE + lane) * 8
+                          : X + (int64_t)min(m * 16 + lq, M - 1) * ldx + g * 8;
+  const int64_t xks = ldx == X_FRAG ? (int64_t)mt * WAVE * 8 : 32;
   // round start of the i-th round (c = kt0 + i * KC) after the rotation
   auto kmap = [&](int c) {
     int r = c - kt0 + rot;
@@ -182,7 +188,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
 #pragma unroll
       for (int t = 0; t < T; ++t) w[j][t] = wp[t][(int64_t)kk * 64];
 #pragma unroll
-      for (int m = 0; m < MT; ++m) x[j][m] = *reinterpret_cast<const bf16x8*>(xp[m] + kk * 32);
+      for (int m = 0; m < MT; ++m) x[j][m] = *reinterpret_cast<const bf16x8*>(xp[m] + kk * xks);
     }
   };
   f32x4 acc[T][MT];
@@ -301,30 +307,29 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
   return ADT_OK;
 }
 
-// Tiles per workgroup T and K ranges S for M rows of an N x K product.  Measured on the 7B
-// layer shapes (K 4096 / 11008, N 4096 - 65536) at 4, 11 and 61 rows: one workgroup per CU
-// (256) with the widest T the registers allow wins; at 61 rows QKV 768 tiles T = 3 (256
-// workgroups) 27 against 48 us, O and down (256 tiles) T = 4 with 4 K ranges 12 / 26 against
-// 20 / 52 us, gate/up T = 4 (344) 62 against 96 us; at <= 16 rows the narrower T = 1-3 that
-// give 256-2048 workgroups (LM head T = 2, 86 against 112 us).  partial: the caller adds the
-// K-range sums (residual projections), so S may exceed 1.
+// Tiles per workgroup T and K ranges S for M rows of an N x K product, measured with inputs in
+// the fragment layout on the 7B layer shapes (K 4096 / 8192 / 11008, N 4096 - 65536) at 4,
+// 17 and 61 rows.  One K range: T as wide as the registers allow while the launch keeps
+// >= 256 workgroups, and wider than 2 only where that is exactly one workgroup per CU (61
+// rows: QKV 768 tiles T = 3, 22 us against 25 at T = 4; gate/up 1376 tiles T = 2, 49
+// against 58; LM head 4096 tiles T = 2, 135 against 144).  partial: the caller adds the
+// K-range sums (residual projections), so S may exceed 1 as long as every wave keeps about
+// ten k-tiles (a shorter range never reaches its steady state): O (K 4096) T = 1 S = 1
+// 9.1 us against 11.5 at T = 4 S = 4, down (K 11008) T = 4 S = 4 21 against 28 at S = 1.
 RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
   const int mt = (M + 15) / 16, tiles = N / 16, KT = K / 32;
   const int tmax = mt <= 4 ? 4 : 2;
   auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
   if (!partial || (mt == 1 && tiles >= 192)) {
-    // one K range: the widest T that still gives >= 256 workgroups (at one row block, wider
-    // than 2 only if that is exactly one workgroup per CU)
     int T = 1;
     for (int t : {4, 3, 2})
-      if (ok(t) && tiles / t >= 256 && (mt > 1 || t <= 2 || tiles / t <= 256)) {
+      if (ok(t) && tiles / t >= 256 && (t <= 2 || tiles / t == 256)) {
         T = t;
         break;
       }
     return {T, 1};
   }
-  // K ranges: each wave keeps at least two k-tiles
-  const int smax = std::max(1, std::min(GEMM_MAX_SPLITS, KT / (2 * TILE_WAVES)));
+  const int smax = std::max(1, std::min(GEMM_MAX_SPLITS, KT / (10 * TILE_WAVES)));
   int T = 1;
   for (int t : {4, 3, 2})
     if (ok(t) && (tiles / t) * smax >= 192) {
@@ -346,7 +351,8 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     if (splits) *splits = 1;
     return ADT_OK;
   }
-  ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0 && ldx % 8 == 0, ADT_E_SHAPE, "gemm: N=%d K=%d ldx=%d misaligned", N, K, ldx);
+  ADT_CHECK_ARG(N % 16 == 0 && K % 32 == 0 && ldx % 8 == 0 && (ldx == X_FRAG || ldx >= K), ADT_E_SHAPE,
+                "gemm: N=%d K=%d ldx=%d misaligned", N, K, ldx);
   switch (epi.mode) {
     case EPI_STORE: ADT_CHECK_ARG(epi.out && epi.ldo % 4 == 0, ADT_E_ARG, "gemm: store target"); break;
     case EPI_PART: ADT_CHECK_ARG(epi.part != nullptr, ADT_E_ARG, "gemm: partial-sum buffer"); break;
@@ -356,7 +362,10 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
                         epi.slot0 && epi.pos && epi.rope,
                     ADT_E_ARG, "gemm: QKV epilogue (Dh=%d, N=%d)", epi.Dh, N);
       break;
-    case EPI_SWIGLU: ADT_CHECK_ARG(epi.act != nullptr, ADT_E_ARG, "gemm: SwiGLU output"); break;
+    case EPI_SWIGLU:
+      ADT_CHECK_ARG(epi.act != nullptr && (epi.act_pk == 0 || (N / 2 % 32 == 0 && epi.act_pk * 16 >= M)), ADT_E_ARG,
+                    "gemm: SwiGLU output (layout %d)", epi.act_pk);
+      break;
     default: ADT_CHECK_ARG(false, ADT_E_ARG, "gemm: epilogue %d", epi.mode);
   }
   const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART);

@@ -11,11 +11,11 @@ namespace adt {
 
 constexpr int ROW_THREADS = 256;
 
-// h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) in dtype T.
+// h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) in dtype T (layout a_pk).
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                  int d, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ a, Branches br) {
+                                                                 T* __restrict__ a, Branches br, int a_pk) {
   __shared__ float red[16];
   const int m = blockIdx.x;
   const T* e = E + (int64_t)tok[m / br.nb + (m % br.nb) * br.tok_boff] * d;
@@ -26,17 +26,20 @@ __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __rest
     ss += v * v;
   }
   const float r = rsqrtf(block_sum(ss, red) / d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x) Elem<T>::store(a, (int64_t)m * d + i, h[(int64_t)m * d + i] * r);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    Elem<T>::store(a, act_index(m, i, d, a_pk), h[(int64_t)m * d + i] * r);
 }
 
 // Finish of a residual projection, one row per workgroup: the K-range sums of the row are
 // added in range order, added to (or, with assign, written as) the residual row, and the
-// row's RMSNorm is stored in the model dtype for the next projection.  Each thread keeps its
-// columns (4 at a time) between the two passes, so the norm reads nothing back.
-template <typename T, int VPT>
-__global__ __launch_bounds__(ROW_THREADS) void resid_norm_kernel(const float* __restrict__ part, int S, int M, int d,
-                                                                 int assign, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ out) {
+// row's RMSNorm is stored in the model dtype for the next projection (layout out_pk; out2, if
+// given, gets a second copy in layout out2_pk).  With at most 128 rows the launch is a few
+// dozen workgroups, so its time is load latency: every thread requests all S sums and the
+// residual of its columns (VPT groups of 4) before adding any, and keeps them for the norm.
+template <typename T, int VPT, int S>
+__global__ __launch_bounds__(1024) void resid_norm_kernel(const float* __restrict__ part, int M, int d, int assign,
+                                                          float eps, float* __restrict__ h, T* __restrict__ out,
+                                                          int out_pk, T* __restrict__ out2, int out2_pk) {
   __shared__ float red[16];
   const int m = blockIdx.x;
   const int64_t split = (int64_t)M * d;
@@ -46,42 +49,39 @@ __global__ __launch_bounds__(ROW_THREADS) void resid_norm_kernel(const float* __
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < VPT; ++j) {
-    const int i = (j * ROW_THREADS + threadIdx.x) * 4;
+    const int i = (j * blockDim.x + threadIdx.x) * 4;
     if (i >= d) continue;
-    float4 v = *reinterpret_cast<const float4*>(pr + i);
-    for (int sp = 1; sp < S; ++sp) {
-      const float4 w = *reinterpret_cast<const float4*>(pr + sp * split + i);
-      v = make_float4(v.x + w.x, v.y + w.y, v.z + w.z, v.w + w.w);
-    }
-    if (!assign) {
-      const float4 o = *reinterpret_cast<const float4*>(hr + i);
-      v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
-    }
+    float4 w[S];
+#pragma unroll
+    for (int sp = 0; sp < S; ++sp) w[sp] = *reinterpret_cast<const float4*>(pr + sp * split + i);
+    const float4 o = assign ? make_float4(0.f, 0.f, 0.f, 0.f) : *reinterpret_cast<const float4*>(hr + i);
+    float4 v = w[0];
+#pragma unroll
+    for (int sp = 1; sp < S; ++sp) v = make_float4(v.x + w[sp].x, v.y + w[sp].y, v.z + w[sp].z, v.w + w[sp].w);
+    if (!assign) v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
     *reinterpret_cast<float4*>(hr + i) = v;
     y[j] = v;
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float r = rsqrtf(block_sum(ss, red) / d + eps);
-  T* o = out + (int64_t)m * d;
 #pragma unroll
   for (int j = 0; j < VPT; ++j) {
-    const int i = (j * ROW_THREADS + threadIdx.x) * 4;
+    const int i = (j * blockDim.x + threadIdx.x) * 4;
     if (i >= d) continue;
-    Elem<T>::store(o, i, y[j].x * r);
-    Elem<T>::store(o, i + 1, y[j].y * r);
-    Elem<T>::store(o, i + 2, y[j].z * r);
-    Elem<T>::store(o, i + 3, y[j].w * r);
+    // four columns from a multiple of 4: contiguous in either layout
+    store4(out + act_index(m, i, d, out_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
+    if (out2) store4(out2 + act_index(m, i, d, out2_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
   }
 }
 
 // Draft-head input row m: [E[tok[m]] ; parent feature].  fsrc[m] >= 0 picks row fsrc of the
 // committed-feature buffer fa, fsrc[m] == -1 gives zeros, fsrc[m] <= -2 picks row -fsrc-2 of
-// the draft-feature buffer fb.
+// the draft-feature buffer fb.  x is [M][2d] in layout x_pk.
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                   const int32_t* __restrict__ fsrc, const T* __restrict__ fa,
                                                                   const T* __restrict__ fb, int d, T* __restrict__ x,
-                                                                  Branches br) {
+                                                                  Branches br, int x_pk) {
   const int m = blockIdx.x, node = m / br.nb, b = m % br.nb;
   const T* e = E + (int64_t)tok[node + b * br.tok_boff] * d;
   const int s = fsrc[node];
@@ -89,9 +89,10 @@ __global__ __launch_bounds__(ROW_THREADS) void draft_input_kernel(const T* __res
   const T* f = s >= 0 ? fa + ((int64_t)s * br.nb + b) * d
                       : (s <= -2 ? fb + ((int64_t)(-s - 2) * br.nb + b) * d : nullptr);
   for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    x[(int64_t)m * 2 * d + i] = e[i];
-    if (f) x[(int64_t)m * 2 * d + d + i] = f[i];
-    else Elem<T>::store(x, (int64_t)m * 2 * d + d + i, 0.f);
+    x[act_index(m, i, 2 * d, x_pk)] = e[i];
+    const int64_t xf = act_index(m, d + i, 2 * d, x_pk);
+    if (f) x[xf] = f[i];
+    else Elem<T>::store(x, xf, 0.f);
   }
 }
 
@@ -392,31 +393,57 @@ __global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int3
     __VA_ARGS__;                               \
   }
 
+// A fragment layout needs bf16, K % 32 == 0 and enough row blocks for M rows.
+static bool frag_ok(int pk, int M, int K, int dtype) {
+  return pk == 0 || (dtype == ADT_BF16 && K % 32 == 0 && pk * 16 >= M);
+}
+
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st, const Branches& br) {
+                             hipStream_t st, const Branches& br, int a_pk) {
   ADT_CHECK_ARG(a != nullptr && h != nullptr, ADT_E_ARG, "embed_norm: outputs");
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br));
+  ADT_CHECK_ARG(frag_ok(a_pk, M, d, dtype), ADT_E_SHAPE, "embed_norm: fragment layout of %d blocks for %d x %d", a_pk,
+                M, d);
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br, a_pk));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
 adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign, float eps, float* h, void* out,
-                             int dtype, hipStream_t st) {
-  ADT_CHECK_ARG(part && h && out && S >= 1 && M >= 1, ADT_E_ARG, "resid_norm: bad arguments");
-  ADT_CHECK_ARG(d % 4 == 0 && d <= 8 * 4 * ROW_THREADS, ADT_E_SHAPE, "resid_norm: d=%d (a multiple of 4, <= 8192)", d);
-  const int vpt = (d + 4 * ROW_THREADS - 1) / (4 * ROW_THREADS);
-#define ADT_RN(V) resid_norm_kernel<T, V><<<M, ROW_THREADS, 0, st>>>(part, S, M, d, assign, eps, h, (T*)out)
-  ADT_DISPATCH_T(dtype, if (vpt <= 1) ADT_RN(1); else if (vpt <= 2) ADT_RN(2); else if (vpt <= 4) ADT_RN(4);
-                 else ADT_RN(8));
+                             int out_pk, void* out2, int out2_pk, int dtype, hipStream_t st) {
+  ADT_CHECK_ARG(part && h && out && S >= 1 && S <= GEMM_MAX_SPLITS && M >= 1, ADT_E_ARG, "resid_norm: bad arguments");
+  ADT_CHECK_ARG(d % 4 == 0 && d <= 2 * 4 * 1024, ADT_E_SHAPE, "resid_norm: d=%d (a multiple of 4, <= 8192)", d);
+  ADT_CHECK_ARG(frag_ok(out_pk, M, d, dtype) && frag_ok(out2 ? out2_pk : 0, M, d, dtype), ADT_E_SHAPE,
+                "resid_norm: fragment layouts %d / %d for %d x %d", out_pk, out2_pk, M, d);
+  // one group of 4 columns per thread up to 4096 columns (1024 threads), two beyond
+  const int vpt = d > 4 * 1024 ? 2 : 1;
+  const int threads = std::max(WAVE, (d / 4 / vpt + WAVE - 1) / WAVE * WAVE);
+#define ADT_RN(V, SV)                                                                                          \
+  resid_norm_kernel<T, V, SV><<<M, threads, 0, st>>>(part, M, d, assign, eps, h, (T*)out, out_pk, (T*)out2, \
+                                                     out2_pk)
+#define ADT_RN_S(V)                  \
+  switch (S) {                       \
+    case 1: ADT_RN(V, 1); break;     \
+    case 2: ADT_RN(V, 2); break;     \
+    case 3: ADT_RN(V, 3); break;     \
+    case 4: ADT_RN(V, 4); break;     \
+    case 5: ADT_RN(V, 5); break;     \
+    case 6: ADT_RN(V, 6); break;     \
+    case 7: ADT_RN(V, 7); break;     \
+    default: ADT_RN(V, 8); break;    \
+  }
+  ADT_DISPATCH_T(dtype, if (vpt == 1) { ADT_RN_S(1) } else { ADT_RN_S(2) });
+#undef ADT_RN_S
 #undef ADT_RN
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
 
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
-                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br) {
+                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br, int x_pk) {
+  ADT_CHECK_ARG(frag_ok(x_pk, M, 2 * d, dtype), ADT_E_SHAPE, "draft_input: fragment layout of %d blocks for %d x %d",
+                x_pk, M, 2 * d);
   ADT_DISPATCH_T(dtype, draft_input_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, fsrc, (const T*)fa,
-                                                                          (const T*)fb, d, (T*)x, br));
+                                                                          (const T*)fb, d, (T*)x, br, x_pk));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -20,12 +20,18 @@ struct Branches {
 // row: b * ms_b + qr.  Separate sequences: (nq_max, 1, nq_max).  Guidance branches of one
 // tree interleaved node by node: (1, B, 0), one mask per node.  With row_off (device, [B])
 // the rows of sequence b start at row_off[b] instead (packed trees of different sizes), for
-// q, out and masks alike.
+// q, out and masks alike.  o_pk > 0 stores out (bf16) in the fragment layout of o_pk row
+// blocks (the input layout of the O projection), else row-major.
 struct AttnRows {
   int rs_b, rs_i, ms_b;
   const int32_t* row_off = nullptr;
+  int o_pk = 0;
   __device__ __forceinline__ int64_t q_row(int b, int qr) const {
     return (row_off ? (int64_t)row_off[b] : (int64_t)b * rs_b) + (int64_t)qr * rs_i;
+  }
+  // element (head h, dim d) of query qr's output row
+  __device__ __forceinline__ int64_t o_index(int b, int qr, int H, int DH, int h, int d) const {
+    return act_index(q_row(b, qr), h * DH + d, (int64_t)H * DH, o_pk);
   }
   __device__ __forceinline__ int64_t m_row(int b, int qr) const {
     return (row_off ? (int64_t)row_off[b] : (int64_t)b * ms_b) + qr;
@@ -69,8 +75,10 @@ struct GemmEpi {
   int Dh = 0;
   int nb = 1;              // guidance branches: row m is node m / nb of branch m % nb, whose
   int64_t cache_sb = 0;    // caches sit cache_sb elements further; q keeps row m
-  // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up
+  // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up, in
+  // the fragment layout of act_pk row blocks (0: row-major)
   uint16_t* act = nullptr;
+  int act_pk = 0;
 };
 struct RowsPlan {
   int T, S;       // 16-column tiles per workgroup, K ranges
@@ -78,7 +86,9 @@ struct RowsPlan {
 RowsPlan gemm_rows_plan(int M, int N, int K, bool partial);
 constexpr int GEMM_MAX_SPLITS = 8;
 // fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the kernel above with the
-// epilogue epi; *splits (if given) gets S.
+// epilogue epi; *splits (if given) gets S.  bf16 X is row-major with leading dimension ldx, or
+// with ldx == X_FRAG in the fragment layout of (M + 15) / 16 row blocks.
+constexpr int X_FRAG = 0;
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
                        const GemmEpi& epi, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr,
                        int* splits = nullptr);
@@ -91,18 +101,22 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
                           bool packed = false, float* part = nullptr, size_t part_elems = 0);
 size_t gemm_nt_part_elems(int M, int N, int K);
 // rows.hip
-// h = embedding rows, a = RMSNorm(h) in the model dtype.
+// h = embedding rows, a = RMSNorm(h) in the model dtype (bf16: fragment layout of a_pk row
+// blocks when a_pk > 0, else row-major).
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st, const Branches& br = Branches{});
+                             hipStream_t st, const Branches& br = Branches{}, int a_pk = 0);
 // The residual projection's finish, one row per workgroup: y = sum over s < S of part[s][m][:]
-// (in s order), h[m] = y (assign) or h[m] + y, then out[m] = RMSNorm(h[m]) in the model dtype
-// (the next projection's input, or the final features).
+// (in s order), h[m] = y (assign) or h[m] + y, then RMSNorm(h[m]) in the model dtype into out
+// (layout out_pk: the next projection's input, or the final features) and, if out2 is given,
+// into out2 as well (layout out2_pk).
 adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign, float eps, float* h, void* out,
-                             int dtype, hipStream_t st);
+                             int out_pk, void* out2, int out2_pk, int dtype, hipStream_t st);
 // x[m] = [E[token] ; parent feature]: fsrc >= 0 is a node of fa, -1 zeros, <= -2 node
-// (-2 - fsrc) of fb; fa and fb hold the nb branch rows of a node consecutively.
+// (-2 - fsrc) of fb; fa and fb hold the nb branch rows of a node consecutively.  x is [M][2d]
+// row-major, or in the fragment layout of x_pk row blocks.
 adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* fsrc, const void* fa, const void* fb,
-                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br = Branches{});
+                              int M, int d, void* x, int dtype, hipStream_t st, const Branches& br = Branches{},
+                              int x_pk = 0);
 adt_status launch_add_norm(const float* part, int splits, int M, int d, int assign, float eps, float* h, void* a,
                            int dtype, hipStream_t st);
 adt_status launch_rope_table(float2* tab, int positions, int Dh, double theta, hipStream_t st);
