@@ -374,7 +374,9 @@ typedef struct {
   const int32_t* tokens_host;   /* [host] committed ids */
   /* scratch of the last forward (last layer run): rotated queries [rows][d] dtype, attention
    * output [rows][d] dtype, normed activations [rows][d] dtype, residual stream [rows][d] fp32.
-   * In bf16 sessions att and act hold the fragment layout of the projections' inputs: with
+   * In bf16 sessions act holds the bf16 residual rows (each projection applies its RMSNorm
+   * itself) except after a forward's last layer, where it holds the final norm; att and act
+   * are then in the fragment layout of the projections' inputs: with
    * B = (rows + 15) / 16 row blocks, element (r, k) sits at
    * (((k / 32) * B + r / 16) * 64 + r % 16 + 16 * ((k % 32) / 8)) * 8 + k % 8. */
   void* q; void* att; void* act; float* resid;

@@ -54,6 +54,12 @@ class OracleModel:
         """Storage rounding of a bf16 model; identity for f32 models."""
         return bf16_round(x) if self.bf16 else x
 
+    def normed_input(self, h: np.ndarray) -> np.ndarray:
+        """Input of a layer's projections: the RMSNorm of the residual copy kept in storage
+        precision (a bf16 model stores the residual rows, not their norm, and the scale is
+        applied in full precision)."""
+        return rmsnorm(self.rnd(h))
+
     def embed_rows(self, tokens: Sequence[int]) -> np.ndarray:
         return self.w("embed")[np.asarray(tokens, dtype=np.int64)]
 
@@ -66,7 +72,7 @@ class OracleModel:
         m = self.m
         rows = h.shape[0]
         H, Dh = m.n_heads, m.head_dim
-        a = self.rnd(rmsnorm(h))
+        a = self.normed_input(h)
         q = (a @ self.w(pre + ".wq").T).reshape(rows, H, Dh)
         k = (a @ self.w(pre + ".wk").T).reshape(rows, H, Dh)
         v = (a @ self.w(pre + ".wv").T).reshape(rows, H, Dh)
@@ -81,7 +87,7 @@ class OracleModel:
 
     def mlp_block(self, pre: str, h: np.ndarray):
         """Second half: h + SwiGLU(RMSNorm(h)) W_down.  Returns (new residual, b, s)."""
-        b = self.rnd(rmsnorm(h))
+        b = self.normed_input(h)
         s = self.rnd(silu(b @ self.w(pre + ".wg").T) * (b @ self.w(pre + ".wu").T))
         return h + s @ self.w(pre + ".wd").T, b, s
 

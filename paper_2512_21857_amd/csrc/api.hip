@@ -875,6 +875,34 @@ static adt_status resid_finish(adt_session_s* s, int splits, int rows, int assig
 // of this many 16-row blocks; fp32 forwards keep them row-major.
 static int act_blocks(const adt_session_s* s, int rows) { return s->dt == ADT_BF16 ? (rows + 15) / 16 : 0; }
 
+// A bf16 residual projection (O, down, draft FC) of the rows X (fragment layout, K columns)
+// into the residual h (assign: h = Y): with one K range the product's epilogue adds it and
+// leaves bf16(h) in act for the next projection, which normalises its own input; with
+// several, the K-range sums and the element-wise finish.
+static adt_status resid_proj(adt_session_s* s, const void* X, const void* W, int rows, int K, int assign,
+                             hipStream_t st) {
+  const int dm = s->dm, pk = act_blocks(s, rows);
+  if (gemm_rows_plan(rows, dm, K, true).S == 1) {
+    GemmEpi e;
+    e.mode = EPI_RESID;
+    e.resid = s->h;
+    e.assign = assign;
+    e.act = (uint16_t*)s->act;
+    e.act_pk = pk;
+    return gemm_p(X, X_FRAG, W, rows, dm, K, s->dt, s->part, st, e);
+  }
+  GemmEpi e;
+  e.mode = EPI_PART;
+  e.part = s->part;
+  e.part_elems = s->part_elems;
+  int sp = 1;
+  TRY(gemm_p(X, X_FRAG, W, rows, dm, K, s->dt, s->part, st, e, &sp));
+  const int ev = prof_begin(st);
+  TRY(launch_resid_add(s->part, sp, rows, dm, assign, s->h, s->act, pk, st));
+  prof_end(ev, ADT_PROF_ROWS, (double)sp * rows * dm * 4.0 + rows * dm * ((assign ? 4.0 : 8.0) + 2.0), 0.0, st);
+  return ADT_OK;
+}
+
 // Decoder layers over the nb * M rows of M tree nodes (branches interleaved node by node).
 // The final norm goes to final_out (row-major; bf16: act if null) and, with act_too (bf16),
 // also to act.
@@ -904,10 +932,10 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
     return ADT_OK;
   };
   if (dt == ADT_BF16) {
-    // Per layer: QKV (RoPE + cache append) from the normalised rows in act, attention, O (K-range
-    // sums) and its finish (residual add, the MLP's RMSNorm into act), gate/up (SwiGLU), down
-    // and its finish (residual add, the next layer's RMSNorm into act, or the final norm into
-    // final_out after the last layer).
+    // Per layer: QKV (RoPE + cache append) from the bf16 residual rows in act, normalised inside
+    // the product; attention; O added to the residual (act = its new bf16 copy); gate/up
+    // (the MLP's norm inside, SwiGLU); down added likewise, or after the last layer with the
+    // final norm into final_out.
     GemmEpi pe;
     pe.mode = EPI_PART;
     pe.part = s->part;
@@ -928,19 +956,24 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       qkv.Dh = Dh;
       qkv.nb = nb;
       qkv.cache_sb = cache_sb;
+      qkv.norm_eps = eps;
       TRY(gemm_p(s->act, X_FRAG, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
-      int sp = 1;
-      TRY(gemm_p(s->att, X_FRAG, m->o[l], rows, dm, dm, dt, s->part, st, pe, &sp));
-      TRY(resid_finish(s, sp, rows, 0, s->act, pk, nullptr, 0, st));
+      TRY(resid_proj(s, s->att, m->o[l], rows, dm, 0, st));
       TRY(capt_snap(s, 2 * (l - l0) + 1, st));
       GemmEpi sw;
       sw.mode = EPI_SWIGLU;
       sw.act = (uint16_t*)s->sw;
       sw.act_pk = pk;
+      sw.norm_eps = eps;
       TRY(gemm_p(s->act, X_FRAG, m->gu[l], rows, 2 * F, dm, dt, s->part, st, sw));
+      if (l + 1 < l1) {
+        TRY(resid_proj(s, s->sw, m->down[l], rows, F, 0, st));
+        continue;
+      }
+      int sp = 1;
       TRY(gemm_p(s->sw, X_FRAG, m->down[l], rows, dm, F, dt, s->part, st, pe, &sp));
-      if (l + 1 == l1 && final_out)
+      if (final_out)
         TRY(resid_finish(s, sp, rows, 0, final_out, 0, act_too ? s->act : nullptr, pk, st));
       else
         TRY(resid_finish(s, sp, rows, 0, s->act, pk, nullptr, 0, st));
@@ -998,8 +1031,9 @@ static adt_status target_forward(adt_session_s* s, const int32_t* tok, int M, co
   auto body = [&](hipStream_t cs) -> adt_status {
     TRY(capt_begin(s, false, M, L_pre, slot0, n_tail, tok, pos, mask, cs));
     const int pk = act_blocks(s, s->nb * M);
+    // bf16: act takes the raw embedding rows (the first projection normalises them)
     TRY(launch_embed_norm(s->m->d.embed, tok, s->nb * M, s->dm, s->m->d.norm_eps, s->h, s->act, s->dt, cs,
-                          Branches{s->nb, tok_boff, 0}, pk));
+                          Branches{s->nb, tok_boff, 0}, pk, pk > 0));
     // logits of every row read the final norm from act in the fragment layout
     const bool all = pk && lm_row0 == 0 && lm_rows == M;
     TRY(run_layers(s, false, M, pos, slot0, L_pre, n_tail, mask, s->feat, all, cs));
@@ -1033,13 +1067,7 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
                              (char*)s->capt.xin + s->capt_log[s->capt_cur].xin_off, dt, cs,
                              Branches{s->nb, tok_boff, 0}, 0));
     if (dt == ADT_BF16) {
-      GemmEpi e;
-      e.mode = EPI_PART;
-      e.part = s->part;
-      e.part_elems = s->part_elems;
-      int sp = 1;
-      TRY(gemm_p(s->xin, X_FRAG, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs, e, &sp));
-      TRY(resid_finish(s, sp, rows, 1, s->act, pk, nullptr, 0, cs));
+      TRY(resid_proj(s, s->xin, s->m->d.draft_fc, rows, 2 * dm, 1, cs));
     } else {
       TRY(gemm_p(s->xin, 2 * dm, s->m->d.draft_fc, rows, dm, 2 * dm, dt, s->part, cs));
       TRY(launch_add_norm(s->part, 1, rows, dm, 1, s->m->d.norm_eps, s->h, s->act, dt, cs));

@@ -126,6 +126,17 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
       *reinterpret_cast<u16x4*>(dst + j) = u16x4{f2bf(a[0]), f2bf(a[1]), f2bf(a[2]), f2bf(a[3])};
       *reinterpret_cast<u16x4*>(dst + j + half) = u16x4{f2bf(b[0]), f2bf(b[1]), f2bf(b[2]), f2bf(b[3])};
     }
+  } else if (e.mode == EPI_RESID) {
+    if (live) {
+      float* hp = e.resid + (int64_t)row * N + c;
+      f32x4 h = y;
+      if (!e.assign) {
+        const f32x4 o = *reinterpret_cast<const f32x4*>(hp);
+        h = f32x4{o[0] + y[0], o[1] + y[1], o[2] + y[2], o[3] + y[3]};
+      }
+      *reinterpret_cast<f32x4*>(hp) = h;
+      store4(e.act + act_index(row, c, N, e.act_pk), h[0], h[1], h[2], h[3]);
+    }
   } else if (e.mode == EPI_SWIGLU) {
     const f32x4 u = shfl_xor4(y, 32);
     if (live && g < 2) {
@@ -137,6 +148,16 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
   }
 }
 
+// Sum of squares of eight bf16 values added to s (products exact in fp32).
+__device__ __forceinline__ float sumsq8(bf16x8 v, float s) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 p{v[2 * i], v[2 * i + 1]};
+    s = __builtin_amdgcn_fdot2_f32_bf16(p, p, s, false);
+  }
+  return s;
+}
+
 // MT = 16-row blocks of M, T = 16-column tiles per workgroup, KC = k-tiles per load round.
 // Workgroup b takes column block b / S and K range b % S; wave w takes the w-th eighth of the
 // range.  Rounds are double-buffered: round r + 1's fragments are requested before round r's
@@ -144,7 +165,10 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
 // offset that depends on the workgroup (wrapping around its chunk), so the waves of different
 // CUs do not read the same input lines at the same time; the sum order stays fixed per tile.
 // Loads past the wave's range are clamped to its last k-tile and their products discarded.
-template <int MT, int T, int KC>
+// NORM: the waves also sum the squares of the input fragments they multiply (lane (lq, g)
+// holds row m * 16 + lq), the sums meet in LDS in wave order, and each finished row is scaled
+// by its RMSNorm factor before the epilogue.
+template <int MT, int T, int KC, bool NORM>
 __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t* __restrict__ X, int ldx,
                                                                  const uint16_t* __restrict__ Wp, int M, int N, int K,
                                                                  int S, int stagger, GemmEpi epi) {
@@ -192,6 +216,9 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
     }
   };
   f32x4 acc[T][MT];
+  float ss[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) ss[m] = 0.f;
 #pragma unroll
   for (int t = 0; t < T; ++t)
 #pragma unroll
@@ -200,11 +227,14 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
     const int c0 = kmap(c);
 #pragma unroll
     for (int j = 0; j < KC; ++j)
-      if (c0 + j < kt1)
+      if (c0 + j < kt1) {
 #pragma unroll
-        for (int m = 0; m < MT; ++m)
+        for (int m = 0; m < MT; ++m) {
 #pragma unroll
           for (int t = 0; t < T; ++t) acc[t][m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[j][t], x[j][m], acc[t][m], 0, 0, 0);
+          if (NORM) ss[m] = sumsq8(x[j][m], ss[m]);
+        }
+      }
   };
   if (nk > 0) {
     load(wa, xa, kt0);
@@ -217,6 +247,18 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
       mma(wb, xb, c);
       c += KC;
       if (c >= kt1) break;
+    }
+  }
+  // NORM: the row sums of squares of each wave (its four lane groups first), read back per
+  // row by the finishing waves after the first barrier below
+  __shared__ float red_ss[NORM ? TILE_WAVES : 1][NORM ? MT : 1][16];
+  if (NORM) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float v = ss[m];
+      v += __shfl_xor(v, 16, WAVE);
+      v += __shfl_xor(v, 32, WAVE);
+      if (g == 0) red_ss[wave][m][lq] = v;
     }
   }
   // Sum the waves' partial blocks in wave order; wave i then finishes block q0 + i.
@@ -235,6 +277,13 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
       }
       const int q = q0 + wave;
       const int row = (q % MT) * 16 + lq, nt = cb * T + q / MT;
+      if (NORM) {
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < TILE_WAVES; ++w) t += red_ss[w][q % MT][lq];
+        const float r = rsqrtf(t / K + epi.norm_eps);
+        y = f32x4{y[0] * r, y[1] * r, y[2] * r, y[3] * r};
+      }
       if (epi.mode == EPI_PART) {
         if (row < M) *reinterpret_cast<f32x4*>(epi.part + ((int64_t)sp * M + row) * N + nt * 16 + 4 * g) = y;
       } else {
@@ -308,26 +357,27 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
 }
 
 // Tiles per workgroup T and K ranges S for M rows of an N x K product, measured with inputs in
-// the fragment layout on the 7B layer shapes (K 4096 / 8192 / 11008, N 4096 - 65536) at 4,
-// 17 and 61 rows.  One K range: T as wide as the registers allow while the launch keeps
-// >= 256 workgroups, and wider than 2 only where that is exactly one workgroup per CU (61
-// rows: QKV 768 tiles T = 3, 22 us against 25 at T = 4; gate/up 1376 tiles T = 2, 49
-// against 58; LM head 4096 tiles T = 2, 135 against 144).  partial: the caller adds the
-// K-range sums (residual projections), so S may exceed 1 as long as every wave keeps about
-// ten k-tiles (a shorter range never reaches its steady state): O (K 4096) T = 1 S = 1
-// 9.1 us against 11.5 at T = 4 S = 4, down (K 11008) T = 4 S = 4 21 against 28 at S = 1.
+// the fragment layout on the 7B layer shapes (K 4096 / 8192 / 11008, N 4096 - 65536) at 8,
+// 24, 40 and 61 rows (a round of KC k-tiles per wave: 1 for T >= 3, else 2, or 3 at <= 16
+// rows; see launch_gemm).  One K range: T as wide as the registers allow while the launch
+// keeps >= 256 workgroups; wider than 2 at <= 32 rows only where that is exactly one
+// workgroup per CU or the launch still has >= 1024 (61 rows: QKV T = 3 21 us; gate/up T = 4
+// 48 against 50 at T = 2; LM head T = 4 113 against 139; 24 rows: gate/up T = 2 39 against
+// 44, LM head T = 4 102 against 109).  partial (the caller adds K-range sums): one tile and
+// the whole K per workgroup where that already gives >= 192 workgroups (O 9.1 us and the
+// draft FC 15.5 at 61 rows), except a long K at > 32 rows, which takes T = 4 with about ten
+// k-tiles per wave per range (down at 61 rows: T = 4 S = 4 20.5 us against 28 at S = 1).
 RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
   const int mt = (M + 15) / 16, tiles = N / 16, KT = K / 32;
   const int tmax = mt <= 4 ? 4 : 2;
   auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
+  if (partial && tiles >= 192 && (mt <= 2 || K <= 8192)) return {1, 1};
   if (!partial || (mt == 1 && tiles >= 192)) {
-    int T = 1;
-    for (int t : {4, 3, 2})
-      if (ok(t) && tiles / t >= 256 && (t <= 2 || tiles / t == 256)) {
-        T = t;
-        break;
-      }
-    return {T, 1};
+    for (int t : {4, 3, 2}) {
+      if (!ok(t) || tiles / t < 256) continue;
+      if (t <= 2 || tiles / t == 256 || mt >= 3 || (mt == 2 && tiles / t >= 1024)) return {t, 1};
+    }
+    return {1, 1};
   }
   const int smax = std::max(1, std::min(GEMM_MAX_SPLITS, KT / (10 * TILE_WAVES)));
   int T = 1;
@@ -366,9 +416,17 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
       ADT_CHECK_ARG(epi.act != nullptr && (epi.act_pk == 0 || (N / 2 % 32 == 0 && epi.act_pk * 16 >= M)), ADT_E_ARG,
                     "gemm: SwiGLU output (layout %d)", epi.act_pk);
       break;
+    case EPI_RESID:
+      ADT_CHECK_ARG(epi.resid && epi.act && (epi.act_pk == 0 || (N % 32 == 0 && epi.act_pk * 16 >= M)), ADT_E_ARG,
+                    "gemm: residual epilogue (layout %d)", epi.act_pk);
+      break;
     default: ADT_CHECK_ARG(false, ADT_E_ARG, "gemm: epilogue %d", epi.mode);
   }
-  const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART);
+  ADT_CHECK_ARG(epi.norm_eps == 0.f || (epi.norm_eps > 0.f && epi.mode != EPI_PART && epi.mode != EPI_RESID),
+                ADT_E_ARG, "gemm: the input norm needs one K range");
+  // the residual epilogue takes the residual projections' plan, which must keep one K range
+  const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART || epi.mode == EPI_RESID);
+  ADT_CHECK_ARG(epi.mode != EPI_RESID || p.S == 1, ADT_E_ARG, "gemm: residual epilogue with %d K ranges", p.S);
   ADT_CHECK_ARG(epi.mode != EPI_PART || (size_t)p.S * M * N <= epi.part_elems, ADT_E_CAPACITY,
                 "gemm: %d K-range sums of %d x %d exceed the partial buffer", p.S, M, N);
   const int mt = (M + 15) / 16;
@@ -376,13 +434,20 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
   const dim3 grid(N / 16 / p.T * p.S), block(TILE_THREADS);
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)Wp;
-#define ADT_GR(MTV, TV, KCV)                                                                                  \
-  hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, p.S, \
-                        stagger, epi)
+#define ADT_GR(MTV, TV, KCV)                                                                                   \
+  if (epi.norm_eps > 0.f) {                                                                                        \
+    hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV, true>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, \
+                          p.S, stagger, epi);                                                                      \
+  } else {                                                                                                         \
+    hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV, false>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N,   \
+                          K, p.S, stagger, epi);                                                                   \
+  }
+  // k-tiles per round: one with three or four tiles (their fragments already keep enough in
+  // flight), else two, or three for one row block
 #define ADT_GR_T4(MTV, KCV)              \
   switch (p.T) {                         \
-    case 4: ADT_GR(MTV, 4, KCV); break;  \
-    case 3: ADT_GR(MTV, 3, KCV); break;  \
+    case 4: ADT_GR(MTV, 4, 1); break;    \
+    case 3: ADT_GR(MTV, 3, 1); break;    \
     case 2: ADT_GR(MTV, 2, KCV); break;  \
     default: ADT_GR(MTV, 1, KCV); break; \
   }

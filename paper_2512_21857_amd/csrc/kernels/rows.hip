@@ -11,11 +11,12 @@ namespace adt {
 
 constexpr int ROW_THREADS = 256;
 
-// h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) in dtype T (layout a_pk).
+// h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) (raw: h[m] itself) in dtype T
+// (layout a_pk).
 template <typename T>
 __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __restrict__ E, const int32_t* __restrict__ tok,
                                                                  int d, float eps, float* __restrict__ h,
-                                                                 T* __restrict__ a, Branches br, int a_pk) {
+                                                                 T* __restrict__ a, Branches br, int a_pk, int raw) {
   __shared__ float red[16];
   const int m = blockIdx.x;
   const T* e = E + (int64_t)tok[m / br.nb + (m % br.nb) * br.tok_boff] * d;
@@ -25,7 +26,7 @@ __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __rest
     h[(int64_t)m * d + i] = v;
     ss += v * v;
   }
-  const float r = rsqrtf(block_sum(ss, red) / d + eps);
+  const float r = raw ? 1.f : rsqrtf(block_sum(ss, red) / d + eps);
   for (int i = threadIdx.x; i < d; i += blockDim.x)
     Elem<T>::store(a, act_index(m, i, d, a_pk), h[(int64_t)m * d + i] * r);
 }
@@ -72,6 +73,28 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(const float* __restric
     store4(out + act_index(m, i, d, out_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
     if (out2) store4(out2 + act_index(m, i, d, out2_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
   }
+}
+
+// The finish without the norm: element-wise over the M x d residual, four columns per thread;
+// the S sums are requested before any is added, and added in range order.
+template <int S>
+__global__ __launch_bounds__(ROW_THREADS) void resid_add_kernel(const float* __restrict__ part, int M, int d, int assign,
+                                                                float* __restrict__ h, uint16_t* __restrict__ out,
+                                                                int out_pk) {
+  const int64_t i4 = (int64_t)blockIdx.x * ROW_THREADS + threadIdx.x, n4 = (int64_t)M * d / 4;
+  if (i4 >= n4) return;
+  const int64_t i = i4 * 4, split = (int64_t)M * d;
+  float4 w[S];
+#pragma unroll
+  for (int sp = 0; sp < S; ++sp) w[sp] = *reinterpret_cast<const float4*>(part + sp * split + i);
+  const float4 o = assign ? make_float4(0.f, 0.f, 0.f, 0.f) : *reinterpret_cast<const float4*>(h + i);
+  float4 v = w[0];
+#pragma unroll
+  for (int sp = 1; sp < S; ++sp) v = make_float4(v.x + w[sp].x, v.y + w[sp].y, v.z + w[sp].z, v.w + w[sp].w);
+  if (!assign) v = make_float4(o.x + v.x, o.y + v.y, o.z + v.z, o.w + v.w);
+  *reinterpret_cast<float4*>(h + i) = v;
+  const int m = (int)(i / d), c = (int)(i % d);
+  store4(out + act_index(m, c, d, out_pk), v.x, v.y, v.z, v.w);
 }
 
 // Draft-head input row m: [E[tok[m]] ; parent feature].  fsrc[m] >= 0 picks row fsrc of the
@@ -399,11 +422,12 @@ static bool frag_ok(int pk, int M, int K, int dtype) {
 }
 
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st, const Branches& br, int a_pk) {
+                             hipStream_t st, const Branches& br, int a_pk, bool raw) {
   ADT_CHECK_ARG(a != nullptr && h != nullptr, ADT_E_ARG, "embed_norm: outputs");
   ADT_CHECK_ARG(frag_ok(a_pk, M, d, dtype), ADT_E_SHAPE, "embed_norm: fragment layout of %d blocks for %d x %d", a_pk,
                 M, d);
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br, a_pk));
+  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br, a_pk,
+                                                                         raw ? 1 : 0));
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -434,6 +458,29 @@ adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign,
   ADT_DISPATCH_T(dtype, if (vpt == 1) { ADT_RN_S(1) } else { ADT_RN_S(2) });
 #undef ADT_RN_S
 #undef ADT_RN
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+
+adt_status launch_resid_add(const float* part, int S, int M, int d, int assign, float* h, void* out, int out_pk,
+                            hipStream_t st) {
+  ADT_CHECK_ARG(part && h && out && S >= 1 && S <= GEMM_MAX_SPLITS && M >= 1, ADT_E_ARG, "resid_add: bad arguments");
+  ADT_CHECK_ARG(d % 4 == 0 && frag_ok(out_pk, M, d, ADT_BF16), ADT_E_SHAPE, "resid_add: %d x %d (layout %d)", M, d,
+                out_pk);
+  const int blocks = (int)(((int64_t)M * d / 4 + ROW_THREADS - 1) / ROW_THREADS);
+#define ADT_RA(SV) \
+  resid_add_kernel<SV><<<blocks, ROW_THREADS, 0, st>>>(part, M, d, assign, h, (uint16_t*)out, out_pk)
+  switch (S) {
+    case 1: ADT_RA(1); break;
+    case 2: ADT_RA(2); break;
+    case 3: ADT_RA(3); break;
+    case 4: ADT_RA(4); break;
+    case 5: ADT_RA(5); break;
+    case 6: ADT_RA(6); break;
+    case 7: ADT_RA(7); break;
+    default: ADT_RA(8); break;
+  }
+#undef ADT_RA
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -54,7 +54,7 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
 // and their partial tiles are summed in LDS in wave order.  With S = 1 the finished tile
 // runs the epilogue; EPI_PART stores the S range sums instead, for resid_norm to add in
 // range order.  T and S come from gemm_rows_plan.
-enum : int { EPI_STORE = 1, EPI_PART = 2, EPI_QKV = 3, EPI_SWIGLU = 4 };
+enum : int { EPI_STORE = 1, EPI_PART = 2, EPI_QKV = 3, EPI_SWIGLU = 4, EPI_RESID = 5 };
 struct GemmEpi {
   int mode = EPI_STORE;
   // EPI_STORE: out[m][n] (fp32, leading dimension ldo)
@@ -79,6 +79,14 @@ struct GemmEpi {
   // the fragment layout of act_pk row blocks (0: row-major)
   uint16_t* act = nullptr;
   int act_pk = 0;
+  // EPI_RESID (one K range): resid[m][n] (fp32, [M][N]) += Y (assign: = Y), then act[m][n] =
+  // the new residual in bf16, layout act_pk
+  float* resid = nullptr;
+  int assign = 0;
+  // norm_eps > 0 (not with EPI_PART or EPI_RESID): the input rows are un-normalised and every
+  // output row is scaled by 1 / sqrt(mean of its input row's squares + norm_eps), the RMSNorm
+  // (unit gain) of the bf16 rows the kernel reads
+  float norm_eps = 0.f;
 };
 struct RowsPlan {
   int T, S;       // 16-column tiles per workgroup, K ranges
@@ -101,16 +109,21 @@ adt_status launch_gemm_nt(const void* X, int64_t ldx, const void* W, int64_t ldw
                           bool packed = false, float* part = nullptr, size_t part_elems = 0);
 size_t gemm_nt_part_elems(int M, int N, int K);
 // rows.hip
-// h = embedding rows, a = RMSNorm(h) in the model dtype (bf16: fragment layout of a_pk row
-// blocks when a_pk > 0, else row-major).
+// h = embedding rows, a = RMSNorm(h) (raw: h itself) in the model dtype (bf16: fragment
+// layout of a_pk row blocks when a_pk > 0, else row-major).
 adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, float eps, float* h, void* a, int dtype,
-                             hipStream_t st, const Branches& br = Branches{}, int a_pk = 0);
+                             hipStream_t st, const Branches& br = Branches{}, int a_pk = 0, bool raw = false);
 // The residual projection's finish, one row per workgroup: y = sum over s < S of part[s][m][:]
 // (in s order), h[m] = y (assign) or h[m] + y, then RMSNorm(h[m]) in the model dtype into out
 // (layout out_pk: the next projection's input, or the final features) and, if out2 is given,
 // into out2 as well (layout out2_pk).
 adt_status launch_resid_norm(const float* part, int S, int M, int d, int assign, float eps, float* h, void* out,
                              int out_pk, void* out2, int out2_pk, int dtype, hipStream_t st);
+// The same finish without the norm (the next projection normalises its own input rows):
+// h[m] = y (assign) or h[m] + y, out[m] = h[m] in bf16, fragment layout out_pk.  Elementwise,
+// four columns per thread.
+adt_status launch_resid_add(const float* part, int S, int M, int d, int assign, float* h, void* out, int out_pk,
+                            hipStream_t st);
 // x[m] = [E[token] ; parent feature]: fsrc >= 0 is a node of fa, -1 zeros, <= -2 node
 // (-2 - fsrc) of fb; fa and fb hold the nb branch rows of a node consecutively.  x is [M][2d]
 // row-major, or in the fragment layout of x_pk row blocks.
