@@ -244,7 +244,8 @@ extern "C" adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, in
 }
 
 extern "C" size_t adt_accept_workspace_size(int32_t V) {
-  return align_up(accept_ws_bytes(V), 256) + (size_t)R * 16 * 8 + (size_t)R * 4 + 1024;
+  return align_up(accept_ws_bytes(V), 256) + (size_t)R * 16 * 8 + (size_t)R * 4 + align_up(row_topk_ws_bytes(R, 1), 256) +
+         1024;
 }
 
 static adt_status accept_impl(const float* logits, int64_t ld, int V, const int32_t* parent, const int32_t* token,
@@ -257,8 +258,10 @@ static adt_status accept_impl(const float* logits, int64_t ld, int V, const int3
   float* top_val = b.take<float>((size_t)R * 16);
   float* lse = b.take<float>(R);
   void* rest = b.take<char>(accept_ws_bytes(V));
+  const size_t tk_bytes = row_topk_ws_bytes(R, 1);
+  void* tk = b.take<char>(tk_bytes);
   if (cfg.mode == ADT_ACCEPT_GREEDY) {
-    adt_status e = launch_row_topk(logits, ld, V, allowed, n_max, 1, 1, top_id, top_val, lse, st);
+    adt_status e = launch_row_topk(logits, ld, V, allowed, n_max, 1, 1, top_id, top_val, lse, tk, tk_bytes, st);
     if (e) return e;
     return launch_accept_greedy(top_id, 1, parent, token, n_nodes, n_max, path, n_acc, bonus, st);
   }
@@ -546,6 +549,8 @@ struct adt_session_s {
   float *top_val, *lse;
   void* attn_ws;
   size_t attn_ws_bytes;
+  void* topk_ws;          // per-chunk candidates of the expansions' top-k
+  size_t topk_ws_bytes;
   void* acc_ws;
   size_t acc_ws_bytes;
   uint64_t* samp_w = nullptr;   // stochastic children: [KR][V] q weights of a level's rows
@@ -667,6 +672,8 @@ static size_t session_layout(adt_session_s* s, char* base) {
   s->attn_ws = b.take<char>(std::max<size_t>(s->attn_ws_bytes, 256));
   s->acc_ws_bytes = adt_accept_workspace_size(s->V);
   s->acc_ws = b.take<char>(s->acc_ws_bytes);
+  s->topk_ws_bytes = row_topk_ws_bytes(R, 16);
+  s->topk_ws = b.take<char>(s->topk_ws_bytes);
   if (s->d.accept.mode == ADT_ACCEPT_MSS) s->samp_w = b.take<uint64_t>((size_t)s->KR * s->V);
   return align_up(b.off, 256);
 }
@@ -1265,7 +1272,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     return expand_sampled(s, d_hat, k_hat, n_budget, cu, table, n_nodes_out, st);
   }
   // layer 1: the root's top-k children
-  TRY(launch_row_topk(s->dlogits, V, V, s->allowed_lvl, 1, k_hat, 16, s->top_id, s->top_val, s->lse, st));
+  TRY(launch_row_topk(s->dlogits, V, V, s->allowed_lvl, 1, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
+                      s->topk_ws_bytes, st));
   int cnt = std::min(k_hat, hi - lo);
   TRY(launch_expand_level(s->pool, nullptr, 1, cnt, 0, 1, k_hat, s->top_id, s->top_val, s->lse, 16, d_hat > 1 ? 1 : 0,
                           L, 0, cu - 1, s->C0, 1, s->nx[0], st));
@@ -1284,7 +1292,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
     }
     cell_range(s, L + lvl - P, lo, hi);
     TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
-    TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, st));
+    TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
+                        s->topk_ws_bytes, st));
     cnt = std::min(k_hat, hi - lo);
     TRY(launch_expand_level(s->pool, s->nx[cur].frontier, nf, cnt, pool_n, lvl, k_hat, s->top_id, s->top_val, s->lse,
                             16, lvl < d_hat ? 1 : 0, L, drow + nf, cu - 1, s->C0, 1 + (lvl - 1) * c.k_hi,

@@ -453,16 +453,22 @@ __global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel
 
   // Slot s (16 bytes) of a block holds row s / CH, chunk (s % CH) ^ swizzle(row); thread t
   // fills slots r * 512 + t.  Keys past the live range repeat the last key (masked below).
-  // P register stages: block blk + P is requested while block blk is computed
+  // P register stages: block blk + P is requested while block blk is computed.  Requests
+  // are never skipped (a block past the range reads the first 16 bytes of the head instead,
+  // one cache line per wave), so the count of loads in flight is the same on every path and
+  // a stage waits only for its own loads.
   u16x8 kr[P][LOADS], vr[P][LOADS];
   auto fetch_block = [&](int u, int blk) {
     const int last = max(total - 1, 0);
+    const bool live = blk < nblk;
 #pragma unroll
     for (int r = 0; r < LOADS; ++r) {
       const int slot = r * NW * WAVE + threadIdx.x, row = slot / CH, phys = slot % CH;
       const int64_t key = min(blk * BLK_KT + row, last);
-      kr[u][r] = *reinterpret_cast<const u16x8*>(kbase + key * DH + (phys ^ blk_swz_k<DH>(row)) * 8);
-      vr[u][r] = *reinterpret_cast<const u16x8*>(vbase + key * DH + (phys ^ blk_swz_v<DH>(row)) * 8);
+      const int64_t ko = live ? key * DH + (phys ^ blk_swz_k<DH>(row)) * 8 : 0;
+      const int64_t vo = live ? key * DH + (phys ^ blk_swz_v<DH>(row)) * 8 : 0;
+      kr[u][r] = *reinterpret_cast<const u16x8*>(kbase + ko);
+      vr[u][r] = *reinterpret_cast<const u16x8*>(vbase + vo);
     }
   };
   auto store_block = [&](int u, int buf) {
@@ -561,20 +567,23 @@ __global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel
       }
     }
   };
+  // (the stages are issued in order: the scheduler may not interleave them, or the first
+  // stage stored could be the last to arrive)
 #pragma unroll
-  for (int u = 0; u < P; ++u)
-    if (blk0 + u < nblk) fetch_block(u, blk0 + u);
+  for (int u = 0; u < P; ++u) {
+    fetch_block(u, blk0 + u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   for (int base = blk0; base < nblk; base += P) {
 #pragma unroll
     for (int u = 0; u < P; ++u) {
       const int blk = base + u;
-      if (blk < nblk) {
-        // the buffer written here was last read two blocks ago, before the previous barrier
-        store_block(u, blk & 1);
-        __syncthreads();
-        if (blk + P < nblk) fetch_block(u, blk + P);
-        if (active) compute(blk);
-      }
+      // the buffer written here was last read two blocks ago, before the previous barrier
+      // (past the range it is written and never read)
+      store_block(u, blk & 1);
+      __syncthreads();
+      fetch_block(u, blk + P);
+      if (active && blk < nblk) compute(blk);
     }
   }
 

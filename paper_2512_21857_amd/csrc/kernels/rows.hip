@@ -31,6 +31,51 @@ __global__ __launch_bounds__(ROW_THREADS) void embed_norm_kernel(const T* __rest
     Elem<T>::store(a, act_index(m, i, d, a_pk), h[(int64_t)m * d + i] * r);
 }
 
+// The bf16 form of embed_norm: 8 columns (16 bytes) per thread and step, VPT steps, every
+// load issued before the first store.
+template <int VPT>
+__global__ __launch_bounds__(ROW_THREADS) void embed_norm_bf16_kernel(const uint16_t* __restrict__ E,
+                                                                      const int32_t* __restrict__ tok, int d, float eps,
+                                                                      float* __restrict__ h, uint16_t* __restrict__ a,
+                                                                      Branches br, int a_pk, int raw) {
+  __shared__ float red[16];
+  const int m = blockIdx.x;
+  const uint16_t* e = E + (int64_t)tok[m / br.nb + (m % br.nb) * br.tok_boff] * d;
+  u16x8 v[VPT];
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int c = (j * ROW_THREADS + threadIdx.x) * 8;
+    if (c < d) v[j] = *reinterpret_cast<const u16x8*>(e + c);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int c = (j * ROW_THREADS + threadIdx.x) * 8;
+    if (c >= d) continue;
+    float f[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      f[t] = bf2f(v[j][t]);
+      ss += f[t] * f[t];
+    }
+    float* hp = h + (int64_t)m * d + c;
+    *reinterpret_cast<float4*>(hp) = make_float4(f[0], f[1], f[2], f[3]);
+    *reinterpret_cast<float4*>(hp + 4) = make_float4(f[4], f[5], f[6], f[7]);
+    if (raw) *reinterpret_cast<u16x8*>(a + act_index(m, c, d, a_pk)) = v[j];
+  }
+  if (raw) return;
+  const float r = rsqrtf(block_sum(ss, red) / d + eps);
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int c = (j * ROW_THREADS + threadIdx.x) * 8;
+    if (c >= d) continue;
+    u16x8 o;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = f2bf(bf2f(v[j][t]) * r);
+    *reinterpret_cast<u16x8*>(a + act_index(m, c, d, a_pk)) = o;
+  }
+}
+
 // Finish of a residual projection, one row per workgroup: the K-range sums of the row are
 // added in range order, added to (or, with assign, written as) the residual row, and the
 // row's RMSNorm is stored in the model dtype for the next projection (layout out_pk; out2, if
@@ -72,6 +117,58 @@ __global__ __launch_bounds__(1024) void resid_norm_kernel(const float* __restric
     // four columns from a multiple of 4: contiguous in either layout
     store4(out + act_index(m, i, d, out_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
     if (out2) store4(out2 + act_index(m, i, d, out2_pk), y[j].x * r, y[j].y * r, y[j].z * r, y[j].w * r);
+  }
+}
+
+// The bf16 form of draft_input: 8 columns per thread and step, loads first.
+template <int VPT>
+__global__ __launch_bounds__(ROW_THREADS) void draft_input_bf16_kernel(const uint16_t* __restrict__ E,
+                                                                       const int32_t* __restrict__ tok,
+                                                                       const int32_t* __restrict__ fsrc,
+                                                                       const uint16_t* __restrict__ fa,
+                                                                       const uint16_t* __restrict__ fb, int d,
+                                                                       uint16_t* __restrict__ x, Branches br, int x_pk) {
+  const int m = blockIdx.x, node = m / br.nb, b = m % br.nb;
+  const uint16_t* e = E + (int64_t)tok[node + b * br.tok_boff] * d;
+  const int s = fsrc[node];
+  const uint16_t* f = s >= 0 ? fa + ((int64_t)s * br.nb + b) * d
+                             : (s <= -2 ? fb + ((int64_t)(-s - 2) * br.nb + b) * d : nullptr);
+  u16x8 ev[VPT], fv[VPT];
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int c = (j * ROW_THREADS + threadIdx.x) * 8;
+    if (c >= d) continue;
+    ev[j] = *reinterpret_cast<const u16x8*>(e + c);
+    fv[j] = f ? *reinterpret_cast<const u16x8*>(f + c) : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+  }
+#pragma unroll
+  for (int j = 0; j < VPT; ++j) {
+    const int c = (j * ROW_THREADS + threadIdx.x) * 8;
+    if (c >= d) continue;
+    *reinterpret_cast<u16x8*>(x + act_index(m, c, 2 * d, x_pk)) = ev[j];
+    *reinterpret_cast<u16x8*>(x + act_index(m, d + c, 2 * d, x_pk)) = fv[j];
+  }
+}
+
+// Rows of 16-byte pieces: dst[i] = src[idx[i]], every piece of a thread loaded before any store.
+__global__ __launch_bounds__(ROW_THREADS) void gather_rows16_kernel(const u16x8* __restrict__ src,
+                                                                    const int32_t* __restrict__ idx, int pieces,
+                                                                    u16x8* __restrict__ dst) {
+  const int i = blockIdx.x;
+  const u16x8* s = src + (int64_t)idx[i] * pieces;
+  u16x8* o = dst + (int64_t)i * pieces;
+  for (int c0 = 0; c0 < pieces; c0 += 4 * ROW_THREADS) {
+    u16x8 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + j * ROW_THREADS + threadIdx.x;
+      if (c < pieces) v[j] = s[c];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = c0 + j * ROW_THREADS + threadIdx.x;
+      if (c < pieces) o[c] = v[j];
+    }
   }
 }
 
@@ -426,8 +523,19 @@ adt_status launch_embed_norm(const void* E, const int32_t* tok, int M, int d, fl
   ADT_CHECK_ARG(a != nullptr && h != nullptr, ADT_E_ARG, "embed_norm: outputs");
   ADT_CHECK_ARG(frag_ok(a_pk, M, d, dtype), ADT_E_SHAPE, "embed_norm: fragment layout of %d blocks for %d x %d", a_pk,
                 M, d);
-  ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br, a_pk,
-                                                                         raw ? 1 : 0));
+  if (dtype == ADT_BF16 && d % 8 == 0 && d <= 4 * 8 * ROW_THREADS) {
+    const int vpt = (d + 8 * ROW_THREADS - 1) / (8 * ROW_THREADS);
+#define ADT_EN(V)                                                                                                 \
+  embed_norm_bf16_kernel<V><<<M, ROW_THREADS, 0, st>>>((const uint16_t*)E, tok, d, eps, h, (uint16_t*)a, br, a_pk, \
+                                                       raw ? 1 : 0)
+    if (vpt <= 1) ADT_EN(1);
+    else if (vpt <= 2) ADT_EN(2);
+    else ADT_EN(4);
+#undef ADT_EN
+  } else {
+    ADT_DISPATCH_T(dtype, embed_norm_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, d, eps, h, (T*)a, br, a_pk,
+                                                                           raw ? 1 : 0));
+  }
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -489,8 +597,19 @@ adt_status launch_draft_input(const void* E, const int32_t* tok, const int32_t* 
                               int M, int d, void* x, int dtype, hipStream_t st, const Branches& br, int x_pk) {
   ADT_CHECK_ARG(frag_ok(x_pk, M, 2 * d, dtype), ADT_E_SHAPE, "draft_input: fragment layout of %d blocks for %d x %d",
                 x_pk, M, 2 * d);
-  ADT_DISPATCH_T(dtype, draft_input_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, fsrc, (const T*)fa,
-                                                                          (const T*)fb, d, (T*)x, br, x_pk));
+  if (dtype == ADT_BF16 && d % 8 == 0 && d <= 4 * 8 * ROW_THREADS) {
+    const int vpt = (d + 8 * ROW_THREADS - 1) / (8 * ROW_THREADS);
+#define ADT_DI(V)                                                                                                  \
+  draft_input_bf16_kernel<V><<<M, ROW_THREADS, 0, st>>>((const uint16_t*)E, tok, fsrc, (const uint16_t*)fa,       \
+                                                        (const uint16_t*)fb, d, (uint16_t*)x, br, x_pk)
+    if (vpt <= 1) ADT_DI(1);
+    else if (vpt <= 2) ADT_DI(2);
+    else ADT_DI(4);
+#undef ADT_DI
+  } else {
+    ADT_DISPATCH_T(dtype, draft_input_kernel<T><<<M, ROW_THREADS, 0, st>>>((const T*)E, tok, fsrc, (const T*)fa,
+                                                                            (const T*)fb, d, (T*)x, br, x_pk));
+  }
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }
@@ -552,7 +671,12 @@ adt_status launch_reduce_store(const float* part, int splits, int M, int N, floa
 adt_status launch_gather_rows(const void* src, const int32_t* idx, int cnt, int d, void* dst, int dtype,
                               hipStream_t st) {
   if (cnt <= 0) return ADT_OK;
-  ADT_DISPATCH_T(dtype, gather_rows_kernel<T><<<cnt, ROW_THREADS, 0, st>>>((const T*)src, idx, d, (T*)dst));
+  const int64_t row_bytes = (int64_t)d * (dtype == ADT_BF16 ? 2 : 4);
+  if (row_bytes % 16 == 0 && ((uintptr_t)src | (uintptr_t)dst) % 16 == 0) {
+    gather_rows16_kernel<<<cnt, ROW_THREADS, 0, st>>>((const u16x8*)src, idx, (int)(row_bytes / 16), (u16x8*)dst);
+  } else {
+    ADT_DISPATCH_T(dtype, gather_rows_kernel<T><<<cnt, ROW_THREADS, 0, st>>>((const T*)src, idx, d, (T*)dst));
+  }
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

@@ -19,8 +19,10 @@ constexpr int SEL_THREADS = 256;
 
 __device__ __forceinline__ bool better(float a, int ia, float b, int ib) { return a > b || (a == b && ia < ib); }
 
-constexpr int TOPK_THREADS = 1024;
+constexpr int TOPK_THREADS = 256;
 constexpr int TOPK_WAVES = TOPK_THREADS / WAVE;
+constexpr int TOPK_CHUNK = 8 * TOPK_THREADS;   // logits per chunk workgroup (two float4 per thread)
+constexpr int TOPK_MAX_CHUNKS = 32;            // vocabularies up to 65536
 
 // Wave-wide argmax of (value desc, id asc) with the owning lane.
 __device__ __forceinline__ void wave_best(float& v, int& id, int& lane) {
@@ -36,26 +38,61 @@ __device__ __forceinline__ void wave_best(float& v, int& id, int& lane) {
   }
 }
 
-// Per row: top-k ids by (logit desc, id asc) over [lo, hi) and the log-sum-exp.  The
-// thread's slice of the row (float4 j*4*T + 4*tid + {0..3}) is loaded into registers in one
-// go, so the loads overlap; then each wave takes k rounds of "best remaining element of
-// each lane" + shuffle argmax, and wave 0 merges the per-wave lists the same way.
-template <int KMAX, int E4>
-__global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __restrict__ logits, int64_t ld, int V,
-                                                                const int32_t* __restrict__ allowed, int k,
-                                                                int32_t* __restrict__ top_id,
-                                                                float* __restrict__ top_val, float* __restrict__ lse) {
+// k rounds of "best remaining value of each lane, then the wave's best" over N values per
+// lane (vals / ids, consumed); round q's winner goes to out_v[q] / out_i[q] (from lane 0).
+// Rounds past the live values give (-inf, 0x7FFFFFFF).
+template <int N>
+__device__ __forceinline__ void wave_select(float (&vals)[N], int (&ids)[N], int kk, float* out_v, int* out_i) {
+  const int lane = threadIdx.x % WAVE;
+  for (int q = 0; q < kk; ++q) {
+    float bv = -INFINITY;
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int j = 0; j < N; ++j)
+      if (better(vals[j], ids[j], bv, bi)) {
+        bv = vals[j];
+        bi = ids[j];
+      }
+    if (bv == -INFINITY) bi = 0x7FFFFFFF;
+    int bl = lane;
+    wave_best(bv, bi, bl);
+    if (lane == bl && bi != 0x7FFFFFFF) {
+#pragma unroll
+      for (int j = 0; j < N; ++j)
+        if (ids[j] == bi) vals[j] = -INFINITY;
+    }
+    if (lane == 0) {
+      out_v[q] = bv;
+      out_i[q] = bi;
+    }
+  }
+}
+
+// Top-k ids by (logit desc, id asc) over the allowed range [lo, hi) of each row, and the
+// row's log-sum-exp, in two launches.  Stage 1, one workgroup per (2048-logit chunk, row):
+// the chunk's per-wave (max, sum of exp) pairs and its own top-k (each wave selects from its
+// 512 logits, wave 0 merges the four lists).  Stage 2, one wave per row: the row's top-k
+// from the chunks' lists and the log-sum-exp from their pairs.  Spreading a row over
+// V / 2048 workgroups keeps the selection rounds (k of them, each a scan and a shuffle
+// argmax) short; one workgroup per row ran them over 64 values per lane on a few CUs.
+template <int KMAX>
+__global__ __launch_bounds__(TOPK_THREADS) void topk_chunk_kernel(const float* __restrict__ logits, int64_t ld, int V,
+                                                                  const int32_t* __restrict__ allowed, int k,
+                                                                  float* __restrict__ cand_v,
+                                                                  int* __restrict__ cand_i,
+                                                                  float2* __restrict__ cand_ms) {
   __shared__ float wv[TOPK_WAVES][KMAX];
   __shared__ int wi[TOPK_WAVES][KMAX];
-  __shared__ float smx[TOPK_WAVES], ssum[TOPK_WAVES];
-  const int row = blockIdx.x, tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
+  const int chunk = blockIdx.x, G = gridDim.x, row = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
   const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
   const float* x = logits + (int64_t)row * ld;
   const bool vec = ((ld & 3) == 0);
-  float r[E4 * 4];
+  float r[8];
+  int id[8];
 #pragma unroll
-  for (int j = 0; j < E4; ++j) {
-    const int base = j * 4 * TOPK_THREADS + 4 * tid;
+  for (int j = 0; j < 2; ++j) {
+    const int base = chunk * TOPK_CHUNK + j * 4 * TOPK_THREADS + 4 * tid;
     if (vec && base + 3 < V) {
       const float4 q = *reinterpret_cast<const float4*>(x + base);
       r[4 * j] = q.x;
@@ -66,86 +103,97 @@ __global__ __launch_bounds__(TOPK_THREADS) void row_topk_kernel(const float* __r
 #pragma unroll
       for (int e = 0; e < 4; ++e) r[4 * j + e] = (base + e < V) ? x[base + e] : -INFINITY;
     }
-  }
-  // mask to the allowed range
-#pragma unroll
-  for (int j = 0; j < E4; ++j)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int i = j * 4 * TOPK_THREADS + 4 * tid + e;
-      if (i < lo || i >= hi) r[4 * j + e] = -INFINITY;
+      id[4 * j + e] = base + e;
+      if (base + e < lo || base + e >= hi) r[4 * j + e] = -INFINITY;
     }
-  // log-sum-exp
+  }
+  // the wave's (max, sum of exp) pair
   float m = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < E4 * 4; ++j) m = fmaxf(m, r[j]);
+  for (int j = 0; j < 8; ++j) m = fmaxf(m, r[j]);
   const float M = wave_max(m);
   float sacc = 0.f;
   if (M != -INFINITY) {
 #pragma unroll
-    for (int j = 0; j < E4 * 4; ++j) sacc += (r[j] == -INFINITY) ? 0.f : expf(r[j] - M);
+    for (int j = 0; j < 8; ++j) sacc += (r[j] == -INFINITY) ? 0.f : expf(r[j] - M);
   }
   const float S = wave_sum(sacc);
-  if (lane == 0) {
-    smx[wave] = M;
-    ssum[wave] = S;
-  }
+  if (lane == 0) cand_ms[((int64_t)row * G + chunk) * TOPK_WAVES + wave] = make_float2(M, S);
   const int kk = min(k, hi - lo);
-  // wave-level selection
-  for (int q = 0; q < kk; ++q) {
-    float bv = -INFINITY;
-    int bi = 0x7FFFFFFF;
-#pragma unroll
-    for (int j = 0; j < E4 * 4; ++j) {
-      const int i = (j / 4) * 4 * TOPK_THREADS + 4 * tid + (j % 4);
-      if (better(r[j], i, bv, bi)) {
-        bv = r[j];
-        bi = i;
-      }
-    }
-    if (bv == -INFINITY) bi = 0x7FFFFFFF;
-    int bl = lane;
-    float wvv = bv;
-    int wii = bi;
-    wave_best(wvv, wii, bl);
-    if (lane == bl && wii != 0x7FFFFFFF) {
-#pragma unroll
-      for (int j = 0; j < E4 * 4; ++j) {
-        const int i = (j / 4) * 4 * TOPK_THREADS + 4 * tid + (j % 4);
-        if (i == wii) r[j] = -INFINITY;
-      }
-    }
-    if (lane == 0) {
-      wv[wave][q] = wvv;
-      wi[wave][q] = wii;
-    }
-  }
+  wave_select(r, id, kk, wv[wave], wi[wave]);
   __syncthreads();
   if (wave != 0) return;
-  if (lane == 0) {
-    float gm = -INFINITY;
-    for (int w = 0; w < TOPK_WAVES; ++w) gm = fmaxf(gm, smx[w]);
-    float gs = 0.f;
-    for (int w = 0; w < TOPK_WAVES; ++w)
-      if (smx[w] != -INFINITY) gs += ssum[w] * expf(smx[w] - gm);
-    lse[row] = gm + logf(gs);
-  }
-  int h2 = 0;
+  // wave 0: the chunk's top-k from the four wave lists (lane w < 4 offers list w's head)
+  float* ov = cand_v + ((int64_t)row * G + chunk) * KMAX;
+  int* oi = cand_i + ((int64_t)row * G + chunk) * KMAX;
+  int h = 0;
   for (int q = 0; q < kk; ++q) {
     float hv = -INFINITY;
     int hid = 0x7FFFFFFF;
-    if (lane < TOPK_WAVES && h2 < kk) {
-      hv = wv[lane][h2];
-      hid = wi[lane][h2];
+    if (lane < TOPK_WAVES && h < kk) {
+      hv = wv[lane][h];
+      hid = wi[lane][h];
     }
     int bl = lane;
     wave_best(hv, hid, bl);
-    if (lane == bl) ++h2;
+    if (lane == bl) ++h;
     if (lane == 0) {
-      top_id[row * KMAX + q] = hid;
-      top_val[row * KMAX + q] = hv;
+      ov[q] = hv;
+      oi[q] = hid;
     }
   }
+}
+
+// Stage 2: one wave per row over the G chunk lists (G * KMAX <= 8 * WAVE candidates).
+template <int KMAX>
+__global__ __launch_bounds__(WAVE) void topk_merge_kernel(const float* __restrict__ cand_v,
+                                                          const int* __restrict__ cand_i,
+                                                          const float2* __restrict__ cand_ms, int G, int V,
+                                                          const int32_t* __restrict__ allowed, int k,
+                                                          int32_t* __restrict__ top_id, float* __restrict__ top_val,
+                                                          float* __restrict__ lse) {
+  constexpr int N = TOPK_MAX_CHUNKS * KMAX / WAVE > 0 ? TOPK_MAX_CHUNKS * KMAX / WAVE : 1;
+  const int row = blockIdx.x, lane = threadIdx.x;
+  const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
+  const int kk = min(k, hi - lo);
+  // chunk c's list holds its min(k, live) entries; the rest of a list is never read
+  float vals[N];
+  int ids[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const int e = j * WAVE + lane, c = e / KMAX, q = e % KMAX;
+    vals[j] = -INFINITY;
+    ids[j] = 0x7FFFFFFF;
+    if (c < G && q < kk) {
+      vals[j] = cand_v[((int64_t)row * G) * KMAX + e];
+      ids[j] = cand_i[((int64_t)row * G) * KMAX + e];
+    }
+  }
+  // log-sum-exp from the G * 4 (max, sum) pairs, in pair order within the lane
+  float pm[2 * TOPK_MAX_CHUNKS * TOPK_WAVES / WAVE], ps[2 * TOPK_MAX_CHUNKS * TOPK_WAVES / WAVE];
+  float gm = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 2 * TOPK_MAX_CHUNKS * TOPK_WAVES / WAVE; ++j) {
+    const int e = j * WAVE + lane;
+    pm[j] = -INFINITY;
+    ps[j] = 0.f;
+    if (e < G * TOPK_WAVES) {
+      const float2 p = cand_ms[(int64_t)row * G * TOPK_WAVES + e];
+      pm[j] = p.x;
+      ps[j] = p.y;
+    }
+    gm = fmaxf(gm, pm[j]);
+  }
+  gm = wave_max(gm);
+  float gs = 0.f;
+#pragma unroll
+  for (int j = 0; j < 2 * TOPK_MAX_CHUNKS * TOPK_WAVES / WAVE; ++j)
+    if (pm[j] != -INFINITY) gs += ps[j] * expf(pm[j] - gm);
+  gs = wave_sum(gs);
+  if (lane == 0) lse[row] = gm + logf(gs);
+  wave_select(vals, ids, kk, top_val + row * KMAX, top_id + row * KMAX);
 }
 
 // Pool (see launch.h): device arrays of capacity C: token, score, depth, parent (pool index,
@@ -420,26 +468,30 @@ __global__ __launch_bounds__(WAVE) void accept_greedy_kernel(const int32_t* __re
 }
 
 // ----------------------------------------------------------------------------- host
+size_t row_topk_ws_bytes(int rows, int kmax) {
+  return (size_t)rows * TOPK_MAX_CHUNKS * (kmax * 8 + TOPK_WAVES * 8) + 256;
+}
+
 adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
-                           int32_t* top_id, float* top_val, float* lse, hipStream_t st) {
+                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st) {
   ADT_CHECK_ARG(k >= 1 && k <= kmax && (kmax == 1 || kmax == 16), ADT_E_UNSUPPORTED, "row_topk: k=%d kmax=%d", k, kmax);
-  const int e4 = (V + 4 * TOPK_THREADS - 1) / (4 * TOPK_THREADS);
-  ADT_CHECK_ARG(e4 <= 16, ADT_E_UNSUPPORTED, "row_topk: vocab %d above 65536", V);
-#define ADT_TOPK(KM, E)                                                                                        \
-  row_topk_kernel<KM, E><<<rows, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, top_id, top_val, lse)
-#define ADT_TOPK_E(KM)            \
-  if (e4 <= 1) ADT_TOPK(KM, 1);   \
-  else if (e4 <= 2) ADT_TOPK(KM, 2); \
-  else if (e4 <= 4) ADT_TOPK(KM, 4); \
-  else if (e4 <= 8) ADT_TOPK(KM, 8); \
-  else ADT_TOPK(KM, 16)
+  const int G = (V + TOPK_CHUNK - 1) / TOPK_CHUNK;
+  ADT_CHECK_ARG(V >= 1 && G <= TOPK_MAX_CHUNKS, ADT_E_UNSUPPORTED, "row_topk: vocab %d above 65536", V);
+  ADT_CHECK_ARG(ws && ws_bytes >= row_topk_ws_bytes(rows, kmax), ADT_E_CAPACITY, "row_topk: workspace %zu < %zu", ws_bytes,
+                row_topk_ws_bytes(rows, kmax));
+  float2* cms = (float2*)ws;
+  float* cv = (float*)(cms + (size_t)rows * G * TOPK_WAVES);
+  int* ci = (int*)(cv + (size_t)rows * G * kmax);
+  const dim3 g1(G, rows);
   if (kmax == 1) {
-    ADT_TOPK_E(1);
+    topk_chunk_kernel<1><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, cv, ci, cms);
+    ADT_LAUNCH_CHECK();
+    topk_merge_kernel<1><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, k, top_id, top_val, lse);
   } else {
-    ADT_TOPK_E(16);
+    topk_chunk_kernel<16><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, cv, ci, cms);
+    ADT_LAUNCH_CHECK();
+    topk_merge_kernel<16><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, k, top_id, top_val, lse);
   }
-#undef ADT_TOPK_E
-#undef ADT_TOPK
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

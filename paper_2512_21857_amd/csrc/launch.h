@@ -170,8 +170,11 @@ struct NextRows {
   uint64_t* mask;
   int32_t* frontier;
 };
+// Top-k (ids and logits, rows of kmax) and log-sum-exp of each row over its allowed range;
+// ws holds row_topk_ws_bytes(rows, kmax) bytes of per-chunk candidates.
+size_t row_topk_ws_bytes(int rows, int kmax);
 adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
-                           int32_t* top_id, float* top_val, float* lse, hipStream_t st);
+                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st);
 adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
                                const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
                                int L, int drow_base, int root_frow, int tree_frow0, int qrow_base, const NextRows& nx,
