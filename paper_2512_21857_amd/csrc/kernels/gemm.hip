@@ -94,10 +94,47 @@ __device__ __forceinline__ f32x4 shfl_xor4(f32x4 v, int mask) {
                __shfl_xor(v[3], mask, WAVE)};
 }
 
+// Inputs of a block's epilogue that do not depend on the product, requested by the wave that
+// will finish the block before the main loop starts: the residual tile (EPI_RESID), or the
+// RoPE factors of the lane's four columns and the cache slot of its row (EPI_QKV).
+struct EpiPre {
+  float v[8];
+  int slot;
+};
+__device__ __forceinline__ EpiPre epi_preload(const GemmEpi& e, int row, int g, int nt, int M, int N) {
+  EpiPre p;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) p.v[i] = 0.f;
+  p.slot = 0;
+  if (row >= M) return p;
+  if (e.mode == EPI_RESID) {
+    if (!e.assign) {
+      const f32x4 h = *reinterpret_cast<const f32x4*>(e.resid + (int64_t)row * N + nt * 16 + 4 * g);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p.v[i] = h[i];
+    }
+  } else if (e.mode == EPI_QKV && g < 2) {
+    const int d = N / 3, half = e.Dh / 2, n0 = nt * 16, within = n0 % d, u = (within % e.Dh) / 16;
+    const int node = e.nb == 1 ? row : row >> 1;
+    p.slot = *e.slot0 + node;
+    if (n0 / d < 2) {
+      const float2* cs = e.rope + (int64_t)e.pos[node] * half + 8 * u + 4 * g;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float2 t = cs[r];
+        p.v[2 * r] = t.x;
+        p.v[2 * r + 1] = t.y;
+      }
+    }
+  }
+  return p;
+}
+
 // Epilogue of one finished 16-row block of tile nt, run by a whole wave: lane (lq, g) holds
 // Y[row][nt*16 + 4g + r], r = 0..3.  In a QKV or gate/up tile, columns 0..7 (lanes g < 2)
 // pair with columns 8..15 (lanes g + 2).
-__device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row, int g, int nt, int M, int N) {
+__device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, const EpiPre& pre, int row, int g, int nt,
+                                              int M, int N) {
   const bool live = row < M;
   const int c = nt * 16 + 4 * g;
   if (e.mode == EPI_STORE) {
@@ -110,19 +147,19 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
       const int j = 8 * u + 4 * g;   // element of the head's first half held in y[0]
       float a[4] = {y[0], y[1], y[2], y[3]}, b[4] = {y2[0], y2[1], y2[2], y2[3]};
       const int node = e.nb == 1 ? row : row >> 1, branch = row - node * e.nb;
+      (void)node;
       if (region < 2) {
-        const float2* cs = e.rope + (int64_t)e.pos[node] * half + j;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float2 t = cs[r];
+          const float cx = pre.v[2 * r], sx = pre.v[2 * r + 1];
           const float x1 = a[r], x2 = b[r];
-          a[r] = x1 * t.x - x2 * t.y;
-          b[r] = x2 * t.x + x1 * t.y;
+          a[r] = x1 * cx - x2 * sx;
+          b[r] = x2 * cx + x1 * sx;
         }
       }
       uint16_t* dst = region == 0 ? e.q + (int64_t)row * d + head * Dh
                                   : (region == 1 ? e.kc : e.vc) + branch * e.cache_sb + head * e.stride_h +
-                                        (*e.slot0 + (int64_t)node) * Dh;
+                                        (int64_t)pre.slot * Dh;
       *reinterpret_cast<u16x4*>(dst + j) = u16x4{f2bf(a[0]), f2bf(a[1]), f2bf(a[2]), f2bf(a[3])};
       *reinterpret_cast<u16x4*>(dst + j + half) = u16x4{f2bf(b[0]), f2bf(b[1]), f2bf(b[2]), f2bf(b[3])};
     }
@@ -130,10 +167,7 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, int row
     if (live) {
       float* hp = e.resid + (int64_t)row * N + c;
       f32x4 h = y;
-      if (!e.assign) {
-        const f32x4 o = *reinterpret_cast<const f32x4*>(hp);
-        h = f32x4{o[0] + y[0], o[1] + y[1], o[2] + y[2], o[3] + y[3]};
-      }
+      if (!e.assign) h = f32x4{pre.v[0] + y[0], pre.v[1] + y[1], pre.v[2] + y[2], pre.v[3] + y[3]};
       *reinterpret_cast<f32x4*>(hp) = h;
       store4(e.act + act_index(row, c, N, e.act_pk), h[0], h[1], h[2], h[3]);
     }
@@ -167,13 +201,15 @@ __device__ __forceinline__ float sumsq8(bf16x8 v, float s) {
 // Loads past the wave's range are clamped to its last k-tile and their products discarded.
 // NORM: the waves also sum the squares of the input fragments they multiply (lane (lq, g)
 // holds row m * 16 + lq), the sums meet in LDS in wave order, and each finished row is scaled
-// by its RMSNorm factor before the epilogue.
-template <int MT, int T, int KC, bool NORM>
+// by its RMSNorm factor before the epilogue.  PRE: the epilogue's own inputs are requested
+// before the main loop (EPI_QKV, EPI_RESID).
+template <int MT, int T, int KC, bool NORM, bool PRE>
 __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t* __restrict__ X, int ldx,
                                                                  const uint16_t* __restrict__ Wp, int M, int N, int K,
                                                                  int S, int stagger, GemmEpi epi) {
-  constexpr int TT = MT * T;                 // 16x16 output blocks per workgroup
-  constexpr int TR = TT < 4 ? TT : 4;        // blocks summed per LDS round
+  constexpr int TT = MT * T;                            // 16x16 output blocks per workgroup
+  constexpr int TR = TT < TILE_WAVES ? TT : TILE_WAVES; // blocks finished per LDS round
+  constexpr int NR = (TT + TR - 1) / TR;                // rounds
   __shared__ f32x4 red[TILE_WAVES][TR][WAVE];
   const int KT = K / 32;
   const int cb = blockIdx.x / S, sp = blockIdx.x % S;
@@ -215,6 +251,13 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
       for (int m = 0; m < MT; ++m) x[j][m] = *reinterpret_cast<const bf16x8*>(xp[m] + kk * xks);
     }
   };
+  // wave w finishes block r * TR + w of round r: its epilogue inputs are requested now
+  EpiPre pre[PRE ? NR : 1];
+#pragma unroll
+  for (int r = 0; r < (PRE ? NR : 1); ++r) {
+    const int q = r * TR + wave;
+    if (PRE && wave < TR && q < TT) pre[r] = epi_preload(epi, (q % MT) * 16 + lq, g, cb * T + q / MT, M, N);
+  }
   f32x4 acc[T][MT];
   float ss[MT];
 #pragma unroll
@@ -263,7 +306,8 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
   }
   // Sum the waves' partial blocks in wave order; wave i then finishes block q0 + i.
 #pragma unroll
-  for (int q0 = 0; q0 < TT; q0 += TR) {
+  for (int rr = 0; rr < NR; ++rr) {
+    const int q0 = rr * TR;
 #pragma unroll
     for (int i = 0; i < TR; ++i)
       if (q0 + i < TT) red[wave][i][lane] = acc[(q0 + i) / MT % T][(q0 + i) % MT];
@@ -287,7 +331,10 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
       if (epi.mode == EPI_PART) {
         if (row < M) *reinterpret_cast<f32x4*>(epi.part + ((int64_t)sp * M + row) * N + nt * 16 + 4 * g) = y;
       } else {
-        tile_epilogue(epi, y, row, g, nt, M, N);
+        EpiPre p{};
+        if (PRE) p = pre[PRE ? rr : 0];
+        else if (epi.mode == EPI_QKV || epi.mode == EPI_RESID) p = epi_preload(epi, row, g, nt, M, N);
+        tile_epilogue(epi, y, p, row, g, nt, M, N);
       }
     }
     __syncthreads();
@@ -434,13 +481,23 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
   const dim3 grid(N / 16 / p.T * p.S), block(TILE_THREADS);
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)Wp;
-#define ADT_GR(MTV, TV, KCV)                                                                                   \
-  if (epi.norm_eps > 0.f) {                                                                                        \
-    hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV, true>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N, K, \
-                          p.S, stagger, epi);                                                                      \
-  } else {                                                                                                         \
-    hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV, false>, grid, block, 0, st, ev0, ev1, 0, x, ldx, w, M, N,   \
-                          K, p.S, stagger, epi);                                                                   \
+  // epilogue inputs requested early for QKV and the residual epilogue (not at > 4 row blocks,
+  // where the registers are taken by the accumulators)
+  const bool pre = (epi.mode == EPI_QKV || epi.mode == EPI_RESID) && mt <= 4;
+#define ADT_GR_L(MTV, TV, KCV, NV, PV)                                                                            \
+  hipExtLaunchKernelGGL(gemm_rows_kernel<MTV, TV, KCV, NV, (PV && MTV <= 4)>, grid, block, 0, st, ev0, ev1, 0, x, \
+                        ldx, w, M, N, K, p.S, stagger, epi)
+#define ADT_GR(MTV, TV, KCV)                  \
+  if (epi.norm_eps > 0.f) {                   \
+    if (pre && MTV <= 4) {                    \
+      ADT_GR_L(MTV, TV, KCV, true, true);     \
+    } else {                                  \
+      ADT_GR_L(MTV, TV, KCV, true, false);    \
+    }                                         \
+  } else if (pre && MTV <= 4) {               \
+    ADT_GR_L(MTV, TV, KCV, false, true);      \
+  } else {                                    \
+    ADT_GR_L(MTV, TV, KCV, false, false);     \
   }
   // k-tiles per round: one with three or four tiles (their fragments already keep enough in
   // flight), else two, or three for one row block
@@ -469,6 +526,7 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
 #undef ADT_GR_T2
 #undef ADT_GR_T4
 #undef ADT_GR
+#undef ADT_GR_L
   ADT_LAUNCH_CHECK();
   if (splits) *splits = p.S;
   return ADT_OK;
