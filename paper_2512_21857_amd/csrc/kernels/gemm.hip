@@ -213,6 +213,10 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
   __shared__ f32x4 red[TILE_WAVES][TR][WAVE];
   const int KT = K / 32;
   const int cb = blockIdx.x / S, sp = blockIdx.x % S;
+  // column group cb of G takes tiles [t0, t0 + tc), tc <= T; a shorter group repeats its last
+  // tile in the remaining slots (the loop stays free of branches; those products are dropped)
+  const int G = gridDim.x / S, tiles = N / 16;
+  const int t0 = (int)((int64_t)cb * tiles / G), tc = (int)((int64_t)(cb + 1) * tiles / G) - t0;
   // the wave index is made scalar, so the K range and the round bounds are uniform branches
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
@@ -223,7 +227,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
   const int rot = (stagger && nk > 0) ? (int)((blockIdx.x * 37u) % (unsigned)(span / KC)) * KC : 0;
   const bf16x8* wp[T];
 #pragma unroll
-  for (int t = 0; t < T; ++t) wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(cb * T + t) * KT * 64 + lane;
+  for (int t = 0; t < T; ++t) wp[t] = reinterpret_cast<const bf16x8*>(Wp) + (int64_t)(t0 + min(t, tc - 1)) * KT * 64 + lane;
   // input fragment m of k-tile kk at xp[m] + kk * xks: row-major rows (clamped to M - 1), or
   // the fragment layout's 1 KB blocks (row blocks past the last clamped to it)
   const int mt = (M + 15) / 16;
@@ -256,7 +260,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
 #pragma unroll
   for (int r = 0; r < (PRE ? NR : 1); ++r) {
     const int q = r * TR + wave;
-    if (PRE && wave < TR && q < TT) pre[r] = epi_preload(epi, (q % MT) * 16 + lq, g, cb * T + q / MT, M, N);
+    if (PRE && wave < TR && q < TT && q / MT < tc) pre[r] = epi_preload(epi, (q % MT) * 16 + lq, g, t0 + q / MT, M, N);
   }
   f32x4 acc[T][MT];
   float ss[MT];
@@ -312,7 +316,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
     for (int i = 0; i < TR; ++i)
       if (q0 + i < TT) red[wave][i][lane] = acc[(q0 + i) / MT % T][(q0 + i) % MT];
     __syncthreads();
-    if (wave < TR && q0 + wave < TT) {
+    if (wave < TR && q0 + wave < TT && (q0 + wave) / MT < tc) {
       f32x4 y = red[0][wave][lane];
 #pragma unroll
       for (int w = 1; w < TILE_WAVES; ++w) {
@@ -320,7 +324,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
         y = f32x4{y[0] + v[0], y[1] + v[1], y[2] + v[2], y[3] + v[3]};
       }
       const int q = q0 + wave;
-      const int row = (q % MT) * 16 + lq, nt = cb * T + q / MT;
+      const int row = (q % MT) * 16 + lq, nt = t0 + q / MT;
       if (NORM) {
         float t = 0.f;
 #pragma unroll
@@ -418,13 +422,19 @@ RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
   const int mt = (M + 15) / 16, tiles = N / 16, KT = K / 32;
   const int tmax = mt <= 4 ? 4 : 2;
   auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
-  if (partial && tiles >= 192 && (mt <= 2 || K <= 8192)) return {1, 1};
+  if (partial && tiles >= 192 && (mt <= 2 || K <= 8192)) return {1, 1, tiles};
   if (!partial || (mt == 1 && tiles >= 192)) {
+    // > 32 rows: a multiple of 256 workgroups (whole rounds of the CUs) with at most tmax tiles
+    // each, spread evenly (gate/up's 1376 tiles: 512 groups of 2-3, 45 us against 48 with 344
+    // groups of 4)
+    if (mt >= 3)
+      for (int g = 256; g <= tiles; g += 256)
+        if ((tiles + g - 1) / g <= tmax) return {(tiles + g - 1) / g, 1, g};
     for (int t : {4, 3, 2}) {
       if (!ok(t) || tiles / t < 256) continue;
-      if (t <= 2 || tiles / t == 256 || mt >= 3 || (mt == 2 && tiles / t >= 1024)) return {t, 1};
+      if (t <= 2 || tiles / t == 256 || (mt == 2 && tiles / t >= 1024)) return {t, 1, tiles / t};
     }
-    return {1, 1};
+    return {1, 1, tiles};
   }
   const int smax = std::max(1, std::min(GEMM_MAX_SPLITS, KT / (10 * TILE_WAVES)));
   int T = 1;
@@ -435,7 +445,7 @@ RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
     }
   const int blocks = tiles / T;
   const int S = blocks >= 192 ? 1 : std::max(1, std::min(smax, 256 / blocks));
-  return {T, S};
+  return {T, S, blocks};
 }
 
 adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int K, int dtype, float* part,
@@ -478,7 +488,7 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
                 "gemm: %d K-range sums of %d x %d exceed the partial buffer", p.S, M, N);
   const int mt = (M + 15) / 16;
   const int stagger = 1;
-  const dim3 grid(N / 16 / p.T * p.S), block(TILE_THREADS);
+  const dim3 grid(p.G * p.S), block(TILE_THREADS);
   const uint16_t* x = (const uint16_t*)X;
   const uint16_t* w = (const uint16_t*)Wp;
   // epilogue inputs requested early for QKV and the residual epilogue (not at > 4 row blocks,

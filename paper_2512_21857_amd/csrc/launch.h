@@ -89,7 +89,8 @@ struct GemmEpi {
   float norm_eps = 0.f;
 };
 struct RowsPlan {
-  int T, S;       // 16-column tiles per workgroup, K ranges
+  int T, S;       // at most T 16-column tiles per workgroup, S K ranges
+  int G;          // column groups: group c takes tiles [c tiles / G, (c + 1) tiles / G)
 };
 RowsPlan gemm_rows_plan(int M, int N, int K, bool partial);
 constexpr int GEMM_MAX_SPLITS = 8;
