@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--traffic-run", action="store_true",
                     help="counter-collection mode: profile every projection launch from the prefill on over the "
                          "warm-up and timed steps of the headline workload and print their count and algorithmic bytes")
+    ap.add_argument("--microbench-run", action="store_true",
+                    help="only the tree-attention and KV-compaction microbenchmarks (for counter collection)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first copy 512 MiB device-to-device (a kernel of known traffic for counter scaling)")
     return ap.parse_args()
@@ -250,7 +252,8 @@ def attn_microbench(rt, sizes=(8, 16, 32, 64, 128), iters=30, sets=3):
         e1.synchronize()
         ms = e0.elapsed_time(e1) / iters
         gbs = byts / iters / (ms * 1e-3) / 1e9
-        out[str(n)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        out[str(n)] = {"us": round(ms * 1e3, 2), "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+                       "bytes_per_launch": int(byts / iters)}
         del bufs, outs
         torch.cuda.empty_cache()
     return out
@@ -452,6 +455,11 @@ def main():
         del src, dst
     threads = min(16, len(os.sched_getaffinity(0)))
     K, W = args.steps, args.warmup
+    if args.microbench_run:
+        log("microbenchmarks only")
+        print(json.dumps({"microbench_run": True, "tree_attn_16x32x128": attn_microbench(rt),
+                          "kv_compact": compact_microbench(rt)}), flush=True)
+        return
 
     # ---- headline: Lumina-mGPT-7B-shaped, Poisson-driven ADT trees, greedy, batch 1
     cfg = synth.get_config("lumina_7b")

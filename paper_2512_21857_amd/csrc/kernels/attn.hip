@@ -681,7 +681,7 @@ static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_m
 // forwards) take the shared-block kernel with the keys split across workgroups instead.
 static bool attn_use_wg(int B, int H, int Dh, int nq_max) {
   int qtw, qg, qsplit;
-  return B * H >= 128 && attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
+  return B * H >= 128 && nq_max <= 16 && attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
 }
 
 // Upper bound over every kv_cap: the splits never exceed ceil(256 / (B*H)).
