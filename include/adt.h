@@ -41,7 +41,8 @@ typedef int32_t adt_status;
 #define ADT_E_CAPACITY (-3)    /* tree, cache or workspace too small */
 #define ADT_E_HIP (-4)         /* a HIP runtime call failed */
 #define ADT_E_UNSUPPORTED (-5) /* valid request outside what this build implements */
-#define ADT_E_STATE (-6)       /* session used out of order (e.g. step before prefill) */
+#define ADT_E_DEVICE_INVARIANT (-6) /* debug builds: a kernel found device data breaking an invariant */
+#define ADT_E_STATE (-7)       /* session used out of order (e.g. step before prefill) */
 
 #define ADT_F32 0
 #define ADT_BF16 1
@@ -73,6 +74,22 @@ int32_t adt_version(void);
 /* Copies the last error message of this thread into buf (NUL-terminated, truncated to cap);
  * returns its full length. */
 size_t adt_last_error(char* buf, size_t cap);
+
+/* Device invariant checks.  The library is also built as libadt_debug.so (same ABI, built
+ * with ADT_DEVICE_CHECKS=1), whose kernels test the device-side data the host cannot see
+ * before launching: a tree's parents come before their children (parent[0] = -1,
+ * 0 <= parent[i] < i; the BFS order of Sec. 4.2's tree arrays), the keys a launch reads or
+ * appends stay inside the cache (kv_len + n <= S_cap), accepted-path entries lie inside the
+ * tree.  A kernel that finds a violation records it in a device error word and continues
+ * within bounds (masked or skipped), so no access leaves its buffers.
+ * adt_device_checks_enabled() is 1 in the debug build, 0 otherwise.
+ * adt_device_check(stream) synchronises `stream` and returns ADT_E_DEVICE_INVARIANT (with a
+ * message naming the invariants) if any kernel of this library recorded a violation since
+ * the last check, clearing the record; ADT_OK otherwise (always in the release build, which
+ * records nothing).  Every session call that synchronises (prefill, adt_step,
+ * adt_session_accept_commit, ...) runs the same check after its own synchronisation. */
+int32_t adt_device_checks_enabled(void);
+adt_status adt_device_check(void* stream);
 
 /* ------------------------------------------------------------------ b2: tree attention
  * Sec. 3.1: node i attends to the committed prefix and to the nodes on its own

@@ -11,9 +11,10 @@ from typing import Optional
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libadt.so")
+DEBUG_LIB_PATH = os.path.join(PKG, "libadt_debug.so")   # device invariant checks compiled in
 
 OK = 0
-E_ARG, E_SHAPE, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_STATE = -1, -2, -3, -4, -5, -6
+E_ARG, E_SHAPE, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_DEVICE_INVARIANT, E_STATE = -1, -2, -3, -4, -5, -6, -7
 F32, BF16 = 0, 1
 MAX_NODES = 128
 MASK_WORDS = 2
@@ -85,6 +86,8 @@ class CaptureRec(C.Structure):
 
 _SIGS = {
     "adt_version": (i32, []),
+    "adt_device_checks_enabled": (i32, []),
+    "adt_device_check": (i32, [p]),
     "adt_last_error": (sz, [C.c_char_p, sz]),
     "adt_tree_attn_workspace_size": (sz, [i32, i32, i32, i32, i32]),
     "adt_tree_attn": (i32, [p, p, p, i64, i64, p, p, p, p, i32, i32, i32, i32, i32, f32, i32, p, p, sz, p]),
@@ -134,6 +137,7 @@ PROF_GEMM, PROF_ATTN, PROF_COMPACT, PROF_ROWS = 0, 1, 2, 3
 EXPORTED = tuple(_SIGS)
 
 _lib: Optional[C.CDLL] = None
+_lib_debug: Optional[C.CDLL] = None
 
 
 class AdtError(RuntimeError):
@@ -142,24 +146,37 @@ class AdtError(RuntimeError):
         self.code = code
 
 
+def _load(path: str) -> C.CDLL:
+    import torch  # noqa: F401  (binds the library to the HIP runtime torch loaded)
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run paper_2512_21857_amd.build.build()")
+    L = C.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    return L
+
+
 def lib() -> C.CDLL:
     global _lib
     if _lib is None:
-        import torch  # noqa: F401  (binds libadt.so to the HIP runtime torch loaded)
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is not built; run paper_2512_21857_amd.build.build()")
-        L = C.CDLL(LIB_PATH)
-        for name, (res, args) in _SIGS.items():
-            fn = getattr(L, name)
-            fn.restype = res
-            fn.argtypes = args
-        _lib = L
+        _lib = _load(LIB_PATH)
     return _lib
 
 
-def last_error() -> str:
+def lib_debug() -> C.CDLL:
+    """The debug build (device invariant checks); its own error message buffer is read with
+    last_error(lib_debug())."""
+    global _lib_debug
+    if _lib_debug is None:
+        _lib_debug = _load(DEBUG_LIB_PATH)
+    return _lib_debug
+
+
+def last_error(L: Optional[C.CDLL] = None) -> str:
     buf = C.create_string_buffer(512)
-    lib().adt_last_error(buf, 512)
+    (L or lib()).adt_last_error(buf, 512)
     return buf.value.decode(errors="replace")
 
 

@@ -1,4 +1,6 @@
-"""Builds libadt.so (the HIP kernels and the C ABI) in-tree with hipcc for gfx950.
+"""Builds libadt.so (the HIP kernels and the C ABI) in-tree with hipcc for gfx950, and
+libadt_debug.so, the same sources with the device invariant checks compiled in
+(ADT_DEVICE_CHECKS=1).
 
 Usage: python -m paper_2512_21857_amd.build   (or build() from Python)."""
 from __future__ import annotations
@@ -12,6 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libadt.so")
+OUT_DEBUG = os.path.join(PKG, "libadt_debug.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -36,9 +39,10 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, src.replace("/", "_").replace(".hip", ".o"))
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(job) -> str:
+    src, debug = job
+    obj = os.path.join(BUILD_DIR, ("debug_" if debug else "") + src.replace("/", "_").replace(".hip", ".o"))
+    cmd = [HIPCC, *FLAGS, *(["-DADT_DEVICE_CHECKS=1"] if debug else []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
@@ -48,18 +52,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(min(8, os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = OUT + ".tmp"
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    jobs = [(s, False) for s in SOURCES] + [(s, True) for s in SOURCES]
+    with ThreadPoolExecutor(min(8, os.cpu_count() or 4)) as ex:
+        objs = list(ex.map(_compile, jobs))
+    _link(objs[:len(SOURCES)], OUT)
+    _link(objs[len(SOURCES):], OUT_DEBUG)
     if verbose:
-        print("built", OUT)
+        print("built", OUT, "and", OUT_DEBUG)
     return OUT
 
 

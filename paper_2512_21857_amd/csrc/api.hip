@@ -963,6 +963,7 @@ static adt_status run_layers(adt_session_s* s, bool draft, int M, const int32_t*
       qkv.Dh = Dh;
       qkv.nb = nb;
       qkv.cache_sb = cache_sb;
+      qkv.slot_cap = s->d.s_cap;
       qkv.norm_eps = eps;
       TRY(gemm_p(s->act, X_FRAG, m->qkv[l], rows, 3 * dm, dm, dt, s->part, st, qkv));
       TRY(attention(kc, vc));
@@ -1091,10 +1092,30 @@ static adt_status draft_forward(adt_session_s* s, const int32_t* tok, const int3
   return key < 0 ? body(st) : run_graph(s, key, st, body);
 }
 
+// Debug builds: the invariant violations the kernels recorded since the last look (cleared).
+static adt_status device_errors() {
+  if (!ADT_DEVICE_CHECKS) return ADT_OK;
+  const uint32_t bits = dev_errors_take_rows() | dev_errors_take_select() | dev_errors_take_attn() |
+                        dev_errors_take_gemm();
+  ADT_CHECK_ARG(!(bits & 0x80000000u), ADT_E_HIP, "device check: the error words could not be read");
+  ADT_CHECK_ARG(bits == 0, ADT_E_DEVICE_INVARIANT, "device invariant violated:%s%s%s",
+                (bits & DEVINV_PARENT) ? " a parent not before its child" : "",
+                (bits & DEVINV_KV_RANGE) ? " keys past the cache capacity" : "",
+                (bits & DEVINV_PATH) ? " an accepted-path entry outside the tree" : "");
+  return ADT_OK;
+}
+
 static adt_status sync_stream(hipStream_t st) {
   ADT_HIP(hipStreamSynchronize(st));
   prof_collect();
-  return ADT_OK;
+  return device_errors();
+}
+
+extern "C" int32_t adt_device_checks_enabled(void) { return ADT_DEVICE_CHECKS ? 1 : 0; }
+
+extern "C" adt_status adt_device_check(void* stream) {
+  ADT_HIP(hipStreamSynchronize((hipStream_t)stream));
+  return device_errors();
 }
 
 static adt_status set_root_only_tree(adt_session_s* s, int root_token, int L, hipStream_t st) {

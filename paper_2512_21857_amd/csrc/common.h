@@ -58,6 +58,33 @@ __host__ __device__ __forceinline__ int64_t act_index(int64_t r, int k, int64_t 
   return pk ? frag_index(r, k, pk) : r * ld + k;
 }
 
+// Debug builds (ADT_DEVICE_CHECKS=1) test invariants of device-side inputs; a kernel that finds
+// one broken sets its bit in the error word of its source file and goes on within bounds.
+#ifndef ADT_DEVICE_CHECKS
+#define ADT_DEVICE_CHECKS 0
+#endif
+enum : uint32_t {
+  DEVINV_PARENT = 1u,     // parent[0] != -1 or parent[i] outside [0, i)
+  DEVINV_KV_RANGE = 2u,   // kv_len + n beyond the cache capacity
+  DEVINV_PATH = 4u,       // an accepted-path entry outside the tree
+};
+// One error word per source file (each file is its own device code object): file-scope
+// `dev_err_word`, set by dev_fail, read and cleared by the file's dev_errors_take_*.
+#define ADT_DEVICE_ERROR_WORD(tag)                                                               \
+  static __device__ uint32_t dev_err_word;                                                       \
+  __device__ __forceinline__ void dev_fail(uint32_t bit) {                                       \
+    if (ADT_DEVICE_CHECKS) atomicOr(&dev_err_word, bit);                                         \
+  }                                                                                              \
+  uint32_t dev_errors_take_##tag() {                                                             \
+    if (!ADT_DEVICE_CHECKS) return 0;                                                            \
+    void* p = nullptr;                                                                           \
+    uint32_t v = 0;                                                                              \
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(dev_err_word)) != hipSuccess || !p) return 0x80000000u; \
+    if (hipMemcpy(&v, p, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return 0x80000000u;    \
+    if (v && hipMemset(p, 0, sizeof(v)) != hipSuccess) return 0x80000000u;                        \
+    return v;                                                                                    \
+  }
+
 // Philox4x32-10 (Salmon et al., SC'11): ten rounds over counter (c0..c3) with key (k0, k1);
 // host and device share it (acceptance draws on the GPU, the Random tree initialisation on
 // the host).

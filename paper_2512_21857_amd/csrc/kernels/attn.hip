@@ -20,6 +20,8 @@
 
 namespace adt {
 
+ADT_DEVICE_ERROR_WORD(attn)
+
 constexpr int ATT_KT = 64;      // keys per LDS tile
 constexpr int ATT_MAX_SPLITS = 64;
 
@@ -83,6 +85,7 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
   const int L = kv_len[b];
   const int nq = dead ? 0 : min(n_q[b], nq_max);
   const int total = dead ? 0 : min(L + n_tail[b], kv_cap);
+  if (!dead && threadIdx.x == 0 && L + n_tail[b] > kv_cap) dev_fail(DEVINV_KV_RANGE);
   int per = (total + KG - 1) / KG;
   per = (per + 15) / 16 * 16;
   const int k0 = min(total, kg * per), k1 = min(total, k0 + per);
@@ -344,6 +347,7 @@ __global__ __launch_bounds__(128) void tree_attn_f32_kernel(
   if (qr >= min(n_q[b], nq_max)) return;
   const int L = kv_len[b];
   const int total = min(L + n_tail[b], kv_cap);
+  if (threadIdx.x == 0 && L + n_tail[b] > kv_cap) dev_fail(DEVINV_KV_RANGE);
   const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
   const uint64_t w0 = mp[0], w1 = mp[1];
   float* qs = smem;
@@ -429,6 +433,7 @@ __global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel
   const int L = kv_len[b];
   const int nq = min(n_q[b], nq_max);
   const int total = min(L + n_tail[b], kv_cap);
+  if (threadIdx.x == 0 && L + n_tail[b] > kv_cap) dev_fail(DEVINV_KV_RANGE);
   // with splits > 1, split sp takes a contiguous share of the live blocks (balanced on the
   // device, so a replayed launch follows the growing prefix)
   const int nblk_all = (total + BLK_KT - 1) / BLK_KT;

@@ -22,6 +22,8 @@
 
 namespace adt {
 
+ADT_DEVICE_ERROR_WORD(gemm)
+
 // ----------------------------------------------------------------------------- packing
 // bf16 tile layout: tile (nt, kt) holds packed rows nt*16..+15, columns kt*32..+31 as 64
 // lanes x 8 values; lane l = g*16 + i carries W[row(nt*16 + i)][kt*32 + g*8 + e], e = 0..7.
@@ -156,6 +158,10 @@ __device__ __forceinline__ void tile_epilogue(const GemmEpi& e, f32x4 y, const E
           a[r] = x1 * cx - x2 * sx;
           b[r] = x2 * cx + x1 * sx;
         }
+      }
+      if (region > 0 && e.slot_cap > 0 && pre.slot >= e.slot_cap) {   // a row past the cache
+        dev_fail(DEVINV_KV_RANGE);
+        return;
       }
       uint16_t* dst = region == 0 ? e.q + (int64_t)row * d + head * Dh
                                   : (region == 1 ? e.kc : e.vc) + branch * e.cache_sb + head * e.stride_h +

@@ -11,6 +11,8 @@ namespace adt {
 
 constexpr int ROW_THREADS = 256;
 
+ADT_DEVICE_ERROR_WORD(rows)
+
 // h[m] = E[tok[m]] (fp32 residual), a[m] = RMSNorm(h[m]) (raw: h[m] itself) in dtype T
 // (layout a_pk).
 template <typename T>
@@ -435,10 +437,16 @@ __global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__
     if (p < total) {
       const int sl = s0 + p / pps, w = p % pps, m = w / per_row + 1, c = w % per_row;
       if (sl < slices && m <= a) {
+        // the node at depth m of a BFS-ordered tree has an index in [m, ADT_MAX_NODES); an
+        // entry outside is recorded (debug builds) and its row left in place
         const int src = path[(int64_t)b * path_stride + m];
-        const int64_t off = b * stride_b + sl * stride_s + (int64_t)(L + src) * Dh;
-        kr[it] = reinterpret_cast<const u16x8*>(kc + off)[c];
-        vr[it] = reinterpret_cast<const u16x8*>(vc + off)[c];
+        if (src >= m && src < ADT_MAX_NODES) {
+          const int64_t off = b * stride_b + sl * stride_s + (int64_t)(L + src) * Dh;
+          kr[it] = reinterpret_cast<const u16x8*>(kc + off)[c];
+          vr[it] = reinterpret_cast<const u16x8*>(vc + off)[c];
+        } else {
+          dev_fail(DEVINV_PATH);
+        }
       }
     }
   }
@@ -448,7 +456,8 @@ __global__ __launch_bounds__(ROW_THREADS) void kv_compact_kernel(T* __restrict__
     const int p = threadIdx.x + it * ROW_THREADS;
     if (p < total) {
       const int sl = s0 + p / pps, w = p % pps, m = w / per_row + 1, c = w % per_row;
-      if (sl < slices && m <= a) {
+      const int src = (sl < slices && m <= a) ? path[(int64_t)b * path_stride + m] : -1;
+      if (sl < slices && m <= a && src >= m && src < ADT_MAX_NODES) {
         const int64_t off = b * stride_b + sl * stride_s + (int64_t)(L + m) * Dh;
         reinterpret_cast<u16x8*>(kc + off)[c] = kr[it];
         reinterpret_cast<u16x8*>(vc + off)[c] = vr[it];
@@ -489,6 +498,7 @@ __global__ void tree_masks_kernel(const int32_t* __restrict__ parent, const int3
     int dp = 0;
     if (i < n) {
       const int p = par[i];
+      if (i == 0 ? p != -1 : !(p >= 0 && p < i)) dev_fail(DEVINV_PARENT);
       if (i > 0 && p >= 0 && p < i) {
         w0 = mk[p * ADT_MASK_WORDS];
         w1 = mk[p * ADT_MASK_WORDS + 1];

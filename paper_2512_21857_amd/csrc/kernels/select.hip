@@ -17,6 +17,8 @@ namespace adt {
 
 constexpr int SEL_THREADS = 256;
 
+ADT_DEVICE_ERROR_WORD(select)
+
 __device__ __forceinline__ bool better(float a, int ia, float b, int ib) { return a > b || (a == b && ia < ib); }
 
 constexpr int TOPK_THREADS = 256;
@@ -419,6 +421,7 @@ __global__ __launch_bounds__(WAVE) void accept_greedy_kernel(const int32_t* __re
     first[i] = ADT_MAX_NODES;
     if (i < n && i > 0) {
       const int p = parent[i];
+      if (!(p >= 0 && p < i)) dev_fail(DEVINV_PARENT);
       match[h] = p >= 0 && p < i && token[i] == argmax[p * kmax];
       jmp[i] = (p >= 0 && p < i) ? p : -1;
     } else {

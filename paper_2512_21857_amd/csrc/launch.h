@@ -15,6 +15,13 @@ struct Branches {
   int64_t cache_sb = 0;
 };
 
+// Device error words of the source files whose kernels test invariants (debug builds; 0 in
+// release builds): read and cleared, with the current device synchronised by the copy.
+uint32_t dev_errors_take_rows();
+uint32_t dev_errors_take_select();
+uint32_t dev_errors_take_attn();
+uint32_t dev_errors_take_gemm();
+
 // attn.hip
 // Row of query qr of sequence b in q and out: b * rs_b + qr * rs_i (rows of H * Dh); its mask
 // row: b * ms_b + qr.  Separate sequences: (nq_max, 1, nq_max).  Guidance branches of one
@@ -75,6 +82,8 @@ struct GemmEpi {
   int Dh = 0;
   int nb = 1;              // guidance branches: row m is node m / nb of branch m % nb, whose
   int64_t cache_sb = 0;    // caches sit cache_sb elements further; q keeps row m
+  int slot_cap = 0;        // cache slots per head (> 0: rows whose slot would pass it are not
+                           // stored; debug builds record them)
   // EPI_SWIGLU (weights packed with ADT_PACK_GATE_UP): act[m][N/2] = silu(gate) * up, in
   // the fragment layout of act_pk row blocks (0: row-major)
   uint16_t* act = nullptr;

@@ -34,6 +34,18 @@ def test_exports_every_declared_symbol(L):
     assert L.adt_version() == 1
 
 
+def test_debug_build_exports_the_same_symbols(L):
+    """libadt_debug.so (device invariant checks compiled in) has the same ABI; only it
+    reports the checks as enabled."""
+    from paper_2512_21857_amd import abi
+    D = abi.lib_debug()
+    for n in declared_symbols():
+        assert hasattr(D, n), n
+    assert D.adt_device_checks_enabled() == 1
+    assert L.adt_device_checks_enabled() == 0
+    assert abi.E_DEVICE_INVARIANT == -6 and abi.E_STATE == -7
+
+
 def test_argument_errors_return_codes_without_launching(L):
     from paper_2512_21857_amd import abi
     assert L.adt_tree_attn(None, None, None, 0, 0, None, None, None, None, 1, 1, 64, 1, 1, 1.0, 1, None, None, 0,
