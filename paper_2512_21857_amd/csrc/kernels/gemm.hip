@@ -424,7 +424,7 @@ adt_status launch_pack(const void* const* srcs, const int32_t* rows, int n_src, 
 // the whole K per workgroup where that already gives >= 192 workgroups (O 9.1 us and the
 // draft FC 15.5 at 61 rows), except a long K at > 32 rows, which takes T = 4 with about ten
 // k-tiles per wave per range (down at 61 rows: T = 4 S = 4 20.5 us against 28 at S = 1).
-RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
+RowsPlan gemm_rows_plan(int M, int N, int K, bool partial, bool wide) {
   const int mt = (M + 15) / 16, tiles = N / 16, KT = K / 32;
   const int tmax = mt <= 4 ? 4 : 2;
   auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
@@ -433,9 +433,15 @@ RowsPlan gemm_rows_plan(int M, int N, int K, bool partial) {
     // > 32 rows: a multiple of 256 workgroups (whole rounds of the CUs) with at most tmax tiles
     // each, spread evenly (gate/up's 1376 tiles: 512 groups of 2-3, 45 us against 48 with 344
     // groups of 4)
-    if (mt >= 3)
+    if (mt >= 3) {
+      // wide (an epilogue without early inputs, whose registers the accumulators can take):
+      // one round of the CUs with up to six tiles each where that suffices (gate/up: 256
+      // groups of 5-6, 45.7 us against 47.0 with 512 groups of 2-3 at 61 rows, 39.9 against
+      // 43.3 at 40 rows)
+      if (wide && mt <= 4 && (tiles + 255) / 256 >= 5 && (tiles + 255) / 256 <= 6) return {6, 1, 256};
       for (int g = 256; g <= tiles; g += 256)
         if ((tiles + g - 1) / g <= tmax) return {(tiles + g - 1) / g, 1, g};
+    }
     for (int t : {4, 3, 2}) {
       if (!ok(t) || tiles / t < 256) continue;
       if (t <= 2 || tiles / t == 256 || (mt == 2 && tiles / t >= 1024)) return {t, 1, tiles / t};
@@ -488,7 +494,8 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
   ADT_CHECK_ARG(epi.norm_eps == 0.f || (epi.norm_eps > 0.f && epi.mode != EPI_PART && epi.mode != EPI_RESID),
                 ADT_E_ARG, "gemm: the input norm needs one K range");
   // the residual epilogue takes the residual projections' plan, which must keep one K range
-  const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART || epi.mode == EPI_RESID);
+  const RowsPlan p = gemm_rows_plan(M, N, K, epi.mode == EPI_PART || epi.mode == EPI_RESID,
+                                    epi.mode == EPI_STORE || epi.mode == EPI_SWIGLU);
   ADT_CHECK_ARG(epi.mode != EPI_RESID || p.S == 1, ADT_E_ARG, "gemm: residual epilogue with %d K ranges", p.S);
   ADT_CHECK_ARG(epi.mode != EPI_PART || (size_t)p.S * M * N <= epi.part_elems, ADT_E_CAPACITY,
                 "gemm: %d K-range sums of %d x %d exceed the partial buffer", p.S, M, N);
@@ -524,6 +531,12 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     case 2: ADT_GR(MTV, 2, KCV); break;  \
     default: ADT_GR(MTV, 1, KCV); break; \
   }
+#define ADT_GR_T6(MTV, KCV)  \
+  if (p.T == 6) {            \
+    ADT_GR(MTV, 6, 1);       \
+  } else {                   \
+    ADT_GR_T4(MTV, KCV)      \
+  }
 #define ADT_GR_T2(MTV, KCV)              \
   if (p.T >= 2) {                        \
     ADT_GR(MTV, 2, KCV);                 \
@@ -533,13 +546,14 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
   switch (mt) {
     case 1: ADT_GR_T4(1, 3) break;
     case 2: ADT_GR_T4(2, 2) break;
-    case 3: ADT_GR_T4(3, 2) break;
-    case 4: ADT_GR_T4(4, 2) break;
+    case 3: ADT_GR_T6(3, 2) break;
+    case 4: ADT_GR_T6(4, 2) break;
     case 5:
     case 6: ADT_GR_T2(6, 2) break;
     default: ADT_GR_T2(8, 2) break;
   }
 #undef ADT_GR_T2
+#undef ADT_GR_T6
 #undef ADT_GR_T4
 #undef ADT_GR
 #undef ADT_GR_L

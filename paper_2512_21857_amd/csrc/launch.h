@@ -101,7 +101,7 @@ struct RowsPlan {
   int T, S;       // at most T 16-column tiles per workgroup, S K ranges
   int G;          // column groups: group c takes tiles [c tiles / G, (c + 1) tiles / G)
 };
-RowsPlan gemm_rows_plan(int M, int N, int K, bool partial);
+RowsPlan gemm_rows_plan(int M, int N, int K, bool partial, bool wide = false);
 constexpr int GEMM_MAX_SPLITS = 8;
 // fp32: part[M][N] = X . W^T (consumed by the row kernels).  bf16: the kernel above with the
 // epilogue epi; *splits (if given) gets S.  bf16 X is row-major with leading dimension ldx, or
