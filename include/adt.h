@@ -382,7 +382,7 @@ typedef struct {
   int32_t step;                 /* next cycle index */
   int32_t n_tokens;             /* committed tokens, prompt included */
   int32_t n_nodes;              /* rows of the current tree */
-  float* logits;                /* [ADT_MAX_NODES][vocab] last verify logits (unmasked) */
+  float* logits;                /* [ADT_MAX_NODES][vocab] last verify logits (unmasked; columns below) */
   void* feat;                   /* [ADT_MAX_NODES][d_model] last verify features */
   float* draft_logits;          /* [1 + (d_hi-1) k_hi][vocab] root row then frontier rows, per level */
   int32_t* parent; int32_t* token; int32_t* depth; float* score; uint64_t* mask;  /* current tree */
@@ -403,6 +403,11 @@ typedef struct {
   int32_t n_branches;
   float* branch_logits;         /* guided: [n][2][vocab] per-branch verify logits, else NULL */
   float* draft_branch_logits;   /* guided: [2][vocab] per-branch logits of the draft root row, else NULL */
+  /* columns [logits_lo, logits_hi) of every logits row above are computed; the others are left
+   * as they were.  bf16 sessions: the union of the image cells' allowed ranges, widened to
+   * multiples of 16 (every step of the cycle reads a row's allowed range only); f32: the
+   * whole vocabulary. */
+  int32_t logits_lo, logits_hi;
 } adt_session_view;
 
 size_t adt_session_workspace_size(const adt_model* m, const adt_session_desc* desc);

@@ -72,7 +72,7 @@ class SessionView(C.Structure):
                 ("logits", p), ("feat", p), ("draft_logits", p), ("parent", p), ("token", p), ("depth", p),
                 ("score", p), ("mask", p), ("allowed_rows", p), ("path", p), ("n_acc", p), ("bonus", p),
                 ("tokens_host", ip), ("q", p), ("att", p), ("act", p), ("resid", p), ("n_branches", i32),
-                ("branch_logits", p), ("draft_branch_logits", p)]
+                ("branch_logits", p), ("draft_branch_logits", p), ("logits_lo", i32), ("logits_hi", i32)]
 
 
 class Capture(C.Structure):

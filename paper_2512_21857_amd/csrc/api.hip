@@ -531,6 +531,10 @@ struct adt_session_s {
   bool expanded = false;   // the current tree came from adt_tree_expand (draft root row written)
   int L = 0, Ld = 0, step = 1, n_nodes = 0;
   std::vector<int32_t> tokens, allowed_h, poisson;
+  // vocabulary columns [lm_lo, lm_hi) the bf16 LM head computes: the union of the image
+  // cells' allowed ranges, widened to whole 16-row weight tiles (every consumer of the logits
+  // reads a cell's allowed range only)
+  int lm_lo = 0, lm_hi = 0;
   std::vector<int32_t> rec_d, rec_k, has_rec;
   bool have_prev = false;
   int a_prev = 0, d_prev = 0, prev_cell = 0;
@@ -734,6 +738,18 @@ extern "C" adt_status adt_session_create(const adt_model* m, const adt_session_d
   session_layout(s, (char*)d->workspace);
   s->graphs = d->use_graphs != 0;
   s->allowed_h.assign(d->allowed, d->allowed + 2 * d->n_image);
+  s->lm_lo = s->V;
+  s->lm_hi = 0;
+  for (int c = 0; c < d->n_image; ++c) {
+    s->lm_lo = std::min(s->lm_lo, (int)s->allowed_h[2 * c]);
+    s->lm_hi = std::max(s->lm_hi, (int)s->allowed_h[2 * c + 1]);
+  }
+  s->lm_lo = std::max(0, s->lm_lo / 16 * 16);
+  s->lm_hi = std::min(s->V, (s->lm_hi + 15) / 16 * 16);
+  if (s->dt != ADT_BF16 || s->lm_lo >= s->lm_hi) {
+    s->lm_lo = 0;
+    s->lm_hi = s->V;
+  }
   if (d->poisson) s->poisson.assign(d->poisson, d->poisson + d->n_image);
   s->rec_d.assign(d->n_image, 0);
   s->rec_k.assign(d->n_image, 0);
@@ -1016,11 +1032,13 @@ static adt_status lm_head(adt_session_s* s, const void* feat_rows, int ldx, int 
   const int rows = s->nb * M;
   float* dst = s->nb > 1 ? raw : out;
   if (s->dt == ADT_BF16) {
+    // columns [lm_lo, lm_hi) only: their packed weight rows start lm_lo * d_model elements in
     GemmEpi e;
     e.mode = EPI_STORE;
-    e.out = dst;
+    e.out = dst + s->lm_lo;
     e.ldo = s->V;
-    TRY(gemm_p(feat_rows, ldx, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st, e));
+    const void* w = (const uint16_t*)s->m->d.lm_head + (size_t)s->lm_lo * s->dm;
+    TRY(gemm_p(feat_rows, ldx, w, rows, s->lm_hi - s->lm_lo, s->dm, s->dt, s->part, st, e));
   } else {
     TRY(gemm_p(feat_rows, s->dm, s->m->d.lm_head, rows, s->V, s->dm, s->dt, s->part, st));
     TRY(launch_reduce_store(s->part, 1, rows, s->V, dst, s->V, st));
@@ -1808,5 +1826,7 @@ extern "C" adt_status adt_session_get_view(const adt_session* s, adt_session_vie
   v->n_branches = s->nb;
   v->branch_logits = s->rawlog;
   v->draft_branch_logits = s->draw;
+  v->logits_lo = s->lm_lo;
+  v->logits_hi = s->lm_hi;
   return ADT_OK;
 }

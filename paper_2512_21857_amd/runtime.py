@@ -457,6 +457,7 @@ class DeviceSession:
             "path": self._ws(v.path, n, torch.int32), "n_acc": self._ws(v.n_acc, 1, torch.int32),
             "bonus": self._ws(v.bonus, 1, torch.int32),
             "tokens": [v.tokens_host[i] for i in range(v.n_tokens)],
+            "logits_range": (v.logits_lo, v.logits_hi),
         }
         if nb == 2:
             out["branch_logits"] = self._ws(v.branch_logits, n * 2 * m.vocab, torch.float32).view(n, 2, m.vocab)

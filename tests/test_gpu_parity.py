@@ -177,11 +177,13 @@ def check_forward(rep, om, sess, rec, what, nb=1):
     return out
 
 
-def check_head(rep, om, feat_gpu, logits_gpu, f_ref, what, scale=None, branch_logits=None):
+def check_head(rep, om, feat_gpu, logits_gpu, f_ref, what, scale=None, branch_logits=None, cols=None):
     """Final features (per branch) against the oracle's norm of the GPU's final residual;
-    logits against the oracle's LM head applied to the GPU's own features.  With guidance the
-    per-branch logits (when given) are checked, and the guided logits l_u + s (l_c - l_u)
-    against the branch logits' combination within the propagated bound (|1 - s| + s) tol."""
+    logits against the oracle's LM head applied to the GPU's own features, over the vocabulary
+    columns cols = (lo, hi) the session computes (the union of the cells' allowed ranges).
+    With guidance the per-branch logits (when given) are checked, and the guided logits
+    l_u + s (l_c - l_u) against the branch logits' combination within the propagated bound
+    (|1 - s| + s) tol."""
     nb = len(f_ref)
     base = []
     for b in range(nb):
@@ -192,7 +194,11 @@ def check_head(rep, om, feat_gpu, logits_gpu, f_ref, what, scale=None, branch_lo
             base.append(f_ref[b])
     if logits_gpu is None:
         return
-    lb = [x @ om.w("lm_head").T for x in base]
+    lo, hi = cols if cols is not None else (0, logits_gpu.shape[-1])
+    lb = [(x @ om.w("lm_head").T)[..., lo:hi] for x in base]
+    logits_gpu = logits_gpu[..., lo:hi]
+    if branch_logits is not None:
+        branch_logits = [x[..., lo:hi] for x in branch_logits]
     if nb == 1:
         rep.check("logits", logits_gpu, lb[0], what)
         return
@@ -339,7 +345,8 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None, fixed_tree=Fal
     bl = f64(_ws_rows(sess, v.branch_logits, nb, V, torch.float32)) if guided else None
     check_head(rep, om, [feat[:, b] for b in range(nb)], None, f_ref, "prefill")
     check_head(rep, om, [feat[cn - 1: cn, b] for b in range(nb)], lg[0:1], [f[cn - 1: cn] for f in f_ref],
-               "prefill last row", gs, None if bl is None else [bl[b: b + 1] for b in range(nb)])
+               "prefill last row", gs, None if bl is None else [bl[b: b + 1] for b in range(nb)],
+               cols=(v.logits_lo, v.logits_hi))
     gfeat = [{} for _ in range(nb)]   # GPU target features (bf16 values as float64) per committed position
     for r in range(cn):
         for b in range(nb):
@@ -389,11 +396,12 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None, fixed_tree=Fal
             dl = f64(t["draft_logits"])
             dbl = f64(t["draft_branch_logits"]) if guided else None
             check_head(rep, om, None, dl[0:1], [f[-1:] for f in fr], f"cycle {cyc} draft root", gs,
-                       None if dbl is None else [dbl[b: b + 1] for b in range(nb)])
+                       None if dbl is None else [dbl[b: b + 1] for b in range(nb)], cols=t["logits_range"])
             for li, r in enumerate(drecs[1:]):
                 fr = check_forward(rep, om, sess, r, f"cycle {cyc} draft level {li + 2}", nb)
                 base = 1 + li * cfg.sched.k_hi
-                check_head(rep, om, None, dl[base: base + r["nodes"]], fr, f"cycle {cyc} draft level {li + 2}", gs)
+                check_head(rep, om, None, dl[base: base + r["nodes"]], fr, f"cycle {cyc} draft level {li + 2}", gs,
+                           cols=t["logits_range"])
             crossfed_expand(rep, cfg, t, drecs[1:], L, tokens[L], d_hat, k_hat, cfg.sched.n_budget, P)
         else:
             sess.set_tree([-1], [tokens[L]])
@@ -408,7 +416,7 @@ def run_parity(rt, cfg, dm, om, n_cycles, poisson=None, knn=None, fixed_tree=Fal
         logits32 = t["logits"].cpu().numpy()
         vbl = f64(t["branch_logits"]) if guided else None
         check_head(rep, om, [feat[:, b] for b in range(nb)], logits32.astype(np.float64), f_ref, f"cycle {cyc} verify",
-                   gs, None if vbl is None else [vbl[:, b] for b in range(nb)])
+                   gs, None if vbl is None else [vbl[:, b] for b in range(nb)], cols=t["logits_range"])
         parent = t["parent"].cpu().numpy()
         token = t["token"].cpu().numpy()
         depth = t["depth"].cpu().numpy()
