@@ -533,6 +533,14 @@ adt_status adt_profile_enable(int32_t on);
 size_t adt_probe_sink_bytes(void);
 adt_status adt_probe_hbm_read(const void* buf, size_t bytes, void* sink, size_t sink_bytes, void* stream);
 adt_status adt_probe_mfma(int32_t iters, void* sink, size_t sink_bytes, double* flops, void* stream);
+/* The integer weights the sampling kernels (exact, relaxed and stochastic-children modes,
+ * Sec. 3.1 Eq. 1) give to float32 exponents d = z - max z: w[i] = rint(exp(d[i]) * 2^32)
+ * with exp evaluated by a fixed sequence of IEEE double operations (y = d log2 e, k = floor y,
+ * f = y - k, 2^f by Horner's rule over the doubles nearest ln(2)^j / j!, j = 13..0, no fused
+ * multiply-add), 0 for d < -40 or NaN.  Exposed so that a reference of the same definition
+ * can be compared with the device's integers.  d, w: [n] device arrays; asynchronous on
+ * `stream`; ADT_E_ARG for null pointers or n < 0. */
+adt_status adt_probe_sample_weights(const float* d, int64_t n, uint64_t* w, void* stream);
 adt_status adt_profile_read(int32_t cls, int64_t* launches, double* ms, double* bytes, double* flops, int32_t reset);
 
 #ifdef __cplusplus

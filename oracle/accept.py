@@ -21,9 +21,11 @@ reduces it to exact mode.
 If a rejection empties the truncated support (possible when top_k is small) the bonus is
 the top-1 id of p.
 
-Numbers: p is quantised once per row to integer weights w = rint(exp(z - max z) * 2^32)
-with z = logit / T over the top-K allowed ids, computed in float32 (the precision the
-kernel decides in); all later arithmetic is exact integer.  A draw is
+Numbers: p is quantised once per row to integer weights w = rint(exp(d) * 2^32), d = z - max z
+with z = logit / T over the top-K allowed ids (z and d in float32, the precision the kernel
+decides in), and exp(d) evaluated by a fixed sequence of IEEE double operations
+(quantised_exp_weight), so that the integers do not depend on any library's exp; all later
+arithmetic is exact integer.  A draw is
 r = floor(U * W / 2^64) with U the 64 bits of Philox4x32-10 at key = seed and
 counter = (step, node, trial, 0), and W the remaining total weight.
 
@@ -46,9 +48,47 @@ from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
 
+from decimal import Decimal, getcontext
+
 from .numerics import draw_below, uniform_u64
 
 DELTA_FRAC_BITS = 16
+
+
+def _exp2_coefficients(n: int = 14) -> Tuple[List[float], float]:
+    """The doubles nearest ln(2)^j / j! (j < n), the Taylor coefficients of 2^f = e^(f ln 2),
+    and the double nearest log2(e), from 60-digit decimal arithmetic (Decimal -> float rounds
+    to nearest)."""
+    getcontext().prec = 60
+    ln2 = Decimal(2).ln()
+    coef, fact = [], Decimal(1)
+    for j in range(n):
+        if j:
+            fact *= j
+        coef.append(float(ln2 ** j / fact))
+    return coef, float(Decimal(1) / ln2)
+
+
+EXP2_COEF, LOG2E = _exp2_coefficients()
+
+
+def quantised_exp_weight(d: np.ndarray) -> np.ndarray:
+    """w = rint(exp(d) * 2^32) for float32 exponents d <= 0, as float64 integers: y = d log2(e),
+    k = floor(y), f = y - k in [0, 1), 2^f by Horner's rule over EXP2_COEF (degree 13, each
+    step one rounded multiply then one rounded add), exp(d) = 2^f 2^k; d < -40 gives 0
+    (exp(d) 2^32 < 2^-25).  Every step is an IEEE double operation, so an implementation that
+    follows the same sequence without fused multiply-adds gets the same integers."""
+    d64 = np.asarray(d, dtype=np.float32).astype(np.float64)
+    live = d64 >= -40.0
+    y = np.where(live, d64, 0.0) * LOG2E
+    k = np.floor(y)
+    f = y - k
+    p = np.full_like(f, EXP2_COEF[-1])
+    for c in EXP2_COEF[-2::-1]:
+        p = p * f
+        p = p + c
+    w = np.rint(np.ldexp(p, (k + 32).astype(np.int64)))
+    return np.where(live, w, 0.0)
 
 
 def codebook_knn(codebook: np.ndarray, k: int) -> np.ndarray:
@@ -102,7 +142,7 @@ def accept_greedy(logits: np.ndarray, parent, token, allowed) -> Tuple[List[int]
 def quantised_weights(logit_row: np.ndarray, lo: int, hi: int, temperature: float, top_k: int) -> np.ndarray:
     """Integer weights (Python ints in an object array) of the sampling distribution p at
     one row: softmax(logit / T) over the allowed ids, truncated to the top_k ids by
-    (logit desc, id asc), as w = rint(exp(z - max z) * 2^32) in float32."""
+    (logit desc, id asc), as w = quantised_exp_weight(z - max z) with z in float32."""
     V = len(logit_row)
     z = np.asarray(logit_row[lo:hi], dtype=np.float32) / np.float32(temperature)
     ids = np.arange(lo, hi)
@@ -110,8 +150,7 @@ def quantised_weights(logit_row: np.ndarray, lo: int, hi: int, temperature: floa
     if top_k > 0:
         keep = keep[:top_k]
     zmax = z[keep].max()
-    e = np.exp(z[keep] - zmax)                              # float32
-    wq = np.rint(e.astype(np.float64) * 4294967296.0)       # e * 2^32 is exact in float64
+    wq = quantised_exp_weight(z[keep] - zmax)               # float32 exponents
     w = np.zeros(V, dtype=object)
     w[:] = 0
     for i, val in zip(ids[keep], wq):

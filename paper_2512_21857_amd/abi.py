@@ -128,6 +128,7 @@ _SIGS = {
     "adt_probe_sink_bytes": (sz, []),
     "adt_probe_hbm_read": (i32, [p, sz, p, sz, p]),
     "adt_probe_mfma": (i32, [i32, p, sz, C.POINTER(C.c_double), p]),
+    "adt_probe_sample_weights": (i32, [p, C.c_int64, p, p]),
     "adt_profile_read": (i32, [i32, C.POINTER(i64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                C.POINTER(C.c_double), i32]),
 }

@@ -124,6 +124,34 @@ __device__ __forceinline__ float xor16_add(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Sampling weight w = rint(exp(d) * 2^32) of a float32 exponent d = z - max z <= 0, with
+// exp(d) evaluated by a fixed sequence of IEEE double operations and no fused multiply-add,
+// so that any implementation following the same sequence gets the same integer: y = d log2(e),
+// k = floor(y), f = y - k, 2^f by Horner's rule over the doubles nearest ln(2)^j / j!
+// (j = 13 .. 0), exp(d) = 2^f 2^k; d < -40 gives 0 (exp(d) 2^32 < 2^-25 there).
+__device__ inline uint64_t quantised_exp_weight(float d) {
+#pragma clang fp contract(off)
+  if (!(d >= -40.f)) return 0;
+  const double y = (double)d * 0x1.71547652b82fep+0;
+  const double k = floor(y);
+  const double f = y - k;
+  double p = 0x1.816193166d0f9p-40;
+  p = p * f + 0x1.c3bd650fc2986p-36;
+  p = p * f + 0x1.e8cac7351bb25p-32;
+  p = p * f + 0x1.e4cf5158b8ecap-28;
+  p = p * f + 0x1.b5253d395e7c4p-24;
+  p = p * f + 0x1.62c0223a5c824p-20;
+  p = p * f + 0x1.ffcbfc588b0c7p-17;
+  p = p * f + 0x1.430912f86c787p-13;
+  p = p * f + 0x1.5d87fe78a6731p-10;
+  p = p * f + 0x1.3b2ab6fba4e77p-7;
+  p = p * f + 0x1.c6b08d704a0c0p-5;
+  p = p * f + 0x1.ebfbdff82c58fp-3;
+  p = p * f + 0x1.62e42fefa39efp-1;
+  p = p * f + 0x1.0p+0;
+  return (uint64_t)rint(ldexp(p, (int)k + 32));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);

@@ -8,8 +8,9 @@
 // stays within delta of the remaining total, and removes the credited set on rejection.
 //
 // p at a row is held as integer weights w = rint(exp(z - max z) * 2^32) over the top_k
-// allowed ids (z = logit / T, fp32); every later operation is exact integer arithmetic,
-// so the walk does not depend on summation order.  One workgroup per tree: the weights of
+// allowed ids (z = logit / T and z - max z in fp32, exp(.) by the fixed double sequence of
+// quantised_exp_weight, so the integers do not depend on a math library); every later
+// operation is exact integer arithmetic, so the walk does not depend on summation order.  One workgroup per tree: the weights of
 // a row are built cooperatively (64-bit radix select for the top-k threshold, block
 // reductions), the sibling walk runs on one lane, the bonus is found by a block-wide
 // prefix scan over ids in ascending order.
@@ -109,7 +110,7 @@ __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T,
   return prefix;
 }
 
-// Integer weights w[i] = rint(exp(z_i - max z) * 2^32), z = x[i] / T, over the top_k ids of
+// Integer weights w[i] = quantised_exp_weight(z_i - max z), z = x[i] / T, over the top_k ids of
 // [lo, hi) by (z desc, id asc) (all of them when top_k is 0 or covers the range), zero
 // elsewhere in [0, V); returns their total.  Every thread must call it.
 __device__ uint64_t build_weights(const float* x, int lo, int hi, int V, float T, int top_k, uint64_t* w,
@@ -129,10 +130,7 @@ __device__ uint64_t build_weights(const float* x, int lo, int hi, int V, float T
     uint64_t wi = 0;
     if (i >= lo && i < hi) {
       const float z = x[i] / T;
-      if (zkey(z, i) >= thr) {
-        const float e = expf(z - zm);
-        wi = (uint64_t)rint((double)e * 4294967296.0);
-      }
+      if (zkey(z, i) >= thr) wi = quantised_exp_weight(z - zm);
     }
     w[i] = wi;
     part += wi;

@@ -65,9 +65,24 @@ __global__ __launch_bounds__(PROBE_THREADS) void probe_mfma_kernel(int iters, fl
   sink[(int64_t)blockIdx.x * PROBE_THREADS + threadIdx.x] = s;
 }
 
+__global__ __launch_bounds__(PROBE_THREADS) void probe_weight_kernel(const float* __restrict__ d, int64_t n,
+                                                                      uint64_t* __restrict__ w) {
+  for (int64_t i = blockIdx.x * (int64_t)PROBE_THREADS + threadIdx.x; i < n; i += (int64_t)gridDim.x * PROBE_THREADS)
+    w[i] = quantised_exp_weight(d[i]);
+}
+
 }  // namespace adt
 
 using namespace adt;
+
+extern "C" adt_status adt_probe_sample_weights(const float* d, int64_t n, uint64_t* w, void* stream) {
+  ADT_CHECK_ARG(d && w && n >= 0, ADT_E_ARG, "probe_sample_weights: bad arguments");
+  if (n == 0) return ADT_OK;
+  const int64_t blocks = std::min<int64_t>((n + PROBE_THREADS - 1) / PROBE_THREADS, 4096);
+  probe_weight_kernel<<<(unsigned)blocks, PROBE_THREADS, 0, (hipStream_t)stream>>>(d, n, w);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
 
 extern "C" size_t adt_probe_sink_bytes(void) {
   return sizeof(float) * (size_t)PROBE_MFMA_BLOCKS * PROBE_THREADS;

@@ -423,3 +423,23 @@ def test_gemm_bf16_batched_verify_shape_sampled(rt):
     got = rt.gemm_bf16(xt, wt).cpu().numpy()
     rows = np.array([0, 1, 31, 32, 255, 256, 511, 767, 768, 900, 975])
     _gemm_ref_check(got, xt.float().cpu().numpy(), wt.float().cpu().numpy(), rows)
+
+
+def test_sample_weights_match_oracle(rt):
+    """The device's sampling weights w = rint(exp(d) 2^32) against the oracle's definition of
+    the same fixed double sequence, bit for bit: every float32 exponent on a dense grid of
+    [-45, 0], random ones, and the edges (0, -0, the -40 cut and its neighbours, -inf)."""
+    from oracle.accept import quantised_exp_weight
+    rng = np.random.default_rng(14)
+    edge = np.array([0.0, -0.0, -40.0, np.nextafter(np.float32(-40.0), np.float32(0.0)),
+                     np.nextafter(np.float32(-40.0), np.float32(-50.0)), -1e-30, -np.inf], dtype=np.float32)
+    d = np.concatenate([(-np.linspace(0.0, 45.0, 2_000_001)).astype(np.float32),
+                        (-rng.random(1_000_000) * 45.0).astype(np.float32), edge])
+    dd = torch.from_numpy(d).cuda()
+    w = torch.empty(d.size, dtype=torch.int64, device="cuda")
+    rt.check(rt.lib().adt_probe_sample_weights(rt._p(dd), d.size, rt._p(w), rt._stream()))
+    torch.cuda.synchronize()
+    got = w.cpu().numpy()
+    ref = quantised_exp_weight(d).astype(np.int64)
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, f"{bad.size} weights differ, first at d = {d[bad[:4]]}: {got[bad[:4]]} vs {ref[bad[:4]]}"

@@ -181,3 +181,31 @@ def test_codebook_knn_by_angle():
         d = np.abs((theta - theta[x] + np.pi) % (2 * np.pi) - np.pi)
         d[x] = np.inf
         assert knn[x, 0] == x and list(knn[x, 1:]) == list(np.argsort(d, kind="stable")[:3])
+
+
+def test_quantised_exp_weight_is_rounded_exp():
+    """The weights' exp (a fixed sequence of double operations) against the platform's
+    float64 exp: w = rint(exp(d) 2^32) on a dense grid of float32 exponents in [-45, 0], apart
+    from values within 1e-4 of a rounding tie; w(0) = 2^32, w = 0 below -40 and for -inf,
+    and w never increases as d decreases."""
+    import math
+    d = (-np.linspace(0.0, 45.0, 1_500_001)).astype(np.float32)
+    w = acc.quantised_exp_weight(d)
+    ref = np.array([math.exp(float(x)) for x in d[::7]]) * 2.0 ** 32
+    wr = w[::7]
+    tie = np.abs(ref - np.floor(ref) - 0.5) < 1e-4
+    assert np.all((wr == np.rint(ref)) | tie)
+    assert np.all((wr == 0) == (d[::7] < -40) | (np.rint(ref) == 0))
+    assert w[0] == 2.0 ** 32 and np.all(np.diff(w) <= 0)
+    assert acc.quantised_exp_weight(np.float32([-np.inf, -40.5]))[:2].tolist() == [0.0, 0.0]
+
+
+def test_quantised_exp_coefficients():
+    """The Horner coefficients are ln(2)^j / j! and log2(e), to the last bit of a double
+    (checked against the math module's ln 2, an independent route to the same values)."""
+    import math
+    for j, c in enumerate(acc.EXP2_COEF):
+        exact = math.log(2.0) ** j / math.factorial(j)
+        assert abs(c - exact) <= 4 * math.ulp(exact), j
+    assert acc.LOG2E == 1.0 / math.log(2.0) or abs(acc.LOG2E - 1.0 / math.log(2.0)) <= math.ulp(acc.LOG2E)
+    assert len(acc.EXP2_COEF) == 14
