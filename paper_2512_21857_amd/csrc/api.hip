@@ -634,15 +634,18 @@ static size_t session_layout(adt_session_s* s, char* base) {
     s->draw = b.take<float>((size_t)s->nb * (1 + s->KR) * s->V);
   }
   TreeBufs& t = s->tr;
+  // path, tree tokens, accepted count and bonus are adjacent in the order of the host staging
+  // (path [R], tokens [R], a, bonus), so one copy reads back an acceptance
+  int32_t* acc = b.take<int32_t>(2 * R + 8);
+  t.path = acc;
+  t.token = acc + R;
+  t.nacc = acc + 2 * R;
+  t.bonus = acc + 2 * R + 1;
   t.parent = b.take<int32_t>(R);
-  t.token = b.take<int32_t>(R);
   t.depth = b.take<int32_t>(R);
   t.pos = b.take<int32_t>(R);
   t.allowed_rows = b.take<int32_t>(2 * R);
   t.n = b.take<int32_t>(4);
-  t.path = b.take<int32_t>(R);
-  t.nacc = b.take<int32_t>(4);
-  t.bonus = b.take<int32_t>(4);
   t.score = b.take<float>(R);
   t.mask = b.take<uint64_t>(2 * R);
   t.qrow = b.take<int32_t>(R);
@@ -1287,32 +1290,29 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
   // catch-up rows: committed positions Ld..L, the root last
   const int cu = L - Ld + 1;
   ADT_CHECK_ARG(cu >= 1 && cu <= std::min(32, s->C0), ADT_E_STATE, "tree_expand: %d catch-up rows", cu);
-  std::vector<int32_t> ctok(s->tokens.begin() + Ld, s->tokens.begin() + L + 1), cf(cu);
-  for (int i = 0; i < cu; ++i) cf[i] = i;
+  std::vector<int32_t> ctok(s->tokens.begin() + Ld, s->tokens.begin() + L + 1);
   const bool table = s->d.draft_table != nullptr;
   const int trows = s->d.draft_table_rows;
-  TRY(launch_set_i32(s->ctok, small_of(ctok.data(), cu), cu, st));
   if (table) {
+    TRY(launch_set_i32(s->ctok, small_of(ctok.data(), cu), cu, st));
     TRY(launch_table_rows(s->ctok + (cu - 1), 1, 0, trows, s->idx, st));
     TRY(launch_gather_rows(s->d.draft_table, s->idx, 1, V, s->dlogits, ADT_F32, st));
   } else {
-    TRY(launch_set_i32(s->cfsrc, small_of(cf.data(), cu), cu, st));
-    TRY(launch_iota(s->cpos, cu, Ld, 1, st));
-    TRY(launch_chain_masks(s->cmask, cu, st));
+    TRY(launch_catchup_rows(small_of(ctok.data(), cu), cu, Ld, s->ctok, s->cfsrc, s->cpos, s->cmask, st));
     TRY(draft_forward(s, s->ctok, s->cfsrc, s->cfeat, cu, s->cpos, Ld, Ld, cu, s->cmask, s->dfeat, cu - 1, 1,
                       s->dlogits, s->draw, st, gkey(2, 0, 0, cu)));
   }
   int lo, hi;
   cell_range(s, L + 1 - P, lo, hi);
-  TRY(launch_fill_pairs(s->allowed_lvl, 1, lo, hi, st));
   if (s->d.accept.mode == ADT_ACCEPT_MSS) {
     ADT_CHECK_ARG(n_budget >= s->d.accept.children, ADT_E_ARG, "tree_expand: n_budget %d below the %d children of one node",
                   n_budget, s->d.accept.children);
+    TRY(launch_fill_pairs(s->allowed_lvl, 1, lo, hi, st));
     return expand_sampled(s, d_hat, k_hat, n_budget, cu, table, n_nodes_out, st);
   }
   // layer 1: the root's top-k children
-  TRY(launch_row_topk(s->dlogits, V, V, s->allowed_lvl, 1, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
-                      s->topk_ws_bytes, st));
+  TRY(launch_row_topk(s->dlogits, V, V, nullptr, 1, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
+                      s->topk_ws_bytes, st, lo, hi));
   int cnt = std::min(k_hat, hi - lo);
   TRY(launch_expand_level(s->pool, nullptr, 1, cnt, 0, 1, k_hat, s->top_id, s->top_val, s->lse, 16, d_hat > 1 ? 1 : 0,
                           L, 0, cu - 1, s->C0, 1, s->nx[0], st));
@@ -1330,9 +1330,8 @@ extern "C" adt_status adt_tree_expand(adt_session* s, int32_t d_hat, int32_t k_h
                         st, gkey(3, lvl, nf, drow)));
     }
     cell_range(s, L + lvl - P, lo, hi);
-    TRY(launch_fill_pairs(s->allowed_lvl, nf, lo, hi, st));
-    TRY(launch_row_topk(lrows, V, V, s->allowed_lvl, nf, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
-                        s->topk_ws_bytes, st));
+    TRY(launch_row_topk(lrows, V, V, nullptr, nf, k_hat, 16, s->top_id, s->top_val, s->lse, s->topk_ws,
+                        s->topk_ws_bytes, st, lo, hi));
     cnt = std::min(k_hat, hi - lo);
     TRY(launch_expand_level(s->pool, s->nx[cur].frontier, nf, cnt, pool_n, lvl, k_hat, s->top_id, s->top_val, s->lse,
                             16, lvl < d_hat ? 1 : 0, L, drow + nf, cu - 1, s->C0, 1 + (lvl - 1) * c.k_hi,
@@ -1401,10 +1400,7 @@ static adt_status accept_launch(adt_session_s* s, hipStream_t st) {
   const int n = s->n_nodes;
   TRY(accept_impl(s->logits, s->V, s->V, s->tr.parent, s->tr.token, s->tr.allowed_rows, s->tr.n, n, session_accept_cfg(s),
                   (uint64_t)s->step, s->tr.path, s->tr.nacc, s->tr.bonus, s->acc_ws, s->acc_ws_bytes, st));
-  ADT_HIP(hipMemcpyAsync(s->h_acc, s->tr.path, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(s->h_acc + R, s->tr.token, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(s->h_acc + 2 * R, s->tr.nacc, sizeof(int32_t), hipMemcpyDeviceToHost, st));
-  ADT_HIP(hipMemcpyAsync(s->h_acc + 2 * R + 1, s->tr.bonus, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+  ADT_HIP(hipMemcpyAsync(s->h_acc, s->tr.path, sizeof(int32_t) * (2 * R + 2), hipMemcpyDeviceToHost, st));
   return ADT_OK;
 }
 

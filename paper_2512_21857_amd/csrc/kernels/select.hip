@@ -79,15 +79,16 @@ __device__ __forceinline__ void wave_select(float (&vals)[N], int (&ids)[N], int
 // argmax) short; one workgroup per row ran them over 64 values per lane on a few CUs.
 template <int KMAX>
 __global__ __launch_bounds__(TOPK_THREADS) void topk_chunk_kernel(const float* __restrict__ logits, int64_t ld, int V,
-                                                                  const int32_t* __restrict__ allowed, int k,
-                                                                  float* __restrict__ cand_v,
+                                                                  const int32_t* __restrict__ allowed, int ulo,
+                                                                  int uhi, int k, float* __restrict__ cand_v,
                                                                   int* __restrict__ cand_i,
                                                                   float2* __restrict__ cand_ms) {
   __shared__ float wv[TOPK_WAVES][KMAX];
   __shared__ int wi[TOPK_WAVES][KMAX];
   const int chunk = blockIdx.x, G = gridDim.x, row = blockIdx.y;
   const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
-  const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
+  const int lo = max(0, min(allowed ? allowed[row * 2] : ulo, V));
+  const int hi = max(lo, min(allowed ? allowed[row * 2 + 1] : uhi, V));
   const float* x = logits + (int64_t)row * ld;
   const bool vec = ((ld & 3) == 0);
   float r[8];
@@ -153,12 +154,13 @@ template <int KMAX>
 __global__ __launch_bounds__(WAVE) void topk_merge_kernel(const float* __restrict__ cand_v,
                                                           const int* __restrict__ cand_i,
                                                           const float2* __restrict__ cand_ms, int G, int V,
-                                                          const int32_t* __restrict__ allowed, int k,
-                                                          int32_t* __restrict__ top_id, float* __restrict__ top_val,
+                                                          const int32_t* __restrict__ allowed, int ulo, int uhi,
+                                                          int k, int32_t* __restrict__ top_id, float* __restrict__ top_val,
                                                           float* __restrict__ lse) {
   constexpr int N = TOPK_MAX_CHUNKS * KMAX / WAVE > 0 ? TOPK_MAX_CHUNKS * KMAX / WAVE : 1;
   const int row = blockIdx.x, lane = threadIdx.x;
-  const int lo = max(0, min(allowed[row * 2], V)), hi = max(lo, min(allowed[row * 2 + 1], V));
+  const int lo = max(0, min(allowed ? allowed[row * 2] : ulo, V));
+  const int hi = max(lo, min(allowed ? allowed[row * 2 + 1] : uhi, V));
   const int kk = min(k, hi - lo);
   // chunk c's list holds its min(k, live) entries; the rest of a list is never read
   float vals[N];
@@ -476,7 +478,8 @@ size_t row_topk_ws_bytes(int rows, int kmax) {
 }
 
 adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
-                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st) {
+                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st,
+                           int lo, int hi) {
   ADT_CHECK_ARG(k >= 1 && k <= kmax && (kmax == 1 || kmax == 16), ADT_E_UNSUPPORTED, "row_topk: k=%d kmax=%d", k, kmax);
   const int G = (V + TOPK_CHUNK - 1) / TOPK_CHUNK;
   ADT_CHECK_ARG(V >= 1 && G <= TOPK_MAX_CHUNKS, ADT_E_UNSUPPORTED, "row_topk: vocab %d above 65536", V);
@@ -487,13 +490,13 @@ adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t
   int* ci = (int*)(cv + (size_t)rows * G * kmax);
   const dim3 g1(G, rows);
   if (kmax == 1) {
-    topk_chunk_kernel<1><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, cv, ci, cms);
+    topk_chunk_kernel<1><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms);
     ADT_LAUNCH_CHECK();
-    topk_merge_kernel<1><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, k, top_id, top_val, lse);
+    topk_merge_kernel<1><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, lo, hi, k, top_id, top_val, lse);
   } else {
-    topk_chunk_kernel<16><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, k, cv, ci, cms);
+    topk_chunk_kernel<16><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms);
     ADT_LAUNCH_CHECK();
-    topk_merge_kernel<16><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, k, top_id, top_val, lse);
+    topk_merge_kernel<16><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, lo, hi, k, top_id, top_val, lse);
   }
   ADT_LAUNCH_CHECK();
   return ADT_OK;

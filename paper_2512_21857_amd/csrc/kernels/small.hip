@@ -29,6 +29,20 @@ __global__ void chain_masks_kernel(uint64_t* mask, int n) {
   }
 }
 
+// The draft's catch-up rows in one launch: tokens from the arguments, feature sources
+// 0..cu-1, positions Ld..Ld+cu-1 and the chain masks of cu rows (row i sees rows 0..i).
+__global__ void catchup_rows_kernel(SmallI32 tok, int cu, int Ld, int32_t* ctok, int32_t* cfsrc, int32_t* cpos,
+                                    uint64_t* cmask) {
+  const int i = threadIdx.x;
+  if (i >= cu) return;
+  ctok[i] = tok.v[i];
+  cfsrc[i] = i;
+  cpos[i] = Ld + i;
+  const int b = i + 1;
+  cmask[i * 2] = b >= 64 ? ~0ull : ((1ull << b) - 1);
+  cmask[i * 2 + 1] = b <= 64 ? 0ull : (b >= 128 ? ~0ull : ((1ull << (b - 64)) - 1));
+}
+
 // Positions, successor allowed ranges and zero scores of a caller-supplied tree.
 __global__ void tree_rows_kernel(const int32_t* depth, const int32_t* n_nodes, int n_max, int L, int P, int n_image,
                                  const int32_t* allowed_img, int32_t* pos, int32_t* allowed_rows, float* score) {
@@ -58,6 +72,13 @@ adt_status launch_set_i32(int32_t* dst, const SmallI32& vals, int count, hipStre
   ADT_CHECK_ARG(count >= 0 && count <= 32, ADT_E_ARG, "set_i32: count %d", count);
   if (count == 0) return ADT_OK;
   set_i32_kernel<<<1, 32, 0, st>>>(dst, vals, count);
+  ADT_LAUNCH_CHECK();
+  return ADT_OK;
+}
+adt_status launch_catchup_rows(const SmallI32& tok, int cu, int Ld, int32_t* ctok, int32_t* cfsrc, int32_t* cpos,
+                               uint64_t* cmask, hipStream_t st) {
+  ADT_CHECK_ARG(cu >= 1 && cu <= 32, ADT_E_ARG, "catchup_rows: %d rows", cu);
+  catchup_rows_kernel<<<1, 32, 0, st>>>(tok, cu, Ld, ctok, cfsrc, cpos, cmask);
   ADT_LAUNCH_CHECK();
   return ADT_OK;
 }

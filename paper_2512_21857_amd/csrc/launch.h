@@ -180,11 +180,13 @@ struct NextRows {
   uint64_t* mask;
   int32_t* frontier;
 };
-// Top-k (ids and logits, rows of kmax) and log-sum-exp of each row over its allowed range;
-// ws holds row_topk_ws_bytes(rows, kmax) bytes of per-chunk candidates.
+// Top-k (ids and logits, rows of kmax) and log-sum-exp of each row over its allowed range
+// (allowed: [rows][2] device pairs, or null for the range [lo, hi) of every row); ws holds
+// row_topk_ws_bytes(rows, kmax) bytes of per-chunk candidates.
 size_t row_topk_ws_bytes(int rows, int kmax);
 adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t* allowed, int rows, int k, int kmax,
-                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st);
+                           int32_t* top_id, float* top_val, float* lse, void* ws, size_t ws_bytes, hipStream_t st,
+                           int lo = 0, int hi = 0);
 adt_status launch_expand_level(const Pool& pool, const int32_t* front, int nf, int cnt, int base, int depth, int k_hat,
                                const int32_t* top_id, const float* top_val, const float* lse, int kmax, int make_next,
                                int L, int drow_base, int root_frow, int tree_frow0, int qrow_base, const NextRows& nx,
@@ -206,6 +208,9 @@ struct SmallI32 {
 };
 adt_status launch_set_i32(int32_t* dst, const SmallI32& vals, int count, hipStream_t st);
 adt_status launch_fill_pairs(int32_t* dst, int rows, int lo, int hi, hipStream_t st);
+// The draft catch-up rows (cu <= 32): ctok = tok, cfsrc = 0..cu-1, cpos = Ld.., chain masks.
+adt_status launch_catchup_rows(const SmallI32& tok, int cu, int Ld, int32_t* ctok, int32_t* cfsrc, int32_t* cpos,
+                               uint64_t* cmask, hipStream_t st);
 adt_status launch_table_rows(const int32_t* tok, int count, int depth, int rows, int32_t* idx, hipStream_t st);
 adt_status launch_iota(int32_t* dst, int count, int start, int step, hipStream_t st);
 adt_status launch_chain_masks(uint64_t* mask, int n, hipStream_t st);
