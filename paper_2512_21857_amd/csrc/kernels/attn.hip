@@ -410,8 +410,37 @@ __device__ __forceinline__ int blk_swz_k(int row) { return DH == 128 ? (row & 15
 template <int DH>
 __device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row & 7) : 2 * ((row >> 1) & 3); }
 
-template <int DH, int KH, int NW, int P, int QW = 1>
-__global__ __launch_bounds__(NW * WAVE, (P > 1 || QW > 1) ? 2 : 4) void tree_attn_blk_kernel(
+// Many pairs in one launch, one key range per pair: the workgroup in grid row y takes the
+// sequence of work rank rho(y) (work = live keys x query tiles; larger first, lower index on
+// ties), rho = y in the first half of the rows and B - 1 - (y - half) in the second.  Rows y
+// and y + half of one head are the two workgroups a CU holds at once in a launch that fits
+// the chip, so each CU gets a long sequence and a short one instead of whatever the sequence
+// order gives (uniform lengths stay as they were).  Every workgroup ranks the B sequences
+// itself, in `scratch` (B + 1 ints of LDS); above 512 sequences the order is kept.
+__device__ int balanced_seq(int y, int B, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                            int nq_max, int kv_cap, int* scratch) {
+  if (B > 512) return y;
+  const int half = (B + 1) / 2, rho = y < half ? y : B - 1 - (y - half);
+  for (int t = threadIdx.x; t < B; t += blockDim.x)
+    scratch[t] = min(kv_len[t] + n_tail[t], kv_cap) * ((min(n_q[t], nq_max) + 15) / 16);
+  __syncthreads();
+  for (int t = threadIdx.x; t < B; t += blockDim.x) {
+    const int wt = scratch[t];
+    int r = 0;
+    for (int u = 0; u < B; ++u) {
+      const int wu = scratch[u];
+      r += (wu > wt) | ((wu == wt) & (u < t));
+    }
+    if (r == rho) scratch[B] = t;
+  }
+  __syncthreads();
+  const int b = scratch[B];
+  __syncthreads();
+  return b;
+}
+
+template <int DH, int KH, int NW, int P>
+__global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
@@ -424,16 +453,17 @@ __global__ __launch_bounds__(NW * WAVE, (P > 1 || QW > 1) ? 2 : 4) void tree_att
   constexpr int LOADS = BLK_BYTES / (NW * WAVE * 16);   // direct loads per thread per block and operand
   constexpr int SUBS = BLK_KT / KH / 16;         // 16-key sub-blocks per wave per block
   static_assert(LOADS >= 1 && SUBS % 2 == 0, "block shape");
-  static_assert(QW == 1 || KH == 1, "two query tiles per wave take whole blocks");
   static_assert((KH - 1) * (NW / KH) * (DT * 4 + 2) * WAVE * 4 <= 4 * BLK_BYTES, "merge area");
   __shared__ __attribute__((aligned(16))) unsigned char smem[4 * BLK_BYTES];   // [buffer][K, V]
 
-  const int h = blockIdx.x, b = blockIdx.y, sp = blockIdx.z;
+  const int h = blockIdx.x, sp = blockIdx.z;
+  const int b = (splits == 1 && gridDim.y > 1)
+                    ? balanced_seq(blockIdx.y, gridDim.y, kv_len, n_q, n_tail, nq_max, kv_cap, (int*)smem)
+                    : blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
-  // wave w owns query tiles (w % QG) * QW .. + QW - 1 and key part w / QG
-  const int QG = ((nq_max + 15) / 16 + QW - 1) / QW;
-  const int tg = wave % QG, kpart = wave / QG;
+  const int QT = (nq_max + 15) / 16;
+  const int tile = wave % QT, kpart = wave / QT;
   const bool active = kpart < KH;                // the remaining waves only load
   const int L = kv_len[b];
   const int nq = min(n_q[b], nq_max);
@@ -447,24 +477,18 @@ __global__ __launch_bounds__(NW * WAVE, (P > 1 || QW > 1) ? 2 : 4) void tree_att
   const uint16_t* kbase = kc + b * stride_b + h * stride_h;
   const uint16_t* vbase = vc + b * stride_b + h * stride_h;
 
-  int qr[QW];
-  bf16x8 qf[QW][KS];
-  uint64_t mw0[QW], mw1[QW];
+  const int qr = tile * 16 + lq;
+  bf16x8 qf[KS];
+  uint64_t mw0 = 0, mw1 = 0;
 #pragma unroll
-  for (int t = 0; t < QW; ++t) {
-    qr[t] = (tg * QW + t) * 16 + lq;
-    mw0[t] = 0;
-    mw1[t] = 0;
+  for (int kk = 0; kk < KS; ++kk) qf[kk] = bf16x8{};
+  if (active && qr < nq) {
+    const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
-    if (active && qr[t] < nq) {
-      const uint16_t* qp = q + (rl.q_row(b, qr[t]) * H + h) * DH;
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) qf[t][kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
-      const uint64_t* mp = mask + rl.m_row(b, qr[t]) * ADT_MASK_WORDS;
-      mw0[t] = mp[0];
-      mw1[t] = mp[1];
-    }
+    for (int kk = 0; kk < KS; ++kk) qf[kk] = *reinterpret_cast<const bf16x8*>(qp + kk * 32 + g * 8);
+    const uint64_t* mp = mask + rl.m_row(b, qr) * ADT_MASK_WORDS;
+    mw0 = mp[0];
+    mw1 = mp[1];
   }
 
   // Slot s (16 bytes) of a block holds row s / CH, chunk (s % CH) ^ swizzle(row); thread t
@@ -497,114 +521,88 @@ __global__ __launch_bounds__(NW * WAVE, (P > 1 || QW > 1) ? 2 : 4) void tree_att
     }
   };
 
-  f32x4 o[QW][DT];
-  float m_run[QW], l_run[QW];
+  f32x4 o[DT];
 #pragma unroll
-  for (int t = 0; t < QW; ++t) {
-#pragma unroll
-    for (int d = 0; d < DT; ++d) o[t][d] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m_run[t] = ATT_M_FLOOR;
-    l_run[t] = 0.f;
-  }
+  for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = ATT_M_FLOOR, l_run = 0.f;
   // this wave's share of block blk, read from LDS buffer blk & 1
   auto compute = [&](int blk) {
     const unsigned char* kb = smem + (blk & 1) * 2 * BLK_BYTES;
     const unsigned char* vb = kb + BLK_BYTES;
     // this wave's keys of the block, 32 at a time: S^T = K Q^T (lane (lq, g) gets keys
-    // key0 + sub*16 + 4g + r for query column lq of each tile; one K read serves every
-    // tile), the online softmax, O^T += V^T P^T (one V^T read serves every tile)
+    // key0 + sub*16 + 4g + r for query column lq), the online softmax, O^T += V^T P^T
 #pragma unroll
     for (int hf = 0; hf < SUBS / 2; ++hf) {
       const int kw0 = kpart * (BLK_KT / KH) + hf * 32;   // first key within the block
       const int key0 = blk * BLK_KT + kw0;
-      f32x4 st[QW][2];
+      f32x4 st[2];
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-        for (int t = 0; t < QW; ++t) st[t][sub] = f32x4{0.f, 0.f, 0.f, 0.f};
+        st[sub] = f32x4{0.f, 0.f, 0.f, 0.f};
         const int row = kw0 + sub * 16 + lq;
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
           const int phys = (kk * 4 + g) ^ blk_swz_k<DH>(row);
           const bf16x8 a = *reinterpret_cast<const bf16x8*>(kb + row * DH * 2 + phys * 16);
-#pragma unroll
-          for (int t = 0; t < QW; ++t)
-            st[t][sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[t][kk], st[t][sub], 0, 0, 0);
+          st[sub] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], st[sub], 0, 0, 0);
         }
       }
-      const bool open = key0 + 32 <= min(L, total);
-      // V^T fragment d of the half-step: the transpose load of lane j of a 16-lane group
-      // addresses row j / 4 and dims 4 (j % 4)..+3 of a 4-row, 16-dim window
+      // the maximum of the raw products (the scale is positive), then the weights
+      // 2^(s * scale - m) in one FMA each; m is floored at ATT_M_FLOOR, so a masked product
+      // (-inf) gives weight 0 and every difference stays finite
+      float mx = -INFINITY;
+      if (key0 + 32 <= min(L, total)) {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, st[sub][r]);
+      } else {
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = key0 + sub * 16 + 4 * g + r;
+            const float v = key_visible(key, total, L, mw0, mw1) ? st[sub][r] : -INFINITY;
+            st[sub][r] = v;
+            mx = fmaxf(mx, v);
+          }
+      }
+      mx = xor16_max(mx);
+      mx = xor32_max(mx);
+      const float m_new = fmaxf(m_run, mx * scale_log2);
+      const float alpha = fast_exp2(m_run - m_new);
+      float rs = 0.f;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float p = fast_exp2(fmaf(st[sub][r], scale_log2, -m_new));
+          st[sub][r] = p;
+          rs += p;
+        }
+      rs = xor16_add(rs);
+      rs = xor32_add(rs);
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+      if (!__all(alpha == 1.f)) {
+#pragma unroll
+        for (int d = 0; d < DT; ++d) o[d] *= alpha;
+      }
+      // the transpose load of lane j of a 16-lane group addresses row j / 4 and dims
+      // 4 (j % 4)..+3 of a 4-row, 16-dim window
+      bf16x8 pb;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) pb[r] = (__bf16)(r < 4 ? st[0][r] : st[1][r - 4]);
       const int r_lo = kw0 + 4 * g + (lq >> 2), r_hi = r_lo + 16;
-      auto read_vt = [&](int d) {
+#pragma unroll
+      for (int d = 0; d < DT; ++d) {
         const int c = 2 * d + ((lq & 3) >> 1), half = lq & 1;
         const int off_lo = r_lo * DH * 2 + ((c ^ blk_swz_v<DH>(r_lo)) * 16) + half * 8;
         const int off_hi = r_hi * DH * 2 + ((c ^ blk_swz_v<DH>(r_hi)) * 16) + half * 8;
         const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vb + off_lo));
         const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(vb + off_hi));
-        return __builtin_bit_cast(bf16x8, v8i16{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-      };
-      // several tiles: the V^T fragments are read once, before the softmax (their LDS reads
-      // overlap it), and each tile's products follow its own softmax, so one tile's MFMAs run
-      // under the next tile's vector work; one tile reads each fragment where it is used
-      bf16x8 vt[QW > 1 ? DT : 1];
-      if constexpr (QW > 1) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) vt[d] = read_vt(d);
-      }
-#pragma unroll
-      for (int t = 0; t < QW; ++t) {
-        // the maximum of the raw products (the scale is positive), then the weights
-        // 2^(s * scale - m) in one FMA each; m is floored at ATT_M_FLOOR, so a masked product
-        // (-inf) gives weight 0 and every difference stays finite
-        float mx = -INFINITY;
-        if (open) {
-#pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, st[t][sub][r]);
-        } else {
-#pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int key = key0 + sub * 16 + 4 * g + r;
-              const float v = key_visible(key, total, L, mw0[t], mw1[t]) ? st[t][sub][r] : -INFINITY;
-              st[t][sub][r] = v;
-              mx = fmaxf(mx, v);
-            }
-        }
-        mx = xor16_max(mx);
-        mx = xor32_max(mx);
-        const float m_new = fmaxf(m_run[t], mx * scale_log2);
-        const float alpha = fast_exp2(m_run[t] - m_new);
-        float rs = 0.f;
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float p = fast_exp2(fmaf(st[t][sub][r], scale_log2, -m_new));
-            st[t][sub][r] = p;
-            rs += p;
-          }
-        rs = xor16_add(rs);
-        rs = xor32_add(rs);
-        l_run[t] = l_run[t] * alpha + rs;
-        m_run[t] = m_new;
-        if (!__all(alpha == 1.f)) {
-#pragma unroll
-          for (int d = 0; d < DT; ++d) o[t][d] *= alpha;
-        }
-        bf16x8 pb;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) pb[r] = (__bf16)(r < 4 ? st[t][0][r] : st[t][1][r - 4]);
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          bf16x8 a;
-          if constexpr (QW > 1) a = vt[d];
-          else a = read_vt(d);
-          o[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[t][d], 0, 0, 0);
-        }
+        const bf16x8 a = __builtin_bit_cast(bf16x8, v8i16{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+        o[d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb, o[d], 0, 0, 0);
       }
     }
   };
@@ -628,56 +626,52 @@ __global__ __launch_bounds__(NW * WAVE, (P > 1 || QW > 1) ? 2 : 4) void tree_att
     }
   }
 
-  // KH > 1 (one tile per wave): parts 1.. of a tile pass their state through LDS to part 0,
-  // which merges them
+  // KH > 1: parts 1.. of a tile pass their state through LDS to part 0, which merges them
   float* mo = reinterpret_cast<float*>(smem);          // [tile][part - 1][DT * 4 + 2][WAVE]
   if (KH > 1) {
     __syncthreads();
     if (active && kpart >= 1) {
-      float* t = mo + (size_t)(tg * (KH - 1) + kpart - 1) * (DT * 4 + 2) * WAVE;
+      float* t = mo + (size_t)(tile * (KH - 1) + kpart - 1) * (DT * 4 + 2) * WAVE;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) t[(d * 4 + r) * WAVE + lane] = o[0][d][r];
-      t[(DT * 4) * WAVE + lane] = m_run[0];
-      t[(DT * 4 + 1) * WAVE + lane] = l_run[0];
+        for (int r = 0; r < 4; ++r) t[(d * 4 + r) * WAVE + lane] = o[d][r];
+      t[(DT * 4) * WAVE + lane] = m_run;
+      t[(DT * 4 + 1) * WAVE + lane] = l_run;
     }
     __syncthreads();
     if (active && kpart == 0) {
 #pragma unroll
       for (int kp = 1; kp < KH; ++kp) {
-        const float* t = mo + (size_t)(tg * (KH - 1) + kp - 1) * (DT * 4 + 2) * WAVE;
+        const float* t = mo + (size_t)(tile * (KH - 1) + kp - 1) * (DT * 4 + 2) * WAVE;
         const float m1 = t[(DT * 4) * WAVE + lane], l1 = t[(DT * 4 + 1) * WAVE + lane];
-        const float M = fmaxf(m_run[0], m1);
-        const float w0 = M == -INFINITY ? 0.f : fast_exp2(m_run[0] - M);
+        const float M = fmaxf(m_run, m1);
+        const float w0 = M == -INFINITY ? 0.f : fast_exp2(m_run - M);
         const float w1 = M == -INFINITY ? 0.f : fast_exp2(m1 - M);
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) o[0][d][r] = o[0][d][r] * w0 + t[(d * 4 + r) * WAVE + lane] * w1;
-        l_run[0] = l_run[0] * w0 + l1 * w1;
-        m_run[0] = M;
+          for (int r = 0; r < 4; ++r) o[d][r] = o[d][r] * w0 + t[(d * 4 + r) * WAVE + lane] * w1;
+        l_run = l_run * w0 + l1 * w1;
+        m_run = M;
       }
     }
   }
+  if (active && kpart == 0 && qr < nq) {
+    if (splits == 1) {
+      const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
 #pragma unroll
-  for (int t = 0; t < QW; ++t) {
-    if (active && kpart == 0 && qr[t] < nq) {
-      if (splits == 1) {
-        const float inv = l_run[t] > 0.f ? 1.f / l_run[t] : 0.f;
+      for (int d = 0; d < DT; ++d)
+        store4(out + rl.o_index(b, qr, H, DH, h, d * 16 + 4 * g), o[d][0] * inv, o[d][1] * inv, o[d][2] * inv,
+               o[d][3] * inv);
+    } else {
+      // this split's (O, m, l) for the log-sum-exp merge (m in the log2 domain)
+      const int64_t pr = (((int64_t)b * H + h) * splits + sp) * nq_max + qr;
 #pragma unroll
-        for (int d = 0; d < DT; ++d)
-          store4(out + rl.o_index(b, qr[t], H, DH, h, d * 16 + 4 * g), o[t][d][0] * inv, o[t][d][1] * inv,
-                 o[t][d][2] * inv, o[t][d][3] * inv);
-      } else {
-        // this split's (O, m, l) for the log-sum-exp merge (m in the log2 domain)
-        const int64_t pr = (((int64_t)b * H + h) * splits + sp) * nq_max + qr[t];
-#pragma unroll
-        for (int d = 0; d < DT; ++d) *reinterpret_cast<f32x4*>(part_o + pr * DH + d * 16 + 4 * g) = o[t][d];
-        if (g == 0) {
-          part_ml[pr * 2] = m_run[t];
-          part_ml[pr * 2 + 1] = l_run[t];
-        }
+      for (int d = 0; d < DT; ++d) *reinterpret_cast<f32x4*>(part_o + pr * DH + d * 16 + 4 * g) = o[d];
+      if (g == 0) {
+        part_ml[pr * 2] = m_run;
+        part_ml[pr * 2 + 1] = l_run;
       }
     }
   }
@@ -789,28 +783,24 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   const dim3 grid(H, B, S);
   const int qt = (nq_max + 15) / 16;
   hipEvent_t e1 = S > 1 ? nullptr : ev1;
-#define ADT_ATTN_BLK_P(DHV, KHV, NWV, PV, QWV)                                                                  \
-  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV, PV, QWV>, grid, dim3(NWV * WAVE), 0, st, ev0, e1, 0,   \
+#define ADT_ATTN_BLK_P(DHV, KHV, NWV, PV)                                                                       \
+  hipExtLaunchKernelGGL(tree_attn_blk_kernel<DHV, KHV, NWV, PV>, grid, dim3(NWV * WAVE), 0, st, ev0, e1, 0,        \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, S, part_o, part_ml)
   // a split workgroup owns the CU and streams a few blocks, so it keeps three in flight; many
   // pairs without splits keep one (two workgroups share a CU)
 #define ADT_ATTN_BLK(DHV, KHV, NWV)        \
   if (S > 1) {                             \
-    ADT_ATTN_BLK_P(DHV, KHV, NWV, 3, 1);   \
+    ADT_ATTN_BLK_P(DHV, KHV, NWV, 3);      \
   } else {                                 \
-    ADT_ATTN_BLK_P(DHV, KHV, NWV, 1, 1);   \
+    ADT_ATTN_BLK_P(DHV, KHV, NWV, 1);      \
   }
   // two tiles at head size 128: four waves (two tiles x two key halves, ~190 VGPRs), so two
   // workgroups share a CU and a 512-pair launch is resident at once (32 nodes: 61 % of
   // 8 TB/s against 58 % with eight waves in 128-key blocks, one workgroup per CU)
-  // five to eight tiles at head size 128 over many pairs: four waves of two tiles each, so
-  // every K and V^T read from LDS feeds two query tiles, two workgroups share a CU and a
-  // 512-pair launch is resident at once
   if (Dh == 128) {
     if (qt <= 2) { ADT_ATTN_BLK(128, 2, 4) }
     else if (qt <= 4) { ADT_ATTN_BLK(128, 2, AWG_W) }
-    else if (S == 1) { ADT_ATTN_BLK_P(128, 1, 4, 1, 2); }
     else { ADT_ATTN_BLK(128, 1, AWG_W) }
   } else {
     if (qt <= 2) { ADT_ATTN_BLK(64, 4, AWG_W) }

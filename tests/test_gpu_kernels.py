@@ -96,8 +96,8 @@ def test_tree_attn_bf16_long_prefix_split_keys(rt, n):
     (8, 16, 128, 33, 500, 700, False),  # 3 tiles at the smallest row count of that shape
     (8, 16, 128, 32, 100, 400, True),   # 2 tiles at head size 128: four waves, keys split in two halves
     (16, 8, 64, 20, 0, 200, False),     # 2 tiles at head size 64, the smallest tree of the path
-    (8, 16, 128, 65, 200, 900, True),   # 5 tiles at head size 128: two tiles a wave, one wave only loads
-    (4, 32, 128, 100, 300, 1100, True), # 7 tiles: the last wave's second tile is past the tree
+    (8, 16, 128, 65, 200, 900, True),   # 5 tiles at head size 128 (three waves only load), ragged trees
+    (4, 32, 128, 100, 300, 1100, True), # 7 tiles, prefixes of very different lengths (work-balanced order)
     (8, 16, 128, 96, 0, 150, False),    # 6 tiles over short prefixes: most blocks cross the tree
 ])
 def test_tree_attn_bf16_many_pairs_blocks(rt, B, H, Dh, n, l_lo, l_hi, vary):
