@@ -412,11 +412,13 @@ __device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row 
 
 // Many pairs in one launch, one key range per pair: the workgroup in grid row y takes the
 // sequence of work rank rho(y) (work = live keys x query tiles; larger first, lower index on
-// ties), rho = y in the first half of the rows and B - 1 - (y - half) in the second.  Rows y
-// and y + half of one head are the two workgroups a CU holds at once in a launch that fits
-// the chip, so each CU gets a long sequence and a short one instead of whatever the sequence
-// order gives (uniform lengths stay as they were).  Every workgroup ranks the B sequences
-// itself, in `scratch` (B + 1 ints of LDS); above 512 sequences the order is kept.
+// ties), rho = y in the first half of the rows and B - 1 - (y - half) in the second.  With
+// the workgroups dealt out in order, rows y and y + half of one head are the two workgroups
+// a CU holds at once in a launch that fits the chip twice, so each CU gets a long sequence
+// and a short one instead of whatever the sequence order gives (uniform lengths stay as they
+// were).  Every workgroup ranks the B sequences itself, in `scratch` (B + 1 ints of LDS);
+// above 512 sequences the order is kept.  (The one-workgroup-per-pair kernel of <= 16-row
+// trees keeps the plain order: the ranking cost it 64 VGPRs and an occupancy step.)
 __device__ int balanced_seq(int y, int B, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
                             int nq_max, int kv_cap, int* scratch) {
   if (B > 512) return y;
@@ -434,7 +436,7 @@ __device__ int balanced_seq(int y, int B, const int32_t* kv_len, const int32_t* 
     if (r == rho) scratch[B] = t;
   }
   __syncthreads();
-  const int b = scratch[B];
+  const int b = __builtin_amdgcn_readfirstlane(scratch[B]);   // uniform: addresses stay scalar
   __syncthreads();
   return b;
 }
