@@ -99,6 +99,7 @@ def test_tree_attn_bf16_long_prefix_split_keys(rt, n):
     (8, 16, 128, 65, 200, 900, True),   # 5 tiles at head size 128 (three waves only load), ragged trees
     (4, 32, 128, 100, 300, 1100, True), # 7 tiles, prefixes of very different lengths (work-balanced order)
     (8, 16, 128, 96, 0, 150, False),    # 6 tiles over short prefixes: most blocks cross the tree
+    (9, 16, 128, 40, 0, 1500, True),    # an odd number of sequences in the work-balanced order
 ])
 def test_tree_attn_bf16_many_pairs_blocks(rt, B, H, Dh, n, l_lo, l_hi, vary):
     """Many (sequence, head) pairs with trees of 17-128 rows take the shared-block kernel."""
