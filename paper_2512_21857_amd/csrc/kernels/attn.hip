@@ -8,12 +8,12 @@
 // Probabilities enter the second product rounded to bf16 (relative error 2^-9 per term, below
 // the bf16 rounding of the output itself); steps wholly inside the unmasked prefix skip the
 // mask test, and the running output is rescaled only when some row's maximum moved.
-// Three kernels by shape: tree_attn_blk_kernel (trees of 17-128 rows over many pairs, and
-// every tree over few pairs with long prefixes: one workgroup per pair, or per pair and key
-// split, sharing each K/V block through LDS; splits write (O, m, l) partials that
-// tree_attn_combine_kernel merges with log-sum-exp weights), tree_attn_wg_kernel (trees of
-// at most 16 rows over many pairs, and few pairs over short prefixes: one workgroup per
-// pair or query slice whose waves split the keys and merge in LDS), and tree_attn_f32_kernel.
+// Three kernels by shape: tree_attn_blk_kernel (trees of 17-128 rows over many pairs, in a
+// work-balanced sequence order, and every tree over few pairs: one workgroup per pair, or
+// per pair and key split, sharing each K/V block through LDS; splits write (O, m, l)
+// partials that tree_attn_combine_kernel merges with log-sum-exp weights),
+// tree_attn_wg_kernel (trees of at most 16 rows over many pairs: one workgroup per pair
+// whose waves split the keys and merge in LDS), and tree_attn_f32_kernel.
 #include <hip/hip_ext.h>
 
 #include "../launch.h"
@@ -62,7 +62,7 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
-    int kv_cap, float scale_log2, uint16_t* __restrict__ out, int pairs, int qsplit) {
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
   constexpr int KG = NW / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
   // V rows of a step, padded by 32 bytes so that the 8 rows a transpose load touches per
@@ -73,23 +73,15 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
   constexpr int MG_BYTES = NW * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
-  // Workgroup i takes query slice qs of pair p, with i = (p / 8) * 8 qsplit + 8 qs + p % 8:
-  // workgroups are dealt to the 8 XCDs in turn, so every slice of a pair runs on one XCD
-  // and its K/V come from HBM into that XCD's L2 once.
-  const int grp = blockIdx.x / (8 * qsplit), rem = blockIdx.x % (8 * qsplit);
-  const int qs = rem / 8, pair = grp * 8 + rem % 8;
-  const int tile0 = qs * QG * QTW;                         // first query tile of this slice
-  // padding, or a slice past every tree: no keys and no rows (no early exit, which would
-  // put a wait for the arguments before the loads below)
-  const bool dead = pair >= pairs || tile0 * 16 >= nq_max;
-  const int h = dead ? 0 : pair % H, b = dead ? 0 : pair / H;
+  // workgroup p takes pair p = b * H + h
+  const int h = blockIdx.x % H, b = blockIdx.x / H;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int qg = wave / KG, kg = wave % KG;
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
   const int L = kv_len[b];
-  const int nq = dead ? 0 : min(n_q[b], nq_max);
-  const int total = dead ? 0 : min(L + n_tail[b], kv_cap);
-  if (!dead && threadIdx.x == 0 && L + n_tail[b] > kv_cap) dev_fail(DEVINV_KV_RANGE);
+  const int nq = min(n_q[b], nq_max);
+  const int total = min(L + n_tail[b], kv_cap);
+  if (threadIdx.x == 0 && L + n_tail[b] > kv_cap) dev_fail(DEVINV_KV_RANGE);
   int per = (total + KG - 1) / KG;
   per = (per + 15) / 16 * 16;
   const int k0 = min(total, kg * per), k1 = min(total, k0 + per);
@@ -111,7 +103,7 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
     for (int d = 0; d < DT; ++d) o[t][d] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) qf[t][kk] = bf16x8{};
-    const int qr = (tile0 + qg * QTW + t) * 16 + lq;
+    const int qr = (qg * QTW + t) * 16 + lq;
     if (qr < nq) {
       const uint16_t* qp = q + (rl.q_row(b, qr) * H + h) * DH;
 #pragma unroll
@@ -269,7 +261,7 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
     __syncthreads();
     for (int idx = threadIdx.x; idx < QG * 16 * DH; idx += NW * WAVE) {
       const int qgr = idx / (16 * DH), row = (idx / DH) % 16, d = idx % DH;
-      const int qr = (tile0 + qgr * QTW + t) * 16 + row;
+      const int qr = (qgr * QTW + t) * 16 + row;
       if (qr >= nq) continue;
       const int w0 = qgr * KG;
       float M = -INFINITY;
@@ -690,21 +682,6 @@ static int attn_splits(int B, int H, int kv_cap) {
   return want < 1 ? 1 : want;
 }
 
-// Query tiles per wave and query groups of the one-workgroup-per-pair kernel, used for many
-// pairs: the tiles of a pair share one workgroup (registers allow 4 tiles of head size 64, 2
-// of 128).  Returns false when nq_max does not fit.
-static bool attn_wg_shape(int B, int H, int Dh, int nq_max, int& qtw, int& qg, int& qsplit) {
-  (void)B;
-  (void)H;
-  const int qt = (nq_max + 15) / 16;
-  const int cap = Dh == 64 ? 4 : 2;
-  qtw = qt < cap ? qt : cap;
-  const int groups = (qt + qtw - 1) / qtw;
-  qg = groups <= 1 ? 1 : (groups <= 2 ? 2 : 4);   // a power of two dividing the 8 waves
-  qsplit = 1;
-  return groups <= 4;
-}
-
 // Waves per workgroup of the one-workgroup-per-pair kernel.  Many pairs at head size 128
 // with trees of 9-16 rows (about 160-190 VGPRs a wave, so one eight-wave workgroup per CU):
 // four waves, so that two workgroups share a CU and every pair of a 512-pair launch is
@@ -720,10 +697,7 @@ static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_m
 
 // Many pairs with trees of at most 16 rows: one workgroup per pair.  Few pairs (one image's
 // forwards) take the shared-block kernel with the keys split across workgroups instead.
-static bool attn_use_wg(int B, int H, int Dh, int nq_max) {
-  int qtw, qg, qsplit;
-  return B * H >= 128 && nq_max <= 16 && attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
-}
+static bool attn_use_wg(int B, int H, int nq_max) { return B * H >= 128 && nq_max <= 16; }
 
 // Upper bound over every kv_cap: the splits never exceed ceil(256 / (B*H)).
 size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
@@ -735,7 +709,7 @@ size_t tree_attn_ws_bytes(int B, int H, int Dh, int nq_max, int kv_cap, int dtyp
 }
 
 size_t tree_attn_ws_need(int B, int H, int Dh, int nq_max, int kv_cap, int dtype) {
-  if (dtype == ADT_F32 || attn_use_blk(B, H, nq_max) || attn_use_wg(B, H, Dh, nq_max)) return 0;
+  if (dtype == ADT_F32 || attn_use_blk(B, H, nq_max) || attn_use_wg(B, H, nq_max)) return 0;
   const int S = attn_splits(B, H, kv_cap);
   return S > 1 ? (size_t)B * H * S * nq_max * (Dh + 2) * sizeof(float) : 0;
 }
@@ -745,28 +719,16 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
                             int nq_max, int kv_cap, float scale, void* out, void* ws, size_t ws_bytes, hipStream_t st,
                             hipEvent_t ev0, hipEvent_t ev1) {
   const float sl2 = scale * LOG2E;
-  if (attn_use_wg(B, H, Dh, nq_max)) {
-    int qtw, qg, qsplit;
-    attn_wg_shape(B, H, Dh, nq_max, qtw, qg, qsplit);
-    const int pairs = B * H;
-    const dim3 grid(qsplit == 1 ? pairs : (pairs + 7) / 8 * 8 * qsplit);
+  if (attn_use_wg(B, H, nq_max)) {
+    const dim3 grid(B * H);
 #define ADT_ATTN_WG(DHV, QTWV, QGV, NWV)                                                                           \
   hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,       \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
-                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, pairs, qsplit)
-    if (Dh == 128) {
-      if (qtw == 1 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4);
-      else if (qtw == 1) ADT_ATTN_WG(128, 1, 1, AWG_W);
-      else if (qg == 1) ADT_ATTN_WG(128, 2, 1, AWG_W);
-      else if (qg == 2) ADT_ATTN_WG(128, 2, 2, AWG_W);
-      else ADT_ATTN_WG(128, 2, 4, AWG_W);
-    } else {
-      if (qtw == 1) ADT_ATTN_WG(64, 1, 1, AWG_W);
-      else if (qtw == 2) ADT_ATTN_WG(64, 2, 1, AWG_W);
-      else if (qtw == 3) ADT_ATTN_WG(64, 3, 1, AWG_W);
-      else if (qg == 1) ADT_ATTN_WG(64, 4, 1, AWG_W);
-      else ADT_ATTN_WG(64, 4, 2, AWG_W);
-    }
+                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
+    // one query tile (at most 16 rows) per workgroup
+    if (Dh == 128 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4);
+    else if (Dh == 128) ADT_ATTN_WG(128, 1, 1, AWG_W);
+    else ADT_ATTN_WG(64, 1, 1, AWG_W);
 #undef ADT_ATTN_WG
     ADT_LAUNCH_CHECK();
     return ADT_OK;
