@@ -508,14 +508,18 @@ def _small_bf16():
     return dataclasses.replace(cfg, prefix_len=16, img_hi=512, prefix_hi=512, grid_h=8, grid_w=8)
 
 
-@pytest.mark.parametrize("variant", ["adt", "fixed", "guided"])
+@pytest.mark.parametrize("variant", ["adt", "fixed", "guided", "subrange"])
 def test_bf16_small_parity(rt, variant):
     """The 2-layer bf16 model (d 256, 4 x 64 heads, V 512, 8 x 8 grid) under the ADT schedule,
-    with fixed 6-deep 10-wide trees, and with classifier-free guidance (scale 3.0): every cycle
-    of the image layer-local within the bf16 tolerance and cross-fed bit-exact."""
+    with fixed 6-deep 10-wide trees, with classifier-free guidance (scale 3.0), and with image
+    ids [64, 320) inside the vocabulary (the LM head then computes those 256 rows only, from
+    weight row 64 on): every cycle of the image layer-local within the bf16 tolerance and
+    cross-fed bit-exact."""
     cfg = _small_bf16()
     if variant == "guided":
         cfg = dataclasses.replace(cfg, guidance=3.0)
+    if variant == "subrange":
+        cfg = dataclasses.replace(cfg, img_lo=64, img_hi=320, prefix_lo=320, prefix_hi=512)
     w = synth.model_weights(cfg)
     dm = rt.DeviceModel(cfg, w)
     om = OracleModel(cfg, w)
