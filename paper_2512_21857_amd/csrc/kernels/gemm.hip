@@ -256,7 +256,7 @@ __global__ __launch_bounds__(TILE_THREADS) void gemm_rows_kernel(const uint16_t*
     for (int j = 0; j < KC; ++j) {
       const int kk = min(c0 + j, kt1 - 1);
 #pragma unroll
-      for (int t = 0; t < T; ++t) w[j][t] = wp[t][(int64_t)kk * 64];
+      for (int t = 0; t < T; ++t) w[j][t] = __builtin_nontemporal_load(wp[t] + (int64_t)kk * 64);
 #pragma unroll
       for (int m = 0; m < MT; ++m) x[j][m] = *reinterpret_cast<const bf16x8*>(xp[m] + kk * xks);
     }
