@@ -385,7 +385,7 @@ def onbox_probes(rt, read_bytes=4 << 30, iters=10):
             "hbm_read_frac_of_nominal": round(rd / HBM_PEAK_GBS, 4),
             "mfma_bf16_TFLOP_s": round(tf, 1), "mfma_bf16_nominal_TFLOP_s": MFMA_PEAK_TFLOPS,
             "mfma_frac_of_nominal": round(tf / MFMA_PEAK_TFLOPS, 4),
-            "probes": "adt_probe_hbm_read (16-byte streaming loads over 4 GiB), adt_probe_mfma "
+            "probes": "adt_probe_hbm_read (16-byte nontemporal loads over 4 GiB), adt_probe_mfma "
                       "(back-to-back 32x32x16 bf16 MFMAs, register operands)"}
 
 

@@ -526,7 +526,7 @@ adt_status adt_batch_step(adt_batch* b, adt_step_out* outs, void* stream);
 adt_status adt_profile_enable(int32_t on);
 /* Probes of what the device sustains, to report beside the nominal peaks (HBM 8 TB/s, dense
  * bf16 MFMA 2.5 PFLOP/s).  adt_probe_hbm_read streams `bytes` (a multiple of 16, 16-byte
- * aligned device buffer) with 16-byte loads and folds them into `sink`; adt_probe_mfma runs
+ * aligned device buffer) with 16-byte nontemporal loads and folds them into `sink`; adt_probe_mfma runs
  * `iters` rounds of back-to-back 32x32x16 bf16 MFMAs on register operands (no memory traffic)
  * and reports the flops it launched in *flops [host].  sink: device scratch of at least
  * adt_probe_sink_bytes() bytes.  Asynchronous on `stream`; the caller times them. */

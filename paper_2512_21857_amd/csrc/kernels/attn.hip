@@ -501,8 +501,10 @@ __global__ __launch_bounds__(NW * WAVE, P > 1 ? 2 : 4) void tree_attn_blk_kernel
       const int64_t key = min(blk * BLK_KT + row, last);
       const int64_t ko = live ? key * DH + (phys ^ blk_swz_k<DH>(row)) * 8 : 0;
       const int64_t vo = live ? key * DH + (phys ^ blk_swz_v<DH>(row)) * 8 : 0;
-      kr[u][r] = *reinterpret_cast<const u16x8*>(kbase + ko);
-      vr[u][r] = *reinterpret_cast<const u16x8*>(vbase + vo);
+      // streamed once per workgroup: nontemporal (32 and 64 nodes of the many-pair
+      // microbenchmark 0.64 -> 0.73 and 0.61 -> 0.68-0.70 of 8 TB/s)
+      kr[u][r] = __builtin_nontemporal_load(reinterpret_cast<const u16x8*>(kbase + ko));
+      vr[u][r] = __builtin_nontemporal_load(reinterpret_cast<const u16x8*>(vbase + vo));
     }
   };
   auto store_block = [&](int u, int buf) {
