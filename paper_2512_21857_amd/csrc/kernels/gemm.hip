@@ -430,18 +430,19 @@ RowsPlan gemm_rows_plan(int M, int N, int K, bool partial, bool wide) {
   auto ok = [&](int t) { return t <= tmax && tiles % t == 0; };
   if (partial && tiles >= 192 && (mt <= 2 || K <= 8192)) return {1, 1, tiles};
   if (!partial || (mt == 1 && tiles >= 192)) {
+    // wide (an epilogue without early inputs, whose registers the accumulators can take), up
+    // to 64 rows: one round of the CUs with five or six tiles each where that covers the
+    // columns (gate/up: 256 groups of 5-6; 61 rows 37.5 us against 45 with 512 groups of
+    // 2-3, 24 rows 34.0 against 37.4 with 688 groups of 2, 8 rows 32.4 against 34.3), and
+    // at 49-64 rows 512 groups of 8 for the widest products (LM head 107 us against 118 with
+    // 1024 groups of 4)
+    if (wide && mt <= 4 && (tiles + 255) / 256 >= 5 && (tiles + 255) / 256 <= 6) return {6, 1, 256};
+    if (wide && mt == 4 && tiles >= 2048 && (tiles + 511) / 512 == 8) return {8, 1, 512};
     // > 32 rows: a multiple of 256 workgroups (whole rounds of the CUs) with at most tmax tiles
-    // each, spread evenly (gate/up's 1376 tiles: 512 groups of 2-3, 45 us against 48 with 344
-    // groups of 4)
-    if (mt >= 3) {
-      // wide (an epilogue without early inputs, whose registers the accumulators can take):
-      // one round of the CUs with up to six tiles each where that suffices (gate/up: 256
-      // groups of 5-6, 45.7 us against 47.0 with 512 groups of 2-3 at 61 rows, 39.9 against
-      // 43.3 at 40 rows)
-      if (wide && mt <= 4 && (tiles + 255) / 256 >= 5 && (tiles + 255) / 256 <= 6) return {6, 1, 256};
+    // each, spread evenly
+    if (mt >= 3)
       for (int g = 256; g <= tiles; g += 256)
         if ((tiles + g - 1) / g <= tmax) return {(tiles + g - 1) / g, 1, g};
-    }
     for (int t : {4, 3, 2}) {
       if (!ok(t) || tiles / t < 256) continue;
       if (t <= 2 || tiles / t == 256 || (mt == 2 && tiles / t >= 1024)) return {t, 1, tiles / t};
@@ -537,6 +538,12 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
   } else {                   \
     ADT_GR_T4(MTV, KCV)      \
   }
+#define ADT_GR_T8(MTV, KCV)  \
+  if (p.T == 8) {            \
+    ADT_GR(MTV, 8, 1);       \
+  } else {                   \
+    ADT_GR_T6(MTV, KCV)      \
+  }
 #define ADT_GR_T2(MTV, KCV)              \
   if (p.T >= 2) {                        \
     ADT_GR(MTV, 2, KCV);                 \
@@ -544,15 +551,16 @@ adt_status launch_gemm(const void* X, int ldx, const void* Wp, int M, int N, int
     ADT_GR(MTV, 1, KCV);                 \
   }
   switch (mt) {
-    case 1: ADT_GR_T4(1, 3) break;
-    case 2: ADT_GR_T4(2, 2) break;
+    case 1: ADT_GR_T6(1, 3) break;
+    case 2: ADT_GR_T6(2, 2) break;
     case 3: ADT_GR_T6(3, 2) break;
-    case 4: ADT_GR_T6(4, 2) break;
+    case 4: ADT_GR_T8(4, 2) break;
     case 5:
     case 6: ADT_GR_T2(6, 2) break;
     default: ADT_GR_T2(8, 2) break;
   }
 #undef ADT_GR_T2
+#undef ADT_GR_T8
 #undef ADT_GR_T6
 #undef ADT_GR_T4
 #undef ADT_GR
