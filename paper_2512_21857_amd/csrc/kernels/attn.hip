@@ -284,40 +284,37 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
 
 // Log-sum-exp merge of the key splits: split s holds the unnormalised O and (m, l) of query
 // qr (m in the log2 domain) at row base + s * nq_max + qr.  A thread merges four dims of one
-// query (DH / 4 threads per query, COMB_THREADS / (DH / 4) queries per block); the splits'
-// values are requested eight at a time before any is used, and weights and sums run in
-// split order.
+// query (DH / 4 threads per query, COMB_THREADS / (DH / 4) queries per block); weights and
+// sums run in split order.  Up to eight splits (every few-pair launch) are merged in one pass
+// whose loads are all requested at the start, together with the live row count, which only
+// decides the store (rows past it read partial rows the split kernel left alone); more splits
+// take two passes of eight-at-a-time requests.
 constexpr int COMB_THREADS = 256;
 __global__ __launch_bounds__(COMB_THREADS) void tree_attn_combine_kernel(
     const float* __restrict__ part_o, const float* __restrict__ part_ml, const int32_t* __restrict__ n_q, AttnRows rl,
     int H, int nq_max, int splits, int DH, uint16_t* __restrict__ out) {
   const int h = blockIdx.y, b = blockIdx.z, per_q = DH / 4;
   const int qr = blockIdx.x * (COMB_THREADS / per_q) + threadIdx.x / per_q, d = (threadIdx.x % per_q) * 4;
-  if (qr >= min(n_q[b], nq_max)) return;
+  if (qr >= nq_max) return;
+  const int nq = min(n_q[b], nq_max);
   const int64_t base = (((int64_t)b * H + h) * splits) * nq_max + qr;
-  float M = -INFINITY;
-  for (int s0 = 0; s0 < splits; s0 += 8) {
-    float mv[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) mv[j] = s0 + j < splits ? part_ml[(base + (int64_t)(s0 + j) * nq_max) * 2] : -INFINITY;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);
-  }
-  float ls = 0.f;
+  float M = -INFINITY, ls = 0.f;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s0 = 0; s0 < splits; s0 += 8) {
+  if (splits <= 8) {
     float mv[8], lv[8];
     float4 ov[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       mv[j] = -INFINITY;
-      if (s0 + j < splits) {
-        const int64_t r = base + (int64_t)(s0 + j) * nq_max;
+      if (j < splits) {
+        const int64_t r = base + (int64_t)j * nq_max;
         mv[j] = part_ml[r * 2];
         lv[j] = part_ml[r * 2 + 1];
         ov[j] = *reinterpret_cast<const float4*>(part_o + r * DH + d);
       }
     }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (mv[j] == -INFINITY) continue;
@@ -325,7 +322,37 @@ __global__ __launch_bounds__(COMB_THREADS) void tree_attn_combine_kernel(
       ls += w * lv[j];
       acc = make_float4(acc.x + w * ov[j].x, acc.y + w * ov[j].y, acc.z + w * ov[j].z, acc.w + w * ov[j].w);
     }
+  } else {
+    for (int s0 = 0; s0 < splits; s0 += 8) {
+      float mv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) mv[j] = s0 + j < splits ? part_ml[(base + (int64_t)(s0 + j) * nq_max) * 2] : -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) M = fmaxf(M, mv[j]);
+    }
+    for (int s0 = 0; s0 < splits; s0 += 8) {
+      float mv[8], lv[8];
+      float4 ov[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        mv[j] = -INFINITY;
+        if (s0 + j < splits) {
+          const int64_t r = base + (int64_t)(s0 + j) * nq_max;
+          mv[j] = part_ml[r * 2];
+          lv[j] = part_ml[r * 2 + 1];
+          ov[j] = *reinterpret_cast<const float4*>(part_o + r * DH + d);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (mv[j] == -INFINITY) continue;
+        const float w = exp2f(mv[j] - M);
+        ls += w * lv[j];
+        acc = make_float4(acc.x + w * ov[j].x, acc.y + w * ov[j].y, acc.z + w * ov[j].z, acc.w + w * ov[j].w);
+      }
+    }
   }
+  if (qr >= nq) return;
   const float inv = ls > 0.f ? 1.f / ls : 0.f;
   store4(out + rl.o_index(b, qr, H, DH, h, d), acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
 }
