@@ -474,14 +474,18 @@ def main():
         L = abi.lib()
         abi.check(L.adt_profile_enable(1))
         L.adt_profile_read(abi.PROF_GEMM, None, None, None, None, 1)
+        L.adt_profile_read(abi.PROF_ATTN, None, None, None, None, 1)
         sess = rt.DeviceSession(dm, cfg, poisson=poisson)
         sess.prefill(pre)
         fast_forward(sess, cfg, mid)
         run_steps(sess, W + K)
         n, ms, by, fl = C.c_int64(), C.c_double(), C.c_double(), C.c_double()
         abi.check(L.adt_profile_read(abi.PROF_GEMM, C.byref(n), C.byref(ms), C.byref(by), C.byref(fl), 1))
+        na, ba = C.c_int64(), C.c_double()
+        abi.check(L.adt_profile_read(abi.PROF_ATTN, C.byref(na), C.byref(ms), C.byref(ba), C.byref(fl), 1))
         abi.check(L.adt_profile_enable(0))
         print(json.dumps({"traffic_run": cfg.name, "gemm_launches": n.value, "gemm_algorithmic_bytes": by.value,
+                          "attn_calls": na.value, "attn_algorithmic_bytes": ba.value,
                           "start_cell": mid, "steps": W + K}), flush=True)
         return
     log(f"{cfg.name}: fast-forward to cell {mid}, {W} warm-up steps, {K} timed steps")
