@@ -47,6 +47,10 @@ __device__ __forceinline__ bool key_visible(int key, int k_end, int L, uint64_t 
 // are zero for every purpose here).
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// The work-balanced sequence order (defined with the shared-block kernel below).
+__device__ int balanced_seq(int y, int B, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
+                            int nq_max, int kv_cap, int* scratch);
+
 // One workgroup per (sequence, head): its W = QG x KG waves form QG query groups of QTW
 // 16-row query tiles, and each group's KG waves take contiguous, balanced slices of the
 // keys (computed on the device from kv_len + n_tail, so no wave idles on an empty split).
@@ -62,7 +66,7 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int64_t stride_b, int64_t stride_h, const int32_t* __restrict__ kv_len, const int32_t* __restrict__ n_q,
     const int32_t* __restrict__ n_tail, const uint64_t* __restrict__ mask, AttnRows rl, int H, int nq_max,
-    int kv_cap, float scale_log2, uint16_t* __restrict__ out) {
+    int kv_cap, float scale_log2, uint16_t* __restrict__ out, int balance) {
   constexpr int KG = NW / QG;                           // key slices per query group
   constexpr int DT = DH / 16, KS = DH / 32;
   // V rows of a step, padded by 32 bytes so that the 8 rows a transpose load touches per
@@ -73,8 +77,12 @@ __global__ __launch_bounds__(NW * WAVE) void tree_attn_wg_kernel(
   constexpr int MG_BYTES = NW * 16 * (DH + 2) * 4;      // one query tile of (O, m, l) per wave
   __shared__ __attribute__((aligned(16))) unsigned char smem[VT_BYTES > MG_BYTES ? VT_BYTES : MG_BYTES];
 
-  // workgroup p takes pair p = b * H + h
-  const int h = blockIdx.x % H, b = blockIdx.x / H;
+  // workgroup p takes head p % H of sequence p / H, or with balance (a launch whose CUs hold
+  // two workgroups each) of the sequence of rank p / H in the work-balanced order, which
+  // pairs a long prefix with a short one on every CU
+  const int h = blockIdx.x % H, nb = gridDim.x / H;
+  const int b = balance && nb > 1 ? balanced_seq(blockIdx.x / H, nb, kv_len, n_q, n_tail, nq_max, kv_cap, (int*)smem)
+                                  : blockIdx.x / H;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
   const int qg = wave / KG, kg = wave % KG;
   const int lane = threadIdx.x % WAVE, lq = lane & 15, g = lane >> 4;
@@ -436,8 +444,8 @@ __device__ __forceinline__ int blk_swz_v(int row) { return DH == 128 ? 2 * (row 
 // a CU holds at once in a launch that fits the chip twice, so each CU gets a long sequence
 // and a short one instead of whatever the sequence order gives (uniform lengths stay as they
 // were).  Every workgroup ranks the B sequences itself, in `scratch` (B + 1 ints of LDS);
-// above 512 sequences the order is kept.  (The one-workgroup-per-pair kernel of <= 16-row
-// trees keeps the plain order: the ranking cost it 64 VGPRs and an occupancy step.)
+// above 512 sequences the order is kept.  The rank index is made scalar, so the ranking adds
+// no vector registers to the kernel that calls it.
 __device__ int balanced_seq(int y, int B, const int32_t* kv_len, const int32_t* n_q, const int32_t* n_tail,
                             int nq_max, int kv_cap, int* scratch) {
   if (B > 512) return y;
@@ -750,14 +758,17 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   const float sl2 = scale * LOG2E;
   if (attn_use_wg(B, H, nq_max)) {
     const dim3 grid(B * H);
-#define ADT_ATTN_WG(DHV, QTWV, QGV, NWV)                                                                           \
+#define ADT_ATTN_WG(DHV, QTWV, QGV, NWV, BAL)                                                                      \
   hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,       \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
-                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out)
-    // one query tile (at most 16 rows) per workgroup
-    if (Dh == 128 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4);
-    else if (Dh == 128) ADT_ATTN_WG(128, 1, 1, AWG_W);
-    else ADT_ATTN_WG(64, 1, 1, AWG_W);
+                        mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, BAL)
+    // one query tile (at most 16 rows) per workgroup; the four-wave variant (two workgroups
+    // per CU) takes the sequences in the work-balanced order (16 nodes of the microbenchmark:
+    // 77-78 -> 73.5 us, 61 -> 64 % of 8 TB/s; with one eight-wave workgroup per CU at 8 nodes
+    // the order measured 1-2 % slower and is not used)
+    if (Dh == 128 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4, 1);
+    else if (Dh == 128) ADT_ATTN_WG(128, 1, 1, AWG_W, 0);
+    else ADT_ATTN_WG(64, 1, 1, AWG_W, 0);
 #undef ADT_ATTN_WG
     ADT_LAUNCH_CHECK();
     return ADT_OK;
