@@ -719,15 +719,6 @@ static int attn_splits(int B, int H, int kv_cap) {
   return want < 1 ? 1 : want;
 }
 
-// Waves per workgroup of the one-workgroup-per-pair kernel.  Many pairs at head size 128
-// with trees of 9-16 rows (about 160-190 VGPRs a wave, so one eight-wave workgroup per CU):
-// four waves, so that two workgroups share a CU and every pair of a 512-pair launch is
-// resident at once (measured: 16 rows 61 % of 8 TB/s against 59.5 %; at 8 rows eight waves
-// stay ahead, 60.7 % against 60.2 %).
-static int attn_wg_waves(int B, int H, int Dh, int nq_max) {
-  return (B * H >= 128 && Dh == 128 && nq_max > 8) ? 4 : AWG_W;
-}
-
 // Many pairs with trees of 17-128 rows: the shared-block kernel (one K/V stream per pair,
 // read by every query tile from LDS).
 static bool attn_use_blk(int B, int H, int nq_max) { return B * H >= 128 && nq_max > 16 && nq_max <= 128; }
@@ -762,12 +753,12 @@ static adt_status attn_bf16(const void* q, const void* k, const void* v, int64_t
   hipExtLaunchKernelGGL(tree_attn_wg_kernel<DHV, QTWV, QGV, NWV>, grid, dim3(NWV * WAVE), 0, st, ev0, ev1, 0,       \
                         (const uint16_t*)q, (const uint16_t*)k, (const uint16_t*)v, sb, sh, kv_len, n_q, n_tail,   \
                         mask, rl, H, nq_max, kv_cap, sl2, (uint16_t*)out, BAL)
-    // one query tile (at most 16 rows) per workgroup; the four-wave variant (two workgroups
-    // per CU) takes the sequences in the work-balanced order (16 nodes of the microbenchmark:
-    // 77-78 -> 73.5 us, 61 -> 64 % of 8 TB/s; with one eight-wave workgroup per CU at 8 nodes
-    // the order measured 1-2 % slower and is not used)
-    if (Dh == 128 && attn_wg_waves(B, H, Dh, nq_max) == 4) ADT_ATTN_WG(128, 1, 1, 4, 1);
-    else if (Dh == 128) ADT_ATTN_WG(128, 1, 1, AWG_W, 0);
+    // one query tile (at most 16 rows) per workgroup.  Head size 128 (160-190 VGPRs a wave):
+    // four waves, so that two workgroups share a CU and every pair of a 512-pair launch is
+    // resident at once, with the sequences in the work-balanced order (microbenchmark at 8 /
+    // 16 nodes: 66 / 64-65 % of 8 TB/s, against 61 / 61 % for eight waves, one workgroup per
+    // CU, in the plain order)
+    if (Dh == 128) ADT_ATTN_WG(128, 1, 1, 4, 1);
     else ADT_ATTN_WG(64, 1, 1, AWG_W, 0);
 #undef ADT_ATTN_WG
     ADT_LAUNCH_CHECK();
