@@ -115,6 +115,15 @@ def test_tree_attn_bf16_many_pairs_one_tile(rt, n):
     assert _attn_case(rt, B=8, H=16, Dh=128, n=n, l_lo=0, l_hi=700, seed=8000 + n, vary_n=True) > 0
 
 
+@pytest.mark.parametrize("n", [5, 16])
+def test_tree_attn_bf16_many_pairs_one_tile_head64(rt, n):
+    """Many (sequence, head) pairs with trees of at most 16 rows at head size 64: the
+    one-workgroup-per-pair kernel with eight waves in the sequence order, ragged trees and
+    prefixes from empty to several hundred keys."""
+    print(f"tree_attn bf16 many pairs one tile head 64 n={n}", flush=True)
+    assert _attn_case(rt, B=16, H=8, Dh=64, n=n, l_lo=0, l_hi=600, seed=9000 + n, vary_n=True) > 0
+
+
 def test_tree_attn_bf16_full_microbench_sampled(rt):
     """The 16 x 32 x 128 microbenchmark at its real size (L in [512, 2400], 128 nodes), checked
     on sampled rows including the root, the last node and a deep node of every sequence."""
