@@ -439,7 +439,7 @@ def cpu_baseline(cfg, weights, budget_s, poisson=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1"}))
+        print(json.dumps({"error": "the library runs on one GPU only; use --gpus 1"}))
         sys.exit(2)
     import torch
     sys.path.insert(0, ROOT)

@@ -40,7 +40,7 @@ typedef int32_t adt_status;
 #define ADT_E_SHAPE (-2)       /* dimension not supported by the kernels (alignment, head size) */
 #define ADT_E_CAPACITY (-3)    /* tree, cache or workspace too small */
 #define ADT_E_HIP (-4)         /* a HIP runtime call failed */
-#define ADT_E_UNSUPPORTED (-5) /* valid request outside what this build implements */
+#define ADT_E_UNSUPPORTED (-5) /* valid request outside what the library implements */
 #define ADT_E_DEVICE_INVARIANT (-6) /* debug builds: a kernel found device data breaking an invariant */
 #define ADT_E_STATE (-7)       /* session used out of order (e.g. step before prefill) */
 
