@@ -176,7 +176,8 @@ adt_status adt_kv_compact(void* k_cache, void* v_cache, int32_t B, int32_t slice
  * parent, token: [n] BFS tree; allowed: [n][2] allowed id range [lo, hi) per row; n_nodes: device
  *   scalar n; n_max [host] = rows allocated in logits/parent/token/allowed (n <= n_max <= ADT_MAX_NODES)
  * path: [ADT_MAX_NODES] out, path[0] = 0 then v_1..v_a; n_acc, bonus: device scalars out.
- * workspace: adt_accept_workspace_size(); only sampling modes use it. */
+ * workspace: adt_accept_workspace_size(); only sampling modes use it.  EXACT and RELAXED need
+ *   V <= 65536 (ADT_E_UNSUPPORTED otherwise). */
 typedef struct {
   int32_t mode;        /* ADT_ACCEPT_* */
   float temperature;   /* > 0 for sampling modes */

@@ -12,14 +12,17 @@
 // quantised_exp_weight, so the integers do not depend on a math library); every later
 // operation is exact integer arithmetic, so the walk does not depend on summation order.  One workgroup per tree: the weights of
 // a row are built cooperatively (64-bit radix select for the top-k threshold, block
-// reductions), the sibling walk runs on one lane, the bonus is found by a block-wide
-// prefix scan over ids in ascending order.
+// reductions), the sibling walk runs on one wave (the tree's parent and token arrays in
+// LDS; a relaxed child's neighbour credit by a wave prefix sum; ids removed by rejections
+// marked in an LDS bitmap over the row's allowed range instead of zeroing their weights),
+// and the bonus is found by a block-wide prefix scan over ids in ascending order.
 #include "../launch.h"
 
 namespace adt {
 
 constexpr int AS_THREADS = 1024;
 constexpr int AS_DELTA_BITS = 16;
+constexpr int AS_MAX_RANGE = 65536;   // allowed ids per row of the exact / relaxed walk (one bitmap bit each)
 
 // 64 random bits at key = seed, counter = (step, node, index, tag): words (x1 << 32 | x0).
 // tag 0: acceptance draws; tag 2: drafted children (stochastic children).
@@ -58,6 +61,28 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = __shfl((uint32_t)v, src, WAVE), hi = __shfl((uint32_t)(v >> 32), src, WAVE);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum over the lanes of a wave (lane order).
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  const int lane = threadIdx.x % WAVE;
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    const uint32_t lo = __shfl_up((uint32_t)v, o, WAVE), hi = __shfl_up((uint32_t)(v >> 32), o, WAVE);
+    if (lane >= o) v += ((uint64_t)hi << 32) | lo;
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+  return v;
+}
+
 __device__ uint64_t block_sum_u64(uint64_t v, SampleShared& sh) {
   for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
   __syncthreads();
@@ -92,14 +117,40 @@ __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T,
       if ((k & mask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255], 1u);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-      int acc = 0, b = 255;
-      for (; b > 0; --b) {
-        if (acc + (int)sh.hist[b] >= need) break;
-        acc += sh.hist[b];
+    // the highest bin b at which the count of keys in bins >= b reaches need (bin 0 if
+    // none does): lane l scans bins 255 - 4l .. 252 - 4l after the prefix sums of the lanes
+    // above it
+    if (threadIdx.x < WAVE) {
+      const int l = threadIdx.x;
+      uint32_t h[4], cnt = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        h[i] = sh.hist[255 - 4 * l - i];
+        cnt += h[i];
       }
-      sh.thr = prefix | ((uint64_t)b << shift);
-      sh.need = need - acc;
+      const uint64_t inc = wave_incl_scan_u64(cnt);
+      uint32_t acc = (uint32_t)(inc - cnt);
+      const uint32_t all = (uint32_t)shfl_u64(inc, WAVE - 1);
+      int fb = -1;
+      uint32_t facc = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int b = 255 - 4 * l - i;
+        if (fb < 0 && b > 0 && acc + h[i] >= (uint32_t)need) {
+          fb = b;
+          facc = acc;
+        }
+        acc += h[i];
+      }
+      const uint64_t m = __ballot(fb >= 0);
+      const int src = m ? __ffsll((long long)m) - 1 : -1;
+      if (src < 0 && l == 0) {
+        sh.thr = prefix;
+        sh.need = need - (int)(all - sh.hist[0]);
+      } else if (l == src) {
+        sh.thr = prefix | ((uint64_t)fb << shift);
+        sh.need = need - (int)facc;
+      }
     }
     __syncthreads();
     prefix = sh.thr;
@@ -112,9 +163,9 @@ __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T,
 
 // Integer weights w[i] = quantised_exp_weight(z_i - max z), z = x[i] / T, over the top_k ids of
 // [lo, hi) by (z desc, id asc) (all of them when top_k is 0 or covers the range), zero
-// elsewhere in [0, V); returns their total.  Every thread must call it.
+// elsewhere in [0, V) (written only with full); returns their total.  Every thread must call it.
 __device__ uint64_t build_weights(const float* x, int lo, int hi, int V, float T, int top_k, uint64_t* w,
-                                  SampleShared& sh) {
+                                  SampleShared& sh, bool full = true) {
   const int tid = threadIdx.x;
   const int cnt = hi - lo;
   uint64_t thr = 0;
@@ -126,7 +177,9 @@ __device__ uint64_t build_weights(const float* x, int lo, int hi, int V, float T
   }
   zm = block_max_f32(zm, sh);
   uint64_t part = 0;
-  for (int i = tid; i < V; i += AS_THREADS) {
+  // full: every id of [0, V) is written (zero outside the range); otherwise only [lo, hi),
+  // and the caller treats ids outside it as weight 0
+  for (int i = full ? tid : lo + tid; i < (full ? V : hi); i += AS_THREADS) {
     uint64_t wi = 0;
     if (i >= lo && i < hi) {
       const float z = x[i] / T;
@@ -175,36 +228,41 @@ __device__ int block_top1(const float* x, int lo, int hi, float T, SampleShared&
   return r;
 }
 
+// Weight of id i of a row whose range starts at lo, with the ids removed so far marked in the
+// bitmap zb (bit i - lo); zb null: no removals.
+__device__ __forceinline__ uint64_t kept_weight(const uint64_t* w, const uint32_t* zb, int lo, int i) {
+  return (zb && ((zb[(i - lo) >> 5] >> ((i - lo) & 31)) & 1u)) ? 0ull : w[i];
+}
+
 // Per-thread chunks of [lo, hi) for inverse-CDF lookups: thread t owns ids [b0, b1) and
 // sh.scan[t] = the total weight of the ids before its chunk.  Every thread calls it.
-__device__ void chunk_scan(const uint64_t* w, int lo, int hi, int& b0, int& b1, uint64_t& own, SampleShared& sh) {
+__device__ void chunk_scan(const uint64_t* w, int lo, int hi, int& b0, int& b1, uint64_t& own, SampleShared& sh,
+                           const uint32_t* zb = nullptr) {
   const int tid = threadIdx.x;
   const int per = (hi - lo + AS_THREADS - 1) / AS_THREADS;
   b0 = lo + tid * per;
   b1 = min(hi, b0 + per);
   uint64_t s = 0;
-  for (int i = b0; i < b1; ++i) s += w[i];
+  for (int i = b0; i < b1; ++i) s += kept_weight(w, zb, lo, i);
   own = s;
-  sh.scan[tid] = s;
+  // block exclusive scan of the per-thread sums: within each wave, then over the waves
+  const uint64_t incl = wave_incl_scan_u64(s);
   __syncthreads();
-  if (tid == 0) {   // exclusive scan of the per-thread sums
-    uint64_t run = 0;
-    for (int t = 0; t < AS_THREADS; ++t) {
-      const uint64_t v = sh.scan[t];
-      sh.scan[t] = run;
-      run += v;
-    }
-  }
+  if (tid % WAVE == WAVE - 1) sh.u64[tid / WAVE] = incl;
+  __syncthreads();
+  uint64_t base = 0;
+  for (int i = 0; i < tid / WAVE; ++i) base += sh.u64[i];
+  sh.scan[tid] = base + incl - s;
   __syncthreads();
 }
 
 // Smallest id with prefix weight > r, if it lies in this thread's chunk (else -1).
-__device__ __forceinline__ int chunk_find(const uint64_t* w, int b0, int b1, uint64_t own, uint64_t r,
-                                          const SampleShared& sh) {
+__device__ __forceinline__ int chunk_find(const uint64_t* w, int lo, int b0, int b1, uint64_t own, uint64_t r,
+                                          const SampleShared& sh, const uint32_t* zb = nullptr) {
   uint64_t run = sh.scan[threadIdx.x];
   if (b0 < b1 && run <= r && r < run + own) {
     for (int i = b0; i < b1; ++i) {
-      run += w[i];
+      run += kept_weight(w, zb, lo, i);
       if (run > r) return i;
     }
   }
@@ -218,8 +276,14 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const int32_t* __restrict__ knn, uint64_t seed, uint32_t step, uint64_t* __restrict__ w,
     int32_t* __restrict__ path, int32_t* __restrict__ n_acc, int32_t* __restrict__ bonus) {
   __shared__ SampleShared sh;
-  const int tid = threadIdx.x;
+  __shared__ uint32_t zb[AS_MAX_RANGE / 32];   // ids of the current row removed by rejections (bit i: id lo + i)
+  __shared__ int32_t par_s[ADT_MAX_NODES], tok_s[ADT_MAX_NODES];
+  const int tid = threadIdx.x, lane = tid % WAVE;
   const int n = min(*n_nodes, n_max);
+  for (int i = tid; i < n; i += AS_THREADS) {
+    par_s[i] = parent[i];
+    tok_s[i] = token[i];
+  }
   if (tid == 0) {
     sh.node = 0;
     sh.a = 0;
@@ -232,28 +296,40 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const int u = sh.node;
     const int lo = max(0, min(allowed[u * 2], V)), hi = max(lo, min(allowed[u * 2 + 1], V));
     const float* x = logits + (int64_t)u * ld;
-    const uint64_t total = build_weights(x, lo, hi, V, T, top_k, w, sh);
-    // --- sibling walk (one lane; w lives in global memory and is only touched by this lane)
-    if (tid == 0) {
+    for (int i = tid; i < (hi - lo + 31) / 32; i += AS_THREADS) zb[i] = 0;
+    const uint64_t total = build_weights(x, lo, hi, V, T, top_k, w, sh, false);
+    // --- sibling walk on wave 0: the children of u in node order, one at a time (every lane
+    // holds the same W, draw and mass); ids outside [lo, hi) weigh 0
+    if (tid < WAVE) {
+      auto weight = [&](int i) -> uint64_t { return (i >= lo && i < hi) ? kept_weight(w, zb, lo, i) : 0ull; };
       uint64_t W = total;
       int trial = 0, acc = -1;
       for (int c = u + 1; c < n; ++c) {
-        if (parent[c] != u) continue;
-        const int xt = min(max(token[c], 0), V - 1);
+        if (par_s[c] != u) continue;
+        const int xt = min(max(tok_s[c], 0), V - 1);
         const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)trial, W);
         ++trial;
-        uint64_t mass = w[xt];
+        uint64_t mass = weight(xt);
         int credit_n = 0;
+        const int32_t* nb = knn + (int64_t)xt * knn_stride;
         if (mode == ADT_ACCEPT_RELAXED && xt < knn_rows) {
+          // neighbours 1.. in order while the credited sum stays <= lim: the first j whose
+          // running sum passes lim ends the run (a wave prefix sum per 64 neighbours)
           const uint64_t lim = (W * (uint64_t)delta_q) >> AS_DELTA_BITS;
           uint64_t extra = 0;
-          const int32_t* nb = knn + (int64_t)xt * knn_stride;
-          for (int j = 1; j < knn_k; ++j) {
-            const int y = nb[j];
-            const uint64_t wy = (y >= 0 && y < V) ? w[y] : 0;
-            if (extra + wy > lim) break;
-            extra += wy;
-            ++credit_n;
+          credit_n = knn_k - 1;
+          for (int base = 1; base < knn_k; base += WAVE) {
+            const int j = base + lane;
+            const uint64_t wy = j < knn_k ? weight(nb[j]) : 0ull;
+            const uint64_t inc = wave_incl_scan_u64(wy);
+            const uint64_t past = __ballot(j < knn_k && extra + inc > lim);
+            if (past) {
+              const int f = __ffsll((long long)past) - 1;
+              credit_n = base - 1 + f;
+              if (f > 0) extra += shfl_u64(inc, f - 1);
+              break;
+            }
+            extra += shfl_u64(inc, WAVE - 1);
           }
           mass += extra;
         }
@@ -261,29 +337,34 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
           acc = c;
           break;
         }
-        W -= w[xt];
-        w[xt] = 0;
-        if (credit_n > 0) {
-          const int32_t* nb = knn + (int64_t)xt * knn_stride;
-          for (int j = 1; j <= credit_n; ++j) {
-            const int y = nb[j];
-            if (y >= 0 && y < V) {
-              W -= w[y];
-              w[y] = 0;
-            }
+        // rejected: x, then its credited neighbours, leave p; an id already removed (an earlier
+        // sibling's credit, a repeat in the list, x itself) subtracts nothing
+        uint64_t gone = 0;
+        if (lane == 0 && xt >= lo && xt < hi) {
+          const uint32_t bit = 1u << ((xt - lo) & 31);
+          if (!(atomicOr(&zb[(xt - lo) >> 5], bit) & bit)) gone = w[xt];
+        }
+        for (int base = 1; base <= credit_n; base += WAVE) {
+          const int j = base + lane;
+          const int y = j <= credit_n ? nb[j] : -1;
+          if (y >= lo && y < hi) {
+            const uint32_t bit = 1u << ((y - lo) & 31);
+            if (!(atomicOr(&zb[(y - lo) >> 5], bit) & bit)) gone += w[y];
           }
         }
+        W -= wave_sum_u64(gone);
       }
-      sh.accepted = acc;
-      sh.trial = trial;
-      sh.total = W;
-      if (acc >= 0) {
-        sh.a += 1;
-        path[sh.a] = acc;
-        sh.node = acc;
+      if (lane == 0) {
+        sh.accepted = acc;
+        sh.trial = trial;
+        sh.total = W;
+        if (acc >= 0) {
+          sh.a += 1;
+          path[sh.a] = acc;
+          sh.node = acc;
+        }
       }
     }
-    __threadfence_block();
     __syncthreads();
     if (sh.accepted >= 0) continue;
     // --- bonus from the residual: smallest id with prefix(w) > r
@@ -298,8 +379,8 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)sh.trial, W);
     int b0, b1;
     uint64_t own;
-    chunk_scan(w, lo, hi, b0, b1, own, sh);
-    const int f = chunk_find(w, b0, b1, own, r, sh);
+    chunk_scan(w, lo, hi, b0, b1, own, sh, zb);
+    const int f = chunk_find(w, lo, b0, b1, own, r, sh, zb);
     if (f >= 0) sh.bonus = f;
     __syncthreads();
     break;
@@ -367,7 +448,7 @@ __global__ __launch_bounds__(AS_THREADS) void row_sample_kernel(const float* __r
   const uint32_t node = front ? (uint32_t)(front[r] + 1) : 0u;
   for (int j = 0; j < cnt; ++j) {
     const uint64_t rj = __umul64hi(philox_u64(seed, step, node, (uint32_t)j, 2u), W);
-    const int id = chunk_find(w, b0, b1, own, rj, sh);
+    const int id = chunk_find(w, lo, b0, b1, own, rj, sh);
     if (id >= 0) {
       top_id[r * kmax + j] = id;
       top_val[r * kmax + j] = x[id];
@@ -484,7 +565,7 @@ __global__ __launch_bounds__(AS_THREADS) void accept_mss_kernel(
     int b0, b1;
     uint64_t own;
     chunk_scan(w, lo, hi, b0, b1, own, sh);
-    const int f = chunk_find(w, b0, b1, own, r, sh);
+    const int f = chunk_find(w, lo, b0, b1, own, r, sh);
     if (f >= 0) sh.bonus = f;
     __syncthreads();
     break;
@@ -517,6 +598,7 @@ adt_status launch_accept_sample(const float* logits, int64_t ld, int V, const in
                                 uint64_t step, int32_t* path, int32_t* n_acc, int32_t* bonus, void* ws, size_t ws_bytes,
                                 hipStream_t st) {
   ADT_CHECK_ARG(ws_bytes >= (size_t)V * 8, ADT_E_CAPACITY, "accept_sample: workspace");
+  ADT_CHECK_ARG(V <= AS_MAX_RANGE, ADT_E_UNSUPPORTED, "accept_sample: vocabulary %d above %d", V, AS_MAX_RANGE);
   const uint32_t dq = (uint32_t)lrintf(cfg.delta * (float)(1 << AS_DELTA_BITS));
   const int relaxed = cfg.mode == ADT_ACCEPT_RELAXED;
   accept_sample_kernel<<<1, AS_THREADS, 0, st>>>(logits, ld, V, parent, token, allowed, n_nodes, n_max, cfg.mode,
