@@ -543,7 +543,7 @@ def main():
             for mode in ("exact", "relaxed"):
                 mcfg = synth.get_config("anole_7b", mode=mode)
                 s, r = workload_run(rt, adm, mcfg, apre, min(K, 100), W, mcfg.n_image // 2,
-                                    knn=knn if mode == "relaxed" else None)
+                                    tag=f"anole {mode} timed", knn=knn if mode == "relaxed" else None)
                 del s
                 res[mode] = r
             line["anole_7b"] = {"workload": "Anole-7B-shaped: 32 layers, d 4096, 32x128 heads, FFN 11008, vocab "
@@ -558,8 +558,8 @@ def main():
             lw = synth.model_weights(lcfg, threads=threads)
             ldm = rt.DeviceModel(lcfg, lw)
             lpre = synth.prefix_ids(lcfg)
-            s, r = workload_run(rt, ldm, lcfg, lpre, min(K, 100), W, lcfg.n_image // 2)
-            lprof = profile_pass(abi, s, args.profile_steps)
+            s, r = workload_run(rt, ldm, lcfg, lpre, min(K, 100), W, lcfg.n_image // 2, tag="llamagen timed")
+            lprof = profile_pass(abi, s, args.profile_steps, "llamagen profile")
             del s
             s, fr = workload_run(rt, ldm, lcfg, lpre, min(K, 50), 3, lcfg.n_image // 2, fixed_tree=True)
             del s

@@ -65,6 +65,11 @@ def test_argument_errors_return_codes_without_launching(L):
     import ctypes as C
     assert L.adt_verify_accept(fake, 16, 16, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake, fake, 1 << 20,
                                None) == abi.E_ARG
+    # the exact and relaxed walks cover at most 65536 ids per row
+    for mode in (abi.ACCEPT_EXACT, abi.ACCEPT_RELAXED):
+        cfg = abi.AcceptCfg(mode, 1.0, 0, 0.1, 1, 0, 0, None, 0)
+        assert L.adt_verify_accept(fake, 70000, 70000, fake, fake, fake, fake, 4, C.byref(cfg), 0, fake, fake, fake,
+                                   fake, 1 << 30, None) == abi.E_UNSUPPORTED
     # stochastic-children acceptance without its q rows (null, short row stride, no rows)
     for q_logits, q_ld, q_row, q_rows in ((None, 16, fake, 4), (fake, 8, fake, 4), (fake, 16, None, 4),
                                           (fake, 16, fake, 0)):
