@@ -82,9 +82,10 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_chunk_kernel(const float* _
                                                                   const int32_t* __restrict__ allowed, int ulo,
                                                                   int uhi, int k, float* __restrict__ cand_v,
                                                                   int* __restrict__ cand_i,
-                                                                  float2* __restrict__ cand_ms) {
+                                                                  float2* __restrict__ cand_ms, int c0) {
   __shared__ float wv[TOPK_WAVES][KMAX];
   __shared__ int wi[TOPK_WAVES][KMAX];
+  // workgroup x covers chunk c0 + x of the row (outputs at x)
   const int chunk = blockIdx.x, G = gridDim.x, row = blockIdx.y;
   const int tid = threadIdx.x, lane = tid % WAVE, wave = tid / WAVE;
   const int lo = max(0, min(allowed ? allowed[row * 2] : ulo, V));
@@ -95,7 +96,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_chunk_kernel(const float* _
   int id[8];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int base = chunk * TOPK_CHUNK + j * 4 * TOPK_THREADS + 4 * tid;
+    const int base = (c0 + chunk) * TOPK_CHUNK + j * 4 * TOPK_THREADS + 4 * tid;
     if (vec && base + 3 < V) {
       const float4 q = *reinterpret_cast<const float4*>(x + base);
       r[4 * j] = q.x;
@@ -488,15 +489,23 @@ adt_status launch_row_topk(const float* logits, int64_t ld, int V, const int32_t
   float2* cms = (float2*)ws;
   float* cv = (float*)(cms + (size_t)rows * G * TOPK_WAVES);
   int* ci = (int*)(cv + (size_t)rows * G * kmax);
-  const dim3 g1(G, rows);
+  // one range for every row: only the chunks it touches (the chunks past it held -inf only;
+  // Anole's 8192 image codes of 65536 ids: 4 chunks instead of 32)
+  int c0 = 0, Gr = G;
+  const int ulo = max(0, min(lo, V)), uhi = max(ulo, min(hi, V));
+  if (!allowed && uhi > ulo) {
+    c0 = ulo / TOPK_CHUNK;
+    Gr = (uhi - 1) / TOPK_CHUNK + 1 - c0;
+  }
+  const dim3 g1(Gr, rows);
   if (kmax == 1) {
-    topk_chunk_kernel<1><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms);
+    topk_chunk_kernel<1><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms, c0);
     ADT_LAUNCH_CHECK();
-    topk_merge_kernel<1><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, lo, hi, k, top_id, top_val, lse);
+    topk_merge_kernel<1><<<rows, WAVE, 0, st>>>(cv, ci, cms, Gr, V, allowed, lo, hi, k, top_id, top_val, lse);
   } else {
-    topk_chunk_kernel<16><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms);
+    topk_chunk_kernel<16><<<g1, TOPK_THREADS, 0, st>>>(logits, ld, V, allowed, lo, hi, k, cv, ci, cms, c0);
     ADT_LAUNCH_CHECK();
-    topk_merge_kernel<16><<<rows, WAVE, 0, st>>>(cv, ci, cms, G, V, allowed, lo, hi, k, top_id, top_val, lse);
+    topk_merge_kernel<16><<<rows, WAVE, 0, st>>>(cv, ci, cms, Gr, V, allowed, lo, hi, k, top_id, top_val, lse);
   }
   ADT_LAUNCH_CHECK();
   return ADT_OK;
