@@ -508,18 +508,23 @@ def _small_bf16():
     return dataclasses.replace(cfg, prefix_len=16, img_hi=512, prefix_hi=512, grid_h=8, grid_w=8)
 
 
-@pytest.mark.parametrize("variant", ["adt", "fixed", "guided", "subrange"])
+@pytest.mark.parametrize("variant", ["adt", "fixed", "guided", "subrange", "subrange_high"])
 def test_bf16_small_parity(rt, variant):
     """The 2-layer bf16 model (d 256, 4 x 64 heads, V 512, 8 x 8 grid) under the ADT schedule,
     with fixed 6-deep 10-wide trees, with classifier-free guidance (scale 3.0), and with image
     ids [64, 320) inside the vocabulary (the LM head then computes those 256 rows only, from
-    weight row 64 on): every cycle of the image layer-local within the bf16 tolerance and
-    cross-fed bit-exact."""
+    weight row 64 on); and with V 8192 and image ids [2500, 6000), so that the root's and each
+    level's top-k cover only the 2048-id chunks 1-2 of the row, starting at a 16-unaligned id:
+    every cycle of the image layer-local within the bf16 tolerance and cross-fed bit-exact."""
     cfg = _small_bf16()
     if variant == "guided":
         cfg = dataclasses.replace(cfg, guidance=3.0)
     if variant == "subrange":
         cfg = dataclasses.replace(cfg, img_lo=64, img_hi=320, prefix_lo=320, prefix_hi=512)
+    if variant == "subrange_high":
+        cfg = synth.shrink(synth.get_config("llamagen_xl"), n_layers=2, d_model=256, n_heads=4, ffn=512, vocab=8192)
+        cfg = dataclasses.replace(cfg, prefix_len=16, img_lo=2500, img_hi=6000, prefix_lo=6000, prefix_hi=8192,
+                                  grid_h=8, grid_w=8)
     w = synth.model_weights(cfg)
     dm = rt.DeviceModel(cfg, w)
     om = OracleModel(cfg, w)
