@@ -53,7 +53,7 @@ struct SampleShared {
   uint64_t thr;
   uint64_t total;
   float zmax;
-  int node, trial, accepted, done, bonus, a, need;
+  int node, trial, accepted, done, bonus, a, need, exact;
 };
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
@@ -105,16 +105,56 @@ __device__ float block_max_f32(float v, SampleShared& sh) {
   return m;
 }
 
-// The K-th largest 64-bit key of the row (K < count): exactly K keys are >= it.
+__device__ uint64_t block_min_u64(uint64_t v, SampleShared& sh) {
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint64_t u = shfl_xor_u64(v, o);
+    v = u < v ? u : v;
+  }
+  __syncthreads();
+  if (threadIdx.x % WAVE == 0) sh.u64[threadIdx.x / WAVE] = v;
+  __syncthreads();
+  uint64_t m = ~0ull;
+  for (int i = 0; i < AS_THREADS / WAVE; ++i) m = sh.u64[i] < m ? sh.u64[i] : m;
+  __syncthreads();
+  return m;
+}
+
+// The K-th largest 64-bit key of the row (K < count): exactly K keys are >= it.  Digits of
+// 8 bits from the top; once the digit chosen holds exactly the keys still needed, the
+// threshold is the smallest key of that digit's bin (one pass of a block minimum instead of
+// the remaining digits: with fp32 logits the bin is usually a single key after 16-24 bits).
 __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T, SampleShared& sh) {
   uint64_t prefix = 0, mask = 0;
   int need = K;   // rank (1-based) of the threshold among keys matching the prefix
+  const int lane = threadIdx.x % WAVE;
   for (int shift = 56; shift >= 0; shift -= 8) {
     for (int i = threadIdx.x; i < 256; i += AS_THREADS) sh.hist[i] = 0;
     __syncthreads();
-    for (int i = lo + threadIdx.x; i < hi; i += AS_THREADS) {
-      const uint64_t k = zkey(x[i] / T, i);
-      if ((k & mask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255], 1u);
+    if (shift == 56) {
+      // the sign-and-exponent digit: most keys of a wave share a few bins, so the keys in the
+      // bins of the wave's first two unassigned lanes are counted with one atomic per bin
+      // (the same counts as one atomic per key)
+      for (int i = lo + threadIdx.x; i < hi; i += AS_THREADS) {
+        const uint32_t bin = (uint32_t)(zkey(x[i] / T, i) >> 56);
+        bool act = true;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const uint64_t am = __ballot(act);
+          if (am) {
+            const int leader = __ffsll((long long)am) - 1;
+            const uint32_t lb = (uint32_t)__shfl((int)bin, leader, WAVE);
+            const uint64_t peers = __ballot(act && bin == lb);
+            if (lane == leader) atomicAdd(&sh.hist[lb], (uint32_t)__popcll(peers));
+            if (bin == lb) act = false;
+          }
+        }
+        if (act) atomicAdd(&sh.hist[bin], 1u);
+      }
+    } else {
+      for (int i = lo + threadIdx.x; i < hi; i += AS_THREADS) {
+        const uint64_t k = zkey(x[i] / T, i);
+        if ((k & mask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255], 1u);
+      }
     }
     __syncthreads();
     // the highest bin b at which the count of keys in bins >= b reaches need (bin 0 if
@@ -147,16 +187,28 @@ __device__ uint64_t radix_select(const float* x, int lo, int hi, int K, float T,
       if (src < 0 && l == 0) {
         sh.thr = prefix;
         sh.need = need - (int)(all - sh.hist[0]);
+        sh.exact = sh.need == (int)sh.hist[0];
       } else if (l == src) {
         sh.thr = prefix | ((uint64_t)fb << shift);
         sh.need = need - (int)facc;
+        sh.exact = sh.need == (int)sh.hist[fb];
       }
     }
     __syncthreads();
     prefix = sh.thr;
     need = sh.need;
     mask |= (uint64_t)255 << shift;
+    const bool exact = sh.exact && shift > 0;
     __syncthreads();
+    if (exact) {
+      // every key of the bin is among the K largest: the threshold is the bin's smallest key
+      uint64_t mn = ~0ull;
+      for (int i = lo + threadIdx.x; i < hi; i += AS_THREADS) {
+        const uint64_t k = zkey(x[i] / T, i);
+        if ((k & mask) == prefix && k < mn) mn = k;
+      }
+      return block_min_u64(mn, sh);
+    }
   }
   return prefix;
 }
