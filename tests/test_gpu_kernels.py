@@ -238,11 +238,15 @@ def _random_tree_tokens(rng, n, V, lo, hi):
     return parent.astype(np.int32), token
 
 
-@pytest.mark.parametrize("mode,top_k,T", [("exact", 2000, 1.0), ("exact", 0, 0.7), ("exact", 3, 1.0),
-                                          ("relaxed", 2000, 1.0), ("relaxed", 50, 1.3)])
-def test_accept_sampling_bit_exact(rt, mode, top_k, T):
+@pytest.mark.parametrize("mode,top_k,T,ties", [("exact", 2000, 1.0, False), ("exact", 0, 0.7, False),
+                                               ("exact", 3, 1.0, False), ("relaxed", 2000, 1.0, False),
+                                               ("relaxed", 50, 1.3, False), ("exact", 2000, 1.0, True),
+                                               ("relaxed", 700, 1.0, True)])
+def test_accept_sampling_bit_exact(rt, mode, top_k, T, ties):
     """Exact / relaxed acceptance on the same fp32 logits: identical path and bonus for every
-    (seed, step).  Logits are sharpened on planted chains so long paths get accepted too."""
+    (seed, step).  Logits are sharpened on planted chains so long paths get accepted too.
+    ties: the logits lie on a grid of 0.5, so hundreds of ids share the value at the top-k
+    boundary and the lower ids among them are the ones kept."""
     from oracle.accept import accept_sampling
     rng = np.random.default_rng(21)
     V, lo, hi = 8448, 0, 8192
@@ -254,6 +258,8 @@ def test_accept_sampling_bit_exact(rt, mode, top_k, T):
         n = int(rng.integers(1, 62))
         parent, token = _random_tree_tokens(rng, n, V, lo, hi)
         logits = (rng.standard_normal((n, V)) * 1.5).astype(np.float32)
+        if ties:
+            logits = np.round(logits * 2.0) / 2.0
         for u in range(n):
             kids = [c for c in range(n) if parent[c] == u]
             if kids and rng.random() < 0.7:
