@@ -26,18 +26,47 @@ constexpr int TOPK_WAVES = TOPK_THREADS / WAVE;
 constexpr int TOPK_CHUNK = 8 * TOPK_THREADS;   // logits per chunk workgroup (two float4 per thread)
 constexpr int TOPK_MAX_CHUNKS = 32;            // vocabularies up to 65536
 
-// Wave-wide argmax of (value desc, id asc) with the owning lane.
-__device__ __forceinline__ void wave_best(float& v, int& id, int& lane) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const float ov = __shfl_xor(v, o, WAVE);
-    const int oi = __shfl_xor(id, o, WAVE), ol = __shfl_xor(lane, o, WAVE);
-    if (better(ov, oi, v, id)) {
-      v = ov;
-      id = oi;
-      lane = ol;
-    }
-  }
+// (value desc, id asc) as one 64-bit key, larger = better: the value's bits made
+// order-preserving (-0 taken as +0) above the id's complement.  For values that are not NaN
+// this is the order of better().
+__device__ __forceinline__ uint64_t best_key(float v, int id) {
+  const uint32_t u = __float_as_uint(v + 0.f);
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)o << 32) | (0xFFFFFFFFu - (uint32_t)id);
+}
+
+// max(v, v of the lane that the DPP pattern CTRL names), in the rows of row mask RM
+template <int CTRL, int RM>
+__device__ __forceinline__ uint64_t dpp_key_max(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, RM, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, RM, 0xF, false);
+  const uint64_t t = ((uint64_t)hi << 32) | lo;
+  return t > v ? t : v;
+}
+
+// The largest key of the wave (all 64 lanes active), as a uniform value: DPP exchanges within
+// quads, half rows and rows (VALU moves, instead of six dependent LDS-pipe permutes), then
+// the row broadcasts carry the maximum to lane 63.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t v) {
+  v = dpp_key_max<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+  v = dpp_key_max<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+  v = dpp_key_max<0x141, 0xF>(v);   // row_half_mirror
+  v = dpp_key_max<0x140, 0xF>(v);   // row_mirror
+  v = dpp_key_max<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+  v = dpp_key_max<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Wave-wide argmax of (value desc, id asc) over every lane's (v, id), none NaN: v and id
+// become the winner's (v exactly as the lane held it) and owner the lowest lane holding it.
+__device__ __forceinline__ void wave_best(float& v, int& id, int& owner) {
+  const uint64_t key = best_key(v, id);
+  const uint64_t top = wave_max_key(key);
+  owner = __ffsll((long long)__ballot(key == top)) - 1;
+  v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), owner));
+  id = (int)(0xFFFFFFFFu - (uint32_t)top);
 }
 
 // k rounds of "best remaining value of each lane, then the wave's best" over N values per
