@@ -353,26 +353,98 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
     // --- sibling walk on wave 0: the children of u in node order, one at a time (every lane
     // holds the same W, draw and mass); ids outside [lo, hi) weigh 0
     if (tid < WAVE) {
-      auto weight = [&](int i) -> uint64_t { return (i >= lo && i < hi) ? kept_weight(w, zb, lo, i) : 0ull; };
+      const bool relaxed = mode == ADT_ACCEPT_RELAXED;
+      auto in_range = [&](int i) { return i >= lo && i < hi; };
+      auto removed = [&](int i) { return (zb[(i - lo) >> 5] >> ((i - lo) & 31)) & 1u; };
+      // the next child of u at or after node `from` (n if none), by a ballot over par_s
+      auto next_child = [&](int from) -> int {
+        for (int b = from; b < n; b += WAVE) {
+          const int i = b + lane;
+          const uint64_t m = __ballot(i < n && par_s[i] == u);
+          if (m) return b + __ffsll((long long)m) - 1;
+        }
+        return n;
+      };
+      // Relaxed mode: a child's inputs (its token, the token's weight, the ids and weights of
+      // its first 128 neighbours) are requested one child ahead.  w does not change during the
+      // walk (removals are bits of zb, tested when the values are used), so the early loads
+      // read what the walk would read later.
+      struct Ahead {
+        int xt, y0, y1;
+        uint64_t wx, w0, w1;
+      };
+      auto fetch = [&](int c) {
+        Ahead f{0, -1, -1, 0ull, 0ull, 0ull};
+        if (c >= n) return f;
+        f.xt = min(max(tok_s[c], 0), V - 1);
+        if (in_range(f.xt)) f.wx = w[f.xt];
+        if (relaxed && f.xt < knn_rows) {
+          const int32_t* nb = knn + (int64_t)f.xt * knn_stride;
+          if (1 + lane < knn_k) f.y0 = nb[1 + lane];
+          if (1 + WAVE + lane < knn_k) f.y1 = nb[1 + WAVE + lane];
+          if (in_range(f.y0)) f.w0 = w[f.y0];
+          if (in_range(f.y1)) f.w1 = w[f.y1];
+        }
+        return f;
+      };
       uint64_t W = total;
       int trial = 0, acc = -1;
-      for (int c = u + 1; c < n; ++c) {
-        if (par_s[c] != u) continue;
-        const int xt = min(max(tok_s[c], 0), V - 1);
+      if (!relaxed) {
+        // exact: a child's one weight is requested when its turn comes, behind its draw (a
+        // request one child ahead measured slower here)
+        for (int c = u + 1; c < n; ++c) {
+          if (par_s[c] != u) continue;
+          const int xt = min(max(tok_s[c], 0), V - 1);
+          const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)trial, W);
+          ++trial;
+          const uint64_t mass = in_range(xt) && !removed(xt) ? w[xt] : 0ull;
+          if (r < mass) {
+            acc = c;
+            break;
+          }
+          uint64_t gone = 0;
+          if (lane == 0 && in_range(xt)) {
+            const uint32_t bit = 1u << ((xt - lo) & 31);
+            if (!(atomicOr(&zb[(xt - lo) >> 5], bit) & bit)) gone = w[xt];
+          }
+          W -= wave_sum_u64(gone);
+        }
+      }
+      int c = relaxed ? next_child(u + 1) : n;
+      Ahead cur = fetch(c);
+      while (c < n) {
+        const int cn = next_child(c + 1);
+        const Ahead nxt = fetch(cn);
+        const int xt = cur.xt;
         const uint64_t r = draw_below(seed, step, (uint32_t)u, (uint32_t)trial, W);
         ++trial;
-        uint64_t mass = weight(xt);
+        uint64_t mass = in_range(xt) && !removed(xt) ? cur.wx : 0ull;
         int credit_n = 0;
         const int32_t* nb = knn + (int64_t)xt * knn_stride;
-        if (mode == ADT_ACCEPT_RELAXED && xt < knn_rows) {
+        // neighbour j = base + lane of batch bi: the fetched id and weight for the first two
+        // batches, a load for later ones
+        auto nbr = [&](int bi, int j, int jmax, uint64_t& wr) -> int {
+          int y;
+          if (bi < 2) {
+            y = bi == 0 ? cur.y0 : cur.y1;
+            wr = bi == 0 ? cur.w0 : cur.w1;
+          } else {
+            y = j <= jmax ? nb[j] : -1;
+            wr = in_range(y) ? w[y] : 0ull;
+          }
+          return j <= jmax ? y : -1;
+        };
+        if (relaxed && xt < knn_rows) {
           // neighbours 1.. in order while the credited sum stays <= lim: the first j whose
           // running sum passes lim ends the run (a wave prefix sum per 64 neighbours)
           const uint64_t lim = (W * (uint64_t)delta_q) >> AS_DELTA_BITS;
           uint64_t extra = 0;
           credit_n = knn_k - 1;
-          for (int base = 1; base < knn_k; base += WAVE) {
+          for (int bi = 0, base = 1; base < knn_k; ++bi, base += WAVE) {
             const int j = base + lane;
-            const uint64_t wy = j < knn_k ? weight(nb[j]) : 0ull;
+            uint64_t wr;
+            const int y = nbr(bi, j, knn_k - 1, wr);
+            const uint64_t wy = in_range(y) && !removed(y) ? wr : 0ull;
             const uint64_t inc = wave_incl_scan_u64(wy);
             const uint64_t past = __ballot(j < knn_k && extra + inc > lim);
             if (past) {
@@ -392,19 +464,21 @@ __global__ __launch_bounds__(AS_THREADS) void accept_sample_kernel(
         // rejected: x, then its credited neighbours, leave p; an id already removed (an earlier
         // sibling's credit, a repeat in the list, x itself) subtracts nothing
         uint64_t gone = 0;
-        if (lane == 0 && xt >= lo && xt < hi) {
+        if (lane == 0 && in_range(xt)) {
           const uint32_t bit = 1u << ((xt - lo) & 31);
-          if (!(atomicOr(&zb[(xt - lo) >> 5], bit) & bit)) gone = w[xt];
+          if (!(atomicOr(&zb[(xt - lo) >> 5], bit) & bit)) gone = cur.wx;
         }
-        for (int base = 1; base <= credit_n; base += WAVE) {
-          const int j = base + lane;
-          const int y = j <= credit_n ? nb[j] : -1;
-          if (y >= lo && y < hi) {
+        for (int bi = 0, base = 1; base <= credit_n; ++bi, base += WAVE) {
+          uint64_t wr;
+          const int y = nbr(bi, base + lane, credit_n, wr);
+          if (in_range(y)) {
             const uint32_t bit = 1u << ((y - lo) & 31);
-            if (!(atomicOr(&zb[(y - lo) >> 5], bit) & bit)) gone += w[y];
+            if (!(atomicOr(&zb[(y - lo) >> 5], bit) & bit)) gone += wr;
           }
         }
         W -= wave_sum_u64(gone);
+        c = cn;
+        cur = nxt;
       }
       if (lane == 0) {
         sh.accepted = acc;
